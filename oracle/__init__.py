@@ -1,0 +1,202 @@
+"""Plain CPU oracle for the Spense hybrid 2:4-sparse / dense linear layer.
+
+TEST INFRASTRUCTURE ONLY: tests, the smoke check and the benchmark's CPU-baseline leg
+may import this package; the product library never does.  It shares no code with the
+GPU path.  The arithmetic lives in ``spense_oracle.c`` (plain C, built with gcc); this
+module only marshals numpy arrays.
+
+Paper references (SpenseGPT): the 2:4 constraint is Eq. (1) in sec. 3.1.1, compressed
+2:4 storage is described in sec. 3.1.1, the output-split / input-split Spense format in
+sec. 3.2, and the dense region being the last one in sec. 3.3.2 and Table "front_back".
+
+Parity status: every function here is pinned by tests that do not re-use it (format
+definition vs torch's converters, brute force over all 2:4 masks, numpy fp64 matmul
+within the Higham bound, exact-integer cases, linearity of the two split variants).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+FP8 = 1
+BF16 = 2
+AXIS_OUTPUT = 0
+AXIS_INPUT = 1
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "spense_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile the C oracle with gcc (OpenMP, no FMA contraction, no fast-math)."""
+    if force or not os.path.exists(_LIB_PATH):
+        tmp = _LIB_PATH + f".tmp{os.getpid()}"
+        cmd = ["gcc", "-O2", "-fopenmp", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared", _SRC,
+               "-o", tmp, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _L():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            build(force=True)
+        lib = ctypes.CDLL(_LIB_PATH)
+        p, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
+        lib.or_decode_e4m3fn.restype = ctypes.c_double
+        lib.or_decode_e4m3fn.argtypes = [ctypes.c_uint8]
+        lib.or_decode_bf16.restype = ctypes.c_float
+        lib.or_decode_bf16.argtypes = [ctypes.c_uint16]
+        lib.or_bf16_rne.restype = ctypes.c_uint16
+        lib.or_bf16_rne.argtypes = [ctypes.c_float]
+        lib.or_decode_e4m3fn_array.argtypes = [p, i64, p]
+        lib.or_decode_bf16_array.argtypes = [p, i64, p]
+        lib.or_bf16_rne_array.argtypes = [p, i64, p]
+        lib.or_layout.restype = i32
+        lib.or_layout.argtypes = [i64, i64, i32, i64, p]
+        lib.or_compress.restype = i64
+        lib.or_compress.argtypes = [p, p, i64, i64, i32, i32, i64, p, p, p]
+        lib.or_decompress.restype = i32
+        lib.or_decompress.argtypes = [p, p, p, i64, i64, i32, i32, i64, p]
+        lib.or_gemm_f32.restype = i32
+        lib.or_gemm_f32.argtypes = [p, p, i64, i64, i64, i32, p, p, p, p, p]
+        lib.or_gemm_f64.restype = i32
+        lib.or_gemm_f64.argtypes = [p, p, i64, i64, i64, i32, p, p, p, p, p]
+        _lib = lib
+    return _lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _codes(a, dtype):
+    want = np.uint8 if dtype == FP8 else np.uint16
+    a = np.ascontiguousarray(a)
+    if a.dtype != want:
+        raise TypeError(f"expected {want} codes, got {a.dtype}")
+    return a
+
+
+def esize(dtype: int) -> int:
+    return 1 if dtype == FP8 else 2
+
+
+# ------------------------------------------------------------------ number formats
+def decode_e4m3fn(codes) -> np.ndarray:
+    c = np.ascontiguousarray(codes, dtype=np.uint8)
+    out = np.empty(c.shape, np.float64)
+    _L().or_decode_e4m3fn_array(_ptr(c), c.size, _ptr(out))
+    return out
+
+
+def decode_bf16(bits) -> np.ndarray:
+    c = np.ascontiguousarray(bits, dtype=np.uint16)
+    out = np.empty(c.shape, np.float32)
+    _L().or_decode_bf16_array(_ptr(c), c.size, _ptr(out))
+    return out
+
+
+def bf16_rne(x) -> np.ndarray:
+    f = np.ascontiguousarray(x, dtype=np.float32)
+    out = np.empty(f.shape, np.uint16)
+    _L().or_bf16_rne_array(_ptr(f), f.size, _ptr(out))
+    return out
+
+
+def decode(codes, dtype) -> np.ndarray:
+    return decode_e4m3fn(codes) if dtype == FP8 else decode_bf16(codes).astype(np.float64)
+
+
+# ------------------------------------------------------------------ format
+def layout(N: int, K: int, axis: int, dense_begin: int) -> dict:
+    out = np.zeros(6, np.int64)
+    if _L().or_layout(N, K, axis, dense_begin, _ptr(out)):
+        raise ValueError("bad split")
+    sr, vld, mld, dr, dld, sc = (int(v) for v in out)
+    return {"sparse_rows": sr, "values_ld": vld, "meta_ld": mld, "dense_rows": dr, "dense_ld": dld,
+            "sparse_cols": sc}
+
+
+def compress(W, mask, dtype: int, axis: int, dense_begin: int):
+    """Canonical 2:4 compression.  Returns (values, meta, dense, bad_groups)."""
+    W = _codes(W, dtype)
+    N, K = W.shape
+    lay = layout(N, K, axis, dense_begin)
+    vt = np.uint8 if dtype == FP8 else np.uint16
+    values = np.zeros((lay["sparse_rows"], lay["values_ld"]), vt)
+    meta = np.zeros((lay["sparse_rows"], lay["meta_ld"]), np.uint32)
+    dense = np.zeros((lay["dense_rows"], lay["dense_ld"]), vt)
+    m = None if mask is None else np.ascontiguousarray(mask, dtype=np.uint8)
+    if m is not None and m.shape != W.shape:
+        raise ValueError("mask shape")
+    bad = _L().or_compress(_ptr(W), _ptr(m), N, K, esize(dtype), axis, dense_begin, _ptr(values), _ptr(meta),
+                           _ptr(dense))
+    if bad < 0:
+        raise ValueError("sparse region K must be a multiple of 4")
+    return values, meta, dense, int(bad)
+
+
+def decompress(values, meta, dense, N: int, K: int, dtype: int, axis: int, dense_begin: int) -> np.ndarray:
+    vt = np.uint8 if dtype == FP8 else np.uint16
+    lay = layout(N, K, axis, dense_begin)
+    values = np.ascontiguousarray(values, dtype=vt).reshape(lay["sparse_rows"], lay["values_ld"])
+    meta = np.ascontiguousarray(meta, dtype=np.uint32).reshape(lay["sparse_rows"], lay["meta_ld"])
+    dense = np.ascontiguousarray(dense, dtype=vt).reshape(lay["dense_rows"], lay["dense_ld"])
+    W = np.empty((N, K), vt)
+    if _L().or_decompress(_ptr(values), _ptr(meta), _ptr(dense), N, K, esize(dtype), axis, dense_begin, _ptr(W)):
+        raise ValueError("bad split")
+    return W
+
+
+# ------------------------------------------------------------------ GEMM
+def gemm(X, W, dtype: int, sw=None, sx=None) -> dict:
+    """Y = X W^T with fp32 ascending-k accumulation and the fp32 scale epilogue.
+
+    Returns {"acc": fp32 M x N, "y_f32": fp32 M x N, "y_bf16": uint16 M x N}."""
+    X = _codes(X, dtype)
+    W = _codes(W, dtype)
+    M, K = X.shape
+    N, K2 = W.shape
+    if K != K2:
+        raise ValueError("K mismatch")
+    swa = None if sw is None else np.ascontiguousarray(sw, dtype=np.float32)
+    sxa = None if sx is None else np.ascontiguousarray(sx, dtype=np.float32)
+    acc = np.empty((M, N), np.float32)
+    yf = np.empty((M, N), np.float32)
+    yb = np.empty((M, N), np.uint16)
+    rc = _L().or_gemm_f32(_ptr(X), _ptr(W), M, N, K, dtype, _ptr(swa), _ptr(sxa), _ptr(acc), _ptr(yf), _ptr(yb))
+    if rc:
+        raise RuntimeError(f"or_gemm_f32 failed {rc}")
+    return {"acc": acc, "y_f32": yf, "y_bf16": yb}
+
+
+def gemm_f64(X, W, dtype: int, sw=None, sx=None) -> dict:
+    """Same contraction in fp64; also returns sum_k |x w| for error bounds."""
+    X = _codes(X, dtype)
+    W = _codes(W, dtype)
+    M, K = X.shape
+    N, _ = W.shape
+    swa = None if sw is None else np.ascontiguousarray(sw, dtype=np.float32)
+    sxa = None if sx is None else np.ascontiguousarray(sx, dtype=np.float32)
+    acc = np.empty((M, N), np.float64)
+    y = np.empty((M, N), np.float64)
+    ad = np.empty((M, N), np.float64)
+    rc = _L().or_gemm_f64(_ptr(X), _ptr(W), M, N, K, dtype, _ptr(swa), _ptr(sxa), _ptr(acc), _ptr(y), _ptr(ad))
+    if rc:
+        raise RuntimeError(f"or_gemm_f64 failed {rc}")
+    return {"acc": acc, "y": y, "abs_dot": ad}
+
+
+def spense_gemm(X, values, meta, dense, N: int, K: int, dtype: int, axis: int, dense_begin: int, sw=None,
+                sx=None) -> dict:
+    """The whole layer from the packed format: decompress, then the plain GEMM."""
+    W = decompress(values, meta, dense, N, K, dtype, axis, dense_begin)
+    return gemm(X, W, dtype, sw, sx)

@@ -1,0 +1,403 @@
+"""Pins for the CPU oracle against facts that do not come from the oracle itself.
+
+- number formats: torch's float8_e4m3fn / bfloat16 converters (library routines);
+- compression: the defining round trip (decompress(compress(W, mask)) == W * mask,
+  bitwise), the 2:4 bound of Eq. (1), exhaustive masks on one group, brute force on tiny
+  matrices, and hand-worked fixtures under tests/golden/;
+- GEMM: numpy fp64 matmul within the Higham bound for fp32 summation, exact integers,
+  and the linearity of the two split variants of sec. 3.2 (output-split concatenates
+  disjoint outputs, input-split sums two partial products).
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+from hypothesis import given, settings, strategies as st
+
+import gen
+import oracle
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+U32 = 2.0 ** -24
+
+
+def tdec(codes, dtype):
+    """Decode via torch (an implementation independent of the oracle)."""
+    if dtype == oracle.FP8:
+        return torch.from_numpy(np.ascontiguousarray(codes, np.uint8)).view(torch.float8_e4m3fn).to(
+            torch.float64).numpy()
+    return torch.from_numpy(np.ascontiguousarray(codes, np.uint16).view(np.int16)).view(torch.bfloat16).to(
+        torch.float64).numpy()
+
+
+def higham(K):
+    return K * U32 / (1 - K * U32)
+
+
+def same_bits(a, b):
+    return np.array_equal(np.asarray(a).view(np.uint8), np.asarray(b).view(np.uint8))
+
+
+# ------------------------------------------------------------------ number formats
+def test_e4m3fn_decode_all_codes_match_torch():
+    codes = np.arange(256, dtype=np.uint8)
+    mine = oracle.decode_e4m3fn(codes)
+    ref = tdec(codes, oracle.FP8)
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(mine), nan)
+    assert np.array_equal(mine[~nan], ref[~nan])
+    assert np.array_equal(np.signbit(mine[~nan]), np.signbit(ref[~nan]))
+    # format facts: NaN only at 0x7f / 0xff, max 448, smallest subnormal 2^-9
+    assert set(np.nonzero(nan)[0]) == {0x7F, 0xFF}
+    assert mine[0x7E] == 448.0 and mine[0x01] == 2.0 ** -9 and mine[0x08] == 2.0 ** -6
+
+
+def test_bf16_decode_all_patterns_match_torch():
+    bits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    mine = oracle.decode_bf16(bits).astype(np.float64)
+    ref = tdec(bits, oracle.BF16)
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(mine), nan)
+    assert np.array_equal(mine[~nan], ref[~nan])
+
+
+def test_bf16_rne_matches_torch():
+    r = np.random.default_rng(5)
+    u = r.integers(0, 2 ** 32, size=200000, dtype=np.uint64).astype(np.uint32)
+    # exact ties with both parities of the kept bit, and values next to overflow
+    ties = (r.integers(0, 2 ** 16, size=2000, dtype=np.uint64).astype(np.uint32) << 16) | 0x8000
+    special = np.array([0x7F7FFFFF, 0x7F7F8000, 0x7F7F7FFF, 0x00008000, 0x00018000, 0x80008000, 0x3F808000,
+                        0x3F818000, 0x7F800000, 0xFF800000], np.uint32)
+    u = np.concatenate([u, ties, special])
+    f = u.view(np.float32)
+    mine = oracle.bf16_rne(f)
+    ref = torch.from_numpy(f.copy()).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    nan = np.isnan(f)
+    assert np.array_equal(mine[~nan], ref[~nan])
+    assert np.all(np.isnan(oracle.decode_bf16(mine[nan])))
+
+
+# ------------------------------------------------------------------ hand-worked fixtures
+def _golden():
+    with open(os.path.join(HERE, "golden", "hand_examples.json")) as f:
+        return json.load(f)["cases"]
+
+
+@pytest.mark.parametrize("case", _golden(), ids=lambda c: c["name"])
+def test_golden_hand_examples(case):
+    dt = oracle.FP8 if case["dtype"] == "fp8" else oracle.BF16
+    ax = oracle.AXIS_OUTPUT if case["axis"] == "output" else oracle.AXIS_INPUT
+    vt = np.uint8 if dt == oracle.FP8 else np.uint16
+    W = np.array(case["W_codes"], vt)
+    # the fixture's codes encode its stated values (checked with torch)
+    assert np.array_equal(tdec(W, dt), np.array(case["W_values"], np.float64))
+    mask = np.array(case["mask"], np.uint8)
+    v, m, d, bad = oracle.compress(W, mask, dt, ax, case["dense_begin"])
+    assert bad == 0
+    assert np.array_equal(v, np.array(case["values"], vt))
+    assert np.array_equal(m, np.array(case["meta"], np.uint32))
+    assert np.array_equal(d, np.array(case["dense"], vt))
+    X = np.array(case["X_codes"], vt)
+    assert np.array_equal(tdec(X, dt), np.array(case["X_values"], np.float64))
+    sw = None if case["sw"] is None else np.array(case["sw"], np.float32)
+    sx = None if case["sx"] is None else np.array(case["sx"], np.float32)
+    out = oracle.spense_gemm(X, v, m, d, case["N"], case["K"], dt, ax, case["dense_begin"], sw, sx)
+    assert np.array_equal(out["acc"], np.array(case["acc"], np.float32))
+    assert np.array_equal(out["y_f32"], np.array(case["y_exact"], np.float32))
+    assert np.array_equal(out["y_bf16"], np.array(case["y_bf16_bits"], np.uint16))
+
+
+# ------------------------------------------------------------------ compression
+def test_compress_exhaustive_single_group():
+    """All 16 masks of one group of 4: >2 kept is rejected, <=2 round-trips and is
+    stored in the canonical way (ascending positions, padding holds +0)."""
+    W = np.array([[0x38, 0x40, 0x44, 0xC0]], np.uint8)  # 1, 2, 3, -2
+    for bits in range(16):
+        mask = np.array([[(bits >> i) & 1 for i in range(4)]], np.uint8)
+        v, m, d, bad = oracle.compress(W, mask, oracle.FP8, oracle.AXIS_OUTPUT, 1)
+        kept = [i for i in range(4) if mask[0, i]]
+        if len(kept) > 2:
+            assert bad == 1
+            continue
+        assert bad == 0
+        code = int(m[0, 0])
+        i0, i1 = code & 3, (code >> 2) & 3
+        assert i0 < i1 and code >> 4 == 0
+        assert set(kept) <= {i0, i1}
+        for j, pos in enumerate((i0, i1)):
+            assert v[0, j] == (W[0, pos] if pos in kept else 0)
+        # padding takes the smallest non-kept positions
+        pad = sorted({i0, i1} - set(kept))
+        free = [i for i in range(4) if i not in kept]
+        assert pad == free[: len(pad)]
+        back = oracle.decompress(v, m, d, 1, 4, oracle.FP8, oracle.AXIS_OUTPUT, 1)
+        assert np.array_equal(back, W * mask)
+
+
+def test_compress_bruteforce_tiny_all_two_of_four_masks():
+    """N=2, K=16: every exactly-2-of-4 mask on row 0 (6^4 of them), random on row 1."""
+    r = np.random.default_rng(0)
+    pats = [(0, 1), (0, 2), (0, 3), (1, 2), (1, 3), (2, 3)]
+    W = r.integers(1, 256, size=(2, 16)).astype(np.uint8)
+    W[W == 0x80] = 0x81
+    import itertools
+    for combo in itertools.product(range(6), repeat=4):
+        mask = np.zeros((2, 16), np.uint8)
+        for g, c in enumerate(combo):
+            a, b = pats[c]
+            mask[0, 4 * g + a] = mask[0, 4 * g + b] = 1
+            a, b = pats[r.integers(0, 6)]
+            mask[1, 4 * g + a] = mask[1, 4 * g + b] = 1
+        v, m, d, bad = oracle.compress(W, mask, oracle.FP8, oracle.AXIS_OUTPUT, 2)
+        assert bad == 0
+        back = oracle.decompress(v, m, d, 2, 16, oracle.FP8, oracle.AXIS_OUTPUT, 2)
+        assert np.array_equal(back, W * mask)
+        # the stored codes are exactly the kept pairs
+        for g, c in enumerate(combo):
+            assert (int(m[0, 0]) >> (4 * g)) & 15 == pats[c][0] | (pats[c][1] << 2)
+
+
+def test_round_trip_all_byte_patterns_including_nan():
+    codes = np.arange(256, dtype=np.uint8)
+    W = np.tile(codes, 4).reshape(8, 128)
+    r = np.random.default_rng(1)
+    for axis, db in ((oracle.AXIS_OUTPUT, 6), (oracle.AXIS_INPUT, 96)):
+        mask = gen.random_mask_24(r, 8, 128, gen.OUTPUT if axis == 0 else gen.INPUT, db, allow_fewer=False)
+        v, m, d, bad = oracle.compress(W, mask, oracle.FP8, axis, db)
+        assert bad == 0
+        back = oracle.decompress(v, m, d, 8, 128, oracle.FP8, axis, db)
+        assert np.array_equal(back, W * mask)
+
+
+def test_second_round_trip_from_packed():
+    r = np.random.default_rng(2)
+    N, K, db = 24, 96, 16
+    W = r.integers(0, 65536, size=(N, K)).astype(np.uint16)
+    mask = gen.random_mask_24(r, N, K, gen.OUTPUT, db)
+    v, m, d, _ = oracle.compress(W, mask, oracle.BF16, oracle.AXIS_OUTPUT, db)
+    Wd = oracle.decompress(v, m, d, N, K, oracle.BF16, oracle.AXIS_OUTPUT, db)
+    # the metadata names the positions that hold the stored values
+    mask2 = np.ones((N, K), np.uint8)
+    mask2[:db] = 0
+    for row in range(db):
+        for g in range(K // 4):
+            code = (int(m[row, g // 8]) >> (4 * (g % 8))) & 15
+            mask2[row, 4 * g + (code & 3)] = 1
+            mask2[row, 4 * g + (code >> 2)] = 1
+    v2, m2, d2, bad = oracle.compress(Wd, mask2, oracle.BF16, oracle.AXIS_OUTPUT, db)
+    assert bad == 0 and np.array_equal(v2, v) and np.array_equal(m2, m) and np.array_equal(d2, d)
+
+
+def test_null_mask_keeps_nonzero_bit_patterns():
+    W = np.array([[0x38, 0, 0x80, 0, 0, 0, 0, 0x44]], np.uint8)  # 1, 0, -0, 0 | 0, 0, 0, 3
+    v, m, d, bad = oracle.compress(W, None, oracle.FP8, oracle.AXIS_OUTPUT, 1)
+    assert bad == 0
+    assert list(v[0]) == [0x38, 0x80, 0x00, 0x44]
+    assert int(m[0, 0]) == (0 | 2 << 2) | ((0 | 3 << 2) << 4)
+    W3 = np.array([[0x38, 0x38, 0x38, 0]], np.uint8)
+    assert oracle.compress(W3, None, oracle.FP8, oracle.AXIS_OUTPUT, 1)[3] == 1
+
+
+@settings(max_examples=60, deadline=None)
+@given(st.integers(1, 40), st.integers(1, 24), st.sampled_from([0, 1]), st.floats(0.0, 1.0),
+       st.sampled_from([1, 2]), st.integers(0, 2 ** 31))
+def test_property_round_trip_and_eq1(N, k4, axis, frac, dtype, seed):
+    K = 4 * k4
+    r = np.random.default_rng(seed)
+    vt = np.uint8 if dtype == 1 else np.uint16
+    W = r.integers(0, 256 if dtype == 1 else 65536, size=(N, K)).astype(vt)
+    if axis == 0:
+        db = int(round(frac * N))
+        mask = gen.random_mask_24(r, N, K, gen.OUTPUT, db)
+    else:
+        db = 4 * int(round(frac * k4))
+        mask = gen.random_mask_24(r, N, K, gen.INPUT, db)
+    v, m, d, bad = oracle.compress(W, mask, dtype, axis, db)
+    assert bad == 0
+    back = oracle.decompress(v, m, d, N, K, dtype, axis, db)
+    assert np.array_equal(back, W * mask.astype(vt))
+    # Eq. (1): every group of 4 in the sparse region has at most 2 non-zero patterns
+    reg = back[:db] if axis == 0 else back[:, :db]
+    if reg.size:
+        nz = (reg != 0).reshape(reg.shape[0], -1, 4).sum(-1)
+        assert nz.max() <= 2
+
+
+def test_bad_groups_are_counted():
+    W = np.full((4, 64), 0x38, np.uint8)
+    mask = np.ones((4, 64), np.uint8)
+    _, _, _, bad = oracle.compress(W, mask, oracle.FP8, oracle.AXIS_INPUT, 32)
+    assert bad == 4 * 8
+    _, _, _, bad = oracle.compress(W, mask, oracle.FP8, oracle.AXIS_OUTPUT, 0)
+    assert bad == 0  # everything is dense
+
+
+# ------------------------------------------------------------------ GEMM
+def _rand_fp8(r, shape, scale=1.0):
+    return gen.to_e4m3fn(r.standard_normal(shape).astype(np.float32) * np.float32(scale))
+
+
+@pytest.mark.parametrize("dtype", [oracle.FP8, oracle.BF16])
+def test_gemm_within_higham_bound_of_fp64_matmul(dtype):
+    r = np.random.default_rng(3)
+    M, N, K = 7, 33, 1024
+    if dtype == oracle.FP8:
+        X, W = _rand_fp8(r, (M, K)), _rand_fp8(r, (N, K), 8.0)
+    else:
+        X = gen.to_bf16(r.standard_normal((M, K)).astype(np.float32))
+        W = gen.to_bf16(r.standard_normal((N, K)).astype(np.float32) * 0.02)
+    xd, wd = tdec(X, dtype), tdec(W, dtype)
+    exact = xd @ wd.T
+    absd = np.abs(xd) @ np.abs(wd).T
+    out = oracle.gemm(X, W, dtype)
+    err = np.abs(out["acc"].astype(np.float64) - exact)
+    assert np.all(err <= higham(K) * absd)
+    assert np.any(err > 0)  # the fp32 oracle really rounds
+    o64 = oracle.gemm_f64(X, W, dtype)
+    assert np.all(np.abs(o64["acc"] - exact) <= 2 * K * 2.0 ** -53 * absd)
+    assert np.allclose(o64["abs_dot"], absd, rtol=1e-12, atol=0)
+
+
+def test_gemm_exact_integers_and_pow2_epilogue():
+    r = np.random.default_rng(4)
+    M, N, K = 5, 19, 4096
+    Wv, Xv = r.integers(-3, 4, size=(N, K)), r.integers(-3, 4, size=(M, K))
+    W, X = gen.int_codes(Wv, gen.FP8), gen.int_codes(Xv, gen.FP8)
+    sw = (2.0 ** r.integers(-4, 3, size=N)).astype(np.float32)
+    sx = (2.0 ** r.integers(-4, 3, size=M)).astype(np.float32)
+    out = oracle.gemm(X, W, oracle.FP8, sw, sx)
+    exact = (Xv @ Wv.T).astype(np.int64)
+    assert np.array_equal(out["acc"].astype(np.int64), exact)
+    y = exact * sw[None, :].astype(np.float64) * sx[:, None].astype(np.float64)
+    assert np.array_equal(out["y_f32"].astype(np.float64), y)
+    ref = torch.from_numpy(y.astype(np.float32)).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(out["y_bf16"], ref)
+
+
+def test_epilogue_two_fp32_roundings_then_bf16():
+    r = np.random.default_rng(6)
+    M, N, K = 9, 21, 256
+    X, W = _rand_fp8(r, (M, K)), _rand_fp8(r, (N, K))
+    sw = r.uniform(1e-4, 1e-2, N).astype(np.float32)
+    sx = r.uniform(1e-3, 1e-1, M).astype(np.float32)
+    out = oracle.gemm(X, W, oracle.FP8, sw, sx)
+    t = (out["acc"] * sw[None, :]).astype(np.float32)
+    t = (t * sx[:, None]).astype(np.float32)
+    assert np.array_equal(out["y_f32"], t)
+    ref = torch.from_numpy(t).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(out["y_bf16"], ref)
+
+
+def _packed(r, N, K, axis, db, dtype):
+    if dtype == oracle.FP8:
+        W = _rand_fp8(r, (N, K), 4.0)
+    else:
+        W = gen.to_bf16(r.standard_normal((N, K)).astype(np.float32))
+    mask = gen.random_mask_24(r, N, K, gen.OUTPUT if axis == 0 else gen.INPUT, db)
+    v, m, d, bad = oracle.compress(W, mask, dtype, axis, db)
+    assert bad == 0
+    return W, mask, v, m, d
+
+
+@pytest.mark.parametrize("dtype", [oracle.FP8, oracle.BF16])
+def test_output_split_is_concatenation_of_two_gemms(dtype):
+    """Sec. 3.2: the sparse GEMM produces one block of output columns, the dense GEMM
+    the other; checked against numpy on the stored pieces directly."""
+    r = np.random.default_rng(7)
+    M, N, K, Ns = 6, 40, 256, 24
+    W, mask, v, m, d = _packed(r, N, K, 0, Ns, dtype)
+    X = _rand_fp8(r, (M, K)) if dtype == oracle.FP8 else gen.to_bf16(r.standard_normal((M, K)).astype(np.float32))
+    out = oracle.spense_gemm(X, v, m, d, N, K, dtype, 0, Ns)
+    xd = tdec(X, dtype)
+    # sparse block from the values + metadata by numpy indexing, dense block as stored
+    vals = tdec(v, dtype)
+    ws = np.zeros((Ns, K))
+    for g in range(K // 4):
+        code = (m[:, g // 8] >> np.uint32(4 * (g % 8))) & np.uint32(15)
+        ws[np.arange(Ns), 4 * g + (code & 3).astype(np.int64)] = vals[:, 2 * g]
+        ws[np.arange(Ns), 4 * g + (code >> 2).astype(np.int64)] = vals[:, 2 * g + 1]
+    y_s = xd @ ws.T
+    y_d = xd @ tdec(d, dtype).T
+    ref = np.concatenate([y_s, y_d], axis=1)
+    absd = np.abs(xd) @ np.abs(np.concatenate([ws, tdec(d, dtype)])).T
+    assert np.all(np.abs(out["acc"] - ref) <= higham(K) * absd)
+
+
+@pytest.mark.parametrize("dtype", [oracle.FP8, oracle.BF16])
+def test_input_split_is_sum_of_two_partial_gemms(dtype):
+    r = np.random.default_rng(8)
+    M, N, K, Ks = 5, 17, 384, 256
+    W, mask, v, m, d = _packed(r, N, K, 1, Ks, dtype)
+    X = _rand_fp8(r, (M, K)) if dtype == oracle.FP8 else gen.to_bf16(r.standard_normal((M, K)).astype(np.float32))
+    out = oracle.spense_gemm(X, v, m, d, N, K, dtype, 1, Ks)
+    xd = tdec(X, dtype)
+    wm = tdec(W, dtype) * mask
+    part_s = xd[:, :Ks] @ wm[:, :Ks].T
+    part_d = xd[:, Ks:] @ tdec(d, dtype).T
+    absd = np.abs(xd) @ np.abs(wm).T
+    assert np.all(np.abs(out["acc"] - (part_s + part_d)) <= higham(K) * absd)
+    # the dense region ignores the mask: it equals the unpruned W columns
+    assert np.array_equal(d, W[:, Ks:])
+
+
+@pytest.mark.parametrize("axis", [0, 1])
+def test_dense_fraction_zero_and_one(axis):
+    r = np.random.default_rng(9)
+    M, N, K = 4, 32, 256
+    X = _rand_fp8(r, (M, K))
+    W = _rand_fp8(r, (N, K))
+    full = N if axis == 0 else K
+    # fraction 1: sparse region empty -> plain GEMM on W
+    v, m, d, _ = oracle.compress(W, None, oracle.FP8, axis, 0)
+    assert v.size == 0 and m.size == 0 and np.array_equal(d, W)
+    out = oracle.spense_gemm(X, v, m, d, N, K, oracle.FP8, axis, 0)
+    assert np.array_equal(out["acc"], oracle.gemm(X, W, oracle.FP8)["acc"])
+    # fraction 0: dense region empty -> pure 2:4 GEMM on W * mask
+    mask = gen.random_mask_24(r, N, K, gen.OUTPUT if axis == 0 else gen.INPUT, full, allow_fewer=False)
+    v, m, d, _ = oracle.compress(W, mask, oracle.FP8, axis, full)
+    assert d.size == 0
+    out = oracle.spense_gemm(X, v, m, d, N, K, oracle.FP8, axis, full)
+    xd, wm = tdec(X, oracle.FP8), tdec(W, oracle.FP8) * mask
+    absd = np.abs(xd) @ np.abs(wm).T
+    assert np.all(np.abs(out["acc"] - xd @ wm.T) <= higham(K) * absd)
+
+
+def test_empty_shapes():
+    W = np.zeros((0, 64), np.uint8)
+    v, m, d, bad = oracle.compress(W, None, oracle.FP8, 0, 0)
+    assert bad == 0 and v.shape == (0, 32) and d.shape == (0, 64)
+    X = np.zeros((0, 64), np.uint8)
+    out = oracle.gemm(X, np.zeros((3, 64), np.uint8), oracle.FP8)
+    assert out["y_bf16"].shape == (0, 3)
+    out = oracle.gemm(np.zeros((2, 0), np.uint8), np.zeros((3, 0), np.uint8), oracle.FP8)
+    assert np.array_equal(out["acc"], np.zeros((2, 3), np.float32))
+
+
+# ------------------------------------------------------------------ input generators
+def test_magnitude_mask_keeps_two_largest_and_row_absmax():
+    r = np.random.default_rng(10)
+    Wf = gen.draw_weight(r, 64, 128)
+    Wf[0, :4] = [0.5, -0.5, 0.5, 0.1]  # tie: the lower indices win
+    mask = gen.magnitude_mask_24(Wf, gen.OUTPUT, 48)
+    assert list(mask[0, :4]) == [1, 1, 0, 0]
+    kept = mask[:48].reshape(48, -1, 4).sum(-1)
+    assert np.all(kept == 2) and np.all(mask[48:] == 1)
+    a = np.abs(Wf[:48]).reshape(48, -1, 4)
+    kmin = np.where(mask[:48].reshape(48, -1, 4) == 1, a, np.inf).min(-1)
+    dmax = np.where(mask[:48].reshape(48, -1, 4) == 0, a, -np.inf).max(-1)
+    assert np.all(kmin >= dmax)
+    # pruning keeps every group's maximum, so the row absmax (the fp8 scale) is unchanged
+    assert np.array_equal(np.abs(Wf[:48] * mask[:48]).max(1), np.abs(Wf[:48]).max(1))
+
+
+def test_quantize_rows_fp8_scale_and_saturation():
+    r = np.random.default_rng(11)
+    A = r.standard_normal((8, 64)).astype(np.float32)
+    A[3] = 0
+    codes, s = gen.quantize_rows_fp8(A)
+    assert s[3] == 1.0 and np.all(codes[3] == 0)
+    d = tdec(codes, oracle.FP8)
+    assert np.all(np.abs(d).max(1)[[0, 1, 2, 4, 5, 6, 7]] == 448.0)
+    assert not np.any(np.isnan(d))
