@@ -1,0 +1,197 @@
+/*
+ * libspense - the Spense hybrid 2:4-sparse / dense linear layer on AMD Instinct MI355X
+ * (gfx950), hand-written HIP kernels behind a plain C ABI.
+ *
+ * The layer computes Y = X W^T (PyTorch's convention, paper sec. 3.1.1) where the weight
+ * W (N x K, out x in) is stored in the Spense format of sec. 3.2: two contiguous regions,
+ * one pruned to 2:4 (Eq. (1): at most two non-zeros in every aligned group of four
+ * input-dimension entries of a row) and stored compressed as values plus 2-bit
+ * positions (sec. 3.1.1), the other kept dense.  The dense region is the trailing one
+ * (sec. 3.3.2, Table "front_back"):
+ *   - output-split (SPENSE_SPLIT_OUTPUT): rows [0, dense_begin) are 2:4, rows
+ *     [dense_begin, N) are dense; the two parts produce disjoint output columns.
+ *   - input-split (SPENSE_SPLIT_INPUT): columns [0, dense_begin) are 2:4, columns
+ *     [dense_begin, K) are dense; both parts accumulate into the same outputs.
+ * Gate/up-style projections use output-split and down-style ones input-split (sec. 3.2).
+ *
+ * Conventions for every call:
+ *   - All int return values are SPENSE_OK (0) or a negative spense_status.  On error
+ *     nothing has been launched and no output buffer has been written, except where a
+ *     call says otherwise.  spense_last_error() returns a thread-local message.
+ *   - Matrices are row-major with an explicit leading dimension in elements.
+ *   - Device pointers are plain HIP device addresses; the caller allocates and frees
+ *     every buffer.  The library allocates no device or host memory of its own and
+ *     keeps no mutable global state.
+ *   - Calls take a hipStream_t (0 = the null stream) and are asynchronous on it unless
+ *     stated otherwise.
+ */
+#ifndef SPENSE_H_
+#define SPENSE_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SPENSE_ABI_VERSION 1
+
+typedef enum spense_status {
+  SPENSE_OK = 0,
+  SPENSE_ERR_ARG = -1,    /* NULL pointer, negative size, unknown enum, bad split point */
+  SPENSE_ERR_ALIGN = -2,  /* a size or pointer misses the alignment the kernels need */
+  SPENSE_ERR_MASK = -3,   /* the mask keeps more than 2 of 4 in some sparse-region group */
+  SPENSE_ERR_WS = -4,     /* workspace missing or too small */
+  SPENSE_ERR_HIP = -5,    /* a HIP runtime call or kernel launch failed */
+  SPENSE_ERR_DEVICE = -6  /* the current device is not a gfx950 */
+} spense_status;
+
+typedef enum spense_dtype {
+  SPENSE_FP8_E4M3FN = 1, /* OCP fp8 e4m3fn, 1 byte; NaN = 0x7f/0xff, max 448 */
+  SPENSE_BF16 = 2        /* bfloat16, 2 bytes */
+} spense_dtype;
+
+typedef enum spense_split {
+  SPENSE_SPLIT_OUTPUT = 0, /* split along N: 2:4 rows first, dense rows last */
+  SPENSE_SPLIT_INPUT = 1   /* split along K: 2:4 columns first, dense columns last */
+} spense_split;
+
+/* Output flags for spense_gemm / spense_dense_gemm. */
+#define SPENSE_OUT_BF16 0u /* Y is bfloat16, round to nearest even (default) */
+#define SPENSE_OUT_F32 1u  /* Y is fp32 (the value before the bf16 rounding; for tests) */
+
+/*
+ * Geometry of a packed weight, filled by spense_layout.  All counts are in elements
+ * of the weight dtype, except meta_* which count 32-bit words.
+ *
+ * Sparse region (sparse_rows x sparse_cols logical entries):
+ *   values: sparse_rows x values_ld elements; entry (r, 2g + j), j in {0, 1}, is the
+ *           j-th kept value of group g (logical columns 4g..4g+3 of the region) in
+ *           ascending position order.
+ *   meta:   sparse_rows x meta_ld uint32 words; group g of row r owns bits
+ *           [4(g%8), 4(g%8)+4) of word (r, g/8): i0 | i1 << 2 with 0 <= i0 < i1 <= 3 the
+ *           positions of the two stored values inside the group.  Unused bits are 0.
+ * Dense region: dense_rows x dense_ld elements, row-major, the trailing rows (output-
+ *   split) or the trailing columns of every row (input-split) of W unchanged.
+ */
+typedef struct spense_layout_t {
+  int64_t sparse_rows, sparse_cols; /* logical extent of the 2:4 region */
+  int64_t values_ld;                /* = sparse_cols / 2 */
+  int64_t meta_ld;                  /* = sparse_cols / 32 */
+  int64_t dense_rows, dense_cols;
+  int64_t dense_ld; /* = dense_cols */
+  size_t values_bytes, meta_bytes, dense_bytes;
+} spense_layout_t;
+
+/*
+ * A packed weight: POD descriptor plus three caller-owned device buffers laid out as in
+ * spense_layout_t.  The library never takes ownership of the buffers.
+ */
+typedef struct spense_packed_t {
+  int32_t dtype;       /* spense_dtype */
+  int32_t split;       /* spense_split */
+  int64_t N, K;        /* logical weight shape (out x in) */
+  int64_t dense_begin; /* first dense row (output-split) or column (input-split) */
+  void* values;
+  int64_t values_ld;
+  uint32_t* meta;
+  int64_t meta_ld;
+  void* dense;
+  int64_t dense_ld;
+} spense_packed_t;
+
+/*
+ * Fill *out with the packed geometry of an N x K weight split at dense_begin.
+ * Pure host call.  Requirements (SPENSE_ERR_ALIGN otherwise): K % 32 == 0, and for
+ * input-split dense_begin % 32 == 0.  0 <= dense_begin <= N (output) or K (input),
+ * else SPENSE_ERR_ARG.  Sec. 3.2 (format), sec. 3.1.1 (compressed storage).
+ */
+int spense_layout(int64_t N, int64_t K, int32_t dtype, int32_t split, int64_t dense_begin,
+                  spense_layout_t* out);
+
+/* Device workspace (bytes) needed by spense_compress: a counter. */
+size_t spense_compress_workspace_size(void);
+
+/*
+ * Pack W (N x K device matrix, leading dimension ldw elements, dtype codes) into the
+ * Spense format.  mask is an optional N x K device byte matrix (leading dimension ldm);
+ * non-zero means keep.  With mask == NULL an entry is kept when its bit pattern is not
+ * all zeros.  The mask is ignored in the dense region.  A sparse-region group that keeps
+ * fewer than two entries is padded with its smallest non-kept positions holding +0.
+ *
+ * `packed` must have dtype, split, N, K, dense_begin and the three buffer pointers and
+ * leading dimensions set as spense_layout describes (leading dimensions may be larger).
+ * ws: device memory of spense_compress_workspace_size() bytes.
+ *
+ * SYNCHRONOUS: waits for `stream` to finish, to read the count of groups that keep more
+ * than two entries.  If that count is non-zero the call returns SPENSE_ERR_MASK, stores
+ * the count in *bad_groups (if not NULL) and the packed buffers hold unspecified data.
+ * Sec. 3.1.1 (Eq. (1), compressed storage), sec. 3.2 (regions).
+ */
+int spense_compress(const void* W, int64_t ldw, const uint8_t* mask, int64_t ldm, const spense_packed_t* packed,
+                    int64_t* bad_groups, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Inverse of spense_compress: W_out (N x K, leading dimension ldw) receives the dense
+ * matrix, with +0 at every sparse-region position the metadata does not name.
+ * Asynchronous.  A test aid; sec. 3.1.1.
+ */
+int spense_decompress(const spense_packed_t* packed, void* W_out, int64_t ldw, hipStream_t stream);
+
+/*
+ * Device workspace (bytes) that spense_gemm needs for this M and weight; 0 means none.
+ * The workspace holds split-K partial sums and per-tile arrival counters.  Zero-fill it
+ * before its first use: the counters must start at zero.  Every call returns the
+ * counters to zero before it completes, so the same workspace serves later calls in
+ * stream order without clearing.  Calls that may run concurrently (different streams)
+ * need separate workspaces.
+ */
+size_t spense_gemm_workspace_size(int64_t M, const spense_packed_t* packed);
+
+/*
+ * Y = X W^T for a packed Spense weight, in one kernel launch:
+ *   Y[m, n] = round((sum_k x[m, k] * w[n, k]) * w_scale[n] * x_scale[m])
+ * X: M x K device matrix of the weight's dtype, leading dimension ldx (elements).
+ * w_scale: N fp32 per-output-channel scales; x_scale: M fp32 per-token scales; either
+ *   may be NULL, meaning 1.0.  The two multiplications are separate fp32 roundings in
+ *   the order shown.
+ * Y: M x N device matrix, leading dimension ldy (elements), bf16 (round to nearest even)
+ *   or fp32 with SPENSE_OUT_F32.
+ * The sparse region runs on gfx950 structured-sparse matrix instructions, the dense
+ * region on dense ones; with output-split they write disjoint columns, with input-split
+ * one fp32 accumulator crosses the region boundary (no rounding between the regions).
+ * Accumulation is fp32; the summation order differs from a sequential sum.
+ * Alignment (SPENSE_ERR_ALIGN): X, values, meta, dense 16-byte aligned; ldx, values_ld,
+ * dense_ld multiples of 16 bytes; K % 32 == 0 (and dense_begin % 32 for input-split).
+ * Sec. 3.2 (output-split / input-split), sec. 3.1.1.
+ */
+int spense_gemm(const void* X, int64_t M, int64_t ldx, const spense_packed_t* packed, const float* w_scale,
+                const float* x_scale, void* Y, int64_t ldy, uint32_t out_flags, void* ws, size_t ws_bytes,
+                hipStream_t stream);
+
+/* Device workspace (bytes) that spense_dense_gemm needs; same rules as above. */
+size_t spense_dense_gemm_workspace_size(int64_t M, int64_t N, int64_t K, int32_t dtype);
+
+/*
+ * The dense baseline: Y = X W^T for a plain N x K weight W (leading dimension ldw), with
+ * the same scales, epilogue, alignment rules and dense kernel as spense_gemm.  Used as
+ * the speed reference for the Spense format (every weight byte stored).
+ */
+int spense_dense_gemm(const void* X, int64_t M, int64_t ldx, const void* W, int64_t ldw, int64_t N, int64_t K,
+                      int32_t dtype, const float* w_scale, const float* x_scale, void* Y, int64_t ldy,
+                      uint32_t out_flags, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Thread-local description of the last error raised on this thread ("" if none). */
+const char* spense_last_error(void);
+
+/* SPENSE_ABI_VERSION of the built library. */
+int spense_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPENSE_H_ */

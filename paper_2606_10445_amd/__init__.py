@@ -1,0 +1,290 @@
+"""Python binding of libspense: the Spense hybrid 2:4-sparse / dense linear layer on
+MI355X (gfx950).
+
+Argument marshalling only.  Every step of the computation runs in the HIP kernels of
+``libspense.so``; there is no fallback: importing this package without the built
+library raises.  PyTorch is used for device memory and streams.
+
+Low-level functions carry the C names (``spense_layout``, ``spense_compress``,
+``spense_decompress``, ``spense_gemm``, ``spense_dense_gemm``, ...) and take raw
+pointers; ``PackedWeight``, ``compress``, ``gemm`` and ``dense_gemm`` wrap them for torch
+tensors.  Paper: SpenseGPT, sec. 3.1.1 (2:4 storage) and sec. 3.2 (Spense format).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libspense.so")
+
+SPENSE_OK = 0
+SPENSE_ERR_ARG = -1
+SPENSE_ERR_ALIGN = -2
+SPENSE_ERR_MASK = -3
+SPENSE_ERR_WS = -4
+SPENSE_ERR_HIP = -5
+SPENSE_ERR_DEVICE = -6
+SPENSE_FP8_E4M3FN = 1
+SPENSE_BF16 = 2
+SPENSE_SPLIT_OUTPUT = 0
+SPENSE_SPLIT_INPUT = 1
+SPENSE_OUT_BF16 = 0
+SPENSE_OUT_F32 = 1
+
+EXPORTS = ["spense_abi_version", "spense_last_error", "spense_layout", "spense_compress_workspace_size",
+           "spense_compress", "spense_decompress", "spense_gemm_workspace_size", "spense_gemm",
+           "spense_dense_gemm_workspace_size", "spense_dense_gemm"]
+
+
+class SpenseError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"spense error {code}: {msg}")
+        self.code = code
+
+
+class spense_layout_t(ctypes.Structure):
+    _fields_ = [("sparse_rows", ctypes.c_int64), ("sparse_cols", ctypes.c_int64), ("values_ld", ctypes.c_int64),
+                ("meta_ld", ctypes.c_int64), ("dense_rows", ctypes.c_int64), ("dense_cols", ctypes.c_int64),
+                ("dense_ld", ctypes.c_int64), ("values_bytes", ctypes.c_size_t), ("meta_bytes", ctypes.c_size_t),
+                ("dense_bytes", ctypes.c_size_t)]
+
+
+class spense_packed_t(ctypes.Structure):
+    _fields_ = [("dtype", ctypes.c_int32), ("split", ctypes.c_int32), ("N", ctypes.c_int64), ("K", ctypes.c_int64),
+                ("dense_begin", ctypes.c_int64), ("values", ctypes.c_void_p), ("values_ld", ctypes.c_int64),
+                ("meta", ctypes.c_void_p), ("meta_ld", ctypes.c_int64), ("dense", ctypes.c_void_p),
+                ("dense_ld", ctypes.c_int64)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2606_10445_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    p, i64, i32, u32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_uint32, ctypes.c_size_t
+    P = ctypes.POINTER
+    sig = {
+        "spense_abi_version": (ctypes.c_int, []),
+        "spense_last_error": (ctypes.c_char_p, []),
+        "spense_layout": (ctypes.c_int, [i64, i64, i32, i32, i64, P(spense_layout_t)]),
+        "spense_compress_workspace_size": (sz, []),
+        "spense_compress": (ctypes.c_int, [p, i64, p, i64, P(spense_packed_t), P(i64), p, sz, p]),
+        "spense_decompress": (ctypes.c_int, [P(spense_packed_t), p, i64, p]),
+        "spense_gemm_workspace_size": (sz, [i64, P(spense_packed_t)]),
+        "spense_gemm": (ctypes.c_int, [p, i64, i64, P(spense_packed_t), p, p, p, i64, u32, p, sz, p]),
+        "spense_dense_gemm_workspace_size": (sz, [i64, i64, i64, i32]),
+        "spense_dense_gemm": (ctypes.c_int, [p, i64, i64, p, i64, i64, i64, i32, p, p, p, i64, u32, p, sz, p]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+    return lib
+
+
+_lib = _load()
+
+
+# ------------------------------------------------------------------ raw C calls
+def spense_abi_version() -> int:
+    return _lib.spense_abi_version()
+
+
+def spense_last_error() -> str:
+    return _lib.spense_last_error().decode()
+
+
+def _check(rc: int):
+    if rc != SPENSE_OK:
+        raise SpenseError(rc, spense_last_error())
+
+
+def spense_layout(N: int, K: int, dtype: int, split: int, dense_begin: int) -> spense_layout_t:
+    L = spense_layout_t()
+    _check(_lib.spense_layout(N, K, dtype, split, dense_begin, ctypes.byref(L)))
+    return L
+
+
+def spense_compress_workspace_size() -> int:
+    return _lib.spense_compress_workspace_size()
+
+
+def spense_compress(W, ldw, mask, ldm, packed: spense_packed_t, ws, ws_bytes, stream) -> tuple[int, int]:
+    """Returns (status, bad_groups); does not raise so callers can inspect the count."""
+    bad = ctypes.c_int64(0)
+    rc = _lib.spense_compress(W, ldw, mask, ldm, ctypes.byref(packed), ctypes.byref(bad), ws, ws_bytes, stream)
+    return rc, bad.value
+
+
+def spense_decompress(packed: spense_packed_t, W_out, ldw, stream) -> int:
+    return _lib.spense_decompress(ctypes.byref(packed), W_out, ldw, stream)
+
+
+def spense_gemm_workspace_size(M: int, packed: spense_packed_t) -> int:
+    return _lib.spense_gemm_workspace_size(M, ctypes.byref(packed))
+
+
+def spense_gemm(X, M, ldx, packed: spense_packed_t, w_scale, x_scale, Y, ldy, out_flags, ws, ws_bytes,
+                stream) -> int:
+    return _lib.spense_gemm(X, M, ldx, ctypes.byref(packed), w_scale, x_scale, Y, ldy, out_flags, ws, ws_bytes,
+                            stream)
+
+
+def spense_dense_gemm_workspace_size(M: int, N: int, K: int, dtype: int) -> int:
+    return _lib.spense_dense_gemm_workspace_size(M, N, K, dtype)
+
+
+def spense_dense_gemm(X, M, ldx, W, ldw, N, K, dtype, w_scale, x_scale, Y, ldy, out_flags, ws, ws_bytes,
+                      stream) -> int:
+    return _lib.spense_dense_gemm(X, M, ldx, W, ldw, N, K, dtype, w_scale, x_scale, Y, ldy, out_flags, ws, ws_bytes,
+                                  stream)
+
+
+# ------------------------------------------------------------------ torch helpers
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype in (torch.uint8, torch.float8_e4m3fn):
+        return SPENSE_FP8_E4M3FN
+    if t.dtype in (torch.bfloat16, torch.int16, torch.uint16):
+        return SPENSE_BF16
+    raise TypeError(f"unsupported weight dtype {t.dtype}")
+
+
+def _storage_dtype(dtype: int):
+    return torch.uint8 if dtype == SPENSE_FP8_E4M3FN else torch.int16
+
+
+def _stream(device) -> int:
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _row_major(t: torch.Tensor, name: str):
+    if t.dim() != 2 or t.stride(1) != 1:
+        raise ValueError(f"{name} must be a 2-D row-major tensor")
+
+
+class Workspace:
+    """A zero-filled device buffer the library leaves zero-filled after every call."""
+
+    def __init__(self, device):
+        self.device = torch.device(device)
+        self.buf = None
+
+    def get(self, nbytes: int):
+        if nbytes == 0:
+            return None, 0
+        if self.buf is None or self.buf.numel() < nbytes:
+            self.buf = torch.zeros(max(nbytes, 1 << 20), dtype=torch.uint8, device=self.device)
+        return self.buf.data_ptr(), self.buf.numel()
+
+
+_workspaces: dict = {}
+
+
+def workspace_for(device) -> Workspace:
+    d = torch.device(device)
+    key = (d.type, d.index if d.index is not None else torch.cuda.current_device())
+    if key not in _workspaces:
+        _workspaces[key] = Workspace(torch.device("cuda", key[1]))
+    return _workspaces[key]
+
+
+class PackedWeight:
+    """A weight in the Spense format: device buffers (values, meta, dense) + descriptor."""
+
+    def __init__(self, N, K, dtype, split, dense_begin, values, meta, dense):
+        self.N, self.K, self.dtype, self.split, self.dense_begin = N, K, dtype, split, dense_begin
+        self.values, self.meta, self.dense = values, meta, dense
+        self.layout = spense_layout(N, K, dtype, split, dense_begin)
+        self.desc = spense_packed_t(dtype, split, N, K, dense_begin, _ptr(values), self.layout.values_ld, _ptr(meta),
+                                    self.layout.meta_ld, _ptr(dense), self.layout.dense_ld)
+
+    @classmethod
+    def empty(cls, N, K, dtype, split, dense_begin, device="cuda"):
+        L = spense_layout(N, K, dtype, split, dense_begin)
+        st = _storage_dtype(dtype)
+        values = torch.empty((L.sparse_rows, L.values_ld), dtype=st, device=device)
+        meta = torch.empty((L.sparse_rows, L.meta_ld), dtype=torch.int32, device=device)
+        dense = torch.empty((L.dense_rows, L.dense_ld), dtype=st, device=device)
+        return cls(N, K, dtype, split, dense_begin, values, meta, dense)
+
+    def weight_bytes(self) -> int:
+        return self.layout.values_bytes + self.layout.meta_bytes + self.layout.dense_bytes
+
+
+def compress(W: torch.Tensor, mask: torch.Tensor | None, split: int, dense_begin: int) -> PackedWeight:
+    """Pack a device weight (codes) into the Spense format with spense_compress."""
+    _row_major(W, "W")
+    dtype = _dtype_code(W)
+    N, K = W.shape
+    pw = PackedWeight.empty(N, K, dtype, split, dense_begin, device=W.device)
+    if mask is not None:
+        _row_major(mask, "mask")
+        if mask.shape != W.shape or mask.dtype != torch.uint8 or mask.device != W.device:
+            raise ValueError("mask must be a uint8 tensor of W's shape on W's device")
+    ws = torch.zeros(spense_compress_workspace_size(), dtype=torch.uint8, device=W.device)
+    rc, bad = spense_compress(_ptr(W), W.stride(0), _ptr(mask), 0 if mask is None else mask.stride(0), pw.desc,
+                              ws.data_ptr(), ws.numel(), _stream(W.device))
+    if rc != SPENSE_OK:
+        err = SpenseError(rc, spense_last_error())
+        err.bad_groups = bad
+        raise err
+    return pw
+
+
+def decompress(pw: PackedWeight) -> torch.Tensor:
+    dev = (pw.dense if pw.dense.numel() else pw.values).device
+    W = torch.empty((pw.N, pw.K), dtype=_storage_dtype(pw.dtype), device=dev)
+    _check(spense_decompress(pw.desc, _ptr(W), W.stride(0), _stream(dev)))
+    return W
+
+
+def _check_scale(s, n, dev, name):
+    if s is None:
+        return
+    if s.dtype != torch.float32 or s.dim() != 1 or s.shape[0] != n or not s.is_contiguous() or s.device != dev:
+        raise ValueError(f"{name} must be a contiguous fp32 vector of length {n} on {dev}")
+
+
+def gemm(X: torch.Tensor, pw: PackedWeight, w_scale=None, x_scale=None, out=None, out_f32=False,
+         workspace: Workspace | None = None) -> torch.Tensor:
+    """Y = X W^T for a packed weight (spense_gemm)."""
+    _row_major(X, "X")
+    M = X.shape[0]
+    _check_scale(w_scale, pw.N, X.device, "w_scale")
+    _check_scale(x_scale, M, X.device, "x_scale")
+    if X.shape[1] != pw.K:
+        raise ValueError("X.shape[1] != K")
+    if out is None:
+        out = torch.empty((M, pw.N), dtype=torch.float32 if out_f32 else torch.bfloat16, device=X.device)
+    ws = workspace or workspace_for(X.device)
+    need = spense_gemm_workspace_size(M, pw.desc)
+    wp, wn = ws.get(need)
+    _check(spense_gemm(_ptr(X), M, X.stride(0), pw.desc, _ptr(w_scale), _ptr(x_scale), _ptr(out), out.stride(0),
+                       SPENSE_OUT_F32 if out_f32 else SPENSE_OUT_BF16, wp, wn, _stream(X.device)))
+    return out
+
+
+def dense_gemm(X: torch.Tensor, W: torch.Tensor, w_scale=None, x_scale=None, out=None, out_f32=False,
+               workspace: Workspace | None = None) -> torch.Tensor:
+    """The dense baseline Y = X W^T (spense_dense_gemm)."""
+    _row_major(X, "X")
+    _row_major(W, "W")
+    dtype = _dtype_code(W)
+    M, K = X.shape
+    N = W.shape[0]
+    _check_scale(w_scale, N, X.device, "w_scale")
+    _check_scale(x_scale, M, X.device, "x_scale")
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.float32 if out_f32 else torch.bfloat16, device=X.device)
+    ws = workspace or workspace_for(X.device)
+    wp, wn = ws.get(spense_dense_gemm_workspace_size(M, N, K, dtype))
+    _check(spense_dense_gemm(_ptr(X), M, X.stride(0), _ptr(W), W.stride(0), N, K, dtype, _ptr(w_scale),
+                             _ptr(x_scale), _ptr(out), out.stride(0), SPENSE_OUT_F32 if out_f32 else SPENSE_OUT_BF16,
+                             wp, wn, _stream(X.device)))
+    return out

@@ -1,0 +1,407 @@
+// Host side of libspense: argument validation (no device synchronisation except in
+// spense_compress), work planning and kernel dispatch.  See include/spense.h.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <atomic>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <string>
+
+#include "../../include/spense.h"
+#include "spense_internal.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int ok() {
+  g_err.clear();
+  return SPENSE_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int esize(int32_t dtype) { return dtype == SPENSE_FP8_E4M3FN ? 1 : 2; }
+
+// Per-device cache of "is this a gfx950" (0 unknown, 1 yes, 2 no).
+std::atomic<int> g_arch[64];
+
+int check_device() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return fail(SPENSE_ERR_HIP, "hipGetDevice failed");
+  if (dev < 0 || dev >= 64) return fail(SPENSE_ERR_DEVICE, "device index %d out of range", dev);
+  int st = g_arch[dev].load(std::memory_order_relaxed);
+  if (st == 0) {
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return fail(SPENSE_ERR_HIP, "hipGetDeviceProperties failed");
+    st = strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : 2;
+    g_arch[dev].store(st, std::memory_order_relaxed);
+  }
+  if (st != 1) return fail(SPENSE_ERR_DEVICE, "libspense needs a gfx950 (MI355X) device");
+  return SPENSE_OK;
+}
+
+int layout_impl(int64_t N, int64_t K, int32_t dtype, int32_t split, int64_t dense_begin, spense_layout_t* L) {
+  if (!L) return fail(SPENSE_ERR_ARG, "layout: out is NULL");
+  if (dtype != SPENSE_FP8_E4M3FN && dtype != SPENSE_BF16) return fail(SPENSE_ERR_ARG, "unknown dtype %d", dtype);
+  if (split != SPENSE_SPLIT_OUTPUT && split != SPENSE_SPLIT_INPUT)
+    return fail(SPENSE_ERR_ARG, "unknown split %d", split);
+  if (N < 0 || K < 0) return fail(SPENSE_ERR_ARG, "negative shape N=%lld K=%lld", (long long)N, (long long)K);
+  if (N > INT32_MAX || K > INT32_MAX) return fail(SPENSE_ERR_ARG, "shape too large");
+  if (K % 32) return fail(SPENSE_ERR_ALIGN, "K=%lld is not a multiple of 32", (long long)K);
+  const int64_t extent = split == SPENSE_SPLIT_OUTPUT ? N : K;
+  if (dense_begin < 0 || dense_begin > extent)
+    return fail(SPENSE_ERR_ARG, "dense_begin=%lld outside [0, %lld]", (long long)dense_begin, (long long)extent);
+  if (split == SPENSE_SPLIT_INPUT && dense_begin % 32)
+    return fail(SPENSE_ERR_ALIGN, "input-split dense_begin=%lld is not a multiple of 32", (long long)dense_begin);
+  const int es = esize(dtype);
+  if (split == SPENSE_SPLIT_OUTPUT) {
+    L->sparse_rows = dense_begin;
+    L->sparse_cols = K;
+    L->dense_rows = N - dense_begin;
+    L->dense_cols = K;
+  } else {
+    L->sparse_rows = N;
+    L->sparse_cols = dense_begin;
+    L->dense_rows = N;
+    L->dense_cols = K - dense_begin;
+  }
+  L->values_ld = L->sparse_cols / 2;
+  L->meta_ld = L->sparse_cols / 32;
+  L->dense_ld = L->dense_cols;
+  L->values_bytes = (size_t)(L->sparse_rows * L->values_ld * es);
+  L->meta_bytes = (size_t)(L->sparse_rows * L->meta_ld * 4);
+  L->dense_bytes = (size_t)(L->dense_rows * L->dense_ld * es);
+  return ok();
+}
+
+// Validate a packed descriptor against its own geometry.
+int check_packed(const spense_packed_t* P, spense_layout_t* L) {
+  if (!P) return fail(SPENSE_ERR_ARG, "packed is NULL");
+  int rc = layout_impl(P->N, P->K, P->dtype, P->split, P->dense_begin, L);
+  if (rc) return rc;
+  const int es = esize(P->dtype);
+  if (L->sparse_rows > 0 && L->sparse_cols > 0) {
+    if (!P->values || !P->meta) return fail(SPENSE_ERR_ARG, "values/meta NULL with a non-empty 2:4 region");
+    if (P->values_ld < L->values_ld || P->meta_ld < L->meta_ld)
+      return fail(SPENSE_ERR_ARG, "values_ld/meta_ld smaller than the region");
+    if (!aligned16(P->values) || (P->values_ld * es) % 16)
+      return fail(SPENSE_ERR_ALIGN, "values must be 16-byte aligned with a 16-byte multiple row pitch");
+    if ((reinterpret_cast<uintptr_t>(P->meta) & 3u)) return fail(SPENSE_ERR_ALIGN, "meta must be 4-byte aligned");
+  }
+  if (L->dense_rows > 0 && L->dense_cols > 0) {
+    if (!P->dense) return fail(SPENSE_ERR_ARG, "dense NULL with a non-empty dense region");
+    if (P->dense_ld < L->dense_ld) return fail(SPENSE_ERR_ARG, "dense_ld smaller than the region");
+    if (!aligned16(P->dense) || (P->dense_ld * es) % 16)
+      return fail(SPENSE_ERR_ALIGN, "dense must be 16-byte aligned with a 16-byte multiple row pitch");
+  }
+  return SPENSE_OK;
+}
+
+// ------------------------------------------------------------------ planning
+struct Plan {
+  spense::LaunchShape ls;
+  spense::GemmArgs args;  // geometry part filled
+  size_t part_bytes;      // split-K partials
+  size_t ws_bytes;
+};
+
+// Workspace layout: [arrival counters, fixed kCounterBytes][split-K partials].  The
+// counters sit at the same place for every plan, so partial sums written by one call can
+// never land on counters used by a later call with a different decomposition.
+constexpr size_t kCounterBytes = 256 * 1024;
+constexpr int64_t kMaxCounters = kCounterBytes / 4;
+
+int env_int(const char* name, int dflt) {
+  const char* v = getenv(name);
+  if (!v || !*v) return dflt;
+  return atoi(v);
+}
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// The plan depends only on the dtype, M, and the regions' (rows, K ranges), so the same
+// geometry always gets the same decomposition and the same summation order.
+void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, int64_t dense_begin, Plan* pl) {
+  using spense::Region;
+  memset(pl, 0, sizeof *pl);
+  const int es = esize(dtype);
+  const int64_t gran = dtype == SPENSE_FP8_E4M3FN ? 128 : 64;  // K per 2:4 instruction
+  const double sparse_cost = 0.5 * es + 0.125;                 // bytes per logical 2:4 entry
+  const int ct = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
+  const int rt = env_int("SPENSE_RT", 1) == 2 ? 2 : 1;
+  const int waves = 4;
+  const int rows_per_unit = 16 * rt * waves;
+  const int64_t target_units = std::max(1, env_int("SPENSE_TARGET_UNITS", 1024));
+  const int64_t min_split_k = std::max(32, env_int("SPENSE_MIN_SPLIT_K", 1024));
+  pl->ls.ct = ct;
+  pl->ls.rt = rt;
+  pl->ls.waves = waves;
+  pl->ls.mblocks = (int)ceil_div(M, 16 * ct);
+
+  Region regs[2];
+  int nreg = 0;
+  auto add = [&](int64_t row0, int64_t rows, int64_t kbound, int64_t dro, int64_t dco) {
+    Region r;
+    memset(&r, 0, sizeof r);
+    r.row0 = (int32_t)row0;
+    r.rows = (int32_t)rows;
+    r.kbeg = 0;
+    r.kend = (int32_t)K;
+    r.kbound = (int32_t)kbound;
+    r.dense_row_off = (int32_t)dro;
+    r.dense_col_off = (int32_t)dco;
+    r.nrb = (int32_t)ceil_div(rows, rows_per_unit);
+    regs[nreg++] = r;
+  };
+  if (split == SPENSE_SPLIT_OUTPUT) {
+    if (dense_begin > 0) add(0, dense_begin, K, 0, 0);
+    if (N - dense_begin > 0) add(dense_begin, N - dense_begin, 0, dense_begin, 0);
+  } else if (N > 0) {
+    add(0, N, dense_begin, 0, dense_begin);
+  }
+  // cost of the K prefix [0, k) of one row of a region, in bytes
+  auto cost = [&](const Region& r, double k) {
+    const double ks = std::min<double>(k, r.kbound);
+    return sparse_cost * ks + es * std::max(0.0, k - r.kbound);
+  };
+  auto inv_cost = [&](const Region& r, double c) {
+    const double cs = sparse_cost * r.kbound;
+    return c <= cs ? c / sparse_cost : r.kbound + (c - cs) / es;
+  };
+  double total = 0;
+  int64_t counters_needed = 0;
+  for (int i = 0; i < nreg; ++i) {
+    total += regs[i].rows * cost(regs[i], (double)K);
+    counters_needed += (int64_t)regs[i].nrb * pl->ls.mblocks;
+  }
+  const bool may_split = counters_needed <= kMaxCounters;
+  int32_t unit = 0, ctr = 0, max_s = 1;
+  for (int i = 0; i < nreg; ++i) {
+    Region& r = regs[i];
+    const double rc = r.rows * cost(r, (double)K);
+    int64_t want = 1;
+    if (may_split && total > 0) {
+      want = (int64_t)std::llround(rc / total * (double)target_units /
+                                   ((double)std::max<int32_t>(1, r.nrb) * pl->ls.mblocks));
+      want = std::max<int64_t>(1, std::min<int64_t>(want, std::max<int64_t>(1, K / min_split_k)));
+      want = std::min<int64_t>(want, spense::kMaxSplits);
+    }
+    // cut [0, K) into `want` pieces of equal byte cost, on multiples of the instruction K
+    const double row_cost = cost(r, (double)K);
+    int n = 0;
+    r.cut[n++] = 0;
+    for (int64_t j = 1; j < want; ++j) {
+      int64_t k = (int64_t)std::llround(inv_cost(r, row_cost * j / want) / gran) * gran;
+      if (k > r.cut[n - 1] && k < K) r.cut[n++] = (int32_t)k;
+    }
+    r.cut[n++] = (int32_t)K;
+    r.splits = n - 1;
+    r.unit0 = unit;
+    r.ctr0 = ctr;
+    unit += r.nrb * r.splits;
+    ctr += r.nrb;
+    max_s = std::max(max_s, (int)r.splits);
+  }
+  spense::GemmArgs& a = pl->args;
+  a.nreg = nreg;
+  for (int i = 0; i < nreg; ++i) a.reg[i] = regs[i];
+  a.units = unit;
+  a.counters_per_mb = ctr;
+  if (max_s > 1 && M > 0) {
+    pl->part_bytes = (size_t)max_s * (size_t)M * (size_t)N * 4;
+    pl->ws_bytes = kCounterBytes + pl->part_bytes;
+  }
+}
+
+int gemm_common(const void* X, int64_t M, int64_t ldx, int32_t dtype, int32_t split, int64_t N, int64_t K,
+                int64_t dense_begin, const void* values, int64_t values_ld, const uint32_t* meta, int64_t meta_ld,
+                const void* dense, int64_t dense_ld, const float* w_scale, const float* x_scale, void* Y, int64_t ldy,
+                uint32_t out_flags, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (M < 0) return fail(SPENSE_ERR_ARG, "negative M");
+  if (M > INT32_MAX) return fail(SPENSE_ERR_ARG, "M too large");
+  if (out_flags & ~1u) return fail(SPENSE_ERR_ARG, "unknown out_flags 0x%x", out_flags);
+  if (M == 0 || N == 0) return ok();
+  const int es = esize(dtype);
+  if (!Y) return fail(SPENSE_ERR_ARG, "Y is NULL");
+  if (ldy < N) return fail(SPENSE_ERR_ARG, "ldy=%lld < N=%lld", (long long)ldy, (long long)N);
+  if (K > 0) {
+    if (!X) return fail(SPENSE_ERR_ARG, "X is NULL");
+    if (ldx < K) return fail(SPENSE_ERR_ARG, "ldx=%lld < K=%lld", (long long)ldx, (long long)K);
+    if (!aligned16(X) || (ldx * es) % 16)
+      return fail(SPENSE_ERR_ALIGN, "X must be 16-byte aligned with a 16-byte multiple row pitch");
+  }
+  const int out_es = (out_flags & SPENSE_OUT_F32) ? 4 : 2;
+  if ((reinterpret_cast<uintptr_t>(Y) % out_es)) return fail(SPENSE_ERR_ALIGN, "Y misaligned");
+  if ((int64_t)M * ldy > (int64_t)1 << 40) return fail(SPENSE_ERR_ARG, "Y too large");
+  Plan pl;
+  make_plan(dtype, M, N, split, K, dense_begin, &pl);
+  if (pl.ws_bytes > 0) {
+    if (!ws || ws_bytes < pl.ws_bytes)
+      return fail(SPENSE_ERR_WS, "workspace of %zu bytes needed, %zu given", pl.ws_bytes, ws ? ws_bytes : (size_t)0);
+    if (!aligned16(ws)) return fail(SPENSE_ERR_ALIGN, "workspace must be 16-byte aligned");
+  }
+  int rc = check_device();
+  if (rc) return rc;
+  spense::GemmArgs& a = pl.args;
+  a.X = static_cast<const uint8_t*>(X);
+  a.ldx_b = ldx * es;
+  a.values = static_cast<const uint8_t*>(values);
+  a.v_ld_b = values_ld * es;
+  a.meta = meta;
+  a.m_ld = meta_ld;
+  a.dense = static_cast<const uint8_t*>(dense);
+  a.d_ld_b = dense_ld * es;
+  a.sw = w_scale;
+  a.sx = x_scale;
+  a.Y = Y;
+  a.ldy = ldy;
+  a.M = (int32_t)M;
+  a.N = (int32_t)N;
+  a.out_f32 = (out_flags & SPENSE_OUT_F32) ? 1 : 0;
+  bool vec = (ldy % 4 == 0) && (reinterpret_cast<uintptr_t>(Y) % (4 * out_es) == 0);
+  for (int i = 0; i < a.nreg; ++i) vec = vec && (a.reg[i].row0 % 4 == 0);
+  a.vec_store = vec ? 1 : 0;
+  a.counters = pl.ws_bytes ? static_cast<uint32_t*>(ws) : nullptr;
+  a.part = pl.ws_bytes ? reinterpret_cast<float*>(static_cast<char*>(ws) + kCounterBytes) : nullptr;
+  if (a.units == 0) return ok();
+  hipError_t e = spense::launch_gemm(dtype, pl.ls, a, stream);
+  if (e != hipSuccess) return fail(SPENSE_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+int spense_abi_version(void) { return SPENSE_ABI_VERSION; }
+
+const char* spense_last_error(void) { return g_err.c_str(); }
+
+int spense_layout(int64_t N, int64_t K, int32_t dtype, int32_t split, int64_t dense_begin, spense_layout_t* out) {
+  return layout_impl(N, K, dtype, split, dense_begin, out);
+}
+
+size_t spense_compress_workspace_size(void) { return 256; }
+
+int spense_compress(const void* W, int64_t ldw, const uint8_t* mask, int64_t ldm, const spense_packed_t* packed,
+                    int64_t* bad_groups, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (bad_groups) *bad_groups = 0;
+  spense_layout_t L;
+  int rc = check_packed(packed, &L);
+  if (rc) return rc;
+  const int64_t N = packed->N, K = packed->K;
+  const int es = esize(packed->dtype);
+  if (N == 0 || K == 0) return ok();
+  if (!W) return fail(SPENSE_ERR_ARG, "W is NULL");
+  if (ldw < K) return fail(SPENSE_ERR_ARG, "ldw < K");
+  if (!aligned16(W) || (ldw * es) % 16) return fail(SPENSE_ERR_ALIGN, "W must be 16-byte aligned, 16-byte pitch");
+  if (mask) {
+    if (ldm < K) return fail(SPENSE_ERR_ARG, "ldm < K");
+    if (!aligned16(mask) || ldm % 16) return fail(SPENSE_ERR_ALIGN, "mask must be 16-byte aligned, 16-byte pitch");
+  }
+  if (!ws || ws_bytes < spense_compress_workspace_size() || (reinterpret_cast<uintptr_t>(ws) & 7u))
+    return fail(SPENSE_ERR_WS, "compress needs an 8-byte aligned workspace of %zu bytes",
+                spense_compress_workspace_size());
+  rc = check_device();
+  if (rc) return rc;
+  unsigned long long* bad = static_cast<unsigned long long*>(ws);
+  hipError_t e = spense::launch_zero_u64(bad, stream);
+  if (e != hipSuccess) return fail(SPENSE_ERR_HIP, "launch failed: %s", hipGetErrorString(e));
+  const uint8_t* w8 = static_cast<const uint8_t*>(W);
+  const uint8_t* dsrc = packed->split == SPENSE_SPLIT_OUTPUT ? w8 + packed->dense_begin * ldw * es
+                                                              : w8 + packed->dense_begin * es;
+  e = spense::launch_compress(packed->dtype, w8, ldw * es, mask, ldm, L.sparse_rows, L.sparse_cols,
+                              static_cast<uint8_t*>(packed->values), packed->values_ld * es, packed->meta,
+                              packed->meta_ld, dsrc, L.dense_rows, L.dense_cols * es,
+                              static_cast<uint8_t*>(packed->dense), packed->dense_ld * es, bad, stream);
+  if (e != hipSuccess) return fail(SPENSE_ERR_HIP, "launch failed: %s", hipGetErrorString(e));
+  unsigned long long host_bad = 0;
+  e = hipMemcpyAsync(&host_bad, bad, sizeof host_bad, hipMemcpyDeviceToHost, stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  if (e != hipSuccess) return fail(SPENSE_ERR_HIP, "compress failed: %s", hipGetErrorString(e));
+  if (bad_groups) *bad_groups = (int64_t)host_bad;
+  if (host_bad) return fail(SPENSE_ERR_MASK, "%llu group(s) of the 2:4 region keep more than 2 of 4", host_bad);
+  return ok();
+}
+
+int spense_decompress(const spense_packed_t* packed, void* W_out, int64_t ldw, hipStream_t stream) {
+  spense_layout_t L;
+  int rc = check_packed(packed, &L);
+  if (rc) return rc;
+  const int64_t N = packed->N, K = packed->K;
+  const int es = esize(packed->dtype);
+  if (N == 0 || K == 0) return ok();
+  if (!W_out) return fail(SPENSE_ERR_ARG, "W_out is NULL");
+  if (ldw < K) return fail(SPENSE_ERR_ARG, "ldw < K");
+  if (!aligned16(W_out) || (ldw * es) % 16) return fail(SPENSE_ERR_ALIGN, "W_out must be 16-byte aligned");
+  rc = check_device();
+  if (rc) return rc;
+  uint8_t* w8 = static_cast<uint8_t*>(W_out);
+  uint8_t* ddst = packed->split == SPENSE_SPLIT_OUTPUT ? w8 + packed->dense_begin * ldw * es
+                                                       : w8 + packed->dense_begin * es;
+  hipError_t e = spense::launch_decompress(packed->dtype, static_cast<const uint8_t*>(packed->values),
+                                           packed->values_ld * es, packed->meta, packed->meta_ld, L.sparse_rows,
+                                           L.sparse_cols, w8, ldw * es, static_cast<const uint8_t*>(packed->dense),
+                                           packed->dense_ld * es, L.dense_rows, L.dense_cols * es, ddst, stream);
+  if (e != hipSuccess) return fail(SPENSE_ERR_HIP, "launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+size_t spense_gemm_workspace_size(int64_t M, const spense_packed_t* packed) {
+  spense_layout_t L;
+  if (M <= 0 || check_packed(packed, &L)) return 0;
+  Plan pl;
+  make_plan(packed->dtype, M, packed->N, packed->split, packed->K, packed->dense_begin, &pl);
+  return pl.ws_bytes;
+}
+
+int spense_gemm(const void* X, int64_t M, int64_t ldx, const spense_packed_t* packed, const float* w_scale,
+                const float* x_scale, void* Y, int64_t ldy, uint32_t out_flags, void* ws, size_t ws_bytes,
+                hipStream_t stream) {
+  spense_layout_t L;
+  int rc = check_packed(packed, &L);
+  if (rc) return rc;
+  return gemm_common(X, M, ldx, packed->dtype, packed->split, packed->N, packed->K, packed->dense_begin,
+                     packed->values, packed->values_ld, packed->meta, packed->meta_ld, packed->dense,
+                     packed->dense_ld, w_scale, x_scale, Y, ldy, out_flags, ws, ws_bytes, stream);
+}
+
+size_t spense_dense_gemm_workspace_size(int64_t M, int64_t N, int64_t K, int32_t dtype) {
+  spense_layout_t L;
+  if (M <= 0 || layout_impl(N, K, dtype, SPENSE_SPLIT_OUTPUT, 0, &L)) return 0;
+  Plan pl;
+  make_plan(dtype, M, N, SPENSE_SPLIT_OUTPUT, K, 0, &pl);
+  return pl.ws_bytes;
+}
+
+int spense_dense_gemm(const void* X, int64_t M, int64_t ldx, const void* W, int64_t ldw, int64_t N, int64_t K,
+                      int32_t dtype, const float* w_scale, const float* x_scale, void* Y, int64_t ldy,
+                      uint32_t out_flags, void* ws, size_t ws_bytes, hipStream_t stream) {
+  spense_layout_t L;
+  int rc = layout_impl(N, K, dtype, SPENSE_SPLIT_OUTPUT, 0, &L);
+  if (rc) return rc;
+  const int es = esize(dtype);
+  if (N > 0 && K > 0) {
+    if (!W) return fail(SPENSE_ERR_ARG, "W is NULL");
+    if (ldw < K) return fail(SPENSE_ERR_ARG, "ldw < K");
+    if (!aligned16(W) || (ldw * es) % 16) return fail(SPENSE_ERR_ALIGN, "W must be 16-byte aligned, 16-byte pitch");
+  }
+  return gemm_common(X, M, ldx, dtype, SPENSE_SPLIT_OUTPUT, N, K, 0, nullptr, 0, nullptr, 0, W, ldw, w_scale, x_scale,
+                     Y, ldy, out_flags, ws, ws_bytes, stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,76 @@
+// Internal declarations shared by the libspense translation units (host + device).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace spense {
+
+enum : int32_t { kFP8 = 1, kBF16 = 2 };
+enum : int32_t { kSplitOutput = 0, kSplitInput = 1 };
+
+constexpr int kMaxSplits = 32;
+
+// One contiguous part of the weight covered by a set of work units: a range of output
+// rows and a logical K range [kbeg, kend) whose columns below kbound are stored 2:4 and
+// the rest dense.  Output-split has up to two regions (2:4 rows with kbound = K, dense
+// rows with kbound = 0); input-split has one region with kbound = the first dense column,
+// so a unit whose K range contains kbound runs the 2:4 loop and then the dense loop into
+// the same fp32 accumulator.
+struct Region {
+  int32_t row0, rows;                // output rows [row0, row0 + rows)
+  int32_t kbeg, kend, kbound;        // K range, first dense column
+  int32_t dense_row_off;             // dense storage row = n - dense_row_off
+  int32_t dense_col_off;             // dense storage column = k - dense_col_off
+  int32_t nrb;                       // row blocks
+  int32_t splits;                    // K pieces per row block
+  int32_t unit0;                     // first work unit of this region
+  int32_t ctr0;                      // first arrival counter of this region
+  int32_t cut[kMaxSplits + 1];       // K piece boundaries, cut[0] = kbeg, cut[splits] = kend
+};
+
+struct GemmArgs {
+  const uint8_t* X;
+  int64_t ldx_b;  // bytes
+  const uint8_t* values;
+  int64_t v_ld_b;  // bytes per 2:4 row
+  const uint32_t* meta;
+  int64_t m_ld;  // words per 2:4 row
+  const uint8_t* dense;
+  int64_t d_ld_b;  // bytes per dense row
+  const float* sw;
+  const float* sx;
+  void* Y;
+  int64_t ldy;  // elements
+  float* part;  // split-K partial sums [split][M][N]
+  uint32_t* counters;
+  int32_t M, N;
+  int32_t out_f32;
+  int32_t vec_store;  // 4 consecutive outputs may be stored as one vector
+  int32_t nreg;
+  int32_t units;
+  int32_t counters_per_mb;
+  int32_t pad_;
+  Region reg[2];
+};
+
+struct LaunchShape {
+  int ct;       // 16-column tiles of M per unit (1, 2, 4)
+  int rt;       // 16-row tiles per wave
+  int waves;    // waves per workgroup
+  int mblocks;  // grid.y
+};
+
+hipError_t launch_gemm(int dtype, const LaunchShape& ls, const GemmArgs& a, hipStream_t s);
+
+hipError_t launch_compress(int dtype, const uint8_t* W, int64_t ldw_b, const uint8_t* mask, int64_t ldm,
+                           int64_t s_rows, int64_t s_cols, uint8_t* values, int64_t v_ld_b, uint32_t* meta,
+                           int64_t m_ld, const uint8_t* dsrc, int64_t d_rows, int64_t d_cols_b, uint8_t* dense,
+                           int64_t d_ld_b, unsigned long long* bad, hipStream_t s);
+
+hipError_t launch_decompress(int dtype, const uint8_t* values, int64_t v_ld_b, const uint32_t* meta, int64_t m_ld,
+                             int64_t s_rows, int64_t s_cols, uint8_t* W, int64_t ldw_b, const uint8_t* dense,
+                             int64_t d_ld_b, int64_t d_rows, int64_t d_cols_b, uint8_t* ddst, hipStream_t s);
+
+hipError_t launch_zero_u64(unsigned long long* p, hipStream_t s);
+
+}  // namespace spense

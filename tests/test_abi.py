@@ -1,0 +1,131 @@
+"""C-ABI checks that need no GPU: every function declared in include/*.h is exported by
+the built library, the layout query agrees with the oracle's geometry, and argument
+validation rejects bad calls before anything touches a device."""
+import ctypes
+import glob
+import os
+import re
+
+import pytest
+
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    names = set()
+    for h in glob.glob(os.path.join(ROOT, "include", "*.h")):
+        text = open(h).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        for m in re.finditer(r"^[A-Za-z_][\w \*]*?\b(spense_\w+)\s*\(", text, flags=re.M):
+            names.add(m.group(1))
+    return sorted(names)
+
+
+@pytest.fixture(scope="module")
+def S():
+    import paper_2606_10445_amd as S
+    return S
+
+
+def test_header_declares_the_boundary():
+    names = _declared()
+    for n in ("spense_layout", "spense_compress", "spense_decompress", "spense_gemm", "spense_dense_gemm",
+              "spense_last_error", "spense_gemm_workspace_size"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(S):
+    lib = ctypes.CDLL(S.LIB_PATH)
+    for n in _declared():
+        assert hasattr(lib, n), f"{n} declared in include/ but not exported"
+    assert set(_declared()) == set(S.EXPORTS)
+    assert S.spense_abi_version() == 1
+
+
+@pytest.mark.parametrize("N,K,split,db", [(256, 512, 0, 192), (256, 512, 1, 384), (25600, 5120, 0, 19200),
+                                          (5120, 25600, 1, 19200), (17, 96, 0, 0), (17, 96, 1, 96), (0, 64, 0, 0)])
+@pytest.mark.parametrize("dtype", [1, 2])
+def test_layout_matches_oracle_geometry(S, N, K, split, db, dtype):
+    L = S.spense_layout(N, K, dtype, split, db)
+    o = oracle.layout(N, K, split, db)
+    assert (L.sparse_rows, L.sparse_cols, L.values_ld, L.meta_ld) == (o["sparse_rows"], o["sparse_cols"],
+                                                                       o["values_ld"], o["meta_ld"])
+    assert (L.dense_rows, L.dense_ld) == (o["dense_rows"], o["dense_ld"])
+    es = 1 if dtype == 1 else 2
+    assert L.values_bytes == L.sparse_rows * L.values_ld * es
+    assert L.meta_bytes == L.sparse_rows * L.meta_ld * 4
+    assert L.dense_bytes == L.dense_rows * L.dense_ld * es
+
+
+@pytest.mark.parametrize("args,code", [
+    ((256, 500, 1, 0, 0), -2),    # K not a multiple of 32
+    ((256, 512, 1, 1, 100), -2),  # input-split point not a multiple of 32
+    ((256, 512, 1, 0, 300), -1),  # split point past N
+    ((256, 512, 3, 0, 0), -1),    # unknown dtype
+    ((256, 512, 1, 2, 0), -1),    # unknown split
+    ((-1, 512, 1, 0, 0), -1),
+])
+def test_layout_rejects(S, args, code):
+    with pytest.raises(S.SpenseError) as e:
+        S.spense_layout(*args)
+    assert e.value.code == code
+    assert S.spense_last_error()
+
+
+def test_gemm_validation_happens_before_any_device_call(S):
+    """Bad arguments return an error code without a GPU (the device is queried last)."""
+    L = S.spense_layout(64, 128, 1, 0, 32)
+    good = S.spense_packed_t(1, 0, 64, 128, 32, 4096, L.values_ld, 8192, L.meta_ld, 16384, L.dense_ld)
+    # NULL packed
+    assert S._lib.spense_gemm(4096, 4, 128, None, None, None, 4096, 64, 0, None, 0, None) == S.SPENSE_ERR_ARG
+    # NULL Y
+    assert S.spense_gemm(4096, 4, 128, good, None, None, None, 64, 0, None, 0, None) == S.SPENSE_ERR_ARG
+    # misaligned X
+    assert S.spense_gemm(4097, 4, 128, good, None, None, 4096, 64, 0, None, 0, None) == S.SPENSE_ERR_ALIGN
+    # ldx < K
+    assert S.spense_gemm(4096, 4, 64, good, None, None, 4096, 64, 0, None, 0, None) == S.SPENSE_ERR_ARG
+    # ldy < N
+    assert S.spense_gemm(4096, 4, 128, good, None, None, 4096, 32, 0, None, 0, None) == S.SPENSE_ERR_ARG
+    # unknown flags
+    assert S.spense_gemm(4096, 4, 128, good, None, None, 4096, 64, 8, None, 0, None) == S.SPENSE_ERR_ARG
+    # values pointer NULL with a non-empty 2:4 region
+    bad = S.spense_packed_t(1, 0, 64, 128, 32, None, L.values_ld, 8192, L.meta_ld, 16384, L.dense_ld)
+    assert S.spense_gemm(4096, 4, 128, bad, None, None, 4096, 64, 0, None, 0, None) == S.SPENSE_ERR_ARG
+    # misaligned dense
+    bad = S.spense_packed_t(1, 0, 64, 128, 32, 4096, L.values_ld, 8192, L.meta_ld, 16392, L.dense_ld)
+    assert S.spense_gemm(4096, 4, 128, bad, None, None, 4096, 64, 0, None, 0, None) == S.SPENSE_ERR_ALIGN
+    # M == 0 and N == 0 are no-ops that succeed without touching anything
+    assert S.spense_gemm(None, 0, 128, good, None, None, None, 64, 0, None, 0, None) == S.SPENSE_OK
+    # workspace: a split-K plan needs one; none given -> SPENSE_ERR_WS
+    Ld = S.spense_layout(1024, 8192, 1, 1, 6144)
+    big = S.spense_packed_t(1, 1, 1024, 8192, 6144, 4096, Ld.values_ld, 8192, Ld.meta_ld, 16384, Ld.dense_ld)
+    need = S.spense_gemm_workspace_size(1, big)
+    assert need > 0
+    assert S.spense_gemm(4096, 1, 8192, big, None, None, 4096, 1024, 0, None, 0, None) == S.SPENSE_ERR_WS
+    assert "workspace" in S.spense_last_error()
+
+
+def test_compress_validation(S):
+    L = S.spense_layout(64, 128, 1, 0, 32)
+    pk = S.spense_packed_t(1, 0, 64, 128, 32, 4096, L.values_ld, 8192, L.meta_ld, 16384, L.dense_ld)
+    rc, bad = S.spense_compress(None, 128, None, 0, pk, 4096, 256, None)
+    assert rc == S.SPENSE_ERR_ARG and bad == 0
+    rc, _ = S.spense_compress(4096, 128, 4097, 128, pk, 4096, 256, None)
+    assert rc == S.SPENSE_ERR_ALIGN
+    rc, _ = S.spense_compress(4096, 128, None, 0, pk, None, 0, None)
+    assert rc == S.SPENSE_ERR_WS
+
+
+def test_workspace_size_is_a_pure_function_of_geometry(S):
+    L = S.spense_layout(5120, 25600, 1, 1, 19200)
+    pk = S.spense_packed_t(1, 1, 5120, 25600, 19200, 4096, L.values_ld, 8192, L.meta_ld, 16384, L.dense_ld)
+    a = [S.spense_gemm_workspace_size(m, pk) for m in (1, 16, 64, 65)]
+    b = [S.spense_gemm_workspace_size(m, pk) for m in (1, 16, 64, 65)]
+    assert a == b
+    # the dense baseline with all rows dense plans exactly like a Spense weight with no 2:4 part
+    L0 = S.spense_layout(4096, 5120, 1, 0, 0)
+    pk0 = S.spense_packed_t(1, 0, 4096, 5120, 0, None, L0.values_ld, None, L0.meta_ld, 16384, L0.dense_ld)
+    for m in (1, 8, 64):
+        assert S.spense_gemm_workspace_size(m, pk0) == S.spense_dense_gemm_workspace_size(m, 4096, 5120, 1)
