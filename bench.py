@@ -1,0 +1,262 @@
+#!/usr/bin/env python3
+"""Benchmark of the Spense linear layer on one MI355X.
+
+One step = one spense_gemm call (2:4 smfmac region + dense mfma region + fused scale
+epilogue, one kernel launch) over one batch of activations, on the Qwen3-32B-like MLP
+gate/up projection: W 25600 x 5120 fp8 e4m3, the trailing 25% of output rows dense
+(output-split), the rest magnitude-pruned 2:4, X 64 x 5120 fp8 with per-token scales,
+bf16 output.  Inputs are synthetic and already resident in HBM; the timed loop rotates
+over several copies of the packed weight so that no step is served from the 256 MB
+Infinity Cache.
+
+Printed JSON line: value = algorithmic bytes / time (GB/s) at M = 64; the M = 1/8/32/64
+sweep, the dense fp8 baseline built in the same library, the roofline of the dominant
+kernel (HIP events around a graph replay of exactly `steps` launches, on the launch
+stream) and the CPU oracle baseline are extra fields.
+
+    python bench.py [--gpus 1] [--steps 500] [--warmup 50] [--skip-cpu]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, AMD datasheet
+N, K, DENSE_FRAC = 25600, 5120, 0.25
+M_SWEEP = [1, 8, 32, 64]
+M_MAIN = 64
+MALL_BYTES = 256 << 20
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_spense_gemm_gate_up_m64.json")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2606_10445_amd", "csrc", f) for f in
+                  ("spense_gemm.hip", "spense_api.cpp", "spense_internal.h")]
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def alg_bytes_spense(M, N, K, n_sparse_rows, n_dense_rows):
+    """Bytes the method must move: dense weights 1 B, 2:4 weights 0.5 B values + 1/8 B
+    metadata per logical entry, activations M*K, scales 4(M+N), bf16 output 2MN."""
+    return n_dense_rows * K + (0.5 + 0.125) * n_sparse_rows * K + M * K + 4 * (M + N) + 2 * M * N
+
+
+def alg_bytes_dense(M, N, K):
+    return N * K + M * K + 4 * (M + N) + 2 * M * N
+
+
+def kernel_source_sha():
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+EAGER = False
+
+
+def time_launches(fn, steps, warmup, torch):
+    """Run `warmup` eager steps, capture exactly `steps` launches in one HIP graph, and
+    time one replay with HIP events on the stream the kernels run on (the current
+    stream); returns ms per step.  The graph removes host launch overhead between the
+    kernels, as in a graph-captured decode loop."""
+    for i in range(warmup):
+        fn(i)
+    torch.cuda.synchronize()
+    if EAGER:  # for profilers that follow individual dispatches
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record()
+        for i in range(steps):
+            fn(i)
+        t1.record()
+        torch.cuda.synchronize()
+        return t0.elapsed_time(t1) / steps
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for i in range(steps):
+            fn(i)
+    g.replay()  # untimed: first replay uploads the graph
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    g.replay()
+    t1.record(stream)
+    torch.cuda.synchronize()
+    return t0.elapsed_time(t1) / steps
+
+
+def cpu_baseline(mx, Wcodes_dense, X, sx, M):
+    """The oracle (plain C, OpenMP, never tuned) on a bounded sample of the same GEMM:
+    the whole M x N x K product repeated for about 10 s (median run), or a slice of the
+    weight rows extrapolated linearly when one full run would take longer than 20 s."""
+    import statistics
+
+    import oracle
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    t = time.perf_counter()
+    oracle.gemm(X, Wcodes_dense[:256], oracle.FP8, mx.sw[:256], sx)
+    est_full = (time.perf_counter() - t) * N / 256
+    b = alg_bytes_spense(M, N, K, mx.dense_begin, N - mx.dense_begin)
+    if est_full <= 20.0:
+        runs = []
+        t_stop = time.perf_counter() + 10.0
+        while len(runs) < 3 or (time.perf_counter() < t_stop and len(runs) < 200):
+            t = time.perf_counter()
+            oracle.gemm(X, Wcodes_dense, oracle.FP8, mx.sw, sx)
+            runs.append(time.perf_counter() - t)
+        full_s = statistics.median(runs)
+        sample = (f"oracle fp32 GEMM over the whole decompressed {N}x{K} weight at M={M}, {len(runs)} runs "
+                  f"({sum(runs):.1f} s), median run")
+    else:
+        rows = int(min(N, max(256, 15.0 / est_full * N)))
+        t = time.perf_counter()
+        oracle.gemm(X, Wcodes_dense[:rows], oracle.FP8, mx.sw[:rows], sx)
+        dt = time.perf_counter() - t
+        full_s = dt * N / rows
+        sample = f"oracle fp32 GEMM over {rows} of {N} weight rows at M={M}, {dt:.1f} s, extrapolated linearly"
+    return {"value": round(b / full_s / 1e9, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "sample": sample, "seconds_per_gemm": round(full_s, 4)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=500)
+    ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--skip-cpu", action="store_true", help="omit the CPU oracle baseline")
+    ap.add_argument("--only-main", action="store_true", help="time only the M=64 Spense GEMM (for profiling)")
+    ap.add_argument("--eager", action="store_true", help="launch steps one by one instead of one graph")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MiB",
+                    help="run only a torch device copy of this size (rocprof counter calibration)")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    global EAGER
+    EAGER = args.eager
+    if args.copy_calibration:  # an elementwise copy kernel of known size
+        n = args.copy_calibration << 20
+        x = torch.ones(n, dtype=torch.uint8, device="cuda")
+        y = torch.empty_like(x)
+        for _ in range(args.steps):
+            torch.mul(x, 1, out=y)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_per_launch": n, "launches": args.steps}))
+        return
+
+    import gen
+    import paper_2606_10445_amd as S
+
+    t_setup = time.perf_counter()
+    mx = gen.make_matrix(2, 0, "gate_up", N, K, gen.OUTPUT, DENSE_FRAC, gen.FP8)
+    log(f"[bench] inputs drawn in {time.perf_counter() - t_setup:.1f} s; dense_begin={mx.dense_begin}")
+    Wd = torch.from_numpy(mx.W).cuda()
+    maskd = torch.from_numpy(mx.mask).cuda()
+    swd = torch.from_numpy(mx.sw).cuda()
+    # compress once (offline step), timed separately
+    torch.cuda.synchronize()
+    t = time.perf_counter()
+    pw0 = S.compress(Wd, maskd, S.SPENSE_SPLIT_OUTPUT, mx.dense_begin)
+    torch.cuda.synchronize()
+    compress_ms = (time.perf_counter() - t) * 1e3
+    wbytes = pw0.weight_bytes()
+    copies = max(2, -(-2 * MALL_BYTES // wbytes))
+    pws = [pw0] + [S.PackedWeight(pw0.N, pw0.K, pw0.dtype, pw0.split, pw0.dense_begin, pw0.values.clone(),
+                                  pw0.meta.clone(), pw0.dense.clone()) for _ in range(copies - 1)]
+    dense_copies = max(2, -(-2 * MALL_BYTES // (N * K)))
+    dws = [Wd] + [Wd.clone() for _ in range(dense_copies - 1)]
+    n_sp, n_de = mx.dense_begin, N - mx.dense_begin
+    log(f"[bench] packed weight {wbytes / 1e6:.2f} MB x {copies} copies; dense {N * K / 1e6:.2f} MB x {dense_copies}")
+
+    results = {}
+    ws = S.Workspace("cuda")
+    ms_list = [M_MAIN] if args.only_main else M_SWEEP
+    for M in ms_list:
+        X, sx = gen.make_x(2, 0, M, K, gen.FP8, "normal")
+        Xd, sxd = torch.from_numpy(X).cuda(), torch.from_numpy(sx).cuda()
+        Y = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+
+        def run_sp(i):
+            S.gemm(Xd, pws[i % copies], swd, sxd, out=Y, workspace=ws)
+
+        step_ms = time_launches(run_sp, args.steps, args.warmup, torch)
+        res = {"M": M, "us_per_step": round(step_ms * 1e3, 3)}
+        b = alg_bytes_spense(M, N, K, n_sp, n_de)
+        res["alg_bytes"] = int(b)
+        res["gbs"] = round(b / (step_ms * 1e-3) / 1e9, 1)
+        if not args.only_main:
+            Yd = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+
+            def run_de(i):
+                S.dense_gemm(Xd, dws[i % dense_copies], swd, sxd, out=Yd, workspace=ws)
+
+            dstep_ms = time_launches(run_de, args.steps, args.warmup, torch)
+            res["dense_us_per_step"] = round(dstep_ms * 1e3, 3)
+            res["dense_gbs"] = round(alg_bytes_dense(M, N, K) / (dstep_ms * 1e-3) / 1e9, 1)
+            res["speedup_vs_dense"] = round(dstep_ms / step_ms, 4)
+            res["byte_ratio_bound"] = round(alg_bytes_dense(M, N, K) / b, 4)
+        results[M] = res
+        log(f"[bench] M={M}: {res}")
+
+    main_res = results[M_MAIN]
+    traffic = None
+    if os.path.exists(TRAFFIC_FILE):
+        with open(TRAFFIC_FILE) as f:
+            tr = json.load(f)
+        if tr.get("kernel_source_sha256") == kernel_source_sha():
+            traffic = tr.get("hbm_bytes_per_launch")
+    ach = main_res["alg_bytes"] / (main_res["us_per_step"] * 1e-6) / 1e9
+    out = {
+        "metric": "µs per Spense GEMM, HBM GB/s %peak, speedup vs dense fp8 GEMM at M=1–64",
+        "value": round(main_res["alg_bytes"] / (main_res["us_per_step"] * 1e-6) / 1e9, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(main_res["us_per_step"] / 1e3, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "fp8",
+        "data": "synthetic (seeded N(0,0.02) weights, magnitude 2:4 mask, N(0,1) activations, absmax fp8 scales)",
+        "config": {"workload": "qwen3-32b-like MLP gate/up 25600x5120 fp8 e4m3, trailing 25% rows dense "
+                               "(output-split), rest 2:4, decode batch M=64, bf16 out",
+                   "N": N, "K": K, "M": M_MAIN, "split": "output", "dense_fraction": DENSE_FRAC,
+                   "weight_copies_rotated": copies},
+        "us_per_gemm": main_res["us_per_step"],
+        "pct_hbm_peak": round(100 * ach / HBM_PEAK_GBS, 2),
+        "speedup_vs_dense": main_res.get("speedup_vs_dense"),
+        "compress_ms": round(compress_ms, 3),
+        "roofline": {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": traffic,
+                     "kernel": "spense_gemm_kernel (fp8, 2:4 smfmac + dense mfma)"},
+        "sweep": [results[m] for m in ms_list],
+    }
+    if not args.skip_cpu:
+        X, sx = gen.make_x(2, 0, M_MAIN, K, gen.FP8, "normal")
+        import oracle
+        v, m, d, _ = oracle.compress(mx.W, mx.mask, oracle.FP8, oracle.AXIS_OUTPUT, mx.dense_begin)
+        Wdense = oracle.decompress(v, m, d, N, K, oracle.FP8, oracle.AXIS_OUTPUT, mx.dense_begin)
+        log("[bench] cpu baseline (oracle) ...")
+        out["cpu_baseline"] = cpu_baseline(mx, Wdense, X, sx, M_MAIN)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

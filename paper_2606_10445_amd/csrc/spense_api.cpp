@@ -115,15 +115,8 @@ int check_packed(const spense_packed_t* P, spense_layout_t* L) {
 struct Plan {
   spense::LaunchShape ls;
   spense::GemmArgs args;  // geometry part filled
-  size_t part_bytes;      // split-K partials
-  size_t ws_bytes;
+  size_t ws_bytes;        // device workspace needed (none at present)
 };
-
-// Workspace layout: [arrival counters, fixed kCounterBytes][split-K partials].  The
-// counters sit at the same place for every plan, so partial sums written by one call can
-// never land on counters used by a later call with a different decomposition.
-constexpr size_t kCounterBytes = 256 * 1024;
-constexpr int64_t kMaxCounters = kCounterBytes / 4;
 
 int env_int(const char* name, int dflt) {
   const char* v = getenv(name);
@@ -133,8 +126,12 @@ int env_int(const char* name, int dflt) {
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-// The plan depends only on the dtype, M, and the regions' (rows, K ranges), so the same
-// geometry always gets the same decomposition and the same summation order.
+// Workgroup shapes the kernels are built for: (row tiles, waves).
+const int kShapes[][2] = {{2, 4}, {1, 4}, {2, 8}, {1, 8}, {1, 16}, {4, 4}};
+
+// The plan depends only on the dtype, M and the weight geometry, so equal geometry gets
+// the same decomposition and summation order (the dense baseline and a Spense weight
+// with no 2:4 part are planned identically).
 void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, int64_t dense_begin, Plan* pl) {
   using spense::Region;
   memset(pl, 0, sizeof *pl);
@@ -142,15 +139,32 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
   const int64_t gran = dtype == SPENSE_FP8_E4M3FN ? 128 : 64;  // K per 2:4 instruction
   const double sparse_cost = 0.5 * es + 0.125;                 // bytes per logical 2:4 entry
   const int ct = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
-  const int rt = env_int("SPENSE_RT", 1) == 2 ? 2 : 1;
-  const int waves = 4;
-  const int rows_per_unit = 16 * rt * waves;
-  const int64_t target_units = std::max(1, env_int("SPENSE_TARGET_UNITS", 1024));
-  const int64_t min_split_k = std::max(32, env_int("SPENSE_MIN_SPLIT_K", 1024));
   pl->ls.ct = ct;
+  pl->ls.mblocks = (int)ceil_div(M, 16 * ct);
+
+  // Workgroup shape (measured on MI355X with the gate/up and down shapes):
+  //  - one activation tile (M <= 16): 16 rows per workgroup; 4 waves when that gives
+  //    >= 4096 waves, else 8 (the waves split K);
+  //  - more activation tiles: more rows per workgroup so that each activation fragment
+  //    feeds more weight rows, as long as enough workgroups remain.
+  int rt, waves;
+  auto groups_for = [&](int r) { return ceil_div(N, 16 * r) * pl->ls.mblocks; };
+  if (ct == 1) {
+    rt = 1;
+    waves = groups_for(1) * 4 >= 4096 ? 4 : 8;
+  } else {
+    rt = groups_for(4) >= 300 ? 4 : 2;
+    waves = 4;
+  }
+  const int ert = env_int("SPENSE_RT", 0), ew = env_int("SPENSE_WAVES", 0);
+  for (const auto& sh : kShapes)
+    if (sh[0] == ert && sh[1] == ew) {
+      rt = ert;
+      waves = ew;
+    }
   pl->ls.rt = rt;
   pl->ls.waves = waves;
-  pl->ls.mblocks = (int)ceil_div(M, 16 * ct);
+  pl->ls.u8 = (ct == 1 && rt == 1 && (waves == 4 || waves == 8) && env_int("SPENSE_U8", 0)) ? 1 : 0;
 
   Region regs[2];
   int nreg = 0;
@@ -159,72 +173,41 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
     memset(&r, 0, sizeof r);
     r.row0 = (int32_t)row0;
     r.rows = (int32_t)rows;
-    r.kbeg = 0;
-    r.kend = (int32_t)K;
     r.kbound = (int32_t)kbound;
     r.dense_row_off = (int32_t)dro;
     r.dense_col_off = (int32_t)dco;
-    r.nrb = (int32_t)ceil_div(rows, rows_per_unit);
+    r.nrb = (int32_t)ceil_div(rows, 16 * rt);
+    // cut [0, K) into `waves` parts of equal byte cost, on multiples of the instruction K
+    const double cs = sparse_cost * kbound, total = cs + es * (double)(K - kbound);
+    r.cut[0] = 0;
+    for (int w = 1; w < waves; ++w) {
+      const double c = total * w / waves;
+      const double k = c <= cs ? c / sparse_cost : kbound + (c - cs) / es;
+      int64_t kr = (int64_t)std::llround(k / gran) * gran;
+      kr = std::max<int64_t>(r.cut[w - 1], std::min<int64_t>(kr, K));
+      r.cut[w] = (int32_t)kr;
+    }
+    r.cut[waves] = (int32_t)K;
     regs[nreg++] = r;
   };
   if (split == SPENSE_SPLIT_OUTPUT) {
-    if (dense_begin > 0) add(0, dense_begin, K, 0, 0);
+    // dense rows first: their workgroups carry more bytes, so dispatching them early
+    // keeps them out of the tail
     if (N - dense_begin > 0) add(dense_begin, N - dense_begin, 0, dense_begin, 0);
+    if (dense_begin > 0) add(0, dense_begin, K, 0, 0);
   } else if (N > 0) {
     add(0, N, dense_begin, 0, dense_begin);
   }
-  // cost of the K prefix [0, k) of one row of a region, in bytes
-  auto cost = [&](const Region& r, double k) {
-    const double ks = std::min<double>(k, r.kbound);
-    return sparse_cost * ks + es * std::max(0.0, k - r.kbound);
-  };
-  auto inv_cost = [&](const Region& r, double c) {
-    const double cs = sparse_cost * r.kbound;
-    return c <= cs ? c / sparse_cost : r.kbound + (c - cs) / es;
-  };
-  double total = 0;
-  int64_t counters_needed = 0;
-  for (int i = 0; i < nreg; ++i) {
-    total += regs[i].rows * cost(regs[i], (double)K);
-    counters_needed += (int64_t)regs[i].nrb * pl->ls.mblocks;
-  }
-  const bool may_split = counters_needed <= kMaxCounters;
-  int32_t unit = 0, ctr = 0, max_s = 1;
-  for (int i = 0; i < nreg; ++i) {
-    Region& r = regs[i];
-    const double rc = r.rows * cost(r, (double)K);
-    int64_t want = 1;
-    if (may_split && total > 0) {
-      want = (int64_t)std::llround(rc / total * (double)target_units /
-                                   ((double)std::max<int32_t>(1, r.nrb) * pl->ls.mblocks));
-      want = std::max<int64_t>(1, std::min<int64_t>(want, std::max<int64_t>(1, K / min_split_k)));
-      want = std::min<int64_t>(want, spense::kMaxSplits);
-    }
-    // cut [0, K) into `want` pieces of equal byte cost, on multiples of the instruction K
-    const double row_cost = cost(r, (double)K);
-    int n = 0;
-    r.cut[n++] = 0;
-    for (int64_t j = 1; j < want; ++j) {
-      int64_t k = (int64_t)std::llround(inv_cost(r, row_cost * j / want) / gran) * gran;
-      if (k > r.cut[n - 1] && k < K) r.cut[n++] = (int32_t)k;
-    }
-    r.cut[n++] = (int32_t)K;
-    r.splits = n - 1;
-    r.unit0 = unit;
-    r.ctr0 = ctr;
-    unit += r.nrb * r.splits;
-    ctr += r.nrb;
-    max_s = std::max(max_s, (int)r.splits);
-  }
   spense::GemmArgs& a = pl->args;
   a.nreg = nreg;
-  for (int i = 0; i < nreg; ++i) a.reg[i] = regs[i];
-  a.units = unit;
-  a.counters_per_mb = ctr;
-  if (max_s > 1 && M > 0) {
-    pl->part_bytes = (size_t)max_s * (size_t)M * (size_t)N * 4;
-    pl->ws_bytes = kCounterBytes + pl->part_bytes;
+  int32_t groups = 0;
+  for (int i = 0; i < nreg; ++i) {
+    regs[i].wg0 = groups;
+    groups += regs[i].nrb;
+    a.reg[i] = regs[i];
   }
+  a.groups = groups;
+  pl->ws_bytes = 0;
 }
 
 int gemm_common(const void* X, int64_t M, int64_t ldx, int32_t dtype, int32_t split, int64_t N, int64_t K,
@@ -262,7 +245,7 @@ int gemm_common(const void* X, int64_t M, int64_t ldx, int32_t dtype, int32_t sp
   a.values = static_cast<const uint8_t*>(values);
   a.v_ld_b = values_ld * es;
   a.meta = meta;
-  a.m_ld = meta_ld;
+  a.m_ld_b = meta_ld * 4;
   a.dense = static_cast<const uint8_t*>(dense);
   a.d_ld_b = dense_ld * es;
   a.sw = w_scale;
@@ -275,9 +258,23 @@ int gemm_common(const void* X, int64_t M, int64_t ldx, int32_t dtype, int32_t sp
   bool vec = (ldy % 4 == 0) && (reinterpret_cast<uintptr_t>(Y) % (4 * out_es) == 0);
   for (int i = 0; i < a.nreg; ++i) vec = vec && (a.reg[i].row0 % 4 == 0);
   a.vec_store = vec ? 1 : 0;
-  a.counters = pl.ws_bytes ? static_cast<uint32_t*>(ws) : nullptr;
-  a.part = pl.ws_bytes ? reinterpret_cast<float*>(static_cast<char*>(ws) + kCounterBytes) : nullptr;
-  if (a.units == 0) return ok();
+  // extents of the range-checked loads; every one must stay below 2^31
+  int64_t sparse_rows = split == SPENSE_SPLIT_OUTPUT ? dense_begin : N;
+  int64_t sparse_cols = split == SPENSE_SPLIT_OUTPUT ? K : dense_begin;
+  int64_t dense_rows = split == SPENSE_SPLIT_OUTPUT ? N - dense_begin : N;
+  int64_t dense_cols = split == SPENSE_SPLIT_OUTPUT ? K : K - dense_begin;
+  const int64_t xb = K > 0 ? ((M - 1) * ldx + K) * es : 0;
+  const int64_t vb = sparse_rows > 0 && sparse_cols > 0 ? ((sparse_rows - 1) * values_ld + sparse_cols / 2) * es : 0;
+  const int64_t mb = sparse_rows > 0 && sparse_cols > 0 ? ((sparse_rows - 1) * meta_ld + sparse_cols / 32) * 4 : 0;
+  const int64_t db = dense_rows > 0 && dense_cols > 0 ? ((dense_rows - 1) * dense_ld + dense_cols) * es : 0;
+  const int64_t lim = (int64_t)1 << 31;
+  if (xb >= lim || vb >= lim || mb >= lim || db >= lim)
+    return fail(SPENSE_ERR_ARG, "an operand spans 2 GiB or more; split the layer");
+  a.x_bytes = (uint32_t)xb;
+  a.v_bytes = (uint32_t)vb;
+  a.m_bytes = (uint32_t)mb;
+  a.d_bytes = (uint32_t)db;
+  if (a.groups == 0) return ok();
   hipError_t e = spense::launch_gemm(dtype, pl.ls, a, stream);
   if (e != hipSuccess) return fail(SPENSE_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();

@@ -8,24 +8,23 @@ namespace spense {
 enum : int32_t { kFP8 = 1, kBF16 = 2 };
 enum : int32_t { kSplitOutput = 0, kSplitInput = 1 };
 
-constexpr int kMaxSplits = 32;
+constexpr int kMaxWaves = 16;
 
-// One contiguous part of the weight covered by a set of work units: a range of output
-// rows and a logical K range [kbeg, kend) whose columns below kbound are stored 2:4 and
-// the rest dense.  Output-split has up to two regions (2:4 rows with kbound = K, dense
-// rows with kbound = 0); input-split has one region with kbound = the first dense column,
-// so a unit whose K range contains kbound runs the 2:4 loop and then the dense loop into
-// the same fp32 accumulator.
+// One contiguous part of the weight: a range of output rows and the logical K range
+// [0, K) whose columns below kbound are stored 2:4 and the rest dense.  Output-split has
+// up to two regions (2:4 rows with kbound = K, dense rows with kbound = 0); input-split
+// has one region with kbound = the first dense column.  A workgroup owns 16*RT rows of
+// one region; its waves split K at cut[0..waves] (cost-balanced), each wave running the
+// 2:4 loop over its part below kbound and the dense loop over the rest into one fp32
+// accumulator; the waves' partial sums are added in LDS in wave order.
 struct Region {
-  int32_t row0, rows;                // output rows [row0, row0 + rows)
-  int32_t kbeg, kend, kbound;        // K range, first dense column
-  int32_t dense_row_off;             // dense storage row = n - dense_row_off
-  int32_t dense_col_off;             // dense storage column = k - dense_col_off
-  int32_t nrb;                       // row blocks
-  int32_t splits;                    // K pieces per row block
-  int32_t unit0;                     // first work unit of this region
-  int32_t ctr0;                      // first arrival counter of this region
-  int32_t cut[kMaxSplits + 1];       // K piece boundaries, cut[0] = kbeg, cut[splits] = kend
+  int32_t row0, rows;          // output rows [row0, row0 + rows)
+  int32_t kbound;              // first dense column (K for all-2:4, 0 for all-dense)
+  int32_t dense_row_off;       // dense storage row = n - dense_row_off
+  int32_t dense_col_off;       // dense storage column = k - dense_col_off
+  int32_t nrb;                 // row groups (workgroups per activation block)
+  int32_t wg0;                 // first workgroup of this region
+  int32_t cut[kMaxWaves + 1];  // K boundaries of the waves' parts
 };
 
 struct GemmArgs {
@@ -34,30 +33,28 @@ struct GemmArgs {
   const uint8_t* values;
   int64_t v_ld_b;  // bytes per 2:4 row
   const uint32_t* meta;
-  int64_t m_ld;  // words per 2:4 row
+  int64_t m_ld_b;  // bytes per 2:4 row of metadata
   const uint8_t* dense;
   int64_t d_ld_b;  // bytes per dense row
   const float* sw;
   const float* sx;
   void* Y;
   int64_t ldy;  // elements
-  float* part;  // split-K partial sums [split][M][N]
-  uint32_t* counters;
+  uint32_t x_bytes, v_bytes, m_bytes, d_bytes;  // buffer extents for range-checked loads
   int32_t M, N;
   int32_t out_f32;
   int32_t vec_store;  // 4 consecutive outputs may be stored as one vector
   int32_t nreg;
-  int32_t units;
-  int32_t counters_per_mb;
-  int32_t pad_;
+  int32_t groups;
   Region reg[2];
 };
 
 struct LaunchShape {
-  int ct;       // 16-column tiles of M per unit (1, 2, 4)
-  int rt;       // 16-row tiles per wave
-  int waves;    // waves per workgroup
+  int ct;       // 16-column tiles of M per workgroup (1, 2, 4)
+  int rt;       // 16-row tiles per workgroup (1, 2, 4)
+  int waves;    // waves per workgroup (4, 8, 16): they split K
   int mblocks;  // grid.y
+  int u8;       // eight instruction steps per batch of loads (single activation tile only)
 };
 
 hipError_t launch_gemm(int dtype, const LaunchShape& ls, const GemmArgs& a, hipStream_t s);
