@@ -245,7 +245,8 @@ def main():
         "compress_ms": round(compress_ms, 3),
         "roofline": {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": traffic,
-                     "kernel": "spense_gemm_kernel (fp8, 2:4 smfmac + dense mfma)"},
+                     "kernel": "spense_gemm_rows_kernel (fp8; 2:4 smfmac + dense mfma, activations staged "
+                               "in LDS, one launch)"},
         "sweep": [results[m] for m in ms_list],
     }
     if not args.skip_cpu:

@@ -129,6 +129,47 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 // Workgroup shapes the kernels are built for: (row tiles, waves).
 const int kShapes[][2] = {{2, 4}, {1, 4}, {2, 8}, {1, 8}, {1, 16}, {4, 4}};
 
+constexpr int kCUs = 256;  // compute units of an MI355X
+
+// Row-split kernel: how many of a workgroup's waves own rows in each region.  A region
+// whose rows carry more bytes (dense rows) gets fewer rows per workgroup, so that the
+// workgroups are alike in bytes.  Model: with W workgroups on kCUs CUs the time is
+// ceil(W / kCUs) rounds of the largest workgroup, whose cost is its weight bytes plus a
+// quarter of the activation bytes it stages from L2; the cheapest assignment wins, ties
+// going to fewer workgroups.
+void choose_rows_per_group(spense::Region* regs, int nreg, int rt, int waves, int ct, int mblocks, int64_t K, int es,
+                           double sparse_cost) {
+  double tile_b[2];
+  for (int i = 0; i < nreg; ++i)
+    tile_b[i] = 16.0 * rt * (sparse_cost * regs[i].kbound + (double)es * (K - regs[i].kbound));
+  const double x_cost = 0.25 * 16.0 * ct * K * es;
+  double best = 0;
+  int64_t best_wg = 0;
+  int bw[2] = {waves, waves};
+  for (int w0 = 1; w0 <= waves; ++w0)
+    for (int w1 = 1; w1 <= (nreg > 1 ? waves : 1); ++w1) {
+      const int wu[2] = {w0, w1};
+      int64_t wg = 0;
+      double big = 0;
+      for (int i = 0; i < nreg; ++i) {
+        wg += ceil_div(regs[i].rows, 16 * rt * wu[i]) * mblocks;
+        big = std::max(big, wu[i] * tile_b[i]);
+      }
+      const double t = (double)ceil_div(wg, kCUs) * (big + x_cost);
+      if (best_wg == 0 || t < best * (1 - 1e-9) || (t <= best * (1 + 1e-9) && wg < best_wg)) {
+        best = t;
+        best_wg = wg;
+        bw[0] = w0;
+        bw[1] = w1;
+      }
+    }
+  const int ew = env_int("SPENSE_WUSED", 0);
+  for (int i = 0; i < nreg; ++i) {
+    regs[i].wused = ew > 0 ? std::min(ew, waves) : bw[i];
+    regs[i].nrb = (int32_t)ceil_div(regs[i].rows, 16 * rt * regs[i].wused);
+  }
+}
+
 // The plan depends only on the dtype, M and the weight geometry, so equal geometry gets
 // the same decomposition and summation order (the dense baseline and a Spense weight
 // with no 2:4 part are planned identically).
@@ -156,14 +197,31 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
     rt = groups_for(4) >= 300 ? 4 : 2;
     waves = 4;
   }
+  // Row-split workgroups (activations staged once per workgroup in LDS, weights
+  // prefetched two chunks ahead) measured faster than K-split on the q/k/o/gate/down
+  // shapes at every M > 16, and at M <= 16 whenever there are at least as many 16-row
+  // tiles as CUs; with fewer rows the K split gives the single activation tile more
+  // parallelism.  Eight waves for several activation tiles, four for one.
+  int rows_mode = (ct > 1 || ceil_div(N, 16) * pl->ls.mblocks >= kCUs) ? 1 : 0;
+  if (rows_mode) {
+    rt = 1;
+    waves = ct > 1 ? 8 : 4;
+  }
+  const int erows = env_int("SPENSE_ROWS", -1);
+  if (erows >= 0) rows_mode = erows ? 1 : 0;
   const int ert = env_int("SPENSE_RT", 0), ew = env_int("SPENSE_WAVES", 0);
   for (const auto& sh : kShapes)
     if (sh[0] == ert && sh[1] == ew) {
       rt = ert;
       waves = ew;
     }
+  if (rows_mode && !(rt == 1 && (waves == 4 || waves == 8))) {
+    rt = 1;
+    waves = 4;
+  }
   pl->ls.rt = rt;
   pl->ls.waves = waves;
+  pl->ls.rows = rows_mode;
   pl->ls.u8 = (ct == 1 && rt == 1 && (waves == 4 || waves == 8) && env_int("SPENSE_U8", 0)) ? 1 : 0;
 
   Region regs[2];
@@ -176,6 +234,8 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
     r.kbound = (int32_t)kbound;
     r.dense_row_off = (int32_t)dro;
     r.dense_col_off = (int32_t)dco;
+    r.kend = (int32_t)K;
+    r.wused = waves;
     r.nrb = (int32_t)ceil_div(rows, 16 * rt);
     // cut [0, K) into `waves` parts of equal byte cost, on multiples of the instruction K
     const double cs = sparse_cost * kbound, total = cs + es * (double)(K - kbound);
@@ -198,6 +258,7 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
   } else if (N > 0) {
     add(0, N, dense_begin, 0, dense_begin);
   }
+  if (rows_mode) choose_rows_per_group(regs, nreg, rt, waves, pl->ls.ct, pl->ls.mblocks, K, es, sparse_cost);
   spense::GemmArgs& a = pl->args;
   a.nreg = nreg;
   int32_t groups = 0;

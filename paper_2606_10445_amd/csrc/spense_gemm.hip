@@ -13,7 +13,10 @@
 // Operand layouts (measured on gfx950 with one-hot and random-integer probes):
 //   A row = lane % 16 for all four instructions; D[lane][r] = (row 4*(lane/16) + r,
 //   column lane % 16).  Dense: lane group q = lane/16 holds K [32q, 32q+32) (fp8) or
-//   [8q, 8q+8) (bf16) of both A and B.  Sparse fp8: lane group q holds the 16 kept values
+//   [8q, 8q+8) (bf16) of both A and B.  Any permutation of K applied to both operands
+//   gives the same dot products, so the dense fp8 step feeds lane group q the K range
+//   [16q, 16q+16) in bytes 0..15 and [64+16q, 64+16q+16) in bytes 16..31 (the sparse B
+//   order): each 16-byte load instruction then covers 64 contiguous bytes of a row.  Sparse fp8: lane group q holds the 16 kept values
 //   of logical K [32q, 32q+32) with their 2-bit positions in bits [2c, 2c+2) of the
 //   index register, i.e. exactly one canonical metadata word; B holds K [16q, 16q+16) in
 //   bytes 0..15 and [64+16q, 64+16q+16) in bytes 16..31.  Sparse bf16: lane group q
@@ -45,16 +48,30 @@ constexpr int kNT = 0;
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* p, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
 }
+// voffset: per-lane byte offset; soffset: wave-uniform byte offset (scalar register)
 template <int AUX>
-__device__ __forceinline__ v4i bl16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
-  return __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, AUX));
+__device__ __forceinline__ v4i bl16(__amdgpu_buffer_rsrc_t r, uint32_t off, int soff = 0) {
+  return __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, soff, AUX));
 }
 template <int AUX>
-__device__ __forceinline__ int bl4(__amdgpu_buffer_rsrc_t r, uint32_t off) {
-  return (int)__builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, AUX);
+__device__ __forceinline__ int bl4(__amdgpu_buffer_rsrc_t r, uint32_t off, int soff = 0) {
+  return (int)__builtin_amdgcn_raw_buffer_load_b32(r, (int)off, soff, AUX);
 }
 __device__ __forceinline__ v8i cat8(v4i a, v4i b) { return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7); }
 __device__ __forceinline__ uint32_t sel(bool ok, uint32_t off) { return ok ? off : kOOB; }
+
+// Matrix-core results are written several cycles after the instruction issues (up to
+// about a dozen wait states for the 8-pass fp8 instruction), and the hardware does not
+// interlock a later non-matrix read (or a matrix read of a different register) against
+// that write.  Where such a read sits in another basic block than the producing matrix
+// instruction (loop exits, the 2:4 -> dense switch, the epilogue), the compiler's own
+// padding was measured to fall short on gfx950, so these points get 20 explicit wait
+// states.  The scheduling barriers keep instructions from moving across them.
+__device__ __forceinline__ void xdl_fence() {
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 3" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+}
 
 template <int DT>
 struct Traits;
@@ -108,7 +125,9 @@ struct LaneCtx {
   int lq;
 };
 
-template <int DT, int CT, int RT, int U, bool WM>
+// FULL: every step of the stage lies inside [k, kend): no per-lane masks, the step's K
+// offset travels in the scalar offset.  Otherwise lanes past kend read zeros.
+template <int DT, int CT, int RT, int U, bool WM, bool FULL>
 __device__ __forceinline__ void load_sparse(SparseStage<DT, CT, RT, U>& st, const LaneCtx& L, const uint32_t (&vrow)[RT],
                                             const uint32_t (&mrow)[RT], const uint32_t (&xrow)[CT],
                                             const bool (&xok)[CT], int k, int kend) {
@@ -116,7 +135,18 @@ __device__ __forceinline__ void load_sparse(SparseStage<DT, CT, RT, U>& st, cons
 #pragma unroll
   for (int j = 0; j < U; ++j) {
     const int kk = k + j * Traits<DT>::KS;
-    if constexpr (DT == kFP8) {
+    if constexpr (DT == kFP8 && FULL) {
+#pragma unroll
+      for (int t = 0; t < RT; ++t) {
+        st.a[j][t] = bl16<kNT>(L.rv, vrow[t], kk >> 1);
+        if constexpr (!WM) st.ix[j][t] = bl4<kNT>(L.rm, mrow[t], 4 * (kk >> 5));
+      }
+#pragma unroll
+      for (int c = 0; c < CT; ++c) {
+        const uint32_t o = xok[c] ? xrow[c] : kOOB;
+        st.b[j][c] = cat8(bl16<0>(L.rx, o, kk), bl16<0>(L.rx, o, kk + 64));
+      }
+    } else if constexpr (DT == kFP8) {
       const bool oka = kk + 32 * lq < kend;  // this lane group's 32 logical K
 #pragma unroll
       for (int t = 0; t < RT; ++t) {
@@ -157,7 +187,8 @@ __device__ __forceinline__ void load_sparse(SparseStage<DT, CT, RT, U>& st, cons
       const int kk = k + j0 * Traits<DT>::KS;
 #pragma unroll
       for (int t = 0; t < RT; ++t) {
-        const v4i w = bl16<kNT>(L.rm, sel(kk + 128 * lq < kend, mrow[t] + 4 * (kk >> 5) + 12 * lq));
+        const v4i w = FULL ? bl16<kNT>(L.rm, mrow[t] + 12 * lq, 4 * (kk >> 5))
+                           : bl16<kNT>(L.rm, sel(kk + 128 * lq < kend, mrow[t] + 4 * (kk >> 5) + 12 * lq));
         const auto s02 = __builtin_amdgcn_permlane32_swap((unsigned)w[0], (unsigned)w[2], false, false);
         const auto s13 = __builtin_amdgcn_permlane32_swap((unsigned)w[1], (unsigned)w[3], false, false);
         const auto s01 = __builtin_amdgcn_permlane16_swap(s02[0], s13[0], false, false);
@@ -171,7 +202,7 @@ __device__ __forceinline__ void load_sparse(SparseStage<DT, CT, RT, U>& st, cons
   }
 }
 
-template <int DT, int CT, int RT, int U>
+template <int DT, int CT, int RT, int U, bool FULL>
 __device__ __forceinline__ void load_dense(DenseStage<DT, CT, RT, U>& st, const LaneCtx& L, const uint32_t (&drow)[RT],
                                            const uint32_t (&xrow)[CT], const bool (&xok)[CT], int k, int kend,
                                            int dco) {
@@ -180,17 +211,25 @@ __device__ __forceinline__ void load_dense(DenseStage<DT, CT, RT, U>& st, const 
 #pragma unroll
   for (int j = 0; j < U; ++j) {
     const int kk = k + j * Traits<DT>::KD;
-    if constexpr (DT == kFP8) {
-      const bool ok = kk + 32 * lq < kend;
+    if constexpr (DT == kFP8 && FULL) {
+#pragma unroll
+      for (int t = 0; t < RT; ++t) st.a[j][t] = cat8(bl16<kNT>(L.rd, drow[t], kk - dco), bl16<kNT>(L.rd, drow[t], kk - dco + 64));
+#pragma unroll
+      for (int c = 0; c < CT; ++c) {
+        const uint32_t o = xok[c] ? xrow[c] : kOOB;
+        st.b[j][c] = cat8(bl16<0>(L.rx, o, kk), bl16<0>(L.rx, o, kk + 64));
+      }
+    } else if constexpr (DT == kFP8) {
+      const bool ok0 = kk + 16 * lq < kend, ok1 = kk + 64 + 16 * lq < kend;
 #pragma unroll
       for (int t = 0; t < RT; ++t) {
-        const uint32_t o = sel(ok, drow[t] + (uint32_t)(kk - dco));
-        st.a[j][t] = cat8(bl16<kNT>(L.rd, o), bl16<kNT>(L.rd, o + 16));
+        const uint32_t o = drow[t] + (uint32_t)(kk - dco);
+        st.a[j][t] = cat8(bl16<kNT>(L.rd, sel(ok0, o)), bl16<kNT>(L.rd, sel(ok1, o + 64)));
       }
 #pragma unroll
       for (int c = 0; c < CT; ++c) {
-        const uint32_t o = sel(ok && xok[c], xrow[c] + kk);
-        st.b[j][c] = cat8(bl16<0>(L.rx, o), bl16<0>(L.rx, o + 16));
+        const uint32_t o = xrow[c] + kk;
+        st.b[j][c] = cat8(bl16<0>(L.rx, sel(ok0 && xok[c], o)), bl16<0>(L.rx, sel(ok1 && xok[c], o + 64)));
       }
     } else {
       const bool ok = kk + 8 * lq < kend;
@@ -225,14 +264,24 @@ __device__ __forceinline__ void mma_stage(v4f (&acc)[RT][CT], const DenseStage<D
 
 // One stage at a time: issue all loads of U steps, then feed the matrix cores.  Latency
 // is hidden by the many resident waves rather than by register double buffering, which
-// measured slower on MI355X for this access pattern.
-template <typename Stage, typename LoadFn, int RT, int CT>
-__device__ __forceinline__ void run_pipeline(v4f (&acc)[RT][CT], int k0, int kend, int step, LoadFn load) {
-  for (int k = k0; k < kend; k += step) {
+// measured slower on MI355X for this access pattern.  Whole stages run unmasked with
+// wave-uniform offsets; the last, partial stage masks lanes past kend.
+template <typename Stage, typename LoadFull, typename LoadTail, int RT, int CT>
+__device__ __forceinline__ void run_stages(v4f (&acc)[RT][CT], int k0, int kend, int step, LoadFull full,
+                                           LoadTail tail) {
+  int k = k0;
+  for (; k + step <= kend; k += step) {
     Stage st;
-    load(st, k);
+    full(st, k);
     mma_stage(acc, st);
   }
+  if (k < kend) {
+    Stage st;
+    tail(st, k);
+    xdl_fence();
+    mma_stage(acc, st);
+  }
+  xdl_fence();
 }
 
 // ---------------------------------------------------------------- epilogue
@@ -280,7 +329,7 @@ __device__ __forceinline__ void store4(const GemmArgs& a, v4f acc, int m, int n0
 template <int DT, int CT, int RT, int W, int U, bool WM>
 __global__ __launch_bounds__(64 * W) void spense_gemm_kernel(GemmArgs a) {
   typedef Traits<DT> T;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int li = lane & 15, lq = lane >> 4;
   const int g = blockIdx.x, mb = blockIdx.y;
   const int ri = (a.nreg > 1 && g >= a.reg[1].wg0) ? 1 : 0;
@@ -311,8 +360,8 @@ __global__ __launch_bounds__(64 * W) void spense_gemm_kernel(GemmArgs a) {
   for (int c = 0; c < CT; ++c) {
     const int m = m0 + 16 * c + li;
     xok[c] = m < a.M;
-    // lane group offset inside a step: sparse B pieces start at 16q (fp8) / 8q (bf16)
-    // logical K, dense B at 32q / 8q; both are encoded at load time from kk.
+    // the lane group's offset inside a step (16 bytes per group for every kind of step)
+    // is added per region below
     xrow[c] = (uint32_t)((int64_t)(xok[c] ? m : 0) * a.ldx_b);
   }
 
@@ -327,43 +376,358 @@ __global__ __launch_bounds__(64 * W) void spense_gemm_kernel(GemmArgs a) {
     uint32_t xr[CT];
 #pragma unroll
     for (int c = 0; c < CT; ++c) xr[c] = xrow[c] + (DT == kFP8 ? 16u * lq : 16u * lq);
-    run_pipeline<SparseStage<DT, CT, RT, U>>(acc, ka, ks_end, U * T::KS, [&](SparseStage<DT, CT, RT, U>& st, int k) {
-      load_sparse<DT, CT, RT, U, WM>(st, L, vrow, mrow, xr, xok, k, ks_end);
-    });
+    run_stages<SparseStage<DT, CT, RT, U>>(
+        acc, ka, ks_end, U * T::KS,
+        [&](SparseStage<DT, CT, RT, U>& st, int k) {
+          load_sparse<DT, CT, RT, U, WM, true>(st, L, vrow, mrow, xr, xok, k, ks_end);
+        },
+        [&](SparseStage<DT, CT, RT, U>& st, int k) {
+          load_sparse<DT, CT, RT, U, WM, false>(st, L, vrow, mrow, xr, xok, k, ks_end);
+        });
   }
   if (kd_beg < kb) {
     uint32_t drow[RT];
 #pragma unroll
     for (int t = 0; t < RT; ++t) {
       const int n = min(nbase + 16 * t + li, rowend - 1);
-      drow[t] = (uint32_t)((int64_t)(n - R.dense_row_off) * a.d_ld_b) + (DT == kFP8 ? 32u * lq : 16u * lq);
+      drow[t] = (uint32_t)((int64_t)(n - R.dense_row_off) * a.d_ld_b) + 16u * lq;
     }
     uint32_t xr[CT];
 #pragma unroll
-    for (int c = 0; c < CT; ++c) xr[c] = xrow[c] + (DT == kFP8 ? 32u * lq : 16u * lq);
+    for (int c = 0; c < CT; ++c) xr[c] = xrow[c] + 16u * lq;
     const int dco = R.dense_col_off;
-    run_pipeline<DenseStage<DT, CT, RT, U>>(acc, kd_beg, kb, U * T::KD, [&](DenseStage<DT, CT, RT, U>& st, int k) {
-      load_dense<DT, CT, RT, U>(st, L, drow, xr, xok, k, kb, dco);
-    });
+    run_stages<DenseStage<DT, CT, RT, U>>(
+        acc, kd_beg, kb, U * T::KD,
+        [&](DenseStage<DT, CT, RT, U>& st, int k) { load_dense<DT, CT, RT, U, true>(st, L, drow, xr, xok, k, kb, dco); },
+        [&](DenseStage<DT, CT, RT, U>& st, int k) {
+          load_dense<DT, CT, RT, U, false>(st, L, drow, xr, xok, k, kb, dco);
+        });
   }
 
-  // ---- add the waves' partial sums in LDS (wave order), then the epilogue
-  __shared__ v4f red[W * RT * CT * 64];
+  // ---- add the waves' partial sums in LDS (wave order), then the epilogue; one
+  // activation tile at a time keeps the buffer at W * RT KB
+  __shared__ v4f red[W * RT * 64];
 #pragma unroll
-  for (int t = 0; t < RT; ++t)
+  for (int c = 0; c < CT; ++c) {
+    if (c) __syncthreads();  // the previous tile's reads are done
 #pragma unroll
-    for (int c = 0; c < CT; ++c) red[((wave * RT + t) * CT + c) * 64 + lane] = acc[t][c];
-  __syncthreads();
-  for (int e = threadIdx.x; e < RT * CT * 64; e += 64 * W) {
-    const int ln = e & 63, tc = e >> 6;
-    const int t = tc / CT, c = tc - t * CT;
-    v4f s = red[e];
+    for (int t = 0; t < RT; ++t) red[(wave * RT + t) * 64 + lane] = acc[t][c];
+    __syncthreads();
+    for (int e = threadIdx.x; e < RT * 64; e += 64 * W) {
+      const int ln = e & 63, t = e >> 6;
+      v4f s = red[e];
 #pragma unroll
-    for (int w = 1; w < W; ++w) s += red[w * RT * CT * 64 + e];
-    const int m = m0 + 16 * c + (ln & 15);
-    const int n0 = nbase + 16 * t + 4 * (ln >> 4);
-    if (m < a.M && n0 < rowend) store4(a, s, m, n0, rowend);
+      for (int w = 1; w < W; ++w) s += red[w * RT * 64 + e];
+      const int m = m0 + 16 * c + (ln & 15);
+      const int n0 = nbase + 16 * t + 4 * (ln >> 4);
+      if (m < a.M && n0 < rowend) store4(a, s, m, n0, rowend);
+    }
   }
+}
+
+// ---------------------------------------------------------------- row-split kernel
+// For several activation tiles the activations are the reused operand.  Here each of the
+// first `wused` waves of a workgroup owns 16 weight rows and all of K; the waves walk K
+// together in chunks of four instruction steps.  Each chunk of activations (16*CT rows)
+// is copied once per workgroup from global memory straight into LDS (buffer loads with
+// an LDS destination; 16-byte blocks XOR-swizzled by row so the fragment reads are
+// conflict-free; two buffers), and every wave reads its B fragments from there.  The
+// weights are requested D chunks ahead into registers; the barrier that publishes the
+// next activation chunk waits only for the activation loads, so the weight loads stay
+// in flight across it.  No wave splits K: the epilogue stores from the accumulators.
+template <int DT, int CT>
+struct XTile {
+  static constexpr int KS = Traits<DT>::KS;
+  static constexpr int CHUNK_K = 4 * KS;                  // logical K per chunk
+  static constexpr int ROW_B = CHUNK_K * Traits<DT>::ES;  // bytes per activation row (512)
+  static constexpr int ROWS = 16 * CT;
+  static constexpr int BYTES = ROWS * ROW_B;
+  // LDS byte address of 16-byte block b of row r
+  __device__ static __forceinline__ int addr(int r, int b) { return r * ROW_B + ((b ^ (r & 31)) << 4); }
+};
+
+template <int DT, int CT>
+__device__ __forceinline__ v4i xlds(const uint8_t* lds, int r, int byte) {
+  return *reinterpret_cast<const v4i*>(lds + XTile<DT, CT>::addr(r, byte >> 4) + (byte & 15));
+}
+
+// B fragments of one step from the LDS tile (step_b: byte offset of the step in a row).
+// 2:4 steps and dense fp8 steps read K [16q, 16q+16) and [64+16q, 64+16q+16) of the
+// step; dense bf16 steps read K [8q, 8q+8).
+template <int DT, int CT>
+__device__ __forceinline__ void frag_pair(v8i (&b)[CT], const uint8_t* lds, int li, int lq, int step_b) {
+#pragma unroll
+  for (int c = 0; c < CT; ++c) {
+    const int r = 16 * c + li;
+    b[c] = cat8(xlds<DT, CT>(lds, r, step_b + 16 * lq), xlds<DT, CT>(lds, r, step_b + 64 + 16 * lq));
+  }
+}
+template <int DT, int CT>
+__device__ __forceinline__ void frag_one(v8i (&b)[CT], const uint8_t* lds, int li, int lq, int step_b) {
+  const v4i z = {0, 0, 0, 0};
+#pragma unroll
+  for (int c = 0; c < CT; ++c) b[c] = cat8(xlds<DT, CT>(lds, 16 * c + li, step_b + 16 * lq), z);
+}
+
+// Copy activations [m0, m0+16CT) x [kc, kc+CHUNK_K) into an LDS tile: each wave fills XI
+// consecutive 1 KB blocks (lane l writes bytes 16l..16l+15 of its block; the source
+// address applies the swizzle).  Rows past M and columns past kend are written as zeros.
+template <int DT, int CT, int XI>
+__device__ __forceinline__ void x_to_lds(uint8_t* lds, const GemmArgs& a, __amdgpu_buffer_rsrc_t rx, int m0, int kc,
+                                         int kend, int wave, int lane) {
+  typedef XTile<DT, CT> XT;
+#pragma unroll
+  for (int i = 0; i < XI; ++i) {
+    const int blk = wave * XI + i;                           // 1 KB block of the tile
+    const int r = (blk * 1024 + 16 * lane) / XT::ROW_B;      // tile row
+    const int pb = ((blk * 1024 + 16 * lane) % XT::ROW_B) >> 4;  // physical 16-byte slot
+    const int b = pb ^ (r & 31);                             // logical block stored there
+    const int kcol = kc + b * 16 / Traits<DT>::ES;
+    const int m = m0 + r;
+    const uint32_t off = sel(m < a.M && kcol < kend, (uint32_t)((int64_t)m * a.ldx_b + (int64_t)kcol * Traits<DT>::ES));
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (__attribute__((address_space(3))) void*)(lds + blk * 1024), 16, off,
+                                             0, 0, 0);
+  }
+}
+
+// Weights of one chunk in registers: eight 16-byte fragments and four metadata words.
+// fp8 (both kinds of chunk have four 128-wide steps): w[j] is step j's 2:4 value fragment
+// or the first half of its dense fragment, w[4+j] the dense second half.  bf16: w[j] is
+// step j's value fragment (2:4, j < 4) or dense fragment (eight 32-wide steps).
+struct WChunk {
+  v4i w[8];
+  int ix[4];
+};
+
+// Load instructions one chunk issues; the same for 2:4 and dense chunks (the unused ones
+// get out-of-range offsets), so the loads need no branches and the compiler keeps the
+// fragments in place while they are in flight.
+template <bool WM>
+struct ChunkLoads {
+  static constexpr int N = 8 + (WM ? 1 : 4);
+};
+
+// ok = false masks every lane (past the last chunk, or a wave that owns no rows).
+template <int DT, bool WM>
+__device__ __forceinline__ void load_chunk(WChunk& W, bool sparse, bool ok, int kc, int ke, int lq, uint32_t vrow,
+                                           uint32_t mrow, uint32_t drow, int dco, __amdgpu_buffer_rsrc_t rv,
+                                           __amdgpu_buffer_rsrc_t rm, __amdgpu_buffer_rsrc_t rd) {
+  const __amdgpu_buffer_rsrc_t rw = sparse ? rv : rd;
+  if constexpr (DT == kFP8) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int kk = kc + 128 * j;
+      // 2:4: 16 kept values of logical K [kk+32q, kk+32q+32); dense: K [kk+16q, +16) and
+      // [kk+64+16q, +16)
+      const bool oka = ok && kk + (sparse ? 32 : 16) * lq < ke;
+      const bool okb = ok && !sparse && kk + 64 + 16 * lq < ke;
+      const uint32_t oa = sparse ? vrow + (uint32_t)(kk >> 1) : drow + (uint32_t)(kk - dco);
+      W.w[j] = bl16<kNT>(rw, sel(oka, oa));
+      W.w[4 + j] = bl16<kNT>(rd, sel(okb, oa + 64));
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int kk = kc + (sparse ? 64 : 32) * j;
+      const bool okj = ok && (!sparse || j < 4) && kk + (sparse ? 16 : 8) * lq < ke;
+      const uint32_t o = sparse ? vrow + (uint32_t)kk : drow + 2 * (uint32_t)(kk - dco);
+      W.w[j] = bl16<kNT>(rw, sel(okj, o));
+    }
+  }
+  if constexpr (WM) {
+    // lane group q loads step q's four words (16 bytes of the row); they are transposed
+    // when the chunk is consumed (meta_words), not here, so the load stays in flight
+    const v4i w = bl16<kNT>(rm, sel(ok && sparse && kc + 128 * lq < ke, mrow + 4 * (kc >> 5) + 12 * lq));
+#pragma unroll
+    for (int j = 0; j < 4; ++j) W.ix[j] = w[j];
+  } else {
+    constexpr int KS = Traits<DT>::KS;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int kk = kc + j * KS;
+      W.ix[j] = bl4<kNT>(rm, sel(ok && sparse && kk + (DT == kFP8 ? 32 : 16) * lq < ke, mrow + 4 * (kk >> 5)));
+    }
+  }
+}
+
+// The metadata word of each step for this lane group.  Wide loads: lane group q holds
+// step q's four words; a 4x4 transpose across lane groups (two lane swaps) gives lane
+// group q word 4j+q of every step j.
+template <bool WM>
+__device__ __forceinline__ void meta_words(int (&ix)[4], const WChunk& W) {
+  if constexpr (WM) {
+    const auto s02 = __builtin_amdgcn_permlane32_swap((unsigned)W.ix[0], (unsigned)W.ix[2], false, false);
+    const auto s13 = __builtin_amdgcn_permlane32_swap((unsigned)W.ix[1], (unsigned)W.ix[3], false, false);
+    const auto s01 = __builtin_amdgcn_permlane16_swap(s02[0], s13[0], false, false);
+    const auto s23 = __builtin_amdgcn_permlane16_swap(s02[1], s13[1], false, false);
+    ix[0] = (int)s01[0];
+    ix[1] = (int)s01[1];
+    ix[2] = (int)s23[0];
+    ix[3] = (int)s23[1];
+  } else {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) ix[j] = W.ix[j];
+  }
+}
+
+template <int DT, int CT, bool WM>
+__device__ __forceinline__ void mma_chunk(v4f (&acc)[CT], const WChunk& W, bool sparse, const uint8_t* lds, int li,
+                                          int lq) {
+  if (sparse) {
+    int mw[4];
+    meta_words<WM>(mw, W);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      v8i b[CT];
+      frag_pair<DT, CT>(b, lds, li, lq, j * 128);
+      const int ix = DT == kFP8 ? mw[j] : (int)((uint32_t)mw[j] >> (16 * (lq & 1)));
+#pragma unroll
+      for (int c = 0; c < CT; ++c) acc[c] = mma_sparse(W.w[j], b[c], acc[c], ix, std::integral_constant<int, DT>());
+    }
+  } else if constexpr (DT == kFP8) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      v8i b[CT];
+      frag_pair<DT, CT>(b, lds, li, lq, j * 128);
+      const v8i av = cat8(W.w[j], W.w[4 + j]);
+#pragma unroll
+      for (int c = 0; c < CT; ++c) acc[c] = mma_dense(av, b[c], acc[c], std::integral_constant<int, DT>());
+    }
+  } else {
+    const v4i z = {0, 0, 0, 0};
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      v8i b[CT];
+      frag_one<DT, CT>(b, lds, li, lq, j * 64);
+      const v8i av = cat8(W.w[j], z);
+#pragma unroll
+      for (int c = 0; c < CT; ++c) acc[c] = mma_dense(av, b[c], acc[c], std::integral_constant<int, DT>());
+    }
+  }
+}
+
+// Workgroup barrier that first waits until at most N of this wave's vector-memory
+// operations are outstanding (loads complete in issue order, so every older one is
+// done).  The wait is the builtin, which the compiler's own wait insertion takes into
+// account; the barrier's memory clobber keeps LDS accesses from moving across it.
+template <int N>
+__device__ __forceinline__ void barrier_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  // s_waitcnt fields: vmcnt[3:0] and [15:14], expcnt [6:4] and lgkmcnt [11:8] left at max
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+  asm volatile("s_barrier" ::: "memory");
+}
+
+// Pipeline (per wave, in issue order within chunk step c):
+//   activations of chunk c+2 -> LDS buffer (c+2) % 3, weights of chunk c+2 -> register
+//   slot (c+2) % 3, MMAs of chunk c (LDS buffer c % 3, slot c % 3), then a barrier that
+//   waits for the activations of chunk c+1 (issued in step c-1, before that step's
+//   weights), so two chunks of weights stay in flight across it.  Three LDS buffers: the
+//   one being read, the one being published, the one being filled.
+template <int DT, int CT, int WR, bool WM>
+__global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
+  typedef XTile<DT, CT> XT;
+  constexpr int KC = XT::CHUNK_K;
+  constexpr int XI = XT::BYTES / 1024 / WR;  // 1 KB activation blocks per wave per chunk
+  static_assert(XI >= 1 && XI * 1024 * WR == XT::BYTES, "activation tile must split evenly");
+  constexpr int NL = ChunkLoads<WM>::N;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int li = lane & 15, lq = lane >> 4;
+  const int g = blockIdx.x, mb = blockIdx.y;
+  const int ri = (a.nreg > 1 && g >= a.reg[1].wg0) ? 1 : 0;
+  const Region& R = a.reg[ri];
+  const int rowend = R.row0 + R.rows;
+  const int nbase = R.row0 + ((g - R.wg0) * R.wused + wave) * 16;
+  const int m0 = mb * 16 * CT;
+  const int K = R.kend;
+  const int kbound = R.kbound;
+  const bool active = wave < R.wused && nbase < rowend;
+
+  __shared__ __attribute__((aligned(1024))) uint8_t xbuf[3][XT::BYTES];
+  const __amdgpu_buffer_rsrc_t rx = rsrc(a.X, a.x_bytes), rv = rsrc(a.values, a.v_bytes),
+                               rm = rsrc(a.meta, a.m_bytes), rd = rsrc(a.dense, a.d_bytes);
+
+  v4f acc[CT];
+#pragma unroll
+  for (int c = 0; c < CT; ++c) acc[c] = (v4f){0.f, 0.f, 0.f, 0.f};
+
+  const int n = min(nbase + li, rowend - 1);
+  const uint32_t vrow = (uint32_t)((int64_t)n * a.v_ld_b) + 16u * lq;
+  const uint32_t mrow = (uint32_t)((int64_t)n * a.m_ld_b) + (DT == kFP8 ? 4u * lq : 4u * (lq >> 1));
+  const uint32_t drow = (uint32_t)((int64_t)max(n - R.dense_row_off, 0) * a.d_ld_b) + 16u * lq;
+
+  // chunk list: 2:4 chunks start at 0 and cover [0, kbound); dense chunks start at kbound
+  const int n_sp = (kbound + KC - 1) / KC;
+  const int n_de = (K - kbound + KC - 1) / KC;
+  const int nch = n_sp + n_de;
+  auto chunk_k = [&](int c) { return c < n_sp ? c * KC : kbound + (c - n_sp) * KC; };
+  auto chunk_end = [&](int c) { return c < n_sp ? kbound : K; };
+  auto load = [&](WChunk& W, int c) {
+    load_chunk<DT, WM>(W, c < n_sp, active && c < nch, chunk_k(c), chunk_end(c), lq, vrow, mrow, drow,
+                       R.dense_col_off, rv, rm, rd);
+  };
+  auto xload = [&](int buf, int c) {
+    x_to_lds<DT, CT, XI>(xbuf[buf], a, rx, m0, chunk_k(c), c < nch ? chunk_end(c) : -1, wave, lane);
+  };
+
+  // A wave that owns rows loads weights and runs the MMAs; the others only stage
+  // activations and take part in the barriers.  The two loops are separate so that no
+  // path leaves a weight load pending where the compiler would have to wait for it.
+  auto run = [&](auto act_const) {
+    constexpr bool ACT = decltype(act_const)::value;
+    // loads issued after the activations of chunk c+1, at the barrier of chunk c
+    constexpr int AFTER = ACT ? 2 * NL + XI : XI;
+    WChunk slot[3];
+    xload(0, 0);
+    if constexpr (ACT) load(slot[0], 0);
+    xload(1, 1);
+    if constexpr (ACT) load(slot[1], 1);
+    barrier_vm<0>();
+    auto step = [&](auto s_const, int c) {
+      constexpr int S = decltype(s_const)::value;
+      constexpr int S2 = (S + 2) % 3;
+      xload(S2, c + 2);
+      __builtin_amdgcn_sched_barrier(0);
+      if constexpr (ACT) {
+        load(slot[S2], c + 2);
+        __builtin_amdgcn_sched_barrier(0);
+        mma_chunk<DT, CT, WM>(acc, slot[S], c < n_sp, xbuf[S], li, lq);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      barrier_vm<AFTER>();
+    };
+    int c = 0;
+    for (; c + 3 <= nch; c += 3) {
+      step(std::integral_constant<int, 0>(), c);
+      step(std::integral_constant<int, 1>(), c + 1);
+      step(std::integral_constant<int, 2>(), c + 2);
+    }
+    if (c < nch) step(std::integral_constant<int, 0>(), c);
+    if (c + 1 < nch) step(std::integral_constant<int, 1>(), c + 1);
+  };
+  if (active)
+    run(std::true_type());
+  else
+    run(std::false_type());
+
+  if (!active) return;
+  xdl_fence();
+#pragma unroll
+  for (int cc = 0; cc < CT; ++cc) {
+    const int m = m0 + 16 * cc + li;
+    const int n0 = nbase + 4 * lq;
+    if (m < a.M && n0 < rowend) store4(a, acc[cc], m, n0, rowend);
+  }
+}
+
+template <int DT, int CT, int WR>
+hipError_t launch_rows(const LaunchShape& ls, const GemmArgs& a, hipStream_t s) {
+  dim3 grid(a.groups, ls.mblocks), block(64 * WR);
+  if (DT == kFP8 && a.m_ld_b % 16 == 0)
+    hipLaunchKernelGGL((spense_gemm_rows_kernel<DT, CT, WR, DT == kFP8>), grid, block, 0, s, a);
+  else
+    hipLaunchKernelGGL((spense_gemm_rows_kernel<DT, CT, WR, false>), grid, block, 0, s, a);
+  return hipGetLastError();
 }
 
 template <int DT, int CT, int RT, int W, int UMAX = 0>
@@ -385,7 +749,7 @@ hipError_t launch_t(const LaunchShape& ls, const GemmArgs& a, hipStream_t s) {
 
 template <int DT, int CT>
 hipError_t launch_ct(const LaunchShape& ls, const GemmArgs& a, hipStream_t s) {
-  // W * RT * CT <= 64 keeps the LDS reduction buffer at 64 KB
+  // the LDS reduction buffer is W * RT KB
   switch (ls.rt * 100 + ls.waves + (ls.u8 && CT == 1 ? 10000 : 0)) {
     case 104: return launch_t<DT, CT, 1, 4>(ls, a, s);
     case 108: return launch_t<DT, CT, 1, 8>(ls, a, s);
@@ -399,8 +763,22 @@ hipError_t launch_ct(const LaunchShape& ls, const GemmArgs& a, hipStream_t s) {
   }
 }
 
+template <int DT, int CT>
+hipError_t launch_rows_ct(const LaunchShape& ls, const GemmArgs& a, hipStream_t s) {
+  switch (ls.rt * 100 + ls.waves) {
+    case 104: return launch_rows<DT, CT, 4>(ls, a, s);
+    case 108: return launch_rows<DT, CT, 8>(ls, a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 template <int DT>
 hipError_t launch_dt(const LaunchShape& ls, const GemmArgs& a, hipStream_t s) {
+  if (ls.rows) {
+    if (ls.ct == 1) return launch_rows_ct<DT, 1>(ls, a, s);
+    if (ls.ct == 2) return launch_rows_ct<DT, 2>(ls, a, s);
+    return launch_rows_ct<DT, 4>(ls, a, s);
+  }
   if (ls.ct == 1) return launch_ct<DT, 1>(ls, a, s);
   if (ls.ct == 2) return launch_ct<DT, 2>(ls, a, s);
   return launch_ct<DT, 4>(ls, a, s);

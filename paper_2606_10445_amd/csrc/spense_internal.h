@@ -16,14 +16,18 @@ constexpr int kMaxWaves = 16;
 // has one region with kbound = the first dense column.  A workgroup owns 16*RT rows of
 // one region; its waves split K at cut[0..waves] (cost-balanced), each wave running the
 // 2:4 loop over its part below kbound and the dense loop over the rest into one fp32
-// accumulator; the waves' partial sums are added in LDS in wave order.
+// accumulator; the waves' partial sums are added in LDS in wave order.  The row-split
+// kernel instead gives each of the first `wused` waves of a workgroup 16*RT rows over all
+// of K (fewer rows per workgroup where rows carry more bytes, to balance the CUs).
 struct Region {
   int32_t row0, rows;          // output rows [row0, row0 + rows)
   int32_t kbound;              // first dense column (K for all-2:4, 0 for all-dense)
+  int32_t kend;                // K
   int32_t dense_row_off;       // dense storage row = n - dense_row_off
   int32_t dense_col_off;       // dense storage column = k - dense_col_off
   int32_t nrb;                 // row groups (workgroups per activation block)
   int32_t wg0;                 // first workgroup of this region
+  int32_t wused;               // row-split kernel: waves of a workgroup that own rows here
   int32_t cut[kMaxWaves + 1];  // K boundaries of the waves' parts
 };
 
@@ -55,6 +59,7 @@ struct LaunchShape {
   int waves;    // waves per workgroup (4, 8, 16): they split K
   int mblocks;  // grid.y
   int u8;       // eight instruction steps per batch of loads (single activation tile only)
+  int rows;     // row-split workgroups with activations staged in LDS
 };
 
 hipError_t launch_gemm(int dtype, const LaunchShape& ls, const GemmArgs& a, hipStream_t s);

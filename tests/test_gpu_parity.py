@@ -228,6 +228,38 @@ def test_repeated_calls_are_bitwise_identical(S):
     assert all(np.array_equal(outs[0], o) for o in outs[1:])
 
 
+KERNEL_SHAPES = [dict(), dict(SPENSE_WAVES="4", SPENSE_RT="1"), dict(SPENSE_WAVES="16", SPENSE_RT="1"),
+                 dict(SPENSE_WAVES="8", SPENSE_RT="2"), dict(SPENSE_WAVES="8", SPENSE_RT="1", SPENSE_U8="1"),
+                 dict(SPENSE_ROWS="1", SPENSE_WAVES="4", SPENSE_RT="1"),
+                 dict(SPENSE_ROWS="1", SPENSE_WAVES="8", SPENSE_RT="1")]
+
+
+@pytest.mark.parametrize("axis,db", [(1, 6144), (0, 1536)])
+@pytest.mark.parametrize("dtype", [FP8, BF16])
+def test_every_kernel_shape_is_repeatable_and_within_bound(S, dtype, axis, db, monkeypatch):
+    """Repeated calls on the same inputs are bitwise identical and inside the error bound
+    for every kernel and workgroup shape, with both regions present.  This guards the
+    points where a matrix-core result is read by a later instruction in another basic
+    block (2:4 -> dense switch, loop tails, the reduction and the epilogue): a result read
+    before the matrix core has written it shows up as run-to-run differences."""
+    N, K = 2048, 8192
+    W, mask, X, sw, sx = random_case(6, 64, N, K, axis, db, dtype)
+    pw, (v, m, d) = compress_both(S, W, mask, dtype, axis, db)
+    Wd = oracle.decompress(v, m, d, N, K, dtype, axis, db)
+    for cfg in KERNEL_SHAPES:
+        for k in ("SPENSE_WAVES", "SPENSE_RT", "SPENSE_U8", "SPENSE_ROWS"):
+            monkeypatch.delenv(k, raising=False)
+        for k, val in cfg.items():
+            monkeypatch.setenv(k, val)
+        for M in (64, 33, 7, 1):
+            swd = None if sw is None else tdev(sw)
+            sxd = None if sx is None else tdev(sx[:M])
+            Xd = tdev(X[:M])
+            outs = [tnp(S.gemm(Xd, pw, swd, sxd, out_f32=True)) for _ in range(4)]
+            assert all(np.array_equal(outs[0], o) for o in outs[1:]), f"{cfg} M={M}: calls differ"
+            assert_f32_bound(outs[0], X[:M], Wd, dtype, sw, None if sx is None else sx[:M])
+
+
 def test_back_to_back_calls_with_smaller_second_call(S):
     N, K, db = 2048, 8192, 6144
     W, mask, X, sw, sx = random_case(6, 64, N, K, 1, db, FP8)
@@ -351,12 +383,18 @@ def test_full_size_exact_integers_whole_output(S, name, N, K, axis, M):
         assert np.array_equal(y32, ref["y_f32"]) and np.array_equal(ybf, ref["y_bf16"])
 
 
-@pytest.mark.parametrize("rt,waves", [(1, 4), (2, 4), (1, 8), (2, 8), (1, 16), (4, 4)])
-@pytest.mark.parametrize("dtype,axis,M", [(FP8, 1, 3), (FP8, 0, 40), (BF16, 1, 20), (FP8, 1, 64)])
-def test_every_workgroup_shape_is_exact(S, rt, waves, dtype, axis, M, monkeypatch):
-    """All built (row tiles, waves) shapes give bit-exact results on exact-integer data."""
+@pytest.mark.parametrize("rows,rt,waves,wused", [(0, 1, 4, 0), (0, 2, 4, 0), (0, 1, 8, 0), (0, 2, 8, 0), (0, 1, 16, 0),
+                                                 (0, 4, 4, 0), (1, 1, 4, 0), (1, 1, 8, 0), (1, 1, 4, 3), (1, 1, 8, 5),
+                                                 (1, 1, 8, 8)])
+@pytest.mark.parametrize("dtype,axis,M", [(FP8, 1, 3), (FP8, 0, 40), (BF16, 1, 20), (FP8, 1, 64), (BF16, 0, 17)])
+def test_every_workgroup_shape_is_exact(S, rows, rt, waves, wused, dtype, axis, M, monkeypatch):
+    """All built kernels and (row tiles, waves) shapes - K split across the waves of a
+    workgroup, or rows split with activations staged in LDS and `wused` of the waves
+    owning rows - give bit-exact results on exact-integer data."""
+    monkeypatch.setenv("SPENSE_ROWS", str(rows))
     monkeypatch.setenv("SPENSE_RT", str(rt))
     monkeypatch.setenv("SPENSE_WAVES", str(waves))
+    monkeypatch.setenv("SPENSE_WUSED", str(wused))
     N, K = 200, 1056
     db = 800 if axis == 1 else 72
     W, mask, X, sw, sx = gen.make_exact_int(12, rt * 10 + waves, M, N, K, gaxis(axis), db, gdt(dtype))
