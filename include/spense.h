@@ -37,7 +37,7 @@
 extern "C" {
 #endif
 
-#define SPENSE_ABI_VERSION 1
+#define SPENSE_ABI_VERSION 2
 
 typedef enum spense_status {
   SPENSE_OK = 0,
@@ -58,6 +58,12 @@ typedef enum spense_split {
   SPENSE_SPLIT_OUTPUT = 0, /* split along N: 2:4 rows first, dense rows last */
   SPENSE_SPLIT_INPUT = 1   /* split along K: 2:4 columns first, dense columns last */
 } spense_split;
+
+/* Storage order of a packed weight's three buffers (spense_packed_t.layout). */
+typedef enum spense_layout_kind {
+  SPENSE_LAYOUT_ROWMAJOR = 0, /* the canonical layout of spense_layout_t */
+  SPENSE_LAYOUT_TILED = 1     /* the gfx950 execution layout of spense_tiled_layout_t */
+} spense_layout_kind;
 
 /* Output flags for spense_gemm / spense_dense_gemm. */
 #define SPENSE_OUT_BF16 0u /* Y is bfloat16, round to nearest even (default) */
@@ -87,8 +93,34 @@ typedef struct spense_layout_t {
 } spense_layout_t;
 
 /*
+ * Tiled execution layout (fp8 only), filled by spense_tiled_layout.  The same bytes as
+ * the row-major layout, reordered so that every 16-byte load of the GEMM kernel's wave
+ * comes from one contiguous kilobyte (row-major storage makes each load instruction read
+ * sixteen 64-byte pieces of sixteen rows).  Each region is cut into tiles of 16 rows
+ * (the last one padded with zero rows) and chunks of 512 logical columns (the last one
+ * padded with zero columns).  With i in [0,16), q, j in [0,4), p in {0,1}, b in [0,16):
+ *   values: 4096 bytes per (tile t, chunk c) at byte (t * sparse_chunks + c) * 4096;
+ *           byte 1024 j + 16 (i + 16 q) + b is row-major value byte 256 c + 64 j + 16 q + b
+ *           of row 16 t + i of the 2:4 region.
+ *   meta:   1024 bytes per (t, c) at byte (t * sparse_chunks + c) * 1024; bytes
+ *           16 (i + 16 q) .. +15 are metadata words 16 c + 4 q .. +3 of row 16 t + i.
+ *   dense:  8192 bytes per (t, c) at byte (t * dense_chunks + c) * 8192; byte
+ *           1024 (2 j + p) + 16 (i + 16 q) + b is dense byte 512 c + 128 j + 64 p + 16 q + b
+ *           of row 16 t + i of the dense region.
+ * Positions past a region's rows or columns hold zero.  (cuSPARSELt likewise keeps its
+ * compressed matrices in a device-specific order.)
+ */
+typedef struct spense_tiled_layout_t {
+  int64_t sparse_tiles, sparse_chunks; /* 16-row tiles x 512-column chunks, 2:4 region */
+  int64_t dense_tiles, dense_chunks;   /* the same for the dense region */
+  size_t values_bytes, meta_bytes, dense_bytes;
+} spense_tiled_layout_t;
+
+/*
  * A packed weight: POD descriptor plus three caller-owned device buffers laid out as in
- * spense_layout_t.  The library never takes ownership of the buffers.
+ * spense_layout_t (layout = SPENSE_LAYOUT_ROWMAJOR, with the leading dimensions) or as
+ * in spense_tiled_layout_t (layout = SPENSE_LAYOUT_TILED; the leading dimensions are
+ * ignored).  The library never takes ownership of the buffers.
  */
 typedef struct spense_packed_t {
   int32_t dtype;       /* spense_dtype */
@@ -101,6 +133,7 @@ typedef struct spense_packed_t {
   int64_t meta_ld;
   void* dense;
   int64_t dense_ld;
+  int32_t layout; /* spense_layout_kind; 0 (row-major) when the field is left zero */
 } spense_packed_t;
 
 /*
@@ -111,6 +144,14 @@ typedef struct spense_packed_t {
  */
 int spense_layout(int64_t N, int64_t K, int32_t dtype, int32_t split, int64_t dense_begin,
                   spense_layout_t* out);
+
+/*
+ * Fill *out with the tiled execution layout of the same weight (see
+ * spense_tiled_layout_t).  Pure host call; the same requirements as spense_layout, and
+ * dtype must be SPENSE_FP8_E4M3FN (SPENSE_ERR_ARG otherwise).
+ */
+int spense_tiled_layout(int64_t N, int64_t K, int32_t dtype, int32_t split, int64_t dense_begin,
+                        spense_tiled_layout_t* out);
 
 /* Device workspace (bytes) needed by spense_compress: a counter. */
 size_t spense_compress_workspace_size(void);
@@ -142,17 +183,24 @@ int spense_compress(const void* W, int64_t ldw, const uint8_t* mask, int64_t ldm
 int spense_decompress(const spense_packed_t* packed, void* W_out, int64_t ldw, hipStream_t stream);
 
 /*
+ * Reorder a row-major packed weight (src, as written by spense_compress) into the tiled
+ * execution layout (dst: the same dtype, split, N, K and dense_begin, layout =
+ * SPENSE_LAYOUT_TILED, buffers of the sizes spense_tiled_layout gives, not overlapping
+ * src).  Every destination byte is written, padding included.  Asynchronous; fp8 only.
+ * An offline step like spense_compress: the format is the one of sec. 3.1.1 and 3.2, in
+ * the order the gfx950 kernels read it.
+ */
+int spense_tile(const spense_packed_t* src, const spense_packed_t* dst, hipStream_t stream);
+
+/*
  * Device workspace (bytes) that spense_gemm needs for this M and weight; 0 means none.
- * The workspace holds split-K partial sums and per-tile arrival counters.  Zero-fill it
- * before its first use: the counters must start at zero.  Every call returns the
- * counters to zero before it completes, so the same workspace serves later calls in
- * stream order without clearing.  Calls that may run concurrently (different streams)
- * need separate workspaces.
+ * The current kernels need none (they split K only inside a workgroup) and return 0;
+ * the workspace arguments are kept so that a later kernel may use one.
  */
 size_t spense_gemm_workspace_size(int64_t M, const spense_packed_t* packed);
 
 /*
- * Y = X W^T for a packed Spense weight, in one kernel launch:
+ * Y = X W^T for a packed Spense weight (either layout), in one kernel launch:
  *   Y[m, n] = round((sum_k x[m, k] * w[n, k]) * w_scale[n] * x_scale[m])
  * X: M x K device matrix of the weight's dtype, leading dimension ldx (elements).
  * w_scale: N fp32 per-output-channel scales; x_scale: M fp32 per-token scales; either

@@ -33,10 +33,12 @@ SPENSE_SPLIT_OUTPUT = 0
 SPENSE_SPLIT_INPUT = 1
 SPENSE_OUT_BF16 = 0
 SPENSE_OUT_F32 = 1
+SPENSE_LAYOUT_ROWMAJOR = 0
+SPENSE_LAYOUT_TILED = 1
 
-EXPORTS = ["spense_abi_version", "spense_last_error", "spense_layout", "spense_compress_workspace_size",
-           "spense_compress", "spense_decompress", "spense_gemm_workspace_size", "spense_gemm",
-           "spense_dense_gemm_workspace_size", "spense_dense_gemm"]
+EXPORTS = ["spense_abi_version", "spense_last_error", "spense_layout", "spense_tiled_layout",
+           "spense_compress_workspace_size", "spense_compress", "spense_decompress", "spense_tile",
+           "spense_gemm_workspace_size", "spense_gemm", "spense_dense_gemm_workspace_size", "spense_dense_gemm"]
 
 
 class SpenseError(RuntimeError):
@@ -52,11 +54,17 @@ class spense_layout_t(ctypes.Structure):
                 ("dense_bytes", ctypes.c_size_t)]
 
 
+class spense_tiled_layout_t(ctypes.Structure):
+    _fields_ = [("sparse_tiles", ctypes.c_int64), ("sparse_chunks", ctypes.c_int64), ("dense_tiles", ctypes.c_int64),
+                ("dense_chunks", ctypes.c_int64), ("values_bytes", ctypes.c_size_t), ("meta_bytes", ctypes.c_size_t),
+                ("dense_bytes", ctypes.c_size_t)]
+
+
 class spense_packed_t(ctypes.Structure):
     _fields_ = [("dtype", ctypes.c_int32), ("split", ctypes.c_int32), ("N", ctypes.c_int64), ("K", ctypes.c_int64),
                 ("dense_begin", ctypes.c_int64), ("values", ctypes.c_void_p), ("values_ld", ctypes.c_int64),
                 ("meta", ctypes.c_void_p), ("meta_ld", ctypes.c_int64), ("dense", ctypes.c_void_p),
-                ("dense_ld", ctypes.c_int64)]
+                ("dense_ld", ctypes.c_int64), ("layout", ctypes.c_int32)]
 
 
 def _load():
@@ -69,6 +77,8 @@ def _load():
         "spense_abi_version": (ctypes.c_int, []),
         "spense_last_error": (ctypes.c_char_p, []),
         "spense_layout": (ctypes.c_int, [i64, i64, i32, i32, i64, P(spense_layout_t)]),
+        "spense_tiled_layout": (ctypes.c_int, [i64, i64, i32, i32, i64, P(spense_tiled_layout_t)]),
+        "spense_tile": (ctypes.c_int, [P(spense_packed_t), P(spense_packed_t), p]),
         "spense_compress_workspace_size": (sz, []),
         "spense_compress": (ctypes.c_int, [p, i64, p, i64, P(spense_packed_t), P(i64), p, sz, p]),
         "spense_decompress": (ctypes.c_int, [P(spense_packed_t), p, i64, p]),
@@ -105,6 +115,16 @@ def spense_layout(N: int, K: int, dtype: int, split: int, dense_begin: int) -> s
     L = spense_layout_t()
     _check(_lib.spense_layout(N, K, dtype, split, dense_begin, ctypes.byref(L)))
     return L
+
+
+def spense_tiled_layout(N: int, K: int, dtype: int, split: int, dense_begin: int) -> spense_tiled_layout_t:
+    T = spense_tiled_layout_t()
+    _check(_lib.spense_tiled_layout(N, K, dtype, split, dense_begin, ctypes.byref(T)))
+    return T
+
+
+def spense_tile(src: spense_packed_t, dst: spense_packed_t, stream) -> int:
+    return _lib.spense_tile(ctypes.byref(src), ctypes.byref(dst), stream)
 
 
 def spense_compress_workspace_size() -> int:
@@ -195,14 +215,19 @@ def workspace_for(device) -> Workspace:
 
 
 class PackedWeight:
-    """A weight in the Spense format: device buffers (values, meta, dense) + descriptor."""
+    """A weight in the Spense format: device buffers (values, meta, dense) + descriptor.
+    ``kind`` is the storage order: SPENSE_LAYOUT_ROWMAJOR (as spense_compress writes it;
+    ``layout`` is its spense_layout_t) or SPENSE_LAYOUT_TILED (``tiled`` is its
+    spense_tiled_layout_t)."""
 
-    def __init__(self, N, K, dtype, split, dense_begin, values, meta, dense):
+    def __init__(self, N, K, dtype, split, dense_begin, values, meta, dense, kind=SPENSE_LAYOUT_ROWMAJOR):
         self.N, self.K, self.dtype, self.split, self.dense_begin = N, K, dtype, split, dense_begin
         self.values, self.meta, self.dense = values, meta, dense
+        self.kind = kind
         self.layout = spense_layout(N, K, dtype, split, dense_begin)
+        self.tiled = spense_tiled_layout(N, K, dtype, split, dense_begin) if kind == SPENSE_LAYOUT_TILED else None
         self.desc = spense_packed_t(dtype, split, N, K, dense_begin, _ptr(values), self.layout.values_ld, _ptr(meta),
-                                    self.layout.meta_ld, _ptr(dense), self.layout.dense_ld)
+                                    self.layout.meta_ld, _ptr(dense), self.layout.dense_ld, kind)
 
     @classmethod
     def empty(cls, N, K, dtype, split, dense_begin, device="cuda"):
@@ -214,7 +239,13 @@ class PackedWeight:
         return cls(N, K, dtype, split, dense_begin, values, meta, dense)
 
     def weight_bytes(self) -> int:
-        return self.layout.values_bytes + self.layout.meta_bytes + self.layout.dense_bytes
+        """Bytes of the three buffers (the tiled layout includes its zero padding)."""
+        g = self.tiled if self.kind == SPENSE_LAYOUT_TILED else self.layout
+        return g.values_bytes + g.meta_bytes + g.dense_bytes
+
+    def clone(self) -> "PackedWeight":
+        return PackedWeight(self.N, self.K, self.dtype, self.split, self.dense_begin, self.values.clone(),
+                            self.meta.clone(), self.dense.clone(), self.kind)
 
 
 def compress(W: torch.Tensor, mask: torch.Tensor | None, split: int, dense_begin: int) -> PackedWeight:
@@ -235,6 +266,18 @@ def compress(W: torch.Tensor, mask: torch.Tensor | None, split: int, dense_begin
         err.bad_groups = bad
         raise err
     return pw
+
+
+def tile(pw: PackedWeight) -> PackedWeight:
+    """The same fp8 weight in the tiled execution layout (spense_tile)."""
+    dev = (pw.dense if pw.dense.numel() else pw.values).device
+    T = spense_tiled_layout(pw.N, pw.K, pw.dtype, pw.split, pw.dense_begin)
+    values = torch.empty(T.values_bytes, dtype=torch.uint8, device=dev)
+    meta = torch.empty(T.meta_bytes // 4, dtype=torch.int32, device=dev)
+    dense = torch.empty(T.dense_bytes, dtype=torch.uint8, device=dev)
+    out = PackedWeight(pw.N, pw.K, pw.dtype, pw.split, pw.dense_begin, values, meta, dense, SPENSE_LAYOUT_TILED)
+    _check(spense_tile(pw.desc, out.desc, _stream(dev)))
+    return out
 
 
 def decompress(pw: PackedWeight) -> torch.Tensor:

@@ -88,11 +88,43 @@ int layout_impl(int64_t N, int64_t K, int32_t dtype, int32_t split, int64_t dens
   return ok();
 }
 
-// Validate a packed descriptor against its own geometry.
+constexpr int64_t kTileRows = 16, kTileCols = 512;  // tiled layout: rows x logical columns
+
+int tiled_impl(int64_t N, int64_t K, int32_t dtype, int32_t split, int64_t dense_begin, spense_tiled_layout_t* T) {
+  if (!T) return fail(SPENSE_ERR_ARG, "tiled layout: out is NULL");
+  spense_layout_t L;
+  int rc = layout_impl(N, K, dtype, split, dense_begin, &L);
+  if (rc) return rc;
+  if (dtype != SPENSE_FP8_E4M3FN) return fail(SPENSE_ERR_ARG, "the tiled layout is defined for fp8 weights only");
+  auto cdiv = [](int64_t a, int64_t b) { return (a + b - 1) / b; };
+  const bool sp = L.sparse_rows > 0 && L.sparse_cols > 0, de = L.dense_rows > 0 && L.dense_cols > 0;
+  T->sparse_tiles = sp ? cdiv(L.sparse_rows, kTileRows) : 0;
+  T->sparse_chunks = sp ? cdiv(L.sparse_cols, kTileCols) : 0;
+  T->dense_tiles = de ? cdiv(L.dense_rows, kTileRows) : 0;
+  T->dense_chunks = de ? cdiv(L.dense_cols, kTileCols) : 0;
+  T->values_bytes = (size_t)(T->sparse_tiles * T->sparse_chunks * 4096);
+  T->meta_bytes = (size_t)(T->sparse_tiles * T->sparse_chunks * 1024);
+  T->dense_bytes = (size_t)(T->dense_tiles * T->dense_chunks * 8192);
+  return ok();
+}
+
+// Validate a packed descriptor against its own geometry (either layout).
 int check_packed(const spense_packed_t* P, spense_layout_t* L) {
   if (!P) return fail(SPENSE_ERR_ARG, "packed is NULL");
   int rc = layout_impl(P->N, P->K, P->dtype, P->split, P->dense_begin, L);
   if (rc) return rc;
+  if (P->layout == SPENSE_LAYOUT_TILED) {
+    spense_tiled_layout_t T;
+    rc = tiled_impl(P->N, P->K, P->dtype, P->split, P->dense_begin, &T);
+    if (rc) return rc;
+    if (T.values_bytes && (!P->values || !P->meta))
+      return fail(SPENSE_ERR_ARG, "values/meta NULL with a non-empty 2:4 region");
+    if (T.dense_bytes && !P->dense) return fail(SPENSE_ERR_ARG, "dense NULL with a non-empty dense region");
+    if ((T.values_bytes && (!aligned16(P->values) || !aligned16(P->meta))) || (T.dense_bytes && !aligned16(P->dense)))
+      return fail(SPENSE_ERR_ALIGN, "tiled buffers must be 16-byte aligned");
+    return SPENSE_OK;
+  }
+  if (P->layout != SPENSE_LAYOUT_ROWMAJOR) return fail(SPENSE_ERR_ARG, "unknown layout %d", P->layout);
   const int es = esize(P->dtype);
   if (L->sparse_rows > 0 && L->sparse_cols > 0) {
     if (!P->values || !P->meta) return fail(SPENSE_ERR_ARG, "values/meta NULL with a non-empty 2:4 region");
@@ -173,7 +205,8 @@ void choose_rows_per_group(spense::Region* regs, int nreg, int rt, int waves, in
 // The plan depends only on the dtype, M and the weight geometry, so equal geometry gets
 // the same decomposition and summation order (the dense baseline and a Spense weight
 // with no 2:4 part are planned identically).
-void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, int64_t dense_begin, Plan* pl) {
+void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, int64_t dense_begin, bool tiled,
+               Plan* pl) {
   using spense::Region;
   memset(pl, 0, sizeof *pl);
   const int es = esize(dtype);
@@ -202,13 +235,14 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
   // shapes at every M > 16, and at M <= 16 whenever there are at least as many 16-row
   // tiles as CUs; with fewer rows the K split gives the single activation tile more
   // parallelism.  Eight waves for several activation tiles, four for one.
-  int rows_mode = (ct > 1 || ceil_div(N, 16) * pl->ls.mblocks >= kCUs) ? 1 : 0;
+  // (only the row-split kernel reads the tiled layout)
+  int rows_mode = (tiled || ct > 1 || ceil_div(N, 16) * pl->ls.mblocks >= kCUs) ? 1 : 0;
   if (rows_mode) {
     rt = 1;
     waves = ct > 1 ? 8 : 4;
   }
   const int erows = env_int("SPENSE_ROWS", -1);
-  if (erows >= 0) rows_mode = erows ? 1 : 0;
+  if (erows >= 0 && !tiled) rows_mode = erows ? 1 : 0;
   const int ert = env_int("SPENSE_RT", 0), ew = env_int("SPENSE_WAVES", 0);
   for (const auto& sh : kShapes)
     if (sh[0] == ert && sh[1] == ew) {
@@ -268,13 +302,15 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
     a.reg[i] = regs[i];
   }
   a.groups = groups;
+  a.tiled = tiled ? 1 : 0;
   pl->ws_bytes = 0;
 }
 
 int gemm_common(const void* X, int64_t M, int64_t ldx, int32_t dtype, int32_t split, int64_t N, int64_t K,
-                int64_t dense_begin, const void* values, int64_t values_ld, const uint32_t* meta, int64_t meta_ld,
-                const void* dense, int64_t dense_ld, const float* w_scale, const float* x_scale, void* Y, int64_t ldy,
-                uint32_t out_flags, void* ws, size_t ws_bytes, hipStream_t stream) {
+                int64_t dense_begin, int32_t layout, const void* values, int64_t values_ld, const uint32_t* meta,
+                int64_t meta_ld, const void* dense, int64_t dense_ld, const float* w_scale, const float* x_scale,
+                void* Y, int64_t ldy, uint32_t out_flags, void* ws, size_t ws_bytes, hipStream_t stream) {
+  const bool tiled = layout == SPENSE_LAYOUT_TILED;
   if (M < 0) return fail(SPENSE_ERR_ARG, "negative M");
   if (M > INT32_MAX) return fail(SPENSE_ERR_ARG, "M too large");
   if (out_flags & ~1u) return fail(SPENSE_ERR_ARG, "unknown out_flags 0x%x", out_flags);
@@ -292,7 +328,7 @@ int gemm_common(const void* X, int64_t M, int64_t ldx, int32_t dtype, int32_t sp
   if ((reinterpret_cast<uintptr_t>(Y) % out_es)) return fail(SPENSE_ERR_ALIGN, "Y misaligned");
   if ((int64_t)M * ldy > (int64_t)1 << 40) return fail(SPENSE_ERR_ARG, "Y too large");
   Plan pl;
-  make_plan(dtype, M, N, split, K, dense_begin, &pl);
+  make_plan(dtype, M, N, split, K, dense_begin, tiled, &pl);
   if (pl.ws_bytes > 0) {
     if (!ws || ws_bytes < pl.ws_bytes)
       return fail(SPENSE_ERR_WS, "workspace of %zu bytes needed, %zu given", pl.ws_bytes, ws ? ws_bytes : (size_t)0);
@@ -325,9 +361,16 @@ int gemm_common(const void* X, int64_t M, int64_t ldx, int32_t dtype, int32_t sp
   int64_t dense_rows = split == SPENSE_SPLIT_OUTPUT ? N - dense_begin : N;
   int64_t dense_cols = split == SPENSE_SPLIT_OUTPUT ? K : K - dense_begin;
   const int64_t xb = K > 0 ? ((M - 1) * ldx + K) * es : 0;
-  const int64_t vb = sparse_rows > 0 && sparse_cols > 0 ? ((sparse_rows - 1) * values_ld + sparse_cols / 2) * es : 0;
-  const int64_t mb = sparse_rows > 0 && sparse_cols > 0 ? ((sparse_rows - 1) * meta_ld + sparse_cols / 32) * 4 : 0;
-  const int64_t db = dense_rows > 0 && dense_cols > 0 ? ((dense_rows - 1) * dense_ld + dense_cols) * es : 0;
+  int64_t vb = sparse_rows > 0 && sparse_cols > 0 ? ((sparse_rows - 1) * values_ld + sparse_cols / 2) * es : 0;
+  int64_t mb = sparse_rows > 0 && sparse_cols > 0 ? ((sparse_rows - 1) * meta_ld + sparse_cols / 32) * 4 : 0;
+  int64_t db = dense_rows > 0 && dense_cols > 0 ? ((dense_rows - 1) * dense_ld + dense_cols) * es : 0;
+  if (tiled) {
+    spense_tiled_layout_t T;
+    tiled_impl(N, K, dtype, split, dense_begin, &T);  // validated by check_packed
+    vb = (int64_t)T.values_bytes;
+    mb = (int64_t)T.meta_bytes;
+    db = (int64_t)T.dense_bytes;
+  }
   const int64_t lim = (int64_t)1 << 31;
   if (xb >= lim || vb >= lim || mb >= lim || db >= lim)
     return fail(SPENSE_ERR_ARG, "an operand spans 2 GiB or more; split the layer");
@@ -355,12 +398,60 @@ int spense_layout(int64_t N, int64_t K, int32_t dtype, int32_t split, int64_t de
 
 size_t spense_compress_workspace_size(void) { return 256; }
 
+int spense_tiled_layout(int64_t N, int64_t K, int32_t dtype, int32_t split, int64_t dense_begin,
+                        spense_tiled_layout_t* out) {
+  return tiled_impl(N, K, dtype, split, dense_begin, out);
+}
+
+int spense_tile(const spense_packed_t* src, const spense_packed_t* dst, hipStream_t stream) {
+  spense_layout_t L, Ld;
+  int rc = check_packed(src, &L);
+  if (rc) return rc;
+  rc = check_packed(dst, &Ld);
+  if (rc) return rc;
+  if (src->layout != SPENSE_LAYOUT_ROWMAJOR || dst->layout != SPENSE_LAYOUT_TILED)
+    return fail(SPENSE_ERR_ARG, "spense_tile reorders a row-major weight into a tiled one");
+  if (src->dtype != dst->dtype || src->split != dst->split || src->N != dst->N || src->K != dst->K ||
+      src->dense_begin != dst->dense_begin)
+    return fail(SPENSE_ERR_ARG, "source and destination describe different weights");
+  spense_tiled_layout_t T;
+  rc = tiled_impl(src->N, src->K, src->dtype, src->split, src->dense_begin, &T);
+  if (rc) return rc;
+  auto overlaps = [](const void* a, size_t na, const void* b, size_t nb) {
+    const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+    return na && nb && x < y + nb && y < x + na;
+  };
+  const void* srcs[3] = {src->values, src->meta, src->dense};
+  const size_t srcn[3] = {L.values_bytes, L.meta_bytes, L.dense_bytes};
+  const void* dsts[3] = {dst->values, dst->meta, dst->dense};
+  const size_t dstn[3] = {T.values_bytes, T.meta_bytes, T.dense_bytes};
+  for (int i = 0; i < 3; ++i)
+    for (int j = 0; j < 3; ++j)
+      if (overlaps(srcs[i], srcn[i], dsts[j], dstn[j])) return fail(SPENSE_ERR_ARG, "source and destination overlap");
+  rc = check_device();
+  if (rc) return rc;
+  hipError_t e = spense::launch_tile(0, static_cast<const uint8_t*>(src->values), src->values_ld, L.sparse_rows,
+                                     L.sparse_cols / 2, T.sparse_tiles, T.sparse_chunks,
+                                     static_cast<uint8_t*>(dst->values), stream);
+  if (e == hipSuccess)
+    e = spense::launch_tile(1, reinterpret_cast<const uint8_t*>(src->meta), src->meta_ld * 4, L.sparse_rows,
+                            L.sparse_cols / 32 * 4, T.sparse_tiles, T.sparse_chunks,
+                            reinterpret_cast<uint8_t*>(dst->meta), stream);
+  if (e == hipSuccess)
+    e = spense::launch_tile(2, static_cast<const uint8_t*>(src->dense), src->dense_ld, L.dense_rows, L.dense_cols,
+                            T.dense_tiles, T.dense_chunks, static_cast<uint8_t*>(dst->dense), stream);
+  if (e != hipSuccess) return fail(SPENSE_ERR_HIP, "launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
 int spense_compress(const void* W, int64_t ldw, const uint8_t* mask, int64_t ldm, const spense_packed_t* packed,
                     int64_t* bad_groups, void* ws, size_t ws_bytes, hipStream_t stream) {
   if (bad_groups) *bad_groups = 0;
   spense_layout_t L;
   int rc = check_packed(packed, &L);
   if (rc) return rc;
+  if (packed->layout != SPENSE_LAYOUT_ROWMAJOR)
+    return fail(SPENSE_ERR_ARG, "spense_compress writes the row-major layout (then spense_tile)");
   const int64_t N = packed->N, K = packed->K;
   const int es = esize(packed->dtype);
   if (N == 0 || K == 0) return ok();
@@ -400,6 +491,7 @@ int spense_decompress(const spense_packed_t* packed, void* W_out, int64_t ldw, h
   spense_layout_t L;
   int rc = check_packed(packed, &L);
   if (rc) return rc;
+  if (packed->layout != SPENSE_LAYOUT_ROWMAJOR) return fail(SPENSE_ERR_ARG, "spense_decompress reads the row-major layout");
   const int64_t N = packed->N, K = packed->K;
   const int es = esize(packed->dtype);
   if (N == 0 || K == 0) return ok();
@@ -423,7 +515,8 @@ size_t spense_gemm_workspace_size(int64_t M, const spense_packed_t* packed) {
   spense_layout_t L;
   if (M <= 0 || check_packed(packed, &L)) return 0;
   Plan pl;
-  make_plan(packed->dtype, M, packed->N, packed->split, packed->K, packed->dense_begin, &pl);
+  make_plan(packed->dtype, M, packed->N, packed->split, packed->K, packed->dense_begin,
+            packed->layout == SPENSE_LAYOUT_TILED, &pl);
   return pl.ws_bytes;
 }
 
@@ -434,7 +527,7 @@ int spense_gemm(const void* X, int64_t M, int64_t ldx, const spense_packed_t* pa
   int rc = check_packed(packed, &L);
   if (rc) return rc;
   return gemm_common(X, M, ldx, packed->dtype, packed->split, packed->N, packed->K, packed->dense_begin,
-                     packed->values, packed->values_ld, packed->meta, packed->meta_ld, packed->dense,
+                     packed->layout, packed->values, packed->values_ld, packed->meta, packed->meta_ld, packed->dense,
                      packed->dense_ld, w_scale, x_scale, Y, ldy, out_flags, ws, ws_bytes, stream);
 }
 
@@ -442,7 +535,7 @@ size_t spense_dense_gemm_workspace_size(int64_t M, int64_t N, int64_t K, int32_t
   spense_layout_t L;
   if (M <= 0 || layout_impl(N, K, dtype, SPENSE_SPLIT_OUTPUT, 0, &L)) return 0;
   Plan pl;
-  make_plan(dtype, M, N, SPENSE_SPLIT_OUTPUT, K, 0, &pl);
+  make_plan(dtype, M, N, SPENSE_SPLIT_OUTPUT, K, 0, false, &pl);
   return pl.ws_bytes;
 }
 
@@ -458,8 +551,8 @@ int spense_dense_gemm(const void* X, int64_t M, int64_t ldx, const void* W, int6
     if (ldw < K) return fail(SPENSE_ERR_ARG, "ldw < K");
     if (!aligned16(W) || (ldw * es) % 16) return fail(SPENSE_ERR_ALIGN, "W must be 16-byte aligned, 16-byte pitch");
   }
-  return gemm_common(X, M, ldx, dtype, SPENSE_SPLIT_OUTPUT, N, K, 0, nullptr, 0, nullptr, 0, W, ldw, w_scale, x_scale,
-                     Y, ldy, out_flags, ws, ws_bytes, stream);
+  return gemm_common(X, M, ldx, dtype, SPENSE_SPLIT_OUTPUT, N, K, 0, SPENSE_LAYOUT_ROWMAJOR, nullptr, 0, nullptr, 0, W,
+                     ldw, w_scale, x_scale, Y, ldy, out_flags, ws, ws_bytes, stream);
 }
 
 }  // extern "C"

@@ -165,6 +165,42 @@ __global__ __launch_bounds__(256) void copy2d_kernel(const uint8_t* __restrict__
 
 __global__ void zero_u64_kernel(unsigned long long* p) { *p = 0ull; }
 
+// Reorder one region of a row-major packed fp8 weight into the tiled execution layout
+// (one thread per 16-byte destination block; positions past the region are zero).
+// Destination block g lies in tile-chunk tc = g / per (tile t = tc / chunks, chunk
+// c = tc % chunks); within it, instruction n = (g % per) / 64 and lane l = g % 64 =
+// i + 16 q read 16 bytes of row 16 t + i:
+//   kind 0 (2:4 values, per = 256): value bytes 256 c + 64 n + 16 q;
+//   kind 1 (metadata, per = 64):   words 16 c + 4 q .. +3 (copied one word at a time);
+//   kind 2 (dense, per = 512):     bytes 512 c + 128 (n / 2) + 64 (n % 2) + 16 q.
+__global__ __launch_bounds__(256) void tile_kernel(int kind, const uint8_t* __restrict__ src, int64_t src_ld_b,
+                                                   int64_t rows, int64_t row_bytes, int64_t chunks,
+                                                   uint8_t* __restrict__ dst, int64_t nblocks) {
+  const int per = kind == 0 ? 256 : (kind == 1 ? 64 : 512);
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; g < nblocks; g += stride) {
+    const int64_t tc = g / per;
+    const int w = (int)(g - tc * per);
+    const int64_t t = tc / chunks, c = tc - t * chunks;
+    const int l = w & 63, n = w >> 6, i = l & 15, q = l >> 4;
+    const int64_t row = 16 * t + i;
+    const int64_t byte = kind == 0 ? 256 * c + 64 * n + 16 * q
+                                   : (kind == 1 ? 4 * (16 * c + 4 * q) : 512 * c + 128 * (n >> 1) + 64 * (n & 1) + 16 * q);
+    v4i v = {0, 0, 0, 0};
+    if (row < rows) {
+      const uint8_t* sp = src + row * src_ld_b + byte;
+      if (kind == 1) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          if (byte + 4 * k + 4 <= row_bytes) v[k] = reinterpret_cast<const int*>(sp)[k];
+      } else if (byte + 16 <= row_bytes) {
+        v = *reinterpret_cast<const v4i*>(sp);
+      }
+    }
+    *reinterpret_cast<v4i*>(dst + 16 * g) = v;
+  }
+}
+
 inline unsigned grid_for(int64_t n) {
   int64_t g = (n + 255) / 256;
   if (g > 8192) g = 8192;
@@ -172,6 +208,16 @@ inline unsigned grid_for(int64_t n) {
 }
 
 }  // namespace
+
+hipError_t launch_tile(int kind, const uint8_t* src, int64_t src_ld_b, int64_t rows, int64_t row_bytes, int64_t tiles,
+                       int64_t chunks, uint8_t* dst, hipStream_t s) {
+  const int64_t per = kind == 0 ? 256 : (kind == 1 ? 64 : 512);
+  const int64_t nblocks = tiles * chunks * per;
+  if (nblocks == 0) return hipSuccess;
+  hipLaunchKernelGGL(tile_kernel, dim3(grid_for(nblocks)), dim3(256), 0, s, kind, src, src_ld_b, rows, row_bytes,
+                     chunks, dst, nblocks);
+  return hipGetLastError();
+}
 
 hipError_t launch_zero_u64(unsigned long long* p, hipStream_t s) {
   hipLaunchKernelGGL(zero_u64_kernel, dim3(1), dim3(1), 0, s, p);

@@ -555,6 +555,27 @@ __device__ __forceinline__ void load_chunk(WChunk& W, bool sparse, bool ok, int 
   }
 }
 
+// Tiled layout (fp8): each fragment of the chunk is one contiguous kilobyte.  vt, mt, dt:
+// this lane's byte offset in its tile's first 2:4 / metadata / dense chunk (16 * lane
+// included); cs, cd >= 0: the chunk's index within the 2:4 / dense part.  The chunk part
+// of the address travels in the scalar offset; ok = false masks every lane.
+__device__ __forceinline__ void load_chunk_tiled(WChunk& W, bool sparse, bool ok, int cs, int cd, uint32_t vt,
+                                                 uint32_t mt, uint32_t dt, __amdgpu_buffer_rsrc_t rv,
+                                                 __amdgpu_buffer_rsrc_t rm, __amdgpu_buffer_rsrc_t rd) {
+  const __amdgpu_buffer_rsrc_t rw = sparse ? rv : rd;
+  const uint32_t base = sel(ok, sparse ? vt : dt);
+  const uint32_t dbase = sel(ok && !sparse, dt);
+  const int s0 = sparse ? cs * 4096 : cd * 8192, sj = sparse ? 1024 : 2048;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    W.w[j] = bl16<kNT>(rw, base, s0 + sj * j);
+    W.w[4 + j] = bl16<kNT>(rd, dbase, cd * 8192 + 2048 * j + 1024);
+  }
+  const v4i w = bl16<kNT>(rm, sel(ok && sparse, mt), cs * 1024);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) W.ix[j] = w[j];
+}
+
 // The metadata word of each step for this lane group.  Wide loads: lane group q holds
 // step q's four words; a 4x4 transpose across lane groups (two lane swaps) gives lane
 // group q word 4j+q of every step j.
@@ -575,38 +596,57 @@ __device__ __forceinline__ void meta_words(int (&ix)[4], const WChunk& W) {
   }
 }
 
-template <int DT, int CT, bool WM>
+// MMAs of one chunk.  The B fragments of P steps are read from LDS before their MMAs,
+// so the LDS latency is paid once per group rather than once per step.
+template <int DT, int CT, bool WM, int P>
 __device__ __forceinline__ void mma_chunk(v4f (&acc)[CT], const WChunk& W, bool sparse, const uint8_t* lds, int li,
                                           int lq) {
+  static_assert(P == 1 || P == 2 || P == 4, "fragment group size");
   if (sparse) {
     int mw[4];
     meta_words<WM>(mw, W);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      v8i b[CT];
-      frag_pair<DT, CT>(b, lds, li, lq, j * 128);
-      const int ix = DT == kFP8 ? mw[j] : (int)((uint32_t)mw[j] >> (16 * (lq & 1)));
+    for (int j0 = 0; j0 < 4; j0 += P) {
+      v8i b[P][CT];
 #pragma unroll
-      for (int c = 0; c < CT; ++c) acc[c] = mma_sparse(W.w[j], b[c], acc[c], ix, std::integral_constant<int, DT>());
+      for (int j = 0; j < P; ++j) frag_pair<DT, CT>(b[j], lds, li, lq, (j0 + j) * 128);
+      if constexpr (P > 1) __builtin_amdgcn_sched_barrier(0);  // all reads of the group before its MMAs
+#pragma unroll
+      for (int j = 0; j < P; ++j) {
+        const int ix = DT == kFP8 ? mw[j0 + j] : (int)((uint32_t)mw[j0 + j] >> (16 * (lq & 1)));
+#pragma unroll
+        for (int c = 0; c < CT; ++c)
+          acc[c] = mma_sparse(W.w[j0 + j], b[j][c], acc[c], ix, std::integral_constant<int, DT>());
+      }
     }
   } else if constexpr (DT == kFP8) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      v8i b[CT];
-      frag_pair<DT, CT>(b, lds, li, lq, j * 128);
-      const v8i av = cat8(W.w[j], W.w[4 + j]);
+    for (int j0 = 0; j0 < 4; j0 += P) {
+      v8i b[P][CT];
 #pragma unroll
-      for (int c = 0; c < CT; ++c) acc[c] = mma_dense(av, b[c], acc[c], std::integral_constant<int, DT>());
+      for (int j = 0; j < P; ++j) frag_pair<DT, CT>(b[j], lds, li, lq, (j0 + j) * 128);
+      if constexpr (P > 1) __builtin_amdgcn_sched_barrier(0);  // all reads of the group before its MMAs
+#pragma unroll
+      for (int j = 0; j < P; ++j) {
+        const v8i av = cat8(W.w[j0 + j], W.w[4 + j0 + j]);
+#pragma unroll
+        for (int c = 0; c < CT; ++c) acc[c] = mma_dense(av, b[j][c], acc[c], std::integral_constant<int, DT>());
+      }
     }
   } else {
     const v4i z = {0, 0, 0, 0};
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      v8i b[CT];
-      frag_one<DT, CT>(b, lds, li, lq, j * 64);
-      const v8i av = cat8(W.w[j], z);
+    for (int j0 = 0; j0 < 8; j0 += 2 * P) {
+      v8i b[2 * P][CT];
 #pragma unroll
-      for (int c = 0; c < CT; ++c) acc[c] = mma_dense(av, b[c], acc[c], std::integral_constant<int, DT>());
+      for (int j = 0; j < 2 * P; ++j) frag_one<DT, CT>(b[j], lds, li, lq, (j0 + j) * 64);
+      if constexpr (P > 1) __builtin_amdgcn_sched_barrier(0);  // all reads of the group before its MMAs
+#pragma unroll
+      for (int j = 0; j < 2 * P; ++j) {
+        const v8i av = cat8(W.w[j0 + j], z);
+#pragma unroll
+        for (int c = 0; c < CT; ++c) acc[c] = mma_dense(av, b[j][c], acc[c], std::integral_constant<int, DT>());
+      }
     }
   }
 }
@@ -623,14 +663,17 @@ __device__ __forceinline__ void barrier_vm() {
   asm volatile("s_barrier" ::: "memory");
 }
 
-// Pipeline (per wave, in issue order within chunk step c):
-//   activations of chunk c+2 -> LDS buffer (c+2) % 3, weights of chunk c+2 -> register
-//   slot (c+2) % 3, MMAs of chunk c (LDS buffer c % 3, slot c % 3), then a barrier that
-//   waits for the activations of chunk c+1 (issued in step c-1, before that step's
-//   weights), so two chunks of weights stay in flight across it.  Three LDS buffers: the
-//   one being read, the one being published, the one being filled.
-template <int DT, int CT, int WR, bool WM>
+// Pipeline with NS register slots and NS LDS buffers, D = NS-1 chunks ahead (per wave,
+// in issue order within chunk step c): activations of chunk c+D -> LDS buffer
+// (c+D) % NS, weights of chunk c+D -> register slot (c+D) % NS, MMAs of chunk c (buffer
+// and slot c % NS), then a barrier that waits for the activations of chunk c+1 (issued
+// in step c+1-D, before that step's weights), so D chunks of weights stay in flight
+// across it.  The buffer being filled held chunk c-1, which every wave has finished.
+template <int DT, int CT, int WR, bool WM, int NS, int P, bool TL>
 __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
+  static_assert(NS == 3 || NS == 4, "three or four pipeline slots");
+  static_assert(!TL || (DT == kFP8 && WM), "the tiled layout is fp8 with whole-chunk metadata loads");
+  constexpr int D = NS - 1;
   typedef XTile<DT, CT> XT;
   constexpr int KC = XT::CHUNK_K;
   constexpr int XI = XT::BYTES / 1024 / WR;  // 1 KB activation blocks per wave per chunk
@@ -648,7 +691,7 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
   const int kbound = R.kbound;
   const bool active = wave < R.wused && nbase < rowend;
 
-  __shared__ __attribute__((aligned(1024))) uint8_t xbuf[3][XT::BYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t xbuf[NS][XT::BYTES];
   const __amdgpu_buffer_rsrc_t rx = rsrc(a.X, a.x_bytes), rv = rsrc(a.values, a.v_bytes),
                                rm = rsrc(a.meta, a.m_bytes), rd = rsrc(a.dense, a.d_bytes);
 
@@ -667,9 +710,20 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
   const int nch = n_sp + n_de;
   auto chunk_k = [&](int c) { return c < n_sp ? c * KC : kbound + (c - n_sp) * KC; };
   auto chunk_end = [&](int c) { return c < n_sp ? kbound : K; };
+  // tiled layout: offsets of this lane in its tile's first chunk of each part
+  uint32_t vt = 0, mt = 0, dt = 0;
+  if constexpr (TL) {
+    const uint32_t ts = (uint32_t)(nbase / 16), td = (uint32_t)((nbase - R.dense_row_off) / 16);
+    vt = ts * (uint32_t)n_sp * 4096u + 16u * lane;
+    mt = ts * (uint32_t)n_sp * 1024u + 16u * lane;
+    dt = td * (uint32_t)n_de * 8192u + 16u * lane;
+  }
   auto load = [&](WChunk& W, int c) {
-    load_chunk<DT, WM>(W, c < n_sp, active && c < nch, chunk_k(c), chunk_end(c), lq, vrow, mrow, drow,
-                       R.dense_col_off, rv, rm, rd);
+    if constexpr (TL)
+      load_chunk_tiled(W, c < n_sp, active && c < nch, c, max(c - n_sp, 0), vt, mt, dt, rv, rm, rd);
+    else
+      load_chunk<DT, WM>(W, c < n_sp, active && c < nch, chunk_k(c), chunk_end(c), lq, vrow, mrow, drow,
+                         R.dense_col_off, rv, rm, rd);
   };
   auto xload = [&](int buf, int c) {
     x_to_lds<DT, CT, XI>(xbuf[buf], a, rx, m0, chunk_k(c), c < nch ? chunk_end(c) : -1, wave, lane);
@@ -680,35 +734,40 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
   // path leaves a weight load pending where the compiler would have to wait for it.
   auto run = [&](auto act_const) {
     constexpr bool ACT = decltype(act_const)::value;
-    // loads issued after the activations of chunk c+1, at the barrier of chunk c
-    constexpr int AFTER = ACT ? 2 * NL + XI : XI;
-    WChunk slot[3];
-    xload(0, 0);
-    if constexpr (ACT) load(slot[0], 0);
-    xload(1, 1);
-    if constexpr (ACT) load(slot[1], 1);
+    // loads issued after the activations of chunk c+1, at the barrier of chunk c: that
+    // step's weights, then D-1 further steps of activations and weights
+    constexpr int AFTER = ACT ? NL + (D - 1) * (XI + NL) : (D - 1) * XI;
+    WChunk slot[NS];
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      xload(d, d);
+      if constexpr (ACT) load(slot[d], d);
+    }
     barrier_vm<0>();
     auto step = [&](auto s_const, int c) {
       constexpr int S = decltype(s_const)::value;
-      constexpr int S2 = (S + 2) % 3;
-      xload(S2, c + 2);
+      constexpr int SD = (S + D) % NS;
+      xload(SD, c + D);
       __builtin_amdgcn_sched_barrier(0);
       if constexpr (ACT) {
-        load(slot[S2], c + 2);
+        load(slot[SD], c + D);
         __builtin_amdgcn_sched_barrier(0);
-        mma_chunk<DT, CT, WM>(acc, slot[S], c < n_sp, xbuf[S], li, lq);
+        mma_chunk<DT, CT, WM, P>(acc, slot[S], c < n_sp, xbuf[S], li, lq);
         __builtin_amdgcn_sched_barrier(0);
       }
       barrier_vm<AFTER>();
     };
     int c = 0;
-    for (; c + 3 <= nch; c += 3) {
+    for (; c + NS <= nch; c += NS) {
       step(std::integral_constant<int, 0>(), c);
       step(std::integral_constant<int, 1>(), c + 1);
       step(std::integral_constant<int, 2>(), c + 2);
+      if constexpr (NS == 4) step(std::integral_constant<int, 3 % NS>(), c + 3);
     }
     if (c < nch) step(std::integral_constant<int, 0>(), c);
     if (c + 1 < nch) step(std::integral_constant<int, 1>(), c + 1);
+    if constexpr (NS == 4)
+      if (c + 2 < nch) step(std::integral_constant<int, 2>(), c + 2);
   };
   if (active)
     run(std::true_type());
@@ -725,14 +784,29 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
   }
 }
 
+// Pipeline depth and fragment grouping per instance, chosen to stay within the register
+// file: four slots and whole-chunk fragment groups for up to two activation tiles, three
+// slots and two-step groups for four; fp8 without wide metadata loads (metadata rows not
+// 16-byte aligned, four separately masked loads per chunk) one step lighter, and even so
+// its four-tile, eight-wave instance spills a few registers.
+template <int DT, int CT, int WR, bool WM, bool TL>
+hipError_t launch_rows_wm(const dim3& grid, const dim3& block, const GemmArgs& a, hipStream_t s) {
+  constexpr bool light = DT == kFP8 && !WM;
+  constexpr int NS = CT <= 2 && !light ? 4 : 3;
+  constexpr int P = CT == 1 ? 4 : 1;
+  hipLaunchKernelGGL((spense_gemm_rows_kernel<DT, CT, WR, WM, NS, P, TL>), grid, block, 0, s, a);
+  return hipGetLastError();
+}
+
 template <int DT, int CT, int WR>
 hipError_t launch_rows(const LaunchShape& ls, const GemmArgs& a, hipStream_t s) {
   dim3 grid(a.groups, ls.mblocks), block(64 * WR);
-  if (DT == kFP8 && a.m_ld_b % 16 == 0)
-    hipLaunchKernelGGL((spense_gemm_rows_kernel<DT, CT, WR, DT == kFP8>), grid, block, 0, s, a);
-  else
-    hipLaunchKernelGGL((spense_gemm_rows_kernel<DT, CT, WR, false>), grid, block, 0, s, a);
-  return hipGetLastError();
+  if constexpr (DT == kFP8) {
+    if (a.tiled) return launch_rows_wm<DT, CT, WR, true, true>(grid, block, a, s);
+    if (a.m_ld_b % 16 == 0) return launch_rows_wm<DT, CT, WR, true, false>(grid, block, a, s);
+  }
+  if (a.tiled) return hipErrorInvalidValue;
+  return launch_rows_wm<DT, CT, WR, false, false>(grid, block, a, s);
 }
 
 template <int DT, int CT, int RT, int W, int UMAX = 0>
@@ -779,6 +853,7 @@ hipError_t launch_rows_ct(const LaunchShape& ls, const GemmArgs& a, hipStream_t 
 
 template <int DT>
 hipError_t launch_dt(const LaunchShape& ls, const GemmArgs& a, hipStream_t s) {
+  if (a.tiled && !ls.rows) return hipErrorInvalidValue;  // only the row-split kernel reads the tiled layout
   if (ls.rows) {
     if (ls.ct == 1) return launch_rows_ct<DT, 1>(ls, a, s);
     if (ls.ct == 2) return launch_rows_ct<DT, 2>(ls, a, s);

@@ -50,6 +50,7 @@ struct GemmArgs {
   int32_t vec_store;  // 4 consecutive outputs may be stored as one vector
   int32_t nreg;
   int32_t groups;
+  int32_t tiled;  // weight buffers in the tiled execution layout (fp8, row-split kernel)
   Region reg[2];
 };
 
@@ -74,5 +75,10 @@ hipError_t launch_decompress(int dtype, const uint8_t* values, int64_t v_ld_b, c
                              int64_t d_ld_b, int64_t d_rows, int64_t d_cols_b, uint8_t* ddst, hipStream_t s);
 
 hipError_t launch_zero_u64(unsigned long long* p, hipStream_t s);
+
+// Tiled execution layout: kind 0 values, 1 metadata, 2 dense (fp8).  src is one row-major
+// region (rows x row_bytes, pitch src_ld_b); dst receives tiles x chunks blocks.
+hipError_t launch_tile(int kind, const uint8_t* src, int64_t src_ld_b, int64_t rows, int64_t row_bytes, int64_t tiles,
+                       int64_t chunks, uint8_t* dst, hipStream_t s);
 
 }  // namespace spense

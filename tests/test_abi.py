@@ -41,7 +41,7 @@ def test_library_exports_every_declared_symbol(S):
     for n in _declared():
         assert hasattr(lib, n), f"{n} declared in include/ but not exported"
     assert set(_declared()) == set(S.EXPORTS)
-    assert S.spense_abi_version() == 1
+    assert S.spense_abi_version() == 2
 
 
 @pytest.mark.parametrize("N,K,split,db", [(256, 512, 0, 192), (256, 512, 1, 384), (25600, 5120, 0, 19200),
@@ -127,3 +127,50 @@ def test_workspace_size_is_a_pure_function_of_geometry(S):
     pk0 = S.spense_packed_t(1, 0, 4096, 5120, 0, None, L0.values_ld, None, L0.meta_ld, 16384, L0.dense_ld)
     for m in (1, 8, 64):
         assert S.spense_gemm_workspace_size(m, pk0) == S.spense_dense_gemm_workspace_size(m, 4096, 5120, 1)
+
+
+@pytest.mark.parametrize("N,K,split,db", [(25600, 5120, 0, 19200), (5120, 25600, 1, 19200), (17, 96, 0, 0),
+                                          (17, 96, 1, 96), (200, 1056, 1, 800), (200, 1056, 0, 72), (0, 64, 0, 0)])
+def test_tiled_layout_geometry(S, N, K, split, db):
+    """Tiles of 16 rows and chunks of 512 logical columns per region, 4096 / 1024 / 8192
+    bytes per (tile, chunk) for values / metadata / dense (the header's definition)."""
+    T = S.spense_tiled_layout(N, K, 1, split, db)
+    sr, sc = (db, K) if split == 0 else (N, db)
+    dr, dc = (N - db, K) if split == 0 else (N, K - db)
+    cdiv = lambda a, b: -(-a // b)
+    st, sch = (cdiv(sr, 16), cdiv(sc, 512)) if sr and sc else (0, 0)
+    dt, dch = (cdiv(dr, 16), cdiv(dc, 512)) if dr and dc else (0, 0)
+    assert (T.sparse_tiles, T.sparse_chunks, T.dense_tiles, T.dense_chunks) == (st, sch, dt, dch)
+    assert (T.values_bytes, T.meta_bytes, T.dense_bytes) == (st * sch * 4096, st * sch * 1024, dt * dch * 8192)
+
+
+def test_tiled_layout_is_fp8_only(S):
+    with pytest.raises(S.SpenseError) as e:
+        S.spense_tiled_layout(64, 128, 2, 0, 32)
+    assert e.value.code == S.SPENSE_ERR_ARG
+
+
+def test_tiled_descriptor_validation(S):
+    """Tiled descriptors are checked before any device call; their leading dimensions
+    are ignored."""
+    good = S.spense_packed_t(1, 0, 64, 128, 32, 4096, 0, 8192, 0, 16384, 0, S.SPENSE_LAYOUT_TILED)
+    assert S.spense_gemm(None, 0, 128, good, None, None, None, 64, 0, None, 0, None) == S.SPENSE_OK
+    bad = S.spense_packed_t(1, 0, 64, 128, 32, None, 0, 8192, 0, 16384, 0, S.SPENSE_LAYOUT_TILED)
+    assert S.spense_gemm(4096, 4, 128, bad, None, None, 4096, 64, 0, None, 0, None) == S.SPENSE_ERR_ARG
+    bad = S.spense_packed_t(1, 0, 64, 128, 32, 4104, 0, 8192, 0, 16384, 0, S.SPENSE_LAYOUT_TILED)
+    assert S.spense_gemm(4096, 4, 128, bad, None, None, 4096, 64, 0, None, 0, None) == S.SPENSE_ERR_ALIGN
+    bad = S.spense_packed_t(2, 0, 64, 128, 32, 4096, 0, 8192, 0, 16384, 0, S.SPENSE_LAYOUT_TILED)
+    assert S.spense_gemm(4096, 4, 128, bad, None, None, 4096, 64, 0, None, 0, None) == S.SPENSE_ERR_ARG
+    bad = S.spense_packed_t(1, 0, 64, 128, 32, 4096, 0, 8192, 0, 16384, 0, 7)
+    assert S.spense_gemm(4096, 4, 128, bad, None, None, 4096, 64, 0, None, 0, None) == S.SPENSE_ERR_ARG
+    # spense_tile takes a row-major source and a tiled destination of the same weight
+    L = S.spense_layout(64, 128, 1, 0, 32)
+    src = S.spense_packed_t(1, 0, 64, 128, 32, 4096, L.values_ld, 8192, L.meta_ld, 16384, L.dense_ld)
+    dst = S.spense_packed_t(1, 0, 64, 128, 32, 1 << 20, 0, 2 << 20, 0, 3 << 20, 0, S.SPENSE_LAYOUT_TILED)
+    assert S.spense_tile(dst, src, None) == S.SPENSE_ERR_ARG
+    other = S.spense_packed_t(1, 0, 64, 128, 48, 1 << 20, 0, 2 << 20, 0, 3 << 20, 0, S.SPENSE_LAYOUT_TILED)
+    assert S.spense_tile(src, other, None) == S.SPENSE_ERR_ARG
+    overlap = S.spense_packed_t(1, 0, 64, 128, 32, 4096 + 1024, 0, 2 << 20, 0, 3 << 20, 0, S.SPENSE_LAYOUT_TILED)
+    assert S.spense_tile(src, overlap, None) == S.SPENSE_ERR_ARG
+    # compress and decompress work on the row-major layout only
+    assert S.spense_decompress(dst, 4096, 128, None) == S.SPENSE_ERR_ARG

@@ -300,6 +300,76 @@ def test_error_paths_leave_output_untouched(S):
     assert torch.all(Y == 3.0)
 
 
+# ------------------------------------------------------------------ tiled execution layout
+def tiled_reference(v, m, d, N, K, axis, db):
+    """The tiled layout built on the CPU from the row-major buffers, by padding and
+    reshaping as the header defines it (tiles of 16 rows, chunks of 512 columns)."""
+    sr, sc = (db, K) if axis == 0 else (N, db)
+    dr, dc = (N - db, K) if axis == 0 else (N, K - db)
+
+    def pad(a, rows, cols):
+        out = np.zeros((rows, cols), a.dtype)
+        out[:a.shape[0], :a.shape[1]] = a
+        return out
+
+    vt = mt = np.zeros(0, np.uint8)
+    if sr and sc:
+        T, C = -(-sr // 16), -(-sc // 512)
+        vp = pad(v.reshape(sr, sc // 2), 16 * T, 256 * C)  # byte 256c + 64j + 16q + b of row 16t + i
+        vt = vp.reshape(T, 16, C, 4, 4, 16).transpose(0, 2, 3, 4, 1, 5).ravel()
+        mp = pad(m.reshape(sr, sc // 32), 16 * T, 16 * C)  # word 16c + 4q + k of row 16t + i
+        mt = mp.reshape(T, 16, C, 4, 4).transpose(0, 2, 3, 1, 4).ravel().view(np.uint8)
+    dt = np.zeros(0, np.uint8)
+    if dr and dc:
+        T, C = -(-dr // 16), -(-dc // 512)
+        dp = pad(d.reshape(dr, dc), 16 * T, 512 * C)  # byte 512c + 128j + 64p + 16q + b
+        dt = dp.reshape(T, 16, C, 4, 2, 4, 16).transpose(0, 2, 3, 4, 5, 1, 6).ravel()
+    return vt, mt, dt
+
+
+TILE_CASES = [(0, 256, 1024, 192), (1, 256, 1024, 768), (0, 200, 1056, 72), (1, 200, 1056, 800), (0, 17, 96, 0),
+              (1, 17, 96, 96), (0, 40, 544, 40), (1, 33, 2080, 32)]
+
+
+@pytest.mark.parametrize("axis,N,K,db", TILE_CASES)
+def test_tile_matches_definition(S, axis, N, K, db):
+    W, mask, X, sw, sx = random_case(30 + N, 4, N, K, axis, db, FP8)
+    pw, (v, m, d) = compress_both(S, W, mask, FP8, axis, db)
+    pwt = S.tile(pw)
+    torch.cuda.synchronize()
+    vt, mt, dt = tiled_reference(v, m, d, N, K, axis, db)
+    assert np.array_equal(tnp(pwt.values), vt)
+    assert np.array_equal(tnp(pwt.meta).view(np.uint8), mt)
+    assert np.array_equal(tnp(pwt.dense), dt)
+
+
+@pytest.mark.parametrize("axis,N,K,db", TILE_CASES)
+@pytest.mark.parametrize("M", [1, 7, 20, 64, 130])
+def test_tiled_gemm_equals_row_major(S, axis, N, K, db, M, monkeypatch):
+    """The tiled weight gives bit-for-bit the output of the row-major weight under the
+    same (row-split) plan, and stays inside the error bound against the oracle."""
+    W, mask, X, sw, sx = random_case(40 + N, M, N, K, axis, db, FP8)
+    pw, (v, m, d) = compress_both(S, W, mask, FP8, axis, db)
+    pwt = S.tile(pw)
+    monkeypatch.setenv("SPENSE_ROWS", "1")
+    for f32 in (True, False):
+        a = run_gemm(S, pw, X, sw, sx, f32)
+        b = run_gemm(S, pwt, X, sw, sx, f32)
+        assert np.array_equal(a, b)
+    Wd = oracle.decompress(v, m, d, N, K, FP8, axis, db)
+    assert_f32_bound(run_gemm(S, pwt, X, sw, sx, True), X, Wd, FP8, sw, sx)
+
+
+def test_tiled_exact_integers(S):
+    for axis, N, K, db in TILE_CASES:
+        W, mask, X, sw, sx = gen.make_exact_int(21, N, 37, N, K, gaxis(axis), db, gen.FP8)
+        pw, (v, m, d) = compress_both(S, W, mask, FP8, axis, db)
+        ref = oracle.spense_gemm(X, v, m, d, N, K, FP8, axis, db, sw, sx)
+        pwt = S.tile(pw)
+        assert np.array_equal(run_gemm(S, pwt, X, sw, sx, True), ref["y_f32"])
+        assert np.array_equal(run_gemm(S, pwt, X, sw, sx, False).view(np.uint16), ref["y_bf16"])
+
+
 # ------------------------------------------------------------------ full-size workloads
 @functools.lru_cache(maxsize=4)
 def _matrix(cfg, mat, name, N, K, axis, frac, dtype):
@@ -308,20 +378,24 @@ def _matrix(cfg, mat, name, N, K, axis, frac, dtype):
 
 
 def _full_case(S, cfg, mat, name, N, K, axis, frac, ms, xdist, sample_rows=384):
+    """Both storage layouts (row-major as compressed, and tiled) against the oracle on a
+    sample of weight rows (every activation row)."""
     mx = _matrix(cfg, mat, name, N, K, axis, frac, gen.FP8)
     ax = 0 if axis == gen.OUTPUT else 1
     say(f"[compress] cfg{cfg} {name} dense_begin={mx.dense_begin}")
     pw, (v, m, d) = compress_both(S, mx.W, mx.mask, FP8, ax, mx.dense_begin)
+    pwt = S.tile(pw)
     Wd = oracle.decompress(v, m, d, N, K, FP8, ax, mx.dense_begin)
     rows = np.sort(np.random.default_rng(cfg * 100 + mat).choice(N, size=min(N, sample_rows), replace=False))
     for M in ms:
         X, sx = gen.make_x(cfg, mat, M, K, gen.FP8, xdist)
-        say(f"[gemm] cfg{cfg} {name} M={M}")
-        y = run_gemm(S, pw, X, mx.sw, sx, False).view(np.uint16)
         ref = oracle.gemm(X, Wd[rows], FP8, mx.sw[rows], sx)
-        assert_bf16_close(y[:, rows], ref["y_bf16"], FP8)
-        y32 = run_gemm(S, pw, X, mx.sw, sx, True)
-        assert_f32_bound(y32[:, rows], X, Wd[rows], FP8, mx.sw[rows], sx)
+        for w, lay in ((pw, "row-major"), (pwt, "tiled")):
+            say(f"[gemm] cfg{cfg} {name} M={M} {lay}")
+            y = run_gemm(S, w, X, mx.sw, sx, False).view(np.uint16)
+            assert_bf16_close(y[:, rows], ref["y_bf16"], FP8)
+            y32 = run_gemm(S, w, X, mx.sw, sx, True)
+            assert_f32_bound(y32[:, rows], X, Wd[rows], FP8, mx.sw[rows], sx)
 
 
 def test_full_tiny_bf16_both_axes(S):
@@ -371,16 +445,13 @@ def test_full_size_exact_integers_whole_output(S, name, N, K, axis, M):
     W, mask, X, sw, sx = gen.make_exact_int(20, N % 97, M, N, K, axis, db, gen.FP8)
     say(f"[exact] {name} M={M}")
     pw, (v, m, d) = compress_both(S, W, mask, FP8, ax, db)
-    y32 = run_gemm(S, pw, X, sw, sx, True)
-    ybf = run_gemm(S, pw, X, sw, sx, False).view(np.uint16)
     Wd = oracle.decompress(v, m, d, N, K, FP8, ax, db)
-    if M > 256:  # the oracle on a sample of activation rows keeps this within seconds
-        sel = np.sort(np.random.default_rng(1).choice(M, 64, replace=False))
-        ref = oracle.gemm(X[sel], Wd, FP8, sw, sx[sel])
+    sel = np.arange(M) if M <= 256 else np.sort(np.random.default_rng(1).choice(M, 64, replace=False))
+    ref = oracle.gemm(X[sel], Wd, FP8, sw, sx[sel])  # a sample of activation rows past M = 256
+    for w in (pw, S.tile(pw)):
+        y32 = run_gemm(S, w, X, sw, sx, True)
+        ybf = run_gemm(S, w, X, sw, sx, False).view(np.uint16)
         assert np.array_equal(y32[sel], ref["y_f32"]) and np.array_equal(ybf[sel], ref["y_bf16"])
-    else:
-        ref = oracle.gemm(X, Wd, FP8, sw, sx)
-        assert np.array_equal(y32, ref["y_f32"]) and np.array_equal(ybf, ref["y_bf16"])
 
 
 @pytest.mark.parametrize("rows,rt,waves,wused", [(0, 1, 4, 0), (0, 2, 4, 0), (0, 1, 8, 0), (0, 2, 8, 0), (0, 1, 16, 0),
