@@ -5,14 +5,16 @@ One step = one spense_gemm call (2:4 smfmac region + dense mfma region + fused s
 epilogue, one kernel launch) over one batch of activations, on the Qwen3-32B-like MLP
 gate/up projection: W 25600 x 5120 fp8 e4m3, the trailing 25% of output rows dense
 (output-split), the rest magnitude-pruned 2:4, X 64 x 5120 fp8 with per-token scales,
-bf16 output.  Inputs are synthetic and already resident in HBM; the timed loop rotates
-over several copies of the packed weight so that no step is served from the 256 MB
-Infinity Cache.
+bf16 output.  The packed weight is in the tiled execution layout (spense_compress, then
+spense_tile: offline steps, timed separately).  Inputs are synthetic and already
+resident in HBM; the timed loop rotates over several copies of the packed weight so
+that no step is served from the 256 MB Infinity Cache.
 
 Printed JSON line: value = algorithmic bytes / time (GB/s) at M = 64; the M = 1/8/32/64
-sweep, the dense fp8 baseline built in the same library, the roofline of the dominant
-kernel (HIP events around a graph replay of exactly `steps` launches, on the launch
-stream) and the CPU oracle baseline are extra fields.
+sweep, the dense fp8 baseline built in the same library (the same weight with every row
+dense, same layout and kernel), the row-major-layout timings, the roofline of the
+dominant kernel (HIP events around a graph replay of exactly `steps` launches, on the
+launch stream) and the CPU oracle baseline are extra fields.
 
     python bench.py [--gpus 1] [--steps 500] [--warmup 50] [--skip-cpu]
 """
@@ -169,20 +171,27 @@ def main():
     Wd = torch.from_numpy(mx.W).cuda()
     maskd = torch.from_numpy(mx.mask).cuda()
     swd = torch.from_numpy(mx.sw).cuda()
-    # compress once (offline step), timed separately
+    # compress and tile once (offline steps), timed separately
     torch.cuda.synchronize()
     t = time.perf_counter()
-    pw0 = S.compress(Wd, maskd, S.SPENSE_SPLIT_OUTPUT, mx.dense_begin)
+    pw_rm = S.compress(Wd, maskd, S.SPENSE_SPLIT_OUTPUT, mx.dense_begin)
     torch.cuda.synchronize()
     compress_ms = (time.perf_counter() - t) * 1e3
+    t = time.perf_counter()
+    pw0 = S.tile(pw_rm)
+    torch.cuda.synchronize()
+    tile_ms = (time.perf_counter() - t) * 1e3
     wbytes = pw0.weight_bytes()
     copies = max(2, -(-2 * MALL_BYTES // wbytes))
-    pws = [pw0] + [S.PackedWeight(pw0.N, pw0.K, pw0.dtype, pw0.split, pw0.dense_begin, pw0.values.clone(),
-                                  pw0.meta.clone(), pw0.dense.clone()) for _ in range(copies - 1)]
-    dense_copies = max(2, -(-2 * MALL_BYTES // (N * K)))
-    dws = [Wd] + [Wd.clone() for _ in range(dense_copies - 1)]
+    pws = [pw0] + [pw0.clone() for _ in range(copies - 1)]
+    rms = [pw_rm] + [pw_rm.clone() for _ in range(copies - 1)]
+    # dense baseline: the same weight with every row dense, same layout and kernel
+    dw0 = S.tile(S.compress(Wd, None, S.SPENSE_SPLIT_OUTPUT, 0))
+    dense_copies = max(2, -(-2 * MALL_BYTES // dw0.weight_bytes()))
+    dws = [dw0] + [dw0.clone() for _ in range(dense_copies - 1)]
     n_sp, n_de = mx.dense_begin, N - mx.dense_begin
-    log(f"[bench] packed weight {wbytes / 1e6:.2f} MB x {copies} copies; dense {N * K / 1e6:.2f} MB x {dense_copies}")
+    log(f"[bench] packed weight {wbytes / 1e6:.2f} MB x {copies} copies; dense {dw0.weight_bytes() / 1e6:.2f} MB "
+        f"x {dense_copies}")
 
     results = {}
     ws = S.Workspace("cuda")
@@ -204,13 +213,18 @@ def main():
             Yd = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
 
             def run_de(i):
-                S.dense_gemm(Xd, dws[i % dense_copies], swd, sxd, out=Yd, workspace=ws)
+                S.gemm(Xd, dws[i % dense_copies], swd, sxd, out=Yd, workspace=ws)
 
             dstep_ms = time_launches(run_de, args.steps, args.warmup, torch)
             res["dense_us_per_step"] = round(dstep_ms * 1e3, 3)
             res["dense_gbs"] = round(alg_bytes_dense(M, N, K) / (dstep_ms * 1e-3) / 1e9, 1)
             res["speedup_vs_dense"] = round(dstep_ms / step_ms, 4)
             res["byte_ratio_bound"] = round(alg_bytes_dense(M, N, K) / b, 4)
+
+            def run_rm(i):
+                S.gemm(Xd, rms[i % copies], swd, sxd, out=Y, workspace=ws)
+
+            res["rowmajor_us_per_step"] = round(time_launches(run_rm, args.steps, args.warmup, torch) * 1e3, 3)
         results[M] = res
         log(f"[bench] M={M}: {res}")
 
@@ -238,15 +252,16 @@ def main():
         "config": {"workload": "qwen3-32b-like MLP gate/up 25600x5120 fp8 e4m3, trailing 25% rows dense "
                                "(output-split), rest 2:4, decode batch M=64, bf16 out",
                    "N": N, "K": K, "M": M_MAIN, "split": "output", "dense_fraction": DENSE_FRAC,
-                   "weight_copies_rotated": copies},
+                   "layout": "tiled", "weight_copies_rotated": copies},
         "us_per_gemm": main_res["us_per_step"],
         "pct_hbm_peak": round(100 * ach / HBM_PEAK_GBS, 2),
         "speedup_vs_dense": main_res.get("speedup_vs_dense"),
         "compress_ms": round(compress_ms, 3),
+        "tile_ms": round(tile_ms, 3),
         "roofline": {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": traffic,
-                     "kernel": "spense_gemm_rows_kernel (fp8; 2:4 smfmac + dense mfma, activations staged "
-                               "in LDS, one launch)"},
+                     "kernel": "spense_gemm_rows_kernel (fp8, tiled layout; 2:4 smfmac + dense mfma, "
+                               "activations staged in LDS, one launch)"},
         "sweep": [results[m] for m in ms_list],
     }
     if not args.skip_cpu:
