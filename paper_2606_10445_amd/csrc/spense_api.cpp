@@ -212,7 +212,9 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
   const int es = esize(dtype);
   const int64_t gran = dtype == SPENSE_FP8_E4M3FN ? 128 : 64;  // K per 2:4 instruction
   const double sparse_cost = 0.5 * es + 0.125;                 // bytes per logical 2:4 entry
-  const int ct = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
+  int ct = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
+  const int ect = env_int("SPENSE_CT", 0);  // testing knob: at most this many activation tiles
+  if (ect == 1 || ect == 2) ct = std::min(ct, ect);
   pl->ls.ct = ct;
   pl->ls.mblocks = (int)ceil_div(M, 16 * ct);
 

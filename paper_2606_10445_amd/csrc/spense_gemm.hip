@@ -47,8 +47,10 @@ typedef __bf16 v16bf __attribute__((ext_vector_type(16)));
 
 constexpr uint32_t kOOB = 0x80000000u;  // any offset past every buffer extent
 // Cache policy of the weight loads.  Measured on MI355X: for rows read as 16 x 64-byte
-// segments per instruction the default policy streams ~15% faster than non-temporal.
+// segments per instruction the default policy streams ~15% faster than non-temporal;
+// for the tiled layout (1 KB contiguous per instruction) non-temporal is 5-9% faster.
 constexpr int kNT = 0;
+constexpr int kTiledNT = 2;
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* p, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
@@ -568,10 +570,10 @@ __device__ __forceinline__ void load_chunk_tiled(WChunk& W, bool sparse, bool ok
   const int s0 = sparse ? cs * 4096 : cd * 8192, sj = sparse ? 1024 : 2048;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    W.w[j] = bl16<kNT>(rw, base, s0 + sj * j);
-    W.w[4 + j] = bl16<kNT>(rd, dbase, cd * 8192 + 2048 * j + 1024);
+    W.w[j] = bl16<kTiledNT>(rw, base, s0 + sj * j);
+    W.w[4 + j] = bl16<kTiledNT>(rd, dbase, cd * 8192 + 2048 * j + 1024);
   }
-  const v4i w = bl16<kNT>(rm, sel(ok && sparse, mt), cs * 1024);
+  const v4i w = bl16<kTiledNT>(rm, sel(ok && sparse, mt), cs * 1024);
 #pragma unroll
   for (int j = 0; j < 4; ++j) W.ix[j] = w[j];
 }
