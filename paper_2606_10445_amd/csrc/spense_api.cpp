@@ -170,11 +170,11 @@ constexpr int kCUs = 256;  // compute units of an MI355X
 // quarter of the activation bytes it stages from L2; the cheapest assignment wins, ties
 // going to fewer workgroups.
 void choose_rows_per_group(spense::Region* regs, int nreg, int rt, int waves, int ct, int mblocks, int64_t K, int es,
-                           double sparse_cost) {
+                           double sparse_cost, int ksplit) {
   double tile_b[2];
   for (int i = 0; i < nreg; ++i)
-    tile_b[i] = 16.0 * rt * (sparse_cost * regs[i].kbound + (double)es * (K - regs[i].kbound));
-  const double x_cost = 0.25 * 16.0 * ct * K * es;
+    tile_b[i] = 16.0 * rt * (sparse_cost * regs[i].kbound + (double)es * (K - regs[i].kbound)) / ksplit;
+  const double x_cost = 0.25 * 16.0 * ct * K * es / ksplit;
   double best = 0;
   int64_t best_wg = 0;
   int bw[2] = {waves, waves};
@@ -184,7 +184,7 @@ void choose_rows_per_group(spense::Region* regs, int nreg, int rt, int waves, in
       int64_t wg = 0;
       double big = 0;
       for (int i = 0; i < nreg; ++i) {
-        wg += ceil_div(regs[i].rows, 16 * rt * wu[i]) * mblocks;
+        wg += ceil_div(regs[i].rows, 16 * rt * wu[i]) * mblocks * ksplit;
         big = std::max(big, wu[i] * tile_b[i]);
       }
       const double t = (double)ceil_div(wg, kCUs) * (big + x_cost);
@@ -198,8 +198,46 @@ void choose_rows_per_group(spense::Region* regs, int nreg, int rt, int waves, in
   const int ew = env_int("SPENSE_WUSED", 0);
   for (int i = 0; i < nreg; ++i) {
     regs[i].wused = ew > 0 ? std::min(ew, waves) : bw[i];
-    regs[i].nrb = (int32_t)ceil_div(regs[i].rows, 16 * rt * regs[i].wused);
+    regs[i].nrb = (int32_t)(ceil_div(regs[i].rows, 16 * rt * regs[i].wused) * ksplit);
   }
+}
+
+// Row-split kernel: number of K slices.  Slicing K multiplies the waves of a weight with
+// few 16-row tiles, at the price of an fp32 partial-sum pass.  Measured on the q / k / o /
+// down shapes (tiled fp8): it pays only for one block of 17-64 tokens (one activation
+// tile streams fast enough without it; several blocks already multiply the workgroups),
+// on weights with fewer than 1024 tiles, and when each slice keeps enough chunks: down
+// (320 tiles, 50 chunks) gains up to 1.5x with 4 slices, k/v (64 tiles, 10 chunks) ~1.2x
+// with 3, q and o (10 and 16 chunks) lose.
+int choose_ksplit(const spense::Region* regs, int nreg, int ct, int mblocks, int64_t chunks) {
+  int64_t tiles = 0;
+  for (int i = 0; i < nreg; ++i) tiles += ceil_div(regs[i].rows, 16);
+  int S = 1;
+  if (ct > 1 && mblocks == 1 && tiles < 1024) {
+    const int64_t min_chunks = tiles >= 256 ? 12 : 3;
+    S = (int)std::max<int64_t>(1, std::min<int64_t>({4, ceil_div(1024, std::max<int64_t>(tiles, 1)), chunks / min_chunks}));
+  }
+  const int e = env_int("SPENSE_KSPLIT", 0);
+  if (e >= 1 && e <= 8) S = (int)std::max<int64_t>(1, std::min<int64_t>(e, chunks));
+  return S;
+}
+
+// Chunk boundaries of S slices of a row-split region with equal byte cost (2:4 chunks
+// cost sparse_cost bytes per logical column, dense chunks es).
+void slice_cuts(spense::Region& r, int S, int64_t kc, int es, double sparse_cost) {
+  const int64_t n_sp = ceil_div(r.kbound, kc), n_de = ceil_div(r.kend - r.kbound, kc);
+  const int64_t nch = n_sp + n_de;
+  const double cs = sparse_cost * n_sp, total = cs + (double)es * n_de;
+  r.cut[0] = 0;
+  for (int s = 1; s < S; ++s) {
+    const double c = total * s / S;
+    const double k = c <= cs ? c / sparse_cost : n_sp + (c - cs) / es;
+    int64_t cut = std::llround(k);
+    cut = std::max<int64_t>(r.cut[s - 1] + 1, std::min<int64_t>(cut, nch - (S - s)));
+    r.cut[s] = (int32_t)cut;
+  }
+  r.cut[S] = (int32_t)nch;
+  r.ksplit = S;
 }
 
 // The plan depends only on the dtype, M and the weight geometry, so equal geometry gets
@@ -272,6 +310,7 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
     r.dense_col_off = (int32_t)dco;
     r.kend = (int32_t)K;
     r.wused = waves;
+    r.ksplit = 1;
     r.nrb = (int32_t)ceil_div(rows, 16 * rt);
     // cut [0, K) into `waves` parts of equal byte cost, on multiples of the instruction K
     const double cs = sparse_cost * kbound, total = cs + es * (double)(K - kbound);
@@ -294,7 +333,16 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
   } else if (N > 0) {
     add(0, N, dense_begin, 0, dense_begin);
   }
-  if (rows_mode) choose_rows_per_group(regs, nreg, rt, waves, pl->ls.ct, pl->ls.mblocks, K, es, sparse_cost);
+  int ksplit = 1;
+  if (rows_mode) {
+    // chunks of 4 instruction steps: 512 logical columns (fp8), 256 (bf16)
+    const int64_t kc = dtype == SPENSE_FP8_E4M3FN ? 512 : 256;
+    int64_t chunks = 0;
+    for (int i = 0; i < nreg; ++i) chunks = std::max(chunks, ceil_div(regs[i].kbound, kc) + ceil_div(K - regs[i].kbound, kc));
+    ksplit = chunks > 0 ? choose_ksplit(regs, nreg, pl->ls.ct, pl->ls.mblocks, chunks) : 1;
+    for (int i = 0; i < nreg; ++i) slice_cuts(regs[i], ksplit, kc, es, sparse_cost);
+    choose_rows_per_group(regs, nreg, rt, waves, pl->ls.ct, pl->ls.mblocks, K, es, sparse_cost, ksplit);
+  }
   spense::GemmArgs& a = pl->args;
   a.nreg = nreg;
   int32_t groups = 0;
@@ -305,7 +353,8 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
   }
   a.groups = groups;
   a.tiled = tiled ? 1 : 0;
-  pl->ws_bytes = 0;
+  // K-sliced regions keep fp32 partial sums: slices x M x N floats
+  pl->ws_bytes = ksplit > 1 ? (size_t)ksplit * (size_t)M * (size_t)N * sizeof(float) : 0;
 }
 
 int gemm_common(const void* X, int64_t M, int64_t ldx, int32_t dtype, int32_t split, int64_t N, int64_t K,
@@ -381,7 +430,9 @@ int gemm_common(const void* X, int64_t M, int64_t ldx, int32_t dtype, int32_t sp
   a.m_bytes = (uint32_t)mb;
   a.d_bytes = (uint32_t)db;
   if (a.groups == 0) return ok();
+  a.part = static_cast<float*>(ws);
   hipError_t e = spense::launch_gemm(dtype, pl.ls, a, stream);
+  if (e == hipSuccess && pl.ws_bytes > 0) e = spense::launch_splitk_reduce(a, stream);
   if (e != hipSuccess) return fail(SPENSE_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();
 }

@@ -687,7 +687,9 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
   const int ri = (a.nreg > 1 && g >= a.reg[1].wg0) ? 1 : 0;
   const Region& R = a.reg[ri];
   const int rowend = R.row0 + R.rows;
-  const int nbase = R.row0 + ((g - R.wg0) * R.wused + wave) * 16;
+  // workgroups of a region: (row group, K slice), slices of one row group adjacent
+  const int slice = (g - R.wg0) % R.ksplit, rgroup = (g - R.wg0) / R.ksplit;
+  const int nbase = R.row0 + (rgroup * R.wused + wave) * 16;
   const int m0 = mb * 16 * CT;
   const int K = R.kend;
   const int kbound = R.kbound;
@@ -706,10 +708,11 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
   const uint32_t mrow = (uint32_t)((int64_t)n * a.m_ld_b) + (DT == kFP8 ? 4u * lq : 4u * (lq >> 1));
   const uint32_t drow = (uint32_t)((int64_t)max(n - R.dense_row_off, 0) * a.d_ld_b) + 16u * lq;
 
-  // chunk list: 2:4 chunks start at 0 and cover [0, kbound); dense chunks start at kbound
+  // chunk list: 2:4 chunks start at 0 and cover [0, kbound); dense chunks start at kbound;
+  // this workgroup's K slice is chunks [c_lo, c_hi)
   const int n_sp = (kbound + KC - 1) / KC;
   const int n_de = (K - kbound + KC - 1) / KC;
-  const int nch = n_sp + n_de;
+  const int c_lo = R.cut[slice], c_hi = R.cut[slice + 1];
   auto chunk_k = [&](int c) { return c < n_sp ? c * KC : kbound + (c - n_sp) * KC; };
   auto chunk_end = [&](int c) { return c < n_sp ? kbound : K; };
   // tiled layout: offsets of this lane in its tile's first chunk of each part
@@ -722,13 +725,13 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
   }
   auto load = [&](WChunk& W, int c) {
     if constexpr (TL)
-      load_chunk_tiled(W, c < n_sp, active && c < nch, c, max(c - n_sp, 0), vt, mt, dt, rv, rm, rd);
+      load_chunk_tiled(W, c < n_sp, active && c < c_hi, c, max(c - n_sp, 0), vt, mt, dt, rv, rm, rd);
     else
-      load_chunk<DT, WM>(W, c < n_sp, active && c < nch, chunk_k(c), chunk_end(c), lq, vrow, mrow, drow,
+      load_chunk<DT, WM>(W, c < n_sp, active && c < c_hi, chunk_k(c), chunk_end(c), lq, vrow, mrow, drow,
                          R.dense_col_off, rv, rm, rd);
   };
   auto xload = [&](int buf, int c) {
-    x_to_lds<DT, CT, XI>(xbuf[buf], a, rx, m0, chunk_k(c), c < nch ? chunk_end(c) : -1, wave, lane);
+    x_to_lds<DT, CT, XI>(xbuf[buf], a, rx, m0, chunk_k(c), c < c_hi ? chunk_end(c) : -1, wave, lane);
   };
 
   // A wave that owns rows loads weights and runs the MMAs; the others only stage
@@ -742,8 +745,8 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
     WChunk slot[NS];
 #pragma unroll
     for (int d = 0; d < D; ++d) {
-      xload(d, d);
-      if constexpr (ACT) load(slot[d], d);
+      xload(d, c_lo + d);
+      if constexpr (ACT) load(slot[d], c_lo + d);
     }
     barrier_vm<0>();
     auto step = [&](auto s_const, int c) {
@@ -759,17 +762,17 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
       }
       barrier_vm<AFTER>();
     };
-    int c = 0;
-    for (; c + NS <= nch; c += NS) {
+    int c = c_lo;
+    for (; c + NS <= c_hi; c += NS) {
       step(std::integral_constant<int, 0>(), c);
       step(std::integral_constant<int, 1>(), c + 1);
       step(std::integral_constant<int, 2>(), c + 2);
       if constexpr (NS == 4) step(std::integral_constant<int, 3 % NS>(), c + 3);
     }
-    if (c < nch) step(std::integral_constant<int, 0>(), c);
-    if (c + 1 < nch) step(std::integral_constant<int, 1>(), c + 1);
+    if (c < c_hi) step(std::integral_constant<int, 0>(), c);
+    if (c + 1 < c_hi) step(std::integral_constant<int, 1>(), c + 1);
     if constexpr (NS == 4)
-      if (c + 2 < nch) step(std::integral_constant<int, 2>(), c + 2);
+      if (c + 2 < c_hi) step(std::integral_constant<int, 2>(), c + 2);
   };
   if (active)
     run(std::true_type());
@@ -782,7 +785,36 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
   for (int cc = 0; cc < CT; ++cc) {
     const int m = m0 + 16 * cc + li;
     const int n0 = nbase + 4 * lq;
-    if (m < a.M && n0 < rowend) store4(a, acc[cc], m, n0, rowend);
+    if (m >= a.M || n0 >= rowend) continue;
+    if (R.ksplit == 1) {
+      store4(a, acc[cc], m, n0, rowend);
+    } else {  // unscaled fp32 partial of this K slice
+      float* pp = a.part + ((int64_t)slice * a.M + m) * a.N + n0;
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        if (n0 + r < rowend) pp[r] = acc[cc][r];
+    }
+  }
+}
+
+// Y rows of the K-sliced regions: sum of the slices' fp32 partials in slice order, then
+// the epilogue of store4 ((sum * w_scale[n]) * x_scale[m], bf16 or fp32).  One thread per
+// output element.
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a) {
+  const int64_t total = (int64_t)a.M * a.N;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += stride) {
+    const int m = (int)(e / a.N), n = (int)(e - (int64_t)m * a.N);
+    const Region& R = (a.nreg > 1 && n >= a.reg[1].row0 && n < a.reg[1].row0 + a.reg[1].rows) ? a.reg[1] : a.reg[0];
+    if (R.ksplit == 1 || n < R.row0 || n >= R.row0 + R.rows) continue;
+    float v = a.part[(int64_t)m * a.N + n];
+    for (int sl = 1; sl < R.ksplit; ++sl) v += a.part[((int64_t)sl * a.M + m) * a.N + n];
+    if (a.sw) v = v * a.sw[n];
+    v = v * (a.sx ? a.sx[m] : 1.0f);
+    if (a.out_f32)
+      reinterpret_cast<float*>(a.Y)[(int64_t)m * a.ldy + n] = v;
+    else
+      reinterpret_cast<uint16_t*>(a.Y)[(int64_t)m * a.ldy + n] = (uint16_t)bf16_bits(v);
   }
 }
 
@@ -867,6 +899,14 @@ hipError_t launch_dt(const LaunchShape& ls, const GemmArgs& a, hipStream_t s) {
 }
 
 }  // namespace
+
+hipError_t launch_splitk_reduce(const GemmArgs& a, hipStream_t s) {
+  const int64_t total = (int64_t)a.M * a.N;
+  int64_t g = (total + 255) / 256;
+  if (g > 4096) g = 4096;
+  hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)(g < 1 ? 1 : g)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
 
 hipError_t launch_gemm(int dtype, const LaunchShape& ls, const GemmArgs& a, hipStream_t s) {
   return dtype == kFP8 ? launch_dt<kFP8>(ls, a, s) : launch_dt<kBF16>(ls, a, s);

@@ -17,8 +17,10 @@ constexpr int kMaxWaves = 16;
 // one region; its waves split K at cut[0..waves] (cost-balanced), each wave running the
 // 2:4 loop over its part below kbound and the dense loop over the rest into one fp32
 // accumulator; the waves' partial sums are added in LDS in wave order.  The row-split
-// kernel instead gives each of the first `wused` waves of a workgroup 16*RT rows over all
-// of K (fewer rows per workgroup where rows carry more bytes, to balance the CUs).
+// kernel instead gives each of the first `wused` waves of a workgroup 16 rows over a
+// slice of K (fewer rows per workgroup where rows carry more bytes, to balance the CUs;
+// several slices where the weight has too few rows to fill the CUs, their fp32 partial
+// sums added afterwards in slice order by splitk_reduce).
 struct Region {
   int32_t row0, rows;          // output rows [row0, row0 + rows)
   int32_t kbound;              // first dense column (K for all-2:4, 0 for all-dense)
@@ -28,7 +30,9 @@ struct Region {
   int32_t nrb;                 // row groups (workgroups per activation block)
   int32_t wg0;                 // first workgroup of this region
   int32_t wused;               // row-split kernel: waves of a workgroup that own rows here
-  int32_t cut[kMaxWaves + 1];  // K boundaries of the waves' parts
+  int32_t ksplit;              // row-split kernel: K slices (1 = none); >1 writes fp32 partials
+  int32_t cut[kMaxWaves + 1];  // K-split kernel: K boundaries of the waves' parts;
+                               // row-split kernel: chunk boundaries of the K slices
 };
 
 struct GemmArgs {
@@ -51,6 +55,7 @@ struct GemmArgs {
   int32_t nreg;
   int32_t groups;
   int32_t tiled;  // weight buffers in the tiled execution layout (fp8, row-split kernel)
+  float* part;    // fp32 partial sums of K-sliced regions: part[(slice * M + m) * N + n]
   Region reg[2];
 };
 
@@ -64,6 +69,10 @@ struct LaunchShape {
 };
 
 hipError_t launch_gemm(int dtype, const LaunchShape& ls, const GemmArgs& a, hipStream_t s);
+
+// Y for the rows of K-sliced regions: the sum of their fp32 partials in slice order, then
+// the epilogue (after launch_gemm, on the same stream).
+hipError_t launch_splitk_reduce(const GemmArgs& a, hipStream_t s);
 
 hipError_t launch_compress(int dtype, const uint8_t* W, int64_t ldw_b, const uint8_t* mask, int64_t ldm,
                            int64_t s_rows, int64_t s_cols, uint8_t* values, int64_t v_ld_b, uint32_t* meta,

@@ -174,3 +174,18 @@ def test_tiled_descriptor_validation(S):
     assert S.spense_tile(src, overlap, None) == S.SPENSE_ERR_ARG
     # compress and decompress work on the row-major layout only
     assert S.spense_decompress(dst, 4096, 128, None) == S.SPENSE_ERR_ARG
+
+
+def test_k_slices_need_a_workspace(S):
+    """Weights with few rows (down: 5120 x 25600) are sliced along K at decode M; the
+    partial sums need slices x M x N floats of workspace, checked before any device call."""
+    L = S.spense_layout(5120, 25600, 1, 1, 19200)
+    pk = S.spense_packed_t(1, 1, 5120, 25600, 19200, 4096, L.values_ld, 8192, L.meta_ld, 16384, L.dense_ld)
+    need = S.spense_gemm_workspace_size(64, pk)
+    assert need > 0 and need % (64 * 5120 * 4) == 0 and need // (64 * 5120 * 4) <= 8
+    assert S.spense_gemm(4096, 64, 25600, pk, None, None, 4096, 5120, 0, None, 0, None) == S.SPENSE_ERR_WS
+    assert S.spense_gemm(4096, 64, 25600, pk, None, None, 4096, 5120, 0, 4096, need - 4, None) == S.SPENSE_ERR_WS
+    # a weight with many rows (gate/up) is not sliced
+    Lg = S.spense_layout(25600, 5120, 1, 0, 19200)
+    pg = S.spense_packed_t(1, 0, 25600, 5120, 19200, 4096, Lg.values_ld, 8192, Lg.meta_ld, 16384, Lg.dense_ld)
+    assert all(S.spense_gemm_workspace_size(m, pg) == 0 for m in (1, 8, 32, 64))

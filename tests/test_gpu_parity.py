@@ -231,7 +231,9 @@ def test_repeated_calls_are_bitwise_identical(S):
 KERNEL_SHAPES = [dict(), dict(SPENSE_WAVES="4", SPENSE_RT="1"), dict(SPENSE_WAVES="16", SPENSE_RT="1"),
                  dict(SPENSE_WAVES="8", SPENSE_RT="2"), dict(SPENSE_WAVES="8", SPENSE_RT="1", SPENSE_U8="1"),
                  dict(SPENSE_ROWS="1", SPENSE_WAVES="4", SPENSE_RT="1"),
-                 dict(SPENSE_ROWS="1", SPENSE_WAVES="8", SPENSE_RT="1")]
+                 dict(SPENSE_ROWS="1", SPENSE_WAVES="8", SPENSE_RT="1"),
+                 dict(SPENSE_ROWS="1", SPENSE_WAVES="8", SPENSE_RT="1", SPENSE_KSPLIT="4"),
+                 dict(SPENSE_ROWS="1", SPENSE_WAVES="4", SPENSE_RT="1", SPENSE_KSPLIT="7")]
 
 
 @pytest.mark.parametrize("axis,db", [(1, 6144), (0, 1536)])
@@ -247,7 +249,7 @@ def test_every_kernel_shape_is_repeatable_and_within_bound(S, dtype, axis, db, m
     pw, (v, m, d) = compress_both(S, W, mask, dtype, axis, db)
     Wd = oracle.decompress(v, m, d, N, K, dtype, axis, db)
     for cfg in KERNEL_SHAPES:
-        for k in ("SPENSE_WAVES", "SPENSE_RT", "SPENSE_U8", "SPENSE_ROWS"):
+        for k in ("SPENSE_WAVES", "SPENSE_RT", "SPENSE_U8", "SPENSE_ROWS", "SPENSE_KSPLIT"):
             monkeypatch.delenv(k, raising=False)
         for k, val in cfg.items():
             monkeypatch.setenv(k, val)
@@ -454,18 +456,21 @@ def test_full_size_exact_integers_whole_output(S, name, N, K, axis, M):
         assert np.array_equal(y32[sel], ref["y_f32"]) and np.array_equal(ybf[sel], ref["y_bf16"])
 
 
-@pytest.mark.parametrize("rows,rt,waves,wused", [(0, 1, 4, 0), (0, 2, 4, 0), (0, 1, 8, 0), (0, 2, 8, 0), (0, 1, 16, 0),
-                                                 (0, 4, 4, 0), (1, 1, 4, 0), (1, 1, 8, 0), (1, 1, 4, 3), (1, 1, 8, 5),
-                                                 (1, 1, 8, 8)])
+@pytest.mark.parametrize("rows,rt,waves,wused,ks", [(0, 1, 4, 0, 0), (0, 2, 4, 0, 0), (0, 1, 8, 0, 0), (0, 2, 8, 0, 0),
+                                                    (0, 1, 16, 0, 0), (0, 4, 4, 0, 0), (1, 1, 4, 0, 1), (1, 1, 8, 0, 1),
+                                                    (1, 1, 4, 3, 1), (1, 1, 8, 5, 1), (1, 1, 8, 8, 1), (1, 1, 4, 0, 2),
+                                                    (1, 1, 8, 3, 3), (1, 1, 8, 8, 2)])
 @pytest.mark.parametrize("dtype,axis,M", [(FP8, 1, 3), (FP8, 0, 40), (BF16, 1, 20), (FP8, 1, 64), (BF16, 0, 17)])
-def test_every_workgroup_shape_is_exact(S, rows, rt, waves, wused, dtype, axis, M, monkeypatch):
+def test_every_workgroup_shape_is_exact(S, rows, rt, waves, wused, ks, dtype, axis, M, monkeypatch):
     """All built kernels and (row tiles, waves) shapes - K split across the waves of a
-    workgroup, or rows split with activations staged in LDS and `wused` of the waves
-    owning rows - give bit-exact results on exact-integer data."""
+    workgroup, or rows split with activations staged in LDS, `wused` of the waves owning
+    rows and K cut into `ks` slices whose partial sums are added afterwards - give
+    bit-exact results on exact-integer data."""
     monkeypatch.setenv("SPENSE_ROWS", str(rows))
     monkeypatch.setenv("SPENSE_RT", str(rt))
     monkeypatch.setenv("SPENSE_WAVES", str(waves))
     monkeypatch.setenv("SPENSE_WUSED", str(wused))
+    monkeypatch.setenv("SPENSE_KSPLIT", str(ks))
     N, K = 200, 1056
     db = 800 if axis == 1 else 72
     W, mask, X, sw, sx = gen.make_exact_int(12, rt * 10 + waves, M, N, K, gaxis(axis), db, gdt(dtype))
