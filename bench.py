@@ -31,6 +31,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, AMD datasheet
+FP8_PEAK_TFLOPS = 5033.2  # MI355X dense fp8 matrix peak: 256 CUs x 2.4 GHz x 8192 flop/clk
 N, K, DENSE_FRAC = 25600, 5120, 0.25
 M_SWEEP = [1, 8, 32, 64]
 M_MAIN = 64
@@ -52,6 +53,11 @@ def alg_bytes_spense(M, N, K, n_sparse_rows, n_dense_rows):
 
 def alg_bytes_dense(M, N, K):
     return N * K + M * K + 4 * (M + N) + 2 * M * N
+
+
+def alg_flops_spense(M, n_sparse_elems, n_dense_elems):
+    """Only the stored non-zeros count: 2 M (dense + sparse / 2)."""
+    return 2.0 * M * (n_dense_elems + n_sparse_elems / 2)
 
 
 def kernel_source_sha():
@@ -131,6 +137,72 @@ def cpu_baseline(mx, Wcodes_dense, X, sx, M):
             "sample": sample, "seconds_per_gemm": round(full_s, 4)}
 
 
+def measure_extras(args, torch, gen, S, ws, pws, copies, swd, mx, dws, dense_copies, results):
+    """Extra fields: %peak against a measured copy bandwidth, per-launch (eager) timing of
+    the main GEMM, MFMA utilisation at M = 2048 and the Qwen3-32B-like decoder-layer set
+    (q, k, v, o, gate, up, down at M = 64, seven GEMMs back to back, x64 layers)."""
+    ex = {}
+    # device copy bandwidth (read + write) of 256 MiB, as a measured ceiling
+    n = 256 << 20
+    x = torch.ones(n, dtype=torch.uint8, device="cuda")
+    y = torch.empty_like(x)
+    cms = time_launches(lambda i: torch.mul(x, 1, out=y), 50, 5, torch)
+    copy_gbs = 2 * n / (cms * 1e-3) / 1e9
+    del x, y
+    main = results[M_MAIN]
+    ex["copy_gbs"] = round(copy_gbs, 1)
+    ex["pct_copy_bw"] = round(100 * main["gbs"] / copy_gbs, 1)
+    # eager per-launch timing of the main GEMM
+    global EAGER
+    X, sx = gen.make_x(2, 0, M_MAIN, K, gen.FP8, "normal")
+    Xd, sxd = torch.from_numpy(X).cuda(), torch.from_numpy(sx).cuda()
+    Y = torch.empty((M_MAIN, N), dtype=torch.bfloat16, device="cuda")
+    EAGER, prev = True, EAGER
+    ex["us_per_gemm_eager"] = round(time_launches(lambda i: S.gemm(Xd, pws[i % copies], swd, sxd, out=Y, workspace=ws),
+                                                  200, 20, torch) * 1e3, 3)
+    EAGER = prev
+    # compute-bound point: M = 2048 on the same weight
+    Mb = 2048
+    Xb, sxb = gen.make_x(2, 0, Mb, K, gen.FP8, "normal")
+    Xbd, sxbd = torch.from_numpy(Xb).cuda(), torch.from_numpy(sxb).cuda()
+    Yb = torch.empty((Mb, N), dtype=torch.bfloat16, device="cuda")
+    bms = time_launches(lambda i: S.gemm(Xbd, pws[i % copies], swd, sxbd, out=Yb, workspace=ws), 20, 3, torch)
+    fl = alg_flops_spense(Mb, mx.dense_begin * K, (N - mx.dense_begin) * K)
+    dms = time_launches(lambda i: S.gemm(Xbd, dws[i % dense_copies], swd, sxbd, out=Yb, workspace=ws), 20, 3, torch)
+    ex["m2048"] = {"us_per_gemm": round(bms * 1e3, 1), "tflops": round(fl / (bms * 1e-3) / 1e12, 1),
+                   "mfma_util": round(fl / (bms * 1e-3) / 1e12 / FP8_PEAK_TFLOPS, 4),
+                   "dense_us_per_gemm": round(dms * 1e3, 1), "speedup_vs_dense": round(dms / bms, 3)}
+    del Xbd, Yb
+    # decoder-layer set at M = 64 (each matrix its own seeded draw), tiled, with the dense
+    # layer (every row dense) for comparison; weights rotated over two copies of the set
+    Ml = 64
+    layer = [(name, n_, k_, ax) for (name, n_, k_, ax) in gen.QWEN3_32B_LAYER]
+    sets, dsets, io = [], [], []
+    for i, (name, n_, k_, ax) in enumerate(layer):
+        m = gen.make_matrix(4, i, name, n_, k_, ax, DENSE_FRAC, gen.FP8)
+        Wt = torch.from_numpy(m.W).cuda()
+        p = S.tile(S.compress(Wt, torch.from_numpy(m.mask).cuda(), 0 if ax == gen.OUTPUT else 1, m.dense_begin))
+        dp = S.tile(S.compress(Wt, None, S.SPENSE_SPLIT_OUTPUT, 0))
+        del Wt
+        sets.append([p, p.clone()])
+        dsets.append([dp, dp.clone()])
+        Xl, sxl = gen.make_x(4, i, Ml, k_, gen.FP8, "normal")
+        io.append((torch.from_numpy(Xl).cuda(), torch.from_numpy(sxl).cuda(), torch.from_numpy(m.sw).cuda(),
+                   torch.empty((Ml, n_), dtype=torch.bfloat16, device="cuda")))
+
+    def run_layer(ws_sets):
+        def f(i):
+            for (Xd_, sx_, sw_, Y_), ps in zip(io, ws_sets):
+                S.gemm(Xd_, ps[i % 2], sw_, sx_, out=Y_, workspace=ws)
+        return f
+
+    lms = time_launches(run_layer(sets), 100, 10, torch)
+    dlms = time_launches(run_layer(dsets), 100, 10, torch)
+    ex["qwen3_layer_m64"] = {"us_per_layer": round(lms * 1e3, 1), "ms_per_64_layers": round(lms * 64, 3),
+                             "dense_us_per_layer": round(dlms * 1e3, 1), "speedup_vs_dense": round(dlms / lms, 3)}
+    return ex
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -141,6 +213,8 @@ def main():
     ap.add_argument("--eager", action="store_true", help="launch steps one by one instead of one graph")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MiB",
                     help="run only a torch device copy of this size (rocprof counter calibration)")
+    ap.add_argument("--skip-extras", action="store_true",
+                    help="omit the layer-set, M=2048 and copy-bandwidth measurements")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -228,6 +302,10 @@ def main():
         results[M] = res
         log(f"[bench] M={M}: {res}")
 
+    extras = {}
+    if not args.only_main and not args.skip_extras:
+        extras = measure_extras(args, torch, gen, S, ws, pws, copies, swd, mx, dws, dense_copies, results)
+
     main_res = results[M_MAIN]
     traffic = None
     if os.path.exists(TRAFFIC_FILE):
@@ -264,6 +342,7 @@ def main():
                                "activations staged in LDS, one launch)"},
         "sweep": [results[m] for m in ms_list],
     }
+    out.update(extras)
     if not args.skip_cpu:
         X, sx = gen.make_x(2, 0, M_MAIN, K, gen.FP8, "normal")
         import oracle
