@@ -274,12 +274,14 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
   // prefetched two chunks ahead) measured faster than K-split on the q/k/o/gate/down
   // shapes at every M > 16, and at M <= 16 whenever there are at least as many 16-row
   // tiles as CUs; with fewer rows the K split gives the single activation tile more
-  // parallelism.  Eight waves for several activation tiles, four for one.
-  // (only the row-split kernel reads the tiled layout)
+  // parallelism (only the row-split kernel reads the tiled layout).  Eight waves per
+  // workgroup: with warmed weights and interleaved repeats they measured as fast as four
+  // for one activation tile and up to 1.6x faster for several (q/k/o/gate/down); two row
+  // tiles per wave won only on q at M = 256.
   int rows_mode = (tiled || ct > 1 || ceil_div(N, 16) * pl->ls.mblocks >= kCUs) ? 1 : 0;
   if (rows_mode) {
     rt = 1;
-    waves = ct > 1 ? 8 : 4;
+    waves = 8;
   }
   const int erows = env_int("SPENSE_ROWS", -1);
   if (erows >= 0 && !tiled) rows_mode = erows ? 1 : 0;
@@ -289,7 +291,7 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
       rt = ert;
       waves = ew;
     }
-  if (rows_mode && !(rt == 1 && (waves == 4 || waves == 8))) {
+  if (rows_mode && !((rt == 1 && (waves == 4 || waves == 8)) || (rt == 2 && waves == 4))) {
     rt = 1;
     waves = 4;
   }

@@ -600,13 +600,15 @@ __device__ __forceinline__ void meta_words(int (&ix)[4], const WChunk& W) {
 
 // MMAs of one chunk.  The B fragments of P steps are read from LDS before their MMAs,
 // so the LDS latency is paid once per group rather than once per step.
-template <int DT, int CT, bool WM, int P>
-__device__ __forceinline__ void mma_chunk(v4f (&acc)[CT], const WChunk& W, bool sparse, const uint8_t* lds, int li,
-                                          int lq) {
+template <int DT, int CT, int RT, bool WM, int P>
+__device__ __forceinline__ void mma_chunk(v4f (&acc)[RT][CT], const WChunk (&W)[RT], bool sparse, const uint8_t* lds,
+                                          int li, int lq) {
   static_assert(P == 1 || P == 2 || P == 4, "fragment group size");
+  // each B fragment read from LDS feeds the RT row tiles of this wave
   if (sparse) {
-    int mw[4];
-    meta_words<WM>(mw, W);
+    int mw[RT][4];
+#pragma unroll
+    for (int t = 0; t < RT; ++t) meta_words<WM>(mw[t], W[t]);
 #pragma unroll
     for (int j0 = 0; j0 < 4; j0 += P) {
       v8i b[P][CT];
@@ -614,12 +616,14 @@ __device__ __forceinline__ void mma_chunk(v4f (&acc)[CT], const WChunk& W, bool 
       for (int j = 0; j < P; ++j) frag_pair<DT, CT>(b[j], lds, li, lq, (j0 + j) * 128);
       if constexpr (P > 1) __builtin_amdgcn_sched_barrier(0);  // all reads of the group before its MMAs
 #pragma unroll
-      for (int j = 0; j < P; ++j) {
-        const int ix = DT == kFP8 ? mw[j0 + j] : (int)((uint32_t)mw[j0 + j] >> (16 * (lq & 1)));
+      for (int j = 0; j < P; ++j)
 #pragma unroll
-        for (int c = 0; c < CT; ++c)
-          acc[c] = mma_sparse(W.w[j0 + j], b[j][c], acc[c], ix, std::integral_constant<int, DT>());
-      }
+        for (int t = 0; t < RT; ++t) {
+          const int ix = DT == kFP8 ? mw[t][j0 + j] : (int)((uint32_t)mw[t][j0 + j] >> (16 * (lq & 1)));
+#pragma unroll
+          for (int c = 0; c < CT; ++c)
+            acc[t][c] = mma_sparse(W[t].w[j0 + j], b[j][c], acc[t][c], ix, std::integral_constant<int, DT>());
+        }
     }
   } else if constexpr (DT == kFP8) {
 #pragma unroll
@@ -629,11 +633,13 @@ __device__ __forceinline__ void mma_chunk(v4f (&acc)[CT], const WChunk& W, bool 
       for (int j = 0; j < P; ++j) frag_pair<DT, CT>(b[j], lds, li, lq, (j0 + j) * 128);
       if constexpr (P > 1) __builtin_amdgcn_sched_barrier(0);  // all reads of the group before its MMAs
 #pragma unroll
-      for (int j = 0; j < P; ++j) {
-        const v8i av = cat8(W.w[j0 + j], W.w[4 + j0 + j]);
+      for (int j = 0; j < P; ++j)
 #pragma unroll
-        for (int c = 0; c < CT; ++c) acc[c] = mma_dense(av, b[j][c], acc[c], std::integral_constant<int, DT>());
-      }
+        for (int t = 0; t < RT; ++t) {
+          const v8i av = cat8(W[t].w[j0 + j], W[t].w[4 + j0 + j]);
+#pragma unroll
+          for (int c = 0; c < CT; ++c) acc[t][c] = mma_dense(av, b[j][c], acc[t][c], std::integral_constant<int, DT>());
+        }
     }
   } else {
     const v4i z = {0, 0, 0, 0};
@@ -644,11 +650,13 @@ __device__ __forceinline__ void mma_chunk(v4f (&acc)[CT], const WChunk& W, bool 
       for (int j = 0; j < 2 * P; ++j) frag_one<DT, CT>(b[j], lds, li, lq, (j0 + j) * 64);
       if constexpr (P > 1) __builtin_amdgcn_sched_barrier(0);  // all reads of the group before its MMAs
 #pragma unroll
-      for (int j = 0; j < 2 * P; ++j) {
-        const v8i av = cat8(W.w[j0 + j], z);
+      for (int j = 0; j < 2 * P; ++j)
 #pragma unroll
-        for (int c = 0; c < CT; ++c) acc[c] = mma_dense(av, b[j][c], acc[c], std::integral_constant<int, DT>());
-      }
+        for (int t = 0; t < RT; ++t) {
+          const v8i av = cat8(W[t].w[j0 + j], z);
+#pragma unroll
+          for (int c = 0; c < CT; ++c) acc[t][c] = mma_dense(av, b[j][c], acc[t][c], std::integral_constant<int, DT>());
+        }
     }
   }
 }
@@ -671,7 +679,7 @@ __device__ __forceinline__ void barrier_vm() {
 // and slot c % NS), then a barrier that waits for the activations of chunk c+1 (issued
 // in step c+1-D, before that step's weights), so D chunks of weights stay in flight
 // across it.  The buffer being filled held chunk c-1, which every wave has finished.
-template <int DT, int CT, int WR, bool WM, int NS, int P, bool TL>
+template <int DT, int CT, int RT, int WR, bool WM, int NS, int P, bool TL>
 __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
   static_assert(NS == 3 || NS == 4, "three or four pipeline slots");
   static_assert(!TL || (DT == kFP8 && WM), "the tiled layout is fp8 with whole-chunk metadata loads");
@@ -689,7 +697,7 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
   const int rowend = R.row0 + R.rows;
   // workgroups of a region: (row group, K slice), slices of one row group adjacent
   const int slice = (g - R.wg0) % R.ksplit, rgroup = (g - R.wg0) / R.ksplit;
-  const int nbase = R.row0 + (rgroup * R.wused + wave) * 16;
+  const int nbase = R.row0 + (rgroup * R.wused + wave) * 16 * RT;  // first row of the wave's RT tiles
   const int m0 = mb * 16 * CT;
   const int K = R.kend;
   const int kbound = R.kbound;
@@ -699,14 +707,22 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
   const __amdgpu_buffer_rsrc_t rx = rsrc(a.X, a.x_bytes), rv = rsrc(a.values, a.v_bytes),
                                rm = rsrc(a.meta, a.m_bytes), rd = rsrc(a.dense, a.d_bytes);
 
-  v4f acc[CT];
+  v4f acc[RT][CT];
 #pragma unroll
-  for (int c = 0; c < CT; ++c) acc[c] = (v4f){0.f, 0.f, 0.f, 0.f};
+  for (int t = 0; t < RT; ++t)
+#pragma unroll
+    for (int c = 0; c < CT; ++c) acc[t][c] = (v4f){0.f, 0.f, 0.f, 0.f};
 
-  const int n = min(nbase + li, rowend - 1);
-  const uint32_t vrow = (uint32_t)((int64_t)n * a.v_ld_b) + 16u * lq;
-  const uint32_t mrow = (uint32_t)((int64_t)n * a.m_ld_b) + (DT == kFP8 ? 4u * lq : 4u * (lq >> 1));
-  const uint32_t drow = (uint32_t)((int64_t)max(n - R.dense_row_off, 0) * a.d_ld_b) + 16u * lq;
+  bool tok[RT];  // tile t of this wave holds rows of the region
+  uint32_t vrow[RT], mrow[RT], drow[RT];
+#pragma unroll
+  for (int t = 0; t < RT; ++t) {
+    tok[t] = nbase + 16 * t < rowend;
+    const int n = min(nbase + 16 * t + li, rowend - 1);
+    vrow[t] = (uint32_t)((int64_t)n * a.v_ld_b) + 16u * lq;
+    mrow[t] = (uint32_t)((int64_t)n * a.m_ld_b) + (DT == kFP8 ? 4u * lq : 4u * (lq >> 1));
+    drow[t] = (uint32_t)((int64_t)max(n - R.dense_row_off, 0) * a.d_ld_b) + 16u * lq;
+  }
 
   // chunk list: 2:4 chunks start at 0 and cover [0, kbound); dense chunks start at kbound;
   // this workgroup's K slice is chunks [c_lo, c_hi)
@@ -715,20 +731,27 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
   const int c_lo = R.cut[slice], c_hi = R.cut[slice + 1];
   auto chunk_k = [&](int c) { return c < n_sp ? c * KC : kbound + (c - n_sp) * KC; };
   auto chunk_end = [&](int c) { return c < n_sp ? kbound : K; };
-  // tiled layout: offsets of this lane in its tile's first chunk of each part
-  uint32_t vt = 0, mt = 0, dt = 0;
-  if constexpr (TL) {
-    const uint32_t ts = (uint32_t)(nbase / 16), td = (uint32_t)((nbase - R.dense_row_off) / 16);
-    vt = ts * (uint32_t)n_sp * 4096u + 16u * lane;
-    mt = ts * (uint32_t)n_sp * 1024u + 16u * lane;
-    dt = td * (uint32_t)n_de * 8192u + 16u * lane;
+  // tiled layout: offsets of this lane in its tiles' first chunk of each part
+  uint32_t vt[RT], mt[RT], dt[RT];
+#pragma unroll
+  for (int t = 0; t < RT; ++t) {
+    vt[t] = mt[t] = dt[t] = 0;
+    if constexpr (TL) {
+      const uint32_t ts = (uint32_t)(nbase / 16 + t), td = (uint32_t)((nbase - R.dense_row_off) / 16 + t);
+      vt[t] = ts * (uint32_t)n_sp * 4096u + 16u * lane;
+      mt[t] = ts * (uint32_t)n_sp * 1024u + 16u * lane;
+      dt[t] = td * (uint32_t)n_de * 8192u + 16u * lane;
+    }
   }
-  auto load = [&](WChunk& W, int c) {
-    if constexpr (TL)
-      load_chunk_tiled(W, c < n_sp, active && c < c_hi, c, max(c - n_sp, 0), vt, mt, dt, rv, rm, rd);
-    else
-      load_chunk<DT, WM>(W, c < n_sp, active && c < c_hi, chunk_k(c), chunk_end(c), lq, vrow, mrow, drow,
-                         R.dense_col_off, rv, rm, rd);
+  auto load = [&](WChunk (&W)[RT], int c) {
+#pragma unroll
+    for (int t = 0; t < RT; ++t) {
+      if constexpr (TL)
+        load_chunk_tiled(W[t], c < n_sp, tok[t] && c < c_hi, c, max(c - n_sp, 0), vt[t], mt[t], dt[t], rv, rm, rd);
+      else
+        load_chunk<DT, WM>(W[t], c < n_sp, tok[t] && c < c_hi, chunk_k(c), chunk_end(c), lq, vrow[t], mrow[t],
+                           drow[t], R.dense_col_off, rv, rm, rd);
+    }
   };
   auto xload = [&](int buf, int c) {
     x_to_lds<DT, CT, XI>(xbuf[buf], a, rx, m0, chunk_k(c), c < c_hi ? chunk_end(c) : -1, wave, lane);
@@ -741,8 +764,8 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
     constexpr bool ACT = decltype(act_const)::value;
     // loads issued after the activations of chunk c+1, at the barrier of chunk c: that
     // step's weights, then D-1 further steps of activations and weights
-    constexpr int AFTER = ACT ? NL + (D - 1) * (XI + NL) : (D - 1) * XI;
-    WChunk slot[NS];
+    constexpr int AFTER = ACT ? RT * NL + (D - 1) * (XI + RT * NL) : (D - 1) * XI;
+    WChunk slot[NS][RT];
 #pragma unroll
     for (int d = 0; d < D; ++d) {
       xload(d, c_lo + d);
@@ -757,7 +780,7 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
       if constexpr (ACT) {
         load(slot[SD], c + D);
         __builtin_amdgcn_sched_barrier(0);
-        mma_chunk<DT, CT, WM, P>(acc, slot[S], c < n_sp, xbuf[S], li, lq);
+        mma_chunk<DT, CT, RT, WM, P>(acc, slot[S], c < n_sp, xbuf[S], li, lq);
         __builtin_amdgcn_sched_barrier(0);
       }
       barrier_vm<AFTER>();
@@ -782,19 +805,21 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
   if (!active) return;
   xdl_fence();
 #pragma unroll
-  for (int cc = 0; cc < CT; ++cc) {
-    const int m = m0 + 16 * cc + li;
-    const int n0 = nbase + 4 * lq;
-    if (m >= a.M || n0 >= rowend) continue;
-    if (R.ksplit == 1) {
-      store4(a, acc[cc], m, n0, rowend);
-    } else {  // unscaled fp32 partial of this K slice
-      float* pp = a.part + ((int64_t)slice * a.M + m) * a.N + n0;
+  for (int t = 0; t < RT; ++t)
 #pragma unroll
-      for (int r = 0; r < 4; ++r)
-        if (n0 + r < rowend) pp[r] = acc[cc][r];
+    for (int cc = 0; cc < CT; ++cc) {
+      const int m = m0 + 16 * cc + li;
+      const int n0 = nbase + 16 * t + 4 * lq;
+      if (m >= a.M || n0 >= rowend) continue;
+      if (R.ksplit == 1) {
+        store4(a, acc[t][cc], m, n0, rowend);
+      } else {  // unscaled fp32 partial of this K slice
+        float* pp = a.part + ((int64_t)slice * a.M + m) * a.N + n0;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (n0 + r < rowend) pp[r] = acc[t][cc][r];
+      }
     }
-  }
 }
 
 // Y rows of the K-sliced regions: sum of the slices' fp32 partials in slice order, then
@@ -823,24 +848,24 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a) {
 // slots and two-step groups for four; fp8 without wide metadata loads (metadata rows not
 // 16-byte aligned, four separately masked loads per chunk) one step lighter, and even so
 // its four-tile, eight-wave instance spills a few registers.
-template <int DT, int CT, int WR, bool WM, bool TL>
+template <int DT, int CT, int RT, int WR, bool WM, bool TL>
 hipError_t launch_rows_wm(const dim3& grid, const dim3& block, const GemmArgs& a, hipStream_t s) {
   constexpr bool light = DT == kFP8 && !WM;
-  constexpr int NS = CT <= 2 && !light ? 4 : 3;
-  constexpr int P = CT == 1 ? 4 : 1;
-  hipLaunchKernelGGL((spense_gemm_rows_kernel<DT, CT, WR, WM, NS, P, TL>), grid, block, 0, s, a);
+  constexpr int NS = CT <= 2 && RT == 1 && !light ? 4 : 3;
+  constexpr int P = CT == 1 && RT == 1 ? 4 : 1;
+  hipLaunchKernelGGL((spense_gemm_rows_kernel<DT, CT, RT, WR, WM, NS, P, TL>), grid, block, 0, s, a);
   return hipGetLastError();
 }
 
-template <int DT, int CT, int WR>
+template <int DT, int CT, int RT, int WR>
 hipError_t launch_rows(const LaunchShape& ls, const GemmArgs& a, hipStream_t s) {
   dim3 grid(a.groups, ls.mblocks), block(64 * WR);
   if constexpr (DT == kFP8) {
-    if (a.tiled) return launch_rows_wm<DT, CT, WR, true, true>(grid, block, a, s);
-    if (a.m_ld_b % 16 == 0) return launch_rows_wm<DT, CT, WR, true, false>(grid, block, a, s);
+    if (a.tiled) return launch_rows_wm<DT, CT, RT, WR, true, true>(grid, block, a, s);
+    if (a.m_ld_b % 16 == 0) return launch_rows_wm<DT, CT, RT, WR, true, false>(grid, block, a, s);
   }
   if (a.tiled) return hipErrorInvalidValue;
-  return launch_rows_wm<DT, CT, WR, false, false>(grid, block, a, s);
+  return launch_rows_wm<DT, CT, RT, WR, false, false>(grid, block, a, s);
 }
 
 template <int DT, int CT, int RT, int W, int UMAX = 0>
@@ -879,8 +904,9 @@ hipError_t launch_ct(const LaunchShape& ls, const GemmArgs& a, hipStream_t s) {
 template <int DT, int CT>
 hipError_t launch_rows_ct(const LaunchShape& ls, const GemmArgs& a, hipStream_t s) {
   switch (ls.rt * 100 + ls.waves) {
-    case 104: return launch_rows<DT, CT, 4>(ls, a, s);
-    case 108: return launch_rows<DT, CT, 8>(ls, a, s);
+    case 104: return launch_rows<DT, CT, 1, 4>(ls, a, s);
+    case 108: return launch_rows<DT, CT, 1, 8>(ls, a, s);
+    case 204: return launch_rows<DT, CT, 2, 4>(ls, a, s);
     default: return hipErrorInvalidValue;
   }
 }

@@ -233,7 +233,9 @@ KERNEL_SHAPES = [dict(), dict(SPENSE_WAVES="4", SPENSE_RT="1"), dict(SPENSE_WAVE
                  dict(SPENSE_ROWS="1", SPENSE_WAVES="4", SPENSE_RT="1"),
                  dict(SPENSE_ROWS="1", SPENSE_WAVES="8", SPENSE_RT="1"),
                  dict(SPENSE_ROWS="1", SPENSE_WAVES="8", SPENSE_RT="1", SPENSE_KSPLIT="4"),
-                 dict(SPENSE_ROWS="1", SPENSE_WAVES="4", SPENSE_RT="1", SPENSE_KSPLIT="7")]
+                 dict(SPENSE_ROWS="1", SPENSE_WAVES="4", SPENSE_RT="1", SPENSE_KSPLIT="7"),
+                 dict(SPENSE_ROWS="1", SPENSE_WAVES="4", SPENSE_RT="2"),
+                 dict(SPENSE_ROWS="1", SPENSE_WAVES="4", SPENSE_RT="2", SPENSE_KSPLIT="3")]
 
 
 @pytest.mark.parametrize("axis,db", [(1, 6144), (0, 1536)])
@@ -459,7 +461,7 @@ def test_full_size_exact_integers_whole_output(S, name, N, K, axis, M):
 @pytest.mark.parametrize("rows,rt,waves,wused,ks", [(0, 1, 4, 0, 0), (0, 2, 4, 0, 0), (0, 1, 8, 0, 0), (0, 2, 8, 0, 0),
                                                     (0, 1, 16, 0, 0), (0, 4, 4, 0, 0), (1, 1, 4, 0, 1), (1, 1, 8, 0, 1),
                                                     (1, 1, 4, 3, 1), (1, 1, 8, 5, 1), (1, 1, 8, 8, 1), (1, 1, 4, 0, 2),
-                                                    (1, 1, 8, 3, 3), (1, 1, 8, 8, 2)])
+                                                    (1, 1, 8, 3, 3), (1, 1, 8, 8, 2), (1, 2, 4, 0, 1), (1, 2, 4, 3, 2)])
 @pytest.mark.parametrize("dtype,axis,M", [(FP8, 1, 3), (FP8, 0, 40), (BF16, 1, 20), (FP8, 1, 64), (BF16, 0, 17)])
 def test_every_workgroup_shape_is_exact(S, rows, rt, waves, wused, ks, dtype, axis, M, monkeypatch):
     """All built kernels and (row tiles, waves) shapes - K split across the waves of a
