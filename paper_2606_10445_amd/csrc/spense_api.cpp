@@ -162,6 +162,8 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 const int kShapes[][2] = {{2, 4}, {1, 4}, {2, 8}, {1, 8}, {1, 16}, {4, 4}};
 
 constexpr int kCUs = 256;  // compute units of an MI355X
+constexpr int64_t kBigMinM = 256;      // tokens from which the large-M kernel is used (fp8)
+constexpr int64_t kBigMinTiles = 192;  // and workgroup tiles (128 rows x 256 tokens) it needs
 
 // Row-split kernel: how many of a workgroup's waves own rows in each region.  A region
 // whose rows carry more bytes (dense rows) gets fewer rows per workgroup, so that the
@@ -299,6 +301,16 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
   pl->ls.waves = waves;
   pl->ls.rows = rows_mode;
   pl->ls.u8 = (ct == 1 && rt == 1 && (waves == 4 || waves == 8) && env_int("SPENSE_U8", 0)) ? 1 : 0;
+  // Many tokens (fp8): 128-row x 256-token workgroup tiles, where the matrix cores bound.
+  // Measured on MI355X (q/k/gate/down shapes, M = 128 .. 2048): it wins from M = 256 once
+  // there are at least 192 such tiles; with fewer, the row-split kernel's finer grid
+  // keeps more CUs busy.
+  int big = (dtype == SPENSE_FP8_E4M3FN && M >= kBigMinM && ceil_div(N, 128) * ceil_div(M, 256) >= kBigMinTiles) ? 1 : 0;
+  const int ebig = env_int("SPENSE_BIG", -1);  // testing knob: force the large-M kernel on or off
+  if (ebig >= 0) big = (ebig && dtype == SPENSE_FP8_E4M3FN) ? 1 : 0;
+  pl->ls.big = big;
+  if (big) pl->ls.waves = env_int("SPENSE_BIG_WAVES", 8) == 4 ? 4 : 8;  // testing knob
+  const int64_t tblocks = ceil_div(M, 256);
 
   Region regs[2];
   int nreg = 0;
@@ -313,7 +325,7 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
     r.kend = (int32_t)K;
     r.wused = waves;
     r.ksplit = 1;
-    r.nrb = (int32_t)ceil_div(rows, 16 * rt);
+    r.nrb = (int32_t)(big ? ceil_div(rows, 128) * tblocks : ceil_div(rows, 16 * rt));
     // cut [0, K) into `waves` parts of equal byte cost, on multiples of the instruction K
     const double cs = sparse_cost * kbound, total = cs + es * (double)(K - kbound);
     r.cut[0] = 0;
@@ -336,7 +348,7 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
     add(0, N, dense_begin, 0, dense_begin);
   }
   int ksplit = 1;
-  if (rows_mode) {
+  if (rows_mode && !big) {
     // chunks of 4 instruction steps: 512 logical columns (fp8), 256 (bf16)
     const int64_t kc = dtype == SPENSE_FP8_E4M3FN ? 512 : 256;
     int64_t chunks = 0;
@@ -355,6 +367,7 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
   }
   a.groups = groups;
   a.tiled = tiled ? 1 : 0;
+  a.tblocks = (int32_t)tblocks;
   // K-sliced regions keep fp32 partial sums: slices x M x N floats
   pl->ws_bytes = ksplit > 1 ? (size_t)ksplit * (size_t)M * (size_t)N * sizeof(float) : 0;
 }

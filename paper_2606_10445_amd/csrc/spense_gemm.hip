@@ -911,9 +911,279 @@ hipError_t launch_rows_ct(const LaunchShape& ls, const GemmArgs& a, hipStream_t 
   }
 }
 
+// ---------------------------------------------------------------- large-M kernel
+// For many tokens the matrix cores become the bound, and every byte moved should feed
+// many MMAs.  A workgroup computes 128 weight rows x 256 tokens; its waves form a grid of
+// 2 row halves x 2 or 4 token parts, each wave 64 rows (4 row tiles) x 128 or 64 tokens:
+// 32 or 16 accumulators and MMAs per 128-column step (with 8 waves, two per SIMD, one
+// wave's LDS waits are covered by the other's MMAs).  Both operands of a step are copied once into LDS by
+// direct loads (activations 256 x 128 bytes, with 16-byte blocks swizzled so that the
+// fragment reads of 16 rows are conflict-free; the weight fragments of the 8 row tiles
+// in lane order), three stages deep, so that two steps of loads are in flight without
+// holding registers.  Each B fragment read feeds 4 MMAs, each A fragment 8 or 4.  Workgroups
+// of one row block are adjacent (token block fastest), so with 8 token blocks each XCD
+// keeps one activation block in its L2.  fp8 only.
+constexpr int kBigRows = 128, kBigTokens = 256;
+
+__device__ __forceinline__ v4i lo4(v8i v) { return (v4i){v[0], v[1], v[2], v[3]}; }
+
+struct BigStage {
+  static constexpr int X_B = kBigTokens * 128;  // activations: 256 tokens x 128 bytes
+  static constexpr int W_B = 8 * 2048;          // per row tile: 2:4 values or dense halves
+  static constexpr int M_B = 8 * 256;           // per row tile: metadata words
+  static constexpr int BYTES = X_B + W_B + M_B;
+  __device__ static __forceinline__ int xaddr(int r, int b) { return r * 128 + ((b ^ ((r >> 1) & 7)) << 4); }
+};
+
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_impl(F& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>()), ...);
+}
+// f(integral_constant<int, i>) for i = 0 .. N-1, each index a compile-time constant.
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>());
+}
+
+// Where the loads of one step go and what they cover.
+struct BigStepLd {
+  uint8_t* st;                 // stage buffer
+  int ks, ke, cs, js, cd, jd;  // first column, column end, tiled-layout chunk and step
+  bool in, sparse;
+};
+
+template <bool TL, int WV>
+__global__ __launch_bounds__(64 * WV) void spense_gemm_big_kernel(GemmArgs a) {
+  static_assert(WV == 4 || WV == 8, "4 or 8 waves");
+  constexpr int NS = 3, D = NS - 1;
+  constexpr int TC = 32 / WV;                    // token tiles per wave
+  constexpr int TU = 8 / WV;                     // row tiles whose weights a wave copies
+  constexpr int XI = BigStage::X_B / 1024 / WV;  // 1 KB activation blocks per wave per step
+  constexpr int NL = XI + 3 * TU;                // loads per wave per step
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int li = lane & 15, lq = lane >> 4;
+  const int wr = wave & 1, wc = wave >> 1;
+  const int g = blockIdx.x;
+  const int ri = (a.nreg > 1 && g >= a.reg[1].wg0) ? 1 : 0;
+  const Region& R = a.reg[ri];
+  const int rowend = R.row0 + R.rows;
+  const int rb = (g - R.wg0) / a.tblocks, tb = (g - R.wg0) % a.tblocks;
+  const int rblk = R.row0 + rb * kBigRows;  // first row of the workgroup
+  const int m0 = tb * kBigTokens;
+  const int K = R.kend, kbound = R.kbound;
+
+  extern __shared__ __attribute__((aligned(1024))) uint8_t big_lds[];
+  const __amdgpu_buffer_rsrc_t rx = rsrc(a.X, a.x_bytes), rv = rsrc(a.values, a.v_bytes),
+                               rm = rsrc(a.meta, a.m_bytes), rd = rsrc(a.dense, a.d_bytes);
+  v4f acc[4][TC];
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+#pragma unroll
+    for (int c = 0; c < TC; ++c) acc[t][c] = (v4f){0.f, 0.f, 0.f, 0.f};
+
+  // steps of 128 columns: 2:4 steps cover [0, kbound), dense steps start at kbound
+  const int n_sp = (kbound + 127) / 128, n_de = (K - kbound + 127) / 128, nst = n_sp + n_de;
+  const int nch_sp = (n_sp + 3) / 4, nch_de = (n_de + 3) / 4;  // tiled layout chunks
+  auto step_k = [&](int s) { return s < n_sp ? 128 * s : kbound + 128 * (s - n_sp); };
+
+  // This wave copies the weights of row tiles TU wave .. TU wave + TU - 1.
+  bool tok[TU];
+  uint32_t vb[TU], mb[TU], db[TU];
+#pragma unroll
+  for (int u = 0; u < TU; ++u) {
+    const int r0 = rblk + 16 * (TU * wave + u);
+    tok[u] = r0 < rowend;
+    if constexpr (TL) {
+      const uint32_t ts = (uint32_t)(r0 / 16), td = (uint32_t)((r0 - R.dense_row_off) / 16);
+      vb[u] = ts * (uint32_t)nch_sp * 4096u + 16u * lane;
+      mb[u] = ts * (uint32_t)nch_sp * 1024u + 16u * li + 4u * lq;
+      db[u] = td * (uint32_t)nch_de * 8192u + 16u * lane;
+    } else {
+      const int n = min(r0 + li, rowend - 1);
+      vb[u] = (uint32_t)((int64_t)n * a.v_ld_b) + 16u * lq;
+      mb[u] = (uint32_t)((int64_t)n * a.m_ld_b) + 4u * lq;
+      db[u] = (uint32_t)((int64_t)max(n - R.dense_row_off, 0) * a.d_ld_b) + 16u * lq;
+    }
+  }
+
+  // Loads of step s into a stage buffer, numbered 0 .. NL-1: the activation blocks, then
+  // for each of the wave's row tiles the value (or first dense) fragment, the second
+  // dense fragment and the metadata word.  The ones a step does not use get out-of-range
+  // offsets, so every step issues the same loads.
+  auto prep = [&](int buf, int s) {
+    BigStepLd p;
+    p.st = big_lds + buf * BigStage::BYTES;
+    // wave-uniform (readfirstlane), so that the buffer resources chosen by them stay scalar
+    p.in = __builtin_amdgcn_readfirstlane(s < nst ? 1 : 0) != 0;
+    p.sparse = __builtin_amdgcn_readfirstlane(s < n_sp ? 1 : 0) != 0;
+    p.ks = step_k(s);
+    p.ke = !p.in ? -1 : (p.sparse ? kbound : K);
+    const int sd = max(s - n_sp, 0);
+    p.cs = s / 4;
+    p.js = s & 3;
+    p.cd = sd / 4;
+    p.jd = sd & 3;
+    return p;
+  };
+  auto load_one = [&](auto i_const, const BigStepLd& p) {
+    constexpr int i = decltype(i_const)::value;
+    if constexpr (i < XI) {
+      const int blk = wave * XI + i;
+      const int r = 8 * blk + (lane >> 3), pb = lane & 7, b = pb ^ ((r >> 1) & 7);
+      const int m = m0 + r, kcol = p.ks + 16 * b;
+      const uint32_t off = sel(m < a.M && kcol < p.ke, (uint32_t)((int64_t)m * a.ldx_b + kcol));
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (__attribute__((address_space(3))) void*)(p.st + blk * 1024), 16, off,
+                                               0, 0, 0);
+    } else {
+      constexpr int u = (i - XI) / 3, kind = (i - XI) % 3;
+      const int tile = TU * wave + u;
+      const bool ok = p.in && tok[u];
+      if constexpr (kind == 0) {
+        uint32_t off;
+        bool k;
+        if constexpr (TL) {
+          off = p.sparse ? vb[u] + (uint32_t)(p.cs * 4096 + 1024 * p.js) : db[u] + (uint32_t)(p.cd * 8192 + 2048 * p.jd);
+          k = ok;
+        } else {
+          off = p.sparse ? vb[u] + (uint32_t)(p.ks >> 1) : db[u] + (uint32_t)(p.ks - R.dense_col_off);
+          k = ok && p.ks + (p.sparse ? 32 : 16) * lq < p.ke;
+        }
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(p.sparse ? rv : rd,
+                                                 (__attribute__((address_space(3))) void*)(p.st + BigStage::X_B + tile * 2048),
+                                                 16, sel(k, off), 0, 0, TL ? kTiledNT : kNT);
+      } else if constexpr (kind == 1) {
+        uint32_t off;
+        bool k;
+        if constexpr (TL) {
+          off = db[u] + (uint32_t)(p.cd * 8192 + 2048 * p.jd + 1024);
+          k = ok;
+        } else {
+          off = db[u] + (uint32_t)(p.ks - R.dense_col_off) + 64;
+          k = ok && p.ks + 64 + 16 * lq < p.ke;
+        }
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            rd, (__attribute__((address_space(3))) void*)(p.st + BigStage::X_B + tile * 2048 + 1024), 16,
+            sel(k && !p.sparse, off), 0, 0, TL ? kTiledNT : kNT);
+      } else {
+        uint32_t off;
+        bool k;
+        if constexpr (TL) {
+          off = mb[u] + (uint32_t)(p.cs * 1024 + 256 * p.js);
+          k = ok;
+        } else {
+          off = mb[u] + 4u * (uint32_t)(p.ks >> 5);
+          k = ok && p.ks + 32 * lq < p.ke;
+        }
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            rm, (__attribute__((address_space(3))) void*)(p.st + BigStage::X_B + BigStage::W_B + tile * 256), 4,
+            sel(k && p.sparse, off), 0, 0, TL ? kTiledNT : kNT);
+      }
+    }
+  };
+
+  // MMAs of one step: the A fragments of the wave's 4 row tiles, then per token tile its
+  // B fragment (read one tile ahead) and 4 MMAs, each group followed by PER of the loads
+  // of a later step.  A load instruction waits at issue until the CU's address unit takes
+  // it, so spreading them between the MMAs keeps the matrix core busy meanwhile.
+  constexpr int PER = (NL + TC - 1) / TC;
+  auto mma = [&](auto sparse_const, const uint8_t* st, const BigStepLd& ld) {
+    constexpr bool SPARSE = decltype(sparse_const)::value;
+    const uint8_t* wl = st + BigStage::X_B + (4 * wr) * 2048 + 16 * lane;
+    const int* ml = reinterpret_cast<const int*>(st + BigStage::X_B + BigStage::W_B + (4 * wr) * 256) + lane;
+    auto bfrag = [&](int c) {
+      const int r = 16 * (TC * wc + c) + li;
+      return cat8(*reinterpret_cast<const v4i*>(st + BigStage::xaddr(r, lq)),
+                  *reinterpret_cast<const v4i*>(st + BigStage::xaddr(r, 4 + lq)));
+    };
+    v8i w[4];
+    int ix[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const v4i lo = *reinterpret_cast<const v4i*>(wl + t * 2048);
+      if constexpr (SPARSE) {
+        w[t] = cat8(lo, lo);
+        ix[t] = ml[t * 64];
+      } else {
+        w[t] = cat8(lo, *reinterpret_cast<const v4i*>(wl + t * 2048 + 1024));
+      }
+    }
+    v8i b = bfrag(0);
+    static_for<TC>([&](auto c_const) {
+      constexpr int c = decltype(c_const)::value;
+      const v8i bn = bfrag(c < TC - 1 ? c + 1 : TC - 1);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        if constexpr (SPARSE)
+          acc[t][c] = mma_sparse(lo4(w[t]), b, acc[t][c], ix[t], std::integral_constant<int, kFP8>());
+        else
+          acc[t][c] = mma_dense(w[t], b, acc[t][c], std::integral_constant<int, kFP8>());
+      }
+      static_for<PER>([&](auto j_const) {
+        constexpr int i = c * PER + decltype(j_const)::value;
+        if constexpr (i < NL) load_one(std::integral_constant<int, i>(), ld);
+      });
+      __builtin_amdgcn_sched_barrier(0);
+      b = bn;
+    });
+  };
+
+  // Pipeline: step s issues the loads of step s + D into stage (s + D) % NS (it held step
+  // s - 1, which every wave has finished), runs the MMAs of step s, then waits for its own
+  // loads of step s + 1 (only step s + D's are younger) and meets the other waves.  The
+  // 2:4 steps and the dense steps are separate loops, so each loop body is one block.
+#pragma unroll
+  for (int d = 0; d < D; ++d) {
+    const BigStepLd p = prep(d, d);
+    static_for<NL>([&](auto i_const) { load_one(i_const, p); });
+  }
+  barrier_vm<0>();
+  int s = 0, cur = 0;  // cur = s % NS
+  auto step = [&](auto sparse_const) {
+    const int nxt = cur == 0 ? D : cur - 1;  // (s + D) % NS
+    mma(sparse_const, big_lds + cur * BigStage::BYTES, prep(nxt, s + D));
+    __builtin_amdgcn_sched_barrier(0);
+    barrier_vm<(D - 1) * NL>();
+    ++s;
+    cur = cur == NS - 1 ? 0 : cur + 1;
+  };
+  while (s < n_sp) step(std::true_type());
+  while (s < nst) step(std::false_type());
+
+  xdl_fence();
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+#pragma unroll
+    for (int c = 0; c < TC; ++c) {
+      const int m = m0 + 16 * (TC * wc + c) + li;
+      const int n0 = rblk + 16 * (4 * wr + t) + 4 * lq;
+      if (m < a.M && n0 < rowend) store4(a, acc[t][c], m, n0, rowend);
+    }
+}
+
+constexpr int kBigLds = 3 * BigStage::BYTES;
+
+template <int WV>
+hipError_t launch_big_wv(const GemmArgs& a, hipStream_t s) {
+  static_assert(kBigLds <= 160 * 1024, "LDS of a CU");
+  auto k = a.tiled ? spense_gemm_big_kernel<true, WV> : spense_gemm_big_kernel<false, WV>;
+  static bool attr_set[2] = {false, false};
+  if (!attr_set[a.tiled]) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize, kBigLds);
+    if (e != hipSuccess) return e;
+    attr_set[a.tiled] = true;
+  }
+  hipLaunchKernelGGL(k, dim3(a.groups), dim3(64 * WV), kBigLds, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_big(const LaunchShape& ls, const GemmArgs& a, hipStream_t s) {
+  return ls.waves == 4 ? launch_big_wv<4>(a, s) : launch_big_wv<8>(a, s);
+}
+
 template <int DT>
 hipError_t launch_dt(const LaunchShape& ls, const GemmArgs& a, hipStream_t s) {
-  if (a.tiled && !ls.rows) return hipErrorInvalidValue;  // only the row-split kernel reads the tiled layout
+  if (ls.big) return DT == kFP8 ? launch_big(ls, a, s) : hipErrorInvalidValue;
+  if (a.tiled && !ls.rows) return hipErrorInvalidValue;  // the K-split kernel reads the row-major layout only
   if (ls.rows) {
     if (ls.ct == 1) return launch_rows_ct<DT, 1>(ls, a, s);
     if (ls.ct == 2) return launch_rows_ct<DT, 2>(ls, a, s);

@@ -56,6 +56,7 @@ struct GemmArgs {
   int32_t groups;
   int32_t tiled;  // weight buffers in the tiled execution layout (fp8, row-split kernel)
   float* part;    // fp32 partial sums of K-sliced regions: part[(slice * M + m) * N + n]
+  int32_t tblocks;  // large-M kernel: 256-token blocks (workgroups of a row block are adjacent)
   Region reg[2];
 };
 
@@ -66,6 +67,7 @@ struct LaunchShape {
   int mblocks;  // grid.y
   int u8;       // eight instruction steps per batch of loads (single activation tile only)
   int rows;     // row-split workgroups with activations staged in LDS
+  int big;      // large-M kernel: 128-row x 256-token workgroup tiles (fp8)
 };
 
 hipError_t launch_gemm(int dtype, const LaunchShape& ls, const GemmArgs& a, hipStream_t s);

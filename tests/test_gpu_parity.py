@@ -374,6 +374,45 @@ def test_tiled_exact_integers(S):
         assert np.array_equal(run_gemm(S, pwt, X, sw, sx, False).view(np.uint16), ref["y_bf16"])
 
 
+# ------------------------------------------------------------------ large-M kernel
+BIG_CASES = [  # axis, M, N, K, dense_begin: ragged tokens, rows and columns around its 256 x 128 x 128 tiles
+    (0, 1, 200, 1056, 72), (0, 300, 272, 1024, 208), (1, 257, 200, 1056, 800), (1, 513, 136, 640, 128),
+    (0, 600, 136, 384, 0), (0, 300, 136, 384, 136), (1, 300, 64, 512, 0), (1, 300, 64, 512, 512)]
+
+
+@pytest.mark.parametrize("waves", [4, 8])
+@pytest.mark.parametrize("axis,M,N,K,db", BIG_CASES)
+def test_large_m_kernel_exact_both_layouts(S, axis, M, N, K, db, waves, monkeypatch):
+    """The 128-row x 256-token kernel (4 or 8 waves), forced on at any M, on exact-integer
+    data: bit-exact against the oracle with the row-major and the tiled weight."""
+    W, mask, X, sw, sx = gen.make_exact_int(13, M + N, M, N, K, gaxis(axis), db, gen.FP8)
+    pw, (v, m, d) = compress_both(S, W, mask, FP8, axis, db)
+    ref = oracle.spense_gemm(X, v, m, d, N, K, FP8, axis, db, sw, sx)
+    monkeypatch.setenv("SPENSE_BIG", "1")
+    monkeypatch.setenv("SPENSE_BIG_WAVES", str(waves))
+    for w in (pw, S.tile(pw)):
+        assert np.array_equal(run_gemm(S, w, X, sw, sx, True), ref["y_f32"])
+        assert np.array_equal(run_gemm(S, w, X, sw, sx, False).view(np.uint16), ref["y_bf16"])
+
+
+@pytest.mark.parametrize("axis,db", [(0, 744), (1, 1536)])
+def test_large_m_kernel_random_within_bound(S, axis, db, monkeypatch):
+    """Random data through the large-M kernel: inside the error bound against the oracle,
+    equal with both layouts and bitwise repeatable."""
+    M, N, K = 520, 1000, 2080
+    W, mask, X, sw, sx = random_case(6, M, N, K, axis, db, FP8)
+    pw, (v, m, d) = compress_both(S, W, mask, FP8, axis, db)
+    ref = oracle.spense_gemm(X, v, m, d, N, K, FP8, axis, db, sw, sx)
+    Wd = oracle.decompress(v, m, d, N, K, FP8, axis, db)
+    pwt = S.tile(pw)
+    monkeypatch.setenv("SPENSE_BIG", "1")
+    y32 = run_gemm(S, pw, X, sw, sx, True)
+    assert_f32_bound(y32, X, Wd, FP8, sw, sx)
+    assert_bf16_close(run_gemm(S, pw, X, sw, sx, False).view(np.uint16), ref["y_bf16"], FP8)
+    for _ in range(2):
+        assert np.array_equal(run_gemm(S, pwt, X, sw, sx, True), y32)
+
+
 # ------------------------------------------------------------------ full-size workloads
 @functools.lru_cache(maxsize=4)
 def _matrix(cfg, mat, name, N, K, axis, frac, dtype):
