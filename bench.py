@@ -172,6 +172,22 @@ def measure_extras(args, torch, gen, S, ws, pws, copies, swd, mx, dws, dense_cop
     ex["m2048"] = {"us_per_gemm": round(bms * 1e3, 1), "tflops": round(fl / (bms * 1e-3) / 1e12, 1),
                    "mfma_util": round(fl / (bms * 1e-3) / 1e12 / FP8_PEAK_TFLOPS, 4),
                    "dense_us_per_gemm": round(dms * 1e3, 1), "speedup_vs_dense": round(dms / bms, 3)}
+    # vendor reference: the same weight, every entry stored (dense fp8), through ROCm's fp8
+    # GEMM library (torch._scaled_mm, hipBLASLt); three copies rotated past the MALL
+    try:
+        f8 = torch.float8_e4m3fn
+        vws = [torch.from_numpy(mx.W).cuda().view(f8) for _ in range(3)]
+        one = torch.ones((), dtype=torch.float32, device="cuda")
+        vend = {}
+        for Mv, Xv, us_sp in ((M_MAIN, Xd, main["us_per_step"]), (Mb, Xbd, bms * 1e3)):
+            Xf = Xv.view(f8)
+            vms = time_launches(lambda i: torch._scaled_mm(Xf, vws[i % 3].t(), scale_a=one, scale_b=one,
+                                                           out_dtype=torch.bfloat16), 50 if Mv < 1024 else 20, 5, torch)
+            vend[f"m{Mv}"] = {"us_per_gemm": round(vms * 1e3, 2), "spense_speedup": round(vms * 1e3 / us_sp, 3)}
+        ex["vendor_dense_fp8"] = vend
+        del vws
+    except Exception as e:  # the reference is context only
+        ex["vendor_dense_fp8"] = {"error": repr(e)[:120]}
     del Xbd, Yb
     # decoder-layer set at M = 64 (each matrix its own seeded draw), tiled, with the dense
     # layer (every row dense) for comparison; weights rotated over two copies of the set

@@ -309,7 +309,13 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
   const int ebig = env_int("SPENSE_BIG", -1);  // testing knob: force the large-M kernel on or off
   if (ebig >= 0) big = (ebig && dtype == SPENSE_FP8_E4M3FN) ? 1 : 0;
   pl->ls.big = big;
-  if (big) pl->ls.waves = env_int("SPENSE_BIG_WAVES", 8) == 4 ? 4 : 8;  // testing knob
+  int big_rows = 128;  // rows of a large-M workgroup tile
+  if (big) {
+    // testing knobs: waves of a workgroup and row tiles of a wave (8 only with 4 waves)
+    pl->ls.waves = env_int("SPENSE_BIG_WAVES", 8) == 4 ? 4 : 8;
+    pl->ls.rt = (env_int("SPENSE_BIG_RPW", 4) == 8 && pl->ls.waves == 4) ? 8 : 4;
+    big_rows = 32 * pl->ls.rt;
+  }
   const int64_t tblocks = ceil_div(M, 256);
 
   Region regs[2];
@@ -325,7 +331,7 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
     r.kend = (int32_t)K;
     r.wused = waves;
     r.ksplit = 1;
-    r.nrb = (int32_t)(big ? ceil_div(rows, 128) * tblocks : ceil_div(rows, 16 * rt));
+    r.nrb = (int32_t)(big ? ceil_div(rows, big_rows) * tblocks : ceil_div(rows, 16 * rt));
     // cut [0, K) into `waves` parts of equal byte cost, on multiples of the instruction K
     const double cs = sparse_cost * kbound, total = cs + es * (double)(K - kbound);
     r.cut[0] = 0;

@@ -913,25 +913,29 @@ hipError_t launch_rows_ct(const LaunchShape& ls, const GemmArgs& a, hipStream_t 
 
 // ---------------------------------------------------------------- large-M kernel
 // For many tokens the matrix cores become the bound, and every byte moved should feed
-// many MMAs.  A workgroup computes 128 weight rows x 256 tokens; its waves form a grid of
-// 2 row halves x 2 or 4 token parts, each wave 64 rows (4 row tiles) x 128 or 64 tokens:
-// 32 or 16 accumulators and MMAs per 128-column step (with 8 waves, two per SIMD, one
-// wave's LDS waits are covered by the other's MMAs).  Both operands of a step are copied once into LDS by
+// many MMAs.  A workgroup computes 32 RPW weight rows x 256 tokens; its waves form a grid
+// of 2 row halves x 2 or 4 token parts, each wave 16 RPW rows (RPW row tiles) x 128 or 64
+// tokens (with 8 waves, two per SIMD, one wave's LDS waits are covered by the other's
+// MMAs).  RPW = 4: 128-row workgroups; RPW = 8 with 4 waves: 256 x 256 tiles, 64 MMAs of
+// a wave per step and 256 accumulators in the matrix-core registers, which halves the
+// bytes each MMA moves through the CU's load path.  Both operands of a step are copied once into LDS by
 // direct loads (activations 256 x 128 bytes, with 16-byte blocks swizzled so that the
 // fragment reads of 16 rows are conflict-free; the weight fragments of the 8 row tiles
 // in lane order), three stages deep, so that two steps of loads are in flight without
 // holding registers.  Each B fragment read feeds 4 MMAs, each A fragment 8 or 4.  Workgroups
 // of one row block are adjacent (token block fastest), so with 8 token blocks each XCD
 // keeps one activation block in its L2.  fp8 only.
-constexpr int kBigRows = 128, kBigTokens = 256;
+constexpr int kBigTokens = 256;
 
 __device__ __forceinline__ v4i lo4(v8i v) { return (v4i){v[0], v[1], v[2], v[3]}; }
 
+template <int NT>  // row tiles of a workgroup
 struct BigStage {
   static constexpr int X_B = kBigTokens * 128;  // activations: 256 tokens x 128 bytes
-  static constexpr int W_B = 8 * 2048;          // per row tile: 2:4 values or dense halves
-  static constexpr int M_B = 8 * 256;           // per row tile: metadata words
+  static constexpr int W_B = NT * 2048;         // per row tile: 2:4 values or dense halves
+  static constexpr int M_B = NT * 256;          // per row tile: metadata words
   static constexpr int BYTES = X_B + W_B + M_B;
+  static constexpr int NS = 3 * BYTES <= 160 * 1024 ? 3 : 2;  // stages that fit in LDS
   __device__ static __forceinline__ int xaddr(int r, int b) { return r * 128 + ((b ^ ((r >> 1) & 7)) << 4); }
 };
 
@@ -952,13 +956,16 @@ struct BigStepLd {
   bool in, sparse;
 };
 
-template <bool TL, int WV>
+template <bool TL, int WV, int RPW>
 __global__ __launch_bounds__(64 * WV) void spense_gemm_big_kernel(GemmArgs a) {
   static_assert(WV == 4 || WV == 8, "4 or 8 waves");
-  constexpr int NS = 3, D = NS - 1;
+  constexpr int NT = 2 * RPW;                 // row tiles of the workgroup
+  typedef BigStage<NT> St;
+  constexpr int NS = St::NS, D = NS - 1;
   constexpr int TC = 32 / WV;                    // token tiles per wave
-  constexpr int TU = 8 / WV;                     // row tiles whose weights a wave copies
-  constexpr int XI = BigStage::X_B / 1024 / WV;  // 1 KB activation blocks per wave per step
+  constexpr int TU = NT / WV;                    // row tiles whose weights a wave copies
+  static_assert(TU >= 1 && TU * WV == NT, "weight copies split evenly");
+  constexpr int XI = St::X_B / 1024 / WV;  // 1 KB activation blocks per wave per step
   constexpr int NL = XI + 3 * TU;                // loads per wave per step
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int li = lane & 15, lq = lane >> 4;
@@ -968,16 +975,16 @@ __global__ __launch_bounds__(64 * WV) void spense_gemm_big_kernel(GemmArgs a) {
   const Region& R = a.reg[ri];
   const int rowend = R.row0 + R.rows;
   const int rb = (g - R.wg0) / a.tblocks, tb = (g - R.wg0) % a.tblocks;
-  const int rblk = R.row0 + rb * kBigRows;  // first row of the workgroup
+  const int rblk = R.row0 + rb * 16 * NT;  // first row of the workgroup
   const int m0 = tb * kBigTokens;
   const int K = R.kend, kbound = R.kbound;
 
   extern __shared__ __attribute__((aligned(1024))) uint8_t big_lds[];
   const __amdgpu_buffer_rsrc_t rx = rsrc(a.X, a.x_bytes), rv = rsrc(a.values, a.v_bytes),
                                rm = rsrc(a.meta, a.m_bytes), rd = rsrc(a.dense, a.d_bytes);
-  v4f acc[4][TC];
+  v4f acc[RPW][TC];
 #pragma unroll
-  for (int t = 0; t < 4; ++t)
+  for (int t = 0; t < RPW; ++t)
 #pragma unroll
     for (int c = 0; c < TC; ++c) acc[t][c] = (v4f){0.f, 0.f, 0.f, 0.f};
 
@@ -1012,7 +1019,7 @@ __global__ __launch_bounds__(64 * WV) void spense_gemm_big_kernel(GemmArgs a) {
   // offsets, so every step issues the same loads.
   auto prep = [&](int buf, int s) {
     BigStepLd p;
-    p.st = big_lds + buf * BigStage::BYTES;
+    p.st = big_lds + buf * St::BYTES;
     // wave-uniform (readfirstlane), so that the buffer resources chosen by them stay scalar
     p.in = __builtin_amdgcn_readfirstlane(s < nst ? 1 : 0) != 0;
     p.sparse = __builtin_amdgcn_readfirstlane(s < n_sp ? 1 : 0) != 0;
@@ -1049,7 +1056,7 @@ __global__ __launch_bounds__(64 * WV) void spense_gemm_big_kernel(GemmArgs a) {
           k = ok && p.ks + (p.sparse ? 32 : 16) * lq < p.ke;
         }
         __builtin_amdgcn_raw_ptr_buffer_load_lds(p.sparse ? rv : rd,
-                                                 (__attribute__((address_space(3))) void*)(p.st + BigStage::X_B + tile * 2048),
+                                                 (__attribute__((address_space(3))) void*)(p.st + St::X_B + tile * 2048),
                                                  16, sel(k, off), 0, 0, TL ? kTiledNT : kNT);
       } else if constexpr (kind == 1) {
         uint32_t off;
@@ -1062,7 +1069,7 @@ __global__ __launch_bounds__(64 * WV) void spense_gemm_big_kernel(GemmArgs a) {
           k = ok && p.ks + 64 + 16 * lq < p.ke;
         }
         __builtin_amdgcn_raw_ptr_buffer_load_lds(
-            rd, (__attribute__((address_space(3))) void*)(p.st + BigStage::X_B + tile * 2048 + 1024), 16,
+            rd, (__attribute__((address_space(3))) void*)(p.st + St::X_B + tile * 2048 + 1024), 16,
             sel(k && !p.sparse, off), 0, 0, TL ? kTiledNT : kNT);
       } else {
         uint32_t off;
@@ -1075,7 +1082,7 @@ __global__ __launch_bounds__(64 * WV) void spense_gemm_big_kernel(GemmArgs a) {
           k = ok && p.ks + 32 * lq < p.ke;
         }
         __builtin_amdgcn_raw_ptr_buffer_load_lds(
-            rm, (__attribute__((address_space(3))) void*)(p.st + BigStage::X_B + BigStage::W_B + tile * 256), 4,
+            rm, (__attribute__((address_space(3))) void*)(p.st + St::X_B + St::W_B + tile * 256), 4,
             sel(k && p.sparse, off), 0, 0, TL ? kTiledNT : kNT);
       }
     }
@@ -1088,17 +1095,17 @@ __global__ __launch_bounds__(64 * WV) void spense_gemm_big_kernel(GemmArgs a) {
   constexpr int PER = (NL + TC - 1) / TC;
   auto mma = [&](auto sparse_const, const uint8_t* st, const BigStepLd& ld) {
     constexpr bool SPARSE = decltype(sparse_const)::value;
-    const uint8_t* wl = st + BigStage::X_B + (4 * wr) * 2048 + 16 * lane;
-    const int* ml = reinterpret_cast<const int*>(st + BigStage::X_B + BigStage::W_B + (4 * wr) * 256) + lane;
+    const uint8_t* wl = st + St::X_B + (RPW * wr) * 2048 + 16 * lane;
+    const int* ml = reinterpret_cast<const int*>(st + St::X_B + St::W_B + (RPW * wr) * 256) + lane;
     auto bfrag = [&](int c) {
       const int r = 16 * (TC * wc + c) + li;
-      return cat8(*reinterpret_cast<const v4i*>(st + BigStage::xaddr(r, lq)),
-                  *reinterpret_cast<const v4i*>(st + BigStage::xaddr(r, 4 + lq)));
+      return cat8(*reinterpret_cast<const v4i*>(st + St::xaddr(r, lq)),
+                  *reinterpret_cast<const v4i*>(st + St::xaddr(r, 4 + lq)));
     };
-    v8i w[4];
-    int ix[4];
+    v8i w[RPW];
+    int ix[RPW];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
+    for (int t = 0; t < RPW; ++t) {
       const v4i lo = *reinterpret_cast<const v4i*>(wl + t * 2048);
       if constexpr (SPARSE) {
         w[t] = cat8(lo, lo);
@@ -1112,7 +1119,7 @@ __global__ __launch_bounds__(64 * WV) void spense_gemm_big_kernel(GemmArgs a) {
       constexpr int c = decltype(c_const)::value;
       const v8i bn = bfrag(c < TC - 1 ? c + 1 : TC - 1);
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
+      for (int t = 0; t < RPW; ++t) {
         if constexpr (SPARSE)
           acc[t][c] = mma_sparse(lo4(w[t]), b, acc[t][c], ix[t], std::integral_constant<int, kFP8>());
         else
@@ -1140,7 +1147,7 @@ __global__ __launch_bounds__(64 * WV) void spense_gemm_big_kernel(GemmArgs a) {
   int s = 0, cur = 0;  // cur = s % NS
   auto step = [&](auto sparse_const) {
     const int nxt = cur == 0 ? D : cur - 1;  // (s + D) % NS
-    mma(sparse_const, big_lds + cur * BigStage::BYTES, prep(nxt, s + D));
+    mma(sparse_const, big_lds + cur * St::BYTES, prep(nxt, s + D));
     __builtin_amdgcn_sched_barrier(0);
     barrier_vm<(D - 1) * NL>();
     ++s;
@@ -1151,33 +1158,35 @@ __global__ __launch_bounds__(64 * WV) void spense_gemm_big_kernel(GemmArgs a) {
 
   xdl_fence();
 #pragma unroll
-  for (int t = 0; t < 4; ++t)
+  for (int t = 0; t < RPW; ++t)
 #pragma unroll
     for (int c = 0; c < TC; ++c) {
       const int m = m0 + 16 * (TC * wc + c) + li;
-      const int n0 = rblk + 16 * (4 * wr + t) + 4 * lq;
+      const int n0 = rblk + 16 * (RPW * wr + t) + 4 * lq;
       if (m < a.M && n0 < rowend) store4(a, acc[t][c], m, n0, rowend);
     }
 }
 
-constexpr int kBigLds = 3 * BigStage::BYTES;
-
-template <int WV>
+template <int WV, int RPW>
 hipError_t launch_big_wv(const GemmArgs& a, hipStream_t s) {
-  static_assert(kBigLds <= 160 * 1024, "LDS of a CU");
-  auto k = a.tiled ? spense_gemm_big_kernel<true, WV> : spense_gemm_big_kernel<false, WV>;
+  typedef BigStage<2 * RPW> St;
+  constexpr int lds = St::NS * St::BYTES;
+  static_assert(lds <= 160 * 1024, "LDS of a CU");
+  auto k = a.tiled ? spense_gemm_big_kernel<true, WV, RPW> : spense_gemm_big_kernel<false, WV, RPW>;
   static bool attr_set[2] = {false, false};
   if (!attr_set[a.tiled]) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize, kBigLds);
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     if (e != hipSuccess) return e;
     attr_set[a.tiled] = true;
   }
-  hipLaunchKernelGGL(k, dim3(a.groups), dim3(64 * WV), kBigLds, s, a);
+  hipLaunchKernelGGL(k, dim3(a.groups), dim3(64 * WV), lds, s, a);
   return hipGetLastError();
 }
 
+// ls.rt: row tiles per wave (4 or 8; 8 only with 4 waves)
 hipError_t launch_big(const LaunchShape& ls, const GemmArgs& a, hipStream_t s) {
-  return ls.waves == 4 ? launch_big_wv<4>(a, s) : launch_big_wv<8>(a, s);
+  if (ls.rt == 8) return ls.waves == 4 ? launch_big_wv<4, 8>(a, s) : hipErrorInvalidValue;
+  return ls.waves == 4 ? launch_big_wv<4, 4>(a, s) : launch_big_wv<8, 4>(a, s);
 }
 
 template <int DT>
