@@ -226,6 +226,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--skip-cpu", action="store_true", help="omit the CPU oracle baseline")
     ap.add_argument("--only-main", action="store_true", help="time only the M=64 Spense GEMM (for profiling)")
+    ap.add_argument("--profile-m", type=int, default=0, metavar="M",
+                    help="time only the Spense GEMM at this M and print its timing (for profiling)")
     ap.add_argument("--eager", action="store_true", help="launch steps one by one instead of one graph")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MiB",
                     help="run only a torch device copy of this size (rocprof counter calibration)")
@@ -285,7 +287,7 @@ def main():
 
     results = {}
     ws = S.Workspace("cuda")
-    ms_list = [M_MAIN] if args.only_main else M_SWEEP
+    ms_list = [args.profile_m] if args.profile_m else ([M_MAIN] if args.only_main else M_SWEEP)
     for M in ms_list:
         X, sx = gen.make_x(2, 0, M, K, gen.FP8, "normal")
         Xd, sxd = torch.from_numpy(X).cuda(), torch.from_numpy(sx).cuda()
@@ -299,7 +301,7 @@ def main():
         b = alg_bytes_spense(M, N, K, n_sp, n_de)
         res["alg_bytes"] = int(b)
         res["gbs"] = round(b / (step_ms * 1e-3) / 1e9, 1)
-        if not args.only_main:
+        if not args.only_main and not args.profile_m:
             Yd = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
 
             def run_de(i):
@@ -318,6 +320,9 @@ def main():
         results[M] = res
         log(f"[bench] M={M}: {res}")
 
+    if args.profile_m:
+        print(json.dumps({"profile_m": args.profile_m, **results[args.profile_m]}))
+        return
     extras = {}
     if not args.only_main and not args.skip_extras:
         extras = measure_extras(args, torch, gen, S, ws, pws, copies, swd, mx, dws, dense_copies, results)
