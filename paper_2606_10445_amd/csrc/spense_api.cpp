@@ -309,13 +309,8 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
   const int ebig = env_int("SPENSE_BIG", -1);  // testing knob: force the large-M kernel on or off
   if (ebig >= 0) big = (ebig && dtype == SPENSE_FP8_E4M3FN) ? 1 : 0;
   pl->ls.big = big;
-  int big_rows = 128;  // rows of a large-M workgroup tile
-  if (big) {
-    // testing knobs: waves of a workgroup and row tiles of a wave (8 only with 4 waves)
-    pl->ls.waves = env_int("SPENSE_BIG_WAVES", 8) == 4 ? 4 : 8;
-    pl->ls.rt = (env_int("SPENSE_BIG_RPW", 4) == 8 && pl->ls.waves == 4) ? 8 : 4;
-    big_rows = 32 * pl->ls.rt;
-  }
+  const int big_rows = 128;  // rows of a large-M workgroup tile
+  if (big) pl->ls.waves = env_int("SPENSE_BIG_WAVES", 8) == 4 ? 4 : 8;  // testing knob
   const int64_t tblocks = ceil_div(M, 256);
 
   Region regs[2];

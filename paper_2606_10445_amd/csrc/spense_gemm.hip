@@ -673,6 +673,14 @@ __device__ __forceinline__ void barrier_vm() {
   asm volatile("s_barrier" ::: "memory");
 }
 
+// As barrier_vm, and also wait for this wave's LDS accesses (lgkmcnt(0)).
+template <int N>
+__device__ __forceinline__ void barrier_vm_lgkm0() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (0 << 8));
+  asm volatile("s_barrier" ::: "memory");
+}
+
 // Pipeline with NS register slots and NS LDS buffers, D = NS-1 chunks ahead (per wave,
 // in issue order within chunk step c): activations of chunk c+D -> LDS buffer
 // (c+D) % NS, weights of chunk c+D -> register slot (c+D) % NS, MMAs of chunk c (buffer
@@ -913,29 +921,25 @@ hipError_t launch_rows_ct(const LaunchShape& ls, const GemmArgs& a, hipStream_t 
 
 // ---------------------------------------------------------------- large-M kernel
 // For many tokens the matrix cores become the bound, and every byte moved should feed
-// many MMAs.  A workgroup computes 32 RPW weight rows x 256 tokens; its waves form a grid
-// of 2 row halves x 2 or 4 token parts, each wave 16 RPW rows (RPW row tiles) x 128 or 64
-// tokens (with 8 waves, two per SIMD, one wave's LDS waits are covered by the other's
-// MMAs).  RPW = 4: 128-row workgroups; RPW = 8 with 4 waves: 256 x 256 tiles, 64 MMAs of
-// a wave per step and 256 accumulators in the matrix-core registers, which halves the
-// bytes each MMA moves through the CU's load path.  Both operands of a step are copied once into LDS by
-// direct loads (activations 256 x 128 bytes, with 16-byte blocks swizzled so that the
-// fragment reads of 16 rows are conflict-free; the weight fragments of the 8 row tiles
-// in lane order), three stages deep, so that two steps of loads are in flight without
-// holding registers.  Each B fragment read feeds 4 MMAs, each A fragment 8 or 4.  Workgroups
-// of one row block are adjacent (token block fastest), so with 8 token blocks each XCD
-// keeps one activation block in its L2.  fp8 only.
-constexpr int kBigTokens = 256;
+// many MMAs.  A workgroup computes 128 weight rows x 256 tokens; its waves form a grid of
+// 2 row halves x 2 or 4 token parts, each wave 64 rows (4 row tiles) x 128 or 64 tokens
+// (with 8 waves, two per SIMD, one wave's stalls are covered by the other's MMAs).  Both
+// operands of a step (128 columns) are copied once into LDS by direct loads
+// (activations 256 x 128 bytes, with 16-byte blocks swizzled so that the fragment reads
+// of 16 rows are conflict-free; the weight fragments of the 8 row tiles in lane order),
+// three stages deep, so that two steps of loads are in flight without holding
+// registers.  Each B fragment read feeds 4 MMAs, each A fragment 4 or 8.  The barrier of
+// a step sits before its last MMA group, and the fragments of the next step are read
+// from LDS right after it, under that group, so that no wave starts a step waiting for
+// LDS.  Workgroups of one row block are adjacent (token block fastest), so with 8 token
+// blocks each XCD keeps one activation block in its L2.  fp8 only.
+constexpr int kBigTokens = 256, kBigRowTiles = 8;
 
-__device__ __forceinline__ v4i lo4(v8i v) { return (v4i){v[0], v[1], v[2], v[3]}; }
-
-template <int NT>  // row tiles of a workgroup
 struct BigStage {
-  static constexpr int X_B = kBigTokens * 128;  // activations: 256 tokens x 128 bytes
-  static constexpr int W_B = NT * 2048;         // per row tile: 2:4 values or dense halves
-  static constexpr int M_B = NT * 256;          // per row tile: metadata words
+  static constexpr int X_B = kBigTokens * 128;       // activations: 256 tokens x 128 bytes
+  static constexpr int W_B = kBigRowTiles * 2048;    // per row tile: 2:4 values or dense halves
+  static constexpr int M_B = kBigRowTiles * 256;     // per row tile: metadata words
   static constexpr int BYTES = X_B + W_B + M_B;
-  static constexpr int NS = 3 * BYTES <= 160 * 1024 ? 3 : 2;  // stages that fit in LDS
   __device__ static __forceinline__ int xaddr(int r, int b) { return r * 128 + ((b ^ ((r >> 1) & 7)) << 4); }
 };
 
@@ -956,17 +960,21 @@ struct BigStepLd {
   bool in, sparse;
 };
 
-template <bool TL, int WV, int RPW>
+// Step kinds for the fragment reads of the next step.
+constexpr int kStepSparse = 0, kStepDense = 1, kStepNone = 2;
+
+template <bool TL, int WV>
 __global__ __launch_bounds__(64 * WV) void spense_gemm_big_kernel(GemmArgs a) {
   static_assert(WV == 4 || WV == 8, "4 or 8 waves");
-  constexpr int NT = 2 * RPW;                 // row tiles of the workgroup
-  typedef BigStage<NT> St;
-  constexpr int NS = St::NS, D = NS - 1;
+  constexpr int RPW = 4, NT = kBigRowTiles;
+  typedef BigStage St;
+  constexpr int NS = 3, D = NS - 1;
   constexpr int TC = 32 / WV;                    // token tiles per wave
   constexpr int TU = NT / WV;                    // row tiles whose weights a wave copies
-  static_assert(TU >= 1 && TU * WV == NT, "weight copies split evenly");
-  constexpr int XI = St::X_B / 1024 / WV;  // 1 KB activation blocks per wave per step
+  constexpr int XI = St::X_B / 1024 / WV;        // 1 KB activation blocks per wave per step
   constexpr int NL = XI + 3 * TU;                // loads per wave per step
+  constexpr int PER = (NL + TC - 1) / TC;        // loads issued after each MMA group
+  constexpr int NL_AT_BAR = (TC - 1) * PER < NL ? (TC - 1) * PER : NL;  // issued before the barrier
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int li = lane & 15, lq = lane >> 4;
   const int wr = wave & 1, wc = wave >> 1;
@@ -991,7 +999,7 @@ __global__ __launch_bounds__(64 * WV) void spense_gemm_big_kernel(GemmArgs a) {
   // steps of 128 columns: 2:4 steps cover [0, kbound), dense steps start at kbound
   const int n_sp = (kbound + 127) / 128, n_de = (K - kbound + 127) / 128, nst = n_sp + n_de;
   const int nch_sp = (n_sp + 3) / 4, nch_de = (n_de + 3) / 4;  // tiled layout chunks
-  auto step_k = [&](int s) { return s < n_sp ? 128 * s : kbound + 128 * (s - n_sp); };
+  auto step_k = [&](int s) __attribute__((always_inline)) { return s < n_sp ? 128 * s : kbound + 128 * (s - n_sp); };
 
   // This wave copies the weights of row tiles TU wave .. TU wave + TU - 1.
   bool tok[TU];
@@ -1017,7 +1025,7 @@ __global__ __launch_bounds__(64 * WV) void spense_gemm_big_kernel(GemmArgs a) {
   // for each of the wave's row tiles the value (or first dense) fragment, the second
   // dense fragment and the metadata word.  The ones a step does not use get out-of-range
   // offsets, so every step issues the same loads.
-  auto prep = [&](int buf, int s) {
+  auto prep = [&](int buf, int s) __attribute__((always_inline)) {
     BigStepLd p;
     p.st = big_lds + buf * St::BYTES;
     // wave-uniform (readfirstlane), so that the buffer resources chosen by them stay scalar
@@ -1032,7 +1040,7 @@ __global__ __launch_bounds__(64 * WV) void spense_gemm_big_kernel(GemmArgs a) {
     p.jd = sd & 3;
     return p;
   };
-  auto load_one = [&](auto i_const, const BigStepLd& p) {
+  auto load_one = [&](auto i_const, const BigStepLd& p) __attribute__((always_inline)) {
     constexpr int i = decltype(i_const)::value;
     if constexpr (i < XI) {
       const int blk = wave * XI + i;
@@ -1088,73 +1096,120 @@ __global__ __launch_bounds__(64 * WV) void spense_gemm_big_kernel(GemmArgs a) {
     }
   };
 
-  // MMAs of one step: the A fragments of the wave's 4 row tiles, then per token tile its
-  // B fragment (read one tile ahead) and 4 MMAs, each group followed by PER of the loads
-  // of a later step.  A load instruction waits at issue until the CU's address unit takes
-  // it, so spreading them between the MMAs keeps the matrix core busy meanwhile.
-  constexpr int PER = (NL + TC - 1) / TC;
-  auto mma = [&](auto sparse_const, const uint8_t* st, const BigStepLd& ld) {
-    constexpr bool SPARSE = decltype(sparse_const)::value;
+  // Fragments.  A of the wave's 4 row tiles (2:4: value fragment and metadata word; dense:
+  // both halves) in two sets that alternate between steps (set P holds the current step's,
+  // the other receives the next step's); B, one register per token tile (the next step's
+  // first two land in registers the current step's last group no longer reads).
+  static_assert(TC >= 3, "the last group must not use B registers 0 and 1");
+  v4i alo[2][RPW], ahi[2][RPW];
+  int aix[2][RPW];
+  v8i bq[TC];
+  auto bfrag = [&](const uint8_t* st, int c) __attribute__((always_inline)) {
+    const int r = 16 * (TC * wc + c) + li;
+    return cat8(*reinterpret_cast<const v4i*>(st + St::xaddr(r, lq)),
+                *reinterpret_cast<const v4i*>(st + St::xaddr(r, 4 + lq)));
+  };
+  auto read_a = [&](auto kind_const, auto set_const, const uint8_t* st) __attribute__((always_inline)) {
+    constexpr int KIND = decltype(kind_const)::value, Q = decltype(set_const)::value;
     const uint8_t* wl = st + St::X_B + (RPW * wr) * 2048 + 16 * lane;
     const int* ml = reinterpret_cast<const int*>(st + St::X_B + St::W_B + (RPW * wr) * 256) + lane;
-    auto bfrag = [&](int c) {
-      const int r = 16 * (TC * wc + c) + li;
-      return cat8(*reinterpret_cast<const v4i*>(st + St::xaddr(r, lq)),
-                  *reinterpret_cast<const v4i*>(st + St::xaddr(r, 4 + lq)));
-    };
-    v8i w[RPW];
-    int ix[RPW];
 #pragma unroll
     for (int t = 0; t < RPW; ++t) {
-      const v4i lo = *reinterpret_cast<const v4i*>(wl + t * 2048);
-      if constexpr (SPARSE) {
-        w[t] = cat8(lo, lo);
-        ix[t] = ml[t * 64];
-      } else {
-        w[t] = cat8(lo, *reinterpret_cast<const v4i*>(wl + t * 2048 + 1024));
-      }
+      alo[Q][t] = *reinterpret_cast<const v4i*>(wl + t * 2048);
+      if constexpr (KIND == kStepSparse) aix[Q][t] = ml[t * 64];
+      if constexpr (KIND == kStepDense) ahi[Q][t] = *reinterpret_cast<const v4i*>(wl + t * 2048 + 1024);
     }
-    v8i b = bfrag(0);
+    bq[0] = bfrag(st, 0);
+    bq[1] = bfrag(st, 1);
+  };
+
+  // One step: MMA group c uses B fragment c; fragment c + 2 is read before it.  Before the
+  // last group: wait for this wave's reads of the stage and for its loads of step s + 1
+  // (the loads of step s + D issued so far are younger), meet the other waves, and read the
+  // first fragments of step s + 1 into the other set, under the last group.  The loads of
+  // step s + D into stage (s + D) % NS (it held step s - 1, which every wave had finished
+  // reading at the previous barrier) follow the MMA groups, PER at a time.
+  int s = 0, cur = 0;  // cur = s % NS
+  auto step = [&](auto kind_const, auto next_const, auto set_const) __attribute__((always_inline)) {
+    constexpr bool SPARSE = decltype(kind_const)::value == kStepSparse;
+    constexpr int NEXT = decltype(next_const)::value, P = decltype(set_const)::value;
+    const int nxt = cur == 0 ? D : cur - 1;  // (s + D) % NS
+    const int nx1 = cur == NS - 1 ? 0 : cur + 1;
+    const uint8_t* st = big_lds + cur * St::BYTES;
+    const BigStepLd ld = prep(nxt, s + D);
     static_for<TC>([&](auto c_const) {
       constexpr int c = decltype(c_const)::value;
-      const v8i bn = bfrag(c < TC - 1 ? c + 1 : TC - 1);
+      if constexpr (c == TC - 1) {
+        barrier_vm_lgkm0<NL_AT_BAR>();
+        if constexpr (NEXT != kStepNone)
+          read_a(std::integral_constant<int, NEXT>(), std::integral_constant<int, 1 - P>(), big_lds + nx1 * St::BYTES);
+      } else if constexpr (c + 2 < TC) {
+        bq[c + 2] = bfrag(st, c + 2);
+      }
 #pragma unroll
       for (int t = 0; t < RPW; ++t) {
         if constexpr (SPARSE)
-          acc[t][c] = mma_sparse(lo4(w[t]), b, acc[t][c], ix[t], std::integral_constant<int, kFP8>());
+          acc[t][c] = mma_sparse(alo[P][t], bq[c], acc[t][c], aix[P][t], std::integral_constant<int, kFP8>());
         else
-          acc[t][c] = mma_dense(w[t], b, acc[t][c], std::integral_constant<int, kFP8>());
+          acc[t][c] = mma_dense(cat8(alo[P][t], ahi[P][t]), bq[c], acc[t][c], std::integral_constant<int, kFP8>());
       }
       static_for<PER>([&](auto j_const) {
         constexpr int i = c * PER + decltype(j_const)::value;
         if constexpr (i < NL) load_one(std::integral_constant<int, i>(), ld);
       });
       __builtin_amdgcn_sched_barrier(0);
-      b = bn;
     });
+    ++s;
+    cur = nx1;
+  };
+  const std::integral_constant<int, 0> S0;
+  const std::integral_constant<int, 1> S1;
+  // Steps [s, e) of one kind, entered with the current fragments in set 0 and left with
+  // the next part's first fragments (kind NEXT) in set 0.
+  auto part = [&](auto kind_const, auto next_const, int e) __attribute__((always_inline)) {
+    while (s + 2 < e) {
+      step(kind_const, kind_const, S0);
+      step(kind_const, kind_const, S1);
+    }
+    if (s + 2 == e) {
+      step(kind_const, kind_const, S0);
+      step(kind_const, next_const, S1);
+    } else {
+      step(kind_const, next_const, S0);
+      if constexpr (decltype(next_const)::value != kStepNone) {
+#pragma unroll
+        for (int t = 0; t < RPW; ++t) {
+          alo[0][t] = alo[1][t];
+          ahi[0][t] = ahi[1][t];
+          aix[0][t] = aix[1][t];
+        }
+      }
+    }
   };
 
-  // Pipeline: step s issues the loads of step s + D into stage (s + D) % NS (it held step
-  // s - 1, which every wave has finished), runs the MMAs of step s, then waits for its own
-  // loads of step s + 1 (only step s + D's are younger) and meets the other waves.  The
-  // 2:4 steps and the dense steps are separate loops, so each loop body is one block.
+  // Prologue: loads of steps 0 .. D-1, then the first fragments of step 0.
 #pragma unroll
   for (int d = 0; d < D; ++d) {
     const BigStepLd p = prep(d, d);
     static_for<NL>([&](auto i_const) { load_one(i_const, p); });
   }
-  barrier_vm<0>();
-  int s = 0, cur = 0;  // cur = s % NS
-  auto step = [&](auto sparse_const) {
-    const int nxt = cur == 0 ? D : cur - 1;  // (s + D) % NS
-    mma(sparse_const, big_lds + cur * St::BYTES, prep(nxt, s + D));
-    __builtin_amdgcn_sched_barrier(0);
-    barrier_vm<(D - 1) * NL>();
-    ++s;
-    cur = cur == NS - 1 ? 0 : cur + 1;
-  };
-  while (s < n_sp) step(std::true_type());
-  while (s < nst) step(std::false_type());
+  barrier_vm<NL>();  // step 0 is in LDS (only step 1's loads may be outstanding)
+  const std::integral_constant<int, kStepSparse> SP;
+  const std::integral_constant<int, kStepDense> DE;
+  const std::integral_constant<int, kStepNone> NO;
+  if (n_sp > 0)
+    read_a(SP, S0, big_lds);
+  else
+    read_a(DE, S0, big_lds);
+
+  // 2:4 steps, then dense steps.
+  if (n_sp > 0) {
+    if (n_de > 0)
+      part(SP, DE, n_sp);
+    else
+      part(SP, NO, n_sp);
+  }
+  if (n_de > 0) part(DE, NO, nst);
 
   xdl_fence();
 #pragma unroll
@@ -1167,12 +1222,11 @@ __global__ __launch_bounds__(64 * WV) void spense_gemm_big_kernel(GemmArgs a) {
     }
 }
 
-template <int WV, int RPW>
+template <int WV>
 hipError_t launch_big_wv(const GemmArgs& a, hipStream_t s) {
-  typedef BigStage<2 * RPW> St;
-  constexpr int lds = St::NS * St::BYTES;
+  constexpr int lds = 3 * BigStage::BYTES;
   static_assert(lds <= 160 * 1024, "LDS of a CU");
-  auto k = a.tiled ? spense_gemm_big_kernel<true, WV, RPW> : spense_gemm_big_kernel<false, WV, RPW>;
+  auto k = a.tiled ? spense_gemm_big_kernel<true, WV> : spense_gemm_big_kernel<false, WV>;
   static bool attr_set[2] = {false, false};
   if (!attr_set[a.tiled]) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize, lds);
@@ -1183,10 +1237,8 @@ hipError_t launch_big_wv(const GemmArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-// ls.rt: row tiles per wave (4 or 8; 8 only with 4 waves)
 hipError_t launch_big(const LaunchShape& ls, const GemmArgs& a, hipStream_t s) {
-  if (ls.rt == 8) return ls.waves == 4 ? launch_big_wv<4, 8>(a, s) : hipErrorInvalidValue;
-  return ls.waves == 4 ? launch_big_wv<4, 4>(a, s) : launch_big_wv<8, 4>(a, s);
+  return ls.waves == 4 ? launch_big_wv<4>(a, s) : launch_big_wv<8>(a, s);
 }
 
 template <int DT>

@@ -380,26 +380,25 @@ BIG_CASES = [  # axis, M, N, K, dense_begin: ragged tokens, rows and columns aro
     (0, 600, 136, 384, 0), (0, 300, 136, 384, 136), (1, 300, 64, 512, 0), (1, 300, 64, 512, 512)]
 
 
-@pytest.mark.parametrize("waves,rpw", [(4, 4), (8, 4), (4, 8)])
+@pytest.mark.parametrize("waves", [4, 8])
 @pytest.mark.parametrize("axis,M,N,K,db", BIG_CASES)
-def test_large_m_kernel_exact_both_layouts(S, axis, M, N, K, db, waves, rpw, monkeypatch):
-    """The large-M kernel (128 x 256 tiles with 4 or 8 waves, 256 x 256 tiles with 4),
-    forced on at any M, on exact-integer data: bit-exact against the oracle with the
-    row-major and the tiled weight."""
+def test_large_m_kernel_exact_both_layouts(S, axis, M, N, K, db, waves, monkeypatch):
+    """The large-M kernel (128-row x 256-token tiles, 4 or 8 waves), forced on at any M, on
+    exact-integer data: bit-exact against the oracle with the row-major and the tiled
+    weight."""
     W, mask, X, sw, sx = gen.make_exact_int(13, M + N, M, N, K, gaxis(axis), db, gen.FP8)
     pw, (v, m, d) = compress_both(S, W, mask, FP8, axis, db)
     ref = oracle.spense_gemm(X, v, m, d, N, K, FP8, axis, db, sw, sx)
     monkeypatch.setenv("SPENSE_BIG", "1")
     monkeypatch.setenv("SPENSE_BIG_WAVES", str(waves))
-    monkeypatch.setenv("SPENSE_BIG_RPW", str(rpw))
     for w in (pw, S.tile(pw)):
         assert np.array_equal(run_gemm(S, w, X, sw, sx, True), ref["y_f32"])
         assert np.array_equal(run_gemm(S, w, X, sw, sx, False).view(np.uint16), ref["y_bf16"])
 
 
-@pytest.mark.parametrize("rpw", [4, 8])
+@pytest.mark.parametrize("waves", [4, 8])
 @pytest.mark.parametrize("axis,db", [(0, 744), (1, 1536)])
-def test_large_m_kernel_random_within_bound(S, axis, db, rpw, monkeypatch):
+def test_large_m_kernel_random_within_bound(S, axis, db, waves, monkeypatch):
     """Random data through the large-M kernel: inside the error bound against the oracle,
     equal with both layouts and bitwise repeatable."""
     M, N, K = 520, 1000, 2080
@@ -409,8 +408,7 @@ def test_large_m_kernel_random_within_bound(S, axis, db, rpw, monkeypatch):
     Wd = oracle.decompress(v, m, d, N, K, FP8, axis, db)
     pwt = S.tile(pw)
     monkeypatch.setenv("SPENSE_BIG", "1")
-    monkeypatch.setenv("SPENSE_BIG_RPW", str(rpw))
-    monkeypatch.setenv("SPENSE_BIG_WAVES", "4" if rpw == 8 else "8")
+    monkeypatch.setenv("SPENSE_BIG_WAVES", str(waves))
     y32 = run_gemm(S, pw, X, sw, sx, True)
     assert_f32_bound(y32, X, Wd, FP8, sw, sx)
     assert_bf16_close(run_gemm(S, pw, X, sw, sx, False).view(np.uint16), ref["y_bf16"], FP8)
