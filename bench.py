@@ -161,6 +161,18 @@ def measure_extras(args, torch, gen, S, ws, pws, copies, swd, mx, dws, dense_cop
     ex["us_per_gemm_eager"] = round(time_launches(lambda i: S.gemm(Xd, pws[i % copies], swd, sxd, out=Y, workspace=ws),
                                                   200, 20, torch) * 1e3, 3)
     EAGER = prev
+    # distribution over 200 eager launches, each between two HIP events on the stream
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(201)]
+    stream = torch.cuda.current_stream()
+    for i in range(20):
+        S.gemm(Xd, pws[i % copies], swd, sxd, out=Y, workspace=ws)
+    evs[0].record(stream)
+    for i in range(200):
+        S.gemm(Xd, pws[i % copies], swd, sxd, out=Y, workspace=ws)
+        evs[i + 1].record(stream)
+    torch.cuda.synchronize()
+    per = sorted(evs[i].elapsed_time(evs[i + 1]) * 1e3 for i in range(200))
+    ex["per_launch_us"] = {"p10": round(per[20], 2), "median": round(per[100], 2), "p90": round(per[180], 2)}
     # compute-bound point: M = 2048 on the same weight
     Mb = 2048
     Xb, sxb = gen.make_x(2, 0, Mb, K, gen.FP8, "normal")
