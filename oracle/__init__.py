@@ -11,7 +11,9 @@ sec. 3.2, and the dense region being the last one in sec. 3.3.2 and Table "front
 
 Parity status: every function here is pinned by tests that do not re-use it (format
 definition vs torch's converters, brute force over all 2:4 masks, numpy fp64 matmul
-within the Higham bound, exact-integer cases, linearity of the two split variants).
+within the Higham bound, exact-integer cases, linearity of the two split variants; for
+the GLU-MLP steps: every e4m3fn code's round trip and midpoint, torch's converter, the
+odd and even parts of SiLU, and the permutation invariance of Eq. (4)).
 """
 from __future__ import annotations
 
@@ -69,6 +71,11 @@ def _L():
         lib.or_gemm_f32.argtypes = [p, p, i64, i64, i64, i32, p, p, p, p, p]
         lib.or_gemm_f64.restype = i32
         lib.or_gemm_f64.argtypes = [p, p, i64, i64, i64, i32, p, p, p, p, p]
+        lib.or_encode_e4m3fn.restype = ctypes.c_uint8
+        lib.or_encode_e4m3fn.argtypes = [ctypes.c_float]
+        lib.or_encode_e4m3fn_array.argtypes = [p, i64, p]
+        lib.or_quantize_rows.argtypes = [p, i64, i64, i64, p, p]
+        lib.or_glu_f64.argtypes = [p, p, i64, p]
         _lib = lib
     return _lib
 
@@ -200,3 +207,55 @@ def spense_gemm(X, values, meta, dense, N: int, K: int, dtype: int, axis: int, d
     """The whole layer from the packed format: decompress, then the plain GEMM."""
     W = decompress(values, meta, dense, N, K, dtype, axis, dense_begin)
     return gemm(X, W, dtype, sw, sx)
+
+
+# ------------------------------------------------------------------ activation quantisation
+def encode_e4m3fn(x) -> np.ndarray:
+    """fp32 values -> e4m3fn codes: nearest, ties to an even mantissa, saturating to
+    +-448 (the definition the GLU-MLP steps use; sec. 3.3.1, Eq. (4))."""
+    f = np.ascontiguousarray(x, dtype=np.float32)
+    out = np.empty(f.shape, np.uint8)
+    _L().or_encode_e4m3fn_array(_ptr(f), f.size, _ptr(out))
+    return out
+
+
+def quantize_rows(a):
+    """Per-token fp8 quantisation of an M x K fp32 matrix: scale = absmax / 448 (1.0 for a
+    zero row) and codes = e4m3fn(a / scale), all in fp32.  Returns (codes, scales)."""
+    f = np.ascontiguousarray(a, dtype=np.float32)
+    M, K = f.shape
+    q = np.empty((M, K), np.uint8)
+    s = np.empty(M, np.float32)
+    _L().or_quantize_rows(_ptr(f), M, K, K, _ptr(q), _ptr(s))
+    return q, s
+
+
+def glu_f64(g, u) -> np.ndarray:
+    """h = u * silu(g) = u * g / (1 + exp(-g)) in fp64 (the GLU of the MLP, sec. 3.3.1
+    Eq. (4), with sigma read as SiLU)."""
+    ga = np.ascontiguousarray(g, dtype=np.float64)
+    ua = np.ascontiguousarray(u, dtype=np.float64)
+    if ga.shape != ua.shape:
+        raise ValueError("g and u differ in shape")
+    h = np.empty(ga.shape, np.float64)
+    _L().or_glu_f64(_ptr(ga), _ptr(ua), ga.size, _ptr(h))
+    return h
+
+
+def mlp(X, sx, gate, up, down, dtype=FP8):
+    """The GLU MLP of sec. 3.3.1 Eq. (4) through the Spense format, step by step:
+    G = gate(X), U = up(X) (output-split GEMMs), H = U * silu(G), (Hq, sh) = per-token fp8
+    quantisation of H (from the fp32 rounding of the fp64 H), Y = down(Hq) (input-split).
+    gate / up / down are (values, meta, dense, N, K, axis, dense_begin, sw) tuples.
+    Returns a dict with the intermediate results."""
+    def run(Xq, s, w, out_f64=False):
+        v, m, d, N, K, axis, db, sw = w
+        Wd = decompress(v, m, d, N, K, dtype, axis, db)
+        return gemm_f64(Xq, Wd, dtype, sw, s)["y"] if out_f64 else gemm(Xq, Wd, dtype, sw, s)["y_f32"]
+    G = run(X, sx, gate, True)
+    U = run(X, sx, up, True)
+    H = glu_f64(G, U)
+    Hq, sh = quantize_rows(H.astype(np.float32))
+    Y = run(Hq, sh, down)
+    return {"G": G, "U": U, "H": H, "Hq": Hq, "sh": sh, "Y": Y}
+

@@ -314,3 +314,60 @@ int or_gemm_f64(const void* X, const void* W, int64_t M, int64_t N, int64_t K, i
   free(xd);
   return 0;
 }
+
+/* ---------------------------------------------------------------- activation quantisation
+ *
+ * The steps on either side of the GEMMs in the GLU MLP the paper prunes (sec. 3.3.1,
+ * Eq. (4)): MLP(X) = ((X Wup^T) .* sigma(X Wgate^T)) Wdown^T, with Wgate / Wup
+ * output-split and Wdown input-split (sec. 3.2).  The activation function sigma is read
+ * as SiLU (x * sigmoid(x)), the SwiGLU of the Qwen3 and Seed-OSS models the paper
+ * evaluates.  Each GEMM consumes fp8 e4m3fn activations with one fp32 scale per token:
+ * s[m] = max_k |a[m,k]| / 448 (1.0 for an all-zero row) and q[m,k] = e4m3fn(a[m,k] / s[m]),
+ * both in fp32, the encode rounding to nearest-even and saturating to +-448.
+ */
+
+/* fp32 -> e4m3fn code from the format definition: round to nearest, ties to an even
+ * mantissa; magnitudes that round past 448 saturate to 448 (the format has no infinity;
+ * its all-ones pattern is NaN); NaN maps to 0x7F with the input's sign. */
+uint8_t or_encode_e4m3fn(float f) {
+  const uint8_t sign = signbit(f) ? 0x80 : 0x00;
+  if (isnan(f)) return (uint8_t)(sign | 0x7F);
+  double a = fabs((double)f);
+  if (a >= 464.0) return (uint8_t)(sign | 0x7E); /* 464 is halfway from 448 to 480 */
+  if (a < ldexp(1.0, -6)) {                      /* subnormal range: multiples of 2^-9 */
+    double q = nearbyint(a * 512.0);             /* exact scaling; rounds half to even */
+    return (uint8_t)(sign | (uint8_t)q);         /* q = 8 is the smallest normal, 0x08 */
+  }
+  int e = 0;
+  double fr = frexp(a, &e); /* a = fr * 2^e, fr in [0.5, 1) */
+  int ex = e - 1;           /* a = (1 + m) * 2^ex, m in [0, 1) */
+  double m = nearbyint((fr * 2.0 - 1.0) * 8.0);
+  if (m >= 8.0) {
+    m = 0.0;
+    ex += 1;
+  }
+  int code = ((ex + 7) << 3) | (int)m;
+  if (code > 0x7E) code = 0x7E;
+  return (uint8_t)(sign | code);
+}
+
+void or_encode_e4m3fn_array(const float* f, int64_t n, uint8_t* out) {
+  for (int64_t i = 0; i < n; ++i) out[i] = or_encode_e4m3fn(f[i]);
+}
+
+/* Per-token quantisation of an M x K fp32 matrix (row stride ld). */
+void or_quantize_rows(const float* a, int64_t M, int64_t K, int64_t ld, uint8_t* q, float* s) {
+  for (int64_t m = 0; m < M; ++m) {
+    const float* r = a + m * ld;
+    float amax = 0.0f;
+    for (int64_t k = 0; k < K; ++k) amax = fmaxf(amax, fabsf(r[k]));
+    const float sc = amax > 0.0f ? amax / 448.0f : 1.0f;
+    s[m] = sc;
+    for (int64_t k = 0; k < K; ++k) q[m * K + k] = or_encode_e4m3fn(r[k] / sc);
+  }
+}
+
+/* GLU: h = u * silu(g) = u * g / (1 + exp(-g)), in fp64. */
+void or_glu_f64(const double* g, const double* u, int64_t n, double* h) {
+  for (int64_t i = 0; i < n; ++i) h[i] = u[i] * (g[i] / (1.0 + exp(-g[i])));
+}

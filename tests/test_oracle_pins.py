@@ -401,3 +401,100 @@ def test_quantize_rows_fp8_scale_and_saturation():
     d = tdec(codes, oracle.FP8)
     assert np.all(np.abs(d).max(1)[[0, 1, 2, 4, 5, 6, 7]] == 448.0)
     assert not np.any(np.isnan(d))
+
+
+# ------------------------------------------------------------------ activation quantisation and GLU
+def _finite_codes():
+    return np.array([c for c in range(256) if c & 0x7F != 0x7F], np.uint8)
+
+
+def test_encode_e4m3fn_round_trips_every_finite_code():
+    c = _finite_codes()
+    v = tdec(c, oracle.FP8).astype(np.float32)
+    assert np.array_equal(oracle.encode_e4m3fn(v), c)  # -0 included (0x80)
+
+
+def test_encode_e4m3fn_ties_go_to_even_mantissa_and_neighbours_to_nearest():
+    pos = np.arange(0, 0x7F, dtype=np.uint8)  # 0 .. 448
+    v = tdec(pos, oracle.FP8)
+    mid = ((v[:-1] + v[1:]) / 2).astype(np.float32)  # dyadic, exact in fp32
+    assert np.array_equal(mid.astype(np.float64), (v[:-1] + v[1:]) / 2)
+    want = np.where(pos[:-1] % 2 == 0, pos[:-1], pos[1:])
+    assert np.array_equal(oracle.encode_e4m3fn(mid), want)
+    assert np.array_equal(oracle.encode_e4m3fn(-mid), want | 0x80)
+    below = np.nextafter(mid, np.float32(0))
+    above = np.nextafter(mid, np.float32(np.inf))
+    assert np.array_equal(oracle.encode_e4m3fn(below), pos[:-1])
+    assert np.array_equal(oracle.encode_e4m3fn(above), pos[1:])
+
+
+def test_encode_e4m3fn_saturates_and_keeps_nan():
+    big = np.array([448.0, 449.0, 463.99, 464.0, 480.0, 1e6, 3.4e38, np.inf], np.float32)
+    assert np.all(oracle.encode_e4m3fn(big) == 0x7E)
+    assert np.all(oracle.encode_e4m3fn(-big) == 0xFE)
+    assert oracle.encode_e4m3fn(np.array([np.nan], np.float32))[0] & 0x7F == 0x7F
+
+
+def test_encode_e4m3fn_matches_torch_in_range():
+    r = np.random.default_rng(21)
+    x = np.concatenate([r.uniform(-448, 448, 20000), r.standard_normal(20000) * 0.05,
+                        r.uniform(-2 ** -6, 2 ** -6, 5000)]).astype(np.float32)
+    want = torch.from_numpy(x).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    assert np.array_equal(oracle.encode_e4m3fn(x), want)
+
+
+def test_quantize_rows_matches_generator_and_its_invariants():
+    r = np.random.default_rng(22)
+    A = (r.standard_normal((12, 300)) * np.exp(r.uniform(-6, 6, (12, 1)))).astype(np.float32)
+    A[4] = 0
+    A[7, 5] = -A[7].__abs__().max() * 3  # a single dominant negative entry
+    q, s = oracle.quantize_rows(A)
+    gq, gs = gen.quantize_rows_fp8(A)  # torch's converter, independent of the oracle
+    assert np.array_equal(q, gq) and np.array_equal(s.view(np.uint32), gs.view(np.uint32))
+    d = tdec(q, oracle.FP8)
+    assert s[4] == 1.0 and np.all(q[4] == 0)
+    nz = [i for i in range(12) if i != 4]
+    assert np.all(np.abs(d[nz]).max(axis=1) == 448.0)
+    # every entry is within half a step of its code (relative 2^-4 for normals, 2^-10 * s
+    # absolute in the subnormal range)
+    err = np.abs(d * s[:, None].astype(np.float64) - A.astype(np.float64))
+    bound = np.maximum(2.0 ** -4 * np.abs(A), 2.0 ** -10 * s[:, None]) * (1 + 1e-6)
+    assert np.all(err <= bound)
+    # scaling a row by a power of two leaves the codes and scales the scale
+    q2, s2 = oracle.quantize_rows(A * np.float32(2.0 ** 5))
+    assert np.array_equal(q2, q) and np.array_equal(s2[nz], s[nz] * np.float32(32.0))
+
+
+def test_glu_silu_odd_and_even_parts_and_linearity():
+    g = np.linspace(-30, 30, 4001)
+    one = np.ones_like(g)
+    h = oracle.glu_f64(g, one)
+    hn = oracle.glu_f64(-g, one)
+    assert np.allclose(h - hn, g, rtol=0, atol=1e-13)  # silu(x) - silu(-x) = x
+    assert np.allclose(h + hn, g * np.tanh(g / 2), rtol=1e-13, atol=1e-300)  # = x tanh(x/2)
+    u = np.random.default_rng(23).standard_normal(g.size)
+    assert np.array_equal(oracle.glu_f64(g, 2 * u), 2 * oracle.glu_f64(g, u))
+    assert oracle.glu_f64(np.zeros(1), np.ones(1))[0] == 0.0
+
+
+def test_mlp_is_invariant_under_a_permutation_of_intermediate_indices():
+    """Eq. (4): permuting the intermediate dimension (rows of gate and up, columns of
+    down) consistently leaves the MLP output unchanged; with every weight dense only the
+    fp32 summation order of the down GEMM changes."""
+    r = np.random.default_rng(24)
+    M, D, I = 3, 64, 96
+    X, sx = gen.quantize_rows_fp8(r.standard_normal((M, D)).astype(np.float32))
+
+    Wg, Wu, Wd = [(r.standard_normal(shape) * 0.05).astype(np.float32) for shape in ((I, D), (I, D), (D, I))]
+    p = r.permutation(I)
+
+    def pack(Wf, axis):  # every entry dense (dense_begin 0 on either axis)
+        q, s = gen.quantize_rows_fp8(Wf)
+        N, K = q.shape
+        v, m, d, bad = oracle.compress(q, np.ones_like(q), oracle.FP8, axis, 0)
+        return (v, m, d, N, K, axis, 0, s)
+
+    a = oracle.mlp(X, sx, pack(Wg, 0), pack(Wu, 0), pack(Wd, 1))
+    b = oracle.mlp(X, sx, pack(Wg[p], 0), pack(Wu[p], 0), pack(Wd[:, p], 1))
+    assert np.array_equal(b["Hq"], a["Hq"][:, p]) and np.array_equal(b["sh"], a["sh"])
+    assert np.allclose(b["Y"], a["Y"], rtol=1e-5, atol=1e-6 * np.abs(a["Y"]).max())
