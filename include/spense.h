@@ -37,7 +37,7 @@
 extern "C" {
 #endif
 
-#define SPENSE_ABI_VERSION 2
+#define SPENSE_ABI_VERSION 3
 
 typedef enum spense_status {
   SPENSE_OK = 0,
@@ -51,7 +51,8 @@ typedef enum spense_status {
 
 typedef enum spense_dtype {
   SPENSE_FP8_E4M3FN = 1, /* OCP fp8 e4m3fn, 1 byte; NaN = 0x7f/0xff, max 448 */
-  SPENSE_BF16 = 2        /* bfloat16, 2 bytes */
+  SPENSE_BF16 = 2,       /* bfloat16, 2 bytes */
+  SPENSE_F32 = 3         /* fp32, 4 bytes: inputs of the quantisation calls only */
 } spense_dtype;
 
 typedef enum spense_split {
@@ -194,8 +195,10 @@ int spense_tile(const spense_packed_t* src, const spense_packed_t* dst, hipStrea
 
 /*
  * Device workspace (bytes) that spense_gemm needs for this M and weight; 0 means none.
- * The current kernels need none (they split K only inside a workgroup) and return 0;
- * the workspace arguments are kept so that a later kernel may use one.
+ * It is non-zero when the plan cuts K into slices run by separate workgroups (weights
+ * with few 16-row tiles at 17-64 tokens): S x M x N fp32 partial sums, added in slice
+ * order by a second kernel of the same call.  The workspace is only scratch between the
+ * two kernels of one call; calls that overlap on one workspace race.
  */
 size_t spense_gemm_workspace_size(int64_t M, const spense_packed_t* packed);
 
@@ -231,6 +234,36 @@ size_t spense_dense_gemm_workspace_size(int64_t M, int64_t N, int64_t K, int32_t
 int spense_dense_gemm(const void* X, int64_t M, int64_t ldx, const void* W, int64_t ldw, int64_t N, int64_t K,
                       int32_t dtype, const float* w_scale, const float* x_scale, void* Y, int64_t ldy,
                       uint32_t out_flags, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Per-token fp8 quantisation of activations, as spense_gemm consumes them (the inputs of
+ * the GLU MLP's GEMMs, sec. 3.3.1 Eq. (4)):
+ *   scales[m] = max_k |a[m, k]| / 448 (1.0 for an all-zero row),
+ *   q[m, k] = e4m3fn(a[m, k] / scales[m]),
+ * in fp32 with a correctly rounded division; the encode rounds to nearest, ties to an
+ * even mantissa, and saturates to +-448; NaN stays NaN (0x7f / 0xff).
+ * src: M x K device matrix of src_type (SPENSE_BF16 or SPENSE_F32), leading dimension
+ *   ld_src (elements).  q: M x K fp8 codes, leading dimension ldq (bytes).  scales: M
+ *   fp32.  Caller-owned device buffers; q and scales must not overlap src.
+ * One workgroup per row.  Asynchronous.  SPENSE_ERR_ARG for NULL pointers, negative
+ * sizes, ld below K, M above 2^31-1 or another src_type.
+ */
+int spense_quantize_fp8(const void* src, int32_t src_type, int64_t M, int64_t K, int64_t ld_src, uint8_t* q,
+                        int64_t ldq, float* scales, hipStream_t stream);
+
+/*
+ * The GLU step of the MLP between the output-split gate / up GEMMs and the input-split
+ * down GEMM (sec. 3.2 and sec. 3.3.1, Eq. (4), the activation read as SiLU), fused with
+ * the per-token fp8 quantisation of its result:
+ *   h[m, i] = u[m, i] * (g[m, i] / (1 + exp(-g[m, i]))) in fp32 (exp from the device
+ *   math library, within a few ulp), then scales / q of h as in spense_quantize_fp8.
+ * g, u: M x I device matrices of gu_type (SPENSE_BF16 or SPENSE_F32), leading dimensions
+ *   ldg, ldu (elements), with the same intermediate-index order (the order of the down
+ *   weight's input columns).  q: M x I codes (ldq bytes); scales: M fp32.  Caller-owned.
+ * Asynchronous.  Errors as spense_quantize_fp8.
+ */
+int spense_glu_quantize_fp8(const void* g, int64_t ldg, const void* u, int64_t ldu, int32_t gu_type, int64_t M,
+                            int64_t I, uint8_t* q, int64_t ldq, float* scales, hipStream_t stream);
 
 /* Thread-local description of the last error raised on this thread ("" if none). */
 const char* spense_last_error(void);

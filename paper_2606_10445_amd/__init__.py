@@ -29,6 +29,7 @@ SPENSE_ERR_HIP = -5
 SPENSE_ERR_DEVICE = -6
 SPENSE_FP8_E4M3FN = 1
 SPENSE_BF16 = 2
+SPENSE_F32 = 3
 SPENSE_SPLIT_OUTPUT = 0
 SPENSE_SPLIT_INPUT = 1
 SPENSE_OUT_BF16 = 0
@@ -38,7 +39,8 @@ SPENSE_LAYOUT_TILED = 1
 
 EXPORTS = ["spense_abi_version", "spense_last_error", "spense_layout", "spense_tiled_layout",
            "spense_compress_workspace_size", "spense_compress", "spense_decompress", "spense_tile",
-           "spense_gemm_workspace_size", "spense_gemm", "spense_dense_gemm_workspace_size", "spense_dense_gemm"]
+           "spense_gemm_workspace_size", "spense_gemm", "spense_dense_gemm_workspace_size", "spense_dense_gemm",
+           "spense_quantize_fp8", "spense_glu_quantize_fp8"]
 
 
 class SpenseError(RuntimeError):
@@ -86,6 +88,8 @@ def _load():
         "spense_gemm": (ctypes.c_int, [p, i64, i64, P(spense_packed_t), p, p, p, i64, u32, p, sz, p]),
         "spense_dense_gemm_workspace_size": (sz, [i64, i64, i64, i32]),
         "spense_dense_gemm": (ctypes.c_int, [p, i64, i64, p, i64, i64, i64, i32, p, p, p, i64, u32, p, sz, p]),
+        "spense_quantize_fp8": (ctypes.c_int, [p, i32, i64, i64, i64, p, i64, p, p]),
+        "spense_glu_quantize_fp8": (ctypes.c_int, [p, i64, p, i64, i32, i64, i64, p, i64, p, p]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -162,6 +166,14 @@ def spense_dense_gemm(X, M, ldx, W, ldw, N, K, dtype, w_scale, x_scale, Y, ldy, 
                                   stream)
 
 
+def spense_quantize_fp8(src, src_type, M, K, ld_src, q, ldq, scales, stream) -> int:
+    return _lib.spense_quantize_fp8(src, src_type, M, K, ld_src, q, ldq, scales, stream)
+
+
+def spense_glu_quantize_fp8(g, ldg, u, ldu, gu_type, M, I, q, ldq, scales, stream) -> int:
+    return _lib.spense_glu_quantize_fp8(g, ldg, u, ldu, gu_type, M, I, q, ldq, scales, stream)
+
+
 # ------------------------------------------------------------------ torch helpers
 def _dtype_code(t: torch.Tensor) -> int:
     if t.dtype in (torch.uint8, torch.float8_e4m3fn):
@@ -189,7 +201,8 @@ def _row_major(t: torch.Tensor, name: str):
 
 
 class Workspace:
-    """A zero-filled device buffer the library leaves zero-filled after every call."""
+    """A device buffer for spense_gemm's scratch, grown on demand and reused across calls
+    (calls that overlap on one workspace race)."""
 
     def __init__(self, device):
         self.device = torch.device(device)
@@ -331,3 +344,50 @@ def dense_gemm(X: torch.Tensor, W: torch.Tensor, w_scale=None, x_scale=None, out
                              _ptr(x_scale), _ptr(out), out.stride(0), SPENSE_OUT_F32 if out_f32 else SPENSE_OUT_BF16,
                              wp, wn, _stream(X.device)))
     return out
+
+
+def _act_type(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return SPENSE_BF16
+    if t.dtype == torch.float32:
+        return SPENSE_F32
+    raise TypeError(f"activations must be bfloat16 or float32, got {t.dtype}")
+
+
+def quantize_fp8(A: torch.Tensor, q=None, scales=None):
+    """Per-token fp8 quantisation (spense_quantize_fp8): returns (codes uint8 M x K,
+    scales fp32 M) with scales = row absmax / 448 and codes = e4m3fn(A / scale)."""
+    _row_major(A, "A")
+    M, K = A.shape
+    q = torch.empty((M, K), dtype=torch.uint8, device=A.device) if q is None else q
+    scales = torch.empty(M, dtype=torch.float32, device=A.device) if scales is None else scales
+    _check(spense_quantize_fp8(_ptr(A), _act_type(A), M, K, A.stride(0), _ptr(q), q.stride(0), _ptr(scales),
+                               _stream(A.device)))
+    return q, scales
+
+
+def glu_quantize_fp8(G: torch.Tensor, U: torch.Tensor, q=None, scales=None):
+    """The GLU step fused with per-token fp8 quantisation (spense_glu_quantize_fp8):
+    H = U * silu(G), returned as (codes uint8 M x I, scales fp32 M)."""
+    _row_major(G, "G")
+    _row_major(U, "U")
+    if G.shape != U.shape or G.dtype != U.dtype:
+        raise ValueError("G and U must have the same shape and dtype")
+    M, I = G.shape
+    q = torch.empty((M, I), dtype=torch.uint8, device=G.device) if q is None else q
+    scales = torch.empty(M, dtype=torch.float32, device=G.device) if scales is None else scales
+    _check(spense_glu_quantize_fp8(_ptr(G), G.stride(0), _ptr(U), U.stride(0), _act_type(G), M, I, _ptr(q),
+                                   q.stride(0), _ptr(scales), _stream(G.device)))
+    return q, scales
+
+
+def mlp(X: torch.Tensor, x_scale: torch.Tensor, gate: PackedWeight, up: PackedWeight, down: PackedWeight,
+        gate_scale=None, up_scale=None, down_scale=None, out=None, workspace: Workspace | None = None):
+    """The GLU MLP of the paper's sec. 3.3.1 Eq. (4) on Spense weights, as five library
+    calls: G = gate(X), U = up(X) (output-split, fp32 out), (Hq, sh) = GLU + per-token
+    fp8 quantisation, Y = down(Hq) (input-split, bf16 out).  X: fp8 codes with x_scale."""
+    G = gemm(X, gate, gate_scale, x_scale, out_f32=True, workspace=workspace)
+    U = gemm(X, up, up_scale, x_scale, out_f32=True, workspace=workspace)
+    Hq, sh = glu_quantize_fp8(G, U)
+    return gemm(Hq, down, down_scale, sh, out=out, workspace=workspace)
+

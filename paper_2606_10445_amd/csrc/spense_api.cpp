@@ -39,6 +39,21 @@ int esize(int32_t dtype) { return dtype == SPENSE_FP8_E4M3FN ? 1 : 2; }
 // Per-device cache of "is this a gfx950" (0 unknown, 1 yes, 2 no).
 std::atomic<int> g_arch[64];
 
+int check_device();
+
+// Arguments of the quantisation calls.
+int check_quant_args(const void* src, int32_t type, int64_t M, int64_t K, int64_t ld, const uint8_t* q, int64_t ldq,
+                     const float* scales, const char* what) {
+  if (type != SPENSE_BF16 && type != SPENSE_F32) return fail(SPENSE_ERR_ARG, "%s type %d is not bf16 or f32", what, type);
+  if (M < 0 || K < 0) return fail(SPENSE_ERR_ARG, "negative size");
+  if (M > INT32_MAX) return fail(SPENSE_ERR_ARG, "M too large");
+  if (M == 0) return SPENSE_OK;
+  if (!scales) return fail(SPENSE_ERR_ARG, "scales is NULL");
+  if (K > 0 && (!src || !q)) return fail(SPENSE_ERR_ARG, "%s or q is NULL", what);
+  if (ld < K || ldq < K) return fail(SPENSE_ERR_ARG, "leading dimension below K");
+  return SPENSE_OK;
+}
+
 int check_device() {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return fail(SPENSE_ERR_HIP, "hipGetDevice failed");
@@ -460,6 +475,34 @@ extern "C" {
 int spense_abi_version(void) { return SPENSE_ABI_VERSION; }
 
 const char* spense_last_error(void) { return g_err.c_str(); }
+
+int spense_quantize_fp8(const void* src, int32_t src_type, int64_t M, int64_t K, int64_t ld_src, uint8_t* q,
+                        int64_t ldq, float* scales, hipStream_t stream) {
+  int rc = check_quant_args(src, src_type, M, K, ld_src, q, ldq, scales, "src");
+  if (rc) return rc;
+  if (M == 0) return ok();
+  rc = check_device();
+  if (rc) return rc;
+  const int64_t es = src_type == SPENSE_BF16 ? 2 : 4;
+  if (spense::launch_quantize(src_type, src, ld_src * es, M, K, q, ldq, scales, stream) != hipSuccess)
+    return fail(SPENSE_ERR_HIP, "quantize launch failed");
+  return ok();
+}
+
+int spense_glu_quantize_fp8(const void* g, int64_t ldg, const void* u, int64_t ldu, int32_t gu_type, int64_t M,
+                            int64_t I, uint8_t* q, int64_t ldq, float* scales, hipStream_t stream) {
+  int rc = check_quant_args(g, gu_type, M, I, ldg, q, ldq, scales, "g");
+  if (rc) return rc;
+  rc = check_quant_args(u, gu_type, M, I, ldu, q, ldq, scales, "u");
+  if (rc) return rc;
+  if (M == 0) return ok();
+  rc = check_device();
+  if (rc) return rc;
+  const int64_t es = gu_type == SPENSE_BF16 ? 2 : 4;
+  if (spense::launch_glu_quantize(gu_type, g, ldg * es, u, ldu * es, M, I, q, ldq, scales, stream) != hipSuccess)
+    return fail(SPENSE_ERR_HIP, "glu quantize launch failed");
+  return ok();
+}
 
 int spense_layout(int64_t N, int64_t K, int32_t dtype, int32_t split, int64_t dense_begin, spense_layout_t* out) {
   return layout_impl(N, K, dtype, split, dense_begin, out);

@@ -87,6 +87,13 @@ hipError_t launch_decompress(int dtype, const uint8_t* values, int64_t v_ld_b, c
 
 hipError_t launch_zero_u64(unsigned long long* p, hipStream_t s);
 
+// Per-token fp8 quantisation (type = SPENSE_BF16 / SPENSE_F32; leading dimensions in bytes
+// for the sources) and the GLU step fused with it.
+hipError_t launch_quantize(int type, const void* src, int64_t ld_b, int64_t M, int64_t K, uint8_t* q, int64_t ldq,
+                           float* scales, hipStream_t st);
+hipError_t launch_glu_quantize(int type, const void* g, int64_t ldg_b, const void* u, int64_t ldu_b, int64_t M,
+                               int64_t I, uint8_t* q, int64_t ldq, float* scales, hipStream_t st);
+
 // Tiled execution layout: kind 0 values, 1 metadata, 2 dense (fp8).  src is one row-major
 // region (rows x row_bytes, pitch src_ld_b); dst receives tiles x chunks blocks.
 hipError_t launch_tile(int kind, const uint8_t* src, int64_t src_ld_b, int64_t rows, int64_t row_bytes, int64_t tiles,

@@ -41,7 +41,7 @@ def test_library_exports_every_declared_symbol(S):
     for n in _declared():
         assert hasattr(lib, n), f"{n} declared in include/ but not exported"
     assert set(_declared()) == set(S.EXPORTS)
-    assert S.spense_abi_version() == 2
+    assert S.spense_abi_version() == 3
 
 
 @pytest.mark.parametrize("N,K,split,db", [(256, 512, 0, 192), (256, 512, 1, 384), (25600, 5120, 0, 19200),
@@ -189,3 +189,19 @@ def test_k_slices_need_a_workspace(S):
     Lg = S.spense_layout(25600, 5120, 1, 0, 19200)
     pg = S.spense_packed_t(1, 0, 25600, 5120, 19200, 4096, Lg.values_ld, 8192, Lg.meta_ld, 16384, Lg.dense_ld)
     assert all(S.spense_gemm_workspace_size(m, pg) == 0 for m in (1, 8, 32, 64))
+
+
+def test_quantize_calls_validate_arguments_on_the_host(S):
+    """Error paths of the quantisation calls return before touching the device."""
+    q = S.spense_quantize_fp8
+    assert q(None, S.SPENSE_BF16, 0, 16, 16, None, 16, None, None) == S.SPENSE_OK  # M = 0: nothing to do
+    assert q(None, S.SPENSE_FP8_E4M3FN, 4, 16, 16, None, 16, None, None) == S.SPENSE_ERR_ARG  # fp8 input
+    assert q(None, S.SPENSE_F32, -1, 16, 16, None, 16, None, None) == S.SPENSE_ERR_ARG
+    assert q(None, S.SPENSE_F32, 4, 16, 16, None, 16, None, None) == S.SPENSE_ERR_ARG  # NULL pointers
+    assert "NULL" in S.spense_last_error()
+    assert q(8, S.SPENSE_F32, 4, 16, 15, 8, 16, 8, None) == S.SPENSE_ERR_ARG  # ld < K
+    assert q(8, S.SPENSE_F32, 1 << 31, 16, 16, 8, 16, 8, None) == S.SPENSE_ERR_ARG  # M too large
+    g = S.spense_glu_quantize_fp8
+    assert g(None, 16, None, 16, S.SPENSE_BF16, 0, 16, None, 16, None, None) == S.SPENSE_OK
+    assert g(8, 16, None, 16, S.SPENSE_BF16, 2, 16, 8, 16, 8, None) == S.SPENSE_ERR_ARG  # u NULL
+    assert g(8, 16, 8, 8, S.SPENSE_F32, 2, 16, 8, 16, 8, None) == S.SPENSE_ERR_ARG  # ldu < I

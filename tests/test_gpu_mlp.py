@@ -1,0 +1,168 @@
+"""GPU parity of the steps around the GEMMs of the GLU MLP (sec. 3.3.1, Eq. (4)), through
+the C ABI, against the CPU oracle:
+
+- per-token fp8 quantisation (spense_quantize_fp8): codes and scales bit-exact (both
+  sides take the same fp32 decisions: exact absmax, a correctly rounded division, the
+  e4m3fn encode);
+- GLU + quantisation (spense_glu_quantize_fp8): the device exp differs from the oracle's
+  fp64 one in the last bits, so the scale is checked to 1e-6 relative and each code to be
+  the nearest e4m3fn value of the fp64 reference h / scale, or its neighbour when that
+  value lies within 1e-5 relative of the midpoint between the two;
+- the whole MLP on Spense weights (gate / up output-split, down input-split): the
+  bf16-output tolerances of the GEMM tests (relative Frobenius <= 5e-3, max element
+  <= 1e-2 max|Y_ref|).
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import gen
+import oracle
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def S():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2606_10445_amd as S
+    return S
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def dec(codes):
+    return torch.from_numpy(np.ascontiguousarray(codes)).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+
+
+def rows(seed, M, K):
+    """Rows with a spread of magnitudes, a zero row, a NaN, exact midpoints and ragged K."""
+    r = np.random.default_rng(seed)
+    A = (r.standard_normal((M, K)) * np.exp(r.uniform(-8, 8, (M, 1)))).astype(np.float32)
+    if M > 2:
+        A[1] = 0
+    if M > 3 and K >= 8:
+        # scale 1 exactly (absmax 448), the rest exact midpoints between e4m3fn values
+        v = dec(np.arange(0, 0x7F, dtype=np.uint8))
+        mids = ((v[:-1] + v[1:]) / 2).astype(np.float32)
+        A[3] = np.resize(mids, K)
+        A[3, 0] = 448.0
+    if M > 5 and K > 3:
+        A[5, 2] = np.nan
+    return A
+
+
+QCASES = [(1, 1), (3, 17), (7, 256), (9, 1000), (64, 5120), (5, 25600), (300, 257)]
+
+
+@pytest.mark.parametrize("M,K", QCASES)
+@pytest.mark.parametrize("src", ["f32", "bf16"])
+def test_quantize_fp8_bit_exact(S, M, K, src):
+    say(f"[quantize] {src} M={M} K={K}")
+    A = rows(31 + K, M, K)
+    if src == "bf16":
+        At = torch.from_numpy(A).to(torch.bfloat16)
+        A = At.to(torch.float32).numpy()  # the values the kernel sees
+        dev = At.cuda()
+    else:
+        dev = torch.from_numpy(A).cuda()
+    q, s = S.quantize_fp8(dev)
+    torch.cuda.synchronize()
+    rq, rs = oracle.quantize_rows(A)
+    assert np.array_equal(q.cpu().numpy(), rq)
+    assert np.array_equal(s.cpu().numpy().view(np.uint32), rs.view(np.uint32))
+
+
+def test_quantize_fp8_strided_rows(S):
+    A = rows(40, 6, 300)
+    big = torch.zeros((6, 512), dtype=torch.float32)
+    big[:, :300] = torch.from_numpy(A)
+    dev = big.cuda()[:, :300]
+    qbuf = torch.full((6, 384), 0xAB, dtype=torch.uint8, device="cuda")
+    q, s = S.quantize_fp8(dev, q=qbuf[:, :300])
+    torch.cuda.synchronize()
+    rq, rs = oracle.quantize_rows(A)
+    assert np.array_equal(qbuf[:, :300].cpu().numpy(), rq)
+    assert torch.all(qbuf[:, 300:] == 0xAB)  # nothing written past K
+    assert np.array_equal(s.cpu().numpy(), rs)
+
+
+def check_glu_codes(q, s, G, U):
+    h = oracle.glu_f64(G.astype(np.float64), U.astype(np.float64))
+    amax = np.abs(h).max(axis=1)
+    s_ref = np.where(amax > 0, amax / 448.0, 1.0)
+    assert np.all(np.abs(s.astype(np.float64) - s_ref) <= 1e-6 * s_ref)
+    t = h / s.astype(np.float64)[:, None]
+    c_ref = oracle.encode_e4m3fn(t.astype(np.float32))
+    same = q == c_ref
+    if not same.all():
+        # any other code must be the neighbour across a midpoint that t nearly touches
+        bad = ~same
+        a, b = dec(q[bad]), dec(c_ref[bad])
+        mid = (a + b) / 2
+        tt = t[bad]
+        neighbour = np.abs(q[bad].astype(int) - c_ref[bad].astype(int)) == 1
+        assert np.all(neighbour & (np.abs(tt - mid) <= 1e-5 * np.abs(tt)))
+    assert same.mean() >= 0.999
+
+
+@pytest.mark.parametrize("M,I", [(1, 64), (5, 1000), (64, 25600), (33, 257)])
+@pytest.mark.parametrize("src", ["f32", "bf16"])
+def test_glu_quantize_fp8_valid_rounding(S, M, I, src):
+    say(f"[glu-quantize] {src} M={M} I={I}")
+    r = np.random.default_rng(50 + I)
+    G = (r.standard_normal((M, I)) * 3).astype(np.float32)
+    U = r.standard_normal((M, I)).astype(np.float32)
+    if M > 2:
+        U[1] = 0  # an all-zero h row
+    if src == "bf16":
+        Gt, Ut = torch.from_numpy(G).to(torch.bfloat16), torch.from_numpy(U).to(torch.bfloat16)
+        G, U = Gt.float().numpy(), Ut.float().numpy()
+        Gd, Ud = Gt.cuda(), Ut.cuda()
+    else:
+        Gd, Ud = torch.from_numpy(G).cuda(), torch.from_numpy(U).cuda()
+    q, s = S.glu_quantize_fp8(Gd, Ud)
+    torch.cuda.synchronize()
+    q, s = q.cpu().numpy(), s.cpu().numpy()
+    if M > 2:
+        assert s[1] == 1.0 and np.all(dec(q[1]) == 0)  # +0 or -0 (0 * negative silu)
+    check_glu_codes(q, s, G, U)
+
+
+def _packed(S, seed, name, N, K, axis, frac):
+    mx = gen.make_matrix(seed, 0 if axis == gen.OUTPUT else 1, name, N, K, axis, frac, gen.FP8)
+    ax = 0 if axis == gen.OUTPUT else 1
+    pw = S.compress(torch.from_numpy(mx.W).cuda(), torch.from_numpy(mx.mask).cuda(), ax, mx.dense_begin)
+    v, m, d, bad = oracle.compress(mx.W, mx.mask, oracle.FP8, ax, mx.dense_begin)
+    assert bad == 0
+    return pw, (v, m, d, N, K, ax, mx.dense_begin, mx.sw), torch.from_numpy(mx.sw).cuda()
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("D,I,Ms,frac", [(256, 512, [1, 5, 33], 0.25), (512, 768, [7], 0.5),
+                                         (5120, 25600, [64], 0.25)])
+def test_mlp_block_matches_oracle(S, D, I, Ms, frac):
+    """gate / up (I x D, output-split) -> GLU + quantise -> down (D x I, input-split), in
+    both storage layouts of the weights."""
+    say(f"[mlp] D={D} I={I} Ms={Ms}")
+    gate, gref, gsw = _packed(S, 60, "gate", I, D, gen.OUTPUT, frac)
+    up, uref, usw = _packed(S, 61, "up", I, D, gen.OUTPUT, frac)
+    down, dref, dsw = _packed(S, 62, "down", D, I, gen.INPUT, frac)
+    tiled = [S.tile(w) for w in (gate, up, down)]
+    for M in Ms:
+        X, sx = gen.make_x(60, 0, M, D, gen.FP8)
+        ref = oracle.mlp(X, sx, gref, uref, dref)
+        yref = oracle.bf16_rne(ref["Y"].astype(np.float32))
+        for (g, u, d), lay in (((gate, up, down), "row-major"), (tuple(tiled), "tiled")):
+            say(f"[mlp] M={M} {lay}")
+            Y = S.mlp(torch.from_numpy(X).cuda(), torch.from_numpy(sx).cuda(), g, u, d, gsw, usw, dsw)
+            torch.cuda.synchronize()
+            y = oracle.decode_bf16(Y.view(torch.int16).cpu().numpy().view(np.uint16)).astype(np.float64)
+            yr = oracle.decode_bf16(yref).astype(np.float64)
+            rel = np.linalg.norm(y - yr) / max(np.linalg.norm(yr), 1e-30)
+            assert rel <= 5e-3, rel
+            assert np.abs(y - yr).max() <= 1e-2 * np.abs(yr).max()
