@@ -228,6 +228,33 @@ def measure_extras(args, torch, gen, S, ws, pws, copies, swd, mx, dws, dense_cop
     dlms = time_launches(run_layer(dsets), 100, 10, torch)
     ex["qwen3_layer_m64"] = {"us_per_layer": round(lms * 1e3, 1), "ms_per_64_layers": round(lms * 64, 3),
                              "dense_us_per_layer": round(dlms * 1e3, 1), "speedup_vs_dense": round(dlms / lms, 3)}
+    # the GLU MLP block of the same layer (Eq. (4)): gate, up (output-split) -> GLU + per-token
+    # fp8 quantisation -> down (input-split), four launches; and the GLU step alone
+    names = [n for (n, _, _, _) in layer]
+    gi, ui, di = names.index("gate"), names.index("up"), names.index("down")
+    Xg, sxg, swg, _ = io[gi]
+    swu, swd_ = io[ui][2], io[di][2]
+    Gb = torch.empty((Ml, layer[gi][1]), dtype=torch.float32, device="cuda")
+    Ub = torch.empty_like(Gb)
+    Hq = torch.empty((Ml, layer[gi][1]), dtype=torch.uint8, device="cuda")
+    sh = torch.empty(Ml, dtype=torch.float32, device="cuda")
+    Yb = torch.empty((Ml, layer[di][1]), dtype=torch.bfloat16, device="cuda")
+
+    def run_mlp(ws_sets):
+        def f(i):
+            S.gemm(Xg, ws_sets[gi][i % 2], swg, sxg, out=Gb, out_f32=True, workspace=ws)
+            S.gemm(Xg, ws_sets[ui][i % 2], swu, sxg, out=Ub, out_f32=True, workspace=ws)
+            S.glu_quantize_fp8(Gb, Ub, q=Hq, scales=sh)
+            S.gemm(Hq, ws_sets[di][i % 2], swd_, sh, out=Yb, workspace=ws)
+        return f
+
+    mms = time_launches(run_mlp(sets), 100, 10, torch)
+    dmms = time_launches(run_mlp(dsets), 100, 10, torch)
+    gms = time_launches(lambda i: S.glu_quantize_fp8(Gb, Ub, q=Hq, scales=sh), 200, 10, torch)
+    glu_bytes = 2 * 2 * Gb.numel() * 4 + Hq.numel() + 4 * Ml  # g, u read twice (two passes), codes, scales
+    ex["qwen3_mlp_m64"] = {"us_per_block": round(mms * 1e3, 1), "dense_us_per_block": round(dmms * 1e3, 1),
+                           "speedup_vs_dense": round(dmms / mms, 3), "glu_quantize_us": round(gms * 1e3, 2),
+                           "glu_quantize_gbs": round(glu_bytes / (gms * 1e-3) / 1e9, 1)}
     return ex
 
 

@@ -241,7 +241,7 @@ int spense_dense_gemm(const void* X, int64_t M, int64_t ldx, const void* W, int6
  *   scales[m] = max_k |a[m, k]| / 448 (1.0 for an all-zero row),
  *   q[m, k] = e4m3fn(a[m, k] / scales[m]),
  * in fp32 with a correctly rounded division; the encode rounds to nearest, ties to an
- * even mantissa, and saturates to +-448; NaN stays NaN (0x7f / 0xff).
+ * even mantissa, and saturates to +-448; NaN stays NaN (0xff, whatever its sign).
  * src: M x K device matrix of src_type (SPENSE_BF16 or SPENSE_F32), leading dimension
  *   ld_src (elements).  q: M x K fp8 codes, leading dimension ldq (bytes).  scales: M
  *   fp32.  Caller-owned device buffers; q and scales must not overlap src.
@@ -255,8 +255,9 @@ int spense_quantize_fp8(const void* src, int32_t src_type, int64_t M, int64_t K,
  * The GLU step of the MLP between the output-split gate / up GEMMs and the input-split
  * down GEMM (sec. 3.2 and sec. 3.3.1, Eq. (4), the activation read as SiLU), fused with
  * the per-token fp8 quantisation of its result:
- *   h[m, i] = u[m, i] * (g[m, i] / (1 + exp(-g[m, i]))) in fp32 (exp from the device
- *   math library, within a few ulp), then scales / q of h as in spense_quantize_fp8.
+ *   h[m, i] = u[m, i] * g[m, i] / (1 + exp(-g[m, i])) in fp32 (exp and the reciprocal
+ *   from the hardware approximations, within a few ulp), then scales / q of h as in
+ *   spense_quantize_fp8.
  * g, u: M x I device matrices of gu_type (SPENSE_BF16 or SPENSE_F32), leading dimensions
  *   ldg, ldu (elements), with the same intermediate-index order (the order of the down
  *   weight's input columns).  q: M x I codes (ldq bytes); scales: M fp32.  Caller-owned.
