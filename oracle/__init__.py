@@ -259,3 +259,41 @@ def mlp(X, sx, gate, up, down, dtype=FP8):
     Y = run(Hq, sh, down)
     return {"G": G, "U": U, "H": H, "Hq": Hq, "sh": sh, "Y": Y}
 
+
+# ------------------------------------------------------------------ dense-index selection
+def index_scores(Wg, Wu, Wd, h_in, h_mid, eps: float = 1e-8) -> dict:
+    """SpenseGPT+ priority of each intermediate index (sec. 3.3.1, the Wanda-style
+    element score S_ij = |W_ij| sqrt(H_jj) aggregated per index, each projection's score
+    vector normalised by its mean, the three summed).  Wg, Wu: I x D (index i = row i),
+    Wd: D x I (index i = column i); h_in: diag(X^T X) of the MLP input (D), h_mid: the
+    same for the down projection's input (I).  Reading for down: index i's score is the
+    mean over the column's entries, |Wd[n, i]| sqrt(h_mid[i]).  fp64, plain loops over
+    numpy rows.  Returns the three raw score vectors and their normalised sum."""
+    Wg = np.asarray(Wg, np.float64)
+    Wu = np.asarray(Wu, np.float64)
+    Wd = np.asarray(Wd, np.float64)
+    I, D = Wg.shape
+    sx = np.sqrt(np.asarray(h_in, np.float64))
+    sm = np.sqrt(np.asarray(h_mid, np.float64))
+    s_gate = np.array([np.sum(np.abs(Wg[i]) * sx) / D for i in range(I)])
+    s_up = np.array([np.sum(np.abs(Wu[i]) * sx) / D for i in range(I)])
+    s_down = np.array([np.sum(np.abs(Wd[:, i])) * sm[i] / Wd.shape[0] for i in range(I)])
+
+    def norm(v):
+        return v / (np.sum(v) / v.size + eps)
+
+    return {"gate": s_gate, "up": s_up, "down": s_down, "total": norm(s_gate) + norm(s_up) + norm(s_down)}
+
+
+def dense_index_permutation(total, n_dense: int) -> dict:
+    """TopK of the priorities (the n_dense largest; ties keep the lower index) and the
+    permutation that moves them to the back (sec. 3.3.1): perm[new] = old, the sparse
+    indices first and the dense ones last, each in ascending order."""
+    t = np.asarray(total, np.float64)
+    order = np.argsort(-t, kind="stable")  # a library sort; stable keeps lower indices first on ties
+    dense = np.sort(order[:n_dense])
+    is_dense = np.zeros(t.size, bool)
+    is_dense[dense] = True
+    perm = np.concatenate([np.flatnonzero(~is_dense), dense]).astype(np.int32)
+    return {"dense": dense, "perm": perm}
+

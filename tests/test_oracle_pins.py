@@ -8,6 +8,7 @@
   and the linearity of the two split variants of sec. 3.2 (output-split concatenates
   disjoint outputs, input-split sums two partial products).
 """
+import itertools
 import json
 import os
 
@@ -498,3 +499,51 @@ def test_mlp_is_invariant_under_a_permutation_of_intermediate_indices():
     b = oracle.mlp(X, sx, pack(Wg[p], 0), pack(Wu[p], 0), pack(Wd[:, p], 1))
     assert np.array_equal(b["Hq"], a["Hq"][:, p]) and np.array_equal(b["sh"], a["sh"])
     assert np.allclose(b["Y"], a["Y"], rtol=1e-5, atol=1e-6 * np.abs(a["Y"]).max())
+
+
+# ------------------------------------------------------------------ dense-index selection (sec. 3.3.1)
+def test_index_scores_closed_forms():
+    I, D = 6, 8
+    ones = np.ones((I, D))
+    r = oracle.index_scores(ones, ones, np.ones((D, I)), np.full(D, 4.0), np.full(I, 9.0), eps=0.0)
+    assert np.allclose(r["gate"], 2.0) and np.allclose(r["up"], 2.0) and np.allclose(r["down"], 3.0)
+    assert np.allclose(r["total"], 3.0)  # each normalised vector is all ones
+    # one row / column scaled: its raw score scales, the normalised sum keeps mean 3 (eps 0)
+    Wg = ones.copy()
+    Wg[2] *= 5
+    Wd = np.ones((D, I))
+    Wd[:, 4] *= -7  # signs do not matter
+    r = oracle.index_scores(Wg, ones, Wd, np.full(D, 4.0), np.full(I, 9.0), eps=0.0)
+    assert r["gate"][2] == 10.0 and r["down"][4] == 21.0
+    assert np.isclose(r["total"].mean(), 3.0)
+    assert np.argmax(r["total"]) in (2, 4)
+
+
+def test_index_scores_wanda_identity_against_activations():
+    """With h = diag(X^T X), the score is the mean over j of |W_ij| * ||X[:, j]||_2."""
+    rng = np.random.default_rng(70)
+    I, D, T = 20, 12, 30
+    X = rng.standard_normal((T, D))
+    Hm = rng.standard_normal((T, I))
+    Wg, Wu, Wd = rng.standard_normal((I, D)), rng.standard_normal((I, D)), rng.standard_normal((D, I))
+    r = oracle.index_scores(Wg, Wu, Wd, np.einsum("td,td->d", X, X), np.einsum("ti,ti->i", Hm, Hm))
+    colnorm = np.linalg.norm(X, axis=0)
+    assert np.allclose(r["gate"], (np.abs(Wg) @ colnorm) / D, rtol=1e-12)
+    assert np.allclose(r["down"], np.abs(Wd).mean(axis=0) * np.linalg.norm(Hm, axis=0), rtol=1e-12)
+
+
+def test_dense_index_permutation_brute_force():
+    rng = np.random.default_rng(71)
+    for trial in range(50):
+        n = int(rng.integers(1, 12))
+        k = int(rng.integers(0, n + 1))
+        t = rng.integers(0, 4, n).astype(np.float64)  # many ties
+        r = oracle.dense_index_permutation(t, k)
+        # brute force over every k-subset: the largest score sum, then the lexicographically
+        # smallest index list (ties keep lower indices)
+        best = min(itertools.combinations(range(n), k), key=lambda c: (-sum(t[i] for i in c), c))
+        assert np.array_equal(r["dense"], np.array(sorted(best), dtype=r["dense"].dtype))
+        perm = r["perm"]
+        assert sorted(perm.tolist()) == list(range(n))  # a permutation
+        assert set(perm[n - k:].tolist()) == set(best)  # dense indices at the back
+        assert np.all(np.diff(perm[: n - k]) > 0) and np.all(np.diff(perm[n - k:]) > 0)
