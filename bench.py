@@ -251,11 +251,43 @@ def measure_extras(args, torch, gen, S, ws, pws, copies, swd, mx, dws, dense_cop
     mms = time_launches(run_mlp(sets), 100, 10, torch)
     dmms = time_launches(run_mlp(dsets), 100, 10, torch)
     gms = time_launches(lambda i: S.glu_quantize_fp8(Gb, Ub, q=Hq, scales=sh), 200, 10, torch)
-    glu_bytes = 2 * 2 * Gb.numel() * 4 + Hq.numel() + 4 * Ml  # g, u read twice (two passes), codes, scales
+    glu_bytes = 2 * Gb.numel() * 4 + Hq.numel() + 4 * Ml  # g, u read once, codes and scales written
     ex["qwen3_mlp_m64"] = {"us_per_block": round(mms * 1e3, 1), "dense_us_per_block": round(dmms * 1e3, 1),
                            "speedup_vs_dense": round(dmms / mms, 3), "glu_quantize_us": round(gms * 1e3, 2),
                            "glu_quantize_gbs": round(glu_bytes / (gms * 1e-3) / 1e9, 1)}
+    del sets, dsets, io, Gb, Ub, Hq
+    ex["qwen3_index_selection"] = measure_index_selection(torch, S)
     return ex
+
+
+def measure_index_selection(torch, S):
+    """The offline SpenseGPT+ index step (sec. 3.3.1) at the MLP size of the workload: bf16
+    gate / up (25600 x 5120) and down (5120 x 25600), 25% of the indices dense.  Times the
+    priorities, the TopK permutation and the three weight gathers separately."""
+    I, D, n_dense = 25600, 5120, 6400
+    g = torch.Generator(device="cuda").manual_seed(11)
+    Wg = (torch.randn((I, D), generator=g, device="cuda") * 0.02).to(torch.bfloat16)
+    Wu = (torch.randn((I, D), generator=g, device="cuda") * 0.02).to(torch.bfloat16)
+    Wd = (torch.randn((D, I), generator=g, device="cuda") * 0.02).to(torch.bfloat16)
+    h_in = torch.rand(D, generator=g, device="cuda") * 64
+    h_mid = torch.rand(I, generator=g, device="cuda") * 64
+    sc = S.index_scores(Wg, Wu, Wd, h_in, h_mid)
+    flags, perm = S.dense_permutation(sc["total"], n_dense)
+    outs = [torch.empty_like(Wg), torch.empty_like(Wu), torch.empty_like(Wd)]
+    sms = time_launches(lambda i: S.index_scores(Wg, Wu, Wd, h_in, h_mid), 10, 2, torch)
+    pms = time_launches(lambda i: S.dense_permutation(sc["total"], n_dense), 10, 2, torch)
+
+    def gathers(i):
+        S.gather_rows(Wg, perm, out=outs[0])
+        S.gather_rows(Wu, perm, out=outs[1])
+        S.gather_cols(Wd, perm, out=outs[2])
+
+    gms = time_launches(gathers, 10, 2, torch)
+    wbytes = 3 * I * D * 2
+    return {"I": I, "D": D, "n_dense": n_dense, "scores_us": round(sms * 1e3, 1),
+            "scores_gbs": round(wbytes / (sms * 1e-3) / 1e9, 1), "permutation_us": round(pms * 1e3, 1),
+            "gathers_us": round(gms * 1e3, 1), "gathers_gbs": round(2 * wbytes / (gms * 1e-3) / 1e9, 1),
+            "total_ms": round(sms + pms + gms, 3)}
 
 
 def main():

@@ -37,7 +37,7 @@
 extern "C" {
 #endif
 
-#define SPENSE_ABI_VERSION 3
+#define SPENSE_ABI_VERSION 4
 
 typedef enum spense_status {
   SPENSE_OK = 0,
@@ -265,6 +265,54 @@ int spense_quantize_fp8(const void* src, int32_t src_type, int64_t M, int64_t K,
  */
 int spense_glu_quantize_fp8(const void* g, int64_t ldg, const void* u, int64_t ldu, int32_t gu_type, int64_t M,
                             int64_t I, uint8_t* q, int64_t ldq, float* scales, hipStream_t stream);
+
+/*
+ * SpenseGPT+ dense-index priorities of a GLU MLP (sec. 3.3.1: the Wanda-style element
+ * score |W_ij| sqrt(H_jj) of Eq. (8) averaged per intermediate index, Eq. (9), each
+ * projection's vector divided by its mean plus eps, Eq. (10), the three summed, Eq. (11);
+ * for down the index is a column, so its scores average over that column):
+ *   raw[0*I + i] = mean_j |w_gate[i, j]| sqrt(h_in[j]),   raw[1*I + i] likewise for w_up,
+ *   raw[2*I + i] = mean_n |w_down[n, i]| sqrt(h_mid[i]),
+ *   total[i] = sum_v raw[v*I + i] / (mean_i raw[v*I + i] + eps).
+ * w_gate, w_up: I x D (leading dimension ld_gu elements); w_down: D x I (ld_down); all of
+ * wtype SPENSE_BF16 or SPENSE_F32 (the weights before quantisation).  h_in: D fp32, the
+ * diagonal of X^T X for the MLP input; h_mid: I fp32, the same for the down projection's
+ * input.  raw: 3 x I fp32, total: I fp32 (outputs).  fp32 sums in a fixed order
+ * (deterministic).  Offline, asynchronous.  SPENSE_ERR_ARG for NULL pointers, sizes
+ * below 1, ld below the row length, I or D above 2^31-1.
+ */
+int spense_index_scores(const void* w_gate, const void* w_up, int64_t ld_gu, const void* w_down, int64_t ld_down,
+                        int32_t wtype, int64_t I, int64_t D, const float* h_in, const float* h_mid, float eps,
+                        float* raw, float* total, hipStream_t stream);
+
+/*
+ * TopK of the priorities (Eq. (12)) and the permutation that moves the chosen indices
+ * to the back (sec. 3.3.1): flags[i] = 1 for the n_dense indices with the largest total (ties: the
+ * lower index first; NaN below every number), 0 otherwise; perm[new] = old lists the
+ * unflagged indices in ascending order, then the flagged ones.  perm applies to the rows
+ * of Wgate and Wup (spense_gather_rows) and the columns of Wdown (spense_gather_cols),
+ * after which the dense region is the trailing one of all three (Eq. (4) keeps the MLP
+ * unchanged).  total: I fp32; flags: I bytes; perm: I int32 (outputs).  Asynchronous.
+ * SPENSE_ERR_ARG for NULL pointers, I < 1 or above 2^31-1, n_dense outside [0, I].
+ */
+int spense_dense_permutation(const float* total, int64_t I, int64_t n_dense, uint8_t* flags, int32_t* perm,
+                             hipStream_t stream);
+
+/*
+ * dst[r, :] = src[perm[r], :] for r < rows (row_bytes bytes per row; leading dimensions
+ * in bytes).  perm must hold indices in [0, rows) (others are clamped into that range).
+ * src and dst must not overlap.  Asynchronous.
+ */
+int spense_gather_rows(const void* src, int64_t ld_src_b, void* dst, int64_t ld_dst_b, int64_t rows,
+                       int64_t row_bytes, const int32_t* perm, hipStream_t stream);
+
+/*
+ * dst[n, c] = src[n, perm[c]] for n < rows, c < cols, elements of elem_bytes (1, 2 or 4)
+ * bytes, leading dimensions in elements.  perm must hold indices in [0, cols) (others
+ * are clamped).  src and dst must not overlap.  Asynchronous.
+ */
+int spense_gather_cols(const void* src, int64_t ld_src, void* dst, int64_t ld_dst, int64_t rows, int64_t cols,
+                       int32_t elem_bytes, const int32_t* perm, hipStream_t stream);
 
 /* Thread-local description of the last error raised on this thread ("" if none). */
 const char* spense_last_error(void);

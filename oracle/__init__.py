@@ -262,9 +262,10 @@ def mlp(X, sx, gate, up, down, dtype=FP8):
 
 # ------------------------------------------------------------------ dense-index selection
 def index_scores(Wg, Wu, Wd, h_in, h_mid, eps: float = 1e-8) -> dict:
-    """SpenseGPT+ priority of each intermediate index (sec. 3.3.1, the Wanda-style
-    element score S_ij = |W_ij| sqrt(H_jj) aggregated per index, each projection's score
-    vector normalised by its mean, the three summed).  Wg, Wu: I x D (index i = row i),
+    """SpenseGPT+ priority of each intermediate index (sec. 3.3.1: the Wanda-style
+    element score S_ij = |W_ij| sqrt(H_jj) of Eq. (8) averaged per index, Eq. (9), each
+    projection's score vector normalised by its mean, Eq. (10), the three summed,
+    Eq. (11)).  Wg, Wu: I x D (index i = row i),
     Wd: D x I (index i = column i); h_in: diag(X^T X) of the MLP input (D), h_mid: the
     same for the down projection's input (I).  Reading for down: index i's score is the
     mean over the column's entries, |Wd[n, i]| sqrt(h_mid[i]).  fp64, plain loops over
@@ -286,7 +287,7 @@ def index_scores(Wg, Wu, Wd, h_in, h_mid, eps: float = 1e-8) -> dict:
 
 
 def dense_index_permutation(total, n_dense: int) -> dict:
-    """TopK of the priorities (the n_dense largest; ties keep the lower index) and the
+    """TopK of the priorities, Eq. (12) (the n_dense largest; ties keep the lower index) and the
     permutation that moves them to the back (sec. 3.3.1): perm[new] = old, the sparse
     indices first and the dense ones last, each in ascending order."""
     t = np.asarray(total, np.float64)

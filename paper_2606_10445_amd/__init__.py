@@ -40,7 +40,8 @@ SPENSE_LAYOUT_TILED = 1
 EXPORTS = ["spense_abi_version", "spense_last_error", "spense_layout", "spense_tiled_layout",
            "spense_compress_workspace_size", "spense_compress", "spense_decompress", "spense_tile",
            "spense_gemm_workspace_size", "spense_gemm", "spense_dense_gemm_workspace_size", "spense_dense_gemm",
-           "spense_quantize_fp8", "spense_glu_quantize_fp8"]
+           "spense_quantize_fp8", "spense_glu_quantize_fp8", "spense_index_scores", "spense_dense_permutation",
+           "spense_gather_rows", "spense_gather_cols"]
 
 
 class SpenseError(RuntimeError):
@@ -90,6 +91,10 @@ def _load():
         "spense_dense_gemm": (ctypes.c_int, [p, i64, i64, p, i64, i64, i64, i32, p, p, p, i64, u32, p, sz, p]),
         "spense_quantize_fp8": (ctypes.c_int, [p, i32, i64, i64, i64, p, i64, p, p]),
         "spense_glu_quantize_fp8": (ctypes.c_int, [p, i64, p, i64, i32, i64, i64, p, i64, p, p]),
+        "spense_index_scores": (ctypes.c_int, [p, p, i64, p, i64, i32, i64, i64, p, p, ctypes.c_float, p, p, p]),
+        "spense_dense_permutation": (ctypes.c_int, [p, i64, i64, p, p, p]),
+        "spense_gather_rows": (ctypes.c_int, [p, i64, p, i64, i64, i64, p, p]),
+        "spense_gather_cols": (ctypes.c_int, [p, i64, p, i64, i64, i64, i32, p, p]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -172,6 +177,24 @@ def spense_quantize_fp8(src, src_type, M, K, ld_src, q, ldq, scales, stream) -> 
 
 def spense_glu_quantize_fp8(g, ldg, u, ldu, gu_type, M, I, q, ldq, scales, stream) -> int:
     return _lib.spense_glu_quantize_fp8(g, ldg, u, ldu, gu_type, M, I, q, ldq, scales, stream)
+
+
+def spense_index_scores(w_gate, w_up, ld_gu, w_down, ld_down, wtype, I, D, h_in, h_mid, eps, raw, total,
+                        stream) -> int:
+    return _lib.spense_index_scores(w_gate, w_up, ld_gu, w_down, ld_down, wtype, I, D, h_in, h_mid, eps, raw, total,
+                                    stream)
+
+
+def spense_dense_permutation(total, I, n_dense, flags, perm, stream) -> int:
+    return _lib.spense_dense_permutation(total, I, n_dense, flags, perm, stream)
+
+
+def spense_gather_rows(src, ld_src_b, dst, ld_dst_b, rows, row_bytes, perm, stream) -> int:
+    return _lib.spense_gather_rows(src, ld_src_b, dst, ld_dst_b, rows, row_bytes, perm, stream)
+
+
+def spense_gather_cols(src, ld_src, dst, ld_dst, rows, cols, elem_bytes, perm, stream) -> int:
+    return _lib.spense_gather_cols(src, ld_src, dst, ld_dst, rows, cols, elem_bytes, perm, stream)
 
 
 # ------------------------------------------------------------------ torch helpers
@@ -391,3 +414,77 @@ def mlp(X: torch.Tensor, x_scale: torch.Tensor, gate: PackedWeight, up: PackedWe
     Hq, sh = glu_quantize_fp8(G, U)
     return gemm(Hq, down, down_scale, sh, out=out, workspace=workspace)
 
+
+
+# ------------------------------------------------------------------ dense-index selection
+def index_scores(Wg: torch.Tensor, Wu: torch.Tensor, Wd: torch.Tensor, h_in: torch.Tensor, h_mid: torch.Tensor,
+                 eps: float = 1e-8) -> dict:
+    """SpenseGPT+ priorities of the intermediate indices of a GLU MLP (spense_index_scores,
+    sec. 3.3.1).  Wg, Wu: I x D, Wd: D x I (bf16 or fp32, the same dtype); h_in (D) and
+    h_mid (I): fp32 diagonals of the input Hessians.  Returns the raw gate / up / down
+    score vectors and their mean-normalised sum ``total`` (fp32, on the device)."""
+    for t, n in ((Wg, "Wg"), (Wu, "Wu"), (Wd, "Wd")):
+        _row_major(t, n)
+    if Wg.shape != Wu.shape or Wg.stride(0) != Wu.stride(0) or Wd.shape != (Wg.shape[1], Wg.shape[0]):
+        raise ValueError("Wg, Wu must be I x D with one leading dimension and Wd D x I")
+    if not (Wg.dtype == Wu.dtype == Wd.dtype):
+        raise ValueError("the three weights must have one dtype")
+    I, D = Wg.shape
+    h_in = h_in.to(torch.float32).contiguous()
+    h_mid = h_mid.to(torch.float32).contiguous()
+    if h_in.numel() != D or h_mid.numel() != I:
+        raise ValueError("h_in must have D entries and h_mid I")
+    raw = torch.empty((3, I), dtype=torch.float32, device=Wg.device)
+    total = torch.empty(I, dtype=torch.float32, device=Wg.device)
+    _check(spense_index_scores(_ptr(Wg), _ptr(Wu), Wg.stride(0), _ptr(Wd), Wd.stride(0), _act_type(Wg), I, D,
+                               _ptr(h_in), _ptr(h_mid), eps, _ptr(raw), _ptr(total), _stream(Wg.device)))
+    return {"gate": raw[0], "up": raw[1], "down": raw[2], "total": total}
+
+
+def dense_permutation(total: torch.Tensor, n_dense: int):
+    """TopK of the priorities and the permutation moving them to the back
+    (spense_dense_permutation): returns (flags uint8 I, perm int32 I, perm[new] = old)."""
+    if total.dtype != torch.float32 or total.dim() != 1 or not total.is_contiguous():
+        raise ValueError("total must be a contiguous fp32 vector")
+    I = total.numel()
+    flags = torch.empty(I, dtype=torch.uint8, device=total.device)
+    perm = torch.empty(I, dtype=torch.int32, device=total.device)
+    _check(spense_dense_permutation(_ptr(total), I, n_dense, _ptr(flags), _ptr(perm), _stream(total.device)))
+    return flags, perm
+
+
+def _perm_arg(perm: torch.Tensor, n: int):
+    if perm.dtype != torch.int32 or perm.numel() != n or not perm.is_contiguous():
+        raise ValueError(f"perm must be a contiguous int32 vector of {n} entries")
+
+
+def gather_rows(src: torch.Tensor, perm: torch.Tensor, out=None) -> torch.Tensor:
+    """out[r] = src[perm[r]] (spense_gather_rows) for a row-major 2-D tensor."""
+    _row_major(src, "src")
+    _perm_arg(perm, src.shape[0])
+    out = torch.empty_like(src, memory_format=torch.contiguous_format) if out is None else out
+    es = src.element_size()
+    _check(spense_gather_rows(_ptr(src), src.stride(0) * es, _ptr(out), out.stride(0) * es, src.shape[0],
+                              src.shape[1] * es, _ptr(perm), _stream(src.device)))
+    return out
+
+
+def gather_cols(src: torch.Tensor, perm: torch.Tensor, out=None) -> torch.Tensor:
+    """out[:, c] = src[:, perm[c]] (spense_gather_cols) for a row-major 2-D tensor."""
+    _row_major(src, "src")
+    _perm_arg(perm, src.shape[1])
+    out = torch.empty_like(src, memory_format=torch.contiguous_format) if out is None else out
+    _check(spense_gather_cols(_ptr(src), src.stride(0), _ptr(out), out.stride(0), src.shape[0], src.shape[1],
+                              src.element_size(), _ptr(perm), _stream(src.device)))
+    return out
+
+
+def select_dense_indices(Wg: torch.Tensor, Wu: torch.Tensor, Wd: torch.Tensor, h_in: torch.Tensor,
+                         h_mid: torch.Tensor, n_dense: int, eps: float = 1e-8) -> dict:
+    """The whole SpenseGPT+ index step of sec. 3.3.1 on the device: priorities, TopK, and
+    Wg, Wu (rows) and Wd (columns) permuted so the n_dense chosen indices form the
+    trailing dense region of all three.  Eq. (4): the MLP computes the same function."""
+    sc = index_scores(Wg, Wu, Wd, h_in, h_mid, eps)
+    flags, perm = dense_permutation(sc["total"], n_dense)
+    return {"scores": sc, "flags": flags, "perm": perm, "Wg": gather_rows(Wg, perm), "Wu": gather_rows(Wu, perm),
+            "Wd": gather_cols(Wd, perm)}

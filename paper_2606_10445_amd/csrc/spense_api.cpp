@@ -489,6 +489,63 @@ int spense_quantize_fp8(const void* src, int32_t src_type, int64_t M, int64_t K,
   return ok();
 }
 
+int spense_index_scores(const void* w_gate, const void* w_up, int64_t ld_gu, const void* w_down, int64_t ld_down,
+                        int32_t wtype, int64_t I, int64_t D, const float* h_in, const float* h_mid, float eps,
+                        float* raw, float* total, hipStream_t stream) {
+  if (wtype != SPENSE_BF16 && wtype != SPENSE_F32) return fail(SPENSE_ERR_ARG, "wtype %d is not bf16 or f32", wtype);
+  if (I < 1 || D < 1 || I > INT32_MAX || D > INT32_MAX) return fail(SPENSE_ERR_ARG, "bad I=%lld D=%lld", (long long)I, (long long)D);
+  if (!w_gate || !w_up || !w_down || !h_in || !h_mid || !raw || !total) return fail(SPENSE_ERR_ARG, "NULL pointer");
+  if (ld_gu < D || ld_down < I) return fail(SPENSE_ERR_ARG, "leading dimension below the row length");
+  int rc = check_device();
+  if (rc) return rc;
+  const int64_t es = wtype == SPENSE_BF16 ? 2 : 4;
+  if (spense::launch_index_scores(wtype, w_gate, w_up, ld_gu * es, I, D, w_down, ld_down * es, h_in, h_mid, eps, raw,
+                                  total, stream) != hipSuccess)
+    return fail(SPENSE_ERR_HIP, "index score launch failed");
+  return ok();
+}
+
+int spense_dense_permutation(const float* total, int64_t I, int64_t n_dense, uint8_t* flags, int32_t* perm,
+                             hipStream_t stream) {
+  if (I < 1 || I > INT32_MAX) return fail(SPENSE_ERR_ARG, "bad I=%lld", (long long)I);
+  if (n_dense < 0 || n_dense > I) return fail(SPENSE_ERR_ARG, "n_dense=%lld outside [0, I]", (long long)n_dense);
+  if (!total || !flags || !perm) return fail(SPENSE_ERR_ARG, "NULL pointer");
+  int rc = check_device();
+  if (rc) return rc;
+  if (spense::launch_dense_permutation(total, I, n_dense, flags, perm, stream) != hipSuccess)
+    return fail(SPENSE_ERR_HIP, "permutation launch failed");
+  return ok();
+}
+
+int spense_gather_rows(const void* src, int64_t ld_src_b, void* dst, int64_t ld_dst_b, int64_t rows,
+                       int64_t row_bytes, const int32_t* perm, hipStream_t stream) {
+  if (rows < 0 || row_bytes < 0 || rows > INT32_MAX) return fail(SPENSE_ERR_ARG, "bad size");
+  if (rows == 0 || row_bytes == 0) return ok();
+  if (!src || !dst || !perm) return fail(SPENSE_ERR_ARG, "NULL pointer");
+  if (ld_src_b < row_bytes || ld_dst_b < row_bytes) return fail(SPENSE_ERR_ARG, "leading dimension below the row");
+  int rc = check_device();
+  if (rc) return rc;
+  if (spense::launch_gather_rows(src, ld_src_b, dst, ld_dst_b, rows, row_bytes, perm, stream) != hipSuccess)
+    return fail(SPENSE_ERR_HIP, "gather launch failed");
+  return ok();
+}
+
+int spense_gather_cols(const void* src, int64_t ld_src, void* dst, int64_t ld_dst, int64_t rows, int64_t cols,
+                       int32_t elem_bytes, const int32_t* perm, hipStream_t stream) {
+  if (elem_bytes != 1 && elem_bytes != 2 && elem_bytes != 4) return fail(SPENSE_ERR_ARG, "elem_bytes %d", elem_bytes);
+  if (rows < 0 || cols < 0 || rows > INT32_MAX || cols > INT32_MAX) return fail(SPENSE_ERR_ARG, "bad size");
+  if (rows == 0 || cols == 0) return ok();
+  if (!src || !dst || !perm) return fail(SPENSE_ERR_ARG, "NULL pointer");
+  if (ld_src < cols || ld_dst < cols) return fail(SPENSE_ERR_ARG, "leading dimension below the row");
+  if ((uintptr_t)src % elem_bytes || (uintptr_t)dst % elem_bytes) return fail(SPENSE_ERR_ALIGN, "misaligned matrix");
+  int rc = check_device();
+  if (rc) return rc;
+  if (spense::launch_gather_cols(elem_bytes, src, ld_src * elem_bytes, dst, ld_dst * elem_bytes, rows, cols, perm,
+                                 stream) != hipSuccess)
+    return fail(SPENSE_ERR_HIP, "gather launch failed");
+  return ok();
+}
+
 int spense_glu_quantize_fp8(const void* g, int64_t ldg, const void* u, int64_t ldu, int32_t gu_type, int64_t M,
                             int64_t I, uint8_t* q, int64_t ldq, float* scales, hipStream_t stream) {
   int rc = check_quant_args(g, gu_type, M, I, ldg, q, ldq, scales, "g");

@@ -94,6 +94,17 @@ hipError_t launch_quantize(int type, const void* src, int64_t ld_b, int64_t M, i
 hipError_t launch_glu_quantize(int type, const void* g, int64_t ldg_b, const void* u, int64_t ldu_b, int64_t M,
                                int64_t I, uint8_t* q, int64_t ldq, float* scales, hipStream_t st);
 
+// Dense-index selection (SpenseGPT+): priorities, TopK permutation, row / column gathers.
+hipError_t launch_index_scores(int type, const void* wg, const void* wu, int64_t ld_gu_b, int64_t I, int64_t D,
+                               const void* wd, int64_t ld_d_b, const float* h_in, const float* h_mid, float eps,
+                               float* raw, float* total, hipStream_t st);
+hipError_t launch_dense_permutation(const float* total, int64_t I, int64_t n_dense, uint8_t* flag, int32_t* perm,
+                                    hipStream_t st);
+hipError_t launch_gather_rows(const void* src, int64_t ld_src_b, void* dst, int64_t ld_dst_b, int64_t rows,
+                              int64_t cols_b, const int32_t* perm, hipStream_t st);
+hipError_t launch_gather_cols(int es, const void* src, int64_t ld_src_b, void* dst, int64_t ld_dst_b, int64_t rows,
+                              int64_t cols, const int32_t* perm, hipStream_t st);
+
 // Tiled execution layout: kind 0 values, 1 metadata, 2 dense (fp8).  src is one row-major
 // region (rows x row_bytes, pitch src_ld_b); dst receives tiles x chunks blocks.
 hipError_t launch_tile(int kind, const uint8_t* src, int64_t src_ld_b, int64_t rows, int64_t row_bytes, int64_t tiles,

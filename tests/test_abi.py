@@ -41,7 +41,7 @@ def test_library_exports_every_declared_symbol(S):
     for n in _declared():
         assert hasattr(lib, n), f"{n} declared in include/ but not exported"
     assert set(_declared()) == set(S.EXPORTS)
-    assert S.spense_abi_version() == 3
+    assert S.spense_abi_version() == 4
 
 
 @pytest.mark.parametrize("N,K,split,db", [(256, 512, 0, 192), (256, 512, 1, 384), (25600, 5120, 0, 19200),
@@ -205,3 +205,27 @@ def test_quantize_calls_validate_arguments_on_the_host(S):
     assert g(None, 16, None, 16, S.SPENSE_BF16, 0, 16, None, 16, None, None) == S.SPENSE_OK
     assert g(8, 16, None, 16, S.SPENSE_BF16, 2, 16, 8, 16, 8, None) == S.SPENSE_ERR_ARG  # u NULL
     assert g(8, 16, 8, 8, S.SPENSE_F32, 2, 16, 8, 16, 8, None) == S.SPENSE_ERR_ARG  # ldu < I
+
+
+def test_index_calls_validate_arguments_on_the_host(S):
+    """Error paths of the dense-index selection calls return before touching the device."""
+    sc = S.spense_index_scores
+    assert sc(8, 8, 16, 8, 4, S.SPENSE_FP8_E4M3FN, 4, 16, 8, 8, 1e-8, 8, 8, None) == S.SPENSE_ERR_ARG  # fp8 weights
+    assert sc(8, 8, 16, 8, 4, S.SPENSE_BF16, 0, 16, 8, 8, 1e-8, 8, 8, None) == S.SPENSE_ERR_ARG  # I = 0
+    assert sc(8, None, 16, 8, 4, S.SPENSE_BF16, 4, 16, 8, 8, 1e-8, 8, 8, None) == S.SPENSE_ERR_ARG  # NULL
+    assert sc(8, 8, 15, 8, 4, S.SPENSE_BF16, 4, 16, 8, 8, 1e-8, 8, 8, None) == S.SPENSE_ERR_ARG  # ld_gu < D
+    assert sc(8, 8, 16, 8, 3, S.SPENSE_F32, 4, 16, 8, 8, 1e-8, 8, 8, None) == S.SPENSE_ERR_ARG  # ld_down < I
+    dp = S.spense_dense_permutation
+    assert dp(8, 4, 5, 8, 8, None) == S.SPENSE_ERR_ARG  # n_dense > I
+    assert dp(8, 4, -1, 8, 8, None) == S.SPENSE_ERR_ARG
+    assert dp(8, 0, 0, 8, 8, None) == S.SPENSE_ERR_ARG
+    assert dp(8, 4, 2, None, 8, None) == S.SPENSE_ERR_ARG
+    gr = S.spense_gather_rows
+    assert gr(None, 16, None, 16, 0, 16, None, None) == S.SPENSE_OK  # nothing to do
+    assert gr(8, 8, 8, 16, 4, 16, 8, None) == S.SPENSE_ERR_ARG  # ld_src < row bytes
+    assert gr(8, 16, 8, 16, 4, 16, None, None) == S.SPENSE_ERR_ARG  # NULL perm
+    gc = S.spense_gather_cols
+    assert gc(8, 16, 8, 16, 4, 16, 3, 8, None) == S.SPENSE_ERR_ARG  # element size
+    assert gc(8, 15, 8, 16, 4, 16, 2, 8, None) == S.SPENSE_ERR_ARG  # ld_src < cols
+    assert gc(9, 16, 8, 16, 4, 16, 2, 8, None) == S.SPENSE_ERR_ALIGN  # misaligned source
+    assert gc(None, 16, None, 16, 4, 0, 2, None, None) == S.SPENSE_OK
