@@ -13,7 +13,11 @@ Parity status: every function here is pinned by tests that do not re-use it (for
 definition vs torch's converters, brute force over all 2:4 masks, numpy fp64 matmul
 within the Higham bound, exact-integer cases, linearity of the two split variants; for
 the GLU-MLP steps: every e4m3fn code's round trip and midpoint, torch's converter, the
-odd and even parts of SiLU, and the permutation invariance of Eq. (4)).
+odd and even parts of SiLU, and the permutation invariance of Eq. (4); for the
+SpenseGPT+ index step: closed forms of the scores, the Wanda identity, brute-force TopK;
+for the SparseGPT sweep: the factor's rows against explicit inverse Hessians, Eq. (3)
+with an explicit inverse per step, the diagonal-Hessian case (magnitude pruning), the
+least-squares optimality of the dense buffer, and the edge cases).
 """
 from __future__ import annotations
 
@@ -298,3 +302,68 @@ def dense_index_permutation(total, n_dense: int) -> dict:
     perm = np.concatenate([np.flatnonzero(~is_dense), dense]).astype(np.int32)
     return {"dense": dense, "perm": perm}
 
+
+
+# ------------------------------------------------------------------ SparseGPT 2:4 with a protected dense region
+def obs_damp(H, percdamp: float = 0.01):
+    """Conditioning of the Hessian H = X^T X before the OBS sweep (sec. 3.1.2 uses
+    SparseGPT; the paper gives no constants, so SparseGPT's published ones are read in):
+    a column that no calibration input excites (H_jj = 0) gets H_jj = 1 and is reported as
+    dead (its weights are zeroed); then lambda = percdamp * mean(diag H) is added to the
+    diagonal.  Returns (damped H, dead mask).  fp64."""
+    H = np.array(H, np.float64, copy=True)
+    dead = np.diag(H) == 0
+    idx = np.flatnonzero(dead)
+    H[idx, idx] = 1.0
+    H[np.diag_indices_from(H)] += percdamp * np.mean(np.diag(H))
+    return H, dead
+
+
+def obs_factor(H, percdamp: float = 0.01):
+    """The factor the column sweep reads: U upper triangular with Hd^{-1} = U^T U, Hd the
+    damped Hessian.  Row j of U times U_jj is row j of the inverse Hessian of the columns
+    j..K-1 (those not yet frozen when column j is processed), so U_jj^2 is the OBS
+    denominator [H^{-1}]_mm of Eq. (3) for column j and U[j, j:] / U_jj its compensation
+    direction.  Library primitives: the inverse and the Cholesky factor.  Returns (U, dead)."""
+    Hd, dead = obs_damp(H, percdamp)
+    U = np.linalg.cholesky(np.linalg.inv(Hd)).T
+    return U, dead
+
+
+def obs_prune_24(W, H, dense_begin: int, percdamp: float = 0.01) -> dict:
+    """SparseGPT 2:4 pruning of W (N x K) with the trailing columns [dense_begin, K) kept
+    dense (sec. 3.1.2, Eqs. (2)-(3); sec. 3.3.1: the dense region placed last so that it
+    stays a compensation buffer).  Columns 0 .. dense_begin-1 are processed left to right
+    and frozen once processed.  At the first column of each group of four, every row
+    prunes the two weights of the group with the smallest OBS error w_m^2 / [H^{-1}]_mm
+    (Eq. (3); the denominator is U_mm^2, the one column m has when it is processed; the
+    weights as updated so far; ties prune the lower index).  Each processed column's
+    change (w_j - q_j) is compensated on the columns not yet processed along Eq. (3)'s
+    direction: W[:, j:] -= ((w_j - q_j) / U_jj) U[j, j:].  The dense columns are never
+    pruned and absorb the compensation.  Full updates every column (no blocking).  fp64.
+    Returns the pruned and compensated W, the kept mask (True = kept) and U."""
+    W = np.array(W, np.float64, copy=True)
+    N, K = W.shape
+    if dense_begin % 4 or not 0 <= dense_begin <= K:
+        raise ValueError("dense_begin must be a multiple of 4 in [0, K]")
+    U, dead = obs_factor(H, percdamp)
+    W[:, dead] = 0.0
+    keep = np.ones((N, K), bool)
+    rows = np.arange(N)[:, None]
+    for j in range(dense_begin):
+        if j % 4 == 0:
+            err = W[:, j:j + 4] ** 2 / np.diag(U)[j:j + 4] ** 2
+            order = np.argsort(err, axis=1, kind="stable")  # a library sort; stable: lower index first on ties
+            keep[rows, j + order[:, :2]] = False
+        q = np.where(keep[:, j], W[:, j], 0.0)
+        e = (W[:, j] - q) / U[j, j]
+        W[:, j + 1:] -= np.outer(e, U[j, j + 1:])
+        W[:, j] = q
+    return {"W": W, "keep": keep, "U": U, "dead": dead}
+
+
+def reconstruction_loss(W, W_hat, H) -> float:
+    """The layer reconstruction error of Eq. (2), ||X W^T - X W_hat^T||_F^2, written with
+    H = X^T X: sum over rows of (w - w_hat)^T H (w - w_hat).  fp64."""
+    D = np.asarray(W, np.float64) - np.asarray(W_hat, np.float64)
+    return float(np.einsum("nk,kl,nl->", D, np.asarray(H, np.float64), D))

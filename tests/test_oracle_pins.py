@@ -547,3 +547,120 @@ def test_dense_index_permutation_brute_force():
         assert sorted(perm.tolist()) == list(range(n))  # a permutation
         assert set(perm[n - k:].tolist()) == set(best)  # dense indices at the back
         assert np.all(np.diff(perm[: n - k]) > 0) and np.all(np.diff(perm[n - k:]) > 0)
+
+
+# ---------------------------------------------------------------- SparseGPT 2:4 with a protected dense region
+def _spd(seed, K, M=None, corr=0.3):
+    """H = X^T X of correlated synthetic activations (M x K)."""
+    r = np.random.default_rng(seed)
+    M = M or 4 * K
+    X = r.standard_normal((M, K)) @ (np.eye(K) + corr * r.standard_normal((K, K)) / np.sqrt(K))
+    return X.T @ X
+
+
+def test_obs_factor_rows_are_the_sequential_inverse_hessians():
+    """Row j of U (scaled by U_jj) is row 0 of inv(Hd[j:, j:]), the inverse Hessian of the
+    columns not yet frozen when column j is processed: the OBS quantities of Eq. (3)."""
+    H = _spd(1, 14)
+    U, _ = oracle.obs_factor(H, 0.01)
+    Hd, _ = oracle.obs_damp(H, 0.01)
+    assert np.allclose(np.tril(U, -1), 0)
+    for j in range(14):
+        row = np.linalg.inv(Hd[j:, j:])[0]
+        assert np.allclose(U[j, j] * U[j, j:], row, rtol=1e-10, atol=1e-14)
+
+
+def _explicit_obs(W, H, dense_begin, percdamp=0.01):
+    """Eq. (3) written out with an explicit inverse per step: before column j is processed
+    the free set is F = {j, ..., K-1}; the denominator of column m is [inv(Hd[m:, m:])]_00."""
+    Hd, dead = oracle.obs_damp(H, percdamp)
+    W = np.array(W, np.float64)
+    W[:, dead] = 0
+    N, K = W.shape
+    keep = np.ones((N, K), bool)
+    d = [np.linalg.inv(Hd[m:, m:])[0, 0] for m in range(K)]
+    for j in range(dense_begin):
+        if j % 4 == 0:
+            for n in range(N):
+                errs = [(W[n, j + c] ** 2 / d[j + c], c) for c in range(4)]
+                for _, c in sorted(errs)[:2]:
+                    keep[n, j + c] = False
+        Hinv = np.linalg.inv(Hd[j:, j:])
+        for n in range(N):
+            q = W[n, j] if keep[n, j] else 0.0
+            W[n, j:] -= (W[n, j] - q) / Hinv[0, 0] * Hinv[0]
+            W[n, j] = q
+    return W, keep
+
+
+def test_obs_sweep_matches_eq3_with_explicit_inverses():
+    H = _spd(2, 24)
+    W = np.random.default_rng(3).standard_normal((6, 24))
+    ref_W, ref_keep = _explicit_obs(W, H, 16)
+    out = oracle.obs_prune_24(W, H, 16)
+    assert np.array_equal(out["keep"], ref_keep)
+    assert np.allclose(out["W"], ref_W, rtol=1e-9, atol=1e-12)
+
+
+def test_obs_with_a_diagonal_hessian_is_magnitude_pruning():
+    """Uncorrelated inputs: no compensation (U is diagonal); each group keeps the two
+    weights with the largest |w| sqrt(h_jj + lambda), unchanged; the rest become 0."""
+    r = np.random.default_rng(4)
+    K, N = 32, 7
+    h = r.uniform(0.1, 5.0, K)
+    W = r.standard_normal((N, K))
+    out = oracle.obs_prune_24(W, np.diag(h), 24)
+    hd = h + 0.01 * h.mean()
+    for n in range(N):
+        for g in range(6):
+            s = [abs(W[n, 4 * g + c]) * np.sqrt(hd[4 * g + c]) for c in range(4)]
+            top = sorted(range(4), key=lambda c: -s[c])[:2]
+            for c in range(4):
+                want = W[n, 4 * g + c] if c in top else 0.0
+                assert out["W"][n, 4 * g + c] == want and out["keep"][n, 4 * g + c] == (c in top)
+    assert np.array_equal(out["W"][:, 24:], W[:, 24:])
+
+
+def test_obs_dense_buffer_is_the_least_squares_compensation():
+    """After the sweep the dense columns hold the best compensation for the frozen 2:4
+    columns: w_D - Hd_DD^{-1} Hd_DS (w_hat_S - w_S) minimises Eq. (2) over the dense
+    entries (damped Hessian)."""
+    H = _spd(5, 40)
+    W = np.random.default_rng(6).standard_normal((5, 40))
+    out = oracle.obs_prune_24(W, H, 24)
+    Hd, _ = oracle.obs_damp(H, 0.01)
+    S, D = slice(0, 24), slice(24, 40)
+    want = W[:, D] - np.linalg.solve(Hd[D, D], Hd[D, S] @ (out["W"][:, S] - W[:, S]).T).T
+    assert np.allclose(out["W"][:, D], want, rtol=1e-9, atol=1e-11)
+
+
+def test_obs_edge_cases():
+    H = _spd(7, 16)
+    W = np.random.default_rng(8).standard_normal((3, 16))
+    out = oracle.obs_prune_24(W, H, 0)  # all dense: nothing changes
+    assert np.array_equal(out["W"], W) and out["keep"].all()
+    out = oracle.obs_prune_24(W, H, 16)  # all 2:4
+    assert (out["keep"].reshape(3, 4, 4).sum(-1) == 2).all()
+    assert np.array_equal(out["W"] != 0, out["keep"])
+    H2 = H.copy()
+    H2[5, :] = 0
+    H2[:, 5] = 0  # a column no input excites
+    out = oracle.obs_prune_24(W, H2, 8)
+    assert (out["W"][:, 5] == 0).all() and np.isfinite(out["W"]).all()
+
+
+def test_back_placement_keeps_the_dense_columns_as_a_compensation_buffer():
+    """Sec. 3.3.1 (Table "front_back"): with the same dense columns, processing them last
+    (they absorb the compensation) reconstructs better than processing them first (they
+    are frozen before any 2:4 column is pruned).  Front placement is the sweep over the
+    2:4 columns alone (their inverse Hessians involve only unprocessed 2:4 columns) with
+    the dense columns unchanged.  An observed property on seeded correlated data."""
+    K, nd = 64, 16
+    H = _spd(9, K, corr=1.0)
+    W = np.random.default_rng(10).standard_normal((16, K))
+    back = oracle.obs_prune_24(W, H, K - nd)["W"]
+    S = slice(0, K - nd)
+    front = W.copy()
+    front[:, S] = oracle.obs_prune_24(W[:, S], H[S, S], K - nd)["W"]
+    lb, lf = oracle.reconstruction_loss(W, back, H), oracle.reconstruction_loss(W, front, H)
+    assert lb < 0.9 * lf, (lb, lf)
