@@ -257,7 +257,57 @@ def measure_extras(args, torch, gen, S, ws, pws, copies, swd, mx, dws, dense_cop
                            "glu_quantize_gbs": round(glu_bytes / (gms * 1e-3) / 1e9, 1)}
     del sets, dsets, io, Gb, Ub, Hq
     ex["qwen3_index_selection"] = measure_index_selection(torch, S)
+    ex["sparsegpt_obs"] = measure_obs(torch, S)
     return ex
+
+
+def synthetic_hessian(torch, K, seed, M=4096.0, rank=64):
+    """A calibration-like Hessian on the device: M (C^T C + diag(d)) + F F^T with
+    C = I + 0.3 (shift) and F a K x rank Gaussian block of variance M / (2K)."""
+    g = torch.Generator(device="cuda").manual_seed(seed)
+    d = torch.rand(K, generator=g, device="cuda")
+    H = torch.zeros((K, K), dtype=torch.float32, device="cuda")
+    idx = torch.arange(K, device="cuda")
+    H[idx, idx] = M * (1.09 + d)
+    H[idx[:-1], idx[:-1] + 1] = M * 0.3
+    H[idx[:-1] + 1, idx[:-1]] = M * 0.3
+    F = torch.randn((K, rank), generator=g, device="cuda") * (0.5 * M / K) ** 0.5
+    H += F @ F.t()
+    return H
+
+
+def measure_obs(torch, S):
+    """SparseGPT 2:4 with the dense region last (sec. 3.1.2, 3.3.1) at the MLP shapes of
+    the workload: gate / up (the 19200 2:4 rows of 25600 x 5120, K = 5120) and down
+    (5120 x 25600, the last 6400 columns dense).  The factor is a Cholesky factorisation
+    plus a triangular inverse (2 K^3 / 3 flops); the sweep's trailing updates are
+    sum_blocks 2 N 64 (K - j0 - 64) flops."""
+    out = {}
+    for name, N, K, db in (("gate_up", 19200, 5120, 5120), ("down", 5120, 25600, 19200)):
+        H = synthetic_hessian(torch, K, 7 + K)
+        g = torch.Generator(device="cuda").manual_seed(K)
+        W0 = torch.randn((N, K), generator=g, device="cuda") * 0.02
+        ws = S.Workspace(H.device)
+        S.obs_factor(H, workspace=ws)  # warm
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        ev[0].record()
+        U, dead = S.obs_factor(H, workspace=ws)
+        ev[1].record()
+        W = W0.clone()
+        S.obs_prune_24(W, U, db, dead, workspace=ws)  # warm
+        W.copy_(W0)
+        ev[2].record()
+        S.obs_prune_24(W, U, db, dead, workspace=ws)
+        ev[3].record()
+        torch.cuda.synchronize()
+        fms, pms = ev[0].elapsed_time(ev[1]), ev[2].elapsed_time(ev[3])
+        f_flops = 2.0 * K ** 3 / 3
+        p_flops = sum(2.0 * N * 64 * (K - j0 - 64) for j0 in range(0, db, 64) if K - j0 - 64 > 0)
+        out[name] = {"N": N, "K": K, "dense_begin": db, "factor_ms": round(fms, 2),
+                     "factor_tflops": round(f_flops / (fms * 1e-3) / 1e12, 1), "sweep_ms": round(pms, 2),
+                     "sweep_tflops": round(p_flops / (pms * 1e-3) / 1e12, 1)}
+        del H, U, W, W0, ws
+    return out
 
 
 def measure_index_selection(torch, S):
@@ -304,6 +354,8 @@ def main():
                     help="run only a torch device copy of this size (rocprof counter calibration)")
     ap.add_argument("--skip-extras", action="store_true",
                     help="omit the layer-set, M=2048 and copy-bandwidth measurements")
+    ap.add_argument("--profile-offline", action="store_true",
+                    help="time only the offline steps (index selection, SparseGPT factor and sweep)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -327,6 +379,11 @@ def main():
 
     import gen
     import paper_2606_10445_amd as S
+
+    if args.profile_offline:
+        print(json.dumps({"qwen3_index_selection": measure_index_selection(torch, S),
+                          "sparsegpt_obs": measure_obs(torch, S)}))
+        return
 
     t_setup = time.perf_counter()
     mx = gen.make_matrix(2, 0, "gate_up", N, K, gen.OUTPUT, DENSE_FRAC, gen.FP8)

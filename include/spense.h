@@ -37,7 +37,7 @@
 extern "C" {
 #endif
 
-#define SPENSE_ABI_VERSION 4
+#define SPENSE_ABI_VERSION 5
 
 typedef enum spense_status {
   SPENSE_OK = 0,
@@ -46,7 +46,8 @@ typedef enum spense_status {
   SPENSE_ERR_MASK = -3,   /* the mask keeps more than 2 of 4 in some sparse-region group */
   SPENSE_ERR_WS = -4,     /* workspace missing or too small */
   SPENSE_ERR_HIP = -5,    /* a HIP runtime call or kernel launch failed */
-  SPENSE_ERR_DEVICE = -6  /* the current device is not a gfx950 */
+  SPENSE_ERR_DEVICE = -6, /* the current device is not a gfx950 */
+  SPENSE_ERR_NUMERIC = -7 /* a Hessian is not positive definite even after damping */
 } spense_status;
 
 typedef enum spense_dtype {
@@ -313,6 +314,48 @@ int spense_gather_rows(const void* src, int64_t ld_src_b, void* dst, int64_t ld_
  */
 int spense_gather_cols(const void* src, int64_t ld_src, void* dst, int64_t ld_dst, int64_t rows, int64_t cols,
                        int32_t elem_bytes, const int32_t* perm, hipStream_t stream);
+
+/*
+ * SparseGPT 2:4 pruning with the dense region kept last (sec. 3.1.2, Eqs. (2)-(3); sec.
+ * 3.3.1: the dense columns stay a compensation buffer while the 2:4 columns before them
+ * are pruned).  Two offline calls, both on fp32 weights before quantisation.
+ *
+ * spense_obs_factor: from H = X^T X (K x K fp32, leading dimension ldh; only the lower
+ * triangle is read, so a lower-only accumulation suffices), the damped Hessian
+ * Hd = H + lambda I with lambda = percdamp * mean(diag H), where a zero diagonal entry
+ * (a column no calibration input excites) is read as 1 and flagged in dead[j] (K bytes,
+ * output).  Writes U (K x K fp32, ldu, upper triangular, zeros below the diagonal) with
+ * Hd^{-1} = U^T U: U_jj^2 is the OBS denominator [H^{-1}]_mm of Eq. (3) for column j and
+ * U[j, j:] / U_jj its compensation direction, the inverse Hessian of the columns j..K-1.
+ * ws: spense_obs_factor_workspace_size(K) bytes, 16-byte aligned.  U must not overlap H.
+ * Synchronous (reads back a failure flag).  SPENSE_ERR_NUMERIC if a pivot is not
+ * positive; SPENSE_ERR_ARG for NULL pointers, K < 1 or above 2^31-1, ld < K, percdamp
+ * negative or not finite, overlapping H and U; SPENSE_ERR_ALIGN for unaligned pointers.
+ */
+size_t spense_obs_factor_workspace_size(int64_t K);
+int spense_obs_factor(const float* H, int64_t ldh, int64_t K, float percdamp, float* U, int64_t ldu, uint8_t* dead,
+                      void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * spense_obs_prune_24: prunes W (N x K fp32, ldw; in place) to 2:4 on the columns
+ * [0, dense_begin) and compensates, keeping the columns [dense_begin, K) dense.  Columns
+ * are processed left to right and frozen once processed.  At the first column of each
+ * group of four, each row prunes the two weights with the smallest OBS error w^2 / U_mm^2
+ * (the weights as updated so far; equal errors prune the lower index first); each
+ * processed column's change is then compensated on the later columns along U's row
+ * (Eq. (3)).  dead (K bytes from spense_obs_factor, or NULL): those columns are zeroed
+ * first.  keep (N x K bytes, ldk, output): 1 where a weight is kept (every dense column),
+ * 0 where pruned.  dense_begin % 4 == 0.  For an output-split matrix pass the 2:4 rows
+ * only, with dense_begin = K (the dense rows are not touched).  ws:
+ * spense_obs_prune_workspace_size(N) bytes, 16-byte aligned.  Asynchronous.  U as written
+ * by spense_obs_factor for this K.  SPENSE_ERR_ARG for NULL pointers, sizes below 0 or
+ * above 2^31-1, ld below the row length, dense_begin not a multiple of 4 or outside
+ * [0, K]; SPENSE_ERR_WS for a missing or small workspace.
+ */
+size_t spense_obs_prune_workspace_size(int64_t N);
+int spense_obs_prune_24(float* W, int64_t ldw, int64_t N, int64_t K, const float* U, int64_t ldu, const uint8_t* dead,
+                        int64_t dense_begin, uint8_t* keep, int64_t ldk, void* ws, size_t ws_bytes,
+                        hipStream_t stream);
 
 /* Thread-local description of the last error raised on this thread ("" if none). */
 const char* spense_last_error(void);

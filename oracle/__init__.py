@@ -330,7 +330,7 @@ def obs_factor(H, percdamp: float = 0.01):
     return U, dead
 
 
-def obs_prune_24(W, H, dense_begin: int, percdamp: float = 0.01) -> dict:
+def obs_prune_24(W, H, dense_begin: int, percdamp: float = 0.01, factor=None) -> dict:
     """SparseGPT 2:4 pruning of W (N x K) with the trailing columns [dense_begin, K) kept
     dense (sec. 3.1.2, Eqs. (2)-(3); sec. 3.3.1: the dense region placed last so that it
     stays a compensation buffer).  Columns 0 .. dense_begin-1 are processed left to right
@@ -341,25 +341,29 @@ def obs_prune_24(W, H, dense_begin: int, percdamp: float = 0.01) -> dict:
     change (w_j - q_j) is compensated on the columns not yet processed along Eq. (3)'s
     direction: W[:, j:] -= ((w_j - q_j) / U_jj) U[j, j:].  The dense columns are never
     pruned and absorb the compensation.  Full updates every column (no blocking).  fp64.
-    Returns the pruned and compensated W, the kept mask (True = kept) and U."""
+    factor: (U, dead) from obs_factor of the same H and percdamp, to reuse it over row
+    samples.  Returns the pruned and compensated W, the kept mask (True = kept), the OBS
+    error each 2:4 weight had when its group was chosen ("err", N x dense_begin) and U."""
     W = np.array(W, np.float64, copy=True)
     N, K = W.shape
     if dense_begin % 4 or not 0 <= dense_begin <= K:
         raise ValueError("dense_begin must be a multiple of 4 in [0, K]")
-    U, dead = obs_factor(H, percdamp)
+    U, dead = obs_factor(H, percdamp) if factor is None else factor
     W[:, dead] = 0.0
     keep = np.ones((N, K), bool)
+    errs = np.zeros((N, dense_begin))
     rows = np.arange(N)[:, None]
     for j in range(dense_begin):
         if j % 4 == 0:
             err = W[:, j:j + 4] ** 2 / np.diag(U)[j:j + 4] ** 2
+            errs[:, j:j + 4] = err
             order = np.argsort(err, axis=1, kind="stable")  # a library sort; stable: lower index first on ties
             keep[rows, j + order[:, :2]] = False
         q = np.where(keep[:, j], W[:, j], 0.0)
         e = (W[:, j] - q) / U[j, j]
         W[:, j + 1:] -= np.outer(e, U[j, j + 1:])
         W[:, j] = q
-    return {"W": W, "keep": keep, "U": U, "dead": dead}
+    return {"W": W, "keep": keep, "err": errs, "U": U, "dead": dead}
 
 
 def reconstruction_loss(W, W_hat, H) -> float:

@@ -27,6 +27,7 @@ SPENSE_ERR_MASK = -3
 SPENSE_ERR_WS = -4
 SPENSE_ERR_HIP = -5
 SPENSE_ERR_DEVICE = -6
+SPENSE_ERR_NUMERIC = -7
 SPENSE_FP8_E4M3FN = 1
 SPENSE_BF16 = 2
 SPENSE_F32 = 3
@@ -41,7 +42,8 @@ EXPORTS = ["spense_abi_version", "spense_last_error", "spense_layout", "spense_t
            "spense_compress_workspace_size", "spense_compress", "spense_decompress", "spense_tile",
            "spense_gemm_workspace_size", "spense_gemm", "spense_dense_gemm_workspace_size", "spense_dense_gemm",
            "spense_quantize_fp8", "spense_glu_quantize_fp8", "spense_index_scores", "spense_dense_permutation",
-           "spense_gather_rows", "spense_gather_cols"]
+           "spense_gather_rows", "spense_gather_cols", "spense_obs_factor_workspace_size", "spense_obs_factor",
+           "spense_obs_prune_workspace_size", "spense_obs_prune_24"]
 
 
 class SpenseError(RuntimeError):
@@ -95,6 +97,10 @@ def _load():
         "spense_dense_permutation": (ctypes.c_int, [p, i64, i64, p, p, p]),
         "spense_gather_rows": (ctypes.c_int, [p, i64, p, i64, i64, i64, p, p]),
         "spense_gather_cols": (ctypes.c_int, [p, i64, p, i64, i64, i64, i32, p, p]),
+        "spense_obs_factor_workspace_size": (sz, [i64]),
+        "spense_obs_factor": (ctypes.c_int, [p, i64, i64, ctypes.c_float, p, i64, p, p, sz, p]),
+        "spense_obs_prune_workspace_size": (sz, [i64]),
+        "spense_obs_prune_24": (ctypes.c_int, [p, i64, i64, i64, p, i64, p, i64, p, i64, p, sz, p]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -195,6 +201,22 @@ def spense_gather_rows(src, ld_src_b, dst, ld_dst_b, rows, row_bytes, perm, stre
 
 def spense_gather_cols(src, ld_src, dst, ld_dst, rows, cols, elem_bytes, perm, stream) -> int:
     return _lib.spense_gather_cols(src, ld_src, dst, ld_dst, rows, cols, elem_bytes, perm, stream)
+
+
+def spense_obs_factor_workspace_size(K: int) -> int:
+    return _lib.spense_obs_factor_workspace_size(K)
+
+
+def spense_obs_factor(H, ldh, K, percdamp, U, ldu, dead, ws, ws_bytes, stream) -> int:
+    return _lib.spense_obs_factor(H, ldh, K, percdamp, U, ldu, dead, ws, ws_bytes, stream)
+
+
+def spense_obs_prune_workspace_size(N: int) -> int:
+    return _lib.spense_obs_prune_workspace_size(N)
+
+
+def spense_obs_prune_24(W, ldw, N, K, U, ldu, dead, dense_begin, keep, ldk, ws, ws_bytes, stream) -> int:
+    return _lib.spense_obs_prune_24(W, ldw, N, K, U, ldu, dead, dense_begin, keep, ldk, ws, ws_bytes, stream)
 
 
 # ------------------------------------------------------------------ torch helpers
@@ -488,3 +510,39 @@ def select_dense_indices(Wg: torch.Tensor, Wu: torch.Tensor, Wd: torch.Tensor, h
     flags, perm = dense_permutation(sc["total"], n_dense)
     return {"scores": sc, "flags": flags, "perm": perm, "Wg": gather_rows(Wg, perm), "Wu": gather_rows(Wu, perm),
             "Wd": gather_cols(Wd, perm)}
+
+
+# ------------------------------------------------------------------ SparseGPT 2:4 with a protected dense region
+def obs_factor(H: torch.Tensor, percdamp: float = 0.01, workspace: Workspace | None = None):
+    """The inverse-Hessian factor of the SparseGPT sweep (spense_obs_factor): H (K x K fp32,
+    lower triangle read) -> (U upper K x K with (H + lambda I)^{-1} = U^T U, dead uint8 K).
+    Synchronous."""
+    _row_major(H, "H")
+    if H.dtype != torch.float32 or H.shape[0] != H.shape[1]:
+        raise ValueError("H must be a square fp32 matrix")
+    K = H.shape[0]
+    U = torch.empty((K, K), dtype=torch.float32, device=H.device)
+    dead = torch.empty(K, dtype=torch.uint8, device=H.device)
+    ws = workspace or workspace_for(H.device)
+    wp, wn = ws.get(spense_obs_factor_workspace_size(K))
+    _check(spense_obs_factor(_ptr(H), H.stride(0), K, percdamp, _ptr(U), U.stride(0), _ptr(dead), wp, wn,
+                             _stream(H.device)))
+    return U, dead
+
+
+def obs_prune_24(W: torch.Tensor, U: torch.Tensor, dense_begin: int, dead: torch.Tensor | None = None,
+                 workspace: Workspace | None = None):
+    """SparseGPT 2:4 on W's columns [0, dense_begin) with the columns after it kept dense
+    and compensated (spense_obs_prune_24); W (N x K fp32) is updated in place.  Returns
+    the kept flags (uint8 N x K)."""
+    _row_major(W, "W")
+    _row_major(U, "U")
+    if W.dtype != torch.float32 or U.dtype != torch.float32 or U.shape != (W.shape[1], W.shape[1]):
+        raise ValueError("W (N x K) and U (K x K) must be fp32")
+    N, K = W.shape
+    keep = torch.empty((N, K), dtype=torch.uint8, device=W.device)
+    ws = workspace or workspace_for(W.device)
+    wp, wn = ws.get(spense_obs_prune_workspace_size(N))
+    _check(spense_obs_prune_24(_ptr(W), W.stride(0), N, K, _ptr(U), U.stride(0), _ptr(dead), dense_begin, _ptr(keep),
+                               keep.stride(0), wp, wn, _stream(W.device)))
+    return keep

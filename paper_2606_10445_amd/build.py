@@ -13,7 +13,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libspense.so")
-SOURCES = ["spense_api.cpp", "spense_gemm.hip", "spense_compress.hip", "spense_quant.hip", "spense_index.hip"]
+SOURCES = ["spense_api.cpp", "spense_gemm.hip", "spense_compress.hip", "spense_quant.hip", "spense_index.hip", "spense_obs.hip"]
 ARCH = "gfx950"
 
 # -packed-fp32-ops: keep the compiler from forming packed fp32 VALU instructions.

@@ -2,6 +2,8 @@
 // spense_compress), work planning and kernel dispatch.  See include/spense.h.
 #include <hip/hip_runtime.h>
 
+#include <cmath>
+
 #include <algorithm>
 #include <atomic>
 #include <cstdarg>
@@ -486,6 +488,56 @@ int spense_quantize_fp8(const void* src, int32_t src_type, int64_t M, int64_t K,
   const int64_t es = src_type == SPENSE_BF16 ? 2 : 4;
   if (spense::launch_quantize(src_type, src, ld_src * es, M, K, q, ldq, scales, stream) != hipSuccess)
     return fail(SPENSE_ERR_HIP, "quantize launch failed");
+  return ok();
+}
+
+size_t spense_obs_factor_workspace_size(int64_t K) { return K < 1 ? 0 : spense::obs_factor_workspace(K); }
+
+int spense_obs_factor(const float* H, int64_t ldh, int64_t K, float percdamp, float* U, int64_t ldu, uint8_t* dead,
+                      void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (K < 1 || K > INT32_MAX) return fail(SPENSE_ERR_ARG, "bad K=%lld", (long long)K);
+  if (!H || !U || !dead) return fail(SPENSE_ERR_ARG, "NULL pointer");
+  if (ldh < K || ldu < K) return fail(SPENSE_ERR_ARG, "leading dimension below K");
+  if (!(percdamp >= 0.0f) || !std::isfinite(percdamp)) return fail(SPENSE_ERR_ARG, "percdamp must be >= 0 and finite");
+  const uintptr_t h0 = reinterpret_cast<uintptr_t>(H), h1 = h0 + (uintptr_t)(((K - 1) * ldh + K) * 4);
+  const uintptr_t u0 = reinterpret_cast<uintptr_t>(U), u1 = u0 + (uintptr_t)(((K - 1) * ldu + K) * 4);
+  if (h0 < u1 && u0 < h1) return fail(SPENSE_ERR_ARG, "U overlaps H");
+  if (h0 % 4 || u0 % 4) return fail(SPENSE_ERR_ALIGN, "H and U must be 4-byte aligned");
+  if (!ws || ws_bytes < spense::obs_factor_workspace(K) || !aligned16(ws))
+    return fail(SPENSE_ERR_WS, "a 16-byte aligned workspace of %zu bytes is needed", spense::obs_factor_workspace(K));
+  int rc = check_device();
+  if (rc) return rc;
+  int* flag = spense::obs_factor_fail_flag(ws, K);
+  hipError_t e = spense::launch_zero_u64(reinterpret_cast<unsigned long long*>(flag), stream);
+  if (e == hipSuccess) e = spense::launch_obs_factor(H, ldh, K, percdamp, U, ldu, dead, ws, stream);
+  if (e != hipSuccess) return fail(SPENSE_ERR_HIP, "launch failed: %s", hipGetErrorString(e));
+  int host_fail = 0;
+  e = hipMemcpyAsync(&host_fail, flag, sizeof host_fail, hipMemcpyDeviceToHost, stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  if (e != hipSuccess) return fail(SPENSE_ERR_HIP, "factor failed: %s", hipGetErrorString(e));
+  if (host_fail) return fail(SPENSE_ERR_NUMERIC, "the damped Hessian is not positive definite");
+  return ok();
+}
+
+size_t spense_obs_prune_workspace_size(int64_t N) { return N < 1 ? 0 : spense::obs_prune_workspace(N); }
+
+int spense_obs_prune_24(float* W, int64_t ldw, int64_t N, int64_t K, const float* U, int64_t ldu, const uint8_t* dead,
+                        int64_t dense_begin, uint8_t* keep, int64_t ldk, void* ws, size_t ws_bytes,
+                        hipStream_t stream) {
+  if (N < 0 || K < 0 || N > INT32_MAX || K > INT32_MAX) return fail(SPENSE_ERR_ARG, "bad size");
+  if (dense_begin < 0 || dense_begin > K || dense_begin % 4)
+    return fail(SPENSE_ERR_ARG, "dense_begin=%lld must be a multiple of 4 in [0, K]", (long long)dense_begin);
+  if (N == 0 || K == 0) return ok();
+  if (!W || !U || !keep) return fail(SPENSE_ERR_ARG, "NULL pointer");
+  if (ldw < K || ldu < K || ldk < K) return fail(SPENSE_ERR_ARG, "leading dimension below K");
+  if (reinterpret_cast<uintptr_t>(W) % 4 || reinterpret_cast<uintptr_t>(U) % 4)
+    return fail(SPENSE_ERR_ALIGN, "W and U must be 4-byte aligned");
+  if (!ws || ws_bytes < spense::obs_prune_workspace(N) || !aligned16(ws))
+    return fail(SPENSE_ERR_WS, "a 16-byte aligned workspace of %zu bytes is needed", spense::obs_prune_workspace(N));
+  int rc = check_device();
+  if (rc) return rc;
+  if (spense::launch_obs_prune(W, ldw, N, K, U, ldu, dead, dense_begin, keep, ldk, ws, stream) != hipSuccess)
+    return fail(SPENSE_ERR_HIP, "prune launch failed");
   return ok();
 }
 

@@ -105,6 +105,16 @@ hipError_t launch_gather_rows(const void* src, int64_t ld_src_b, void* dst, int6
 hipError_t launch_gather_cols(int es, const void* src, int64_t ld_src_b, void* dst, int64_t ld_dst_b, int64_t rows,
                               int64_t cols, const int32_t* perm, hipStream_t st);
 
+// SparseGPT 2:4 with a protected dense region: the inverse-Hessian factor and the sweep.
+size_t obs_factor_workspace(int64_t K);
+int* obs_factor_fail_flag(void* ws, int64_t K);
+hipError_t launch_obs_factor(const float* H, int64_t ldh, int64_t K, float percdamp, float* U, int64_t ldu,
+                             uint8_t* dead, void* ws, hipStream_t st);
+size_t obs_prune_workspace(int64_t N);
+hipError_t launch_obs_prune(float* W, int64_t ldw, int64_t N, int64_t K, const float* U, int64_t ldu,
+                            const uint8_t* dead, int64_t dense_begin, uint8_t* keep, int64_t ldk, void* ws,
+                            hipStream_t st);
+
 // Tiled execution layout: kind 0 values, 1 metadata, 2 dense (fp8).  src is one row-major
 // region (rows x row_bytes, pitch src_ld_b); dst receives tiles x chunks blocks.
 hipError_t launch_tile(int kind, const uint8_t* src, int64_t src_ld_b, int64_t rows, int64_t row_bytes, int64_t tiles,

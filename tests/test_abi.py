@@ -41,7 +41,7 @@ def test_library_exports_every_declared_symbol(S):
     for n in _declared():
         assert hasattr(lib, n), f"{n} declared in include/ but not exported"
     assert set(_declared()) == set(S.EXPORTS)
-    assert S.spense_abi_version() == 4
+    assert S.spense_abi_version() == 5
 
 
 @pytest.mark.parametrize("N,K,split,db", [(256, 512, 0, 192), (256, 512, 1, 384), (25600, 5120, 0, 19200),
@@ -229,3 +229,27 @@ def test_index_calls_validate_arguments_on_the_host(S):
     assert gc(8, 15, 8, 16, 4, 16, 2, 8, None) == S.SPENSE_ERR_ARG  # ld_src < cols
     assert gc(9, 16, 8, 16, 4, 16, 2, 8, None) == S.SPENSE_ERR_ALIGN  # misaligned source
     assert gc(None, 16, None, 16, 4, 0, 2, None, None) == S.SPENSE_OK
+
+
+def test_obs_calls_validate_arguments_on_the_host(S):
+    """Error paths of the SparseGPT calls return before touching the device."""
+    f = S.spense_obs_factor
+    ws = S.spense_obs_factor_workspace_size(64)
+    assert ws >= 64 * 64 * 4
+    assert f(None, 64, 64, 0.01, 1 << 30, 64, 16, 1 << 12, ws, None) == S.SPENSE_ERR_ARG  # NULL H
+    assert f(1 << 20, 64, 0, 0.01, 1 << 30, 64, 16, 1 << 12, ws, None) == S.SPENSE_ERR_ARG  # K = 0
+    assert f(1 << 20, 63, 64, 0.01, 1 << 30, 64, 16, 1 << 12, ws, None) == S.SPENSE_ERR_ARG  # ldh < K
+    assert f(1 << 20, 64, 64, -1.0, 1 << 30, 64, 16, 1 << 12, ws, None) == S.SPENSE_ERR_ARG  # negative damping
+    assert f(1 << 20, 64, 64, float("nan"), 1 << 30, 64, 16, 1 << 12, ws, None) == S.SPENSE_ERR_ARG
+    assert f(1 << 20, 64, 64, 0.01, (1 << 20) + 4096, 64, 16, 1 << 12, ws, None) == S.SPENSE_ERR_ARG  # U overlaps H
+    assert "overlaps" in S.spense_last_error()
+    assert f(1 << 20, 64, 64, 0.01, 1 << 30, 64, 16, 1 << 12, ws - 1, None) == S.SPENSE_ERR_WS
+    assert f(1 << 20, 64, 64, 0.01, 1 << 30, 64, 16, (1 << 12) + 8, ws, None) == S.SPENSE_ERR_WS  # unaligned
+    p = S.spense_obs_prune_24
+    pws = S.spense_obs_prune_workspace_size(8)
+    assert p(None, 64, 0, 64, None, 64, None, 0, None, 64, None, 0, None) == S.SPENSE_OK  # N = 0
+    assert p(1 << 20, 64, 8, 64, 1 << 22, 64, None, 6, 1 << 24, 64, 1 << 12, pws, None) == S.SPENSE_ERR_ARG  # % 4
+    assert p(1 << 20, 64, 8, 64, 1 << 22, 64, None, 68, 1 << 24, 64, 1 << 12, pws, None) == S.SPENSE_ERR_ARG  # > K
+    assert p(1 << 20, 64, 8, 64, None, 64, None, 32, 1 << 24, 64, 1 << 12, pws, None) == S.SPENSE_ERR_ARG  # NULL U
+    assert p(1 << 20, 60, 8, 64, 1 << 22, 64, None, 32, 1 << 24, 64, 1 << 12, pws, None) == S.SPENSE_ERR_ARG  # ldw
+    assert p(1 << 20, 64, 8, 64, 1 << 22, 64, None, 32, 1 << 24, 64, 1 << 12, pws - 4, None) == S.SPENSE_ERR_WS
