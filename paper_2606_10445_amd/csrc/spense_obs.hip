@@ -44,13 +44,15 @@ __device__ __forceinline__ void unrolled(F&& f) {
 }
 
 // ------------------------------------------------------------------ fp32 matrix-core GEMM
-// C[i][j] = beta C[i][j] + alpha sum_k A(i, k) B(k, j) over an m x n output, with
-//   A(i, k) = TA ? A[k][i] : A[i][k],   B(k, j) = TB ? B[j][k] : B[k][j]  (row-major, ld).
+// C[i][j] = beta C[i][j] + alpha sum_k A[i][k] B(k, j) over an m x n output, row-major
+// operands, B(k, j) = TB ? B[j][k] : B[k][j].
 // LOWER: only output tiles on or below the diagonal (tile column <= tile row) are formed.
-// TRIA: A is lower triangular (A(i, k) = 0 for k > i): k stops at the tile's last row and
-// entries above the diagonal are read as 0.
-// 64 x 64 output tile per workgroup of 4 waves (2 x 2, 32 x 32 each as 2 x 2
-// v_mfma_f32_16x16x4_f32 tiles), k in steps of 16 staged through LDS (two buffers).
+// TRI (bit mask) marks triangular operands whose other half is read as 0 (and holds
+// anything in memory): 1 = A lower (A[i][k] = 0 for k > i), 2 = B(k, j) = 0 for k > j,
+// 4 = B(k, j) = 0 for k < j; the k loop is cut to the range they leave.
+// BT x BT output tile per workgroup of 4 waves (2 x 2; each BT/2 x BT/2 as TW x TW
+// v_mfma_f32_16x16x4_f32 tiles), k staged through LDS 16 deep in two buffers, 16-byte
+// loads when the operands allow.
 // Operand lanes (measured): A lane l = A[l % 16][l / 16], B lane l = B[l / 16][l % 16],
 // D lane l, element r = D[4 (l / 16) + r][l % 16].
 struct GemmF32 {
@@ -64,111 +66,131 @@ struct GemmF32 {
   float alpha, beta;
 };
 
-constexpr int GP = 68;  // LDS row pitch (floats) of the k-major operand tiles
-
-template <bool TA, bool TB, bool LOWER, bool TRIA>
-__global__ __launch_bounds__(256) void gemm_f32_kernel(GemmF32 g) {
-  __shared__ float As[2][16][GP];  // As[kk][i]
-  __shared__ float Bs[2][16][GP];  // Bs[kk][j]
+template <int BT, bool TB, bool LOWER, int TRI>
+__global__ __launch_bounds__(256) void gemm_f32_kernel(GemmF32 g, int vec) {
+  constexpr int P = BT + 4;        // LDS row pitch (floats)
+  constexpr int TW = BT / 32;      // MFMA tiles per wave and dimension
+  constexpr int NQ = BT / 64;      // 16-byte pieces per thread and operand per step
+  __shared__ float As[2][16][P];   // As[kk][i]
+  __shared__ float Bs[2][16][P];   // Bs[kk][j]
   const int tr = blockIdx.y, tc = blockIdx.x;
   if (LOWER && tc > tr) return;
-  const int64_t i0 = (int64_t)tr * 64, j0 = (int64_t)tc * 64;
+  const int64_t i0 = (int64_t)tr * BT, j0 = (int64_t)tc * BT;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const int wi = (wave >> 1) * 32, wj = (wave & 1) * 32;
-  int64_t kend = g.k;
-  if (TRIA) kend = kend < i0 + 64 ? kend : i0 + 64;
-  const int nsteps = (int)((kend + 15) / 16);
+  const int wi = (wave >> 1) * (BT / 2), wj = (wave & 1) * (BT / 2);
+  int64_t klo = 0, khi = g.k;
+  if (TRI & 1) khi = khi < i0 + BT ? khi : i0 + BT;
+  if (TRI & 2) khi = khi < j0 + BT ? khi : j0 + BT;
+  if (TRI & 4) klo = j0;
+  const int s0 = (int)(klo / 16), s1 = (int)((khi + 15) / 16);
 
-  // global -> register staging of one 16-deep step
-  float ra[4], rb[4];
-  auto load = [&](int s) __attribute__((always_inline)) {
-    const int64_t k0 = (int64_t)s * 16;
-    // A: 64 rows (i) x 16 k
-    if (!TA) {
-      const int64_t i = i0 + (t >> 2), kq = k0 + (t & 3) * 4;
+  float ra[NQ][4], rb[NQ][4];
+  // four consecutive elements of a row-major operand at (row, k), zero outside
+  // [klo, khi), past `rows` and where `keep(k)` says the triangular half is empty
+  auto quad = [&](const float* base, int64_t ld, int64_t row, int64_t rows, int64_t kq, float* out, auto keep)
+      __attribute__((always_inline)) {
+    const bool full = vec && row < rows && kq >= klo && kq + 3 < khi;
+    if (full) {
+      const float4 v = *reinterpret_cast<const float4*>(base + row * ld + kq);
+      out[0] = v.x;
+      out[1] = v.y;
+      out[2] = v.z;
+      out[3] = v.w;
+    } else {
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
         const int64_t kk = kq + c;
-        bool ok = i < g.m && kk < kend;
-        if (TRIA) ok = ok && kk <= i;
-        ra[c] = ok ? g.A[i * g.lda + kk] : 0.0f;
-      }
-    } else {  // A[k][i]: 16 k-rows of 64 i
-      const int64_t kk = k0 + (t >> 4), iq = i0 + (t & 15) * 4;
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const int64_t i = iq + c;
-        ra[c] = (i < g.m && kk < kend) ? g.A[kk * g.lda + i] : 0.0f;
+        out[c] = (row < rows && kk >= klo && kk < khi) ? base[row * ld + kk] : 0.0f;
       }
     }
-    if (!TB) {  // B[k][j]: 16 k-rows of 64 j
-      const int64_t kk = k0 + (t >> 4), jq = j0 + (t & 15) * 4;
 #pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const int64_t j = jq + c;
-        rb[c] = (j < g.n && kk < kend) ? g.B[kk * g.ldb + j] : 0.0f;
-      }
-    } else {  // B[j][k]
-      const int64_t j = j0 + (t >> 2), kq = k0 + (t & 3) * 4;
+    for (int c = 0; c < 4; ++c)
+      if (!keep(kq + c)) out[c] = 0.0f;
+  };
+  auto load = [&](int s) __attribute__((always_inline)) {
+    const int64_t k0 = (int64_t)s * 16;
 #pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const int64_t kk = kq + c;
-        rb[c] = (j < g.n && kk < kend) ? g.B[j * g.ldb + kk] : 0.0f;
+    for (int q = 0; q < NQ; ++q) {
+      const int slot = t + 256 * q;
+      const int64_t i = i0 + (slot >> 2), kq = k0 + (slot & 3) * 4;
+      quad(g.A, g.lda, i, g.m, kq, ra[q], [&](int64_t kk) { return !(TRI & 1) || kk <= i; });
+      if (TB) {
+        const int64_t j = j0 + (slot >> 2);
+        quad(g.B, g.ldb, j, g.n, kq, rb[q], [&](int64_t kk) {
+          return (!(TRI & 2) || kk <= j) && (!(TRI & 4) || kk >= j);
+        });
+      } else {
+        const int64_t kk = k0 + slot / (BT / 4), jq = j0 + (slot % (BT / 4)) * 4;
+        const bool full = vec && kk >= klo && kk < khi && jq + 3 < g.n;
+        if (full) {
+          const float4 v = *reinterpret_cast<const float4*>(g.B + kk * g.ldb + jq);
+          rb[q][0] = v.x;
+          rb[q][1] = v.y;
+          rb[q][2] = v.z;
+          rb[q][3] = v.w;
+        } else {
+#pragma unroll
+          for (int c = 0; c < 4; ++c)
+            rb[q][c] = (kk >= klo && kk < khi && jq + c < g.n) ? g.B[kk * g.ldb + jq + c] : 0.0f;
+        }
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const int64_t j = jq + c;
+          if (((TRI & 2) && kk > j) || ((TRI & 4) && kk < j)) rb[q][c] = 0.0f;
+        }
       }
     }
   };
   auto store = [&](int buf) __attribute__((always_inline)) {
-    if (!TA) {
 #pragma unroll
-      for (int c = 0; c < 4; ++c) As[buf][(t & 3) * 4 + c][t >> 2] = ra[c];
-    } else {
+    for (int q = 0; q < NQ; ++q) {
+      const int slot = t + 256 * q;
 #pragma unroll
-      for (int c = 0; c < 4; ++c) As[buf][t >> 4][(t & 15) * 4 + c] = ra[c];
-    }
-    if (!TB) {
+      for (int c = 0; c < 4; ++c) As[buf][(slot & 3) * 4 + c][slot >> 2] = ra[q][c];
+      if (TB) {
 #pragma unroll
-      for (int c = 0; c < 4; ++c) Bs[buf][t >> 4][(t & 15) * 4 + c] = rb[c];
-    } else {
-#pragma unroll
-      for (int c = 0; c < 4; ++c) Bs[buf][(t & 3) * 4 + c][t >> 2] = rb[c];
+        for (int c = 0; c < 4; ++c) Bs[buf][(slot & 3) * 4 + c][slot >> 2] = rb[q][c];
+      } else {
+        *reinterpret_cast<float4*>(&Bs[buf][slot / (BT / 4)][(slot % (BT / 4)) * 4]) =
+            make_float4(rb[q][0], rb[q][1], rb[q][2], rb[q][3]);
+      }
     }
   };
 
-  f4 acc[2][2];
+  f4 acc[TW][TW];
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < TW; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b) acc[a][b] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+    for (int b = 0; b < TW; ++b) acc[a][b] = f4{0.0f, 0.0f, 0.0f, 0.0f};
 
-  if (nsteps > 0) {
-    load(0);
+  if (s0 < s1) {
+    load(s0);
     store(0);
   }
   __syncthreads();
-  for (int s = 0; s < nsteps; ++s) {
-    const int buf = s & 1;
-    if (s + 1 < nsteps) load(s + 1);
+  for (int s = s0; s < s1; ++s) {
+    const int buf = (s - s0) & 1;
+    if (s + 1 < s1) load(s + 1);
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int kk = q * 4 + (lane >> 4);
-      float av[2], bv[2];
+      float av[TW], bv[TW];
 #pragma unroll
-      for (int a = 0; a < 2; ++a) av[a] = As[buf][kk][wi + a * 16 + (lane & 15)];
+      for (int a = 0; a < TW; ++a) av[a] = As[buf][kk][wi + a * 16 + (lane & 15)];
 #pragma unroll
-      for (int b = 0; b < 2; ++b) bv[b] = Bs[buf][kk][wj + b * 16 + (lane & 15)];
+      for (int b = 0; b < TW; ++b) bv[b] = Bs[buf][kk][wj + b * 16 + (lane & 15)];
 #pragma unroll
-      for (int a = 0; a < 2; ++a)
+      for (int a = 0; a < TW; ++a)
 #pragma unroll
-        for (int b = 0; b < 2; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[a], bv[b], acc[a][b], 0, 0, 0);
+        for (int b = 0; b < TW; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[a], bv[b], acc[a][b], 0, 0, 0);
     }
-    if (s + 1 < nsteps) store(buf ^ 1);
+    if (s + 1 < s1) store(buf ^ 1);
     __syncthreads();
   }
-  // epilogue
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < TW; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
+    for (int b = 0; b < TW; ++b) {
       const int64_t j = j0 + wj + b * 16 + (lane & 15);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
@@ -182,11 +204,17 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmF32 g) {
     }
 }
 
-template <bool TA, bool TB, bool LOWER, bool TRIA>
+template <bool TB, bool LOWER, int TRI>
 hipError_t gemm_f32(const GemmF32& g, hipStream_t st) {
   if (g.m <= 0 || g.n <= 0) return hipSuccess;
-  const dim3 grid((unsigned)((g.n + 63) / 64), (unsigned)((g.m + 63) / 64));
-  hipLaunchKernelGGL((gemm_f32_kernel<TA, TB, LOWER, TRIA>), grid, dim3(256), 0, st, g);
+  const int vec = (g.lda % 4 == 0) && (g.ldb % 4 == 0) && ((uintptr_t)g.A % 16 == 0) && ((uintptr_t)g.B % 16 == 0);
+  if (g.m >= 128 && g.n >= 128) {
+    const dim3 grid((unsigned)((g.n + 127) / 128), (unsigned)((g.m + 127) / 128));
+    hipLaunchKernelGGL((gemm_f32_kernel<128, TB, LOWER, TRI>), grid, dim3(256), 0, st, g, vec);
+  } else {
+    const dim3 grid((unsigned)((g.n + 63) / 64), (unsigned)((g.m + 63) / 64));
+    hipLaunchKernelGGL((gemm_f32_kernel<64, TB, LOWER, TRI>), grid, dim3(256), 0, st, g, vec);
+  }
   return hipGetLastError();
 }
 
@@ -233,61 +261,58 @@ __global__ __launch_bounds__(256) void reverse_damp_kernel(const float* __restri
   }
 }
 
-// Diagonal block k0 of the lower Cholesky factorisation, in place: L_kk (nb x nb, nb <=
-// 64) is factored in LDS, then replaced by its inverse L_kk^{-1} (lower, zeros above
-// the diagonal inside the block).  A non-positive or NaN pivot sets *fail and continues
-// with pivot 1 so that the remaining steps stay finite.
-__global__ __launch_bounds__(256) void potrf_block_kernel(float* __restrict__ A, int64_t lda, int64_t k0, int nb,
-                                                          int* __restrict__ fail) {
-  __shared__ float L[64][65];
-  __shared__ float X[64][65];
+// A diagonal block (n x n, n <= 64) of the lower Cholesky factorisation, in place: L is
+// factored and replaced by its inverse X = L^{-1} (lower, zeros above the diagonal
+// inside the block).  One wave; lane t holds row t of L and of the running right-hand
+// side R of L X = I in registers (every index a compile-time constant).  Step j: the
+// pivot L_jj and column j's entries reach every lane through readlane (no barriers);
+// lanes below j scale their L_tj and update their row; row j of X is R_j / L_jj and the
+// rows below subtract L_tj X_j.  A non-positive or NaN pivot sets *fail and continues
+// with pivot 1 so that the rest stays finite.
+__device__ __forceinline__ float lane_value(float v, int lane) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
+}
+
+__global__ __launch_bounds__(64) void potrf_block_kernel(float* __restrict__ A, int64_t lda, int n,
+                                                         int* __restrict__ fail) {
   const int t = threadIdx.x;
-  for (int e = t; e < 64 * 64; e += 256) {
-    const int i = e >> 6, j = e & 63;
+  float L[64], R[64];
+  unrolled<64>([&](auto cc) __attribute__((always_inline)) {
+    constexpr int c = decltype(cc)::value;
     float v = 0.0f;
-    if (i < nb && j <= i) v = A[(k0 + i) * lda + (k0 + j)];
-    else if (i == j) v = 1.0f;  // padding of a partial block: identity
-    L[i][j] = v;
-  }
-  __syncthreads();
-  for (int j = 0; j < 64; ++j) {
-    float d = L[j][j];
+    if (t < n && c <= t && c < n) v = A[t * lda + c];
+    else if (t == c) v = 1.0f;  // padding of a partial block: identity
+    L[c] = v;
+    R[c] = t == c ? 1.0f : 0.0f;
+  });
+  bool bad = false;
+  unrolled<64>([&](auto jj) __attribute__((always_inline)) {
+    constexpr int j = decltype(jj)::value;
+    float d = lane_value(L[j], j);
     if (!(d > 0.0f)) {
-      if (t == 0 && j < nb) atomicOr(fail, 1);
+      bad = bad || j < n;
       d = 1.0f;
     }
-    const float s = sqrtf(d);
-    __syncthreads();  // everyone has read L[j][j]
-    if (t == 0) L[j][j] = s;
-    if (t > j && t < 64) L[t][j] = L[t][j] / s;
-    __syncthreads();
-    // trailing update of the lower part: rows and columns j+1..63
-    for (int e = t; e < 64 * 64; e += 256) {
-      const int i = e >> 6, c = e & 63;
-      if (c > j && i >= c) L[i][c] -= L[i][j] * L[c][j];
-    }
-    __syncthreads();
-  }
-  // inverse by forward substitution, one column per thread
-  if (t < 64) {
-    const int c = t;
-    for (int i = 0; i < 64; ++i) {
-      float v;
-      if (i < c) v = 0.0f;
-      else if (i == c) v = 1.0f / L[c][c];
-      else {
-        float s = 0.0f;
-        for (int k = c; k < i; ++k) s += L[i][k] * X[k][c];
-        v = -s / L[i][i];
-      }
-      X[i][c] = v;
-    }
-  }
-  __syncthreads();
-  for (int e = t; e < 64 * 64; e += 256) {
-    const int i = e >> 6, j = e & 63;
-    if (i < nb && j < nb) A[(k0 + i) * lda + (k0 + j)] = X[i][j];
-  }
+    const float s = sqrtf(d), inv = 1.0f / s;
+    L[j] = t == j ? s : (t > j ? L[j] * inv : L[j]);
+    const float ltj = t > j ? L[j] : 0.0f;
+    // trailing columns of this lane's row
+    unrolled<63 - j>([&](auto oo) __attribute__((always_inline)) {
+      constexpr int c = j + 1 + decltype(oo)::value;
+      L[c] -= ltj * lane_value(L[j], c);
+    });
+    // row j of X, then the rows below
+    unrolled<j + 1>([&](auto cc) __attribute__((always_inline)) {
+      constexpr int c = decltype(cc)::value;
+      if (t == j) R[c] *= inv;
+      R[c] -= ltj * lane_value(R[c], j);
+    });
+  });
+  if (bad && t == 0) atomicOr(fail, 1);
+  unrolled<64>([&](auto cc) __attribute__((always_inline)) {
+    constexpr int c = decltype(cc)::value;
+    if (t < n && c < n) A[t * lda + c] = c <= t ? R[c] : 0.0f;
+  });
 }
 
 // The reversal back: U[K-1-a][K-1-b] = X[a][b] for a > b (lower -> upper), and the
@@ -336,7 +361,7 @@ __global__ __launch_bounds__(256) void zero_dead_kernel(float* __restrict__ W, i
 __global__ __launch_bounds__(256) void sweep_block_kernel(float* __restrict__ W, int64_t ldw, int64_t N, int64_t K,
                                                           const float* __restrict__ U, int64_t ldu, int64_t j0, int cnt,
                                                           uint8_t* __restrict__ keep, int64_t ldk,
-                                                          float* __restrict__ E) {
+                                                          float* __restrict__ E, int64_t lde) {
   __shared__ float Ub[64][64];
   const int width = (int)(K - j0 < 64 ? K - j0 : 64);
   for (int e = threadIdx.x; e < 64 * 64; e += 256) {
@@ -354,7 +379,7 @@ __global__ __launch_bounds__(256) void sweep_block_kernel(float* __restrict__ W,
 #pragma unroll
   for (int c = 0; c < 64; ++c) w[c] = c < width ? wr[c] : 0.0f;
   uint32_t kept[2] = {0xffffffffu, 0xffffffffu};
-  float* er = E + n * 64;
+  float* er = E + n * lde;
   unrolled<64>([&](auto cc) __attribute__((always_inline)) {
     constexpr int c = decltype(cc)::value;
     if constexpr (c % 4 == 0) {
@@ -400,81 +425,117 @@ __global__ __launch_bounds__(256) void keep_dense_kernel(uint8_t* __restrict__ k
       keep[n * ldk + j] = 1;
 }
 
+__global__ __launch_bounds__(256) void copy_f32_kernel(const float* __restrict__ src, int64_t lds, float* __restrict__ dst,
+                                                       int64_t ldd, int64_t rows, int64_t cols) {
+  for (int64_t r = blockIdx.y; r < rows; r += gridDim.y) {
+    const int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (c < cols) dst[r * ldd + c] = src[r * lds + c];
+  }
+}
+
 dim3 lower_tiles(int64_t K) {
   const unsigned t = (unsigned)((K + 63) / 64);
   return dim3(t, t);
 }
 
+// Recursive factor-and-invert of the lower part of A (n x n, in place): on return A holds
+// X = L^{-1} with L L^T = A.  With A = [[A11, .], [A21, A22]] split at n1 (a multiple of
+// 64): X11 = (L11)^{-1} recursively, L21 = A21 X11^T, A22 -= L21 L21^T, X22 recursively,
+// X21 = -X22 (L21 X11).  Every product is a large, square-ish matrix-core GEMM.
+// Workspace: L21 (n2 x n1) plus the second recursion's, behind it.
+int64_t chol_inv_ws(int64_t n) {
+  if (n <= NB) return 0;
+  const int64_t n1 = (n / 2 + NB - 1) / NB * NB, n2 = n - n1;
+  const int64_t a = chol_inv_ws(n1), b = n2 * n1 + chol_inv_ws(n2);
+  return a > b ? a : b;
+}
+
+hipError_t chol_inv(float* A, int64_t lda, int64_t n, float* ws, int* fail, hipStream_t st) {
+  if (n <= NB) {
+    hipLaunchKernelGGL(potrf_block_kernel, dim3(1), dim3(64), 0, st, A, lda, (int)n, fail);
+    return hipGetLastError();
+  }
+  const int64_t n1 = (n / 2 + NB - 1) / NB * NB, n2 = n - n1;
+  float* A11 = A;
+  float* A21 = A + n1 * lda;
+  float* A22 = A21 + n1;
+  float* L21 = ws;
+  hipError_t e = chol_inv(A11, lda, n1, ws, fail, st);
+  // L21 = A21 X11^T (X11 lower: B(k, j) = X11[j][k] vanishes for k > j)
+  if (e == hipSuccess) e = gemm_f32<true, false, 2>(GemmF32{A21, lda, A11, lda, L21, n1, n2, n1, n1, 1.0f, 0.0f}, st);
+  // A22 -= L21 L21^T, lower tiles
+  if (e == hipSuccess) e = gemm_f32<true, true, 0>(GemmF32{L21, n1, L21, n1, A22, lda, n2, n2, n1, -1.0f, 1.0f}, st);
+  if (e == hipSuccess) e = chol_inv(A22, lda, n2, ws + n2 * n1, fail, st);
+  // T = L21 X11 into A21's place (X11 lower: B(k, j) = X11[k][j] vanishes for k < j)
+  if (e == hipSuccess) e = gemm_f32<false, false, 4>(GemmF32{L21, n1, A11, lda, A21, lda, n2, n1, n1, 1.0f, 0.0f}, st);
+  // X21 = -X22 T into the workspace (X22 lower), then back into A21's place
+  if (e == hipSuccess) e = gemm_f32<false, false, 1>(GemmF32{A22, lda, A21, lda, L21, n1, n2, n1, n2, -1.0f, 0.0f}, st);
+  if (e == hipSuccess) {
+    hipLaunchKernelGGL(copy_f32_kernel, dim3((unsigned)((n1 + 255) / 256), (unsigned)(n2 < 65535 ? n2 : 65535)),
+                       dim3(256), 0, st, L21, n1, A21, lda, n2, n1);
+    e = hipGetLastError();
+  }
+  return e;
+}
+
 }  // namespace
 
-size_t obs_factor_workspace(int64_t K) { return (size_t)(K * NB + 64) * sizeof(float); }
+// Workspace: lambda at float 0, the failure flag at float 16, the recursion's from
+// float 64 on.
+size_t obs_factor_workspace(int64_t K) { return (size_t)(64 + chol_inv_ws(K)) * sizeof(float); }
 
-int* obs_factor_fail_flag(void* ws, int64_t K) { return reinterpret_cast<int*>(static_cast<float*>(ws) + K * NB + 16); }
+int* obs_factor_fail_flag(void* ws, int64_t) { return reinterpret_cast<int*>(static_cast<float*>(ws) + 16); }
 
-// Workspace: T (K x 64 fp32), lambda at float K*64, the failure flag at float K*64 + 16
-// (zeroed by the caller before the launch).
 hipError_t launch_obs_factor(const float* H, int64_t ldh, int64_t K, float percdamp, float* U, int64_t ldu,
                              uint8_t* dead, void* ws, hipStream_t st) {
-  float* T = static_cast<float*>(ws);  // K x 64 staging of the triangular inverse
-  float* stat = T + K * NB;            // lambda
+  float* stat = static_cast<float*>(ws);  // lambda
   int* fail = obs_factor_fail_flag(ws, K);
   hipLaunchKernelGGL(damp_kernel, dim3(1), dim3(1024), 0, st, H, ldh, K, percdamp, dead, stat);
   hipLaunchKernelGGL(reverse_damp_kernel, lower_tiles(K), dim3(256), 0, st, H, ldh, K, dead, stat, U, ldu);
-  const int64_t nblk = (K + NB - 1) / NB;
   hipError_t e = hipGetLastError();
-  // Cholesky, right-looking; each diagonal block is left holding its inverse
-  for (int64_t b = 0; b < nblk && e == hipSuccess; ++b) {
-    const int64_t k0 = b * NB, nb = K - k0 < NB ? K - k0 : NB, r0 = k0 + nb, rows = K - r0;
-    hipLaunchKernelGGL(potrf_block_kernel, dim3(1), dim3(256), 0, st, U, ldu, k0, (int)nb, fail);
-    if (rows > 0) {
-      // panel: L[r0:, k0:k0+nb] = A[r0:, k0:k0+nb] L_kk^{-T} (in place: a workgroup owns its rows)
-      GemmF32 g{U + r0 * ldu + k0, ldu, U + k0 * ldu + k0, ldu, U + r0 * ldu + k0, ldu, rows, nb, nb, 1.0f, 0.0f};
-      e = gemm_f32<false, true, false, false>(g, st);
-      // trailing lower part: A[r0:, r0:] -= L_panel L_panel^T
-      GemmF32 s{U + r0 * ldu + k0, ldu, U + r0 * ldu + k0, ldu, U + r0 * ldu + r0, ldu, rows, rows, nb, -1.0f, 1.0f};
-      if (e == hipSuccess) e = gemm_f32<false, true, true, false>(s, st);
-    }
-    if (e == hipSuccess) e = hipGetLastError();
-  }
-  // triangular inverse, right to left: X[r0:, k0:] = -X[r0:, r0:] (L[r0:, k0:] X_kk)
-  for (int64_t b = nblk - 1; b >= 0 && e == hipSuccess; --b) {
-    const int64_t k0 = b * NB, nb = K - k0 < NB ? K - k0 : NB, r0 = k0 + nb, rows = K - r0;
-    if (rows <= 0) continue;
-    GemmF32 g1{U + r0 * ldu + k0, ldu, U + k0 * ldu + k0, ldu, T, NB, rows, nb, nb, 1.0f, 0.0f};
-    e = gemm_f32<false, false, false, false>(g1, st);
-    GemmF32 g2{U + r0 * ldu + r0, ldu, T, NB, U + r0 * ldu + k0, ldu, rows, nb, rows, -1.0f, 0.0f};
-    if (e == hipSuccess) e = gemm_f32<false, false, false, true>(g2, st);
-  }
+  if (e == hipSuccess) e = chol_inv(U, ldu, K, stat + 64, fail, st);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(reverse_out_kernel, lower_tiles(K), dim3(256), 0, st, U, ldu, K);
   hipLaunchKernelGGL(zero_lower_kernel, lower_tiles(K), dim3(256), 0, st, U, ldu, K);
   return hipGetLastError();
 }
 
-size_t obs_prune_workspace(int64_t N) { return (size_t)N * NB * sizeof(float); }
+// The sweep in two levels: 64-column blocks inside 256-column outer blocks.  Inside an
+// outer block each 64-block's errors update only the rest of the outer block (k = 64);
+// at its end the outer block's errors update every later column at once (k = 256), so
+// the trailing columns are read and written once per 256 columns instead of per 64.
+constexpr int OB = 256;
+
+size_t obs_prune_workspace(int64_t N) { return (size_t)N * OB * sizeof(float); }
 
 hipError_t launch_obs_prune(float* W, int64_t ldw, int64_t N, int64_t K, const float* U, int64_t ldu,
                             const uint8_t* dead, int64_t dense_begin, uint8_t* keep, int64_t ldk, void* ws,
                             hipStream_t st) {
-  float* E = static_cast<float*>(ws);
+  float* E = static_cast<float*>(ws);  // N x OB: the outer block's scaled errors
   const unsigned rows_y = (unsigned)(N < 65535 ? N : 65535);
   if (dead) hipLaunchKernelGGL(zero_dead_kernel, dim3((unsigned)((K + 255) / 256 < 64 ? (K + 255) / 256 : 64), rows_y),
                                dim3(256), 0, st, W, ldw, N, K, dead);
   hipError_t e = hipGetLastError();
-  int64_t j0 = 0;
-  for (; j0 < dense_begin && e == hipSuccess; j0 += NB) {
-    const int cnt = (int)(dense_begin - j0 < NB ? dense_begin - j0 : NB);
-    hipLaunchKernelGGL(sweep_block_kernel, dim3((unsigned)((N + 255) / 256)), dim3(256), 0, st, W, ldw, N, K, U, ldu,
-                       j0, cnt, keep, ldk, E);
-    e = hipGetLastError();
-    const int64_t c0 = j0 + NB;
-    if (e == hipSuccess && c0 < K) {
-      GemmF32 g{E, NB, U + j0 * ldu + c0, ldu, W + c0, ldw, N, K - c0, NB, -1.0f, 1.0f};
-      e = gemm_f32<false, false, false, false>(g, st);
+  int64_t pe = 0;  // end of the processed 64-blocks
+  for (int64_t o0 = 0; o0 < dense_begin && e == hipSuccess; o0 += OB) {
+    const int64_t last = o0 + OB < dense_begin ? o0 + OB : dense_begin;  // 2:4 columns of this outer block end here
+    pe = o0 + (last - o0 + NB - 1) / NB * NB;                             // processed blocks end here
+    for (int64_t j0 = o0; j0 < last && e == hipSuccess; j0 += NB) {
+      const int cnt = (int)(last - j0 < NB ? last - j0 : NB);
+      hipLaunchKernelGGL(sweep_block_kernel, dim3((unsigned)((N + 255) / 256)), dim3(256), 0, st, W, ldw, N, K, U,
+                         ldu, j0, cnt, keep, ldk, E + (j0 - o0), (int64_t)OB);
+      e = hipGetLastError();
+      const int64_t c0 = j0 + NB, c1 = pe < K ? pe : K;  // the rest of the processed blocks
+      if (e == hipSuccess && c0 < c1)
+        e = gemm_f32<false, false, 0>(GemmF32{E + (j0 - o0), OB, U + j0 * ldu + c0, ldu, W + c0, ldw, N, c1 - c0, NB,
+                                              -1.0f, 1.0f}, st);
     }
+    if (e == hipSuccess && pe < K)
+      e = gemm_f32<false, false, 0>(GemmF32{E, OB, U + o0 * ldu + pe, ldu, W + pe, ldw, N, K - pe, pe - o0, -1.0f,
+                                            1.0f}, st);
   }
   if (e != hipSuccess) return e;
-  const int64_t from = j0 < K ? j0 : K;  // the sweep blocks wrote the flags of [0, j0)
+  const int64_t from = pe < K ? pe : K;  // the sweep blocks wrote the flags of [0, pe)
   if (from < K)
     hipLaunchKernelGGL(keep_dense_kernel, dim3((unsigned)((K - from + 255) / 256 < 64 ? (K - from + 255) / 256 : 64), rows_y),
                        dim3(256), 0, st, keep, ldk, N, from, K);
