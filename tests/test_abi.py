@@ -237,7 +237,7 @@ def test_obs_calls_validate_arguments_on_the_host(S):
     ws = S.spense_obs_factor_workspace_size(64)
     assert ws == 256  # a single 64-block: no recursion workspace
     big = S.spense_obs_factor_workspace_size(25600)  # the recursion's L21 blocks, about K^2 / 3 floats
-    assert 25600 ** 2 / 3 * 4 <= big <= 25600 ** 2 / 2 * 4
+    assert 25600 ** 2 / 4 * 4 <= big <= 25600 ** 2 / 2 * 4
     assert f(None, 64, 64, 0.01, 1 << 30, 64, 16, 1 << 12, ws, None) == S.SPENSE_ERR_ARG  # NULL H
     assert f(1 << 20, 64, 0, 0.01, 1 << 30, 64, 16, 1 << 12, ws, None) == S.SPENSE_ERR_ARG  # K = 0
     assert f(1 << 20, 63, 64, 0.01, 1 << 30, 64, 16, 1 << 12, ws, None) == S.SPENSE_ERR_ARG  # ldh < K
