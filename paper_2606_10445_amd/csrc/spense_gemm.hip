@@ -978,7 +978,14 @@ __global__ __launch_bounds__(64 * WV) void spense_gemm_big_kernel(GemmArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int li = lane & 15, lq = lane >> 4;
   const int wr = wave & 1, wc = wave >> 1;
-  const int g = blockIdx.x;
+  int g = blockIdx.x;
+  if (a.xgt > 0) {
+    // XCD-aware order: XCD x (= id % 8) takes token group x % (T / GT) (GT blocks) and
+    // the row blocks of class x / (T / GT) (every RC-th); a bijection on the grid
+    const int T = a.tblocks, GT = a.xgt, RC = a.xrc, TGc = T / GT;
+    const int x = g & 7, l = g >> 3, tg = x % TGc, rc = x / TGc;
+    g = ((l / GT) * RC + rc) * T + tg * GT + l % GT;
+  }
   const int ri = (a.nreg > 1 && g >= a.reg[1].wg0) ? 1 : 0;
   const Region& R = a.reg[ri];
   const int rowend = R.row0 + R.rows;

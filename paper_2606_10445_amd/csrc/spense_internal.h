@@ -57,6 +57,7 @@ struct GemmArgs {
   int32_t tiled;  // weight buffers in the tiled execution layout (fp8, row-split kernel)
   float* part;    // fp32 partial sums of K-sliced regions: part[(slice * M + m) * N + n]
   int32_t tblocks;  // large-M kernel: 256-token blocks (workgroups of a row block are adjacent)
+  int32_t xgt, xrc;  // large-M kernel, XCD-aware order (0 = off): token blocks per XCD, row classes
   Region reg[2];
 };
 

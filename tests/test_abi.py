@@ -255,3 +255,20 @@ def test_obs_calls_validate_arguments_on_the_host(S):
     assert p(1 << 20, 64, 8, 64, None, 64, None, 32, 1 << 24, 64, 1 << 12, pws, None) == S.SPENSE_ERR_ARG  # NULL U
     assert p(1 << 20, 60, 8, 64, 1 << 22, 64, None, 32, 1 << 24, 64, 1 << 12, pws, None) == S.SPENSE_ERR_ARG  # ldw
     assert p(1 << 20, 64, 8, 64, 1 << 22, 64, None, 32, 1 << 24, 64, 1 << 12, pws - 4, None) == S.SPENSE_ERR_WS
+
+
+def test_large_m_xcd_order_is_a_permutation_of_the_grid():
+    """The large-M kernel's XCD-aware workgroup order (the same formula as the kernel and
+    the planner's precondition) visits every (row block, token block) pair exactly once."""
+    for T in range(1, 33):
+        GT = 4 if T % 4 == 0 else (2 if T % 2 == 0 else 1)
+        TGc = T // GT
+        for rbtot in (1, 2, 8, 40, 64, 150, 200, 216):
+            if 8 % TGc or rbtot % (8 // TGc):
+                continue  # the planner keeps the plain order
+            RC, G = 8 // TGc, rbtot * T
+            seen = set()
+            for g in range(G):
+                x, l = g & 7, g >> 3
+                seen.add(((l // GT) * RC + x // TGc) * T + (x % TGc) * GT + l % GT)
+            assert seen == set(range(G)), (T, rbtot)
