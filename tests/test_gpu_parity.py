@@ -377,7 +377,10 @@ def test_tiled_exact_integers(S):
 # ------------------------------------------------------------------ large-M kernel
 BIG_CASES = [  # axis, M, N, K, dense_begin: ragged tokens, rows and columns around its 256 x 128 x 128 tiles
     (0, 1, 200, 1056, 72), (0, 300, 272, 1024, 208), (1, 257, 200, 1056, 800), (1, 513, 136, 640, 128),
-    (0, 600, 136, 384, 0), (0, 300, 136, 384, 136), (1, 300, 64, 512, 0), (1, 300, 64, 512, 512)]
+    (0, 600, 136, 384, 0), (0, 300, 136, 384, 136), (1, 300, 64, 512, 0), (1, 300, 64, 512, 512),
+    # XCD-aware order: T = 2, 4, 8 token blocks with row blocks in 8, 8, 4 classes (two regions
+    # for output-split; ragged tokens)
+    (0, 512, 1024, 128, 512), (0, 1024, 1024, 256, 256), (1, 2048, 512, 384, 128), (1, 1900, 512, 256, 256)]
 
 
 @pytest.mark.parametrize("waves", [4, 8])
