@@ -123,7 +123,7 @@ def test_factor_of_a_diagonal_hessian(S):
     assert (np.abs(np.diag(U) - np.diag(ref)) / np.diag(ref) <= tol).all()
 
 
-@pytest.mark.parametrize("K", [64, 100, 320, 700])
+@pytest.mark.parametrize("K", [64, 98, 100, 320, 700])
 def test_factor_matches_oracle(S, K):
     say(f"[obs factor] K={K}")
     H, _ = hessian(K, K, dead=(3,) if K == 100 else ())
@@ -147,7 +147,7 @@ def run_prune(S, W, H, dense_begin, U=None, dead=None):
 
 
 @pytest.mark.parametrize("N,K,dense_begin", [(300, 256, 192), (77, 200, 100), (64, 128, 128), (33, 96, 0),
-                                             (260, 384, 260)])
+                                             (260, 384, 260), (50, 98, 64), (40, 130, 128), (70, 600, 516)])
 def test_prune_matches_oracle_on_clear_choices(S, N, K, dense_begin):
     say(f"[obs prune] N={N} K={K} dense_begin={dense_begin}")
     H, _ = hessian(N + K, K, dead=(5,) if K == 200 else ())
