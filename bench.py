@@ -261,6 +261,39 @@ def measure_extras(args, torch, gen, S, ws, pws, copies, swd, mx, dws, dense_cop
     return ex
 
 
+def profile_layer(torch, gen, S, steps):
+    """Eager launches for a kernel trace: per iteration the seven GEMMs of the Qwen3-like
+    layer at M = 64 (q, k, v, o, gate, up, down), then the GLU MLP block (gate, up,
+    GLU + quantisation, down).  Returns the launch order of one iteration."""
+    Ml = 64
+    ws = S.Workspace("cuda")
+    io, pk = [], []
+    for i, (name, n_, k_, ax) in enumerate(gen.QWEN3_32B_LAYER):
+        m = gen.make_matrix(4, i, name, n_, k_, ax, DENSE_FRAC, gen.FP8)
+        Wt = torch.from_numpy(m.W).cuda()
+        pk.append(S.tile(S.compress(Wt, torch.from_numpy(m.mask).cuda(), 0 if ax == gen.OUTPUT else 1, m.dense_begin)))
+        del Wt
+        Xl, sxl = gen.make_x(4, i, Ml, k_, gen.FP8, "normal")
+        io.append((torch.from_numpy(Xl).cuda(), torch.from_numpy(sxl).cuda(), torch.from_numpy(m.sw).cuda(),
+                   torch.empty((Ml, n_), dtype=torch.bfloat16, device="cuda")))
+    names = [n for (n, _, _, _) in gen.QWEN3_32B_LAYER]
+    gi, ui, di = names.index("gate"), names.index("up"), names.index("down")
+    Gb = torch.empty((Ml, pk[gi].N), dtype=torch.float32, device="cuda")
+    Ub = torch.empty_like(Gb)
+    Hq = torch.empty((Ml, pk[gi].N), dtype=torch.uint8, device="cuda")
+    sh = torch.empty(Ml, dtype=torch.float32, device="cuda")
+    Yb = torch.empty((Ml, pk[di].N), dtype=torch.bfloat16, device="cuda")
+    for _ in range(steps):
+        for (Xd_, sx_, sw_, Y_), p_ in zip(io, pk):
+            S.gemm(Xd_, p_, sw_, sx_, out=Y_, workspace=ws)
+        S.gemm(io[gi][0], pk[gi], io[gi][2], io[gi][1], out=Gb, out_f32=True, workspace=ws)
+        S.gemm(io[gi][0], pk[ui], io[ui][2], io[gi][1], out=Ub, out_f32=True, workspace=ws)
+        S.glu_quantize_fp8(Gb, Ub, q=Hq, scales=sh)
+        S.gemm(Hq, pk[di], io[di][2], sh, out=Yb, workspace=ws)
+    torch.cuda.synchronize()
+    return {"profile_layer": steps, "order": names + ["mlp.gate", "mlp.up", "mlp.glu_quantize", "mlp.down"]}
+
+
 def synthetic_hessian(torch, K, seed, M=4096.0, rank=64):
     """A calibration-like Hessian on the device: M (C^T C + diag(d)) + F F^T with
     C = I + 0.3 (shift) and F a K x rank Gaussian block of variance M / (2K)."""
@@ -356,6 +389,8 @@ def main():
                     help="omit the layer-set, M=2048 and copy-bandwidth measurements")
     ap.add_argument("--profile-offline", action="store_true",
                     help="time only the offline steps (index selection, SparseGPT factor and sweep)")
+    ap.add_argument("--profile-layer", action="store_true",
+                    help="launch the M=64 decoder-layer set and the GLU MLP block eagerly (for kernel traces)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -380,6 +415,9 @@ def main():
     import gen
     import paper_2606_10445_amd as S
 
+    if args.profile_layer:
+        print(json.dumps(profile_layer(torch, gen, S, args.steps)))
+        return
     if args.profile_offline:
         print(json.dumps({"qwen3_index_selection": measure_index_selection(torch, S),
                           "sparsegpt_obs": measure_obs(torch, S)}))
