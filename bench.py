@@ -226,8 +226,31 @@ def measure_extras(args, torch, gen, S, ws, pws, copies, swd, mx, dws, dense_cop
 
     lms = time_launches(run_layer(sets), 100, 10, torch)
     dlms = time_launches(run_layer(dsets), 100, 10, torch)
+    # the same set in four launches: q, k, v grouped (one X) and gate, up grouped
+    names_ = [n for (n, _, _, _) in layer]
+    qkv = [names_.index(n) for n in ("q", "k", "v")]
+    gu = [names_.index(n) for n in ("gate", "up")]
+    rest = [names_.index(n) for n in ("o", "down")]
+
+    def run_layer_grouped(ws_sets):
+        def f(i):
+            for grp in (qkv, gu):
+                Xg_, sxg_ = io[grp[0]][0], io[grp[0]][1]
+                S.gemm_grouped(Xg_, [ws_sets[j][i % 2] for j in grp], [io[j][2] for j in grp], sxg_,
+                               outs=[io[j][3] for j in grp])
+            for j in rest:
+                Xd_, sx_, sw_, Y_ = io[j]
+                S.gemm(Xd_, ws_sets[j][i % 2], sw_, sx_, out=Y_, workspace=ws)
+        return f
+
+    glms = time_launches(run_layer_grouped(sets), 100, 10, torch)
+    gdlms = time_launches(run_layer_grouped(dsets), 100, 10, torch)
     ex["qwen3_layer_m64"] = {"us_per_layer": round(lms * 1e3, 1), "ms_per_64_layers": round(lms * 64, 3),
-                             "dense_us_per_layer": round(dlms * 1e3, 1), "speedup_vs_dense": round(dlms / lms, 3)}
+                             "dense_us_per_layer": round(dlms * 1e3, 1), "speedup_vs_dense": round(dlms / lms, 3),
+                             "grouped_us_per_layer": round(glms * 1e3, 1),
+                             "grouped_ms_per_64_layers": round(glms * 64, 3),
+                             "grouped_dense_us_per_layer": round(gdlms * 1e3, 1),
+                             "grouped_speedup_vs_dense": round(gdlms / glms, 3)}
     # the GLU MLP block of the same layer (Eq. (4)): gate, up (output-split) -> GLU + per-token
     # fp8 quantisation -> down (input-split), four launches; and the GLU step alone
     names = [n for (n, _, _, _) in layer]

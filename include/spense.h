@@ -37,7 +37,7 @@
 extern "C" {
 #endif
 
-#define SPENSE_ABI_VERSION 5
+#define SPENSE_ABI_VERSION 6
 
 typedef enum spense_status {
   SPENSE_OK = 0,
@@ -223,6 +223,23 @@ size_t spense_gemm_workspace_size(int64_t M, const spense_packed_t* packed);
 int spense_gemm(const void* X, int64_t M, int64_t ldx, const spense_packed_t* packed, const float* w_scale,
                 const float* x_scale, void* Y, int64_t ldy, uint32_t out_flags, void* ws, size_t ws_bytes,
                 hipStream_t stream);
+
+/*
+ * Several Spense weights that share the activations X and K, in one launch: Y[i] =
+ * X W_i^T for i < count (sec. 3.2, output-split, as spense_gemm for each weight; e.g.
+ * the q, k and v projections of a layer, or gate and up).  Each weight keeps its own
+ * 2:4 and dense regions and its own output; together they fill the GPU where one small
+ * weight alone would need K slices and a second pass.  Weights: fp8 e4m3fn, output-split,
+ * tiled layout (spense_tile), equal K; count in [1, 4].  w_scales (array of count
+ * pointers, or NULL for none) and x_scale as in spense_gemm; Y[i] (bf16 or fp32 per
+ * out_flags) with leading dimension ldy[i] >= N_i.  Results equal spense_gemm's up to the
+ * order of the fp32 sum (no K slices here).  Allocates nothing; asynchronous.
+ * SPENSE_ERR_ARG for NULL arrays or pointers, count outside [1, 4], mixed K, dtype,
+ * split or layout; SPENSE_ERR_ALIGN as spense_gemm.
+ */
+int spense_gemm_grouped(const void* X, int64_t M, int64_t ldx, int32_t count, const spense_packed_t* const* packed,
+                        const float* const* w_scales, const float* x_scale, void* const* Y, const int64_t* ldy,
+                        uint32_t out_flags, hipStream_t stream);
 
 /* Device workspace (bytes) that spense_dense_gemm needs; same rules as above. */
 size_t spense_dense_gemm_workspace_size(int64_t M, int64_t N, int64_t K, int32_t dtype);

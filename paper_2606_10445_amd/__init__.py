@@ -43,7 +43,7 @@ EXPORTS = ["spense_abi_version", "spense_last_error", "spense_layout", "spense_t
            "spense_gemm_workspace_size", "spense_gemm", "spense_dense_gemm_workspace_size", "spense_dense_gemm",
            "spense_quantize_fp8", "spense_glu_quantize_fp8", "spense_index_scores", "spense_dense_permutation",
            "spense_gather_rows", "spense_gather_cols", "spense_obs_factor_workspace_size", "spense_obs_factor",
-           "spense_obs_prune_workspace_size", "spense_obs_prune_24"]
+           "spense_obs_prune_workspace_size", "spense_obs_prune_24", "spense_gemm_grouped"]
 
 
 class SpenseError(RuntimeError):
@@ -101,6 +101,7 @@ def _load():
         "spense_obs_factor": (ctypes.c_int, [p, i64, i64, ctypes.c_float, p, i64, p, p, sz, p]),
         "spense_obs_prune_workspace_size": (sz, [i64]),
         "spense_obs_prune_24": (ctypes.c_int, [p, i64, i64, i64, p, i64, p, i64, p, i64, p, sz, p]),
+        "spense_gemm_grouped": (ctypes.c_int, [p, i64, i64, i32, p, p, p, p, p, u32, p]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -201,6 +202,12 @@ def spense_gather_rows(src, ld_src_b, dst, ld_dst_b, rows, row_bytes, perm, stre
 
 def spense_gather_cols(src, ld_src, dst, ld_dst, rows, cols, elem_bytes, perm, stream) -> int:
     return _lib.spense_gather_cols(src, ld_src, dst, ld_dst, rows, cols, elem_bytes, perm, stream)
+
+
+def spense_gemm_grouped(X, M, ldx, count, packed_array, w_scales_array, x_scale, Y_array, ldy_array, out_flags,
+                        stream) -> int:
+    return _lib.spense_gemm_grouped(X, M, ldx, count, packed_array, w_scales_array, x_scale, Y_array, ldy_array,
+                                    out_flags, stream)
 
 
 def spense_obs_factor_workspace_size(K: int) -> int:
@@ -369,6 +376,33 @@ def gemm(X: torch.Tensor, pw: PackedWeight, w_scale=None, x_scale=None, out=None
     _check(spense_gemm(_ptr(X), M, X.stride(0), pw.desc, _ptr(w_scale), _ptr(x_scale), _ptr(out), out.stride(0),
                        SPENSE_OUT_F32 if out_f32 else SPENSE_OUT_BF16, wp, wn, _stream(X.device)))
     return out
+
+
+def gemm_grouped(X: torch.Tensor, pws, w_scales=None, x_scale=None, outs=None, out_f32=False):
+    """One launch for several Spense weights sharing X (spense_gemm_grouped): returns
+    [X W_i^T].  pws: tiled fp8 output-split PackedWeights with equal K (up to 4)."""
+    _row_major(X, "X")
+    M = X.shape[0]
+    n = len(pws)
+    if w_scales is not None and len(w_scales) != n:
+        raise ValueError("one w_scale per weight")
+    if outs is None:
+        outs = [torch.empty((M, p.N), dtype=torch.float32 if out_f32 else torch.bfloat16, device=X.device) for p in pws]
+    if any(p.K != X.shape[1] for p in pws):
+        raise ValueError("X.shape[1] must equal every weight's K")
+    descs = [p.desc for p in pws]
+    for i, p in enumerate(pws):
+        _check_scale(w_scales[i] if w_scales is not None else None, p.N, X.device, "w_scale")
+    _check_scale(x_scale, M, X.device, "x_scale")
+    PP = ctypes.POINTER(spense_packed_t)
+    parr = (PP * n)(*[ctypes.pointer(d) for d in descs])
+    sarr = (ctypes.c_void_p * n)(*[_ptr(w_scales[i]) if w_scales is not None else None for i in range(n)])
+    yarr = (ctypes.c_void_p * n)(*[_ptr(o) for o in outs])
+    larr = (ctypes.c_int64 * n)(*[o.stride(0) for o in outs])
+    _check(spense_gemm_grouped(_ptr(X), M, X.stride(0), n, parr, sarr if w_scales is not None else None,
+                               _ptr(x_scale), yarr, larr, SPENSE_OUT_F32 if out_f32 else SPENSE_OUT_BF16,
+                               _stream(X.device)))
+    return outs
 
 
 def dense_gemm(X: torch.Tensor, W: torch.Tensor, w_scale=None, x_scale=None, out=None, out_f32=False,

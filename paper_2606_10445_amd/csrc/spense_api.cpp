@@ -481,6 +481,10 @@ int gemm_common(const void* X, int64_t M, int64_t ldx, int32_t dtype, int32_t sp
   a.v_bytes = (uint32_t)vb;
   a.m_bytes = (uint32_t)mb;
   a.d_bytes = (uint32_t)db;
+  // the row-split kernel reads the weight through its descriptor
+  a.nmat = 1;
+  a.mat[0] = spense::MatDesc{a.values, a.meta, a.dense, a.v_bytes, a.m_bytes, a.d_bytes, a.Y, a.ldy, a.sw,
+                             a.vec_store};
   if (a.groups == 0) return ok();
   a.part = static_cast<float*>(ws);
   hipError_t e = spense::launch_gemm(dtype, pl.ls, a, stream);
@@ -769,6 +773,144 @@ int spense_gemm(const void* X, int64_t M, int64_t ldx, const spense_packed_t* pa
   return gemm_common(X, M, ldx, packed->dtype, packed->split, packed->N, packed->K, packed->dense_begin,
                      packed->layout, packed->values, packed->values_ld, packed->meta, packed->meta_ld, packed->dense,
                      packed->dense_ld, w_scale, x_scale, Y, ldy, out_flags, ws, ws_bytes, stream);
+}
+
+int spense_gemm_grouped(const void* X, int64_t M, int64_t ldx, int32_t count, const spense_packed_t* const* packed,
+                        const float* const* w_scales, const float* x_scale, void* const* Y, const int64_t* ldy,
+                        uint32_t out_flags, hipStream_t stream) {
+  using spense::Region;
+  if (count < 1 || count > spense::kMaxMats) return fail(SPENSE_ERR_ARG, "count=%d outside [1, %d]", count, spense::kMaxMats);
+  if (!packed || !Y || !ldy) return fail(SPENSE_ERR_ARG, "NULL array");
+  if (M < 0 || M > INT32_MAX) return fail(SPENSE_ERR_ARG, "bad M");
+  if (out_flags & ~1u) return fail(SPENSE_ERR_ARG, "unknown out_flags 0x%x", out_flags);
+  const int out_es = (out_flags & SPENSE_OUT_F32) ? 4 : 2;
+  int64_t K = -1;
+  for (int i = 0; i < count; ++i) {
+    spense_layout_t L;
+    if (!packed[i]) return fail(SPENSE_ERR_ARG, "packed[%d] is NULL", i);
+    int rc = check_packed(packed[i], &L);
+    if (rc) return rc;
+    const spense_packed_t& P = *packed[i];
+    if (P.dtype != SPENSE_FP8_E4M3FN || P.layout != SPENSE_LAYOUT_TILED || P.split != SPENSE_SPLIT_OUTPUT)
+      return fail(SPENSE_ERR_ARG, "grouped weights must be fp8, output-split, in the tiled layout");
+    if (K >= 0 && P.K != K) return fail(SPENSE_ERR_ARG, "grouped weights must share K");
+    K = P.K;
+    if (!Y[i]) return fail(SPENSE_ERR_ARG, "Y[%d] is NULL", i);
+    if (ldy[i] < P.N) return fail(SPENSE_ERR_ARG, "ldy[%d] < N", i);
+    if (reinterpret_cast<uintptr_t>(Y[i]) % out_es) return fail(SPENSE_ERR_ALIGN, "Y[%d] misaligned", i);
+    if ((int64_t)M * ldy[i] > (int64_t)1 << 40) return fail(SPENSE_ERR_ARG, "Y[%d] too large", i);
+  }
+  if (M == 0 || K == 0) return ok();
+  if (!X) return fail(SPENSE_ERR_ARG, "X is NULL");
+  if (ldx < K) return fail(SPENSE_ERR_ARG, "ldx=%lld < K=%lld", (long long)ldx, (long long)K);
+  if (!aligned16(X) || ldx % 16) return fail(SPENSE_ERR_ALIGN, "X must be 16-byte aligned with a 16-byte multiple row pitch");
+  const int64_t xb = (M - 1) * ldx + K;
+  if (xb >= ((int64_t)1 << 31)) return fail(SPENSE_ERR_ARG, "X spans 2 GiB or more");
+
+  // Plan: the row-split kernel as for one weight of this M (activation tiles, 8 waves), no
+  // K slices; the dense rows of every weight first (their workgroups carry more bytes),
+  // then the 2:4 rows; rows per workgroup chosen per kind as for one weight.
+  spense::LaunchShape ls;
+  memset(&ls, 0, sizeof ls);
+  ls.ct = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
+  ls.mblocks = (int)ceil_div(M, 16 * ls.ct);
+  ls.rt = 1;
+  ls.waves = 8;
+  ls.rows = 1;
+  spense::GemmArgs a;
+  memset(&a, 0, sizeof a);
+  const double sparse_cost = 0.625;  // fp8 bytes per logical 2:4 entry
+  const int64_t kc = 512;
+  Region regs[spense::kMaxRegions];
+  int nreg = 0;
+  for (int pass = 0; pass < 2; ++pass)
+    for (int i = 0; i < count; ++i) {
+      const spense_packed_t& P = *packed[i];
+      const int64_t r0 = pass == 0 ? P.dense_begin : 0, rows = pass == 0 ? P.N - P.dense_begin : P.dense_begin;
+      if (rows <= 0) continue;
+      Region r;
+      memset(&r, 0, sizeof r);
+      r.row0 = (int32_t)r0;
+      r.rows = (int32_t)rows;
+      r.kbound = pass == 0 ? 0 : (int32_t)K;
+      r.kend = (int32_t)K;
+      r.dense_row_off = (int32_t)P.dense_begin;
+      r.mat = i;
+      slice_cuts(r, 1, kc, 1, sparse_cost);
+      regs[nreg++] = r;
+    }
+  // rows per workgroup: w0 waves for dense regions, w1 for 2:4 regions (cost model of
+  // choose_rows_per_group)
+  const double tile_d = 16.0 * K, tile_s = 16.0 * sparse_cost * K, x_cost = 0.25 * 16.0 * ls.ct * K;
+  double best = 0;
+  int64_t best_wg = 0;
+  int bw0 = 8, bw1 = 8;
+  for (int w0 = 1; w0 <= 8; ++w0)
+    for (int w1 = 1; w1 <= 8; ++w1) {
+      int64_t wg = 0;
+      double big = 0;
+      for (int i = 0; i < nreg; ++i) {
+        const int w = regs[i].kbound == 0 ? w0 : w1;
+        wg += ceil_div(regs[i].rows, 16 * w) * ls.mblocks;
+        big = std::max(big, w * (regs[i].kbound == 0 ? tile_d : tile_s));
+      }
+      const double t = (double)ceil_div(wg, kCUs) * (big + x_cost);
+      if (best_wg == 0 || t < best * (1 - 1e-9) || (t <= best * (1 + 1e-9) && wg < best_wg)) {
+        best = t;
+        best_wg = wg;
+        bw0 = w0;
+        bw1 = w1;
+      }
+    }
+  int32_t groups = 0;
+  for (int i = 0; i < nreg; ++i) {
+    regs[i].wused = regs[i].kbound == 0 ? bw0 : bw1;
+    regs[i].nrb = (int32_t)ceil_div(regs[i].rows, 16 * regs[i].wused);
+    regs[i].wg0 = groups;
+    groups += regs[i].nrb;
+    a.reg[i] = regs[i];
+  }
+  a.nreg = nreg;
+  a.groups = groups;
+  a.tiled = 1;
+  a.X = static_cast<const uint8_t*>(X);
+  a.ldx_b = ldx;
+  a.x_bytes = (uint32_t)xb;
+  a.sx = x_scale;
+  a.M = (int32_t)M;
+  a.out_f32 = (out_flags & SPENSE_OUT_F32) ? 1 : 0;
+  a.nmat = count;
+  for (int i = 0; i < count; ++i) {
+    const spense_packed_t& P = *packed[i];
+    spense_tiled_layout_t T;
+    tiled_impl(P.N, P.K, P.dtype, P.split, P.dense_begin, &T);
+    if ((int64_t)T.values_bytes >= ((int64_t)1 << 31) || (int64_t)T.meta_bytes >= ((int64_t)1 << 31) ||
+        (int64_t)T.dense_bytes >= ((int64_t)1 << 31))
+      return fail(SPENSE_ERR_ARG, "weight %d spans 2 GiB or more", i);
+    const bool vec = ldy[i] % 4 == 0 && reinterpret_cast<uintptr_t>(Y[i]) % (4 * out_es) == 0 && P.dense_begin % 4 == 0;
+    a.mat[i] = spense::MatDesc{static_cast<const uint8_t*>(P.values), P.meta, static_cast<const uint8_t*>(P.dense),
+                               (uint32_t)T.values_bytes, (uint32_t)T.meta_bytes, (uint32_t)T.dense_bytes, Y[i], ldy[i],
+                               w_scales ? w_scales[i] : nullptr, vec ? 1 : 0};
+  }
+  // one weight: the plain instance, which reads its buffers from a
+  const spense::MatDesc& m0 = a.mat[0];
+  a.values = m0.values;
+  a.meta = m0.meta;
+  a.dense = m0.dense;
+  a.v_bytes = m0.v_bytes;
+  a.m_bytes = m0.m_bytes;
+  a.d_bytes = m0.d_bytes;
+  a.Y = m0.Y;
+  a.ldy = m0.ldy;
+  a.sw = m0.sw;
+  a.vec_store = m0.vec_store;
+  a.N = (int32_t)packed[0]->N;
+  if (groups == 0) return ok();
+  int rc = check_device();
+  if (rc) return rc;
+  hipError_t e = spense::launch_gemm(SPENSE_FP8_E4M3FN, ls, a, stream);
+  if (e != hipSuccess) return fail(SPENSE_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return ok();
 }
 
 size_t spense_dense_gemm_workspace_size(int64_t M, int64_t N, int64_t K, int32_t dtype) {

@@ -297,20 +297,22 @@ __device__ __forceinline__ uint32_t bf16_bits(float v) {
   return (uint32_t)__builtin_bit_cast(uint16_t, h);
 }
 
-// Four consecutive outputs n0..n0+3 of activation row m.
-__device__ __forceinline__ void store4(const GemmArgs& a, v4f acc, int m, int n0, int rowend) {
+// Epilogue of 4 consecutive output rows n0.. of token m: (acc * w_scale[n]) * x_scale[m],
+// bf16 (round to nearest even) or fp32, one vector store where allowed.
+__device__ __forceinline__ void store4(void* Y, int64_t ldy, const float* sw, int vec_store, const GemmArgs& a,
+                                       v4f acc, int m, int n0, int rowend) {
   const float xs = a.sx ? a.sx[m] : 1.0f;
   float v[4];
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int n = n0 + r < rowend ? n0 + r : rowend - 1;
     float y = acc[r];
-    if (a.sw) y = y * a.sw[n];
+    if (sw) y = y * sw[n];
     v[r] = y * xs;
   }
   if (a.out_f32) {
-    float* yp = reinterpret_cast<float*>(a.Y) + (int64_t)m * a.ldy + n0;
-    if (a.vec_store && n0 + 3 < rowend) {
+    float* yp = reinterpret_cast<float*>(Y) + (int64_t)m * ldy + n0;
+    if (vec_store && n0 + 3 < rowend) {
       *reinterpret_cast<v4f*>(yp) = (v4f){v[0], v[1], v[2], v[3]};
     } else {
 #pragma unroll
@@ -318,9 +320,9 @@ __device__ __forceinline__ void store4(const GemmArgs& a, v4f acc, int m, int n0
         if (n0 + r < rowend) yp[r] = v[r];
     }
   } else {
-    uint16_t* yp = reinterpret_cast<uint16_t*>(a.Y) + (int64_t)m * a.ldy + n0;
+    uint16_t* yp = reinterpret_cast<uint16_t*>(Y) + (int64_t)m * ldy + n0;
     const uint32_t b0 = bf16_bits(v[0]), b1 = bf16_bits(v[1]), b2 = bf16_bits(v[2]), b3 = bf16_bits(v[3]);
-    if (a.vec_store && n0 + 3 < rowend) {
+    if (vec_store && n0 + 3 < rowend) {
       typedef uint32_t u2 __attribute__((ext_vector_type(2)));
       *reinterpret_cast<u2*>(yp) = (u2){b0 | (b1 << 16), b2 | (b3 << 16)};
     } else {
@@ -330,6 +332,10 @@ __device__ __forceinline__ void store4(const GemmArgs& a, v4f acc, int m, int n0
         if (n0 + r < rowend) yp[r] = (uint16_t)bb[r];
     }
   }
+}
+
+__device__ __forceinline__ void store4(const GemmArgs& a, v4f acc, int m, int n0, int rowend) {
+  store4(a.Y, a.ldy, a.sw, a.vec_store, a, acc, m, n0, rowend);
 }
 
 // ---------------------------------------------------------------- kernel
@@ -687,7 +693,7 @@ __device__ __forceinline__ void barrier_vm_lgkm0() {
 // and slot c % NS), then a barrier that waits for the activations of chunk c+1 (issued
 // in step c+1-D, before that step's weights), so D chunks of weights stay in flight
 // across it.  The buffer being filled held chunk c-1, which every wave has finished.
-template <int DT, int CT, int RT, int WR, bool WM, int NS, int P, bool TL>
+template <int DT, int CT, int RT, int WR, bool WM, int NS, int P, bool TL, bool GR>
 __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
   static_assert(NS == 3 || NS == 4, "three or four pipeline slots");
   static_assert(!TL || (DT == kFP8 && WM), "the tiled layout is fp8 with whole-chunk metadata loads");
@@ -700,8 +706,18 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int li = lane & 15, lq = lane >> 4;
   const int g = blockIdx.x, mb = blockIdx.y;
-  const int ri = (a.nreg > 1 && g >= a.reg[1].wg0) ? 1 : 0;
+  // GR (grouped launch): up to kMaxRegions regions in workgroup order, each of one weight
+  // (its buffers, output and scales in a.mat); otherwise one weight, up to two regions,
+  // its buffers in a (a shorter prologue).
+  int ri = 0;
+  if constexpr (GR) {
+    for (int i = 1; i < a.nreg; ++i)
+      if (g >= a.reg[i].wg0) ri = i;
+  } else {
+    ri = (a.nreg > 1 && g >= a.reg[1].wg0) ? 1 : 0;
+  }
   const Region& R = a.reg[ri];
+  const MatDesc& MD = a.mat[GR ? R.mat : 0];
   const int rowend = R.row0 + R.rows;
   // workgroups of a region: (row group, K slice), slices of one row group adjacent
   const int slice = (g - R.wg0) % R.ksplit, rgroup = (g - R.wg0) / R.ksplit;
@@ -712,8 +728,9 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
   const bool active = wave < R.wused && nbase < rowend;
 
   __shared__ __attribute__((aligned(1024))) uint8_t xbuf[NS][XT::BYTES];
-  const __amdgpu_buffer_rsrc_t rx = rsrc(a.X, a.x_bytes), rv = rsrc(a.values, a.v_bytes),
-                               rm = rsrc(a.meta, a.m_bytes), rd = rsrc(a.dense, a.d_bytes);
+  const __amdgpu_buffer_rsrc_t rx = rsrc(a.X, a.x_bytes), rv = GR ? rsrc(MD.values, MD.v_bytes) : rsrc(a.values, a.v_bytes),
+                               rm = GR ? rsrc(MD.meta, MD.m_bytes) : rsrc(a.meta, a.m_bytes),
+                               rd = GR ? rsrc(MD.dense, MD.d_bytes) : rsrc(a.dense, a.d_bytes);
 
   v4f acc[RT][CT];
 #pragma unroll
@@ -820,7 +837,10 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
       const int n0 = nbase + 16 * t + 4 * lq;
       if (m >= a.M || n0 >= rowend) continue;
       if (R.ksplit == 1) {
-        store4(a, acc[t][cc], m, n0, rowend);
+        if constexpr (GR)
+          store4(MD.Y, MD.ldy, MD.sw, MD.vec_store, a, acc[t][cc], m, n0, rowend);
+        else
+          store4(a, acc[t][cc], m, n0, rowend);
       } else {  // unscaled fp32 partial of this K slice
         float* pp = a.part + ((int64_t)slice * a.M + m) * a.N + n0;
 #pragma unroll
@@ -856,12 +876,12 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a) {
 // slots and two-step groups for four; fp8 without wide metadata loads (metadata rows not
 // 16-byte aligned, four separately masked loads per chunk) one step lighter, and even so
 // its four-tile, eight-wave instance spills a few registers.
-template <int DT, int CT, int RT, int WR, bool WM, bool TL>
+template <int DT, int CT, int RT, int WR, bool WM, bool TL, bool GR = false>
 hipError_t launch_rows_wm(const dim3& grid, const dim3& block, const GemmArgs& a, hipStream_t s) {
   constexpr bool light = DT == kFP8 && !WM;
   constexpr int NS = CT <= 2 && RT == 1 && !light ? 4 : 3;
   constexpr int P = CT == 1 && RT == 1 ? 4 : 1;
-  hipLaunchKernelGGL((spense_gemm_rows_kernel<DT, CT, RT, WR, WM, NS, P, TL>), grid, block, 0, s, a);
+  hipLaunchKernelGGL((spense_gemm_rows_kernel<DT, CT, RT, WR, WM, NS, P, TL, GR>), grid, block, 0, s, a);
   return hipGetLastError();
 }
 
@@ -869,6 +889,10 @@ template <int DT, int CT, int RT, int WR>
 hipError_t launch_rows(const LaunchShape& ls, const GemmArgs& a, hipStream_t s) {
   dim3 grid(a.groups, ls.mblocks), block(64 * WR);
   if constexpr (DT == kFP8) {
+    if (a.tiled && a.nmat > 1) {  // grouped launch: the tiled fp8 instances with 8 waves
+      if constexpr (RT == 1 && WR == 8) return launch_rows_wm<DT, CT, RT, WR, true, true, true>(grid, block, a, s);
+      return hipErrorInvalidValue;
+    }
     if (a.tiled) return launch_rows_wm<DT, CT, RT, WR, true, true>(grid, block, a, s);
     if (a.m_ld_b % 16 == 0) return launch_rows_wm<DT, CT, RT, WR, true, false>(grid, block, a, s);
   }

@@ -9,6 +9,8 @@ enum : int32_t { kFP8 = 1, kBF16 = 2 };
 enum : int32_t { kSplitOutput = 0, kSplitInput = 1 };
 
 constexpr int kMaxWaves = 16;
+constexpr int kMaxMats = 4;                  // weights of one grouped launch
+constexpr int kMaxRegions = 2 * kMaxMats;    // 2:4 rows and dense rows of each
 
 // One contiguous part of the weight: a range of output rows and the logical K range
 // [0, K) whose columns below kbound are stored 2:4 and the rest dense.  Output-split has
@@ -31,8 +33,23 @@ struct Region {
   int32_t wg0;                 // first workgroup of this region
   int32_t wused;               // row-split kernel: waves of a workgroup that own rows here
   int32_t ksplit;              // row-split kernel: K slices (1 = none); >1 writes fp32 partials
+  int32_t mat;                 // row-split kernel: the weight (GemmArgs::mat) these rows belong to
   int32_t cut[kMaxWaves + 1];  // K-split kernel: K boundaries of the waves' parts;
                                // row-split kernel: chunk boundaries of the K slices
+};
+
+// One weight of a launch as the row-split kernel reads it: its buffers, output and
+// per-row scales.  A plain launch has one (the same buffers as GemmArgs); a grouped launch
+// (several weights sharing X and K) has up to kMaxMats.
+struct MatDesc {
+  const uint8_t* values;
+  const uint32_t* meta;
+  const uint8_t* dense;
+  uint32_t v_bytes, m_bytes, d_bytes;
+  void* Y;
+  int64_t ldy;  // elements
+  const float* sw;
+  int32_t vec_store;
 };
 
 struct GemmArgs {
@@ -58,7 +75,9 @@ struct GemmArgs {
   float* part;    // fp32 partial sums of K-sliced regions: part[(slice * M + m) * N + n]
   int32_t tblocks;  // large-M kernel: 256-token blocks (workgroups of a row block are adjacent)
   int32_t xgt, xrc;  // large-M kernel, XCD-aware order (0 = off): token blocks per XCD, row classes
-  Region reg[2];
+  int32_t nmat;
+  MatDesc mat[kMaxMats];
+  Region reg[kMaxRegions];
 };
 
 struct LaunchShape {

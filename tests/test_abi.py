@@ -41,7 +41,7 @@ def test_library_exports_every_declared_symbol(S):
     for n in _declared():
         assert hasattr(lib, n), f"{n} declared in include/ but not exported"
     assert set(_declared()) == set(S.EXPORTS)
-    assert S.spense_abi_version() == 5
+    assert S.spense_abi_version() == 6
 
 
 @pytest.mark.parametrize("N,K,split,db", [(256, 512, 0, 192), (256, 512, 1, 384), (25600, 5120, 0, 19200),
@@ -272,3 +272,32 @@ def test_large_m_xcd_order_is_a_permutation_of_the_grid():
                 x, l = g & 7, g >> 3
                 seen.add(((l // GT) * RC + x // TGc) * T + (x % TGc) * GT + l % GT)
             assert seen == set(range(G)), (T, rbtot)
+
+
+def test_grouped_gemm_validates_arguments_on_the_host(S):
+    """Error paths of spense_gemm_grouped return before touching the device."""
+    import ctypes
+    g = S.spense_gemm_grouped
+    L = S.spense_layout(64, 256, S.SPENSE_FP8_E4M3FN, S.SPENSE_SPLIT_OUTPUT, 48)
+    T = S.spense_tiled_layout(64, 256, S.SPENSE_FP8_E4M3FN, S.SPENSE_SPLIT_OUTPUT, 48)
+    d = S.spense_packed_t(1, 0, 64, 256, 48, 1 << 20, L.values_ld, 2 << 20, L.meta_ld, 3 << 20, L.dense_ld,
+                          S.SPENSE_LAYOUT_TILED)
+    d2 = S.spense_packed_t(1, 0, 64, 512, 48, 1 << 20, L.values_ld, 2 << 20, L.meta_ld, 3 << 20, L.dense_ld,
+                           S.SPENSE_LAYOUT_TILED)  # another K
+    rm = S.spense_packed_t(1, 0, 64, 256, 48, 1 << 20, L.values_ld, 2 << 20, L.meta_ld, 3 << 20, L.dense_ld,
+                           S.SPENSE_LAYOUT_ROWMAJOR)
+    PP = ctypes.POINTER(S.spense_packed_t)
+    arr = lambda *ds: (PP * len(ds))(*[ctypes.pointer(x) for x in ds])
+    ys = (ctypes.c_void_p * 4)(1 << 24, 1 << 25, 1 << 26, 1 << 27)
+    lds = (ctypes.c_int64 * 4)(64, 64, 64, 64)
+    assert T.sparse_tiles == 3
+    assert g(1 << 28, 8, 256, 0, arr(d), None, None, ys, lds, 0, None) == S.SPENSE_ERR_ARG  # count 0
+    assert g(1 << 28, 8, 256, 5, arr(d, d, d, d, d), None, None, ys, lds, 0, None) == S.SPENSE_ERR_ARG  # > 4
+    assert g(1 << 28, 8, 256, 2, arr(d, d2), None, None, ys, lds, 0, None) == S.SPENSE_ERR_ARG  # mixed K
+    assert g(1 << 28, 8, 256, 2, arr(d, rm), None, None, ys, lds, 0, None) == S.SPENSE_ERR_ARG  # row-major
+    assert g(1 << 28, 8, 256, 1, arr(d), None, None, None, lds, 0, None) == S.SPENSE_ERR_ARG  # NULL Y array
+    short = (ctypes.c_int64 * 1)(32)
+    assert g(1 << 28, 8, 256, 1, arr(d), None, None, ys, short, 0, None) == S.SPENSE_ERR_ARG  # ldy < N
+    assert g(None, 8, 256, 1, arr(d), None, None, ys, lds, 0, None) == S.SPENSE_ERR_ARG  # NULL X
+    assert g((1 << 28) + 8, 8, 256, 1, arr(d), None, None, ys, lds, 0, None) == S.SPENSE_ERR_ALIGN  # unaligned X
+    assert g(1 << 28, 0, 256, 1, arr(d), None, None, ys, lds, 0, None) == S.SPENSE_OK  # M = 0

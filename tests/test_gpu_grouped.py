@@ -1,0 +1,130 @@
+"""GPU parity of the grouped launch (spense_gemm_grouped: several Spense weights that
+share X and K in one launch, e.g. q / k / v or gate / up), through the C ABI.
+
+- exact-integer data (values in [-3, 3], power-of-two scales: every partial sum is an
+  exact integer, so any summation order gives the same fp32 value): every output bit
+  for bit against the oracle, bf16 and fp32, at ragged M and weight sizes that are not
+  multiples of the workgroup's rows;
+- random data: each output within the fp32 error bound of the fp64 oracle;
+- the Qwen3-like q, k, v at M = 64 (full size, exact-integer data) bit for bit.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import gen
+import oracle
+
+pytestmark = pytest.mark.gpu
+
+FP8 = 1
+U32 = 2.0 ** -24
+
+
+@pytest.fixture(scope="module")
+def S():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2606_10445_amd as S
+    return S
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def tdev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def weights(cfg, shapes, M, K, exact=True):
+    """Per weight: (codes, mask, sw, dense_begin); one X and sx for all (the first draw's)."""
+    out, X, sx = [], None, None
+    for i, (N, frac) in enumerate(shapes):
+        db = gen.split_point(N, K, gen.OUTPUT, frac)
+        if exact:
+            W, mask, Xi, sw, sxi = gen.make_exact_int(cfg, i, M, N, K, gen.OUTPUT, db, gen.FP8)
+        else:
+            r = np.random.default_rng(cfg * 10 + i)
+            W, sw = gen.quantize_rows_fp8(gen.draw_weight(r, N, K))
+            Xi, sxi = gen.quantize_rows_fp8(gen.draw_x(r, M, K, "normal"))
+            mask = gen.random_mask_24(r, N, K, gen.OUTPUT, db, True)
+        if X is None:
+            X, sx = Xi, sxi
+        out.append((W, mask, sw, db))
+    return out, X, sx
+
+
+def packed(S, W, mask, db):
+    return S.tile(S.compress(tdev(W), tdev(mask), 0, db))
+
+
+GROUP_CASES = [  # M, K, [(N, dense fraction)]
+    (1, 1024, [(320, 0.25), (64, 0.25), (64, 0.25)]),
+    (17, 512, [(200, 0.25), (48, 0.5)]),
+    (64, 1024, [(320, 0.25), (64, 0.25), (64, 0.25)]),
+    (100, 640, [(256, 0.0), (96, 1.0), (144, 0.25), (16, 0.25)]),
+    (33, 384, [(512, 0.25)]),
+]
+
+
+@pytest.mark.parametrize("M,K,shapes", GROUP_CASES)
+def test_grouped_exact(S, M, K, shapes):
+    say(f"[grouped exact] M={M} K={K} {shapes}")
+    ws, X, sx = weights(5 + M, shapes, M, K)
+    pws = [packed(S, W, mask, db) for (W, mask, sw, db) in ws]
+    sws = [tdev(sw) for (_, _, sw, _) in ws]
+    for out_f32 in (True, False):
+        ys = S.gemm_grouped(tdev(X), pws, sws, tdev(sx), out_f32=out_f32)
+        torch.cuda.synchronize()
+        for (W, mask, sw, db), y in zip(ws, ys):
+            v, m, d, bad = oracle.compress(W, mask, FP8, 0, db)
+            ref = oracle.spense_gemm(X, v, m, d, W.shape[0], K, FP8, 0, db, sw, sx)
+            got = y.cpu().numpy() if out_f32 else y.view(torch.int16).cpu().numpy().view(np.uint16)
+            assert np.array_equal(got, ref["y_f32" if out_f32 else "y_bf16"])
+
+
+def test_grouped_random_within_bound(S):
+    M, K = 48, 1536
+    shapes = [(640, 0.25), (128, 0.25), (128, 0.25)]
+    ws, X, sx = weights(9, shapes, M, K, exact=False)
+    pws = [packed(S, W, mask, db) for (W, mask, sw, db) in ws]
+    ys = S.gemm_grouped(tdev(X), pws, [tdev(sw) for (_, _, sw, _) in ws], tdev(sx), out_f32=True)
+    torch.cuda.synchronize()
+    for (W, mask, sw, db), y in zip(ws, ys):
+        v, m, d, _ = oracle.compress(W, mask, FP8, 0, db)
+        Wd = oracle.decompress(v, m, d, W.shape[0], K, FP8, 0, db)
+        o = oracle.gemm_f64(X, Wd, FP8, sw, sx)
+        gamma = K * U32 / (1 - K * U32)
+        scale = np.abs(sw.astype(np.float64))[None, :] * np.abs(sx.astype(np.float64))[:, None]
+        bound = (2.0 ** -12 + 2 * gamma) * o["abs_dot"] * scale + 4 * U32 * np.abs(o["y"]) + 1e-38
+        assert np.all(np.abs(y.cpu().numpy().astype(np.float64) - o["y"]) <= bound)
+
+
+def test_grouped_qkv_full_size(S):
+    """The q (8192 x 5120), k and v (1024 x 5120) projections of the Qwen3-like layer at
+    M = 64, 25% dense rows each, in one launch: every bf16 output bit for bit."""
+    M, K = 64, 5120
+    ws, X, sx = weights(31, [(8192, 0.25), (1024, 0.25), (1024, 0.25)], M, K)
+    pws = [packed(S, W, mask, db) for (W, mask, sw, db) in ws]
+    ys = S.gemm_grouped(tdev(X), pws, [tdev(sw) for (_, _, sw, _) in ws], tdev(sx))
+    torch.cuda.synchronize()
+    for (W, mask, sw, db), y in zip(ws, ys):
+        v, m, d, _ = oracle.compress(W, mask, FP8, 0, db)
+        ref = oracle.spense_gemm(X, v, m, d, W.shape[0], K, FP8, 0, db, sw, sx)
+        assert np.array_equal(y.view(torch.int16).cpu().numpy().view(np.uint16), ref["y_bf16"])
+
+
+def test_grouped_validates_arguments(S):
+    M, K = 8, 256
+    ws, X, sx = weights(3, [(64, 0.25), (32, 0.25)], M, K)
+    pws = [packed(S, W, mask, db) for (W, mask, sw, db) in ws]
+    other = S.tile(S.compress(tdev(ws[0][0][:, :128]), tdev(ws[0][1][:, :128]), 0, ws[0][3]))
+    with pytest.raises(ValueError):
+        S.gemm_grouped(tdev(X), [pws[0], other])  # K differs
+    rowmajor = S.compress(tdev(ws[0][0]), tdev(ws[0][1]), 0, ws[0][3])
+    with pytest.raises(S.SpenseError):
+        S.gemm_grouped(tdev(X), [pws[0], rowmajor])  # not the tiled layout
+    with pytest.raises(S.SpenseError):
+        S.gemm_grouped(tdev(X), pws * 3)  # more than four weights
