@@ -251,8 +251,9 @@ def measure_extras(args, torch, gen, S, ws, pws, copies, swd, mx, dws, dense_cop
                              "grouped_ms_per_64_layers": round(glms * 64, 3),
                              "grouped_dense_us_per_layer": round(gdlms * 1e3, 1),
                              "grouped_speedup_vs_dense": round(gdlms / glms, 3)}
-    # the GLU MLP block of the same layer (Eq. (4)): gate, up (output-split) -> GLU + per-token
-    # fp8 quantisation -> down (input-split), four launches; and the GLU step alone
+    # the GLU MLP block of the same layer (Eq. (4)): gate and up (output-split, one grouped
+    # launch) -> GLU + per-token fp8 quantisation -> down (input-split), three launches; and
+    # the GLU step alone
     names = [n for (n, _, _, _) in layer]
     gi, ui, di = names.index("gate"), names.index("up"), names.index("down")
     Xg, sxg, swg, _ = io[gi]
@@ -265,8 +266,7 @@ def measure_extras(args, torch, gen, S, ws, pws, copies, swd, mx, dws, dense_cop
 
     def run_mlp(ws_sets):
         def f(i):
-            S.gemm(Xg, ws_sets[gi][i % 2], swg, sxg, out=Gb, out_f32=True, workspace=ws)
-            S.gemm(Xg, ws_sets[ui][i % 2], swu, sxg, out=Ub, out_f32=True, workspace=ws)
+            S.gemm_grouped(Xg, [ws_sets[gi][i % 2], ws_sets[ui][i % 2]], [swg, swu], sxg, outs=[Gb, Ub], out_f32=True)
             S.glu_quantize_fp8(Gb, Ub, q=Hq, scales=sh)
             S.gemm(Hq, ws_sets[di][i % 2], swd_, sh, out=Yb, workspace=ws)
         return f
@@ -286,7 +286,8 @@ def measure_extras(args, torch, gen, S, ws, pws, copies, swd, mx, dws, dense_cop
 
 def profile_layer(torch, gen, S, steps):
     """Eager launches for a kernel trace: per iteration the seven GEMMs of the Qwen3-like
-    layer at M = 64 (q, k, v, o, gate, up, down), then the GLU MLP block (gate, up,
+    layer at M = 64 (q, k, v, o, gate, up, down), the same set in four launches (q, k, v
+    grouped; o; gate, up grouped; down), then the GLU MLP block (gate and up grouped,
     GLU + quantisation, down).  Returns the launch order of one iteration."""
     Ml = 64
     ws = S.Workspace("cuda")
@@ -306,15 +307,22 @@ def profile_layer(torch, gen, S, steps):
     Hq = torch.empty((Ml, pk[gi].N), dtype=torch.uint8, device="cuda")
     sh = torch.empty(Ml, dtype=torch.float32, device="cuda")
     Yb = torch.empty((Ml, pk[di].N), dtype=torch.bfloat16, device="cuda")
+    qkv = [names.index(n) for n in ("q", "k", "v")]
+    oi = names.index("o")
     for _ in range(steps):
         for (Xd_, sx_, sw_, Y_), p_ in zip(io, pk):
             S.gemm(Xd_, p_, sw_, sx_, out=Y_, workspace=ws)
-        S.gemm(io[gi][0], pk[gi], io[gi][2], io[gi][1], out=Gb, out_f32=True, workspace=ws)
-        S.gemm(io[gi][0], pk[ui], io[ui][2], io[gi][1], out=Ub, out_f32=True, workspace=ws)
+        for grp, single in ((qkv, oi), ([gi, ui], di)):
+            S.gemm_grouped(io[grp[0]][0], [pk[j] for j in grp], [io[j][2] for j in grp], io[grp[0]][1],
+                           outs=[io[j][3] for j in grp])
+            Xd_, sx_, sw_, Y_ = io[single]
+            S.gemm(Xd_, pk[single], sw_, sx_, out=Y_, workspace=ws)
+        S.gemm_grouped(io[gi][0], [pk[gi], pk[ui]], [io[gi][2], io[ui][2]], io[gi][1], outs=[Gb, Ub], out_f32=True)
         S.glu_quantize_fp8(Gb, Ub, q=Hq, scales=sh)
         S.gemm(Hq, pk[di], io[di][2], sh, out=Yb, workspace=ws)
     torch.cuda.synchronize()
-    return {"profile_layer": steps, "order": names + ["mlp.gate", "mlp.up", "mlp.glu_quantize", "mlp.down"]}
+    return {"profile_layer": steps, "order": names + ["grouped q,k,v", "grouped o", "grouped gate,up", "grouped down",
+                                                      "mlp.gate,up", "mlp.glu_quantize", "mlp.down"]}
 
 
 def synthetic_hessian(torch, K, seed, M=4096.0, rank=64):

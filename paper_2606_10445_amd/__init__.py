@@ -462,11 +462,17 @@ def glu_quantize_fp8(G: torch.Tensor, U: torch.Tensor, q=None, scales=None):
 
 def mlp(X: torch.Tensor, x_scale: torch.Tensor, gate: PackedWeight, up: PackedWeight, down: PackedWeight,
         gate_scale=None, up_scale=None, down_scale=None, out=None, workspace: Workspace | None = None):
-    """The GLU MLP of the paper's sec. 3.3.1 Eq. (4) on Spense weights, as five library
-    calls: G = gate(X), U = up(X) (output-split, fp32 out), (Hq, sh) = GLU + per-token
-    fp8 quantisation, Y = down(Hq) (input-split, bf16 out).  X: fp8 codes with x_scale."""
-    G = gemm(X, gate, gate_scale, x_scale, out_f32=True, workspace=workspace)
-    U = gemm(X, up, up_scale, x_scale, out_f32=True, workspace=workspace)
+    """The GLU MLP of the paper's sec. 3.3.1 Eq. (4) on Spense weights: G = gate(X), U =
+    up(X) (output-split, fp32 out; one grouped launch for tiled fp8 weights), (Hq, sh) =
+    GLU + per-token fp8 quantisation, Y = down(Hq) (input-split, bf16 out).  X: fp8 codes
+    with x_scale."""
+    if (gate.kind == up.kind == SPENSE_LAYOUT_TILED and gate.K == up.K and gate.dtype == up.dtype == SPENSE_FP8_E4M3FN
+            and gate.split == up.split == SPENSE_SPLIT_OUTPUT):
+        G, U = gemm_grouped(X, [gate, up], None if gate_scale is None else [gate_scale, up_scale], x_scale,
+                            out_f32=True)
+    else:
+        G = gemm(X, gate, gate_scale, x_scale, out_f32=True, workspace=workspace)
+        U = gemm(X, up, up_scale, x_scale, out_f32=True, workspace=workspace)
     Hq, sh = glu_quantize_fp8(G, U)
     return gemm(Hq, down, down_scale, sh, out=out, workspace=workspace)
 
