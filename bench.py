@@ -279,6 +279,8 @@ def measure_extras(args, torch, gen, S, ws, pws, copies, swd, mx, dws, dense_cop
                            "speedup_vs_dense": round(dmms / mms, 3), "glu_quantize_us": round(gms * 1e3, 2),
                            "glu_quantize_gbs": round(glu_bytes / (gms * 1e-3) / 1e9, 1)}
     del sets, dsets, io, Gb, Ub, Hq
+    ex["qwen3_down_dense_sweep"] = measure_down_sweep(torch, gen, S)
+    ex["seed_oss_layer"] = measure_seed_layer(torch, gen, S)
     ex["qwen3_index_selection"] = measure_index_selection(torch, S)
     ex["sparsegpt_obs"] = measure_obs(torch, S)
     return ex
@@ -323,6 +325,100 @@ def profile_layer(torch, gen, S, steps):
     torch.cuda.synchronize()
     return {"profile_layer": steps, "order": names + ["grouped q,k,v", "grouped o", "grouped gate,up", "grouped down",
                                                       "mlp.gate,up", "mlp.glu_quantize", "mlp.down"]}
+
+
+def device_matrix(torch, S, N, K, split, frac, seed, gen):
+    """A synthetic Spense weight drawn on the device (for timing only): W ~ N(0, 0.02),
+    per-row absmax fp8 scales, e4m3fn codes, the 2:4 magnitude mask (the two largest
+    |w| of each group of four) on the 2:4 region, `frac` of the split axis dense; tiled."""
+    g = torch.Generator(device="cuda").manual_seed(seed)
+    W = torch.randn((N, K), generator=g, device="cuda") * 0.02
+    sw = W.abs().amax(dim=1).clamp_min(1e-30) / 448.0
+    codes = (W / sw[:, None]).to(torch.float8_e4m3fn).view(torch.uint8)
+    idx = W.abs().view(N, K // 4, 4).topk(2, dim=2).indices
+    mask = torch.zeros((N, K // 4, 4), dtype=torch.uint8, device="cuda").scatter_(2, idx, 1).view(N, K)
+    axis = gen.OUTPUT if split == 0 else gen.INPUT
+    db = gen.split_point(N, K, axis, frac)
+    pw = S.tile(S.compress(codes, mask, split, db))
+    del W, codes, mask, idx
+    return pw, sw.contiguous(), db
+
+
+def device_x(torch, M, K, seed):
+    g = torch.Generator(device="cuda").manual_seed(seed)
+    X = torch.randn((M, K), generator=g, device="cuda")
+    sx = X.abs().amax(dim=1).clamp_min(1e-30) / 448.0
+    return (X / sx[:, None]).to(torch.float8_e4m3fn).view(torch.uint8).contiguous(), sx.contiguous()
+
+
+def measure_down_sweep(torch, gen, S):
+    """The down projection (5120 x 25600, input-split) at M = 1 / 16 / 64 with the dense
+    fraction swept over 0 / 12.5 / 25 / 50 / 100% (100% = every column dense, the dense
+    baseline); four weight copies rotated past the MALL."""
+    N, K = 5120, 25600
+    out = {}
+    base = {}
+    for frac in (1.0, 0.5, 0.25, 0.125, 0.0):
+        pw, sw, db = device_matrix(torch, S, N, K, 1, frac, 21, gen)
+        pws = [pw] + [pw.clone() for _ in range(3)]
+        row = {}
+        for M in (1, 16, 64):
+            X, sx = device_x(torch, M, K, 22 + M)
+            Y = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+            ms = time_launches(lambda i: S.gemm(X, pws[i % 4], sw, sx, out=Y), 100, 10, torch)
+            byt = alg_bytes_spense(M, N, K, 0, 0) + N * (K - db) + 0.625 * N * db
+            rec = {"us": round(ms * 1e3, 2), "gbs": round(byt / (ms * 1e-3) / 1e9, 1),
+                   "pct_hbm_peak": round(100 * byt / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 1)}
+            if frac == 1.0:
+                base[M] = ms
+            else:
+                rec["speedup_vs_dense"] = round(base[M] / ms, 3)
+            row[f"m{M}"] = rec
+        out[f"dense_{int(frac * 1000) / 10:g}pct"] = row
+        del pws, pw
+    return out
+
+
+def measure_seed_layer(torch, gen, S):
+    """The Seed-OSS-36B-like layer linears (q 10240 x 5120, k / v 1024 x 5120, o 5120 x
+    10240 input-split, gate / up 27648 x 5120, down 5120 x 27648 input-split; 25% dense)
+    per layer at M = 1 / 4 / 16 / 64 / 256 / 2048: seven launches, and at M <= 64 also
+    four (q, k, v and gate, up grouped); two copies of the set rotated."""
+    shapes = gen.SEED_OSS_36B_LAYER
+    mats = []
+    for i, (name, n_, k_, ax) in enumerate(shapes):
+        pw, sw, _ = device_matrix(torch, S, n_, k_, 0 if ax == gen.OUTPUT else 1, DENSE_FRAC, 40 + i, gen)
+        mats.append(([pw, pw.clone()], sw))
+    names = [n for (n, _, _, _) in shapes]
+    qkv = [names.index(n) for n in ("q", "k", "v")]
+    gu = [names.index(n) for n in ("gate", "up")]
+    rest = [names.index(n) for n in ("o", "down")]
+    ws = S.Workspace("cuda")
+    out = {}
+    for M in (1, 4, 16, 64, 256, 2048):
+        io = []
+        for i, (name, n_, k_, ax) in enumerate(shapes):
+            X, sx = device_x(torch, M, k_, 60 + i)
+            io.append((X, sx, torch.empty((M, n_), dtype=torch.bfloat16, device="cuda")))
+
+        def layer(i):
+            for (X_, sx_, Y_), (ps, sw_) in zip(io, mats):
+                S.gemm(X_, ps[i % 2], sw_, sx_, out=Y_, workspace=ws)
+
+        def layer_grouped(i):
+            for grp in (qkv, gu):
+                S.gemm_grouped(io[grp[0]][0], [mats[j][0][i % 2] for j in grp], [mats[j][1] for j in grp],
+                               io[grp[0]][1], outs=[io[j][2] for j in grp])
+            for j in rest:
+                S.gemm(io[j][0], mats[j][0][i % 2], mats[j][1], io[j][1], out=io[j][2], workspace=ws)
+
+        steps = 20 if M >= 256 else 100
+        rec = {"us_per_layer": round(time_launches(layer, steps, 3, torch) * 1e3, 1)}
+        if M <= 64:
+            rec["grouped_us_per_layer"] = round(time_launches(layer_grouped, steps, 3, torch) * 1e3, 1)
+        out[f"m{M}"] = rec
+        del io
+    return out
 
 
 def synthetic_hessian(torch, K, seed, M=4096.0, rank=64):

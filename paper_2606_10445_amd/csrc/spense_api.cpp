@@ -223,18 +223,29 @@ void choose_rows_per_group(spense::Region* regs, int nreg, int rt, int waves, in
 
 // Row-split kernel: number of K slices.  Slicing K multiplies the waves of a weight with
 // few 16-row tiles, at the price of an fp32 partial-sum pass.  Measured on the q / k / o /
-// down shapes (tiled fp8): it pays only for one block of 17-64 tokens (one activation
-// tile streams fast enough without it; several blocks already multiply the workgroups),
-// on weights with fewer than 1024 tiles, and when each slice keeps enough chunks: down
-// (320 tiles, 50 chunks) gains up to 1.5x with 4 slices, k/v (64 tiles, 10 chunks) ~1.2x
-// with 3, q and o (10 and 16 chunks) lose.
-int choose_ksplit(const spense::Region* regs, int nreg, int ct, int mblocks, int64_t chunks) {
+// down shapes (tiled fp8): it pays for one block of tokens (several blocks already
+// multiply the workgroups), on weights with fewer than 1024 tiles, and when each slice
+// keeps enough chunks: down (320 tiles, 50 chunks) gains up to 1.5x with 4 slices at
+// 17-64 tokens and 4-12% at 1-16, k/v (64 tiles, 10 chunks) ~1.2x with 3 at 17-64 tokens
+// and nothing at 1-16, q and o (10 and 16 chunks) lose.
+int choose_ksplit(const spense::Region* regs, int nreg, int ct, int mblocks, int64_t chunks, int64_t M) {
   int64_t tiles = 0;
-  for (int i = 0; i < nreg; ++i) tiles += ceil_div(regs[i].rows, 16);
+  bool has_24 = false;
+  for (int i = 0; i < nreg; ++i) {
+    tiles += ceil_div(regs[i].rows, 16);
+    has_24 = has_24 || (regs[i].kbound > 0 && regs[i].rows > 0);
+  }
   int S = 1;
-  if (ct > 1 && mblocks == 1 && tiles < 1024) {
-    const int64_t min_chunks = tiles >= 256 ? 12 : 3;
+  // One activation tile (M <= 16): only if every slice keeps at least 12 chunks; a weight
+  // with a 2:4 part takes up to 4 slices (its chunks carry fewer bytes, so the waves of
+  // one tile keep too few in flight), an all-dense one 2 and only above 8 tokens.
+  // Measured on down (5120 x 25600, us, slices 1 / 2 / 4): 25% dense M = 1: 23.6 / 21.4 /
+  // 21.0, M = 16: 23.3 / 21.7 / 21.6; all dense M = 1: 25.1 / 25.5 / 26.3, M = 4: 23.9 /
+  // 24.6 / 26.3, M = 16: 27.7 / 25.6 / 27.3; k and q (10 chunks) lose.
+  if (mblocks == 1 && tiles < 1024) {
+    const int64_t min_chunks = ct == 1 || tiles >= 256 ? 12 : 3;
     S = (int)std::max<int64_t>(1, std::min<int64_t>({4, ceil_div(1024, std::max<int64_t>(tiles, 1)), chunks / min_chunks}));
+    if (ct == 1 && !has_24) S = M > 8 ? std::min(S, 2) : 1;
   }
   const int e = env_int("SPENSE_KSPLIT", 0);
   if (e >= 1 && e <= 8) S = (int)std::max<int64_t>(1, std::min<int64_t>(e, chunks));
@@ -372,7 +383,7 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
     const int64_t kc = dtype == SPENSE_FP8_E4M3FN ? 512 : 256;
     int64_t chunks = 0;
     for (int i = 0; i < nreg; ++i) chunks = std::max(chunks, ceil_div(regs[i].kbound, kc) + ceil_div(K - regs[i].kbound, kc));
-    ksplit = chunks > 0 ? choose_ksplit(regs, nreg, pl->ls.ct, pl->ls.mblocks, chunks) : 1;
+    ksplit = chunks > 0 ? choose_ksplit(regs, nreg, pl->ls.ct, pl->ls.mblocks, chunks, M) : 1;
     for (int i = 0; i < nreg; ++i) slice_cuts(regs[i], ksplit, kc, es, sparse_cost);
     choose_rows_per_group(regs, nreg, rt, waves, pl->ls.ct, pl->ls.mblocks, K, es, sparse_cost, ksplit);
   }
