@@ -197,9 +197,10 @@ int spense_tile(const spense_packed_t* src, const spense_packed_t* dst, hipStrea
 /*
  * Device workspace (bytes) that spense_gemm needs for this M and weight; 0 means none.
  * It is non-zero when the plan cuts K into slices run by separate workgroups (weights
- * with few 16-row tiles at 17-64 tokens): S x M x N fp32 partial sums, added in slice
- * order by a second kernel of the same call.  The workspace is only scratch between the
- * two kernels of one call; calls that overlap on one workspace race.
+ * with fewer than 1024 16-row tiles at up to 64 tokens, when every slice keeps enough of
+ * K: e.g. k / v at 17-64 tokens, down from one token on): S x M x N fp32 partial sums,
+ * added in slice order by a second kernel of the same call.  The workspace is only
+ * scratch between the two kernels of one call; calls that overlap on one workspace race.
  */
 size_t spense_gemm_workspace_size(int64_t M, const spense_packed_t* packed);
 
