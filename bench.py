@@ -251,20 +251,29 @@ def measure_extras(args, torch, gen, S, ws, pws, copies, swd, mx, dws, dense_cop
                              "grouped_ms_per_64_layers": round(glms * 64, 3),
                              "grouped_dense_us_per_layer": round(gdlms * 1e3, 1),
                              "grouped_speedup_vs_dense": round(gdlms / glms, 3)}
-    # the GLU MLP block of the same layer (Eq. (4)): gate and up (output-split, one grouped
-    # launch) -> GLU + per-token fp8 quantisation -> down (input-split), three launches; and
-    # the GLU step alone
+    # the GLU MLP block of the same layer (Eq. (4)), three launches: gate and up
+    # (output-split) with the GLU in their epilogue -> per-token fp8 quantisation of H ->
+    # down (input-split); the unfused block (gate and up grouped, G and U in fp32 -> GLU +
+    # quantisation -> down) beside it, and the steps alone
     names = [n for (n, _, _, _) in layer]
     gi, ui, di = names.index("gate"), names.index("up"), names.index("down")
     Xg, sxg, swg, _ = io[gi]
     swu, swd_ = io[ui][2], io[di][2]
     Gb = torch.empty((Ml, layer[gi][1]), dtype=torch.float32, device="cuda")
     Ub = torch.empty_like(Gb)
+    Hf = torch.empty_like(Gb)
     Hq = torch.empty((Ml, layer[gi][1]), dtype=torch.uint8, device="cuda")
     sh = torch.empty(Ml, dtype=torch.float32, device="cuda")
     Yb = torch.empty((Ml, layer[di][1]), dtype=torch.bfloat16, device="cuda")
 
     def run_mlp(ws_sets):
+        def f(i):
+            S.gemm_glu(Xg, ws_sets[gi][i % 2], ws_sets[ui][i % 2], swg, swu, sxg, out=Hf)
+            S.quantize_fp8(Hf, q=Hq, scales=sh)
+            S.gemm(Hq, ws_sets[di][i % 2], swd_, sh, out=Yb, workspace=ws)
+        return f
+
+    def run_mlp_unfused(ws_sets):
         def f(i):
             S.gemm_grouped(Xg, [ws_sets[gi][i % 2], ws_sets[ui][i % 2]], [swg, swu], sxg, outs=[Gb, Ub], out_f32=True)
             S.glu_quantize_fp8(Gb, Ub, q=Hq, scales=sh)
@@ -273,12 +282,22 @@ def measure_extras(args, torch, gen, S, ws, pws, copies, swd, mx, dws, dense_cop
 
     mms = time_launches(run_mlp(sets), 100, 10, torch)
     dmms = time_launches(run_mlp(dsets), 100, 10, torch)
+    umms = time_launches(run_mlp_unfused(sets), 100, 10, torch)
+    fgms = time_launches(lambda i: S.gemm_glu(Xg, sets[gi][i % 2], sets[ui][i % 2], swg, swu, sxg, out=Hf), 100, 10,
+                         torch)
+    ggms = time_launches(lambda i: S.gemm_grouped(Xg, [sets[gi][i % 2], sets[ui][i % 2]], [swg, swu], sxg,
+                                                  outs=[Gb, Ub], out_f32=True), 100, 10, torch)
+    qms = time_launches(lambda i: S.quantize_fp8(Hf, q=Hq, scales=sh), 200, 10, torch)
     gms = time_launches(lambda i: S.glu_quantize_fp8(Gb, Ub, q=Hq, scales=sh), 200, 10, torch)
     glu_bytes = 2 * Gb.numel() * 4 + Hq.numel() + 4 * Ml  # g, u read once, codes and scales written
+    q_bytes = Hf.numel() * 4 + Hq.numel() + 4 * Ml  # h read once, codes and scales written
     ex["qwen3_mlp_m64"] = {"us_per_block": round(mms * 1e3, 1), "dense_us_per_block": round(dmms * 1e3, 1),
-                           "speedup_vs_dense": round(dmms / mms, 3), "glu_quantize_us": round(gms * 1e3, 2),
+                           "speedup_vs_dense": round(dmms / mms, 3), "unfused_us_per_block": round(umms * 1e3, 1),
+                           "gate_up_glu_us": round(fgms * 1e3, 2), "gate_up_grouped_fp32_us": round(ggms * 1e3, 2),
+                           "quantize_us": round(qms * 1e3, 2), "quantize_gbs": round(q_bytes / (qms * 1e-3) / 1e9, 1),
+                           "glu_quantize_us": round(gms * 1e3, 2),
                            "glu_quantize_gbs": round(glu_bytes / (gms * 1e-3) / 1e9, 1)}
-    del sets, dsets, io, Gb, Ub, Hq
+    del sets, dsets, io, Gb, Ub, Hf, Hq
     ex["qwen3_down_dense_sweep"] = measure_down_sweep(torch, gen, S)
     ex["seed_oss_layer"] = measure_seed_layer(torch, gen, S)
     ex["qwen3_index_selection"] = measure_index_selection(torch, S)
@@ -289,8 +308,8 @@ def measure_extras(args, torch, gen, S, ws, pws, copies, swd, mx, dws, dense_cop
 def profile_layer(torch, gen, S, steps):
     """Eager launches for a kernel trace: per iteration the seven GEMMs of the Qwen3-like
     layer at M = 64 (q, k, v, o, gate, up, down), the same set in four launches (q, k, v
-    grouped; o; gate, up grouped; down), then the GLU MLP block (gate and up grouped,
-    GLU + quantisation, down).  Returns the launch order of one iteration."""
+    grouped; o; gate, up grouped; down), then the GLU MLP block (gate and up with the GLU
+    in their epilogue, quantisation, down).  Returns the launch order of one iteration."""
     Ml = 64
     ws = S.Workspace("cuda")
     io, pk = [], []
@@ -304,8 +323,7 @@ def profile_layer(torch, gen, S, steps):
                    torch.empty((Ml, n_), dtype=torch.bfloat16, device="cuda")))
     names = [n for (n, _, _, _) in gen.QWEN3_32B_LAYER]
     gi, ui, di = names.index("gate"), names.index("up"), names.index("down")
-    Gb = torch.empty((Ml, pk[gi].N), dtype=torch.float32, device="cuda")
-    Ub = torch.empty_like(Gb)
+    Hf = torch.empty((Ml, pk[gi].N), dtype=torch.float32, device="cuda")
     Hq = torch.empty((Ml, pk[gi].N), dtype=torch.uint8, device="cuda")
     sh = torch.empty(Ml, dtype=torch.float32, device="cuda")
     Yb = torch.empty((Ml, pk[di].N), dtype=torch.bfloat16, device="cuda")
@@ -319,12 +337,12 @@ def profile_layer(torch, gen, S, steps):
                            outs=[io[j][3] for j in grp])
             Xd_, sx_, sw_, Y_ = io[single]
             S.gemm(Xd_, pk[single], sw_, sx_, out=Y_, workspace=ws)
-        S.gemm_grouped(io[gi][0], [pk[gi], pk[ui]], [io[gi][2], io[ui][2]], io[gi][1], outs=[Gb, Ub], out_f32=True)
-        S.glu_quantize_fp8(Gb, Ub, q=Hq, scales=sh)
+        S.gemm_glu(io[gi][0], pk[gi], pk[ui], io[gi][2], io[ui][2], io[gi][1], out=Hf)
+        S.quantize_fp8(Hf, q=Hq, scales=sh)
         S.gemm(Hq, pk[di], io[di][2], sh, out=Yb, workspace=ws)
     torch.cuda.synchronize()
     return {"profile_layer": steps, "order": names + ["grouped q,k,v", "grouped o", "grouped gate,up", "grouped down",
-                                                      "mlp.gate,up", "mlp.glu_quantize", "mlp.down"]}
+                                                      "mlp.gate,up+glu", "mlp.quantize", "mlp.down"]}
 
 
 def device_matrix(torch, S, N, K, split, frac, seed, gen):

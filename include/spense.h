@@ -37,7 +37,7 @@
 extern "C" {
 #endif
 
-#define SPENSE_ABI_VERSION 6
+#define SPENSE_ABI_VERSION 7
 
 typedef enum spense_status {
   SPENSE_OK = 0,
@@ -241,6 +241,26 @@ int spense_gemm(const void* X, int64_t M, int64_t ldx, const spense_packed_t* pa
 int spense_gemm_grouped(const void* X, int64_t M, int64_t ldx, int32_t count, const spense_packed_t* const* packed,
                         const float* const* w_scales, const float* x_scale, void* const* Y, const int64_t* ldy,
                         uint32_t out_flags, hipStream_t stream);
+
+/*
+ * The gate and up projections of a GLU MLP and the GLU step between them, in one launch
+ * (sec. 3.2 output-split weights; sec. 3.3.1, Eq. (4), the activation read as SiLU):
+ *   g = X Wg^T, u = X Wu^T, each scaled as in spense_gemm ((acc * w_scale[n]) *
+ *   x_scale[m], fp32), then H[m, n] = u * g / (1 + exp(-g)) in fp32 with the same
+ *   arithmetic as spense_glu_quantize_fp8 (so quantising H with spense_quantize_fp8
+ *   gives the codes and scales that spense_glu_quantize_fp8 gives for the G and U of
+ *   spense_gemm_grouped, bit for bit).  A workgroup computes gate and up tiles of the
+ *   same rows and pairs them on chip, so G and U are never written.
+ * gate, up: fp8 e4m3fn, output-split, tiled layout, with equal N, K and dense_begin.
+ * X: M x K fp8 codes (ldx bytes, 16-byte aligned, ldx a multiple of 16).  w_scale_gate /
+ * w_scale_up: N fp32 each or NULL; x_scale: M fp32 or NULL.  H: M x N fp32, leading
+ * dimension ldh >= N (caller-owned).  Allocates nothing; asynchronous.
+ * SPENSE_ERR_ARG for NULL pointers, mismatched or unsupported weights, K = 0, ldh < N;
+ * SPENSE_ERR_ALIGN for a misaligned X or H.
+ */
+int spense_gemm_glu(const void* X, int64_t M, int64_t ldx, const spense_packed_t* gate, const spense_packed_t* up,
+                    const float* w_scale_gate, const float* w_scale_up, const float* x_scale, float* H, int64_t ldh,
+                    hipStream_t stream);
 
 /* Device workspace (bytes) that spense_dense_gemm needs; same rules as above. */
 size_t spense_dense_gemm_workspace_size(int64_t M, int64_t N, int64_t K, int32_t dtype);

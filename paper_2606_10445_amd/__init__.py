@@ -43,7 +43,7 @@ EXPORTS = ["spense_abi_version", "spense_last_error", "spense_layout", "spense_t
            "spense_gemm_workspace_size", "spense_gemm", "spense_dense_gemm_workspace_size", "spense_dense_gemm",
            "spense_quantize_fp8", "spense_glu_quantize_fp8", "spense_index_scores", "spense_dense_permutation",
            "spense_gather_rows", "spense_gather_cols", "spense_obs_factor_workspace_size", "spense_obs_factor",
-           "spense_obs_prune_workspace_size", "spense_obs_prune_24", "spense_gemm_grouped"]
+           "spense_obs_prune_workspace_size", "spense_obs_prune_24", "spense_gemm_grouped", "spense_gemm_glu"]
 
 
 class SpenseError(RuntimeError):
@@ -102,6 +102,7 @@ def _load():
         "spense_obs_prune_workspace_size": (sz, [i64]),
         "spense_obs_prune_24": (ctypes.c_int, [p, i64, i64, i64, p, i64, p, i64, p, i64, p, sz, p]),
         "spense_gemm_grouped": (ctypes.c_int, [p, i64, i64, i32, p, p, p, p, p, u32, p]),
+        "spense_gemm_glu": (ctypes.c_int, [p, i64, i64, p, p, p, p, p, p, i64, p]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -208,6 +209,10 @@ def spense_gemm_grouped(X, M, ldx, count, packed_array, w_scales_array, x_scale,
                         stream) -> int:
     return _lib.spense_gemm_grouped(X, M, ldx, count, packed_array, w_scales_array, x_scale, Y_array, ldy_array,
                                     out_flags, stream)
+
+
+def spense_gemm_glu(X, M, ldx, gate, up, w_scale_gate, w_scale_up, x_scale, H, ldh, stream) -> int:
+    return _lib.spense_gemm_glu(X, M, ldx, gate, up, w_scale_gate, w_scale_up, x_scale, H, ldh, stream)
 
 
 def spense_obs_factor_workspace_size(K: int) -> int:
@@ -405,6 +410,30 @@ def gemm_grouped(X: torch.Tensor, pws, w_scales=None, x_scale=None, outs=None, o
     return outs
 
 
+def gemm_glu(X: torch.Tensor, gate: PackedWeight, up: PackedWeight, gate_scale=None, up_scale=None, x_scale=None,
+             out=None) -> torch.Tensor:
+    """H = glu(X Wg^T, X Wu^T) in one launch (spense_gemm_glu), fp32 M x N: the gate and
+    up GEMMs with the GLU step in their epilogue.  gate, up: tiled fp8 output-split
+    PackedWeights with equal N, K and dense_begin."""
+    _row_major(X, "X")
+    M = X.shape[0]
+    if gate.K != X.shape[1] or up.K != X.shape[1]:
+        raise ValueError("X.shape[1] must equal K")
+    if gate.N != up.N:
+        raise ValueError("gate and up must have the same N")
+    if out is None:
+        out = torch.empty((M, gate.N), dtype=torch.float32, device=X.device)
+    _row_major(out, "out")
+    if out.dtype != torch.float32 or out.shape != (M, gate.N):
+        raise ValueError(f"out must be fp32 of shape {(M, gate.N)}")
+    _check_scale(gate_scale, gate.N, X.device, "gate_scale")
+    _check_scale(up_scale, up.N, X.device, "up_scale")
+    _check_scale(x_scale, M, X.device, "x_scale")
+    _check(spense_gemm_glu(_ptr(X), M, X.stride(0), ctypes.byref(gate.desc), ctypes.byref(up.desc), _ptr(gate_scale),
+                           _ptr(up_scale), _ptr(x_scale), _ptr(out), out.stride(0), _stream(X.device)))
+    return out
+
+
 def dense_gemm(X: torch.Tensor, W: torch.Tensor, w_scale=None, x_scale=None, out=None, out_f32=False,
                workspace: Workspace | None = None) -> torch.Tensor:
     """The dense baseline Y = X W^T (spense_dense_gemm)."""
@@ -462,18 +491,23 @@ def glu_quantize_fp8(G: torch.Tensor, U: torch.Tensor, q=None, scales=None):
 
 def mlp(X: torch.Tensor, x_scale: torch.Tensor, gate: PackedWeight, up: PackedWeight, down: PackedWeight,
         gate_scale=None, up_scale=None, down_scale=None, out=None, workspace: Workspace | None = None):
-    """The GLU MLP of the paper's sec. 3.3.1 Eq. (4) on Spense weights: G = gate(X), U =
-    up(X) (output-split, fp32 out; one grouped launch for tiled fp8 weights), (Hq, sh) =
-    GLU + per-token fp8 quantisation, Y = down(Hq) (input-split, bf16 out).  X: fp8 codes
-    with x_scale."""
-    if (gate.kind == up.kind == SPENSE_LAYOUT_TILED and gate.K == up.K and gate.dtype == up.dtype == SPENSE_FP8_E4M3FN
-            and gate.split == up.split == SPENSE_SPLIT_OUTPUT):
-        G, U = gemm_grouped(X, [gate, up], None if gate_scale is None else [gate_scale, up_scale], x_scale,
-                            out_f32=True)
+    """The GLU MLP of the paper's sec. 3.3.1 Eq. (4) on Spense weights: H = glu(gate(X),
+    up(X)) (output-split; for tiled fp8 weights of one geometry one launch with the GLU in
+    its epilogue, otherwise G and U in fp32 and the GLU fused with the quantisation),
+    (Hq, sh) = per-token fp8 quantisation, Y = down(Hq) (input-split, bf16 out).  X: fp8
+    codes with x_scale."""
+    paired = (gate.kind == up.kind == SPENSE_LAYOUT_TILED and gate.dtype == up.dtype == SPENSE_FP8_E4M3FN
+              and gate.split == up.split == SPENSE_SPLIT_OUTPUT)
+    if paired and gate.N == up.N and gate.K == up.K and gate.dense_begin == up.dense_begin:
+        Hq, sh = quantize_fp8(gemm_glu(X, gate, up, gate_scale, up_scale, x_scale))
     else:
-        G = gemm(X, gate, gate_scale, x_scale, out_f32=True, workspace=workspace)
-        U = gemm(X, up, up_scale, x_scale, out_f32=True, workspace=workspace)
-    Hq, sh = glu_quantize_fp8(G, U)
+        if paired and gate.K == up.K:
+            G, U = gemm_grouped(X, [gate, up], None if gate_scale is None else [gate_scale, up_scale], x_scale,
+                                out_f32=True)
+        else:
+            G = gemm(X, gate, gate_scale, x_scale, out_f32=True, workspace=workspace)
+            U = gemm(X, up, up_scale, x_scale, out_f32=True, workspace=workspace)
+        Hq, sh = glu_quantize_fp8(G, U)
     return gemm(Hq, down, down_scale, sh, out=out, workspace=workspace)
 
 

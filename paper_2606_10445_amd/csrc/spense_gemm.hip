@@ -693,8 +693,11 @@ __device__ __forceinline__ void barrier_vm_lgkm0() {
 // and slot c % NS), then a barrier that waits for the activations of chunk c+1 (issued
 // in step c+1-D, before that step's weights), so D chunks of weights stay in flight
 // across it.  The buffer being filled held chunk c-1, which every wave has finished.
-template <int DT, int CT, int RT, int WR, bool WM, int NS, int P, bool TL, bool GR>
+template <int DT, int CT, int RT, int WR, bool WM, int NS, int P, bool TL, int GM>
 __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
+  constexpr bool GR = GM == 1;   // grouped launch
+  constexpr bool GLU = GM == 2;  // gate and up paired, the GLU step in the epilogue
+  static_assert(!GLU || (RT == 1 && WR == 8), "paired gate / up: four waves per weight");
   static_assert(NS == 3 || NS == 4, "three or four pipeline slots");
   static_assert(!TL || (DT == kFP8 && WM), "the tiled layout is fp8 with whole-chunk metadata loads");
   constexpr int D = NS - 1;
@@ -707,8 +710,8 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
   const int li = lane & 15, lq = lane >> 4;
   const int g = blockIdx.x, mb = blockIdx.y;
   // GR (grouped launch): up to kMaxRegions regions in workgroup order, each of one weight
-  // (its buffers, output and scales in a.mat); otherwise one weight, up to two regions,
-  // its buffers in a (a shorter prologue).
+  // (its buffers, output and scales in a.mat); otherwise one weight (GLU: two weights,
+  // gate and up, of equal geometry), up to two regions, buffers in a or a.mat (GLU).
   int ri = 0;
   if constexpr (GR) {
     for (int i = 1; i < a.nreg; ++i)
@@ -717,20 +720,24 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
     ri = (a.nreg > 1 && g >= a.reg[1].wg0) ? 1 : 0;
   }
   const Region& R = a.reg[ri];
-  const MatDesc& MD = a.mat[GR ? R.mat : 0];
+  // GLU: waves 0-3 own gate tiles, waves 4-7 the up tiles of the same rows
+  const int wsel = GLU ? (wave & 3) : wave;
+  const MatDesc& MD = a.mat[GR ? R.mat : (GLU ? wave >> 2 : 0)];
   const int rowend = R.row0 + R.rows;
   // workgroups of a region: (row group, K slice), slices of one row group adjacent
   const int slice = (g - R.wg0) % R.ksplit, rgroup = (g - R.wg0) / R.ksplit;
-  const int nbase = R.row0 + (rgroup * R.wused + wave) * 16 * RT;  // first row of the wave's RT tiles
+  const int nbase = R.row0 + (rgroup * R.wused + wsel) * 16 * RT;  // first row of the wave's RT tiles
   const int m0 = mb * 16 * CT;
   const int K = R.kend;
   const int kbound = R.kbound;
-  const bool active = wave < R.wused && nbase < rowend;
+  const bool active = wsel < R.wused && nbase < rowend;
 
   __shared__ __attribute__((aligned(1024))) uint8_t xbuf[NS][XT::BYTES];
-  const __amdgpu_buffer_rsrc_t rx = rsrc(a.X, a.x_bytes), rv = GR ? rsrc(MD.values, MD.v_bytes) : rsrc(a.values, a.v_bytes),
-                               rm = GR ? rsrc(MD.meta, MD.m_bytes) : rsrc(a.meta, a.m_bytes),
-                               rd = GR ? rsrc(MD.dense, MD.d_bytes) : rsrc(a.dense, a.d_bytes);
+  constexpr bool FROM_MAT = GR || GLU;
+  const __amdgpu_buffer_rsrc_t rx = rsrc(a.X, a.x_bytes),
+                               rv = FROM_MAT ? rsrc(MD.values, MD.v_bytes) : rsrc(a.values, a.v_bytes),
+                               rm = FROM_MAT ? rsrc(MD.meta, MD.m_bytes) : rsrc(a.meta, a.m_bytes),
+                               rd = FROM_MAT ? rsrc(MD.dense, MD.d_bytes) : rsrc(a.dense, a.d_bytes);
 
   v4f acc[RT][CT];
 #pragma unroll
@@ -827,6 +834,50 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
   else
     run(std::false_type());
 
+  if constexpr (GLU) {
+    // h = glu(g, u) with g, u each scaled as the plain epilogue scales them: the gate waves
+    // pass their accumulators through the (now idle) staging buffers to the up waves of
+    // the same rows, which write H (fp32).  Every wave takes both barriers.
+    xdl_fence();
+    barrier_vm<0>();  // all staging loads of every wave have landed
+    static_assert(XT::BYTES >= 4 * CT * 64 * 16, "gate accumulators fit one staging buffer");
+    float* ex = reinterpret_cast<float*>(&xbuf[0][0]);
+    if (wave < 4 && active) {
+#pragma unroll
+      for (int cc = 0; cc < CT; ++cc) *reinterpret_cast<v4f*>(ex + ((wsel * CT + cc) * 64 + lane) * 4) = acc[0][cc];
+    }
+    barrier_vm_lgkm0<63>();
+    if (wave >= 4 && active) {
+      const MatDesc& G = a.mat[0];
+      const MatDesc& Up = a.mat[1];
+#pragma unroll
+      for (int cc = 0; cc < CT; ++cc) {
+        const int m = m0 + 16 * cc + li;
+        const int n0 = nbase + 4 * lq;
+        if (m >= a.M || n0 >= rowend) continue;
+        const v4f gv = *reinterpret_cast<const v4f*>(ex + ((wsel * CT + cc) * 64 + lane) * 4);
+        const float xs = a.sx ? a.sx[m] : 1.0f;
+        float h[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int n = n0 + r < rowend ? n0 + r : rowend - 1;
+          float gg = gv[r], uu = acc[0][cc][r];
+          if (G.sw) gg = gg * G.sw[n];
+          if (Up.sw) uu = uu * Up.sw[n];
+          h[r] = glu_silu(gg * xs, uu * xs);
+        }
+        float* hp = reinterpret_cast<float*>(G.Y) + (int64_t)m * G.ldy + n0;
+        if (G.vec_store && n0 + 3 < rowend) {
+          *reinterpret_cast<v4f*>(hp) = (v4f){h[0], h[1], h[2], h[3]};
+        } else {
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (n0 + r < rowend) hp[r] = h[r];
+        }
+      }
+    }
+    return;
+  }
   if (!active) return;
   xdl_fence();
 #pragma unroll
@@ -876,12 +927,12 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a) {
 // slots and two-step groups for four; fp8 without wide metadata loads (metadata rows not
 // 16-byte aligned, four separately masked loads per chunk) one step lighter, and even so
 // its four-tile, eight-wave instance spills a few registers.
-template <int DT, int CT, int RT, int WR, bool WM, bool TL, bool GR = false>
+template <int DT, int CT, int RT, int WR, bool WM, bool TL, int GM = 0>
 hipError_t launch_rows_wm(const dim3& grid, const dim3& block, const GemmArgs& a, hipStream_t s) {
   constexpr bool light = DT == kFP8 && !WM;
   constexpr int NS = CT <= 2 && RT == 1 && !light ? 4 : 3;
   constexpr int P = CT == 1 && RT == 1 ? 4 : 1;
-  hipLaunchKernelGGL((spense_gemm_rows_kernel<DT, CT, RT, WR, WM, NS, P, TL, GR>), grid, block, 0, s, a);
+  hipLaunchKernelGGL((spense_gemm_rows_kernel<DT, CT, RT, WR, WM, NS, P, TL, GM>), grid, block, 0, s, a);
   return hipGetLastError();
 }
 
@@ -889,8 +940,11 @@ template <int DT, int CT, int RT, int WR>
 hipError_t launch_rows(const LaunchShape& ls, const GemmArgs& a, hipStream_t s) {
   dim3 grid(a.groups, ls.mblocks), block(64 * WR);
   if constexpr (DT == kFP8) {
-    if (a.tiled && a.nmat > 1) {  // grouped launch: the tiled fp8 instances with 8 waves
-      if constexpr (RT == 1 && WR == 8) return launch_rows_wm<DT, CT, RT, WR, true, true, true>(grid, block, a, s);
+    if (a.tiled && (a.nmat > 1 || ls.glu)) {  // grouped or paired launch: tiled fp8, 8 waves
+      if constexpr (RT == 1 && WR == 8) {
+        if (ls.glu) return launch_rows_wm<DT, CT, RT, WR, true, true, 2>(grid, block, a, s);
+        return launch_rows_wm<DT, CT, RT, WR, true, true, 1>(grid, block, a, s);
+      }
       return hipErrorInvalidValue;
     }
     if (a.tiled) return launch_rows_wm<DT, CT, RT, WR, true, true>(grid, block, a, s);

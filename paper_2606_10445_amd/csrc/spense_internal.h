@@ -80,6 +80,13 @@ struct GemmArgs {
   Region reg[kMaxRegions];
 };
 
+// The GLU step h = u * silu(g) = u * g / (1 + e^-g) as every kernel computes it (the
+// hardware exponential and reciprocal), so that the fused and the separate MLP paths give
+// the same bits.
+__device__ __forceinline__ float glu_silu(float g, float u) {
+  return u * (g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)));
+}
+
 struct LaunchShape {
   int ct;       // 16-column tiles of M per workgroup (1, 2, 4)
   int rt;       // 16-row tiles per workgroup (1, 2, 4)
@@ -88,6 +95,7 @@ struct LaunchShape {
   int u8;       // eight instruction steps per batch of loads (single activation tile only)
   int rows;     // row-split workgroups with activations staged in LDS
   int big;      // large-M kernel: 128-row x 256-token workgroup tiles (fp8)
+  int glu;      // row-split kernel, gate and up paired: waves 0-3 gate tiles, 4-7 the same up tiles
 };
 
 hipError_t launch_gemm(int dtype, const LaunchShape& ls, const GemmArgs& a, hipStream_t s);

@@ -48,10 +48,9 @@ __device__ __forceinline__ float load_elem(const void* row, int64_t i) {
 }
 
 // h = u * silu(g) = u * (g * sigmoid(g)), fp32, exp and the reciprocal of 1 + exp(-g)
-// from the hardware approximations (about 1 ulp each).
-__device__ __forceinline__ float glu(float g, float u) {
-  return u * (g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)));
-}
+// from the hardware approximations (about 1 ulp each); the same helper as the fused
+// gate / up epilogue.
+__device__ __forceinline__ float glu(float g, float u) { return glu_silu(g, u); }
 
 template <int THREADS>
 __device__ __forceinline__ float block_max(float v, float* red) {

@@ -41,7 +41,7 @@ def test_library_exports_every_declared_symbol(S):
     for n in _declared():
         assert hasattr(lib, n), f"{n} declared in include/ but not exported"
     assert set(_declared()) == set(S.EXPORTS)
-    assert S.spense_abi_version() == 6
+    assert S.spense_abi_version() == 7
 
 
 @pytest.mark.parametrize("N,K,split,db", [(256, 512, 0, 192), (256, 512, 1, 384), (25600, 5120, 0, 19200),
@@ -301,3 +301,29 @@ def test_grouped_gemm_validates_arguments_on_the_host(S):
     assert g(None, 8, 256, 1, arr(d), None, None, ys, lds, 0, None) == S.SPENSE_ERR_ARG  # NULL X
     assert g((1 << 28) + 8, 8, 256, 1, arr(d), None, None, ys, lds, 0, None) == S.SPENSE_ERR_ALIGN  # unaligned X
     assert g(1 << 28, 0, 256, 1, arr(d), None, None, ys, lds, 0, None) == S.SPENSE_OK  # M = 0
+
+
+def test_gemm_glu_validates_arguments_on_the_host(S):
+    """Error paths of spense_gemm_glu return before touching the device."""
+    import ctypes
+    f = S.spense_gemm_glu
+    L = S.spense_layout(64, 256, S.SPENSE_FP8_E4M3FN, S.SPENSE_SPLIT_OUTPUT, 48)
+
+    def desc(N=64, K=256, db=48, layout=S.SPENSE_LAYOUT_TILED, dtype=1):
+        return S.spense_packed_t(dtype, 0, N, K, db, 1 << 20, L.values_ld, 2 << 20, L.meta_ld, 3 << 20, L.dense_ld,
+                                 layout)
+    g = desc()
+    ref = ctypes.byref
+    X, H = 1 << 28, 1 << 24
+    assert f(X, 8, 256, ref(g), None, None, None, None, H, 64, None) == S.SPENSE_ERR_ARG  # up NULL
+    assert f(X, 8, 256, ref(g), ref(desc(N=80)), None, None, None, H, 80, None) == S.SPENSE_ERR_ARG  # N differs
+    assert f(X, 8, 256, ref(g), ref(desc(db=32)), None, None, None, H, 64, None) == S.SPENSE_ERR_ARG  # dense_begin
+    assert f(X, 8, 256, ref(g), ref(desc(layout=S.SPENSE_LAYOUT_ROWMAJOR)), None, None, None, H, 64,
+             None) == S.SPENSE_ERR_ARG  # row-major
+    assert f(X, 8, 256, ref(g), ref(g), None, None, None, None, 64, None) == S.SPENSE_ERR_ARG  # H NULL
+    assert f(X, 8, 256, ref(g), ref(g), None, None, None, H, 32, None) == S.SPENSE_ERR_ARG  # ldh < N
+    assert f(X, 8, 256, ref(g), ref(g), None, None, None, H + 2, 64, None) == S.SPENSE_ERR_ALIGN  # H misaligned
+    assert f(None, 8, 256, ref(g), ref(g), None, None, None, H, 64, None) == S.SPENSE_ERR_ARG  # X NULL
+    assert f(X + 8, 8, 256, ref(g), ref(g), None, None, None, H, 64, None) == S.SPENSE_ERR_ALIGN  # X misaligned
+    assert f(X, 8, 128, ref(g), ref(g), None, None, None, H, 64, None) == S.SPENSE_ERR_ARG  # ldx < K
+    assert f(X, 0, 256, ref(g), ref(g), None, None, None, H, 64, None) == S.SPENSE_OK  # M = 0
