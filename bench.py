@@ -252,9 +252,10 @@ def measure_extras(args, torch, gen, S, ws, pws, copies, swd, mx, dws, dense_cop
                              "grouped_dense_us_per_layer": round(gdlms * 1e3, 1),
                              "grouped_speedup_vs_dense": round(gdlms / glms, 3)}
     # the GLU MLP block of the same layer (Eq. (4)), three launches: gate and up
-    # (output-split) with the GLU in their epilogue -> per-token fp8 quantisation of H ->
-    # down (input-split); the unfused block (gate and up grouped, G and U in fp32 -> GLU +
-    # quantisation -> down) beside it, and the steps alone
+    # (output-split) with the GLU in their epilogue, writing H and its row maxima ->
+    # per-token fp8 quantisation of H from those maxima -> down (input-split); the unfused
+    # block (gate and up grouped, G and U in fp32 -> GLU + quantisation -> down) beside it,
+    # and the steps alone
     names = [n for (n, _, _, _) in layer]
     gi, ui, di = names.index("gate"), names.index("up"), names.index("down")
     Xg, sxg, swg, _ = io[gi]
@@ -268,8 +269,7 @@ def measure_extras(args, torch, gen, S, ws, pws, copies, swd, mx, dws, dense_cop
 
     def run_mlp(ws_sets):
         def f(i):
-            S.gemm_glu(Xg, ws_sets[gi][i % 2], ws_sets[ui][i % 2], swg, swu, sxg, out=Hf)
-            S.quantize_fp8(Hf, q=Hq, scales=sh)
+            S.gemm_glu_fp8(Xg, ws_sets[gi][i % 2], ws_sets[ui][i % 2], swg, swu, sxg, q=Hq, scales=sh, workspace=ws)
             S.gemm(Hq, ws_sets[di][i % 2], swd_, sh, out=Yb, workspace=ws)
         return f
 
@@ -287,12 +287,15 @@ def measure_extras(args, torch, gen, S, ws, pws, copies, swd, mx, dws, dense_cop
                          torch)
     ggms = time_launches(lambda i: S.gemm_grouped(Xg, [sets[gi][i % 2], sets[ui][i % 2]], [swg, swu], sxg,
                                                   outs=[Gb, Ub], out_f32=True), 100, 10, torch)
+    fqms = time_launches(lambda i: S.gemm_glu_fp8(Xg, sets[gi][i % 2], sets[ui][i % 2], swg, swu, sxg, q=Hq,
+                                                  scales=sh, workspace=ws), 100, 10, torch)
     qms = time_launches(lambda i: S.quantize_fp8(Hf, q=Hq, scales=sh), 200, 10, torch)
     gms = time_launches(lambda i: S.glu_quantize_fp8(Gb, Ub, q=Hq, scales=sh), 200, 10, torch)
     glu_bytes = 2 * Gb.numel() * 4 + Hq.numel() + 4 * Ml  # g, u read once, codes and scales written
     q_bytes = Hf.numel() * 4 + Hq.numel() + 4 * Ml  # h read once, codes and scales written
     ex["qwen3_mlp_m64"] = {"us_per_block": round(mms * 1e3, 1), "dense_us_per_block": round(dmms * 1e3, 1),
                            "speedup_vs_dense": round(dmms / mms, 3), "unfused_us_per_block": round(umms * 1e3, 1),
+                           "gate_up_glu_fp8_us": round(fqms * 1e3, 2),
                            "gate_up_glu_us": round(fgms * 1e3, 2), "gate_up_grouped_fp32_us": round(ggms * 1e3, 2),
                            "quantize_us": round(qms * 1e3, 2), "quantize_gbs": round(q_bytes / (qms * 1e-3) / 1e9, 1),
                            "glu_quantize_us": round(gms * 1e3, 2),
@@ -323,7 +326,6 @@ def profile_layer(torch, gen, S, steps):
                    torch.empty((Ml, n_), dtype=torch.bfloat16, device="cuda")))
     names = [n for (n, _, _, _) in gen.QWEN3_32B_LAYER]
     gi, ui, di = names.index("gate"), names.index("up"), names.index("down")
-    Hf = torch.empty((Ml, pk[gi].N), dtype=torch.float32, device="cuda")
     Hq = torch.empty((Ml, pk[gi].N), dtype=torch.uint8, device="cuda")
     sh = torch.empty(Ml, dtype=torch.float32, device="cuda")
     Yb = torch.empty((Ml, pk[di].N), dtype=torch.bfloat16, device="cuda")
@@ -337,12 +339,12 @@ def profile_layer(torch, gen, S, steps):
                            outs=[io[j][3] for j in grp])
             Xd_, sx_, sw_, Y_ = io[single]
             S.gemm(Xd_, pk[single], sw_, sx_, out=Y_, workspace=ws)
-        S.gemm_glu(io[gi][0], pk[gi], pk[ui], io[gi][2], io[ui][2], io[gi][1], out=Hf)
-        S.quantize_fp8(Hf, q=Hq, scales=sh)
+        S.gemm_glu_fp8(io[gi][0], pk[gi], pk[ui], io[gi][2], io[ui][2], io[gi][1], q=Hq, scales=sh, workspace=ws)
         S.gemm(Hq, pk[di], io[di][2], sh, out=Yb, workspace=ws)
     torch.cuda.synchronize()
     return {"profile_layer": steps, "order": names + ["grouped q,k,v", "grouped o", "grouped gate,up", "grouped down",
-                                                      "mlp.gate,up+glu", "mlp.quantize", "mlp.down"]}
+                                                      "mlp.gate,up+glu", "mlp.quantize_rowmax",
+                                                      "mlp.down"]}
 
 
 def device_matrix(torch, S, N, K, split, frac, seed, gen):

@@ -37,7 +37,7 @@
 extern "C" {
 #endif
 
-#define SPENSE_ABI_VERSION 7
+#define SPENSE_ABI_VERSION 8
 
 typedef enum spense_status {
   SPENSE_OK = 0,
@@ -261,6 +261,28 @@ int spense_gemm_grouped(const void* X, int64_t M, int64_t ldx, int32_t count, co
 int spense_gemm_glu(const void* X, int64_t M, int64_t ldx, const spense_packed_t* gate, const spense_packed_t* up,
                     const float* w_scale_gate, const float* w_scale_up, const float* x_scale, float* H, int64_t ldh,
                     hipStream_t stream);
+
+/* Device workspace (bytes) that spense_gemm_glu_fp8 needs for M tokens and N gate / up
+ * rows (0 for sizes below 1 or above 2^31-1). */
+size_t spense_gemm_glu_fp8_workspace_size(int64_t M, int64_t N);
+
+/*
+ * The producer half of the GLU MLP (sec. 3.3.1, Eq. (4)) in two launches: gate and up
+ * with the GLU step in their epilogue, as spense_gemm_glu, writing H into the workspace
+ * together with each workgroup's per-token maximum of |h|; then the per-token fp8
+ * quantisation of H from those maxima (one workgroup per 2048 columns of a token row).
+ * q (M x N e4m3fn codes, ldq bytes) and scales (M fp32) equal, bit for bit, those of
+ * spense_quantize_fp8 applied to spense_gemm_glu's H, and of spense_glu_quantize_fp8
+ * applied to the fp32 G and U of spense_gemm_grouped: the input of the down projection.
+ * Weights, X and scales as spense_gemm_glu.  ws: device workspace of at least
+ * spense_gemm_glu_fp8_workspace_size(M, N) bytes, 256-byte aligned, caller-owned, its
+ * contents not kept.  Asynchronous; allocates nothing.  Errors as spense_gemm_glu,
+ * SPENSE_ERR_ARG for a NULL q or scales or ldq < N, SPENSE_ERR_WS for a missing or small
+ * workspace, SPENSE_ERR_ALIGN for a misaligned one.
+ */
+int spense_gemm_glu_fp8(const void* X, int64_t M, int64_t ldx, const spense_packed_t* gate, const spense_packed_t* up,
+                        const float* w_scale_gate, const float* w_scale_up, const float* x_scale, uint8_t* q,
+                        int64_t ldq, float* scales, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Device workspace (bytes) that spense_dense_gemm needs; same rules as above. */
 size_t spense_dense_gemm_workspace_size(int64_t M, int64_t N, int64_t K, int32_t dtype);

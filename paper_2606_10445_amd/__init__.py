@@ -43,7 +43,8 @@ EXPORTS = ["spense_abi_version", "spense_last_error", "spense_layout", "spense_t
            "spense_gemm_workspace_size", "spense_gemm", "spense_dense_gemm_workspace_size", "spense_dense_gemm",
            "spense_quantize_fp8", "spense_glu_quantize_fp8", "spense_index_scores", "spense_dense_permutation",
            "spense_gather_rows", "spense_gather_cols", "spense_obs_factor_workspace_size", "spense_obs_factor",
-           "spense_obs_prune_workspace_size", "spense_obs_prune_24", "spense_gemm_grouped", "spense_gemm_glu"]
+           "spense_obs_prune_workspace_size", "spense_obs_prune_24", "spense_gemm_grouped", "spense_gemm_glu",
+           "spense_gemm_glu_fp8_workspace_size", "spense_gemm_glu_fp8"]
 
 
 class SpenseError(RuntimeError):
@@ -103,6 +104,8 @@ def _load():
         "spense_obs_prune_24": (ctypes.c_int, [p, i64, i64, i64, p, i64, p, i64, p, i64, p, sz, p]),
         "spense_gemm_grouped": (ctypes.c_int, [p, i64, i64, i32, p, p, p, p, p, u32, p]),
         "spense_gemm_glu": (ctypes.c_int, [p, i64, i64, p, p, p, p, p, p, i64, p]),
+        "spense_gemm_glu_fp8_workspace_size": (ctypes.c_size_t, [i64, i64]),
+        "spense_gemm_glu_fp8": (ctypes.c_int, [p, i64, i64, p, p, p, p, p, p, i64, p, p, ctypes.c_size_t, p]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -213,6 +216,16 @@ def spense_gemm_grouped(X, M, ldx, count, packed_array, w_scales_array, x_scale,
 
 def spense_gemm_glu(X, M, ldx, gate, up, w_scale_gate, w_scale_up, x_scale, H, ldh, stream) -> int:
     return _lib.spense_gemm_glu(X, M, ldx, gate, up, w_scale_gate, w_scale_up, x_scale, H, ldh, stream)
+
+
+def spense_gemm_glu_fp8_workspace_size(M: int, N: int) -> int:
+    return _lib.spense_gemm_glu_fp8_workspace_size(M, N)
+
+
+def spense_gemm_glu_fp8(X, M, ldx, gate, up, w_scale_gate, w_scale_up, x_scale, q, ldq, scales, ws, ws_bytes,
+                        stream) -> int:
+    return _lib.spense_gemm_glu_fp8(X, M, ldx, gate, up, w_scale_gate, w_scale_up, x_scale, q, ldq, scales, ws,
+                                    ws_bytes, stream)
 
 
 def spense_obs_factor_workspace_size(K: int) -> int:
@@ -434,6 +447,35 @@ def gemm_glu(X: torch.Tensor, gate: PackedWeight, up: PackedWeight, gate_scale=N
     return out
 
 
+def gemm_glu_fp8(X: torch.Tensor, gate: PackedWeight, up: PackedWeight, gate_scale=None, up_scale=None,
+                 x_scale=None, q=None, scales=None, workspace: Workspace | None = None):
+    """The producer half of the GLU MLP (spense_gemm_glu_fp8): H = glu(X Wg^T, X Wu^T) in
+    the gate / up epilogue, then its per-token fp8 quantisation from the epilogue's row
+    maxima.  Returns (codes uint8 M x N, scales fp32 M), the down projection's input."""
+    _row_major(X, "X")
+    M = X.shape[0]
+    if gate.K != X.shape[1] or up.K != X.shape[1]:
+        raise ValueError("X.shape[1] must equal K")
+    if gate.N != up.N:
+        raise ValueError("gate and up must have the same N")
+    N = gate.N
+    q = torch.empty((M, N), dtype=torch.uint8, device=X.device) if q is None else q
+    scales = torch.empty(M, dtype=torch.float32, device=X.device) if scales is None else scales
+    _row_major(q, "q")
+    if q.dtype != torch.uint8 or q.shape != (M, N):
+        raise ValueError(f"q must be uint8 of shape {(M, N)}")
+    _check_scale(scales, M, X.device, "scales")
+    _check_scale(gate_scale, N, X.device, "gate_scale")
+    _check_scale(up_scale, N, X.device, "up_scale")
+    _check_scale(x_scale, M, X.device, "x_scale")
+    ws = workspace or workspace_for(X.device)
+    wp, wn = ws.get(spense_gemm_glu_fp8_workspace_size(M, N) if M > 0 and N > 0 else 0)
+    _check(spense_gemm_glu_fp8(_ptr(X), M, X.stride(0), ctypes.byref(gate.desc), ctypes.byref(up.desc),
+                               _ptr(gate_scale), _ptr(up_scale), _ptr(x_scale), _ptr(q), q.stride(0), _ptr(scales),
+                               wp, wn, _stream(X.device)))
+    return q, scales
+
+
 def dense_gemm(X: torch.Tensor, W: torch.Tensor, w_scale=None, x_scale=None, out=None, out_f32=False,
                workspace: Workspace | None = None) -> torch.Tensor:
     """The dense baseline Y = X W^T (spense_dense_gemm)."""
@@ -492,14 +534,14 @@ def glu_quantize_fp8(G: torch.Tensor, U: torch.Tensor, q=None, scales=None):
 def mlp(X: torch.Tensor, x_scale: torch.Tensor, gate: PackedWeight, up: PackedWeight, down: PackedWeight,
         gate_scale=None, up_scale=None, down_scale=None, out=None, workspace: Workspace | None = None):
     """The GLU MLP of the paper's sec. 3.3.1 Eq. (4) on Spense weights: H = glu(gate(X),
-    up(X)) (output-split; for tiled fp8 weights of one geometry one launch with the GLU in
-    its epilogue, otherwise G and U in fp32 and the GLU fused with the quantisation),
-    (Hq, sh) = per-token fp8 quantisation, Y = down(Hq) (input-split, bf16 out).  X: fp8
-    codes with x_scale."""
+    up(X)) (output-split) and (Hq, sh) its per-token fp8 quantisation (for tiled fp8
+    weights of one geometry the GLU in the gate / up epilogue, then the quantisation from
+    the epilogue's row maxima; otherwise G and U in fp32 and the GLU fused with the
+    quantisation), Y = down(Hq) (input-split, bf16 out).  X: fp8 codes with x_scale."""
     paired = (gate.kind == up.kind == SPENSE_LAYOUT_TILED and gate.dtype == up.dtype == SPENSE_FP8_E4M3FN
               and gate.split == up.split == SPENSE_SPLIT_OUTPUT)
     if paired and gate.N == up.N and gate.K == up.K and gate.dense_begin == up.dense_begin:
-        Hq, sh = quantize_fp8(gemm_glu(X, gate, up, gate_scale, up_scale, x_scale))
+        Hq, sh = gemm_glu_fp8(X, gate, up, gate_scale, up_scale, x_scale, workspace=workspace)
     else:
         if paired and gate.K == up.K:
             G, U = gemm_grouped(X, [gate, up], None if gate_scale is None else [gate_scale, up_scale], x_scale,

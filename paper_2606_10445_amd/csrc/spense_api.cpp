@@ -504,6 +504,136 @@ int gemm_common(const void* X, int64_t M, int64_t ldx, int32_t dtype, int32_t sp
   return ok();
 }
 
+// Checks of the gate / up pair and X shared by the GLU calls.
+int check_glu_pair(const void* X, int64_t M, int64_t ldx, const spense_packed_t* gate, const spense_packed_t* up) {
+  if (!gate || !up) return fail(SPENSE_ERR_ARG, "gate or up is NULL");
+  if (M < 0 || M > INT32_MAX) return fail(SPENSE_ERR_ARG, "bad M");
+  for (const spense_packed_t* P : {gate, up}) {
+    spense_layout_t L;
+    int rc = check_packed(P, &L);
+    if (rc) return rc;
+    if (P->dtype != SPENSE_FP8_E4M3FN || P->layout != SPENSE_LAYOUT_TILED || P->split != SPENSE_SPLIT_OUTPUT)
+      return fail(SPENSE_ERR_ARG, "gate and up must be fp8, output-split, in the tiled layout");
+  }
+  if (gate->N != up->N || gate->K != up->K || gate->dense_begin != up->dense_begin)
+    return fail(SPENSE_ERR_ARG, "gate and up must have the same N, K and dense_begin");
+  const int64_t N = gate->N, K = gate->K;
+  if (M == 0 || N == 0) return SPENSE_OK;
+  if (K == 0) return fail(SPENSE_ERR_ARG, "K = 0 (H would be glu(0, 0) = 0; not a GEMM)");
+  if (!X) return fail(SPENSE_ERR_ARG, "X is NULL");
+  if (ldx < K) return fail(SPENSE_ERR_ARG, "ldx=%lld < K=%lld", (long long)ldx, (long long)K);
+  if (!aligned16(X) || ldx % 16) return fail(SPENSE_ERR_ALIGN, "X must be 16-byte aligned with a 16-byte multiple row pitch");
+  if ((M - 1) * ldx + K >= ((int64_t)1 << 31)) return fail(SPENSE_ERR_ARG, "X spans 2 GiB or more");
+  spense_tiled_layout_t T;
+  tiled_impl(N, K, SPENSE_FP8_E4M3FN, SPENSE_SPLIT_OUTPUT, gate->dense_begin, &T);
+  if ((int64_t)T.values_bytes >= ((int64_t)1 << 31) || (int64_t)T.meta_bytes >= ((int64_t)1 << 31) ||
+      (int64_t)T.dense_bytes >= ((int64_t)1 << 31))
+    return fail(SPENSE_ERR_ARG, "weights span 2 GiB or more");
+  return SPENSE_OK;
+}
+
+// The paired gate / up launch (arguments checked, M, N > 0): H (fp32, ldh) and, when hmax
+// is given, the per-workgroup maxima of |h| per token, hmax[m * groups + g]; *groups_out
+// receives the number of workgroups along N.
+int launch_glu_pair(const void* X, int64_t M, int64_t ldx, const spense_packed_t* gate, const spense_packed_t* up,
+                    const float* w_scale_gate, const float* w_scale_up, const float* x_scale, float* H, int64_t ldh,
+                    float* hmax, int32_t* groups_out, hipStream_t stream) {
+  using spense::Region;
+  const int64_t N = gate->N, K = gate->K, db = gate->dense_begin;
+  spense_tiled_layout_t T;
+  tiled_impl(N, K, SPENSE_FP8_E4M3FN, SPENSE_SPLIT_OUTPUT, db, &T);
+  // Plan: the row-split kernel with 8 waves, waves 0-3 on gate tiles and 4-7 on the up
+  // tiles of the same rows, no K slices; the dense rows first, then the 2:4 rows; row
+  // tiles per workgroup (1-4) per kind from the same cost model as the grouped launch,
+  // each tile counted twice (gate and up).
+  spense::LaunchShape ls;
+  memset(&ls, 0, sizeof ls);
+  ls.ct = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
+  ls.mblocks = (int)ceil_div(M, 16 * ls.ct);
+  ls.rt = 1;
+  ls.waves = 8;
+  ls.rows = 1;
+  ls.glu = 1;
+  spense::GemmArgs a;
+  memset(&a, 0, sizeof a);
+  const double sparse_cost = 0.625;  // fp8 bytes per logical 2:4 entry
+  Region regs[2];
+  int nreg = 0;
+  for (int pass = 0; pass < 2; ++pass) {
+    const int64_t r0 = pass == 0 ? db : 0, rows = pass == 0 ? N - db : db;
+    if (rows <= 0) continue;
+    Region r;
+    memset(&r, 0, sizeof r);
+    r.row0 = (int32_t)r0;
+    r.rows = (int32_t)rows;
+    r.kbound = pass == 0 ? 0 : (int32_t)K;
+    r.kend = (int32_t)K;
+    r.dense_row_off = (int32_t)db;
+    slice_cuts(r, 1, 512, 1, sparse_cost);
+    regs[nreg++] = r;
+  }
+  const double tile_d = 2 * 16.0 * K, tile_s = 2 * 16.0 * sparse_cost * K, x_cost = 0.25 * 16.0 * ls.ct * K;
+  double best = 0;
+  int64_t best_wg = 0;
+  int bw0 = 4, bw1 = 4;
+  for (int w0 = 1; w0 <= 4; ++w0)
+    for (int w1 = 1; w1 <= 4; ++w1) {
+      int64_t wg = 0;
+      double big = 0;
+      for (int i = 0; i < nreg; ++i) {
+        const int w = regs[i].kbound == 0 ? w0 : w1;
+        wg += ceil_div(regs[i].rows, 16 * w) * ls.mblocks;
+        big = std::max(big, w * (regs[i].kbound == 0 ? tile_d : tile_s));
+      }
+      const double t = (double)ceil_div(wg, kCUs) * (big + x_cost);
+      if (best_wg == 0 || t < best * (1 - 1e-9) || (t <= best * (1 + 1e-9) && wg < best_wg)) {
+        best = t;
+        best_wg = wg;
+        bw0 = w0;
+        bw1 = w1;
+      }
+    }
+  int32_t groups = 0;
+  for (int i = 0; i < nreg; ++i) {
+    regs[i].wused = regs[i].kbound == 0 ? bw0 : bw1;
+    regs[i].nrb = (int32_t)ceil_div(regs[i].rows, 16 * regs[i].wused);
+    regs[i].wg0 = groups;
+    groups += regs[i].nrb;
+    a.reg[i] = regs[i];
+  }
+  a.nreg = nreg;
+  a.groups = groups;
+  a.tiled = 1;
+  a.X = static_cast<const uint8_t*>(X);
+  a.ldx_b = ldx;
+  a.x_bytes = (uint32_t)((M - 1) * ldx + K);
+  a.sx = x_scale;
+  a.M = (int32_t)M;
+  a.N = (int32_t)N;
+  a.out_f32 = 1;
+  a.nmat = 2;
+  const bool vec = ldh % 4 == 0 && reinterpret_cast<uintptr_t>(H) % 16 == 0 && db % 4 == 0;
+  const spense_packed_t* const PW[2] = {gate, up};
+  const float* const SW[2] = {w_scale_gate, w_scale_up};
+  for (int i = 0; i < 2; ++i)
+    a.mat[i] = spense::MatDesc{static_cast<const uint8_t*>(PW[i]->values), PW[i]->meta,
+                               static_cast<const uint8_t*>(PW[i]->dense), (uint32_t)T.values_bytes,
+                               (uint32_t)T.meta_bytes, (uint32_t)T.dense_bytes, H, ldh, SW[i], vec ? 1 : 0};
+  // the row maxima take one slot per workgroup along N: at most ceil(rows / 16) per region
+  if (hmax && groups > ceil_div(N, 16) + 1) return fail(SPENSE_ERR_HIP, "internal: %d workgroups along N", groups);
+  a.hmax = hmax;
+  *groups_out = groups;
+  hipError_t e = spense::launch_gemm(SPENSE_FP8_E4M3FN, ls, a, stream);
+  if (e != hipSuccess) return fail(SPENSE_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return SPENSE_OK;
+}
+
+// Workspace of spense_gemm_glu_fp8: H (fp32, rows padded to 64 elements), then the
+// per-workgroup row maxima (at least 16 weight rows per workgroup, in each of the two
+// regions).
+int64_t glu_ldh(int64_t N) { return (N + 63) / 64 * 64; }
+int64_t glu_hmax_offset(int64_t M, int64_t N) { return (M * glu_ldh(N) * 4 + 255) / 256 * 256; }
+
 }  // namespace
 
 extern "C" {
@@ -927,119 +1057,55 @@ int spense_gemm_grouped(const void* X, int64_t M, int64_t ldx, int32_t count, co
 int spense_gemm_glu(const void* X, int64_t M, int64_t ldx, const spense_packed_t* gate, const spense_packed_t* up,
                     const float* w_scale_gate, const float* w_scale_up, const float* x_scale, float* H, int64_t ldh,
                     hipStream_t stream) {
-  using spense::Region;
-  if (!gate || !up) return fail(SPENSE_ERR_ARG, "gate or up is NULL");
-  if (M < 0 || M > INT32_MAX) return fail(SPENSE_ERR_ARG, "bad M");
-  for (const spense_packed_t* P : {gate, up}) {
-    spense_layout_t L;
-    int rc = check_packed(P, &L);
-    if (rc) return rc;
-    if (P->dtype != SPENSE_FP8_E4M3FN || P->layout != SPENSE_LAYOUT_TILED || P->split != SPENSE_SPLIT_OUTPUT)
-      return fail(SPENSE_ERR_ARG, "gate and up must be fp8, output-split, in the tiled layout");
-  }
-  if (gate->N != up->N || gate->K != up->K || gate->dense_begin != up->dense_begin)
-    return fail(SPENSE_ERR_ARG, "gate and up must have the same N, K and dense_begin");
-  const int64_t N = gate->N, K = gate->K, db = gate->dense_begin;
+  int rc = check_glu_pair(X, M, ldx, gate, up);
+  if (rc) return rc;
+  const int64_t N = gate->N;
   if (!H) return fail(SPENSE_ERR_ARG, "H is NULL");
   if (ldh < N) return fail(SPENSE_ERR_ARG, "ldh < N");
   if (reinterpret_cast<uintptr_t>(H) % 4) return fail(SPENSE_ERR_ALIGN, "H misaligned");
   if ((int64_t)M * ldh > (int64_t)1 << 40) return fail(SPENSE_ERR_ARG, "H too large");
   if (M == 0 || N == 0) return ok();
-  if (K == 0) return fail(SPENSE_ERR_ARG, "K = 0 (H would be glu(0, 0) = 0; not a GEMM)");
-  if (!X) return fail(SPENSE_ERR_ARG, "X is NULL");
-  if (ldx < K) return fail(SPENSE_ERR_ARG, "ldx=%lld < K=%lld", (long long)ldx, (long long)K);
-  if (!aligned16(X) || ldx % 16) return fail(SPENSE_ERR_ALIGN, "X must be 16-byte aligned with a 16-byte multiple row pitch");
-  const int64_t xb = (M - 1) * ldx + K;
-  if (xb >= ((int64_t)1 << 31)) return fail(SPENSE_ERR_ARG, "X spans 2 GiB or more");
-  spense_tiled_layout_t T;
-  tiled_impl(N, K, SPENSE_FP8_E4M3FN, SPENSE_SPLIT_OUTPUT, db, &T);
-  if ((int64_t)T.values_bytes >= ((int64_t)1 << 31) || (int64_t)T.meta_bytes >= ((int64_t)1 << 31) ||
-      (int64_t)T.dense_bytes >= ((int64_t)1 << 31))
-    return fail(SPENSE_ERR_ARG, "weights span 2 GiB or more");
-
-  // Plan: the row-split kernel with 8 waves, waves 0-3 on gate tiles and 4-7 on the up
-  // tiles of the same rows, no K slices; the dense rows first, then the 2:4 rows; row
-  // tiles per workgroup (1-4) per kind from the same cost model as the grouped launch,
-  // each tile counted twice (gate and up).
-  spense::LaunchShape ls;
-  memset(&ls, 0, sizeof ls);
-  ls.ct = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
-  ls.mblocks = (int)ceil_div(M, 16 * ls.ct);
-  ls.rt = 1;
-  ls.waves = 8;
-  ls.rows = 1;
-  ls.glu = 1;
-  spense::GemmArgs a;
-  memset(&a, 0, sizeof a);
-  const double sparse_cost = 0.625;  // fp8 bytes per logical 2:4 entry
-  Region regs[2];
-  int nreg = 0;
-  for (int pass = 0; pass < 2; ++pass) {
-    const int64_t r0 = pass == 0 ? db : 0, rows = pass == 0 ? N - db : db;
-    if (rows <= 0) continue;
-    Region r;
-    memset(&r, 0, sizeof r);
-    r.row0 = (int32_t)r0;
-    r.rows = (int32_t)rows;
-    r.kbound = pass == 0 ? 0 : (int32_t)K;
-    r.kend = (int32_t)K;
-    r.dense_row_off = (int32_t)db;
-    slice_cuts(r, 1, 512, 1, sparse_cost);
-    regs[nreg++] = r;
-  }
-  const double tile_d = 2 * 16.0 * K, tile_s = 2 * 16.0 * sparse_cost * K, x_cost = 0.25 * 16.0 * ls.ct * K;
-  double best = 0;
-  int64_t best_wg = 0;
-  int bw0 = 4, bw1 = 4;
-  for (int w0 = 1; w0 <= 4; ++w0)
-    for (int w1 = 1; w1 <= 4; ++w1) {
-      int64_t wg = 0;
-      double big = 0;
-      for (int i = 0; i < nreg; ++i) {
-        const int w = regs[i].kbound == 0 ? w0 : w1;
-        wg += ceil_div(regs[i].rows, 16 * w) * ls.mblocks;
-        big = std::max(big, w * (regs[i].kbound == 0 ? tile_d : tile_s));
-      }
-      const double t = (double)ceil_div(wg, kCUs) * (big + x_cost);
-      if (best_wg == 0 || t < best * (1 - 1e-9) || (t <= best * (1 + 1e-9) && wg < best_wg)) {
-        best = t;
-        best_wg = wg;
-        bw0 = w0;
-        bw1 = w1;
-      }
-    }
-  int32_t groups = 0;
-  for (int i = 0; i < nreg; ++i) {
-    regs[i].wused = regs[i].kbound == 0 ? bw0 : bw1;
-    regs[i].nrb = (int32_t)ceil_div(regs[i].rows, 16 * regs[i].wused);
-    regs[i].wg0 = groups;
-    groups += regs[i].nrb;
-    a.reg[i] = regs[i];
-  }
-  a.nreg = nreg;
-  a.groups = groups;
-  a.tiled = 1;
-  a.X = static_cast<const uint8_t*>(X);
-  a.ldx_b = ldx;
-  a.x_bytes = (uint32_t)xb;
-  a.sx = x_scale;
-  a.M = (int32_t)M;
-  a.N = (int32_t)N;
-  a.out_f32 = 1;
-  a.nmat = 2;
-  const bool vec = ldh % 4 == 0 && reinterpret_cast<uintptr_t>(H) % 16 == 0 && db % 4 == 0;
-  const spense_packed_t* const PW[2] = {gate, up};
-  const float* const SW[2] = {w_scale_gate, w_scale_up};
-  for (int i = 0; i < 2; ++i)
-    a.mat[i] = spense::MatDesc{static_cast<const uint8_t*>(PW[i]->values), PW[i]->meta,
-                               static_cast<const uint8_t*>(PW[i]->dense), (uint32_t)T.values_bytes,
-                               (uint32_t)T.meta_bytes, (uint32_t)T.dense_bytes, H, ldh, SW[i], vec ? 1 : 0};
-  int rc = check_device();
+  rc = check_device();
   if (rc) return rc;
-  hipError_t e = spense::launch_gemm(SPENSE_FP8_E4M3FN, ls, a, stream);
-  if (e != hipSuccess) return fail(SPENSE_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  int32_t groups = 0;
+  rc = launch_glu_pair(X, M, ldx, gate, up, w_scale_gate, w_scale_up, x_scale, H, ldh, nullptr, &groups, stream);
+  return rc ? rc : ok();
+}
+
+size_t spense_gemm_glu_fp8_workspace_size(int64_t M, int64_t N) {
+  if (M <= 0 || N <= 0 || M > INT32_MAX || N > INT32_MAX) return 0;
+  // workgroups along N: at most ceil(rows / 16) per region, two regions
+  return (size_t)(glu_hmax_offset(M, N) + M * (ceil_div(N, 16) + 1) * 4);
+}
+
+int spense_gemm_glu_fp8(const void* X, int64_t M, int64_t ldx, const spense_packed_t* gate, const spense_packed_t* up,
+                        const float* w_scale_gate, const float* w_scale_up, const float* x_scale, uint8_t* q,
+                        int64_t ldq, float* scales, void* ws, size_t ws_bytes, hipStream_t stream) {
+  int rc = check_glu_pair(X, M, ldx, gate, up);
+  if (rc) return rc;
+  const int64_t N = gate->N;
+  if (M == 0) return ok();
+  if (!scales) return fail(SPENSE_ERR_ARG, "scales is NULL");
+  if (N > 0 && !q) return fail(SPENSE_ERR_ARG, "q is NULL");
+  if (ldq < N) return fail(SPENSE_ERR_ARG, "ldq < N");
+  if (N == 0) return fail(SPENSE_ERR_ARG, "N = 0");
+  const size_t need = spense_gemm_glu_fp8_workspace_size(M, N);
+  if (!ws || ws_bytes < need)
+    return fail(SPENSE_ERR_WS, "workspace of %zu bytes needed, %zu given", need, ws ? ws_bytes : (size_t)0);
+  if (reinterpret_cast<uintptr_t>(ws) % 256) return fail(SPENSE_ERR_ALIGN, "workspace must be 256-byte aligned");
+  rc = check_device();
+  if (rc) return rc;
+  float* H = static_cast<float*>(ws);
+  float* hmax = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + glu_hmax_offset(M, N));
+  int32_t groups = 0;
+  rc = launch_glu_pair(X, M, ldx, gate, up, w_scale_gate, w_scale_up, x_scale, H, glu_ldh(N), hmax, &groups, stream);
+  if (rc) return rc;
+  if (spense::launch_quantize_rowmax(H, glu_ldh(N), M, N, hmax, groups, q, ldq, scales, stream) != hipSuccess)
+    return fail(SPENSE_ERR_HIP, "quantize launch failed");
   return ok();
 }
+
+
 
 size_t spense_dense_gemm_workspace_size(int64_t M, int64_t N, int64_t K, int32_t dtype) {
   spense_layout_t L;

@@ -847,6 +847,9 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
       for (int cc = 0; cc < CT; ++cc) *reinterpret_cast<v4f*>(ex + ((wsel * CT + cc) * 64 + lane) * 4) = acc[0][cc];
     }
     barrier_vm_lgkm0<63>();
+    float tmax[CT];  // per token: the maximum of |h| over this lane's stored rows
+#pragma unroll
+    for (int cc = 0; cc < CT; ++cc) tmax[cc] = 0.0f;
     if (wave >= 4 && active) {
       const MatDesc& G = a.mat[0];
       const MatDesc& Up = a.mat[1];
@@ -865,6 +868,7 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
           if (G.sw) gg = gg * G.sw[n];
           if (Up.sw) uu = uu * Up.sw[n];
           h[r] = glu_silu(gg * xs, uu * xs);
+          if (n0 + r < rowend) tmax[cc] = fmaxf(tmax[cc], fabsf(h[r]));
         }
         float* hp = reinterpret_cast<float*>(G.Y) + (int64_t)m * G.ldy + n0;
         if (G.vec_store && n0 + 3 < rowend) {
@@ -874,6 +878,25 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
           for (int r = 0; r < 4; ++r)
             if (n0 + r < rowend) hp[r] = h[r];
         }
+      }
+    }
+    if (a.hmax) {
+      // per token, the maximum over the workgroup's rows: the four row groups of a lane
+      // column (lanes li, li + 16, li + 32, li + 48), then the four up waves through LDS
+      float* red = reinterpret_cast<float*>(&xbuf[1][0]);
+      if (wave >= 4) {
+#pragma unroll
+        for (int cc = 0; cc < CT; ++cc) {
+          float v = fmaxf(tmax[cc], __shfl_xor(tmax[cc], 16, 64));
+          v = fmaxf(v, __shfl_xor(v, 32, 64));
+          if (lq == 0) red[wsel * 16 * CT + 16 * cc + li] = v;
+        }
+      }
+      barrier_vm_lgkm0<63>();
+      if (wave == 4 && lane < 16 * CT) {
+        const int m = m0 + lane;
+        const float v = fmaxf(fmaxf(red[lane], red[16 * CT + lane]), fmaxf(red[32 * CT + lane], red[48 * CT + lane]));
+        if (m < a.M) a.hmax[(int64_t)m * a.groups + g] = v;
       }
     }
     return;

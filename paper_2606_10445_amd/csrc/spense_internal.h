@@ -76,6 +76,7 @@ struct GemmArgs {
   int32_t tblocks;  // large-M kernel: 256-token blocks (workgroups of a row block are adjacent)
   int32_t xgt, xrc;  // large-M kernel, XCD-aware order (0 = off): token blocks per XCD, row classes
   int32_t nmat;
+  float* hmax;  // paired gate / up launch: per-workgroup maxima of |h| per token, hmax[m * groups + g] (or NULL)
   MatDesc mat[kMaxMats];
   Region reg[kMaxRegions];
 };
@@ -121,6 +122,10 @@ hipError_t launch_quantize(int type, const void* src, int64_t ld_b, int64_t M, i
                            float* scales, hipStream_t st);
 hipError_t launch_glu_quantize(int type, const void* g, int64_t ldg_b, const void* u, int64_t ldu_b, int64_t M,
                                int64_t I, uint8_t* q, int64_t ldq, float* scales, hipStream_t st);
+// Per-token fp8 quantisation of an fp32 M x N matrix H (ldh elements, rows 16-byte
+// aligned) whose row maxima come as partial maxima of |h|: pmax[m * P + p], p < P.
+hipError_t launch_quantize_rowmax(const float* H, int64_t ldh, int64_t M, int64_t N, const float* pmax, int P,
+                                  uint8_t* q, int64_t ldq, float* scales, hipStream_t st);
 
 // Dense-index selection (SpenseGPT+): priorities, TopK permutation, row / column gathers.
 hipError_t launch_index_scores(int type, const void* wg, const void* wu, int64_t ld_gu_b, int64_t I, int64_t D,

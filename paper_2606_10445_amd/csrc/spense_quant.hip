@@ -187,6 +187,59 @@ __global__ __launch_bounds__(kRowThreads) void quantize_rows_reg_kernel(const ui
   }
 }
 
+// fp32 rows whose maxima come as partial maxima (pmax[m * P + p], each the maximum of |h|
+// over some of the row's columns, together all of them; written by the producing GEMM):
+// a workgroup takes 2048 columns of one row, so that a matrix of few, long rows still
+// fills the GPU.  It reduces the row's P partials (exact in any order), forms the scale
+// as the row kernels do, and encodes its columns (16-byte loads, 4-byte code stores).
+constexpr int kPieceThreads = 256, kPieceCols = 8 * kPieceThreads;
+
+__global__ __launch_bounds__(kPieceThreads) void quantize_rowmax_kernel(const float* __restrict__ H, int64_t ldh,
+                                                                        int64_t N, const float* __restrict__ pmax, int P,
+                                                                        uint8_t* __restrict__ q, int64_t ldq,
+                                                                        float* __restrict__ scales, int vec_q,
+                                                                        int pieces) {
+  __shared__ float red[kPieceThreads / 64];
+  const int64_t m = blockIdx.x / pieces;
+  const int piece = blockIdx.x % pieces;
+  const float* hr = H + m * ldh;
+  // the two 4-column pieces of this thread: loads first
+  int64_t k[2];
+  float v[2][4];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    k[j] = (int64_t)piece * kPieceCols + 4 * (threadIdx.x + kPieceThreads * j);
+    if (k[j] + 4 <= N) {
+      const v4i x = *reinterpret_cast<const v4i*>(hr + k[j]);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[j][e] = __int_as_float(x[e]);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[j][e] = k[j] + e < N ? hr[k[j] + e] : 0.0f;
+    }
+  }
+  float amax = 0.0f;
+  const float* pr = pmax + m * P;
+  for (int p = threadIdx.x; p < P; p += kPieceThreads) amax = fmaxf(amax, pr[p]);
+  amax = block_max<kPieceThreads>(amax, red);
+  const float s = amax > 0.0f ? amax / 448.0f : 1.0f;
+  if (piece == 0 && threadIdx.x == 0) scales[m] = s;
+  uint8_t* qr = q + m * ldq;
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    if (k[j] >= N) continue;
+    const uint32_t w =
+        cvt2_e4m3fn<true>(v[j][2] / s, v[j][3] / s, cvt2_e4m3fn<false>(v[j][0] / s, v[j][1] / s, 0u));
+    if (vec_q && k[j] + 4 <= N) {
+      *reinterpret_cast<uint32_t*>(qr + k[j]) = w;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (k[j] + e < N) qr[k[j] + e] = (uint8_t)(w >> (8 * e));
+    }
+  }
+}
+
 template <int TYPE, bool GLU>
 hipError_t launch_quant_type(const uint8_t* a, int64_t ld0_b, const uint8_t* b, int64_t ld1_b, int64_t M, int64_t K,
                              uint8_t* q, int64_t ldq, float* scales, hipStream_t st) {
@@ -227,6 +280,16 @@ hipError_t launch_quant_t(int type, const void* s0, int64_t ld0_b, const void* s
 }
 
 }  // namespace
+
+hipError_t launch_quantize_rowmax(const float* H, int64_t ldh, int64_t M, int64_t N, const float* pmax, int P,
+                                  uint8_t* q, int64_t ldq, float* scales, hipStream_t st) {
+  const int vec_q = (uintptr_t)q % 4 == 0 && ldq % 4 == 0;
+  const int64_t pieces = (N + kPieceCols - 1) / kPieceCols;
+  if (M <= 0 || pieces <= 0 || M * pieces > INT32_MAX) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(quantize_rowmax_kernel, dim3((unsigned)(M * pieces)), dim3(kPieceThreads), 0, st, H, ldh, N, pmax,
+                     P, q, ldq, scales, vec_q, (int)pieces);
+  return hipGetLastError();
+}
 
 hipError_t launch_quantize(int type, const void* src, int64_t ld_b, int64_t M, int64_t K, uint8_t* q, int64_t ldq,
                            float* scales, hipStream_t st) {

@@ -41,7 +41,7 @@ def test_library_exports_every_declared_symbol(S):
     for n in _declared():
         assert hasattr(lib, n), f"{n} declared in include/ but not exported"
     assert set(_declared()) == set(S.EXPORTS)
-    assert S.spense_abi_version() == 7
+    assert S.spense_abi_version() == 8
 
 
 @pytest.mark.parametrize("N,K,split,db", [(256, 512, 0, 192), (256, 512, 1, 384), (25600, 5120, 0, 19200),
@@ -327,3 +327,28 @@ def test_gemm_glu_validates_arguments_on_the_host(S):
     assert f(X + 8, 8, 256, ref(g), ref(g), None, None, None, H, 64, None) == S.SPENSE_ERR_ALIGN  # X misaligned
     assert f(X, 8, 128, ref(g), ref(g), None, None, None, H, 64, None) == S.SPENSE_ERR_ARG  # ldx < K
     assert f(X, 0, 256, ref(g), ref(g), None, None, None, H, 64, None) == S.SPENSE_OK  # M = 0
+
+
+def test_gemm_glu_fp8_validates_arguments_on_the_host(S):
+    """Error paths of spense_gemm_glu_fp8 and its workspace size, before the device."""
+    import ctypes
+    f = S.spense_gemm_glu_fp8
+    L = S.spense_layout(64, 256, S.SPENSE_FP8_E4M3FN, S.SPENSE_SPLIT_OUTPUT, 48)
+    g = S.spense_packed_t(1, 0, 64, 256, 48, 1 << 20, L.values_ld, 2 << 20, L.meta_ld, 3 << 20, L.dense_ld,
+                          S.SPENSE_LAYOUT_TILED)
+    ref = ctypes.byref
+    X, Q, SC, WS = 1 << 28, 1 << 24, 1 << 23, 1 << 30
+    need = S.spense_gemm_glu_fp8_workspace_size(8, 64)
+    # H (8 rows of 64 fp32), then per token one maximum per workgroup along N: at most
+    # one per 16 rows of each of the two regions (48 + 16 rows here: 4, bounded by 5)
+    assert need == 8 * 64 * 4 + 8 * 5 * 4
+    assert S.spense_gemm_glu_fp8_workspace_size(0, 64) == 0
+    assert S.spense_gemm_glu_fp8_workspace_size(8, 0) == 0
+    assert f(X, 8, 256, ref(g), ref(g), None, None, None, Q, 64, SC, WS, need - 1, None) == S.SPENSE_ERR_WS
+    assert f(X, 8, 256, ref(g), ref(g), None, None, None, Q, 64, SC, None, need, None) == S.SPENSE_ERR_WS
+    assert f(X, 8, 256, ref(g), ref(g), None, None, None, Q, 64, SC, WS + 16, need, None) == S.SPENSE_ERR_ALIGN
+    assert f(X, 8, 256, ref(g), ref(g), None, None, None, None, 64, SC, WS, need, None) == S.SPENSE_ERR_ARG
+    assert f(X, 8, 256, ref(g), ref(g), None, None, None, Q, 64, None, WS, need, None) == S.SPENSE_ERR_ARG
+    assert f(X, 8, 256, ref(g), ref(g), None, None, None, Q, 63, SC, WS, need, None) == S.SPENSE_ERR_ARG
+    assert f(X, 8, 256, ref(g), None, None, None, None, Q, 64, SC, WS, need, None) == S.SPENSE_ERR_ARG
+    assert f(X, 0, 256, ref(g), ref(g), None, None, None, Q, 64, SC, WS, need, None) == S.SPENSE_OK

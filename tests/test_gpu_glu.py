@@ -12,6 +12,9 @@ sec. 3.2 output-split weights, sec. 3.3.1 Eq. (4) with SiLU), through the C ABI:
   the fused MLP is the unfused one;
 - random data: H within the fp32 GEMM error bound of the fp64 oracle, carried through
   the GLU (|dh/dg| <= 1.1 |u|, |dh/du| = |silu(g)|);
+- spense_gemm_glu_fp8 (the same launch writing per-workgroup row maxima, then the
+  quantisation from them): codes and scales bit for bit those of spense_quantize_fp8 on
+  spense_gemm_glu's H, with code rows that allow 4-byte stores and rows that do not;
 - the Qwen3-like gate / up (25600 x 5120, 25% dense rows) at M = 64, full size.
 """
 import sys
@@ -107,6 +110,16 @@ def test_gemm_glu_exact(S, M, N, K, split):
     torch.cuda.synchronize()
     assert torch.equal(q0, q1)
     assert torch.equal(s0.view(torch.int32), s1.view(torch.int32))
+    # the quantisation from the epilogue's row maxima, into wide code rows (ldq not a
+    # multiple of 4: element stores) and into packed ones
+    for ldq in (N + 3, N):
+        qbuf = torch.full((M, ldq), 0xAB, dtype=torch.uint8, device="cuda")
+        s2 = torch.empty(M, dtype=torch.float32, device="cuda")
+        S.gemm_glu_fp8(Xd, pg, pu, sgd, sud, sxd, q=qbuf[:, :N], scales=s2)
+        torch.cuda.synchronize()
+        assert torch.equal(qbuf[:, :N], q1)
+        assert torch.all(qbuf[:, N:] == 0xAB)
+        assert torch.equal(s2.view(torch.int32), s1.view(torch.int32))
 
 
 def test_gemm_glu_no_scales(S):
@@ -162,13 +175,39 @@ def test_gemm_glu_qwen3_gate_up_full_size(S):
     G, U = S.gemm_grouped(Xd, [pg, pu], [sgd, sud], sxd, out_f32=True)
     q0, s0 = S.glu_quantize_fp8(G, U)
     q1, s1 = S.quantize_fp8(H)
+    q2, s2 = S.gemm_glu_fp8(Xd, pg, pu, sgd, sud, sxd)
     torch.cuda.synchronize()
-    assert torch.equal(q0, q1)
+    assert torch.equal(q0, q1) and torch.equal(q1, q2)
     assert torch.equal(s0.view(torch.int32), s1.view(torch.int32))
+    assert torch.equal(s2.view(torch.int32), s1.view(torch.int32))
     g = oracle_y(X, Wg, mg, sg, sx, db).astype(np.float64)
     u = oracle_y(X, Wu, mu, su, sx, db).astype(np.float64)
     h_ref = oracle.glu_f64(g, u)
     assert np.all(np.abs(H.cpu().numpy() - h_ref) <= glu_bound(g, u, h_ref))
+
+
+def test_gemm_glu_fp8_random_rows(S):
+    """Random data with rows of very different magnitude and an all-zero token (scale 1):
+    the fused quantisation equals the two-step one bit for bit, over several token
+    blocks (M = 150)."""
+    M, N, K = 150, 1000, 768
+    db = gen.split_point(N, K, gen.OUTPUT, 0.25)
+    r = np.random.default_rng(23)
+    Wg, sg = gen.quantize_rows_fp8(gen.draw_weight(r, N, K))
+    Wu, su = gen.quantize_rows_fp8(gen.draw_weight(r, N, K))
+    Xf = gen.draw_x(r, M, K, "normal") * np.exp(r.uniform(-6, 6, (M, 1))).astype(np.float32)
+    Xf[7] = 0
+    X, sx = gen.quantize_rows_fp8(Xf)
+    mg = gen.random_mask_24(r, N, K, gen.OUTPUT, db, True)
+    mu = gen.random_mask_24(r, N, K, gen.OUTPUT, db, True)
+    pg, pu = packed(S, Wg, mg, db), packed(S, Wu, mu, db)
+    args = (tdev(X), pg, pu, tdev(sg), tdev(su), tdev(sx))
+    q1, s1 = S.quantize_fp8(S.gemm_glu(*args))
+    q2, s2 = S.gemm_glu_fp8(*args)
+    torch.cuda.synchronize()
+    assert torch.equal(q1, q2)
+    assert torch.equal(s1.view(torch.int32), s2.view(torch.int32))
+    assert s2[7].item() == 1.0
 
 
 def test_gemm_glu_validates_arguments(S):
