@@ -924,20 +924,28 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
     }
 }
 
-// Y rows of the K-sliced regions: sum of the slices' fp32 partials in slice order, then
-// the epilogue of store4 ((sum * w_scale[n]) * x_scale[m], bf16 or fp32).  One thread per
-// output element.
+// Y of a K-sliced GEMM (the planner slices every region of a weight alike, KS slices):
+// the sum of the slices' fp32 partials in slice order, then the epilogue of store4
+// ((sum * w_scale[n]) * x_scale[m], bf16 or fp32).  One thread per output element; its
+// KS loads and the scales are issued before the first add, so their latencies overlap.
+template <int KS>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a) {
   const int64_t total = (int64_t)a.M * a.N;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const bool narrow = total < ((int64_t)1 << 31);
   for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += stride) {
-    const int m = (int)(e / a.N), n = (int)(e - (int64_t)m * a.N);
-    const Region& R = (a.nreg > 1 && n >= a.reg[1].row0 && n < a.reg[1].row0 + a.reg[1].rows) ? a.reg[1] : a.reg[0];
-    if (R.ksplit == 1 || n < R.row0 || n >= R.row0 + R.rows) continue;
-    float v = a.part[(int64_t)m * a.N + n];
-    for (int sl = 1; sl < R.ksplit; ++sl) v += a.part[((int64_t)sl * a.M + m) * a.N + n];
-    if (a.sw) v = v * a.sw[n];
-    v = v * (a.sx ? a.sx[m] : 1.0f);
+    const int m = narrow ? (int)e / a.N : (int)(e / a.N);
+    const int n = (int)(e - (int64_t)m * a.N);
+    const float* pe = a.part + e;  // slice sl's partial of this element: pe[sl * M * N]
+    float p[KS];
+#pragma unroll
+    for (int sl = 0; sl < KS; ++sl) p[sl] = pe[sl * total];
+    const float sw = a.sw ? a.sw[n] : 1.0f, sx = a.sx ? a.sx[m] : 1.0f;
+    float v = p[0];
+#pragma unroll
+    for (int sl = 1; sl < KS; ++sl) v += p[sl];
+    if (a.sw) v = v * sw;
+    v = v * sx;
     if (a.out_f32)
       reinterpret_cast<float*>(a.Y)[(int64_t)m * a.ldy + n] = v;
     else
@@ -1369,7 +1377,19 @@ hipError_t launch_splitk_reduce(const GemmArgs& a, hipStream_t s) {
   const int64_t total = (int64_t)a.M * a.N;
   int64_t g = (total + 255) / 256;
   if (g > 4096) g = 4096;
-  hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)(g < 1 ? 1 : g)), dim3(256), 0, s, a);
+  const dim3 grid((unsigned)(g < 1 ? 1 : g)), block(256);
+  for (int i = 1; i < a.nreg; ++i)
+    if (a.reg[i].ksplit != a.reg[0].ksplit) return hipErrorInvalidValue;  // one slice count per weight
+  switch (a.reg[0].ksplit) {
+    case 2: hipLaunchKernelGGL(splitk_reduce_kernel<2>, grid, block, 0, s, a); break;
+    case 3: hipLaunchKernelGGL(splitk_reduce_kernel<3>, grid, block, 0, s, a); break;
+    case 4: hipLaunchKernelGGL(splitk_reduce_kernel<4>, grid, block, 0, s, a); break;
+    case 5: hipLaunchKernelGGL(splitk_reduce_kernel<5>, grid, block, 0, s, a); break;
+    case 6: hipLaunchKernelGGL(splitk_reduce_kernel<6>, grid, block, 0, s, a); break;
+    case 7: hipLaunchKernelGGL(splitk_reduce_kernel<7>, grid, block, 0, s, a); break;
+    case 8: hipLaunchKernelGGL(splitk_reduce_kernel<8>, grid, block, 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 
