@@ -230,7 +230,9 @@ int spense_gemm(const void* X, int64_t M, int64_t ldx, const spense_packed_t* pa
  * X W_i^T for i < count (sec. 3.2, output-split, as spense_gemm for each weight; e.g.
  * the q, k and v projections of a layer, or gate and up).  Each weight keeps its own
  * 2:4 and dense regions and its own output; together they fill the GPU where one small
- * weight alone would need K slices and a second pass.  Weights: fp8 e4m3fn, output-split,
+ * weight alone would need K slices and a second pass.  It runs the row-split kernel,
+ * which pays for up to 64 tokens; above that one spense_gemm per weight (the large-M
+ * kernel from 256 tokens) is faster.  Weights: fp8 e4m3fn, output-split,
  * tiled layout (spense_tile), equal K; count in [1, 4].  w_scales (array of count
  * pointers, or NULL for none) and x_scale as in spense_gemm; Y[i] (bf16 or fp32 per
  * out_flags) with leading dimension ldy[i] >= N_i.  Results equal spense_gemm's up to the
@@ -250,7 +252,9 @@ int spense_gemm_grouped(const void* X, int64_t M, int64_t ldx, int32_t count, co
  *   arithmetic as spense_glu_quantize_fp8 (so quantising H with spense_quantize_fp8
  *   gives the codes and scales that spense_glu_quantize_fp8 gives for the G and U of
  *   spense_gemm_grouped, bit for bit).  A workgroup computes gate and up tiles of the
- *   same rows and pairs them on chip, so G and U are never written.
+ *   same rows and pairs them on chip, so G and U are never written.  Like
+ *   spense_gemm_grouped it runs the row-split kernel, which pays for up to 64 tokens;
+ *   for more, two spense_gemm calls (fp32 out) and spense_glu_quantize_fp8 are faster.
  * gate, up: fp8 e4m3fn, output-split, tiled layout, with equal N, K and dense_begin.
  * X: M x K fp8 codes (ldx bytes, 16-byte aligned, ldx a multiple of 16).  w_scale_gate /
  * w_scale_up: N fp32 each or NULL; x_scale: M fp32 or NULL.  H: M x N fp32, leading

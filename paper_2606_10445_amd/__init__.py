@@ -535,11 +535,16 @@ def mlp(X: torch.Tensor, x_scale: torch.Tensor, gate: PackedWeight, up: PackedWe
         gate_scale=None, up_scale=None, down_scale=None, out=None, workspace: Workspace | None = None):
     """The GLU MLP of the paper's sec. 3.3.1 Eq. (4) on Spense weights: H = glu(gate(X),
     up(X)) (output-split) and (Hq, sh) its per-token fp8 quantisation (for tiled fp8
-    weights of one geometry the GLU in the gate / up epilogue, then the quantisation from
-    the epilogue's row maxima; otherwise G and U in fp32 and the GLU fused with the
-    quantisation), Y = down(Hq) (input-split, bf16 out).  X: fp8 codes with x_scale."""
+    weights of one geometry and up to 64 tokens the GLU in the gate / up epilogue, then
+    the quantisation from the epilogue's row maxima; otherwise G and U in fp32 and the GLU
+    fused with the quantisation), Y = down(Hq) (input-split, bf16 out).  X: fp8 codes
+    with x_scale."""
+    # the paired and grouped launches run the row-split kernel, which pays for one block
+    # of up to 64 tokens; above that two plans of their own (the large-M kernel from 256
+    # tokens) are faster
+    one_block = X.shape[0] <= 64
     paired = (gate.kind == up.kind == SPENSE_LAYOUT_TILED and gate.dtype == up.dtype == SPENSE_FP8_E4M3FN
-              and gate.split == up.split == SPENSE_SPLIT_OUTPUT)
+              and gate.split == up.split == SPENSE_SPLIT_OUTPUT and one_block)
     if paired and gate.N == up.N and gate.K == up.K and gate.dense_begin == up.dense_begin:
         Hq, sh = gemm_glu_fp8(X, gate, up, gate_scale, up_scale, x_scale, workspace=workspace)
     else:
