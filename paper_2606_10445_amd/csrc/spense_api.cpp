@@ -1093,6 +1093,7 @@ int spense_gemm_glu_fp8(const void* X, int64_t M, int64_t ldx, const spense_pack
   if (!ws || ws_bytes < need)
     return fail(SPENSE_ERR_WS, "workspace of %zu bytes needed, %zu given", need, ws ? ws_bytes : (size_t)0);
   if (reinterpret_cast<uintptr_t>(ws) % 256) return fail(SPENSE_ERR_ALIGN, "workspace must be 256-byte aligned");
+  if (M * ceil_div(N, 2048) > INT32_MAX) return fail(SPENSE_ERR_ARG, "M x N too large for the quantisation grid");
   rc = check_device();
   if (rc) return rc;
   float* H = static_cast<float*>(ws);
