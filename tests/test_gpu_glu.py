@@ -83,6 +83,8 @@ EXACT_CASES = [  # M, N, K, dense_begin (a fraction: the trailing share of rows 
     (100, 452, 640, 0.25),
     (7, 200, 512, 98),  # not a multiple of 4: element stores at the region seam
     (20, 136, 640, 72),
+    (3, 48, 96, 0.25),  # K below one 512-column chunk
+    (40, 80, 160, 0.5),
 ]
 
 
