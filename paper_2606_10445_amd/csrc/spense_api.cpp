@@ -222,12 +222,16 @@ void choose_rows_per_group(spense::Region* regs, int nreg, int rt, int waves, in
 }
 
 // Row-split kernel: number of K slices.  Slicing K multiplies the waves of a weight with
-// few 16-row tiles, at the price of an fp32 partial-sum pass.  Measured on the q / k / o /
-// down shapes (tiled fp8): it pays for one block of tokens (several blocks already
-// multiply the workgroups), on weights with fewer than 1024 tiles, and when each slice
-// keeps enough chunks: down (320 tiles, 50 chunks) gains up to 1.5x with 4 slices at
-// 17-64 tokens and 4-12% at 1-16, k/v (64 tiles, 10 chunks) ~1.2x with 3 at 17-64 tokens
-// and nothing at 1-16, q and o (10 and 16 chunks) lose.
+// few 16-row tiles, at the price of an fp32 partial-sum pass (the reduction launch).
+// Measured on the q / k / o / down shapes (tiled fp8, graph replay, with the reduction
+// that issues every slice's load before adding): it pays for one block of tokens
+// (several blocks already multiply the workgroups) on weights with fewer than 1024
+// tiles, when each slice keeps enough chunks.  k / v (64 tiles, 10 chunks): 4 slices,
+// 5-8% faster at every M.  o (320 tiles, 16 chunks): 3 slices from 17 tokens, 3-9%
+// (Seed-OSS o, 20 chunks: 4 slices, 7-13%); none at 1-16.  down (320 tiles, 50 chunks):
+// 4 slices, up to 1.5x at 17-64 tokens and 4-12% at 1-16 (all dense: 2 or 4 slices
+// within run-to-run noise from 17 tokens; 4 kept).
+// q (512 tiles, 10 chunks): 2 slices lose 12-15% at 32-64 tokens, so none.
 int choose_ksplit(const spense::Region* regs, int nreg, int ct, int mblocks, int64_t chunks, int64_t M) {
   int64_t tiles = 0;
   bool has_24 = false;
@@ -236,16 +240,24 @@ int choose_ksplit(const spense::Region* regs, int nreg, int ct, int mblocks, int
     has_24 = has_24 || (regs[i].kbound > 0 && regs[i].rows > 0);
   }
   int S = 1;
-  // One activation tile (M <= 16): only if every slice keeps at least 12 chunks; a weight
-  // with a 2:4 part takes up to 4 slices (its chunks carry fewer bytes, so the waves of
-  // one tile keep too few in flight), an all-dense one 2 and only above 8 tokens.
-  // Measured on down (5120 x 25600, us, slices 1 / 2 / 4): 25% dense M = 1: 23.6 / 21.4 /
-  // 21.0, M = 16: 23.3 / 21.7 / 21.6; all dense M = 1: 25.1 / 25.5 / 26.3, M = 4: 23.9 /
-  // 24.6 / 26.3, M = 16: 27.7 / 25.6 / 27.3; k and q (10 chunks) lose.
+  // Weights of 128 tiles or more with one activation tile (M <= 16): only if every slice
+  // keeps at least 12 chunks; a weight with a 2:4 part takes up to 4 slices (its chunks
+  // carry fewer bytes, so the waves of one tile keep too few in flight), an all-dense one
+  // 2 and only above 8 tokens.  Measured on down (5120 x 25600, us, slices 1 / 2 / 4):
+  // 25% dense M = 1: 23.6 / 21.4 / 21.0, M = 16: 23.3 / 21.7 / 21.6; all dense M = 1:
+  // 25.1 / 25.5 / 26.3, M = 4: 23.9 / 24.6 / 26.3, M = 16: 27.7 / 25.6 / 27.3.  More
+  // activation tiles: slices of at least 5 chunks, below 512 tiles.
   if (mblocks == 1 && tiles < 1024) {
-    const int64_t min_chunks = ct == 1 || tiles >= 256 ? 12 : 3;
-    S = (int)std::max<int64_t>(1, std::min<int64_t>({4, ceil_div(1024, std::max<int64_t>(tiles, 1)), chunks / min_chunks}));
-    if (ct == 1 && !has_24) S = M > 8 ? std::min(S, 2) : 1;
+    const int64_t by_tiles = ceil_div(1024, std::max<int64_t>(tiles, 1));
+    if (tiles < 128) {
+      // few rows (k / v): slices of two or more chunks pay at every M
+      S = (int)std::max<int64_t>(1, std::min<int64_t>({4, by_tiles, chunks / 2}));
+    } else if (ct == 1) {
+      S = (int)std::max<int64_t>(1, std::min<int64_t>({4, by_tiles, chunks / 12}));
+      if (!has_24) S = M > 8 ? std::min(S, 2) : 1;
+    } else if (tiles < 512) {
+      S = (int)std::max<int64_t>(1, std::min<int64_t>({4, by_tiles, chunks / 5}));
+    }
   }
   const int e = env_int("SPENSE_KSPLIT", 0);
   if (e >= 1 && e <= 8) S = (int)std::max<int64_t>(1, std::min<int64_t>(e, chunks));
