@@ -198,7 +198,7 @@ int spense_tile(const spense_packed_t* src, const spense_packed_t* dst, hipStrea
  * Device workspace (bytes) that spense_gemm needs for this M and weight; 0 means none.
  * It is non-zero when the plan cuts K into slices run by separate workgroups (weights
  * with fewer than 1024 16-row tiles at up to 64 tokens, when every slice keeps enough of
- * K: e.g. k / v at 17-64 tokens, down from one token on): S x M x N fp32 partial sums,
+ * K: e.g. k / v and down from one token on, o from 17 tokens): S x M x N fp32 partial sums,
  * added in slice order by a second kernel of the same call.  The workspace is only
  * scratch between the two kernels of one call; calls that overlap on one workspace race.
  */
