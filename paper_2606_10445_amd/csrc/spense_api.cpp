@@ -182,41 +182,68 @@ constexpr int kCUs = 256;  // compute units of an MI355X
 constexpr int64_t kBigMinM = 256;      // tokens from which the large-M kernel is used (fp8)
 constexpr int64_t kBigMinTiles = 128;  // and workgroup tiles (128 rows x 256 tokens) it needs
 
-// Row-split kernel: how many of a workgroup's waves own rows in each region.  A region
-// whose rows carry more bytes (dense rows) gets fewer rows per workgroup, so that the
-// workgroups are alike in bytes.  Model: with W workgroups on kCUs CUs the time is
-// ceil(W / kCUs) rounds of the largest workgroup, whose cost is its weight bytes plus a
-// quarter of the activation bytes it stages from L2; the cheapest assignment wins, ties
-// going to fewer workgroups.
+// Waves (16-row tiles) per workgroup for each kind of region, w[kind] in [1, wmax]:
+// region i (rows[i] rows, kind[i] in {0, 1}, tile[i] the weight bytes one wave streams)
+// gets ceil(rows / (16 rt w)) workgroups per token block and K slice (mult).  Model: with
+// W workgroups on kCUs CUs the time is ceil(W / kCUs) rounds of the largest workgroup,
+// whose cost is its waves' weight bytes plus the activation staging (x_cost); one active
+// wave costs as two (alone it keeps too few loads in flight for the CU's share of HBM).
+// Ties go to more workgroups (more CUs streaming), then to more waves in the smallest
+// workgroup.  Measured on MI355X (graph replay, tiled fp8, M = 1 / 32 / 64, us): q 8192 x
+// 5120 with (dense 1, 2:4 3) waves 8.85 / 11.71 / 14.40, with (2, 2) 7.95 / 10.79 / 13.40;
+// gate / up with (5, 8) 18.04 / 20.40 / 23.72, with (5, 7) 17.82 / 19.89 / 23.13.
+void pick_waves(int n, const int64_t* rows, const int* kind, const double* tile, int rt, int wmax, int64_t mult,
+                double x_cost, int w_out[2]) {
+  bool has1 = false;
+  for (int i = 0; i < n; ++i) has1 = has1 || kind[i] == 1;
+  double best = 0;
+  int64_t best_wg = 0;
+  int best_min = 0;
+  w_out[0] = w_out[1] = wmax;
+  for (int w0 = 1; w0 <= wmax; ++w0)
+    for (int w1 = 1; w1 <= (has1 ? wmax : 1); ++w1) {
+      const int wk[2] = {w0, w1};
+      int64_t wg = 0;
+      double big = 0;
+      int wmin = wmax;
+      for (int i = 0; i < n; ++i) {
+        const int w = wk[kind[i]];
+        wg += ceil_div(rows[i], 16 * rt * w) * mult;
+        big = std::max(big, std::max(w, 2) * tile[i]);
+        wmin = std::min(wmin, w);
+      }
+      const double t = (double)ceil_div(wg, kCUs) * (big + x_cost);
+      const bool tie = best_wg != 0 && t <= best * (1 + 1e-9) && t >= best * (1 - 1e-9);
+      if (best_wg == 0 || t < best * (1 - 1e-9) || (tie && (wg > best_wg || (wg == best_wg && wmin > best_min)))) {
+        best = t;
+        best_wg = wg;
+        best_min = wmin;
+        w_out[0] = w0;
+        w_out[1] = w1;
+      }
+    }
+}
+
+// Row-split kernel: 16-row tiles per workgroup, per region (pick_waves; the dense region
+// of an output-split weight, whose rows carry more bytes, gets fewer, so that the
+// workgroups are alike in bytes).
 void choose_rows_per_group(spense::Region* regs, int nreg, int rt, int waves, int ct, int mblocks, int64_t K, int es,
                            double sparse_cost, int ksplit) {
   double tile_b[2];
-  for (int i = 0; i < nreg; ++i)
-    tile_b[i] = 16.0 * rt * (sparse_cost * regs[i].kbound + (double)es * (K - regs[i].kbound)) / ksplit;
-  const double x_cost = 0.25 * 16.0 * ct * K * es / ksplit;
-  double best = 0;
-  int64_t best_wg = 0;
-  int bw[2] = {waves, waves};
-  for (int w0 = 1; w0 <= waves; ++w0)
-    for (int w1 = 1; w1 <= (nreg > 1 ? waves : 1); ++w1) {
-      const int wu[2] = {w0, w1};
-      int64_t wg = 0;
-      double big = 0;
-      for (int i = 0; i < nreg; ++i) {
-        wg += ceil_div(regs[i].rows, 16 * rt * wu[i]) * mblocks * ksplit;
-        big = std::max(big, wu[i] * tile_b[i]);
-      }
-      const double t = (double)ceil_div(wg, kCUs) * (big + x_cost);
-      if (best_wg == 0 || t < best * (1 - 1e-9) || (t <= best * (1 + 1e-9) && wg < best_wg)) {
-        best = t;
-        best_wg = wg;
-        bw[0] = w0;
-        bw[1] = w1;
-      }
-    }
-  const int ew = env_int("SPENSE_WUSED", 0);
+  int64_t rows[2];
+  const int kind[2] = {0, 1};  // one kind per region
   for (int i = 0; i < nreg; ++i) {
-    regs[i].wused = ew > 0 ? std::min(ew, waves) : bw[i];
+    tile_b[i] = 16.0 * rt * (sparse_cost * regs[i].kbound + (double)es * (K - regs[i].kbound)) / ksplit;
+    rows[i] = regs[i].rows;
+  }
+  const double x_cost = 0.25 * 16.0 * ct * K * es / ksplit;
+  int bw[2];
+  pick_waves(nreg, rows, kind, tile_b, rt, waves, (int64_t)mblocks * ksplit, x_cost, bw);
+  const int ew = env_int("SPENSE_WUSED", 0);  // testing knobs: waves used, all regions / per kind
+  const int ewd = env_int("SPENSE_WUSED_DENSE", 0), ews = env_int("SPENSE_WUSED_24", 0);
+  for (int i = 0; i < nreg; ++i) {
+    const int ek = regs[i].kbound == 0 ? ewd : ews;
+    regs[i].wused = ew > 0 ? std::min(ew, waves) : (ek > 0 ? std::min(ek, waves) : bw[i]);
     regs[i].nrb = (int32_t)(ceil_div(regs[i].rows, 16 * rt * regs[i].wused) * ksplit);
   }
 }
@@ -585,29 +612,19 @@ int launch_glu_pair(const void* X, int64_t M, int64_t ldx, const spense_packed_t
     regs[nreg++] = r;
   }
   const double tile_d = 2 * 16.0 * K, tile_s = 2 * 16.0 * sparse_cost * K, x_cost = 0.25 * 16.0 * ls.ct * K;
-  double best = 0;
-  int64_t best_wg = 0;
-  int bw0 = 4, bw1 = 4;
-  for (int w0 = 1; w0 <= 4; ++w0)
-    for (int w1 = 1; w1 <= 4; ++w1) {
-      int64_t wg = 0;
-      double big = 0;
-      for (int i = 0; i < nreg; ++i) {
-        const int w = regs[i].kbound == 0 ? w0 : w1;
-        wg += ceil_div(regs[i].rows, 16 * w) * ls.mblocks;
-        big = std::max(big, w * (regs[i].kbound == 0 ? tile_d : tile_s));
-      }
-      const double t = (double)ceil_div(wg, kCUs) * (big + x_cost);
-      if (best_wg == 0 || t < best * (1 - 1e-9) || (t <= best * (1 + 1e-9) && wg < best_wg)) {
-        best = t;
-        best_wg = wg;
-        bw0 = w0;
-        bw1 = w1;
-      }
-    }
+  int64_t rows[2];
+  int kind[2];
+  double tile[2];
+  for (int i = 0; i < nreg; ++i) {
+    rows[i] = regs[i].rows;
+    kind[i] = regs[i].kbound == 0 ? 0 : 1;
+    tile[i] = regs[i].kbound == 0 ? tile_d : tile_s;
+  }
+  int bw[2];
+  pick_waves(nreg, rows, kind, tile, 1, 4, ls.mblocks, x_cost, bw);
   int32_t groups = 0;
   for (int i = 0; i < nreg; ++i) {
-    regs[i].wused = regs[i].kbound == 0 ? bw0 : bw1;
+    regs[i].wused = bw[kind[i]];
     regs[i].nrb = (int32_t)ceil_div(regs[i].rows, 16 * regs[i].wused);
     regs[i].wg0 = groups;
     groups += regs[i].nrb;
@@ -993,31 +1010,21 @@ int spense_gemm_grouped(const void* X, int64_t M, int64_t ldx, int32_t count, co
       regs[nreg++] = r;
     }
   // rows per workgroup: w0 waves for dense regions, w1 for 2:4 regions (cost model of
-  // choose_rows_per_group)
+  // pick_waves)
   const double tile_d = 16.0 * K, tile_s = 16.0 * sparse_cost * K, x_cost = 0.25 * 16.0 * ls.ct * K;
-  double best = 0;
-  int64_t best_wg = 0;
-  int bw0 = 8, bw1 = 8;
-  for (int w0 = 1; w0 <= 8; ++w0)
-    for (int w1 = 1; w1 <= 8; ++w1) {
-      int64_t wg = 0;
-      double big = 0;
-      for (int i = 0; i < nreg; ++i) {
-        const int w = regs[i].kbound == 0 ? w0 : w1;
-        wg += ceil_div(regs[i].rows, 16 * w) * ls.mblocks;
-        big = std::max(big, w * (regs[i].kbound == 0 ? tile_d : tile_s));
-      }
-      const double t = (double)ceil_div(wg, kCUs) * (big + x_cost);
-      if (best_wg == 0 || t < best * (1 - 1e-9) || (t <= best * (1 + 1e-9) && wg < best_wg)) {
-        best = t;
-        best_wg = wg;
-        bw0 = w0;
-        bw1 = w1;
-      }
-    }
+  int64_t rows[spense::kMaxRegions];
+  int kind[spense::kMaxRegions];
+  double tile[spense::kMaxRegions];
+  for (int i = 0; i < nreg; ++i) {
+    rows[i] = regs[i].rows;
+    kind[i] = regs[i].kbound == 0 ? 0 : 1;
+    tile[i] = regs[i].kbound == 0 ? tile_d : tile_s;
+  }
+  int bw[2];
+  pick_waves(nreg, rows, kind, tile, 1, 8, ls.mblocks, x_cost, bw);
   int32_t groups = 0;
   for (int i = 0; i < nreg; ++i) {
-    regs[i].wused = regs[i].kbound == 0 ? bw0 : bw1;
+    regs[i].wused = bw[kind[i]];
     regs[i].nrb = (int32_t)ceil_div(regs[i].rows, 16 * regs[i].wused);
     regs[i].wg0 = groups;
     groups += regs[i].nrb;
