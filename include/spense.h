@@ -232,7 +232,7 @@ int spense_gemm(const void* X, int64_t M, int64_t ldx, const spense_packed_t* pa
  * 2:4 and dense regions and its own output; together they fill the GPU where one small
  * weight alone would need K slices and a second pass.  It runs the row-split kernel,
  * which pays for up to 64 tokens; above that one spense_gemm per weight (the large-M
- * kernel from 256 tokens) is faster.  Weights: fp8 e4m3fn, output-split,
+ * kernel on large weights) is faster.  Weights: fp8 e4m3fn, output-split,
  * tiled layout (spense_tile), equal K; count in [1, 4].  w_scales (array of count
  * pointers, or NULL for none) and x_scale as in spense_gemm; Y[i] (bf16 or fp32 per
  * out_flags) with leading dimension ldy[i] >= N_i.  Results equal spense_gemm's up to the

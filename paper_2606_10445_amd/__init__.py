@@ -540,8 +540,8 @@ def mlp(X: torch.Tensor, x_scale: torch.Tensor, gate: PackedWeight, up: PackedWe
     fused with the quantisation), Y = down(Hq) (input-split, bf16 out).  X: fp8 codes
     with x_scale."""
     # the paired and grouped launches run the row-split kernel, which pays for one block
-    # of up to 64 tokens; above that two plans of their own (the large-M kernel from 256
-    # tokens) are faster
+    # of up to 64 tokens; above that two plans of their own (the large-M kernel on large
+    # weights) are faster
     one_block = X.shape[0] <= 64
     paired = (gate.kind == up.kind == SPENSE_LAYOUT_TILED and gate.dtype == up.dtype == SPENSE_FP8_E4M3FN
               and gate.split == up.split == SPENSE_SPLIT_OUTPUT and one_block)

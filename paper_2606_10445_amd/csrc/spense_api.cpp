@@ -179,7 +179,7 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 const int kShapes[][2] = {{2, 4}, {1, 4}, {2, 8}, {1, 8}, {1, 16}, {4, 4}};
 
 constexpr int kCUs = 256;  // compute units of an MI355X
-constexpr int64_t kBigMinM = 256;      // tokens from which the large-M kernel is used (fp8)
+constexpr int64_t kBigMinM = 65;       // tokens from which the large-M kernel is used (fp8)
 constexpr int64_t kBigMinTiles = 128;  // and workgroup tiles (128 rows x 256 tokens) it needs
 
 // Waves (16-row tiles) per workgroup for each kind of region, w[kind] in [1, wmax]:
@@ -369,10 +369,11 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
   pl->ls.rows = rows_mode;
   pl->ls.u8 = (ct == 1 && rt == 1 && (waves == 4 || waves == 8) && env_int("SPENSE_U8", 0)) ? 1 : 0;
   // Many tokens (fp8): 128-row x 256-token workgroup tiles.  Measured on MI355X (q / k /
-  // o / gate / down shapes, M = 256 .. 2048, XCD-aware order): it wins from M = 256 once
-  // there are at least 128 such tiles (q at M = 512: 45 vs 54 us; o and down at M = 1024:
-  // 60 vs 97 and 156 vs 265 us); with fewer (o, down at M = 512 and 768), the row-split
-  // kernel's finer grid keeps more CUs busy.
+  // o / gate / down shapes, M = 65 .. 2048, XCD-aware order): it wins above one row-split
+  // token block (64 tokens) once there are at least 128 such tiles (gate / up at M = 96 /
+  // 128 / 192: 42.5 / 43.2 / 46.0 vs 45.3 / 47.9 / 71.4 us; q at M = 512: 45 vs 54 us; o
+  // and down at M = 1024: 60 vs 97 and 156 vs 265 us); with fewer (q below 512 tokens, o
+  // and down below 1024), the row-split kernel's finer grid keeps more CUs busy.
   int big = (dtype == SPENSE_FP8_E4M3FN && M >= kBigMinM && ceil_div(N, 128) * ceil_div(M, 256) >= kBigMinTiles) ? 1 : 0;
   const int ebig = env_int("SPENSE_BIG", -1);  // testing knob: force the large-M kernel on or off
   if (ebig >= 0) big = (ebig && dtype == SPENSE_FP8_E4M3FN) ? 1 : 0;
