@@ -487,7 +487,10 @@ def test_full_layer_linears(S, layer):
 @pytest.mark.parametrize("name,N,K,axis,M", [("gate_up", 25600, 5120, gen.OUTPUT, 64),
                                              ("down", 5120, 25600, gen.INPUT, 64),
                                              ("seed_gate", 27648, 5120, gen.OUTPUT, 2048),
-                                             ("k", 1024, 5120, gen.OUTPUT, 64)])
+                                             ("k", 1024, 5120, gen.OUTPUT, 64),
+                                             ("k", 1024, 5120, gen.OUTPUT, 1),  # 4 K slices at one token
+                                             ("gate_up", 25600, 5120, gen.OUTPUT, 100),  # large-M kernel, one block
+                                             ("o", 5120, 8192, gen.INPUT, 40)])  # 3 K slices
 def test_full_size_exact_integers_whole_output(S, name, N, K, axis, M):
     ax = 0 if axis == gen.OUTPUT else 1
     db = gen.split_point(N, K, axis, 0.25)
