@@ -534,6 +534,17 @@ int gemm_common(const void* X, int64_t M, int64_t ldx, int32_t dtype, int32_t sp
   a.d_bytes = (uint32_t)db;
   // the row-split kernel reads the weight through its descriptor
   a.nmat = 1;
+  // Row-split kernel with several token blocks: the blocks of a row group on one XCD
+  // (workgroups are dealt to the 8 XCDs round-robin), so that they share its L2 for the
+  // weight rows.  Measured on MI355X (tiled, M = 128 / 256 / 512, us): down 53.8 / 65.6 /
+  // 125.5 -> 50.5 / 65.0 / 123.2; q 18.3 / 34.7 / 46.0 -> 18.2 / 33.3 / 45.8; Seed-OSS q
+  // 19.3 / 38.0 / 47.6 -> 19.2 / 35.5 / 47.0; o and k within 1%.  Needs the row groups
+  // to split evenly over the XCDs; SPENSE_ROWS_ORDER (testing knob) forces 0 (grid of
+  // row groups x token blocks), 1 (token blocks of a row group adjacent) or 2.
+  a.mblk = pl.ls.mblocks;
+  a.rorder = pl.ls.rows && pl.ls.mblocks > 1 ? env_int("SPENSE_ROWS_ORDER", 2) : 0;
+  if (a.rorder == 2 && a.groups % 8) a.rorder = 0;
+  if (a.rorder < 0 || a.rorder > 2) a.rorder = 0;
   a.mat[0] = spense::MatDesc{a.values, a.meta, a.dense, a.v_bytes, a.m_bytes, a.d_bytes, a.Y, a.ldy, a.sw,
                              a.vec_store};
   if (a.groups == 0) return ok();

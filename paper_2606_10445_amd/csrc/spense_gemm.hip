@@ -708,7 +708,15 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
   constexpr int NL = ChunkLoads<WM>::N;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int li = lane & 15, lq = lane >> 4;
-  const int g = blockIdx.x, mb = blockIdx.y;
+  int g = blockIdx.x, mb = blockIdx.y;
+  if (a.rorder == 2) {  // XCD x (= id % 8) runs the token blocks of row groups x, x + 8, ...
+    const int x = (int)blockIdx.x & 7, l = (int)blockIdx.x >> 3;
+    g = (l / a.mblk) * 8 + x;
+    mb = l % a.mblk;
+  } else if (a.rorder == 1) {
+    g = (int)blockIdx.x / a.mblk;
+    mb = (int)blockIdx.x % a.mblk;
+  }
   // GR (grouped launch): up to kMaxRegions regions in workgroup order, each of one weight
   // (its buffers, output and scales in a.mat); otherwise one weight (GLU: two weights,
   // gate and up, of equal geometry), up to two regions, buffers in a or a.mat (GLU).
@@ -969,7 +977,7 @@ hipError_t launch_rows_wm(const dim3& grid, const dim3& block, const GemmArgs& a
 
 template <int DT, int CT, int RT, int WR>
 hipError_t launch_rows(const LaunchShape& ls, const GemmArgs& a, hipStream_t s) {
-  dim3 grid(a.groups, ls.mblocks), block(64 * WR);
+  dim3 grid = a.rorder ? dim3(a.groups * ls.mblocks) : dim3(a.groups, ls.mblocks), block(64 * WR);
   if constexpr (DT == kFP8) {
     if (a.tiled && (a.nmat > 1 || ls.glu)) {  // grouped or paired launch: tiled fp8, 8 waves
       if constexpr (RT == 1 && WR == 8) {

@@ -76,6 +76,10 @@ struct GemmArgs {
   int32_t tblocks;  // large-M kernel: 256-token blocks (workgroups of a row block are adjacent)
   int32_t xgt, xrc;  // large-M kernel, XCD-aware order (0 = off): token blocks per XCD, row classes
   int32_t nmat;
+  // row-split kernel, several token blocks: 0 = grid (row groups, token blocks); 1 = one
+  // dimension, the token blocks of a row group adjacent; 2 = one dimension, the token
+  // blocks of a row group on one XCD (row groups a multiple of 8)
+  int32_t rorder, mblk;
   float* hmax;  // paired gate / up launch: per-workgroup maxima of |h| per token, hmax[m * groups + g] (or NULL)
   MatDesc mat[kMaxMats];
   Region reg[kMaxRegions];

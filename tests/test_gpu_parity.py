@@ -528,3 +528,20 @@ def test_every_workgroup_shape_is_exact(S, rows, rt, waves, wused, ks, dtype, ax
     ref = oracle.spense_gemm(X, v, m, d, N, K, dtype, axis, db, sw, sx)
     assert np.array_equal(run_gemm(S, pw, X, sw, sx, True), ref["y_f32"])
     assert np.array_equal(run_gemm(S, pw, X, sw, sx, False).view(np.uint16), ref["y_bf16"])
+
+
+@pytest.mark.parametrize("order", [0, 1, 2])
+@pytest.mark.parametrize("axis,M,N,K,db", [(0, 200, 1024, 512, 768), (1, 150, 2048, 1024, 768), (0, 97, 640, 384, 480)])
+def test_token_block_orders_exact(S, order, axis, M, N, K, db, monkeypatch):
+    """The row-split kernel's orders of (row group, token block) workgroups: a grid of
+    both, one dimension with a row group's token blocks adjacent, and one dimension with
+    them on one XCD (the default where the row groups split evenly over 8): every output
+    bit for bit against the oracle on exact-integer data, both layouts."""
+    W, mask, X, sw, sx = gen.make_exact_int(17, M + N + order, M, N, K, gaxis(axis), db, gen.FP8)
+    pw, (v, m, d) = compress_both(S, W, mask, FP8, axis, db)
+    ref = oracle.spense_gemm(X, v, m, d, N, K, FP8, axis, db, sw, sx)
+    monkeypatch.setenv("SPENSE_BIG", "0")
+    monkeypatch.setenv("SPENSE_ROWS_ORDER", str(order))
+    for w in (pw, S.tile(pw)):
+        assert np.array_equal(run_gemm(S, w, X, sw, sx, True), ref["y_f32"])
+        assert np.array_equal(run_gemm(S, w, X, sw, sx, False).view(np.uint16), ref["y_bf16"])
