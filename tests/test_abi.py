@@ -352,3 +352,24 @@ def test_gemm_glu_fp8_validates_arguments_on_the_host(S):
     assert f(X, 8, 256, ref(g), ref(g), None, None, None, Q, 63, SC, WS, need, None) == S.SPENSE_ERR_ARG
     assert f(X, 8, 256, ref(g), None, None, None, None, Q, 64, SC, WS, need, None) == S.SPENSE_ERR_ARG
     assert f(X, 0, 256, ref(g), ref(g), None, None, None, Q, 64, SC, WS, need, None) == S.SPENSE_OK
+
+
+def test_k_slice_rule_on_the_layer_shapes(S):
+    """Which Qwen3-like layer weights (tiled layout) the planner slices along K (a
+    workspace is needed exactly then): k / v (64 tiles) at every M up to 64, o (320 tiles, 16 chunks) from 17
+    tokens, down (50 chunks, with a 2:4 part) from one token, q (512 tiles) and gate
+    (1600 tiles) never; none beyond one block of 64 tokens."""
+    def ws(N, K, split, M):
+        db = N * 3 // 4 if split == 0 else K * 3 // 4
+        L = S.spense_layout(N, K, 1, split, db)
+        p = S.spense_packed_t(1, split, N, K, db, 4096, L.values_ld, 8192, L.meta_ld, 16384, L.dense_ld,
+                              S.SPENSE_LAYOUT_TILED)
+        return S.spense_gemm_workspace_size(M, p)
+    for M in (1, 16, 64):
+        assert ws(1024, 5120, 0, M) > 0  # k / v
+        assert ws(5120, 25600, 1, M) > 0  # down
+        assert ws(8192, 5120, 0, M) == 0  # q
+        assert ws(25600, 5120, 0, M) == 0  # gate / up
+    assert ws(5120, 8192, 1, 1) == 0 and ws(5120, 8192, 1, 16) == 0  # o: one token block of 1-16
+    assert ws(5120, 8192, 1, 17) > 0 and ws(5120, 8192, 1, 64) > 0  # o from 17 tokens
+    assert ws(1024, 5120, 0, 65) == 0 and ws(5120, 25600, 1, 200) == 0  # several token blocks
