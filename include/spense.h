@@ -20,8 +20,11 @@
  *     call says otherwise.  spense_last_error() returns a thread-local message.
  *   - Matrices are row-major with an explicit leading dimension in elements.
  *   - Device pointers are plain HIP device addresses; the caller allocates and frees
- *     every buffer.  The library allocates no device or host memory of its own and
- *     keeps no mutable global state.
+ *     every buffer.  The library allocates no device or host memory of its own.  The
+ *     only state it keeps is set once per device and never changes afterwards (the
+ *     gfx950 check, the large-M kernel's LDS attribute, both under std::call_once or
+ *     atomics) and a per-thread cache of recent execution plans; none of it changes a
+ *     result, and no environment variable is read.
  *   - Calls take a hipStream_t (0 = the null stream) and are asynchronous on it unless
  *     stated otherwise.
  */
@@ -37,7 +40,7 @@
 extern "C" {
 #endif
 
-#define SPENSE_ABI_VERSION 8
+#define SPENSE_ABI_VERSION 9
 
 typedef enum spense_status {
   SPENSE_OK = 0,
@@ -224,6 +227,51 @@ size_t spense_gemm_workspace_size(int64_t M, const spense_packed_t* packed);
 int spense_gemm(const void* X, int64_t M, int64_t ldx, const spense_packed_t* packed, const float* w_scale,
                 const float* x_scale, void* Y, int64_t ldy, uint32_t out_flags, void* ws, size_t ws_bytes,
                 hipStream_t stream);
+
+/*
+ * Parts of spense_gemm's execution plan forced by the caller, for tests that check every
+ * kernel and workgroup shape bit for bit, and for tuning sweeps.  spense_gemm itself
+ * reads no such setting: its plan depends only on the dtype, M and the weight geometry.
+ * A zero field (or -1 where stated) leaves that choice to the planner.  A forced plan
+ * changes the order of the fp32 sums, not what is summed.
+ */
+typedef struct spense_plan_override_t {
+  int32_t kernel;           /* 0 planner; 1 K split over a workgroup's waves (row-major
+                               layout only); 2 rows split, activations staged in LDS;
+                               3 large-M tiles (fp8 only) */
+  int32_t row_tiles;        /* K-split kernel: 16-row tiles per workgroup (1, 2, 4); with
+                               kernel 2: 1 or 2 (with 4 waves) */
+  int32_t waves;            /* K-split kernel: 4, 8 or 16 waves per workgroup (row_tiles
+                               1 allows all three, 2 allows 4 and 8, 4 allows 4); row-split:
+                               4 or 8; large-M: 4 or 8 */
+  int32_t act_tiles;        /* at most this many 16-token activation tiles per token block
+                               (1 or 2) */
+  int32_t ksplit;           /* row-split kernel: K slices, 1 .. 8 (capped at the chunk count) */
+  int32_t waves_used;       /* row-split kernel: waves owning rows, every region */
+  int32_t waves_used_dense; /* row-split kernel: the same for the dense region only */
+  int32_t waves_used_24;    /* row-split kernel: the same for the 2:4 region only */
+  int32_t block_order;      /* row-split kernel with several token blocks: -1 planner, 0 grid
+                               of (row group, token block), 1 a row group's blocks adjacent,
+                               2 a row group's blocks on one XCD */
+  int32_t xcd_order;        /* large-M kernel: -1 planner, 0 plain order, 1 XCD-aware where
+                               the grid allows it */
+  int32_t u8;               /* K-split kernel, one activation tile, one row tile, 4 or 8
+                               waves: 1 = eight instruction steps per batch of loads */
+} spense_plan_override_t;
+
+/*
+ * spense_gemm with parts of the plan forced (plan may be NULL: exactly spense_gemm).
+ * Arguments, results and errors as spense_gemm; SPENSE_ERR_ARG also for an override the
+ * weight or dtype cannot run (e.g. the K-split kernel on a tiled weight, the large-M
+ * kernel on bf16, a workgroup shape outside the lists above).
+ * spense_gemm_planned_workspace_size: the workspace this plan needs (0 also when the
+ * override is rejected).
+ */
+size_t spense_gemm_planned_workspace_size(int64_t M, const spense_packed_t* packed,
+                                          const spense_plan_override_t* plan);
+int spense_gemm_planned(const void* X, int64_t M, int64_t ldx, const spense_packed_t* packed, const float* w_scale,
+                        const float* x_scale, void* Y, int64_t ldy, uint32_t out_flags, void* ws, size_t ws_bytes,
+                        const spense_plan_override_t* plan, hipStream_t stream);
 
 /*
  * Several Spense weights that share the activations X and K, in one launch: Y[i] =

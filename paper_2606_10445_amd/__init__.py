@@ -44,7 +44,8 @@ EXPORTS = ["spense_abi_version", "spense_last_error", "spense_layout", "spense_t
            "spense_quantize_fp8", "spense_glu_quantize_fp8", "spense_index_scores", "spense_dense_permutation",
            "spense_gather_rows", "spense_gather_cols", "spense_obs_factor_workspace_size", "spense_obs_factor",
            "spense_obs_prune_workspace_size", "spense_obs_prune_24", "spense_gemm_grouped", "spense_gemm_glu",
-           "spense_gemm_glu_fp8_workspace_size", "spense_gemm_glu_fp8"]
+           "spense_gemm_glu_fp8_workspace_size", "spense_gemm_glu_fp8", "spense_gemm_planned_workspace_size",
+           "spense_gemm_planned"]
 
 
 class SpenseError(RuntimeError):
@@ -71,6 +72,27 @@ class spense_packed_t(ctypes.Structure):
                 ("dense_begin", ctypes.c_int64), ("values", ctypes.c_void_p), ("values_ld", ctypes.c_int64),
                 ("meta", ctypes.c_void_p), ("meta_ld", ctypes.c_int64), ("dense", ctypes.c_void_p),
                 ("dense_ld", ctypes.c_int64), ("layout", ctypes.c_int32)]
+
+
+class spense_plan_override_t(ctypes.Structure):
+    _fields_ = [("kernel", ctypes.c_int32), ("row_tiles", ctypes.c_int32), ("waves", ctypes.c_int32),
+                ("act_tiles", ctypes.c_int32), ("ksplit", ctypes.c_int32), ("waves_used", ctypes.c_int32),
+                ("waves_used_dense", ctypes.c_int32), ("waves_used_24", ctypes.c_int32),
+                ("block_order", ctypes.c_int32), ("xcd_order", ctypes.c_int32), ("u8", ctypes.c_int32)]
+
+
+KERNEL_KSPLIT, KERNEL_ROWS, KERNEL_LARGE_M = 1, 2, 3
+
+
+def plan_override(**kw) -> spense_plan_override_t:
+    """A spense_plan_override_t with the given fields forced and the rest left to the
+    planner (block_order and xcd_order default to -1)."""
+    p = spense_plan_override_t(block_order=-1, xcd_order=-1)
+    for k, v in kw.items():
+        if not hasattr(p, k):
+            raise TypeError(f"unknown plan field {k}")
+        setattr(p, k, int(v))
+    return p
 
 
 def _load():
@@ -106,6 +128,9 @@ def _load():
         "spense_gemm_glu": (ctypes.c_int, [p, i64, i64, p, p, p, p, p, p, i64, p]),
         "spense_gemm_glu_fp8_workspace_size": (ctypes.c_size_t, [i64, i64]),
         "spense_gemm_glu_fp8": (ctypes.c_int, [p, i64, i64, p, p, p, p, p, p, i64, p, p, ctypes.c_size_t, p]),
+        "spense_gemm_planned_workspace_size": (sz, [i64, P(spense_packed_t), P(spense_plan_override_t)]),
+        "spense_gemm_planned": (ctypes.c_int, [p, i64, i64, P(spense_packed_t), p, p, p, i64, u32, p, sz,
+                                               P(spense_plan_override_t), p]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -170,6 +195,16 @@ def spense_gemm(X, M, ldx, packed: spense_packed_t, w_scale, x_scale, Y, ldy, ou
                 stream) -> int:
     return _lib.spense_gemm(X, M, ldx, ctypes.byref(packed), w_scale, x_scale, Y, ldy, out_flags, ws, ws_bytes,
                             stream)
+
+
+def spense_gemm_planned_workspace_size(M: int, packed: spense_packed_t, plan) -> int:
+    return _lib.spense_gemm_planned_workspace_size(M, ctypes.byref(packed), None if plan is None else ctypes.byref(plan))
+
+
+def spense_gemm_planned(X, M, ldx, packed: spense_packed_t, w_scale, x_scale, Y, ldy, out_flags, ws, ws_bytes, plan,
+                        stream) -> int:
+    return _lib.spense_gemm_planned(X, M, ldx, ctypes.byref(packed), w_scale, x_scale, Y, ldy, out_flags, ws,
+                                    ws_bytes, None if plan is None else ctypes.byref(plan), stream)
 
 
 def spense_dense_gemm_workspace_size(M: int, N: int, K: int, dtype: int) -> int:
@@ -370,6 +405,39 @@ def decompress(pw: PackedWeight) -> torch.Tensor:
     return W
 
 
+def _check_x(X: torch.Tensor, dtype: int, K: int):
+    _row_major(X, "X")
+    if _act_code(X) != dtype:
+        raise ValueError(f"X is {X.dtype}; this weight takes {'fp8 codes (uint8)' if dtype == SPENSE_FP8_E4M3FN else 'bfloat16'}")
+    if X.shape[1] != K:
+        raise ValueError(f"X.shape[1] = {X.shape[1]} != K = {K}")
+
+
+def _act_code(t: torch.Tensor):
+    if t.dtype in (torch.uint8, torch.float8_e4m3fn):
+        return SPENSE_FP8_E4M3FN
+    if t.dtype in (torch.bfloat16, torch.int16, torch.uint16):
+        return SPENSE_BF16
+    return None
+
+
+def _out(out, M, N, out_f32, dev, name="out"):
+    """A new output, or the caller's checked: 2-D, rows contiguous, shape (M, N), fp32 or
+    bf16 as out_f32 says, on X's device."""
+    want = torch.float32 if out_f32 else torch.bfloat16
+    if out is None:
+        return torch.empty((M, N), dtype=want, device=dev)
+    if out.dim() != 2 or out.stride(1) != 1 or (M > 1 and out.stride(0) < N):
+        raise ValueError(f"{name} must be a 2-D tensor with contiguous rows")
+    if tuple(out.shape) != (M, N):
+        raise ValueError(f"{name} has shape {tuple(out.shape)}, expected {(M, N)}")
+    if out.dtype != want:
+        raise ValueError(f"{name} is {out.dtype}, expected {want}")
+    if out.device != dev:
+        raise ValueError(f"{name} is on {out.device}, X on {dev}")
+    return out
+
+
 def _check_scale(s, n, dev, name):
     if s is None:
         return
@@ -378,36 +446,43 @@ def _check_scale(s, n, dev, name):
 
 
 def gemm(X: torch.Tensor, pw: PackedWeight, w_scale=None, x_scale=None, out=None, out_f32=False,
-         workspace: Workspace | None = None) -> torch.Tensor:
-    """Y = X W^T for a packed weight (spense_gemm)."""
-    _row_major(X, "X")
+         workspace: Workspace | None = None, plan: spense_plan_override_t | None = None) -> torch.Tensor:
+    """Y = X W^T for a packed weight (spense_gemm; with ``plan``, spense_gemm_planned:
+    parts of the execution plan forced, for tests and tuning)."""
+    _check_x(X, pw.dtype, pw.K)
     M = X.shape[0]
     _check_scale(w_scale, pw.N, X.device, "w_scale")
     _check_scale(x_scale, M, X.device, "x_scale")
-    if X.shape[1] != pw.K:
-        raise ValueError("X.shape[1] != K")
-    if out is None:
-        out = torch.empty((M, pw.N), dtype=torch.float32 if out_f32 else torch.bfloat16, device=X.device)
+    out = _out(out, M, pw.N, out_f32, X.device)
     ws = workspace or workspace_for(X.device)
-    need = spense_gemm_workspace_size(M, pw.desc)
-    wp, wn = ws.get(need)
-    _check(spense_gemm(_ptr(X), M, X.stride(0), pw.desc, _ptr(w_scale), _ptr(x_scale), _ptr(out), out.stride(0),
-                       SPENSE_OUT_F32 if out_f32 else SPENSE_OUT_BF16, wp, wn, _stream(X.device)))
+    flags = SPENSE_OUT_F32 if out_f32 else SPENSE_OUT_BF16
+    if plan is None:
+        wp, wn = ws.get(spense_gemm_workspace_size(M, pw.desc))
+        _check(spense_gemm(_ptr(X), M, X.stride(0), pw.desc, _ptr(w_scale), _ptr(x_scale), _ptr(out), out.stride(0),
+                           flags, wp, wn, _stream(X.device)))
+    else:
+        wp, wn = ws.get(spense_gemm_planned_workspace_size(M, pw.desc, plan))
+        _check(spense_gemm_planned(_ptr(X), M, X.stride(0), pw.desc, _ptr(w_scale), _ptr(x_scale), _ptr(out),
+                                   out.stride(0), flags, wp, wn, plan, _stream(X.device)))
     return out
 
 
 def gemm_grouped(X: torch.Tensor, pws, w_scales=None, x_scale=None, outs=None, out_f32=False):
     """One launch for several Spense weights sharing X (spense_gemm_grouped): returns
     [X W_i^T].  pws: tiled fp8 output-split PackedWeights with equal K (up to 4)."""
-    _row_major(X, "X")
-    M = X.shape[0]
     n = len(pws)
+    if n < 1:
+        raise ValueError("at least one weight")
+    for p in pws:
+        _check_x(X, p.dtype, p.K)
+    M = X.shape[0]
     if w_scales is not None and len(w_scales) != n:
         raise ValueError("one w_scale per weight")
     if outs is None:
-        outs = [torch.empty((M, p.N), dtype=torch.float32 if out_f32 else torch.bfloat16, device=X.device) for p in pws]
-    if any(p.K != X.shape[1] for p in pws):
-        raise ValueError("X.shape[1] must equal every weight's K")
+        outs = [None] * n
+    if len(outs) != n:
+        raise ValueError("one output per weight")
+    outs = [_out(o, M, p.N, out_f32, X.device, f"outs[{i}]") for i, (o, p) in enumerate(zip(outs, pws))]
     descs = [p.desc for p in pws]
     for i, p in enumerate(pws):
         _check_scale(w_scales[i] if w_scales is not None else None, p.N, X.device, "w_scale")
@@ -428,7 +503,7 @@ def gemm_glu(X: torch.Tensor, gate: PackedWeight, up: PackedWeight, gate_scale=N
     """H = glu(X Wg^T, X Wu^T) in one launch (spense_gemm_glu), fp32 M x N: the gate and
     up GEMMs with the GLU step in their epilogue.  gate, up: tiled fp8 output-split
     PackedWeights with equal N, K and dense_begin."""
-    _row_major(X, "X")
+    _check_x(X, SPENSE_FP8_E4M3FN, gate.K)
     M = X.shape[0]
     if gate.K != X.shape[1] or up.K != X.shape[1]:
         raise ValueError("X.shape[1] must equal K")
@@ -452,7 +527,7 @@ def gemm_glu_fp8(X: torch.Tensor, gate: PackedWeight, up: PackedWeight, gate_sca
     """The producer half of the GLU MLP (spense_gemm_glu_fp8): H = glu(X Wg^T, X Wu^T) in
     the gate / up epilogue, then its per-token fp8 quantisation from the epilogue's row
     maxima.  Returns (codes uint8 M x N, scales fp32 M), the down projection's input."""
-    _row_major(X, "X")
+    _check_x(X, SPENSE_FP8_E4M3FN, gate.K)
     M = X.shape[0]
     if gate.K != X.shape[1] or up.K != X.shape[1]:
         raise ValueError("X.shape[1] must equal K")
@@ -479,15 +554,16 @@ def gemm_glu_fp8(X: torch.Tensor, gate: PackedWeight, up: PackedWeight, gate_sca
 def dense_gemm(X: torch.Tensor, W: torch.Tensor, w_scale=None, x_scale=None, out=None, out_f32=False,
                workspace: Workspace | None = None) -> torch.Tensor:
     """The dense baseline Y = X W^T (spense_dense_gemm)."""
-    _row_major(X, "X")
     _row_major(W, "W")
     dtype = _dtype_code(W)
-    M, K = X.shape
-    N = W.shape[0]
+    N, K = W.shape
+    _check_x(X, dtype, K)
+    if W.device != X.device:
+        raise ValueError("W and X must be on one device")
+    M = X.shape[0]
     _check_scale(w_scale, N, X.device, "w_scale")
     _check_scale(x_scale, M, X.device, "x_scale")
-    if out is None:
-        out = torch.empty((M, N), dtype=torch.float32 if out_f32 else torch.bfloat16, device=X.device)
+    out = _out(out, M, N, out_f32, X.device)
     ws = workspace or workspace_for(X.device)
     wp, wn = ws.get(spense_dense_gemm_workspace_size(M, N, K, dtype))
     _check(spense_dense_gemm(_ptr(X), M, X.stride(0), _ptr(W), W.stride(0), N, K, dtype, _ptr(w_scale),
@@ -549,8 +625,8 @@ def mlp(X: torch.Tensor, x_scale: torch.Tensor, gate: PackedWeight, up: PackedWe
         Hq, sh = gemm_glu_fp8(X, gate, up, gate_scale, up_scale, x_scale, workspace=workspace)
     else:
         if paired and gate.K == up.K:
-            G, U = gemm_grouped(X, [gate, up], None if gate_scale is None else [gate_scale, up_scale], x_scale,
-                                out_f32=True)
+            scales = None if gate_scale is None and up_scale is None else [gate_scale, up_scale]
+            G, U = gemm_grouped(X, [gate, up], scales, x_scale, out_f32=True)
         else:
             G = gemm(X, gate, gate_scale, x_scale, out_f32=True, workspace=workspace)
             U = gemm(X, up, up_scale, x_scale, out_f32=True, workspace=workspace)

@@ -28,6 +28,24 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
+# The compiler the kernels' explicit matrix-core wait states (xdl_fence in spense_gemm.hip)
+# were checked with: the padding it inserts across basic blocks fell short there, and the
+# repeatability test over every kernel shape guards it.  A different compiler must pass
+# that test before anything else.
+CHECKED_TOOLCHAIN = ("HIP version: 7.2.26015-fc0010cf6a",
+                     "AMD clang version 22.0.0git (https://github.com/RadeonOpenCompute/llvm-project roc-7.2.0 26014 "
+                     "7b800a19466229b8479a78de19143dc33c3ab9b5)")
+
+
+def toolchain() -> tuple[str, str]:
+    """(HIP version line, clang version line) of the hipcc in use."""
+    r = subprocess.run([hipcc(), "--version"], capture_output=True, text=True)
+    lines = [l.strip() for l in r.stdout.splitlines()]
+    hip = next((l for l in lines if l.startswith("HIP version")), "?")
+    clang = next((l for l in lines if "clang version" in l), "?")
+    return hip, clang
+
+
 def build(verbose: bool = False) -> str:
     objdir = os.path.join(ROOT, "_build", "spense")
     os.makedirs(objdir, exist_ok=True)
@@ -52,6 +70,11 @@ def build(verbose: bool = False) -> str:
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stderr}")
     os.replace(tmp, LIB)
+    tc = toolchain()
+    print(f"toolchain: {tc[0]}; {tc[1]}", flush=True)
+    if tc != CHECKED_TOOLCHAIN:
+        print("WARNING: not the compiler the matrix-core wait states were checked with; run "
+              "tests/test_gpu_parity.py::test_every_kernel_shape_is_repeatable_and_within_bound first", flush=True)
     return LIB
 
 

@@ -167,16 +167,65 @@ struct Plan {
   size_t ws_bytes;        // device workspace needed (none at present)
 };
 
-int env_int(const char* name, int dflt) {
-  const char* v = getenv(name);
-  if (!v || !*v) return dflt;
-  return atoi(v);
-}
+// Parts of the plan a caller forced (spense_gemm_planned); the defaults leave every
+// choice to the planner.
+struct Override {
+  int kernel = 0, rt = 0, waves = 0, ct = 0, ksplit = 0, wused = 0, wused_d = 0, wused_s = 0, order = -1, xcd = -1,
+      u8 = 0;
+  bool operator==(const Override& o) const {
+    return kernel == o.kernel && rt == o.rt && waves == o.waves && ct == o.ct && ksplit == o.ksplit &&
+           wused == o.wused && wused_d == o.wused_d && wused_s == o.wused_s && order == o.order && xcd == o.xcd &&
+           u8 == o.u8;
+  }
+};
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
+constexpr int kMaxWavesUsed = 8;  // row-split kernel: waves per workgroup
+
 // Workgroup shapes the kernels are built for: (row tiles, waves).
 const int kShapes[][2] = {{2, 4}, {1, 4}, {2, 8}, {1, 8}, {1, 16}, {4, 4}};
+
+// Check a caller's override against what the kernels are built for and this weight can
+// run; fills *o (the planner's defaults for ov == NULL).
+int read_override(const spense_plan_override_t* ov, int32_t dtype, bool tiled, Override* o) {
+  *o = Override();
+  if (!ov) return SPENSE_OK;
+  o->kernel = ov->kernel;
+  o->rt = ov->row_tiles;
+  o->waves = ov->waves;
+  o->ct = ov->act_tiles;
+  o->ksplit = ov->ksplit;
+  o->wused = ov->waves_used;
+  o->wused_d = ov->waves_used_dense;
+  o->wused_s = ov->waves_used_24;
+  o->order = ov->block_order;
+  o->xcd = ov->xcd_order;
+  o->u8 = ov->u8;
+  if (o->kernel < 0 || o->kernel > 3) return fail(SPENSE_ERR_ARG, "plan: unknown kernel %d", o->kernel);
+  if (o->kernel == 1 && tiled) return fail(SPENSE_ERR_ARG, "plan: the K-split kernel reads the row-major layout only");
+  if (o->kernel == 3 && dtype != SPENSE_FP8_E4M3FN) return fail(SPENSE_ERR_ARG, "plan: the large-M kernel is fp8 only");
+  if (o->ct < 0 || o->ct > 2) return fail(SPENSE_ERR_ARG, "plan: act_tiles %d (0, 1 or 2)", o->ct);
+  if (o->ksplit < 0 || o->ksplit > 8) return fail(SPENSE_ERR_ARG, "plan: ksplit %d outside [0, 8]", o->ksplit);
+  for (int w : {o->wused, o->wused_d, o->wused_s})
+    if (w < 0 || w > kMaxWavesUsed) return fail(SPENSE_ERR_ARG, "plan: waves used %d outside [0, 8]", w);
+  if (o->order < -1 || o->order > 2) return fail(SPENSE_ERR_ARG, "plan: block_order %d", o->order);
+  if (o->xcd < -1 || o->xcd > 1) return fail(SPENSE_ERR_ARG, "plan: xcd_order %d", o->xcd);
+  if (o->u8 < 0 || o->u8 > 1) return fail(SPENSE_ERR_ARG, "plan: u8 %d", o->u8);
+  if (o->rt || o->waves) {
+    bool okshape = false;
+    if (o->kernel == 1) {
+      for (const auto& sh : kShapes) okshape = okshape || (sh[0] == o->rt && sh[1] == o->waves);
+    } else if (o->kernel == 2) {
+      okshape = (o->rt == 1 && (o->waves == 4 || o->waves == 8)) || (o->rt == 2 && o->waves == 4);
+    } else if (o->kernel == 3) {
+      okshape = o->rt == 0 && (o->waves == 4 || o->waves == 8);
+    }
+    if (!okshape)
+      return fail(SPENSE_ERR_ARG, "plan: no kernel %d built for %d row tiles x %d waves", o->kernel, o->rt, o->waves);
+  }
+  return SPENSE_OK;
+}
 
 constexpr int kCUs = 256;  // compute units of an MI355X
 constexpr int64_t kBigMinM = 65;       // tokens from which the large-M kernel is used (fp8)
@@ -228,7 +277,7 @@ void pick_waves(int n, const int64_t* rows, const int* kind, const double* tile,
 // of an output-split weight, whose rows carry more bytes, gets fewer, so that the
 // workgroups are alike in bytes).
 void choose_rows_per_group(spense::Region* regs, int nreg, int rt, int waves, int ct, int mblocks, int64_t K, int es,
-                           double sparse_cost, int ksplit) {
+                           double sparse_cost, int ksplit, const Override& ov) {
   double tile_b[2];
   int64_t rows[2];
   const int kind[2] = {0, 1};  // one kind per region
@@ -239,8 +288,7 @@ void choose_rows_per_group(spense::Region* regs, int nreg, int rt, int waves, in
   const double x_cost = 0.25 * 16.0 * ct * K * es / ksplit;
   int bw[2];
   pick_waves(nreg, rows, kind, tile_b, rt, waves, (int64_t)mblocks * ksplit, x_cost, bw);
-  const int ew = env_int("SPENSE_WUSED", 0);  // testing knobs: waves used, all regions / per kind
-  const int ewd = env_int("SPENSE_WUSED_DENSE", 0), ews = env_int("SPENSE_WUSED_24", 0);
+  const int ew = ov.wused, ewd = ov.wused_d, ews = ov.wused_s;  // forced: every region / per kind
   for (int i = 0; i < nreg; ++i) {
     const int ek = regs[i].kbound == 0 ? ewd : ews;
     regs[i].wused = ew > 0 ? std::min(ew, waves) : (ek > 0 ? std::min(ek, waves) : bw[i]);
@@ -259,7 +307,8 @@ void choose_rows_per_group(spense::Region* regs, int nreg, int rt, int waves, in
 // 4 slices, up to 1.5x at 17-64 tokens and 4-12% at 1-16 (all dense: 2 or 4 slices
 // within run-to-run noise from 17 tokens; 4 kept).
 // q (512 tiles, 10 chunks): 2 slices lose 12-15% at 32-64 tokens, so none.
-int choose_ksplit(const spense::Region* regs, int nreg, int ct, int mblocks, int64_t chunks, int64_t M) {
+int choose_ksplit(const spense::Region* regs, int nreg, int ct, int mblocks, int64_t chunks, int64_t M,
+                  const Override& ov) {
   int64_t tiles = 0;
   bool has_24 = false;
   for (int i = 0; i < nreg; ++i) {
@@ -286,8 +335,7 @@ int choose_ksplit(const spense::Region* regs, int nreg, int ct, int mblocks, int
       S = (int)std::max<int64_t>(1, std::min<int64_t>({4, by_tiles, chunks / 5}));
     }
   }
-  const int e = env_int("SPENSE_KSPLIT", 0);
-  if (e >= 1 && e <= 8) S = (int)std::max<int64_t>(1, std::min<int64_t>(e, chunks));
+  if (ov.ksplit >= 1) S = (int)std::max<int64_t>(1, std::min<int64_t>(ov.ksplit, chunks));
   return S;
 }
 
@@ -313,15 +361,14 @@ void slice_cuts(spense::Region& r, int S, int64_t kc, int es, double sparse_cost
 // the same decomposition and summation order (the dense baseline and a Spense weight
 // with no 2:4 part are planned identically).
 void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, int64_t dense_begin, bool tiled,
-               Plan* pl) {
+               const Override& ov, Plan* pl) {
   using spense::Region;
   memset(pl, 0, sizeof *pl);
   const int es = esize(dtype);
   const int64_t gran = dtype == SPENSE_FP8_E4M3FN ? 128 : 64;  // K per 2:4 instruction
   const double sparse_cost = 0.5 * es + 0.125;                 // bytes per logical 2:4 entry
   int ct = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
-  const int ect = env_int("SPENSE_CT", 0);  // testing knob: at most this many activation tiles
-  if (ect == 1 || ect == 2) ct = std::min(ct, ect);
+  if (ov.ct == 1 || ov.ct == 2) ct = std::min(ct, ov.ct);
   pl->ls.ct = ct;
   pl->ls.mblocks = (int)ceil_div(M, 16 * ct);
 
@@ -352,22 +399,20 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
     rt = 1;
     waves = 8;
   }
-  const int erows = env_int("SPENSE_ROWS", -1);
-  if (erows >= 0 && !tiled) rows_mode = erows ? 1 : 0;
-  const int ert = env_int("SPENSE_RT", 0), ew = env_int("SPENSE_WAVES", 0);
-  for (const auto& sh : kShapes)
-    if (sh[0] == ert && sh[1] == ew) {
-      rt = ert;
-      waves = ew;
-    }
-  if (rows_mode && !((rt == 1 && (waves == 4 || waves == 8)) || (rt == 2 && waves == 4))) {
+  if (ov.kernel == 1) rows_mode = 0;  // forced (checked against the layout by read_override)
+  if (ov.kernel == 2) rows_mode = 1;
+  if (rows_mode) {
     rt = 1;
-    waves = 4;
+    waves = 8;
+  }
+  if (ov.rt && ov.kernel != 3) {  // a shape checked against the kernel's list
+    rt = ov.rt;
+    waves = ov.waves;
   }
   pl->ls.rt = rt;
   pl->ls.waves = waves;
   pl->ls.rows = rows_mode;
-  pl->ls.u8 = (ct == 1 && rt == 1 && (waves == 4 || waves == 8) && env_int("SPENSE_U8", 0)) ? 1 : 0;
+  pl->ls.u8 = (ct == 1 && rt == 1 && (waves == 4 || waves == 8) && ov.u8) ? 1 : 0;
   // Many tokens (fp8): 128-row x 256-token workgroup tiles.  Measured on MI355X (q / k /
   // o / gate / down shapes, M = 65 .. 2048, XCD-aware order): it wins above one row-split
   // token block (64 tokens) once there are at least 128 such tiles (gate / up at M = 96 /
@@ -375,11 +420,11 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
   // and down at M = 1024: 60 vs 97 and 156 vs 265 us); with fewer (q below 512 tokens, o
   // and down below 1024), the row-split kernel's finer grid keeps more CUs busy.
   int big = (dtype == SPENSE_FP8_E4M3FN && M >= kBigMinM && ceil_div(N, 128) * ceil_div(M, 256) >= kBigMinTiles) ? 1 : 0;
-  const int ebig = env_int("SPENSE_BIG", -1);  // testing knob: force the large-M kernel on or off
-  if (ebig >= 0) big = (ebig && dtype == SPENSE_FP8_E4M3FN) ? 1 : 0;
+  if (ov.kernel == 1 || ov.kernel == 2) big = 0;
+  if (ov.kernel == 3) big = 1;  // fp8 (checked by read_override)
   pl->ls.big = big;
   const int big_rows = 128;  // rows of a large-M workgroup tile
-  if (big) pl->ls.waves = env_int("SPENSE_BIG_WAVES", 8) == 4 ? 4 : 8;  // testing knob
+  if (big) pl->ls.waves = ov.waves == 4 ? 4 : 8;
   const int64_t tblocks = ceil_div(M, 256);
 
   Region regs[2];
@@ -423,9 +468,9 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
     const int64_t kc = dtype == SPENSE_FP8_E4M3FN ? 512 : 256;
     int64_t chunks = 0;
     for (int i = 0; i < nreg; ++i) chunks = std::max(chunks, ceil_div(regs[i].kbound, kc) + ceil_div(K - regs[i].kbound, kc));
-    ksplit = chunks > 0 ? choose_ksplit(regs, nreg, pl->ls.ct, pl->ls.mblocks, chunks, M) : 1;
+    ksplit = chunks > 0 ? choose_ksplit(regs, nreg, pl->ls.ct, pl->ls.mblocks, chunks, M, ov) : 1;
     for (int i = 0; i < nreg; ++i) slice_cuts(regs[i], ksplit, kc, es, sparse_cost);
-    choose_rows_per_group(regs, nreg, rt, waves, pl->ls.ct, pl->ls.mblocks, K, es, sparse_cost, ksplit);
+    choose_rows_per_group(regs, nreg, rt, waves, pl->ls.ct, pl->ls.mblocks, K, es, sparse_cost, ksplit, ov);
   }
   spense::GemmArgs& a = pl->args;
   a.nreg = nreg;
@@ -451,19 +496,63 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
     const int64_t TGc = T / GT;
     int64_t rbtot = 0;
     for (int i = 0; i < nreg; ++i) rbtot += ceil_div(regs[i].rows, big_rows);
-    if (8 % TGc == 0 && rbtot % (8 / TGc) == 0 && env_int("SPENSE_BIG_XCD", 1)) {
+    if (8 % TGc == 0 && rbtot % (8 / TGc) == 0 && ov.xcd != 0) {
       a.xgt = (int32_t)GT;
       a.xrc = (int32_t)(8 / TGc);
     }
   }
+  // Row-split kernel with several token blocks: the blocks of a row group on one XCD
+  // (workgroups are dealt to the 8 XCDs round-robin), so that they share its L2 for the
+  // weight rows.  Measured on MI355X (tiled, M = 128 / 256 / 512, us): down 53.8 / 65.6 /
+  // 125.5 -> 50.5 / 65.0 / 123.2; q 18.3 / 34.7 / 46.0 -> 18.2 / 33.3 / 45.8; Seed-OSS q
+  // 19.3 / 38.0 / 47.6 -> 19.2 / 35.5 / 47.0; o and k within 1%.  Needs the row groups
+  // to split evenly over the XCDs.
+  a.mblk = pl->ls.mblocks;
+  a.rorder = pl->ls.rows && !big && pl->ls.mblocks > 1 ? (ov.order >= 0 ? ov.order : 2) : 0;
+  if (a.rorder == 2 && a.groups % 8) a.rorder = 0;
   // K-sliced regions keep fp32 partial sums: slices x M x N floats
   pl->ws_bytes = ksplit > 1 ? (size_t)ksplit * (size_t)M * (size_t)N * sizeof(float) : 0;
+}
+
+// The plans of the last few calls of this thread, keyed by everything make_plan reads
+// (the plan depends on nothing else): a decode loop that repeats one geometry plans once.
+struct PlanKey {
+  int32_t dtype, split;
+  int64_t M, N, K, dense_begin;
+  bool tiled;
+  Override ov;
+  bool operator==(const PlanKey& o) const {
+    return dtype == o.dtype && split == o.split && M == o.M && N == o.N && K == o.K && dense_begin == o.dense_begin &&
+           tiled == o.tiled && ov == o.ov;
+  }
+};
+constexpr int kPlanCache = 8;
+struct PlanCache {
+  PlanKey key[kPlanCache];
+  Plan plan[kPlanCache];
+  int used = 0, next = 0;
+};
+thread_local PlanCache g_plans;
+
+const Plan& cached_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, int64_t dense_begin, bool tiled,
+                        const Override& ov) {
+  PlanCache& c = g_plans;
+  const PlanKey k{dtype, split, M, N, K, dense_begin, tiled, ov};
+  for (int i = 0; i < c.used; ++i)
+    if (c.key[i] == k) return c.plan[i];
+  const int slot = c.next;
+  c.next = (c.next + 1) % kPlanCache;
+  if (c.used < kPlanCache) ++c.used;
+  c.key[slot] = k;
+  make_plan(dtype, M, N, split, K, dense_begin, tiled, ov, &c.plan[slot]);
+  return c.plan[slot];
 }
 
 int gemm_common(const void* X, int64_t M, int64_t ldx, int32_t dtype, int32_t split, int64_t N, int64_t K,
                 int64_t dense_begin, int32_t layout, const void* values, int64_t values_ld, const uint32_t* meta,
                 int64_t meta_ld, const void* dense, int64_t dense_ld, const float* w_scale, const float* x_scale,
-                void* Y, int64_t ldy, uint32_t out_flags, void* ws, size_t ws_bytes, hipStream_t stream) {
+                void* Y, int64_t ldy, uint32_t out_flags, void* ws, size_t ws_bytes, const Override& ov,
+                hipStream_t stream) {
   const bool tiled = layout == SPENSE_LAYOUT_TILED;
   if (M < 0) return fail(SPENSE_ERR_ARG, "negative M");
   if (M > INT32_MAX) return fail(SPENSE_ERR_ARG, "M too large");
@@ -481,8 +570,7 @@ int gemm_common(const void* X, int64_t M, int64_t ldx, int32_t dtype, int32_t sp
   const int out_es = (out_flags & SPENSE_OUT_F32) ? 4 : 2;
   if ((reinterpret_cast<uintptr_t>(Y) % out_es)) return fail(SPENSE_ERR_ALIGN, "Y misaligned");
   if ((int64_t)M * ldy > (int64_t)1 << 40) return fail(SPENSE_ERR_ARG, "Y too large");
-  Plan pl;
-  make_plan(dtype, M, N, split, K, dense_begin, tiled, &pl);
+  Plan pl = cached_plan(dtype, M, N, split, K, dense_begin, tiled, ov);
   if (pl.ws_bytes > 0) {
     if (!ws || ws_bytes < pl.ws_bytes)
       return fail(SPENSE_ERR_WS, "workspace of %zu bytes needed, %zu given", pl.ws_bytes, ws ? ws_bytes : (size_t)0);
@@ -534,17 +622,6 @@ int gemm_common(const void* X, int64_t M, int64_t ldx, int32_t dtype, int32_t sp
   a.d_bytes = (uint32_t)db;
   // the row-split kernel reads the weight through its descriptor
   a.nmat = 1;
-  // Row-split kernel with several token blocks: the blocks of a row group on one XCD
-  // (workgroups are dealt to the 8 XCDs round-robin), so that they share its L2 for the
-  // weight rows.  Measured on MI355X (tiled, M = 128 / 256 / 512, us): down 53.8 / 65.6 /
-  // 125.5 -> 50.5 / 65.0 / 123.2; q 18.3 / 34.7 / 46.0 -> 18.2 / 33.3 / 45.8; Seed-OSS q
-  // 19.3 / 38.0 / 47.6 -> 19.2 / 35.5 / 47.0; o and k within 1%.  Needs the row groups
-  // to split evenly over the XCDs; SPENSE_ROWS_ORDER (testing knob) forces 0 (grid of
-  // row groups x token blocks), 1 (token blocks of a row group adjacent) or 2.
-  a.mblk = pl.ls.mblocks;
-  a.rorder = pl.ls.rows && pl.ls.mblocks > 1 ? env_int("SPENSE_ROWS_ORDER", 2) : 0;
-  if (a.rorder == 2 && a.groups % 8) a.rorder = 0;
-  if (a.rorder < 0 || a.rorder > 2) a.rorder = 0;
   a.mat[0] = spense::MatDesc{a.values, a.meta, a.dense, a.v_bytes, a.m_bytes, a.d_bytes, a.Y, a.ldy, a.sw,
                              a.vec_store};
   if (a.groups == 0) return ok();
@@ -937,24 +1014,39 @@ int spense_decompress(const spense_packed_t* packed, void* W_out, int64_t ldw, h
   return ok();
 }
 
-size_t spense_gemm_workspace_size(int64_t M, const spense_packed_t* packed) {
+size_t spense_gemm_planned_workspace_size(int64_t M, const spense_packed_t* packed,
+                                          const spense_plan_override_t* plan) {
   spense_layout_t L;
-  if (M <= 0 || check_packed(packed, &L)) return 0;
-  Plan pl;
-  make_plan(packed->dtype, M, packed->N, packed->split, packed->K, packed->dense_begin,
-            packed->layout == SPENSE_LAYOUT_TILED, &pl);
-  return pl.ws_bytes;
+  if (M <= 0 || M > INT32_MAX || check_packed(packed, &L)) return 0;
+  Override ov;
+  if (read_override(plan, packed->dtype, packed->layout == SPENSE_LAYOUT_TILED, &ov)) return 0;
+  return cached_plan(packed->dtype, M, packed->N, packed->split, packed->K, packed->dense_begin,
+                     packed->layout == SPENSE_LAYOUT_TILED, ov)
+      .ws_bytes;
+}
+
+size_t spense_gemm_workspace_size(int64_t M, const spense_packed_t* packed) {
+  return spense_gemm_planned_workspace_size(M, packed, nullptr);
+}
+
+int spense_gemm_planned(const void* X, int64_t M, int64_t ldx, const spense_packed_t* packed, const float* w_scale,
+                        const float* x_scale, void* Y, int64_t ldy, uint32_t out_flags, void* ws, size_t ws_bytes,
+                        const spense_plan_override_t* plan, hipStream_t stream) {
+  spense_layout_t L;
+  int rc = check_packed(packed, &L);
+  if (rc) return rc;
+  Override ov;
+  rc = read_override(plan, packed->dtype, packed->layout == SPENSE_LAYOUT_TILED, &ov);
+  if (rc) return rc;
+  return gemm_common(X, M, ldx, packed->dtype, packed->split, packed->N, packed->K, packed->dense_begin,
+                     packed->layout, packed->values, packed->values_ld, packed->meta, packed->meta_ld, packed->dense,
+                     packed->dense_ld, w_scale, x_scale, Y, ldy, out_flags, ws, ws_bytes, ov, stream);
 }
 
 int spense_gemm(const void* X, int64_t M, int64_t ldx, const spense_packed_t* packed, const float* w_scale,
                 const float* x_scale, void* Y, int64_t ldy, uint32_t out_flags, void* ws, size_t ws_bytes,
                 hipStream_t stream) {
-  spense_layout_t L;
-  int rc = check_packed(packed, &L);
-  if (rc) return rc;
-  return gemm_common(X, M, ldx, packed->dtype, packed->split, packed->N, packed->K, packed->dense_begin,
-                     packed->layout, packed->values, packed->values_ld, packed->meta, packed->meta_ld, packed->dense,
-                     packed->dense_ld, w_scale, x_scale, Y, ldy, out_flags, ws, ws_bytes, stream);
+  return spense_gemm_planned(X, M, ldx, packed, w_scale, x_scale, Y, ldy, out_flags, ws, ws_bytes, nullptr, stream);
 }
 
 int spense_gemm_grouped(const void* X, int64_t M, int64_t ldx, int32_t count, const spense_packed_t* const* packed,
@@ -1141,10 +1233,8 @@ int spense_gemm_glu_fp8(const void* X, int64_t M, int64_t ldx, const spense_pack
 
 size_t spense_dense_gemm_workspace_size(int64_t M, int64_t N, int64_t K, int32_t dtype) {
   spense_layout_t L;
-  if (M <= 0 || layout_impl(N, K, dtype, SPENSE_SPLIT_OUTPUT, 0, &L)) return 0;
-  Plan pl;
-  make_plan(dtype, M, N, SPENSE_SPLIT_OUTPUT, K, 0, false, &pl);
-  return pl.ws_bytes;
+  if (M <= 0 || M > INT32_MAX || layout_impl(N, K, dtype, SPENSE_SPLIT_OUTPUT, 0, &L)) return 0;
+  return cached_plan(dtype, M, N, SPENSE_SPLIT_OUTPUT, K, 0, false, Override()).ws_bytes;
 }
 
 int spense_dense_gemm(const void* X, int64_t M, int64_t ldx, const void* W, int64_t ldw, int64_t N, int64_t K,
@@ -1160,7 +1250,7 @@ int spense_dense_gemm(const void* X, int64_t M, int64_t ldx, const void* W, int6
     if (!aligned16(W) || (ldw * es) % 16) return fail(SPENSE_ERR_ALIGN, "W must be 16-byte aligned, 16-byte pitch");
   }
   return gemm_common(X, M, ldx, dtype, SPENSE_SPLIT_OUTPUT, N, K, 0, SPENSE_LAYOUT_ROWMAJOR, nullptr, 0, nullptr, 0, W,
-                     ldw, w_scale, x_scale, Y, ldy, out_flags, ws, ws_bytes, stream);
+                     ldw, w_scale, x_scale, Y, ldy, out_flags, ws, ws_bytes, Override(), stream);
 }
 
 }  // extern "C"

@@ -34,6 +34,8 @@
 // All loads are range-checked buffer loads: a lane whose chunk lies past the end of its
 // range gets an out-of-range offset and reads zeros, so the loops have no divergent
 // branches.
+#include <mutex>
+
 #include "spense_internal.h"
 
 namespace spense {
@@ -1346,17 +1348,28 @@ __global__ __launch_bounds__(64 * WV) void spense_gemm_big_kernel(GemmArgs a) {
     }
 }
 
+// The large-M kernel's dynamic LDS above the default limit is a per-device function
+// attribute: set once per (device, kernel instance), under std::call_once, so that host
+// threads making their first large-M call together do not race.
+constexpr int kMaxDevices = 64;
+std::once_flag g_big_lds_once[kMaxDevices][2][2];
+hipError_t g_big_lds_rc[kMaxDevices][2][2];
+
 template <int WV>
 hipError_t launch_big_wv(const GemmArgs& a, hipStream_t s) {
   constexpr int lds = 3 * BigStage::BYTES;
   static_assert(lds <= 160 * 1024, "LDS of a CU");
   auto k = a.tiled ? spense_gemm_big_kernel<true, WV> : spense_gemm_big_kernel<false, WV>;
-  static bool attr_set[2] = {false, false};
-  if (!attr_set[a.tiled]) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize, lds);
-    if (e != hipSuccess) return e;
-    attr_set[a.tiled] = true;
-  }
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  const int t = a.tiled ? 1 : 0, w = WV == 8 ? 1 : 0;
+  std::call_once(g_big_lds_once[dev][t][w], [&] {
+    g_big_lds_rc[dev][t][w] =
+        hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  });
+  if (g_big_lds_rc[dev][t][w] != hipSuccess) return g_big_lds_rc[dev][t][w];
   hipLaunchKernelGGL(k, dim3(a.groups), dim3(64 * WV), lds, s, a);
   return hipGetLastError();
 }

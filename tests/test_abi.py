@@ -41,7 +41,7 @@ def test_library_exports_every_declared_symbol(S):
     for n in _declared():
         assert hasattr(lib, n), f"{n} declared in include/ but not exported"
     assert set(_declared()) == set(S.EXPORTS)
-    assert S.spense_abi_version() == 8
+    assert S.spense_abi_version() == 9
 
 
 @pytest.mark.parametrize("N,K,split,db", [(256, 512, 0, 192), (256, 512, 1, 384), (25600, 5120, 0, 19200),
@@ -373,3 +373,75 @@ def test_k_slice_rule_on_the_layer_shapes(S):
     assert ws(5120, 8192, 1, 1) == 0 and ws(5120, 8192, 1, 16) == 0  # o: one token block of 1-16
     assert ws(5120, 8192, 1, 17) > 0 and ws(5120, 8192, 1, 64) > 0  # o from 17 tokens
     assert ws(1024, 5120, 0, 65) == 0 and ws(5120, 25600, 1, 200) == 0  # several token blocks
+
+
+def _down_desc(S, layout=0, dtype=1):
+    L = S.spense_layout(5120, 25600, dtype, 1, 19200)
+    return S.spense_packed_t(dtype, 1, 5120, 25600, 19200, 4096, L.values_ld, 8192, L.meta_ld, 16384, L.dense_ld,
+                             layout)
+
+
+def test_plan_override_is_checked_on_the_host(S):
+    """spense_gemm_planned: a forced plan changes what the planner would choose (seen here
+    through the workspace it needs), and an override no kernel is built for, or this
+    weight cannot run, is rejected with SPENSE_ERR_ARG before any device call."""
+    po = S.plan_override
+    rm, tl, bf = _down_desc(S), _down_desc(S, S.SPENSE_LAYOUT_TILED), _down_desc(S, dtype=2)
+    assert S.spense_gemm_planned_workspace_size(64, rm, None) == S.spense_gemm_workspace_size(64, rm)
+    assert S.spense_gemm_planned_workspace_size(64, tl, po(kernel=2, ksplit=3)) == 3 * 64 * 5120 * 4
+    assert S.spense_gemm_planned_workspace_size(64, tl, po(kernel=2, ksplit=1)) == 0
+    assert S.spense_gemm_planned_workspace_size(64, rm, po(kernel=1)) == 0  # no K slices in the K-split kernel
+    assert S.spense_gemm_planned_workspace_size(64, rm, po(kernel=3)) == 0
+    bad = [(tl, po(kernel=1)),                      # the K-split kernel reads the row-major layout only
+           (bf, po(kernel=3)),                      # large-M is fp8 only
+           (rm, po(kernel=2, row_tiles=4, waves=4)),  # no such row-split shape
+           (rm, po(kernel=1, row_tiles=4, waves=8)),  # no such K-split shape
+           (rm, po(kernel=3, waves=16)),
+           (rm, po(waves=8)),                       # a shape needs the kernel it is for
+           (rm, po(kernel=5)), (rm, po(ksplit=9)), (rm, po(act_tiles=3)), (rm, po(waves_used=9)),
+           (rm, po(block_order=3)), (rm, po(xcd_order=2)), (rm, po(u8=2))]
+    for desc, p in bad:
+        assert S.spense_gemm_planned_workspace_size(64, desc, p) == 0
+        rc = S.spense_gemm_planned(1 << 28, 64, 25600, desc, None, None, 1 << 30, 5120, 0, 1 << 31, 1 << 26, p, None)
+        assert rc == S.SPENSE_ERR_ARG, (p.kernel, rc)
+        assert "plan" in S.spense_last_error()
+
+
+def test_environment_does_not_change_the_plan(S, monkeypatch):
+    """spense_gemm's plan depends on the dtype, M and the weight geometry only: variables
+    that once steered the planner in testing builds change nothing."""
+    tl = _down_desc(S, S.SPENSE_LAYOUT_TILED)
+    before = [S.spense_gemm_workspace_size(m, tl) for m in (1, 16, 64)]
+    for k, v in (("SPENSE_KSPLIT", "2"), ("SPENSE_ROWS", "0"), ("SPENSE_BIG", "1"), ("SPENSE_CT", "1"),
+                 ("SPENSE_WAVES", "4"), ("SPENSE_RT", "2"), ("SPENSE_WUSED", "3")):
+        monkeypatch.setenv(k, v)
+    assert [S.spense_gemm_workspace_size(m, tl) for m in (1, 16, 64)] == before
+
+
+def test_binding_checks_tensors_before_the_library(S):
+    """The torch wrappers reject outputs of the wrong shape, dtype or layout and
+    activations of the wrong dtype before any pointer reaches the library (a short
+    output would otherwise be written past its end)."""
+    import torch
+    N, K, db = 64, 256, 48
+    pw = S.PackedWeight.empty(N, K, S.SPENSE_FP8_E4M3FN, S.SPENSE_SPLIT_OUTPUT, db, device="cpu")
+    X = torch.zeros((8, K), dtype=torch.uint8)
+    cases = [dict(out=torch.empty((7, N), dtype=torch.bfloat16)),                    # too few rows
+             dict(out=torch.empty((8, N), dtype=torch.float32)),                     # fp32 for a bf16 output
+             dict(out=torch.empty((8, N), dtype=torch.bfloat16), out_f32=True),      # bf16 for an fp32 output
+             dict(out=torch.empty((N, 8), dtype=torch.bfloat16).t()),                # columns not contiguous
+             dict(out=torch.empty((8, N, 1), dtype=torch.bfloat16)[:, :, 0])]        # 2-D view, fine shape: ok below
+    for kw in cases[:4]:
+        with pytest.raises(ValueError):
+            S.gemm(X, pw, **kw)
+    with pytest.raises(ValueError):
+        S.gemm(X.to(torch.bfloat16), pw)  # bf16 activations for an fp8 weight
+    with pytest.raises(ValueError):
+        S.gemm(torch.zeros((8, K + 32), dtype=torch.uint8), pw)  # K differs
+    with pytest.raises(ValueError):
+        S.gemm_grouped(X, [pw, pw], outs=[torch.empty((8, N), dtype=torch.bfloat16),
+                                          torch.empty((4, N), dtype=torch.bfloat16)])
+    with pytest.raises(ValueError):
+        S.dense_gemm(X, torch.zeros((N, K), dtype=torch.uint8), out=torch.empty((8, N - 1), dtype=torch.bfloat16))
+    with pytest.raises(ValueError):
+        S.dense_gemm(X.to(torch.bfloat16), torch.zeros((N, K), dtype=torch.uint8))

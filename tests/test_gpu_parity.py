@@ -118,8 +118,9 @@ def assert_f32_bound(y, X, Wd, dtype, sw=None, sx=None):
     assert worst <= 1.0, f"fp32 output exceeds the error bound by {worst:.2f}x"
 
 
-def run_gemm(S, pw, X, sw, sx, out_f32):
-    y = S.gemm(tdev(X), pw, None if sw is None else tdev(sw), None if sx is None else tdev(sx), out_f32=out_f32)
+def run_gemm(S, pw, X, sw, sx, out_f32, plan=None):
+    y = S.gemm(tdev(X), pw, None if sw is None else tdev(sw), None if sx is None else tdev(sx), out_f32=out_f32,
+               plan=plan)
     torch.cuda.synchronize()
     return tnp(y)
 
@@ -228,19 +229,28 @@ def test_repeated_calls_are_bitwise_identical(S):
     assert all(np.array_equal(outs[0], o) for o in outs[1:])
 
 
-KERNEL_SHAPES = [dict(), dict(SPENSE_WAVES="4", SPENSE_RT="1"), dict(SPENSE_WAVES="16", SPENSE_RT="1"),
-                 dict(SPENSE_WAVES="8", SPENSE_RT="2"), dict(SPENSE_WAVES="8", SPENSE_RT="1", SPENSE_U8="1"),
-                 dict(SPENSE_ROWS="1", SPENSE_WAVES="4", SPENSE_RT="1"),
-                 dict(SPENSE_ROWS="1", SPENSE_WAVES="8", SPENSE_RT="1"),
-                 dict(SPENSE_ROWS="1", SPENSE_WAVES="8", SPENSE_RT="1", SPENSE_KSPLIT="4"),
-                 dict(SPENSE_ROWS="1", SPENSE_WAVES="4", SPENSE_RT="1", SPENSE_KSPLIT="7"),
-                 dict(SPENSE_ROWS="1", SPENSE_WAVES="4", SPENSE_RT="2"),
-                 dict(SPENSE_ROWS="1", SPENSE_WAVES="4", SPENSE_RT="2", SPENSE_KSPLIT="3")]
+# forced plans (spense_gemm_planned): kernel 1 = K split over a workgroup's waves, 2 = rows
+# split with activations in LDS, 3 = large-M tiles; None = the planner's own choice
+KSPLIT, ROWS, BIG = 1, 2, 3
+KERNEL_SHAPES = [None, dict(kernel=KSPLIT, waves=4, row_tiles=1), dict(kernel=KSPLIT, waves=16, row_tiles=1),
+                 dict(kernel=KSPLIT, waves=8, row_tiles=2), dict(kernel=KSPLIT, waves=8, row_tiles=1, u8=1),
+                 dict(kernel=KSPLIT, waves=4, row_tiles=2), dict(kernel=KSPLIT, waves=4, row_tiles=4),
+                 dict(kernel=ROWS, waves=4, row_tiles=1),
+                 dict(kernel=ROWS, waves=8, row_tiles=1),
+                 dict(kernel=ROWS, waves=8, row_tiles=1, ksplit=4),
+                 dict(kernel=ROWS, waves=4, row_tiles=1, ksplit=7),
+                 dict(kernel=ROWS, waves=4, row_tiles=2),
+                 dict(kernel=ROWS, waves=4, row_tiles=2, ksplit=3),
+                 dict(kernel=BIG, waves=8), dict(kernel=BIG, waves=4)]
+
+
+def plan(S, cfg):
+    return None if cfg is None else S.plan_override(**cfg)
 
 
 @pytest.mark.parametrize("axis,db", [(1, 6144), (0, 1536)])
 @pytest.mark.parametrize("dtype", [FP8, BF16])
-def test_every_kernel_shape_is_repeatable_and_within_bound(S, dtype, axis, db, monkeypatch):
+def test_every_kernel_shape_is_repeatable_and_within_bound(S, dtype, axis, db):
     """Repeated calls on the same inputs are bitwise identical and inside the error bound
     for every kernel and workgroup shape, with both regions present.  This guards the
     points where a matrix-core result is read by a later instruction in another basic
@@ -251,15 +261,13 @@ def test_every_kernel_shape_is_repeatable_and_within_bound(S, dtype, axis, db, m
     pw, (v, m, d) = compress_both(S, W, mask, dtype, axis, db)
     Wd = oracle.decompress(v, m, d, N, K, dtype, axis, db)
     for cfg in KERNEL_SHAPES:
-        for k in ("SPENSE_WAVES", "SPENSE_RT", "SPENSE_U8", "SPENSE_ROWS", "SPENSE_KSPLIT"):
-            monkeypatch.delenv(k, raising=False)
-        for k, val in cfg.items():
-            monkeypatch.setenv(k, val)
+        if cfg is not None and cfg["kernel"] == BIG and dtype != FP8:
+            continue
         for M in (64, 33, 7, 1):
             swd = None if sw is None else tdev(sw)
             sxd = None if sx is None else tdev(sx[:M])
             Xd = tdev(X[:M])
-            outs = [tnp(S.gemm(Xd, pw, swd, sxd, out_f32=True)) for _ in range(4)]
+            outs = [tnp(S.gemm(Xd, pw, swd, sxd, out_f32=True, plan=plan(S, cfg))) for _ in range(4)]
             assert all(np.array_equal(outs[0], o) for o in outs[1:]), f"{cfg} M={M}: calls differ"
             assert_f32_bound(outs[0], X[:M], Wd, dtype, sw, None if sx is None else sx[:M])
 
@@ -349,16 +357,16 @@ def test_tile_matches_definition(S, axis, N, K, db):
 
 @pytest.mark.parametrize("axis,N,K,db", TILE_CASES)
 @pytest.mark.parametrize("M", [1, 7, 20, 64, 130])
-def test_tiled_gemm_equals_row_major(S, axis, N, K, db, M, monkeypatch):
+def test_tiled_gemm_equals_row_major(S, axis, N, K, db, M):
     """The tiled weight gives bit-for-bit the output of the row-major weight under the
     same (row-split) plan, and stays inside the error bound against the oracle."""
     W, mask, X, sw, sx = random_case(40 + N, M, N, K, axis, db, FP8)
     pw, (v, m, d) = compress_both(S, W, mask, FP8, axis, db)
     pwt = S.tile(pw)
-    monkeypatch.setenv("SPENSE_ROWS", "1")
+    rows = S.plan_override(kernel=ROWS)
     for f32 in (True, False):
-        a = run_gemm(S, pw, X, sw, sx, f32)
-        b = run_gemm(S, pwt, X, sw, sx, f32)
+        a = run_gemm(S, pw, X, sw, sx, f32, rows)
+        b = run_gemm(S, pwt, X, sw, sx, f32, rows)
         assert np.array_equal(a, b)
     Wd = oracle.decompress(v, m, d, N, K, FP8, axis, db)
     assert_f32_bound(run_gemm(S, pwt, X, sw, sx, True), X, Wd, FP8, sw, sx)
@@ -385,23 +393,22 @@ BIG_CASES = [  # axis, M, N, K, dense_begin: ragged tokens, rows and columns aro
 
 @pytest.mark.parametrize("waves", [4, 8])
 @pytest.mark.parametrize("axis,M,N,K,db", BIG_CASES)
-def test_large_m_kernel_exact_both_layouts(S, axis, M, N, K, db, waves, monkeypatch):
+def test_large_m_kernel_exact_both_layouts(S, axis, M, N, K, db, waves):
     """The large-M kernel (128-row x 256-token tiles, 4 or 8 waves), forced on at any M, on
     exact-integer data: bit-exact against the oracle with the row-major and the tiled
     weight."""
     W, mask, X, sw, sx = gen.make_exact_int(13, M + N, M, N, K, gaxis(axis), db, gen.FP8)
     pw, (v, m, d) = compress_both(S, W, mask, FP8, axis, db)
     ref = oracle.spense_gemm(X, v, m, d, N, K, FP8, axis, db, sw, sx)
-    monkeypatch.setenv("SPENSE_BIG", "1")
-    monkeypatch.setenv("SPENSE_BIG_WAVES", str(waves))
+    big = S.plan_override(kernel=BIG, waves=waves)
     for w in (pw, S.tile(pw)):
-        assert np.array_equal(run_gemm(S, w, X, sw, sx, True), ref["y_f32"])
-        assert np.array_equal(run_gemm(S, w, X, sw, sx, False).view(np.uint16), ref["y_bf16"])
+        assert np.array_equal(run_gemm(S, w, X, sw, sx, True, big), ref["y_f32"])
+        assert np.array_equal(run_gemm(S, w, X, sw, sx, False, big).view(np.uint16), ref["y_bf16"])
 
 
 @pytest.mark.parametrize("waves", [4, 8])
 @pytest.mark.parametrize("axis,db", [(0, 744), (1, 1536)])
-def test_large_m_kernel_random_within_bound(S, axis, db, waves, monkeypatch):
+def test_large_m_kernel_random_within_bound(S, axis, db, waves):
     """Random data through the large-M kernel: inside the error bound against the oracle,
     equal with both layouts and bitwise repeatable."""
     M, N, K = 520, 1000, 2080
@@ -410,13 +417,12 @@ def test_large_m_kernel_random_within_bound(S, axis, db, waves, monkeypatch):
     ref = oracle.spense_gemm(X, v, m, d, N, K, FP8, axis, db, sw, sx)
     Wd = oracle.decompress(v, m, d, N, K, FP8, axis, db)
     pwt = S.tile(pw)
-    monkeypatch.setenv("SPENSE_BIG", "1")
-    monkeypatch.setenv("SPENSE_BIG_WAVES", str(waves))
-    y32 = run_gemm(S, pw, X, sw, sx, True)
+    big = S.plan_override(kernel=BIG, waves=waves)
+    y32 = run_gemm(S, pw, X, sw, sx, True, big)
     assert_f32_bound(y32, X, Wd, FP8, sw, sx)
-    assert_bf16_close(run_gemm(S, pw, X, sw, sx, False).view(np.uint16), ref["y_bf16"], FP8)
+    assert_bf16_close(run_gemm(S, pw, X, sw, sx, False, big).view(np.uint16), ref["y_bf16"], FP8)
     for _ in range(2):
-        assert np.array_equal(run_gemm(S, pwt, X, sw, sx, True), y32)
+        assert np.array_equal(run_gemm(S, pwt, X, sw, sx, True, big), y32)
 
 
 # ------------------------------------------------------------------ full-size workloads
@@ -483,6 +489,43 @@ def test_full_layer_linears(S, layer):
                    sample_rows=128)
 
 
+SEED_DECODE_MS = [1, 4, 16, 64, 256]
+
+
+@pytest.mark.timeout(400)
+@pytest.mark.parametrize("name", ["q", "k", "v", "o"])
+def test_full_seed_oss_attention_linears_at_decode_m(S, name):
+    """Seed-OSS-36B-like q (10240 x 5120), k / v (1024 x 5120) and o (5120 x 10240,
+    input-split) at every decode M the benchmark times (1, 4, 16, 64, 256): random data
+    on sampled rows, both layouts, bf16 tolerance and the fp32 bound.  These run the
+    plans the layer timing uses, among them k / v with 4 K slices at every M and o with
+    4 K slices from 17 tokens."""
+    i, (nm, N, K, axis) = next((i, m) for i, m in enumerate(gen.WORKLOADS[5]["mats"]) if m[0] == name)
+    _full_case(S, 5, i, nm, N, K, axis, 0.25, SEED_DECODE_MS, "normal", sample_rows=128)
+
+
+@pytest.mark.timeout(400)
+@pytest.mark.parametrize("name", ["q", "k", "o"])
+def test_seed_oss_decode_exact_whole_output(S, name):
+    """The same weights' shapes on exact-integer data: the whole output bit for bit, in
+    both layouts, at M = 256, 64, 20, 16, 4 and 1 (the activations of a smaller M are the
+    first rows of the larger draw, and each output row depends on its own row only)."""
+    _, N, K, axis = next(m for m in gen.WORKLOADS[5]["mats"] if m[0] == name)
+    ax = 0 if axis == gen.OUTPUT else 1
+    db = gen.split_point(N, K, axis, 0.25)
+    Mmax = 256
+    W, mask, X, sw, sx = gen.make_exact_int(22, N % 89, Mmax, N, K, axis, db, gen.FP8)
+    say(f"[exact seed] {name} {N}x{K}")
+    pw, (v, m, d) = compress_both(S, W, mask, FP8, ax, db)
+    ref = oracle.spense_gemm(X, v, m, d, N, K, FP8, ax, db, sw, sx)
+    for w in (pw, S.tile(pw)):
+        for M in (256, 64, 20, 16, 4, 1):
+            y32 = run_gemm(S, w, X[:M], sw, sx[:M], True)
+            ybf = run_gemm(S, w, X[:M], sw, sx[:M], False).view(np.uint16)
+            assert np.array_equal(y32, ref["y_f32"][:M]), f"{name} M={M} fp32"
+            assert np.array_equal(ybf, ref["y_bf16"][:M]), f"{name} M={M} bf16"
+
+
 @pytest.mark.timeout(400)
 @pytest.mark.parametrize("name,N,K,axis,M", [("gate_up", 25600, 5120, gen.OUTPUT, 64),
                                              ("down", 5120, 25600, gen.INPUT, 64),
@@ -511,28 +554,24 @@ def test_full_size_exact_integers_whole_output(S, name, N, K, axis, M):
                                                     (1, 1, 4, 3, 1), (1, 1, 8, 5, 1), (1, 1, 8, 8, 1), (1, 1, 4, 0, 2),
                                                     (1, 1, 8, 3, 3), (1, 1, 8, 8, 2), (1, 2, 4, 0, 1), (1, 2, 4, 3, 2)])
 @pytest.mark.parametrize("dtype,axis,M", [(FP8, 1, 3), (FP8, 0, 40), (BF16, 1, 20), (FP8, 1, 64), (BF16, 0, 17)])
-def test_every_workgroup_shape_is_exact(S, rows, rt, waves, wused, ks, dtype, axis, M, monkeypatch):
+def test_every_workgroup_shape_is_exact(S, rows, rt, waves, wused, ks, dtype, axis, M):
     """All built kernels and (row tiles, waves) shapes - K split across the waves of a
     workgroup, or rows split with activations staged in LDS, `wused` of the waves owning
     rows and K cut into `ks` slices whose partial sums are added afterwards - give
     bit-exact results on exact-integer data."""
-    monkeypatch.setenv("SPENSE_ROWS", str(rows))
-    monkeypatch.setenv("SPENSE_RT", str(rt))
-    monkeypatch.setenv("SPENSE_WAVES", str(waves))
-    monkeypatch.setenv("SPENSE_WUSED", str(wused))
-    monkeypatch.setenv("SPENSE_KSPLIT", str(ks))
+    p = S.plan_override(kernel=ROWS if rows else KSPLIT, row_tiles=rt, waves=waves, waves_used=wused, ksplit=ks)
     N, K = 200, 1056
     db = 800 if axis == 1 else 72
     W, mask, X, sw, sx = gen.make_exact_int(12, rt * 10 + waves, M, N, K, gaxis(axis), db, gdt(dtype))
     pw, (v, m, d) = compress_both(S, W, mask, dtype, axis, db)
     ref = oracle.spense_gemm(X, v, m, d, N, K, dtype, axis, db, sw, sx)
-    assert np.array_equal(run_gemm(S, pw, X, sw, sx, True), ref["y_f32"])
-    assert np.array_equal(run_gemm(S, pw, X, sw, sx, False).view(np.uint16), ref["y_bf16"])
+    assert np.array_equal(run_gemm(S, pw, X, sw, sx, True, p), ref["y_f32"])
+    assert np.array_equal(run_gemm(S, pw, X, sw, sx, False, p).view(np.uint16), ref["y_bf16"])
 
 
 @pytest.mark.parametrize("order", [0, 1, 2])
 @pytest.mark.parametrize("axis,M,N,K,db", [(0, 200, 1024, 512, 768), (1, 150, 2048, 1024, 768), (0, 97, 640, 384, 480)])
-def test_token_block_orders_exact(S, order, axis, M, N, K, db, monkeypatch):
+def test_token_block_orders_exact(S, order, axis, M, N, K, db):
     """The row-split kernel's orders of (row group, token block) workgroups: a grid of
     both, one dimension with a row group's token blocks adjacent, and one dimension with
     them on one XCD (the default where the row groups split evenly over 8): every output
@@ -540,8 +579,7 @@ def test_token_block_orders_exact(S, order, axis, M, N, K, db, monkeypatch):
     W, mask, X, sw, sx = gen.make_exact_int(17, M + N + order, M, N, K, gaxis(axis), db, gen.FP8)
     pw, (v, m, d) = compress_both(S, W, mask, FP8, axis, db)
     ref = oracle.spense_gemm(X, v, m, d, N, K, FP8, axis, db, sw, sx)
-    monkeypatch.setenv("SPENSE_BIG", "0")
-    monkeypatch.setenv("SPENSE_ROWS_ORDER", str(order))
+    p = S.plan_override(kernel=ROWS, block_order=order)
     for w in (pw, S.tile(pw)):
-        assert np.array_equal(run_gemm(S, w, X, sw, sx, True), ref["y_f32"])
-        assert np.array_equal(run_gemm(S, w, X, sw, sx, False).view(np.uint16), ref["y_bf16"])
+        assert np.array_equal(run_gemm(S, w, X, sw, sx, True, p), ref["y_f32"])
+        assert np.array_equal(run_gemm(S, w, X, sw, sx, False, p).view(np.uint16), ref["y_bf16"])
