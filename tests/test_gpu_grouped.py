@@ -116,6 +116,33 @@ def test_grouped_qkv_full_size(S):
         assert np.array_equal(y.view(torch.int16).cpu().numpy().view(np.uint16), ref["y_bf16"])
 
 
+@pytest.mark.timeout(400)
+@pytest.mark.parametrize("group", ["qkv", "gate_up"])
+def test_grouped_seed_oss_full_size_at_decode_m(S, group):
+    """The Seed-OSS-36B-like q (10240), k and v (1024 rows) or gate and up (27648 rows),
+    K = 5120, 25% dense rows each, grouped in one launch at M = 64, 16, 4 and 1 (the
+    benchmark's grouped layer timing): every output bit for bit, bf16 and fp32, on
+    exact-integer data.  The activations of a smaller M are the first rows of the M = 64
+    draw; each output row depends on its own row only."""
+    shapes = [(10240, 0.25), (1024, 0.25), (1024, 0.25)] if group == "qkv" else [(27648, 0.25), (27648, 0.25)]
+    K, Mmax = 5120, 64
+    ws, X, sx = weights(41 if group == "qkv" else 43, shapes, Mmax, K)
+    say(f"[grouped seed] {group}")
+    pws = [packed(S, W, mask, db) for (W, mask, sw, db) in ws]
+    sws = [tdev(sw) for (_, _, sw, _) in ws]
+    refs = []
+    for (W, mask, sw, db) in ws:
+        v, m, d, _ = oracle.compress(W, mask, FP8, 0, db)
+        refs.append(oracle.spense_gemm(X, v, m, d, W.shape[0], K, FP8, 0, db, sw, sx))
+    for M in (64, 16, 4, 1):
+        for out_f32 in (True, False):
+            ys = S.gemm_grouped(tdev(X[:M]), pws, sws, tdev(sx[:M]), out_f32=out_f32)
+            torch.cuda.synchronize()
+            for ref, y in zip(refs, ys):
+                got = y.cpu().numpy() if out_f32 else y.view(torch.int16).cpu().numpy().view(np.uint16)
+                assert np.array_equal(got, ref["y_f32" if out_f32 else "y_bf16"][:M]), f"{group} M={M}"
+
+
 def test_grouped_validates_arguments(S):
     M, K = 8, 256
     ws, X, sx = weights(3, [(64, 0.25), (32, 0.25)], M, K)

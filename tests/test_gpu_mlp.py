@@ -181,3 +181,29 @@ def test_mlp_block_matches_oracle(S, D, I, Ms, frac):
             rel = np.linalg.norm(y - yr) / max(np.linalg.norm(yr), 1e-30)
             assert rel <= 5e-3, rel
             assert np.abs(y - yr).max() <= 1e-2 * np.abs(yr).max()
+
+
+@pytest.mark.parametrize("which", ["gate", "up"])
+def test_mlp_with_one_of_the_two_scales(S, which):
+    """Gate and up of different geometry (other dense fractions), tiled, up to 64 tokens:
+    mlp() runs them as one grouped launch.  With only one of their per-row scales given,
+    the other weight is unscaled (1.0), as in the oracle; a dropped scale would change Y."""
+    D, I, M = 256, 512, 9
+    gate, gref, gsw = _packed(S, 63, "gate", I, D, gen.OUTPUT, 0.25)
+    up, uref, usw = _packed(S, 64, "up", I, D, gen.OUTPUT, 0.5)
+    down, dref, dsw = _packed(S, 65, "down", D, I, gen.INPUT, 0.25)
+    assert gate.dense_begin != up.dense_begin
+    if which == "gate":
+        gref, usw = gref[:7] + (None,), None
+    else:
+        uref, gsw = uref[:7] + (None,), None
+    X, sx = gen.make_x(63, 0, M, D, gen.FP8)
+    ref = oracle.mlp(X, sx, gref, uref, dref)
+    yr = oracle.decode_bf16(oracle.bf16_rne(ref["Y"].astype(np.float32))).astype(np.float64)
+    Y = S.mlp(torch.from_numpy(X).cuda(), torch.from_numpy(sx).cuda(), S.tile(gate), S.tile(up), S.tile(down),
+              gsw, usw, dsw)
+    torch.cuda.synchronize()
+    y = oracle.decode_bf16(Y.view(torch.int16).cpu().numpy().view(np.uint16)).astype(np.float64)
+    rel = np.linalg.norm(y - yr) / max(np.linalg.norm(yr), 1e-30)
+    assert rel <= 5e-3, rel
+    assert np.abs(y - yr).max() <= 1e-2 * np.abs(yr).max()
