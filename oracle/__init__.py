@@ -17,7 +17,9 @@ odd and even parts of SiLU, and the permutation invariance of Eq. (4); for the
 SpenseGPT+ index step: closed forms of the scores, the Wanda identity, brute-force TopK;
 for the SparseGPT sweep: the factor's rows against explicit inverse Hessians, Eq. (3)
 with an explicit inverse per step, the diagonal-Hessian case (magnitude pruning), the
-least-squares optimality of the dense buffer, and the edge cases).
+least-squares optimality of the dense buffer, and the edge cases; the reconstruction loss
+of Eq. (2) against an explicit calibration matrix; the MLP of Eq. (4) against a
+composition from numpy and torch's converters that shares none of this module's code).
 """
 from __future__ import annotations
 
@@ -80,8 +82,16 @@ def _L():
         lib.or_encode_e4m3fn_array.argtypes = [p, i64, p]
         lib.or_quantize_rows.argtypes = [p, i64, i64, i64, p, p]
         lib.or_glu_f64.argtypes = [p, p, i64, p]
+        lib.or_set_threads.restype = i32
+        lib.or_set_threads.argtypes = [i32]
         _lib = lib
     return _lib
+
+
+def set_threads(n: int) -> int:
+    """OpenMP threads of the oracle's parallel loops (0 keeps them); returns the previous
+    maximum.  Harness only: the results do not depend on it."""
+    return _L().or_set_threads(n)
 
 
 def _ptr(a):

@@ -30,9 +30,18 @@
  * Build: gcc -O2 -fopenmp -ffp-contract=off -fPIC -shared spense_oracle.c -o liboracle.so
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
+
+/* Harness only (no arithmetic): the number of OpenMP threads of the parallel loops below,
+ * for the benchmark's single-thread figure; returns the previous maximum. */
+int or_set_threads(int n) {
+  const int prev = omp_get_max_threads();
+  if (n > 0) omp_set_num_threads(n);
+  return prev;
+}
 
 #define OR_FP8 1  /* OCP fp8 e4m3fn: 1 sign, 4 exponent (bias 7), 3 mantissa bits */
 #define OR_BF16 2 /* bfloat16: the top 16 bits of an IEEE-754 binary32 */

@@ -501,6 +501,91 @@ def test_mlp_is_invariant_under_a_permutation_of_intermediate_indices():
     assert np.allclose(b["Y"], a["Y"], rtol=1e-5, atol=1e-6 * np.abs(a["Y"]).max())
 
 
+def _torch_decode_e4m3fn(codes):
+    """e4m3fn codes -> fp64 through torch's converter (independent of the oracle's decoder)."""
+    return torch.from_numpy(np.ascontiguousarray(codes)).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+
+
+def _independent_mlp(X, sx, Wg, sg, Wu, su, Wd, sd):
+    """Eq. (4) composed with numpy and torch only: inputs and weights decoded by torch,
+    G and U as fp64 matmuls of the scaled values, H = U * G / (1 + exp(-G)), its per-token
+    fp8 quantisation by torch's converter (the generator's), Y = (Hq sh) (Wd sd)^T in fp64.
+    Returns the pieces and, per output, sum |h w| * |sh sd| for the error bound."""
+    Xs = _torch_decode_e4m3fn(X) * sx.astype(np.float64)[:, None]
+    G = Xs @ (_torch_decode_e4m3fn(Wg) * sg.astype(np.float64)[:, None]).T
+    U = Xs @ (_torch_decode_e4m3fn(Wu) * su.astype(np.float64)[:, None]).T
+    H = U * G / (1.0 + np.exp(-G))
+    Hq, sh = gen.quantize_rows_fp8(H.astype(np.float32))
+    hd, wd = _torch_decode_e4m3fn(Hq), _torch_decode_e4m3fn(Wd)
+    scale = sh.astype(np.float64)[:, None] * sd.astype(np.float64)[None, :]
+    Y = (hd @ wd.T) * scale
+    absdot = (np.abs(hd) @ np.abs(wd).T) * np.abs(scale)
+    return {"G": G, "U": U, "H": H, "Hq": Hq, "sh": sh, "Y": Y, "absdot": absdot}
+
+
+def test_mlp_matches_an_independent_composition():
+    """Eq. (4) through the oracle (Spense-packed weights with 2:4 and dense regions)
+    against the same MLP composed with numpy and torch's converters from the decompressed
+    weights: G, U and H agree to fp64 rounding, the codes and token scales of H bit for
+    bit, and Y (fp32 sums, two fp32 scale roundings) is inside the Higham bound of the
+    fp64 Y.  The check tells the plausible mistakes apart: gate and up swapped, or the
+    down GEMM scaled by the input's token scales instead of H's, land far outside it."""
+    r = np.random.default_rng(25)
+    M, D, I = 5, 128, 192
+    X, sx = gen.quantize_rows_fp8(r.standard_normal((M, D)).astype(np.float32))
+    Wg, Wu, Wd = [(r.standard_normal(shape) * 0.05).astype(np.float32) for shape in ((I, D), (I, D), (D, I))]
+    dbg, dbd = 144, 160  # the last 48 rows of gate / up and the last 32 columns of down dense
+
+    def pack(Wf, axis, db):
+        q, s = gen.quantize_rows_fp8(Wf)
+        N, K = q.shape
+        mask = gen.magnitude_mask_24(Wf, gen.OUTPUT if axis == 0 else gen.INPUT, db)
+        v, m, d, bad = oracle.compress(q, mask, oracle.FP8, axis, db)
+        assert bad == 0
+        dense = np.where(mask.astype(bool), q, np.uint8(0))  # masked-out entries are +0
+        return (v, m, d, N, K, axis, db, s), dense, s
+
+    pg, qg, sg = pack(Wg, 0, dbg)
+    pu, qu, su = pack(Wu, 0, dbg)
+    pd, qd, sd = pack(Wd, 1, dbd)
+    o = oracle.mlp(X, sx, pg, pu, pd)
+    ind = _independent_mlp(X, sx, qg, sg, qu, su, qd, sd)
+    for k in ("G", "U", "H"):
+        assert np.allclose(o[k], ind[k], rtol=1e-12, atol=1e-14 * np.abs(ind[k]).max()), k
+    assert np.array_equal(o["Hq"], ind["Hq"]) and np.array_equal(o["sh"].view(np.uint32), ind["sh"].view(np.uint32))
+    gamma = I * 2.0 ** -24 / (1 - I * 2.0 ** -24)
+    bound = 2 * gamma * ind["absdot"] + 4 * 2.0 ** -24 * np.abs(ind["Y"]) + 1e-30
+    assert np.all(np.abs(o["Y"].astype(np.float64) - ind["Y"]) <= bound)
+    # sensitivity of the check: two plausible mistakes fall outside the same bound
+    swapped = _independent_mlp(X, sx, qu, su, qg, sg, qd, sd)["Y"]
+    assert np.abs(o["Y"] - swapped).max() > 100 * bound.max()
+    wrong_scale = ind["Y"] / ind["sh"].astype(np.float64)[:, None] * sx.astype(np.float64)[:, None]
+    assert np.abs(o["Y"] - wrong_scale).max() > 100 * bound.max()
+
+
+def test_reconstruction_loss_is_eq2_with_explicit_activations():
+    """Eq. (2) evaluated from an explicit calibration matrix X, ||X W^T - X W_hat^T||_F^2,
+    equals the oracle's form through H = X^T X; zero for W_hat = W; a single changed
+    weight w[n, k] -> w[n, k] + d costs d^2 ||X[:, k]||^2; losses of disjoint row sets add."""
+    r = np.random.default_rng(26)
+    n, N, K = 300, 12, 40
+    X = r.standard_normal((n, K)) * np.exp(r.uniform(-1, 1, K))[None, :]
+    W = r.standard_normal((N, K))
+    W_hat = W * (r.random((N, K)) > 0.5)
+    H = X.T @ X
+    want = float(np.sum((X @ W.T - X @ W_hat.T) ** 2))
+    assert abs(oracle.reconstruction_loss(W, W_hat, H) - want) <= 1e-10 * want
+    assert oracle.reconstruction_loss(W, W, H) == 0.0
+    W2 = W.copy()
+    W2[3, 7] += 0.25
+    assert np.isclose(oracle.reconstruction_loss(W, W2, H), 0.0625 * np.sum(X[:, 7] ** 2), rtol=1e-12, atol=0)
+    a, b = oracle.reconstruction_loss(W[:5], W_hat[:5], H), oracle.reconstruction_loss(W[5:], W_hat[5:], H)
+    assert np.isclose(a + b, want, rtol=1e-12, atol=0)
+    # transposing W (an N x K vs K x N mix-up) is caught: the shapes no longer fit H
+    with pytest.raises(ValueError):
+        oracle.reconstruction_loss(W.T, W_hat.T, H)
+
+
 # ------------------------------------------------------------------ dense-index selection (sec. 3.3.1)
 def test_index_scores_closed_forms():
     I, D = 6, 8
