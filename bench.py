@@ -104,14 +104,26 @@ def time_launches(fn, steps, warmup, torch):
     return t0.elapsed_time(t1) / steps
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(mx, Wcodes_dense, X, sx, M):
     """The oracle (plain C, OpenMP, never tuned) on a bounded sample of the same GEMM:
     the whole M x N x K product repeated for about 10 s (median run), or a slice of the
-    weight rows extrapolated linearly when one full run would take longer than 20 s."""
+    weight rows extrapolated linearly when one full run would take longer than 20 s; then
+    the same with one thread on a slice of 1024 weight rows (median of 3, extrapolated)."""
     import statistics
 
     import oracle
-    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    threads = oracle.set_threads(0)  # the OpenMP threads the oracle's loops use
     t = time.perf_counter()
     oracle.gemm(X, Wcodes_dense[:256], oracle.FP8, mx.sw[:256], sx)
     est_full = (time.perf_counter() - t) * N / 256
@@ -133,8 +145,23 @@ def cpu_baseline(mx, Wcodes_dense, X, sx, M):
         dt = time.perf_counter() - t
         full_s = dt * N / rows
         sample = f"oracle fp32 GEMM over {rows} of {N} weight rows at M={M}, {dt:.1f} s, extrapolated linearly"
+    # one thread, a slice of the weight rows, extrapolated to the whole weight
+    rows1 = 1024
+    prev = oracle.set_threads(1)
+    try:
+        runs1 = []
+        for _ in range(3):
+            t = time.perf_counter()
+            oracle.gemm(X, Wcodes_dense[:rows1], oracle.FP8, mx.sw[:rows1], sx)
+            runs1.append(time.perf_counter() - t)
+    finally:
+        oracle.set_threads(prev)
+    one_s = statistics.median(runs1) * N / rows1
     return {"value": round(b / full_s / 1e9, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
-            "sample": sample, "seconds_per_gemm": round(full_s, 4)}
+            "sample": sample, "seconds_per_gemm": round(full_s, 4), "cpu_model": cpu_model(),
+            "single_thread": {"value": round(b / one_s / 1e9, 4), "unit": "GB/s", "seconds_per_gemm": round(one_s, 3),
+                              "sample": f"{rows1} of {N} weight rows at M={M}, one thread, median of 3, "
+                                        f"extrapolated linearly"}}
 
 
 def measure_extras(args, torch, gen, S, ws, pws, copies, swd, mx, dws, dense_copies, results):
@@ -601,8 +628,13 @@ def main():
     results = {}
     ws = S.Workspace("cuda")
     ms_list = [args.profile_m] if args.profile_m else ([M_MAIN] if args.only_main else M_SWEEP)
+    # sha256 of every generated input of the main workload (weight codes, 2:4 mask, scales,
+    # and each M's activation codes and token scales)
+    hashes = {"W_codes": gen.sha256(mx.W), "mask": gen.sha256(mx.mask), "w_scale": gen.sha256(mx.sw)}
     for M in ms_list:
         X, sx = gen.make_x(2, 0, M, K, gen.FP8, "normal")
+        hashes[f"X_m{M}"] = gen.sha256(X)
+        hashes[f"x_scale_m{M}"] = gen.sha256(sx)
         Xd, sxd = torch.from_numpy(X).cuda(), torch.from_numpy(sx).cuda()
         Y = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
 
@@ -675,6 +707,7 @@ def main():
                      "kernel": "spense_gemm_rows_kernel (fp8, tiled layout; 2:4 smfmac + dense mfma, "
                                "activations staged in LDS, one launch)"},
         "sweep": [results[m] for m in ms_list],
+        "inputs_sha256": hashes,
     }
     out.update(extras)
     if not args.skip_cpu:
