@@ -40,7 +40,7 @@
 extern "C" {
 #endif
 
-#define SPENSE_ABI_VERSION 9
+#define SPENSE_ABI_VERSION 10
 
 typedef enum spense_status {
   SPENSE_OK = 0,
@@ -227,6 +227,25 @@ size_t spense_gemm_workspace_size(int64_t M, const spense_packed_t* packed);
 int spense_gemm(const void* X, int64_t M, int64_t ldx, const spense_packed_t* packed, const float* w_scale,
                 const float* x_scale, void* Y, int64_t ldy, uint32_t out_flags, void* ws, size_t ws_bytes,
                 hipStream_t stream);
+
+/* Scratch that spense_gemm_noalloc holds on each device it runs on (16 MiB). */
+#define SPENSE_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+
+/*
+ * spense_gemm for callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops and harnesses that forbid allocation): the same arguments
+ * without the workspace, the same plan and kernels, results bit for bit equal to
+ * spense_gemm's.  The fp32 partial sums of K-sliced plans go to a scratch array of
+ * SPENSE_NOALLOC_SCRATCH_BYTES that the library keeps on each device it runs on until the
+ * process ends (the current plans need at most 4 slices x 64 tokens x fewer than 8192 rows x 4
+ * bytes, under 8.4 MB).  Every call on a device shares that array, which keeps the last call's
+ * partial sums (each call writes every partial it reads): calls that overlap on one
+ * device, from any stream or thread, race and must be serialised by the caller.
+ * SPENSE_ERR_WS if the plan would need more scratch than the array holds.  No hipMalloc,
+ * hipFree or other allocation on any path.  Errors otherwise as spense_gemm.
+ */
+int spense_gemm_noalloc(const void* X, int64_t M, int64_t ldx, const spense_packed_t* packed, const float* w_scale,
+                        const float* x_scale, void* Y, int64_t ldy, uint32_t out_flags, hipStream_t stream);
 
 /*
  * Parts of spense_gemm's execution plan forced by the caller, for tests that check every

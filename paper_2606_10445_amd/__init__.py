@@ -37,6 +37,7 @@ SPENSE_OUT_BF16 = 0
 SPENSE_OUT_F32 = 1
 SPENSE_LAYOUT_ROWMAJOR = 0
 SPENSE_LAYOUT_TILED = 1
+SPENSE_NOALLOC_SCRATCH_BYTES = 16 << 20
 
 EXPORTS = ["spense_abi_version", "spense_last_error", "spense_layout", "spense_tiled_layout",
            "spense_compress_workspace_size", "spense_compress", "spense_decompress", "spense_tile",
@@ -45,7 +46,7 @@ EXPORTS = ["spense_abi_version", "spense_last_error", "spense_layout", "spense_t
            "spense_gather_rows", "spense_gather_cols", "spense_obs_factor_workspace_size", "spense_obs_factor",
            "spense_obs_prune_workspace_size", "spense_obs_prune_24", "spense_gemm_grouped", "spense_gemm_glu",
            "spense_gemm_glu_fp8_workspace_size", "spense_gemm_glu_fp8", "spense_gemm_planned_workspace_size",
-           "spense_gemm_planned"]
+           "spense_gemm_planned", "spense_gemm_noalloc"]
 
 
 class SpenseError(RuntimeError):
@@ -129,6 +130,7 @@ def _load():
         "spense_gemm_glu_fp8_workspace_size": (ctypes.c_size_t, [i64, i64]),
         "spense_gemm_glu_fp8": (ctypes.c_int, [p, i64, i64, p, p, p, p, p, p, i64, p, p, ctypes.c_size_t, p]),
         "spense_gemm_planned_workspace_size": (sz, [i64, P(spense_packed_t), P(spense_plan_override_t)]),
+        "spense_gemm_noalloc": (ctypes.c_int, [p, i64, i64, P(spense_packed_t), p, p, p, i64, u32, p]),
         "spense_gemm_planned": (ctypes.c_int, [p, i64, i64, P(spense_packed_t), p, p, p, i64, u32, p, sz,
                                                P(spense_plan_override_t), p]),
     }
@@ -205,6 +207,10 @@ def spense_gemm_planned(X, M, ldx, packed: spense_packed_t, w_scale, x_scale, Y,
                         stream) -> int:
     return _lib.spense_gemm_planned(X, M, ldx, ctypes.byref(packed), w_scale, x_scale, Y, ldy, out_flags, ws,
                                     ws_bytes, None if plan is None else ctypes.byref(plan), stream)
+
+
+def spense_gemm_noalloc(X, M, ldx, packed: spense_packed_t, w_scale, x_scale, Y, ldy, out_flags, stream) -> int:
+    return _lib.spense_gemm_noalloc(X, M, ldx, ctypes.byref(packed), w_scale, x_scale, Y, ldy, out_flags, stream)
 
 
 def spense_dense_gemm_workspace_size(M: int, N: int, K: int, dtype: int) -> int:
@@ -464,6 +470,22 @@ def gemm(X: torch.Tensor, pw: PackedWeight, w_scale=None, x_scale=None, out=None
         wp, wn = ws.get(spense_gemm_planned_workspace_size(M, pw.desc, plan))
         _check(spense_gemm_planned(_ptr(X), M, X.stride(0), pw.desc, _ptr(w_scale), _ptr(x_scale), _ptr(out),
                                    out.stride(0), flags, wp, wn, plan, _stream(X.device)))
+    return out
+
+
+def gemm_noalloc(X: torch.Tensor, pw: PackedWeight, w_scale=None, x_scale=None, out=None,
+                 out_f32=False) -> torch.Tensor:
+    """Y = X W^T through spense_gemm_noalloc: spense_gemm with the K-slice partial sums in
+    the library's per-device scratch instead of a workspace (for callers that cannot
+    allocate; calls that overlap on one device race).  ``out`` should be given by such
+    callers, since allocating it here would defeat the purpose."""
+    _check_x(X, pw.dtype, pw.K)
+    M = X.shape[0]
+    _check_scale(w_scale, pw.N, X.device, "w_scale")
+    _check_scale(x_scale, M, X.device, "x_scale")
+    out = _out(out, M, pw.N, out_f32, X.device)
+    _check(spense_gemm_noalloc(_ptr(X), M, X.stride(0), pw.desc, _ptr(w_scale), _ptr(x_scale), _ptr(out),
+                               out.stride(0), SPENSE_OUT_F32 if out_f32 else SPENSE_OUT_BF16, _stream(X.device)))
     return out
 
 

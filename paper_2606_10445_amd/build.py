@@ -13,7 +13,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libspense.so")
-SOURCES = ["spense_api.cpp", "spense_gemm.hip", "spense_compress.hip", "spense_quant.hip", "spense_index.hip", "spense_obs.hip"]
+SOURCES = ["spense_api.cpp", "spense_gemm.hip", "spense_compress.hip", "spense_quant.hip", "spense_index.hip", "spense_obs.hip",
+           "spense_noalloc.hip"]
 ARCH = "gfx950"
 
 # -packed-fp32-ops: keep the compiler from forming packed fp32 VALU instructions.

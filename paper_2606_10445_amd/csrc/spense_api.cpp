@@ -10,27 +10,30 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
-#include <string>
 
 #include "../../include/spense.h"
 #include "spense_internal.h"
 
 namespace {
 
-thread_local std::string g_err;
+// The last error message of this thread (a fixed buffer: no call allocates host memory).
+thread_local char g_err[512];
+
+int vfail(int code, const char* fmt, va_list ap) {
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  return code;
+}
 
 int fail(int code, const char* fmt, ...) {
-  char buf[512];
   va_list ap;
   va_start(ap, fmt);
-  vsnprintf(buf, sizeof buf, fmt, ap);
+  vfail(code, fmt, ap);
   va_end(ap);
-  g_err = buf;
   return code;
 }
 
 int ok() {
-  g_err.clear();
+  g_err[0] = '\0';
   return SPENSE_OK;
 }
 
@@ -754,11 +757,21 @@ int64_t glu_hmax_offset(int64_t M, int64_t N) { return (M * glu_ldh(N) * 4 + 255
 
 }  // namespace
 
+namespace spense {
+int api_fail(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vfail(code, fmt, ap);
+  va_end(ap);
+  return code;
+}
+}  // namespace spense
+
 extern "C" {
 
 int spense_abi_version(void) { return SPENSE_ABI_VERSION; }
 
-const char* spense_last_error(void) { return g_err.c_str(); }
+const char* spense_last_error(void) { return g_err; }
 
 int spense_quantize_fp8(const void* src, int32_t src_type, int64_t M, int64_t K, int64_t ld_src, uint8_t* q,
                         int64_t ldq, float* scales, hipStream_t stream) {

@@ -105,6 +105,9 @@ struct LaunchShape {
 
 hipError_t launch_gemm(int dtype, const LaunchShape& ls, const GemmArgs& a, hipStream_t s);
 
+// Record an error message for spense_last_error (printf format) and return code.
+int api_fail(int code, const char* fmt, ...);
+
 // Y for the rows of K-sliced regions: the sum of their fp32 partials in slice order, then
 // the epilogue (after launch_gemm, on the same stream).
 hipError_t launch_splitk_reduce(const GemmArgs& a, hipStream_t s);
