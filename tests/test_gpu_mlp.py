@@ -193,10 +193,10 @@ def test_mlp_with_one_of_the_two_scales(S, which):
     up, uref, usw = _packed(S, 64, "up", I, D, gen.OUTPUT, 0.5)
     down, dref, dsw = _packed(S, 65, "down", D, I, gen.INPUT, 0.25)
     assert gate.dense_begin != up.dense_begin
-    if which == "gate":
-        gref, usw = gref[:7] + (None,), None
+    if which == "gate":  # only gate's scale given: up is unscaled on both sides
+        uref, usw = uref[:7] + (None,), None
     else:
-        uref, gsw = uref[:7] + (None,), None
+        gref, gsw = gref[:7] + (None,), None
     X, sx = gen.make_x(63, 0, M, D, gen.FP8)
     ref = oracle.mlp(X, sx, gref, uref, dref)
     yr = oracle.decode_bf16(oracle.bf16_rne(ref["Y"].astype(np.float32))).astype(np.float64)
