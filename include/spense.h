@@ -257,12 +257,14 @@ int spense_gemm_noalloc(const void* X, int64_t M, int64_t ldx, const spense_pack
 typedef struct spense_plan_override_t {
   int32_t kernel;           /* 0 planner; 1 K split over a workgroup's waves (row-major
                                layout only); 2 rows split, activations staged in LDS;
-                               3 large-M tiles (fp8 only) */
+                               3 large-M tiles of 128 rows x 256 tokens; 4 large-M tiles
+                               of 256 x 256 (tiled layout; a row-major weight runs 3)
+                               (3 and 4 fp8 only) */
   int32_t row_tiles;        /* K-split kernel: 16-row tiles per workgroup (1, 2, 4); with
                                kernel 2: 1 or 2 (with 4 waves) */
   int32_t waves;            /* K-split kernel: 4, 8 or 16 waves per workgroup (row_tiles
                                1 allows all three, 2 allows 4 and 8, 4 allows 4); row-split:
-                               4 or 8; large-M: 4 or 8 */
+                               4 or 8; kernel 3: 4 or 8; kernel 4: 8 */
   int32_t act_tiles;        /* at most this many 16-token activation tiles per token block
                                (1 or 2) */
   int32_t ksplit;           /* row-split kernel: K slices, 1 .. 8 (capped at the chunk count) */

@@ -205,9 +205,9 @@ int read_override(const spense_plan_override_t* ov, int32_t dtype, bool tiled, O
   o->order = ov->block_order;
   o->xcd = ov->xcd_order;
   o->u8 = ov->u8;
-  if (o->kernel < 0 || o->kernel > 3) return fail(SPENSE_ERR_ARG, "plan: unknown kernel %d", o->kernel);
+  if (o->kernel < 0 || o->kernel > 4) return fail(SPENSE_ERR_ARG, "plan: unknown kernel %d", o->kernel);
   if (o->kernel == 1 && tiled) return fail(SPENSE_ERR_ARG, "plan: the K-split kernel reads the row-major layout only");
-  if (o->kernel == 3 && dtype != SPENSE_FP8_E4M3FN) return fail(SPENSE_ERR_ARG, "plan: the large-M kernel is fp8 only");
+  if (o->kernel >= 3 && dtype != SPENSE_FP8_E4M3FN) return fail(SPENSE_ERR_ARG, "plan: the large-M kernels are fp8 only");
   if (o->ct < 0 || o->ct > 2) return fail(SPENSE_ERR_ARG, "plan: act_tiles %d (0, 1 or 2)", o->ct);
   if (o->ksplit < 0 || o->ksplit > 8) return fail(SPENSE_ERR_ARG, "plan: ksplit %d outside [0, 8]", o->ksplit);
   for (int w : {o->wused, o->wused_d, o->wused_s})
@@ -223,6 +223,8 @@ int read_override(const spense_plan_override_t* ov, int32_t dtype, bool tiled, O
       okshape = (o->rt == 1 && (o->waves == 4 || o->waves == 8)) || (o->rt == 2 && o->waves == 4);
     } else if (o->kernel == 3) {
       okshape = o->rt == 0 && (o->waves == 4 || o->waves == 8);
+    } else if (o->kernel == 4) {
+      okshape = o->rt == 0 && o->waves == 8;
     }
     if (!okshape)
       return fail(SPENSE_ERR_ARG, "plan: no kernel %d built for %d row tiles x %d waves", o->kernel, o->rt, o->waves);
@@ -408,7 +410,7 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
     rt = 1;
     waves = 8;
   }
-  if (ov.rt && ov.kernel != 3) {  // a shape checked against the kernel's list
+  if (ov.rt && ov.kernel < 3) {  // a shape checked against the kernel's list
     rt = ov.rt;
     waves = ov.waves;
   }
@@ -423,11 +425,24 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
   // and down at M = 1024: 60 vs 97 and 156 vs 265 us); with fewer (q below 512 tokens, o
   // and down below 1024), the row-split kernel's finer grid keeps more CUs busy.
   int big = (dtype == SPENSE_FP8_E4M3FN && M >= kBigMinM && ceil_div(N, 128) * ceil_div(M, 256) >= kBigMinTiles) ? 1 : 0;
+  // 256-row x 256-token tiles (tiled weights) once that grid has at least 160 workgroups:
+  // measured on MI355X (us, 128 x 256 tiles -> 256 x 256): gate / up at M = 1024 / 2048
+  // 177 / 312 -> 159 / 291, Seed-OSS gate 178 / 316 -> 168 / 290, down and o at M = 2048
+  // (160 workgroups) 313 -> 267 and 120 -> 100, q at M = 2048 95 -> 91; with fewer
+  // workgroups it loses (q at M = 1024, 128 workgroups: 49 -> 84; down at M = 1024, 80: 159
+  // -> 279); gate / up at M = 512 (200) is even.
+  if (big && tiled) {
+    const int64_t rb256 = split == SPENSE_SPLIT_OUTPUT
+                              ? ceil_div(dense_begin, 256) + ceil_div(N - dense_begin, 256)
+                              : ceil_div(N, 256);
+    if (rb256 * ceil_div(M, 256) >= 160) big = 2;
+  }
   if (ov.kernel == 1 || ov.kernel == 2) big = 0;
   if (ov.kernel == 3) big = 1;  // fp8 (checked by read_override)
+  if (ov.kernel == 4) big = tiled ? 2 : 1;  // the 256 x 256 kernel reads the tiled layout
   pl->ls.big = big;
-  const int big_rows = 128;  // rows of a large-M workgroup tile
-  if (big) pl->ls.waves = ov.waves == 4 ? 4 : 8;
+  const int big_rows = big == 2 ? 256 : 128;  // rows of a large-M workgroup tile
+  if (big) pl->ls.waves = (big == 1 && ov.waves == 4) ? 4 : 8;
   const int64_t tblocks = ceil_div(M, 256);
 
   Region regs[2];

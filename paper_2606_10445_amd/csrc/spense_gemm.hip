@@ -1348,33 +1348,236 @@ __global__ __launch_bounds__(64 * WV) void spense_gemm_big_kernel(GemmArgs a) {
     }
 }
 
-// The large-M kernel's dynamic LDS above the default limit is a per-device function
+// ---------------------------------------------------------------- large-M kernel, 256 x 256 tiles
+// Both operands through LDS as in spense_gemm_big_kernel, with twice the rows per
+// workgroup and per wave: a workgroup computes 256 weight rows x 256 tokens, its 8 waves a
+// grid of 2 row halves x 4 token quarters, each wave 128 rows (8 row tiles) x 64 tokens (4
+// token tiles, 128 accumulators).  Each B fragment read from LDS feeds 8 MMAs, each A
+// fragment 4.  Tiled weight layout only.
+//
+// The CU's load path moves about 57 bytes per clock from L2 with 16-byte-per-lane loads,
+// into registers or straight into LDS alike, but a load instruction costs at least ~18
+// clocks however few bytes it moves (a 4-byte-per-lane load moves 256 bytes in ~32; all
+// measured on MI355X).  So every load here moves 1 KB: per 128-column step a wave issues 4
+// activation blocks and, for its 2 row tiles, the 2:4 value blocks (the metadata of a whole
+// 512-column chunk, 1 KB per tile, once every 4 steps into its own LDS area) or both
+// dense halves, and nothing else: 6.5 loads per 2:4 step (52 KB per workgroup, ~0.95k
+// clocks) against ~1.07k clocks of its 256 MMAs.  Two loads follow each of the first four
+// groups of 4 MMAs, so that they land before the next barrier.
+// The per-lane offsets are loop-invariant; the step's offset travels in the scalar offset.
+// LDS: two stages of activations (32 KB) and weights (32 KB), two chunk metadata areas
+// (16 KB): 160 KB.  The barrier at the start of a step waits for this wave's loads of the
+// step (issued during the previous one) and for its LDS reads of the previous step.
+constexpr int kB2Rows = 256, kB2Tokens = 256, kB2RowTiles = 16;
+constexpr int kB2XSlot = kB2Tokens * 128;     // activations of one step
+constexpr int kB2WSlot = kB2RowTiles * 2048;  // weights of one step: 2:4 values or both dense halves per row tile
+constexpr int kB2MSlot = kB2RowTiles * 1024;  // 2:4 metadata of one 512-column chunk
+constexpr int kB2Lds = 2 * (kB2XSlot + kB2WSlot + kB2MSlot);
+
+__global__ __launch_bounds__(512) void spense_gemm_big2_kernel(GemmArgs a) {
+  constexpr int WV = 8, NT = kB2RowTiles, RPW = 8, TC = 4;
+  constexpr int TU = NT / WV;                // row tiles whose weights a wave copies
+  constexpr int XI = kB2XSlot / 1024 / WV;  // 1 KB activation blocks per wave per step
+  static_assert(XI + 2 * TU == RPW, "eight loads per step");
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int li = lane & 15, lq = lane >> 4;
+  const int wr = wave & 1, wc = wave >> 1;
+  int g = blockIdx.x;
+  if (a.xgt > 0) {  // XCD-aware order, as in spense_gemm_big_kernel
+    const int T = a.tblocks, GT = a.xgt, RC = a.xrc, TGc = T / GT;
+    const int x = g & 7, l = g >> 3, tg = x % TGc, rc = x / TGc;
+    g = ((l / GT) * RC + rc) * T + tg * GT + l % GT;
+  }
+  const int ri = (a.nreg > 1 && g >= a.reg[1].wg0) ? 1 : 0;
+  const Region& R = a.reg[ri];
+  const int rowend = R.row0 + R.rows;
+  const int rb = (g - R.wg0) / a.tblocks, tb = (g - R.wg0) % a.tblocks;
+  const int rblk = R.row0 + rb * kB2Rows;
+  const int m0 = tb * kB2Tokens;
+  const int K = R.kend, kbound = R.kbound;
+
+  extern __shared__ __attribute__((aligned(1024))) uint8_t big_lds[];
+  uint8_t* const xarea = big_lds;
+  uint8_t* const warea = big_lds + 2 * kB2XSlot;
+  uint8_t* const marea = big_lds + 2 * (kB2XSlot + kB2WSlot);
+  const __amdgpu_buffer_rsrc_t rx = rsrc(a.X, a.x_bytes), rv = rsrc(a.values, a.v_bytes),
+                               rm = rsrc(a.meta, a.m_bytes), rd = rsrc(a.dense, a.d_bytes);
+  v4f acc[RPW][TC];
+#pragma unroll
+  for (int t = 0; t < RPW; ++t)
+#pragma unroll
+    for (int c = 0; c < TC; ++c) acc[t][c] = (v4f){0.f, 0.f, 0.f, 0.f};
+
+  const int n_sp = (kbound + 127) / 128, n_de = (K - kbound + 127) / 128, nst = n_sp + n_de;
+  const int nch_sp = (n_sp + 3) / 4, nch_de = (n_de + 3) / 4;
+
+  // loop-invariant per-lane offsets (kOOB for rows past M or row tiles past the region)
+  uint32_t xo[XI];
+  int xb[XI];  // the column (bytes) of this lane's 16-byte block inside the step
+#pragma unroll
+  for (int i = 0; i < XI; ++i) {
+    const int blk = wave * XI + i;
+    const int r = 8 * blk + (lane >> 3), b = (lane & 7) ^ ((r >> 1) & 7);
+    const int m = m0 + r;
+    xb[i] = 16 * b;
+    xo[i] = m < a.M ? (uint32_t)((int64_t)m * a.ldx_b + 16 * b) : kOOB;
+  }
+  uint32_t vo[TU], mo[TU], dlo[TU];
+#pragma unroll
+  for (int u = 0; u < TU; ++u) {
+    const int r0 = rblk + 16 * (TU * wave + u);
+    const bool ok = r0 < rowend;
+    const uint32_t ts = (uint32_t)(r0 / 16);
+    vo[u] = ok ? ts * (uint32_t)nch_sp * 4096u + 16u * lane : kOOB;
+    mo[u] = ok ? ts * (uint32_t)nch_sp * 1024u + 16u * lane : kOOB;
+    dlo[u] = ok && r0 >= R.dense_row_off ? (uint32_t)((r0 - R.dense_row_off) / 16) * (uint32_t)nch_de * 8192u + 16u * lane
+                                          : kOOB;
+  }
+
+  // Load j (0 .. 7) of this wave for step sn: activation blocks 0-3, then per row tile the
+  // 2:4 value block (j = 4, 5) and, at a chunk's first step, its metadata block (j = 6,
+  // 7); or both dense halves.  Nothing past the last step.
+  auto load_j = [&](auto j_const, int sn) __attribute__((always_inline)) {
+    constexpr int j = decltype(j_const)::value;
+    if (sn >= nst) return;  // uniform
+    const bool sp = sn < n_sp;
+    if constexpr (j < XI) {
+      const int ks = sp ? 128 * sn : kbound + 128 * (sn - n_sp);
+      const int ke = sp ? kbound : K;
+      uint32_t off = xo[j];
+      if (ks + 128 > ke) off = ks + xb[j] < ke ? off : kOOB;  // the region's last, partial step
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rx, (__attribute__((address_space(3))) void*)(xarea + (sn & 1) * kB2XSlot + (wave * XI + j) * 1024), 16, off,
+          ks, 0, 0);
+    } else {
+      constexpr int u = (j - XI) % TU, half = (j - XI) / TU;
+      const int tile = TU * wave + u;
+      uint8_t* const wdst = warea + (sn & 1) * kB2WSlot + tile * 2048;
+      if (sp) {
+        const int cs = sn >> 2, js = sn & 3;
+        if constexpr (half == 0) {
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (__attribute__((address_space(3))) void*)wdst, 16, vo[u],
+                                                   cs * 4096 + 1024 * js, 0, kTiledNT);
+        } else {
+          if (js == 0)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                rm, (__attribute__((address_space(3))) void*)(marea + (cs & 1) * kB2MSlot + tile * 1024), 16, mo[u],
+                cs * 1024, 0, kTiledNT);
+        }
+      } else {
+        const int sd = sn - n_sp, cd = sd >> 2, jd = sd & 3;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rd, (__attribute__((address_space(3))) void*)(wdst + 1024 * half), 16,
+                                                 dlo[u], cd * 8192 + 2048 * jd + 1024 * half, 0, kTiledNT);
+      }
+    }
+  };
+
+  // One step: after the barrier, the B fragments of the wave's 4 token tiles and the A
+  // fragment of its first row tile; then per row tile t the A fragment of tile t + 1 is
+  // read (other register set) before the 4 MMAs of tile t; loads 2t and 2t + 1 of step
+  // s + 1 follow the first four groups.
+  auto step = [&](auto kind_const, int s) __attribute__((always_inline)) {
+    constexpr bool SPARSE = decltype(kind_const)::value == kStepSparse;
+    const uint8_t* xs = xarea + (s & 1) * kB2XSlot;
+    const uint8_t* wl = warea + (s & 1) * kB2WSlot + (RPW * wr) * 2048 + 16 * lane;
+    const uint8_t* ml = marea + ((s >> 2) & 1) * kB2MSlot + (RPW * wr) * 1024 + 256 * (s & 3) + 16 * li + 4 * lq;
+    barrier_vm_lgkm0<0>();
+    v8i bq[TC];
+#pragma unroll
+    for (int c = 0; c < TC; ++c) {
+      const int r = 16 * (TC * wc + c) + li;
+      bq[c] = cat8(*reinterpret_cast<const v4i*>(xs + r * 128 + ((lq ^ ((r >> 1) & 7)) << 4)),
+                   *reinterpret_cast<const v4i*>(xs + r * 128 + (((4 + lq) ^ ((r >> 1) & 7)) << 4)));
+    }
+    v4i alo[2], ahi[2];
+    int aix[2];
+    auto read_a = [&](int t, int q) __attribute__((always_inline)) {
+      alo[q] = *reinterpret_cast<const v4i*>(wl + t * 2048);
+      if constexpr (SPARSE)
+        aix[q] = *reinterpret_cast<const int*>(ml + t * 1024);
+      else
+        ahi[q] = *reinterpret_cast<const v4i*>(wl + t * 2048 + 1024);
+    };
+    read_a(0, 0);
+    static_for<RPW>([&](auto t_const) {
+      constexpr int t = decltype(t_const)::value;
+      constexpr int q = t & 1;
+      if constexpr (t + 1 < RPW) read_a(t + 1, 1 - q);
+#pragma unroll
+      for (int c = 0; c < TC; ++c) {
+        if constexpr (SPARSE)
+          acc[t][c] = mma_sparse(alo[q], bq[c], acc[t][c], aix[q], std::integral_constant<int, kFP8>());
+        else
+          acc[t][c] = mma_dense(cat8(alo[q], ahi[q]), bq[c], acc[t][c], std::integral_constant<int, kFP8>());
+      }
+      if constexpr (2 * t + 1 < RPW) {  // two loads after each of the first four groups
+        load_j(std::integral_constant<int, 2 * t>(), s + 1);
+        load_j(std::integral_constant<int, 2 * t + 1>(), s + 1);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    });
+  };
+
+  static_for<RPW>([&](auto j_const) { load_j(j_const, 0); });  // step 0
+  const std::integral_constant<int, kStepSparse> SP;
+  const std::integral_constant<int, kStepDense> DE;
+  int s = 0;
+  for (; s < n_sp; ++s) step(SP, s);
+  xdl_fence();
+  for (; s < nst; ++s) step(DE, s);
+  xdl_fence();
+#pragma unroll
+  for (int t = 0; t < RPW; ++t)
+#pragma unroll
+    for (int c = 0; c < TC; ++c) {
+      const int m = m0 + 16 * (TC * wc + c) + li;
+      const int n0 = rblk + 16 * (RPW * wr + t) + 4 * lq;
+      if (m < a.M && n0 < rowend) store4(a, acc[t][c], m, n0, rowend);
+    }
+}
+
+// The large-M kernels' dynamic LDS above the default limit is a per-device function
 // attribute: set once per (device, kernel instance), under std::call_once, so that host
 // threads making their first large-M call together do not race.
 constexpr int kMaxDevices = 64;
-std::once_flag g_big_lds_once[kMaxDevices][2][2];
-hipError_t g_big_lds_rc[kMaxDevices][2][2];
+std::once_flag g_big_lds_once[kMaxDevices][2][3];  // [device][tiled][kernel instance]
+hipError_t g_big_lds_rc[kMaxDevices][2][3];
+
+template <typename KernelT>
+hipError_t set_big_lds(KernelT k, int tiled, int which, int lds) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::call_once(g_big_lds_once[dev][tiled][which], [&] {
+    g_big_lds_rc[dev][tiled][which] =
+        hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  });
+  return g_big_lds_rc[dev][tiled][which];
+}
+
+hipError_t launch_big2(const GemmArgs& a, hipStream_t s) {
+  static_assert(kB2Lds <= 160 * 1024, "LDS of a CU");
+  if (!a.tiled) return hipErrorInvalidValue;  // the planner sends row-major weights to the 128 x 256 kernel
+  hipError_t e = set_big_lds(spense_gemm_big2_kernel, 1, 2, kB2Lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(spense_gemm_big2_kernel, dim3(a.groups), dim3(512), kB2Lds, s, a);
+  return hipGetLastError();
+}
 
 template <int WV>
 hipError_t launch_big_wv(const GemmArgs& a, hipStream_t s) {
   constexpr int lds = 3 * BigStage::BYTES;
   static_assert(lds <= 160 * 1024, "LDS of a CU");
   auto k = a.tiled ? spense_gemm_big_kernel<true, WV> : spense_gemm_big_kernel<false, WV>;
-  int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
+  hipError_t e = set_big_lds(k, a.tiled ? 1 : 0, WV == 8 ? 1 : 0, lds);
   if (e != hipSuccess) return e;
-  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
-  const int t = a.tiled ? 1 : 0, w = WV == 8 ? 1 : 0;
-  std::call_once(g_big_lds_once[dev][t][w], [&] {
-    g_big_lds_rc[dev][t][w] =
-        hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize, lds);
-  });
-  if (g_big_lds_rc[dev][t][w] != hipSuccess) return g_big_lds_rc[dev][t][w];
   hipLaunchKernelGGL(k, dim3(a.groups), dim3(64 * WV), lds, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_big(const LaunchShape& ls, const GemmArgs& a, hipStream_t s) {
+  if (ls.big == 2) return launch_big2(a, s);
   return ls.waves == 4 ? launch_big_wv<4>(a, s) : launch_big_wv<8>(a, s);
 }
 

@@ -99,7 +99,7 @@ struct LaunchShape {
   int mblocks;  // grid.y
   int u8;       // eight instruction steps per batch of loads (single activation tile only)
   int rows;     // row-split workgroups with activations staged in LDS
-  int big;      // large-M kernel: 128-row x 256-token workgroup tiles (fp8)
+  int big;      // large-M kernels (fp8): 1 = 128-row x 256-token workgroup tiles, 2 = 256 x 256
   int glu;      // row-split kernel, gate and up paired: waves 0-3 gate tiles, 4-7 the same up tiles
 };
 

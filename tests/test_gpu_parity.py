@@ -231,7 +231,7 @@ def test_repeated_calls_are_bitwise_identical(S):
 
 # forced plans (spense_gemm_planned): kernel 1 = K split over a workgroup's waves, 2 = rows
 # split with activations in LDS, 3 = large-M tiles; None = the planner's own choice
-KSPLIT, ROWS, BIG = 1, 2, 3
+KSPLIT, ROWS, BIG, BIG2 = 1, 2, 3, 4
 KERNEL_SHAPES = [None, dict(kernel=KSPLIT, waves=4, row_tiles=1), dict(kernel=KSPLIT, waves=16, row_tiles=1),
                  dict(kernel=KSPLIT, waves=8, row_tiles=2), dict(kernel=KSPLIT, waves=8, row_tiles=1, u8=1),
                  dict(kernel=KSPLIT, waves=4, row_tiles=2), dict(kernel=KSPLIT, waves=4, row_tiles=4),
@@ -241,7 +241,7 @@ KERNEL_SHAPES = [None, dict(kernel=KSPLIT, waves=4, row_tiles=1), dict(kernel=KS
                  dict(kernel=ROWS, waves=4, row_tiles=1, ksplit=7),
                  dict(kernel=ROWS, waves=4, row_tiles=2),
                  dict(kernel=ROWS, waves=4, row_tiles=2, ksplit=3),
-                 dict(kernel=BIG, waves=8), dict(kernel=BIG, waves=4)]
+                 dict(kernel=BIG, waves=8), dict(kernel=BIG, waves=4), dict(kernel=BIG2, waves=8)]
 
 
 def plan(S, cfg):
@@ -261,7 +261,7 @@ def test_every_kernel_shape_is_repeatable_and_within_bound(S, dtype, axis, db):
     pw, (v, m, d) = compress_both(S, W, mask, dtype, axis, db)
     Wd = oracle.decompress(v, m, d, N, K, dtype, axis, db)
     for cfg in KERNEL_SHAPES:
-        if cfg is not None and cfg["kernel"] == BIG and dtype != FP8:
+        if cfg is not None and cfg["kernel"] in (BIG, BIG2) and dtype != FP8:
             continue
         for M in (64, 33, 7, 1):
             swd = None if sw is None else tdev(sw)
@@ -389,26 +389,33 @@ BIG_CASES = [  # axis, M, N, K, dense_begin: ragged tokens, rows and columns aro
     # XCD-aware order: T = 2, 4, 8 token blocks with row blocks in 8, 8, 4 classes (two regions
     # for output-split; ragged tokens)
     (0, 512, 1024, 128, 512), (0, 1024, 1024, 256, 256), (1, 2048, 512, 384, 128), (1, 1900, 512, 256, 256)]
+# 256 x 256 tiles: rows around 256-row blocks (both regions ragged), XCD-aware grids with
+# 2, 4 and 8 token blocks and 8 / 4 row-block classes
+BIG2_CASES = [(0, 700, 784, 640, 528), (1, 300, 600, 1152, 896), (0, 512, 2048, 256, 1024),
+              (0, 1024, 2048, 384, 1536), (1, 2048, 1024, 256, 128)]
 
 
-@pytest.mark.parametrize("waves", [4, 8])
-@pytest.mark.parametrize("axis,M,N,K,db", BIG_CASES)
-def test_large_m_kernel_exact_both_layouts(S, axis, M, N, K, db, waves):
-    """The large-M kernel (128-row x 256-token tiles, 4 or 8 waves), forced on at any M, on
-    exact-integer data: bit-exact against the oracle with the row-major and the tiled
-    weight."""
+LARGE_M_KERNELS = [(BIG, 4), (BIG, 8), (BIG2, 8)]
+
+
+@pytest.mark.parametrize("kernel,waves", LARGE_M_KERNELS)
+@pytest.mark.parametrize("axis,M,N,K,db", BIG_CASES + BIG2_CASES)
+def test_large_m_kernel_exact_both_layouts(S, axis, M, N, K, db, kernel, waves):
+    """The large-M kernels (128-row x 256-token tiles with 4 or 8 waves, 256 x 256 tiles
+    with 8 waves), forced on at any M, on exact-integer data: bit-exact against the oracle
+    with the row-major and the tiled weight."""
     W, mask, X, sw, sx = gen.make_exact_int(13, M + N, M, N, K, gaxis(axis), db, gen.FP8)
     pw, (v, m, d) = compress_both(S, W, mask, FP8, axis, db)
     ref = oracle.spense_gemm(X, v, m, d, N, K, FP8, axis, db, sw, sx)
-    big = S.plan_override(kernel=BIG, waves=waves)
+    big = S.plan_override(kernel=kernel, waves=waves)
     for w in (pw, S.tile(pw)):
         assert np.array_equal(run_gemm(S, w, X, sw, sx, True, big), ref["y_f32"])
         assert np.array_equal(run_gemm(S, w, X, sw, sx, False, big).view(np.uint16), ref["y_bf16"])
 
 
-@pytest.mark.parametrize("waves", [4, 8])
+@pytest.mark.parametrize("kernel,waves", LARGE_M_KERNELS)
 @pytest.mark.parametrize("axis,db", [(0, 744), (1, 1536)])
-def test_large_m_kernel_random_within_bound(S, axis, db, waves):
+def test_large_m_kernel_random_within_bound(S, axis, db, kernel, waves):
     """Random data through the large-M kernel: inside the error bound against the oracle,
     equal with both layouts and bitwise repeatable."""
     M, N, K = 520, 1000, 2080
@@ -417,7 +424,7 @@ def test_large_m_kernel_random_within_bound(S, axis, db, waves):
     ref = oracle.spense_gemm(X, v, m, d, N, K, FP8, axis, db, sw, sx)
     Wd = oracle.decompress(v, m, d, N, K, FP8, axis, db)
     pwt = S.tile(pw)
-    big = S.plan_override(kernel=BIG, waves=waves)
+    big = S.plan_override(kernel=kernel, waves=waves)
     y32 = run_gemm(S, pw, X, sw, sx, True, big)
     assert_f32_bound(y32, X, Wd, FP8, sw, sx)
     assert_bf16_close(run_gemm(S, pw, X, sw, sx, False, big).view(np.uint16), ref["y_bf16"], FP8)
