@@ -430,12 +430,16 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
   // 177 / 312 -> 159 / 291, Seed-OSS gate 178 / 316 -> 168 / 290, down and o at M = 2048
   // (160 workgroups) 313 -> 267 and 120 -> 100, q at M = 2048 95 -> 91; with fewer
   // workgroups it loses (q at M = 1024, 128 workgroups: 49 -> 84; down at M = 1024, 80: 159
-  // -> 279); gate / up at M = 512 (200) is even.
+  // -> 279).  With two or three token blocks the last one must be full: gate / up at M =
+  // 257 / 384 / 448 / 512 85 / 85 / 87 / 93 against 91 / 88 / 88 / 90, at M = 513 / 640 /
+  // 768 134 / 141 / 151 against 144 / 146 / 152 (Seed-OSS gate alike); from four blocks on
+  // (q at M = 1025-1792: 97-106 -> 88-96) a ragged last block is fine.
   if (big && tiled) {
     const int64_t rb256 = split == SPENSE_SPLIT_OUTPUT
                               ? ceil_div(dense_begin, 256) + ceil_div(N - dense_begin, 256)
                               : ceil_div(N, 256);
-    if (rb256 * ceil_div(M, 256) >= 160) big = 2;
+    const int64_t tb256 = ceil_div(M, 256);
+    if (rb256 * tb256 >= 160 && (tb256 >= 4 || M % 256 == 0)) big = 2;
   }
   if (ov.kernel == 1 || ov.kernel == 2) big = 0;
   if (ov.kernel == 3) big = 1;  // fp8 (checked by read_override)

@@ -10,7 +10,7 @@
 
 #include <mutex>
 
-#include "../../include/spense.h"
+#include "spense.h"
 #include "spense_internal.h"
 
 namespace {
