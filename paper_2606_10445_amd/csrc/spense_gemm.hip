@@ -1362,8 +1362,10 @@ __global__ __launch_bounds__(64 * WV) void spense_gemm_big_kernel(GemmArgs a) {
 // activation blocks and, for its 2 row tiles, the 2:4 value blocks (the metadata of a whole
 // 512-column chunk, 1 KB per tile, once every 4 steps into its own LDS area) or both
 // dense halves, and nothing else: 6.5 loads per 2:4 step (52 KB per workgroup, ~0.95k
-// clocks) against ~1.07k clocks of its 256 MMAs.  Two loads follow each of the first four
-// groups of 4 MMAs, so that they land before the next barrier.
+// clocks) against ~1.07k clocks of its 256 MMAs.  With two stages a load has one step to
+// land in (per-wave timelines showed every wave waiting at the barrier for them), so they
+// are issued early in the step: the activation blocks before the first group of 4 MMAs,
+// the weight blocks before the third.
 // The per-lane offsets are loop-invariant; the step's offset travels in the scalar offset.
 // LDS: two stages of activations (32 KB) and weights (32 KB), two chunk metadata areas
 // (16 KB): 160 KB.  The barrier at the start of a step waits for this wave's loads of the
@@ -1474,8 +1476,9 @@ __global__ __launch_bounds__(512) void spense_gemm_big2_kernel(GemmArgs a) {
 
   // One step: after the barrier, the B fragments of the wave's 4 token tiles and the A
   // fragment of its first row tile; then per row tile t the A fragment of tile t + 1 is
-  // read (other register set) before the 4 MMAs of tile t; loads 2t and 2t + 1 of step
-  // s + 1 follow the first four groups.
+  // read (other register set) before the 4 MMAs of tile t.  The loads of step s + 1 go
+  // out early, since with two stages their latency has only this step to hide in: the
+  // four activation blocks before the MMAs of tile 0, the weight blocks before tile 2.
   auto step = [&](auto kind_const, int s) __attribute__((always_inline)) {
     constexpr bool SPARSE = decltype(kind_const)::value == kStepSparse;
     const uint8_t* xs = xarea + (s & 1) * kB2XSlot;
@@ -1503,16 +1506,18 @@ __global__ __launch_bounds__(512) void spense_gemm_big2_kernel(GemmArgs a) {
       constexpr int t = decltype(t_const)::value;
       constexpr int q = t & 1;
       if constexpr (t + 1 < RPW) read_a(t + 1, 1 - q);
+      if constexpr (t == 0 || t == 2) {  // activation loads before group 0, weight loads before group 2
+        load_j(std::integral_constant<int, 2 * t>(), s + 1);
+        load_j(std::integral_constant<int, 2 * t + 1>(), s + 1);
+        load_j(std::integral_constant<int, 2 * t + 2>(), s + 1);
+        load_j(std::integral_constant<int, 2 * t + 3>(), s + 1);
+      }
 #pragma unroll
       for (int c = 0; c < TC; ++c) {
         if constexpr (SPARSE)
           acc[t][c] = mma_sparse(alo[q], bq[c], acc[t][c], aix[q], std::integral_constant<int, kFP8>());
         else
           acc[t][c] = mma_dense(cat8(alo[q], ahi[q]), bq[c], acc[t][c], std::integral_constant<int, kFP8>());
-      }
-      if constexpr (2 * t + 1 < RPW) {  // two loads after each of the first four groups
-        load_j(std::integral_constant<int, 2 * t>(), s + 1);
-        load_j(std::integral_constant<int, 2 * t + 1>(), s + 1);
       }
       __builtin_amdgcn_sched_barrier(0);
     });
