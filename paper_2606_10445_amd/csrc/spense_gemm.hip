@@ -1359,28 +1359,38 @@ __global__ __launch_bounds__(64 * WV) void spense_gemm_big_kernel(GemmArgs a) {
 // into registers or straight into LDS alike, but a load instruction costs at least ~18
 // clocks however few bytes it moves (a 4-byte-per-lane load moves 256 bytes in ~32; all
 // measured on MI355X).  So every load here moves 1 KB: per 128-column step a wave issues 4
-// activation blocks and, for its 2 row tiles, the 2:4 value blocks (the metadata of a whole
-// 512-column chunk, 1 KB per tile, once every 4 steps into its own LDS area) or both
-// dense halves, and nothing else: 6.5 loads per 2:4 step (52 KB per workgroup, ~0.95k
-// clocks) against ~1.07k clocks of its 256 MMAs.  With two stages a load has one step to
-// land in (per-wave timelines showed every wave waiting at the barrier for them), so they
-// are issued early in the step: the activation blocks before the first group of 4 MMAs,
-// the weight blocks before the third.
-// The per-lane offsets are loop-invariant; the step's offset travels in the scalar offset.
-// LDS: two stages of activations (32 KB) and weights (32 KB), two chunk metadata areas
-// (16 KB): 160 KB.  The barrier at the start of a step waits for this wave's loads of the
-// step (issued during the previous one) and for its LDS reads of the previous step.
+// activation blocks and, for its 2 row tiles, the 2:4 value blocks or both dense halves;
+// a 2:4 step's metadata (256 bytes per row tile) takes 4 more loads, one on each of waves
+// 0-3, each gathering the pieces of 4 row tiles.  6.5 loads per 2:4 step (52 KB per
+// workgroup) against ~1.07k clocks of its 256 MMAs.
+//
+// Per-wave timelines showed every wave waiting at the barrier for the loads when they had
+// one step to land in, so the 2:4 steps run three stages deep (loads two steps ahead; a
+// stage is 52 KB: activations, values, metadata) and the dense steps, whose stage is 64 KB
+// and whose MMAs take twice as long, two.  Within a step the loads go out early: the
+// activation blocks before the first group of 4 MMAs, the weight blocks before the third.
+// An input-split weight switches from the first layout to the second once, after a
+// barrier.  The per-lane offsets are loop-invariant; the step's offset travels in the
+// scalar offset.  The barrier at the start of a step waits for this wave's loads of the
+// step and for its LDS reads of the previous step.
 constexpr int kB2Rows = 256, kB2Tokens = 256, kB2RowTiles = 16;
-constexpr int kB2XSlot = kB2Tokens * 128;     // activations of one step
-constexpr int kB2WSlot = kB2RowTiles * 2048;  // weights of one step: 2:4 values or both dense halves per row tile
-constexpr int kB2MSlot = kB2RowTiles * 1024;  // 2:4 metadata of one 512-column chunk
-constexpr int kB2Lds = 2 * (kB2XSlot + kB2WSlot + kB2MSlot);
+constexpr int kB2XSlot = kB2Tokens * 128;                                      // activations of one step
+constexpr int kB2SStage = kB2XSlot + kB2RowTiles * 1024 + kB2RowTiles * 256;  // + 2:4 values, metadata
+constexpr int kB2DStage = kB2XSlot + kB2RowTiles * 2048;                       // + both dense halves
+constexpr int kB2Lds = 3 * kB2SStage > 2 * kB2DStage ? 3 * kB2SStage : 2 * kB2DStage;
+
+template <int AUX>
+__device__ __forceinline__ void lds_load16(__amdgpu_buffer_rsrc_t r, uint8_t* dst, uint32_t voff, int soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)dst, 16, voff, soff, 0, AUX);
+}
 
 __global__ __launch_bounds__(512) void spense_gemm_big2_kernel(GemmArgs a) {
   constexpr int WV = 8, NT = kB2RowTiles, RPW = 8, TC = 4;
   constexpr int TU = NT / WV;                // row tiles whose weights a wave copies
   constexpr int XI = kB2XSlot / 1024 / WV;  // 1 KB activation blocks per wave per step
-  static_assert(XI + 2 * TU == RPW, "eight loads per step");
+  constexpr int MW = NT * 256 / 1024;       // waves that copy a 2:4 step's metadata
+  static_assert(XI + 2 * TU == RPW, "eight loads per dense step");
+  static_assert(XI == 4 && TU == 2 && MW <= WV, "load schedule");
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int li = lane & 15, lq = lane >> 4;
   const int wr = wave & 1, wc = wave >> 1;
@@ -1399,9 +1409,6 @@ __global__ __launch_bounds__(512) void spense_gemm_big2_kernel(GemmArgs a) {
   const int K = R.kend, kbound = R.kbound;
 
   extern __shared__ __attribute__((aligned(1024))) uint8_t big_lds[];
-  uint8_t* const xarea = big_lds;
-  uint8_t* const warea = big_lds + 2 * kB2XSlot;
-  uint8_t* const marea = big_lds + 2 * (kB2XSlot + kB2WSlot);
   const __amdgpu_buffer_rsrc_t rx = rsrc(a.X, a.x_bytes), rv = rsrc(a.values, a.v_bytes),
                                rm = rsrc(a.meta, a.m_bytes), rd = rsrc(a.dense, a.d_bytes);
   v4f acc[RPW][TC];
@@ -1424,113 +1431,158 @@ __global__ __launch_bounds__(512) void spense_gemm_big2_kernel(GemmArgs a) {
     xb[i] = 16 * b;
     xo[i] = m < a.M ? (uint32_t)((int64_t)m * a.ldx_b + 16 * b) : kOOB;
   }
-  uint32_t vo[TU], mo[TU], dlo[TU];
+  uint32_t vo[TU], dlo[TU];
 #pragma unroll
   for (int u = 0; u < TU; ++u) {
     const int r0 = rblk + 16 * (TU * wave + u);
     const bool ok = r0 < rowend;
-    const uint32_t ts = (uint32_t)(r0 / 16);
-    vo[u] = ok ? ts * (uint32_t)nch_sp * 4096u + 16u * lane : kOOB;
-    mo[u] = ok ? ts * (uint32_t)nch_sp * 1024u + 16u * lane : kOOB;
+    vo[u] = ok ? (uint32_t)(r0 / 16) * (uint32_t)nch_sp * 4096u + 16u * lane : kOOB;
     dlo[u] = ok && r0 >= R.dense_row_off ? (uint32_t)((r0 - R.dense_row_off) / 16) * (uint32_t)nch_de * 8192u + 16u * lane
                                           : kOOB;
   }
+  // a 2:4 step's metadata: wave w < MW copies the 256-byte pieces of row tiles 4w .. 4w + 3
+  // (lane l: 16 bytes of tile 4w + l / 16); a tile's piece for step s sits 256 s bytes into
+  // its metadata
+  uint32_t mo1 = kOOB;
+  if (wave < MW) {
+    const int r0 = rblk + 16 * (4 * wave + (lane >> 4));
+    if (r0 < rowend) mo1 = (uint32_t)(r0 / 16) * (uint32_t)nch_sp * 1024u + 16u * li;
+  }
 
-  // Load j (0 .. 7) of this wave for step sn: activation blocks 0-3, then per row tile the
-  // 2:4 value block (j = 4, 5) and, at a chunk's first step, its metadata block (j = 6,
-  // 7); or both dense halves.  Nothing past the last step.
-  auto load_j = [&](auto j_const, int sn) __attribute__((always_inline)) {
+  // Load j of this wave for 2:4 step sn into stage stg: activation blocks (j < 4), the value
+  // blocks of its two row tiles (j = 4, 5), the metadata gather (j = 6, waves 0-3).
+  auto sp_load = [&](auto j_const, int sn, uint8_t* stg) __attribute__((always_inline)) {
+    constexpr int j = decltype(j_const)::value;
+    if (sn >= n_sp) return;  // uniform
+    if constexpr (j < XI) {
+      const int ks = 128 * sn;
+      uint32_t off = xo[j];
+      if (ks + 128 > kbound) off = ks + xb[j] < kbound ? off : kOOB;  // the region's last, partial step
+      lds_load16<0>(rx, stg + (wave * XI + j) * 1024, off, ks);
+    } else if constexpr (j < XI + TU) {
+      constexpr int u = j - XI;
+      lds_load16<kTiledNT>(rv, stg + kB2XSlot + (TU * wave + u) * 1024, vo[u], 1024 * sn);
+    } else {
+      if (wave < MW) lds_load16<kTiledNT>(rm, stg + kB2XSlot + NT * 1024 + wave * 1024, mo1, 256 * sn);
+    }
+  };
+  // Load j of this wave for dense step sn into stage stg: activation blocks (j < 4), then
+  // the two halves of its two row tiles.
+  auto de_load = [&](auto j_const, int sn, uint8_t* stg) __attribute__((always_inline)) {
     constexpr int j = decltype(j_const)::value;
     if (sn >= nst) return;  // uniform
-    const bool sp = sn < n_sp;
     if constexpr (j < XI) {
-      const int ks = sp ? 128 * sn : kbound + 128 * (sn - n_sp);
-      const int ke = sp ? kbound : K;
+      const int ks = kbound + 128 * (sn - n_sp);
       uint32_t off = xo[j];
-      if (ks + 128 > ke) off = ks + xb[j] < ke ? off : kOOB;  // the region's last, partial step
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          rx, (__attribute__((address_space(3))) void*)(xarea + (sn & 1) * kB2XSlot + (wave * XI + j) * 1024), 16, off,
-          ks, 0, 0);
+      if (ks + 128 > K) off = ks + xb[j] < K ? off : kOOB;
+      lds_load16<0>(rx, stg + (wave * XI + j) * 1024, off, ks);
     } else {
       constexpr int u = (j - XI) % TU, half = (j - XI) / TU;
-      const int tile = TU * wave + u;
-      uint8_t* const wdst = warea + (sn & 1) * kB2WSlot + tile * 2048;
-      if (sp) {
-        const int cs = sn >> 2, js = sn & 3;
-        if constexpr (half == 0) {
-          __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (__attribute__((address_space(3))) void*)wdst, 16, vo[u],
-                                                   cs * 4096 + 1024 * js, 0, kTiledNT);
-        } else {
-          if (js == 0)
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                rm, (__attribute__((address_space(3))) void*)(marea + (cs & 1) * kB2MSlot + tile * 1024), 16, mo[u],
-                cs * 1024, 0, kTiledNT);
-        }
-      } else {
-        const int sd = sn - n_sp, cd = sd >> 2, jd = sd & 3;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rd, (__attribute__((address_space(3))) void*)(wdst + 1024 * half), 16,
-                                                 dlo[u], cd * 8192 + 2048 * jd + 1024 * half, 0, kTiledNT);
-      }
+      lds_load16<kTiledNT>(rd, stg + kB2XSlot + (TU * wave + u) * 2048 + 1024 * half, dlo[u],
+                           2048 * (sn - n_sp) + 1024 * half);
     }
   };
 
-  // One step: after the barrier, the B fragments of the wave's 4 token tiles and the A
-  // fragment of its first row tile; then per row tile t the A fragment of tile t + 1 is
-  // read (other register set) before the 4 MMAs of tile t.  The loads of step s + 1 go
-  // out early, since with two stages their latency has only this step to hide in: the
-  // four activation blocks before the MMAs of tile 0, the weight blocks before tile 2.
-  auto step = [&](auto kind_const, int s) __attribute__((always_inline)) {
-    constexpr bool SPARSE = decltype(kind_const)::value == kStepSparse;
-    const uint8_t* xs = xarea + (s & 1) * kB2XSlot;
-    const uint8_t* wl = warea + (s & 1) * kB2WSlot + (RPW * wr) * 2048 + 16 * lane;
-    const uint8_t* ml = marea + ((s >> 2) & 1) * kB2MSlot + (RPW * wr) * 1024 + 256 * (s & 3) + 16 * li + 4 * lq;
-    barrier_vm_lgkm0<0>();
-    v8i bq[TC];
+  // B fragments of the wave's 4 token tiles from a stage
+  auto read_b = [&](v8i (&bq)[TC], const uint8_t* xs) __attribute__((always_inline)) {
 #pragma unroll
     for (int c = 0; c < TC; ++c) {
       const int r = 16 * (TC * wc + c) + li;
       bq[c] = cat8(*reinterpret_cast<const v4i*>(xs + r * 128 + ((lq ^ ((r >> 1) & 7)) << 4)),
                    *reinterpret_cast<const v4i*>(xs + r * 128 + (((4 + lq) ^ ((r >> 1) & 7)) << 4)));
     }
-    v4i alo[2], ahi[2];
-    int aix[2];
-    auto read_a = [&](int t, int q) __attribute__((always_inline)) {
-      alo[q] = *reinterpret_cast<const v4i*>(wl + t * 2048);
-      if constexpr (SPARSE)
-        aix[q] = *reinterpret_cast<const int*>(ml + t * 1024);
+  };
+
+  // 2:4 step s from stage cur; the loads of step s + 2 go to stage nxt.  Per row tile t the
+  // A fragment of tile t + 1 is read (other register set) before the 4 MMAs of tile t.
+  auto sp_step = [&](int s, const uint8_t* cur, uint8_t* nxt) __attribute__((always_inline)) {
+    // this wave's loads of step s have landed once at most those of step s + 1 are pending
+    if (s + 1 < n_sp) {
+      if (wave < MW)
+        barrier_vm_lgkm0<XI + TU + 1>();
       else
-        ahi[q] = *reinterpret_cast<const v4i*>(wl + t * 2048 + 1024);
-    };
-    read_a(0, 0);
+        barrier_vm_lgkm0<XI + TU>();
+    } else {
+      barrier_vm_lgkm0<0>();
+    }
+    v8i bq[TC];
+    read_b(bq, cur);
+    const uint8_t* vl = cur + kB2XSlot + (RPW * wr) * 1024 + 16 * lane;
+    const uint8_t* ml = cur + kB2XSlot + NT * 1024 + (RPW * wr) * 256 + 16 * li + 4 * lq;
+    v4i av[2];
+    int aix[2];
+    av[0] = *reinterpret_cast<const v4i*>(vl);
+    aix[0] = *reinterpret_cast<const int*>(ml);
     static_for<RPW>([&](auto t_const) {
       constexpr int t = decltype(t_const)::value;
       constexpr int q = t & 1;
-      if constexpr (t + 1 < RPW) read_a(t + 1, 1 - q);
-      if constexpr (t == 0 || t == 2) {  // activation loads before group 0, weight loads before group 2
-        load_j(std::integral_constant<int, 2 * t>(), s + 1);
-        load_j(std::integral_constant<int, 2 * t + 1>(), s + 1);
-        load_j(std::integral_constant<int, 2 * t + 2>(), s + 1);
-        load_j(std::integral_constant<int, 2 * t + 3>(), s + 1);
+      if constexpr (t + 1 < RPW) {
+        av[1 - q] = *reinterpret_cast<const v4i*>(vl + (t + 1) * 1024);
+        aix[1 - q] = *reinterpret_cast<const int*>(ml + (t + 1) * 256);
+      }
+      if constexpr (t == 0) static_for<XI>([&](auto j) { sp_load(j, s + 2, nxt); });
+      if constexpr (t == 2) {
+        sp_load(std::integral_constant<int, XI>(), s + 2, nxt);
+        sp_load(std::integral_constant<int, XI + 1>(), s + 2, nxt);
+        sp_load(std::integral_constant<int, XI + 2>(), s + 2, nxt);
       }
 #pragma unroll
-      for (int c = 0; c < TC; ++c) {
-        if constexpr (SPARSE)
-          acc[t][c] = mma_sparse(alo[q], bq[c], acc[t][c], aix[q], std::integral_constant<int, kFP8>());
-        else
-          acc[t][c] = mma_dense(cat8(alo[q], ahi[q]), bq[c], acc[t][c], std::integral_constant<int, kFP8>());
-      }
+      for (int c = 0; c < TC; ++c)
+        acc[t][c] = mma_sparse(av[q], bq[c], acc[t][c], aix[q], std::integral_constant<int, kFP8>());
       __builtin_amdgcn_sched_barrier(0);
     });
   };
 
-  static_for<RPW>([&](auto j_const) { load_j(j_const, 0); });  // step 0
-  const std::integral_constant<int, kStepSparse> SP;
-  const std::integral_constant<int, kStepDense> DE;
+  // dense step s from stage cur; the loads of step s + 1 go to stage nxt
+  auto de_step = [&](int s, const uint8_t* cur, uint8_t* nxt) __attribute__((always_inline)) {
+    barrier_vm_lgkm0<0>();
+    v8i bq[TC];
+    read_b(bq, cur);
+    const uint8_t* wl = cur + kB2XSlot + (RPW * wr) * 2048 + 16 * lane;
+    v4i alo[2], ahi[2];
+    alo[0] = *reinterpret_cast<const v4i*>(wl);
+    ahi[0] = *reinterpret_cast<const v4i*>(wl + 1024);
+    static_for<RPW>([&](auto t_const) {
+      constexpr int t = decltype(t_const)::value;
+      constexpr int q = t & 1;
+      if constexpr (t + 1 < RPW) {
+        alo[1 - q] = *reinterpret_cast<const v4i*>(wl + (t + 1) * 2048);
+        ahi[1 - q] = *reinterpret_cast<const v4i*>(wl + (t + 1) * 2048 + 1024);
+      }
+      if constexpr (t == 0 || t == 2) {
+        de_load(std::integral_constant<int, 2 * t>(), s + 1, nxt);
+        de_load(std::integral_constant<int, 2 * t + 1>(), s + 1, nxt);
+        de_load(std::integral_constant<int, 2 * t + 2>(), s + 1, nxt);
+        de_load(std::integral_constant<int, 2 * t + 3>(), s + 1, nxt);
+      }
+#pragma unroll
+      for (int c = 0; c < TC; ++c)
+        acc[t][c] = mma_dense(cat8(alo[q], ahi[q]), bq[c], acc[t][c], std::integral_constant<int, kFP8>());
+      __builtin_amdgcn_sched_barrier(0);
+    });
+  };
+
   int s = 0;
-  for (; s < n_sp; ++s) step(SP, s);
-  xdl_fence();
-  for (; s < nst; ++s) step(DE, s);
-  xdl_fence();
+  if (n_sp > 0) {
+    static_for<XI + TU + 1>([&](auto j) { sp_load(j, 0, big_lds); });
+    static_for<XI + TU + 1>([&](auto j) { sp_load(j, 1, big_lds + kB2SStage); });
+    int k = 0;  // stage of step s
+    for (; s < n_sp; ++s) {
+      const int k2 = k == 0 ? 2 : k - 1;  // stage of step s + 2
+      sp_step(s, big_lds + k * kB2SStage, big_lds + k2 * kB2SStage);
+      k = k == 2 ? 0 : k + 1;
+    }
+    xdl_fence();
+  }
+  if (n_de > 0) {
+    if (n_sp > 0) barrier_vm_lgkm0<0>();  // every wave is done with the 2:4 stages
+    static_for<RPW>([&](auto j) { de_load(j, s, big_lds); });
+    for (; s < nst; ++s) {
+      const int k = (s - n_sp) & 1;
+      de_step(s, big_lds + k * kB2DStage, big_lds + (1 - k) * kB2DStage);
+    }
+    xdl_fence();
+  }
 #pragma unroll
   for (int t = 0; t < RPW; ++t)
 #pragma unroll
