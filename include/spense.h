@@ -40,7 +40,7 @@
 extern "C" {
 #endif
 
-#define SPENSE_ABI_VERSION 10
+#define SPENSE_ABI_VERSION 11
 
 typedef enum spense_status {
   SPENSE_OK = 0,
@@ -278,6 +278,9 @@ typedef struct spense_plan_override_t {
                                the grid allows it */
   int32_t u8;               /* K-split kernel, one activation tile, one row tile, 4 or 8
                                waves: 1 = eight instruction steps per batch of loads */
+  int32_t half_row_blocks;  /* 256 x 256 kernel: -1 planner, else this many 256-row blocks
+                               at the end of the last region run as 256 x 128 tiles, after
+                               all 256 x 256 tiles (capped at the region's row blocks) */
 } spense_plan_override_t;
 
 /*

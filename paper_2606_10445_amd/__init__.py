@@ -79,7 +79,8 @@ class spense_plan_override_t(ctypes.Structure):
     _fields_ = [("kernel", ctypes.c_int32), ("row_tiles", ctypes.c_int32), ("waves", ctypes.c_int32),
                 ("act_tiles", ctypes.c_int32), ("ksplit", ctypes.c_int32), ("waves_used", ctypes.c_int32),
                 ("waves_used_dense", ctypes.c_int32), ("waves_used_24", ctypes.c_int32),
-                ("block_order", ctypes.c_int32), ("xcd_order", ctypes.c_int32), ("u8", ctypes.c_int32)]
+                ("block_order", ctypes.c_int32), ("xcd_order", ctypes.c_int32), ("u8", ctypes.c_int32),
+                ("half_row_blocks", ctypes.c_int32)]
 
 
 KERNEL_KSPLIT, KERNEL_ROWS, KERNEL_LARGE_M = 1, 2, 3
@@ -87,8 +88,8 @@ KERNEL_KSPLIT, KERNEL_ROWS, KERNEL_LARGE_M = 1, 2, 3
 
 def plan_override(**kw) -> spense_plan_override_t:
     """A spense_plan_override_t with the given fields forced and the rest left to the
-    planner (block_order and xcd_order default to -1)."""
-    p = spense_plan_override_t(block_order=-1, xcd_order=-1)
+    planner (block_order, xcd_order and half_row_blocks default to -1)."""
+    p = spense_plan_override_t(block_order=-1, xcd_order=-1, half_row_blocks=-1)
     for k, v in kw.items():
         if not hasattr(p, k):
             raise TypeError(f"unknown plan field {k}")

@@ -174,11 +174,11 @@ struct Plan {
 // choice to the planner.
 struct Override {
   int kernel = 0, rt = 0, waves = 0, ct = 0, ksplit = 0, wused = 0, wused_d = 0, wused_s = 0, order = -1, xcd = -1,
-      u8 = 0;
+      u8 = 0, halfrb = -1;
   bool operator==(const Override& o) const {
     return kernel == o.kernel && rt == o.rt && waves == o.waves && ct == o.ct && ksplit == o.ksplit &&
            wused == o.wused && wused_d == o.wused_d && wused_s == o.wused_s && order == o.order && xcd == o.xcd &&
-           u8 == o.u8;
+           u8 == o.u8 && halfrb == o.halfrb;
   }
 };
 
@@ -205,6 +205,7 @@ int read_override(const spense_plan_override_t* ov, int32_t dtype, bool tiled, O
   o->order = ov->block_order;
   o->xcd = ov->xcd_order;
   o->u8 = ov->u8;
+  o->halfrb = ov->half_row_blocks;
   if (o->kernel < 0 || o->kernel > 4) return fail(SPENSE_ERR_ARG, "plan: unknown kernel %d", o->kernel);
   if (o->kernel == 1 && tiled) return fail(SPENSE_ERR_ARG, "plan: the K-split kernel reads the row-major layout only");
   if (o->kernel >= 3 && dtype != SPENSE_FP8_E4M3FN) return fail(SPENSE_ERR_ARG, "plan: the large-M kernels are fp8 only");
@@ -215,6 +216,7 @@ int read_override(const spense_plan_override_t* ov, int32_t dtype, bool tiled, O
   if (o->order < -1 || o->order > 2) return fail(SPENSE_ERR_ARG, "plan: block_order %d", o->order);
   if (o->xcd < -1 || o->xcd > 1) return fail(SPENSE_ERR_ARG, "plan: xcd_order %d", o->xcd);
   if (o->u8 < 0 || o->u8 > 1) return fail(SPENSE_ERR_ARG, "plan: u8 %d", o->u8);
+  if (o->halfrb < -1) return fail(SPENSE_ERR_ARG, "plan: half_row_blocks %d", o->halfrb);
   if (o->rt || o->waves) {
     bool okshape = false;
     if (o->kernel == 1) {
@@ -233,6 +235,46 @@ int read_override(const spense_plan_override_t* ov, int32_t dtype, bool tiled, O
 }
 
 constexpr int kCUs = 256;  // compute units of an MI355X
+// XCD-aware order of the large-M grids: each XCD takes GT of the T token blocks (the
+// divisor of T nearest 4 whose token groups T / GT divide the 8 XCDs; 0 = none) and every
+// RC-th row block (RC = 8 / (T / GT)).
+int64_t xcd_token_group(int64_t T) {
+  int64_t GT = 0;
+  for (int64_t d = 1; d <= T; ++d)
+    if (T % d == 0 && 8 % (T / d) == 0 && (GT == 0 || std::llabs(d - 4) < std::llabs(GT - 4))) GT = d;
+  return GT;
+}
+
+// 256 x 256 kernel: the row blocks at the end of the last region that run as 256 x 128
+// tiles after every full tile.  With whole tiles the last round of the grid leaves CUs
+// idle: gate / up at M = 2048 is 800 tiles of 65 (2:4) and 84 us (dense) on 256 CUs, so
+// some CUs run four tiles while the average load is 218 us (per-workgroup timestamps on
+// MI355X).  Smaller tiles dispatched last fill that round.  Measured (us, half tiles'
+// row blocks 0 -> the best): gate / up M = 2048 277 -> 248 (12-24), down and o at M =
+// 2048 240 -> 220 and 92 -> 87 (4), Seed-OSS gate 278 -> 257 (12); q at M = 2048 (one
+// round of 256 tiles) only loses.  The rule: with more than one round, half tiles worth
+// about an eighth of the work (a dense step costing 1.28 2:4 steps, a half tile 0.6 of a
+// full one), rounded up to whole XCD row classes.
+int64_t choose_half_rows(const spense::Region* regs, int nreg, int64_t T, int64_t M, int64_t rc) {
+  double W = 0;
+  int64_t rbtot = 0;
+  double wl = 0;
+  int64_t rbl = 0;
+  for (int i = 0; i < nreg; ++i) {
+    const int64_t rb = ceil_div(regs[i].rows, 256);
+    const double w = (double)ceil_div(regs[i].kbound, 128) + 1.28 * (double)ceil_div(regs[i].kend - regs[i].kbound, 128);
+    W += (double)(rb * T) * w;
+    rbtot += rb;
+    wl = w;
+    rbl = rb;
+  }
+  if (rbtot * T <= kCUs || wl <= 0) return 0;
+  const double per_rb = (double)ceil_div(M, 128) * 0.6 * wl;
+  int64_t rh = (int64_t)std::ceil(W / 8.0 / per_rb);
+  if (rc > 1) rh = ceil_div(rh, rc) * rc;
+  return std::min(rh, rbl);
+}
+
 constexpr int64_t kBigMinM = 65;       // tokens from which the large-M kernel is used (fp8)
 constexpr int64_t kBigMinTiles = 128;  // and workgroup tiles (128 rows x 256 tokens) it needs
 
@@ -494,6 +536,16 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
     for (int i = 0; i < nreg; ++i) slice_cuts(regs[i], ksplit, kc, es, sparse_cost);
     choose_rows_per_group(regs, nreg, rt, waves, pl->ls.ct, pl->ls.mblocks, K, es, sparse_cost, ksplit, ov);
   }
+  // 256 x 256 kernel: the last row blocks of the last region may run as 256 x 128 tiles
+  // after every 256 x 256 tile, to fill the grid's last round
+  int64_t half_rb = 0, rbl = 0;
+  if (big == 2 && nreg > 0) {
+    rbl = ceil_div(regs[nreg - 1].rows, 256);
+    const int64_t GT = xcd_token_group(tblocks);
+    const int64_t rc = GT > 0 ? 8 / (tblocks / GT) : 1;
+    half_rb = ov.halfrb >= 0 ? std::min<int64_t>(ov.halfrb, rbl) : choose_half_rows(regs, nreg, tblocks, M, rc);
+    regs[nreg - 1].nrb = (int32_t)((rbl - half_rb) * tblocks);
+  }
   spense::GemmArgs& a = pl->args;
   a.nreg = nreg;
   int32_t groups = 0;
@@ -505,22 +557,32 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
   a.groups = groups;
   a.tiled = tiled ? 1 : 0;
   a.tblocks = (int32_t)tblocks;
+  a.hg0 = groups;
+  a.hrb0 = (int32_t)(rbl - half_rb);
+  a.hper = (int32_t)ceil_div(M, 128);
+  a.groups = (int32_t)(groups + half_rb * a.hper);
   // Large-M kernel, XCD-aware order: workgroups are dealt to the 8 XCDs round-robin
   // (XCD = id % 8).  Each XCD is given GT token blocks (up to 4) and every RC-th row
   // block, so a weight block is fetched into an XCD's L2 once for GT token blocks and
   // the activations of those blocks stay there.  Needs T / GT to divide 8 and the row
   // blocks to split evenly into RC classes; otherwise the plain order.  Measured on
   // MI355X (gate / up and down at M = 2048): 9% faster than one token block per XCD.
-  a.xgt = a.xrc = 0;
-  if (big) {
+  a.xgt = a.xrc = a.xg1 = 0;
+  if (big && ov.xcd != 0) {
+    // GT: the divisor of T nearest 4 whose token groups (T / GT) divide the 8 XCDs; the
+    // row blocks beyond the last whole set of RC classes keep the plain order after the
+    // others
     const int64_t T = tblocks;
-    const int64_t GT = T % 4 == 0 ? 4 : (T % 2 == 0 ? 2 : 1);
-    const int64_t TGc = T / GT;
-    int64_t rbtot = 0;
+    const int64_t GT = xcd_token_group(T);
+    int64_t rbtot = -half_rb;  // row blocks of the full-size tiles
     for (int i = 0; i < nreg; ++i) rbtot += ceil_div(regs[i].rows, big_rows);
-    if (8 % TGc == 0 && rbtot % (8 / TGc) == 0 && ov.xcd != 0) {
-      a.xgt = (int32_t)GT;
-      a.xrc = (int32_t)(8 / TGc);
+    if (GT > 0) {
+      const int64_t RC = 8 / (T / GT), rbx = rbtot / RC * RC;
+      if (rbx > 0) {
+        a.xgt = (int32_t)GT;
+        a.xrc = (int32_t)RC;
+        a.xg1 = (int32_t)(rbx * T);
+      }
     }
   }
   // Row-split kernel with several token blocks: the blocks of a row group on one XCD

@@ -1098,9 +1098,9 @@ __global__ __launch_bounds__(64 * WV) void spense_gemm_big_kernel(GemmArgs a) {
   const int li = lane & 15, lq = lane >> 4;
   const int wr = wave & 1, wc = wave >> 1;
   int g = blockIdx.x;
-  if (a.xgt > 0) {
+  if (a.xgt > 0 && g < a.xg1) {
     // XCD-aware order: XCD x (= id % 8) takes token group x % (T / GT) (GT blocks) and
-    // the row blocks of class x / (T / GT) (every RC-th); a bijection on the grid
+    // the row blocks of class x / (T / GT) (every RC-th); a bijection on [0, xg1)
     const int T = a.tblocks, GT = a.xgt, RC = a.xrc, TGc = T / GT;
     const int x = g & 7, l = g >> 3, tg = x % TGc, rc = x / TGc;
     g = ((l / GT) * RC + rc) * T + tg * GT + l % GT;
@@ -1394,18 +1394,32 @@ __global__ __launch_bounds__(512) void spense_gemm_big2_kernel(GemmArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int li = lane & 15, lq = lane >> 4;
   const int wr = wave & 1, wc = wave >> 1;
-  int g = blockIdx.x;
-  if (a.xgt > 0) {  // XCD-aware order, as in spense_gemm_big_kernel
-    const int T = a.tblocks, GT = a.xgt, RC = a.xrc, TGc = T / GT;
-    const int x = g & 7, l = g >> 3, tg = x % TGc, rc = x / TGc;
-    g = ((l / GT) * RC + rc) * T + tg * GT + l % GT;
+  // Workgroups [0, hg0): 256 x 256 tiles, in the XCD-aware order when it is on.  From
+  // hg0 on (dispatched last, so that they fill the tail of the grid): the row blocks
+  // hrb0 .. of the last region as 256 x 128 tiles, hper per row block; their waves of
+  // token quarters 2 and 3 only copy and take part in the barriers.
+  int g = blockIdx.x, ri, rb, m0;
+  bool half = false;
+  if (g < a.hg0) {
+    if (a.xgt > 0 && g < a.xg1) {  // XCD-aware order, as in spense_gemm_big_kernel
+      const int T = a.tblocks, GT = a.xgt, RC = a.xrc, TGc = T / GT;
+      const int x = g & 7, l = g >> 3, tg = x % TGc, rc = x / TGc;
+      g = ((l / GT) * RC + rc) * T + tg * GT + l % GT;
+    }
+    ri = (a.nreg > 1 && g >= a.reg[1].wg0) ? 1 : 0;
+    rb = (g - a.reg[ri].wg0) / a.tblocks;
+    m0 = (g - a.reg[ri].wg0) % a.tblocks * kB2Tokens;
+  } else {
+    const int h = g - a.hg0;
+    ri = a.nreg - 1;
+    rb = a.hrb0 + h / a.hper;
+    m0 = h % a.hper * (kB2Tokens / 2);
+    half = true;
   }
-  const int ri = (a.nreg > 1 && g >= a.reg[1].wg0) ? 1 : 0;
   const Region& R = a.reg[ri];
   const int rowend = R.row0 + R.rows;
-  const int rb = (g - R.wg0) / a.tblocks, tb = (g - R.wg0) % a.tblocks;
   const int rblk = R.row0 + rb * kB2Rows;
-  const int m0 = tb * kB2Tokens;
+  const int ntok = half ? kB2Tokens / 2 : kB2Tokens;
   const int K = R.kend, kbound = R.kbound;
 
   extern __shared__ __attribute__((aligned(1024))) uint8_t big_lds[];
@@ -1429,7 +1443,7 @@ __global__ __launch_bounds__(512) void spense_gemm_big2_kernel(GemmArgs a) {
     const int r = 8 * blk + (lane >> 3), b = (lane & 7) ^ ((r >> 1) & 7);
     const int m = m0 + r;
     xb[i] = 16 * b;
-    xo[i] = m < a.M ? (uint32_t)((int64_t)m * a.ldx_b + 16 * b) : kOOB;
+    xo[i] = m < a.M && r < ntok ? (uint32_t)((int64_t)m * a.ldx_b + 16 * b) : kOOB;
   }
   uint32_t vo[TU], dlo[TU];
 #pragma unroll
@@ -1495,7 +1509,9 @@ __global__ __launch_bounds__(512) void spense_gemm_big2_kernel(GemmArgs a) {
 
   // 2:4 step s from stage cur; the loads of step s + 2 go to stage nxt.  Per row tile t the
   // A fragment of tile t + 1 is read (other register set) before the 4 MMAs of tile t.
-  auto sp_step = [&](int s, const uint8_t* cur, uint8_t* nxt) __attribute__((always_inline)) {
+  // ACT = false: a wave without tokens (the second half of a 256 x 128 tile) only copies.
+  auto sp_step = [&](auto act_const, int s, const uint8_t* cur, uint8_t* nxt) __attribute__((always_inline)) {
+    constexpr bool ACT = decltype(act_const)::value;
     // this wave's loads of step s have landed once at most those of step s + 1 are pending
     if (s + 1 < n_sp) {
       if (wave < MW)
@@ -1506,17 +1522,19 @@ __global__ __launch_bounds__(512) void spense_gemm_big2_kernel(GemmArgs a) {
       barrier_vm_lgkm0<0>();
     }
     v8i bq[TC];
-    read_b(bq, cur);
     const uint8_t* vl = cur + kB2XSlot + (RPW * wr) * 1024 + 16 * lane;
     const uint8_t* ml = cur + kB2XSlot + NT * 1024 + (RPW * wr) * 256 + 16 * li + 4 * lq;
     v4i av[2];
     int aix[2];
-    av[0] = *reinterpret_cast<const v4i*>(vl);
-    aix[0] = *reinterpret_cast<const int*>(ml);
+    if constexpr (ACT) {
+      read_b(bq, cur);
+      av[0] = *reinterpret_cast<const v4i*>(vl);
+      aix[0] = *reinterpret_cast<const int*>(ml);
+    }
     static_for<RPW>([&](auto t_const) {
       constexpr int t = decltype(t_const)::value;
       constexpr int q = t & 1;
-      if constexpr (t + 1 < RPW) {
+      if constexpr (ACT && t + 1 < RPW) {
         av[1 - q] = *reinterpret_cast<const v4i*>(vl + (t + 1) * 1024);
         aix[1 - q] = *reinterpret_cast<const int*>(ml + (t + 1) * 256);
       }
@@ -1526,26 +1544,31 @@ __global__ __launch_bounds__(512) void spense_gemm_big2_kernel(GemmArgs a) {
         sp_load(std::integral_constant<int, XI + 1>(), s + 2, nxt);
         sp_load(std::integral_constant<int, XI + 2>(), s + 2, nxt);
       }
+      if constexpr (ACT) {
 #pragma unroll
-      for (int c = 0; c < TC; ++c)
-        acc[t][c] = mma_sparse(av[q], bq[c], acc[t][c], aix[q], std::integral_constant<int, kFP8>());
+        for (int c = 0; c < TC; ++c)
+          acc[t][c] = mma_sparse(av[q], bq[c], acc[t][c], aix[q], std::integral_constant<int, kFP8>());
+      }
       __builtin_amdgcn_sched_barrier(0);
     });
   };
 
   // dense step s from stage cur; the loads of step s + 1 go to stage nxt
-  auto de_step = [&](int s, const uint8_t* cur, uint8_t* nxt) __attribute__((always_inline)) {
+  auto de_step = [&](auto act_const, int s, const uint8_t* cur, uint8_t* nxt) __attribute__((always_inline)) {
+    constexpr bool ACT = decltype(act_const)::value;
     barrier_vm_lgkm0<0>();
     v8i bq[TC];
-    read_b(bq, cur);
     const uint8_t* wl = cur + kB2XSlot + (RPW * wr) * 2048 + 16 * lane;
     v4i alo[2], ahi[2];
-    alo[0] = *reinterpret_cast<const v4i*>(wl);
-    ahi[0] = *reinterpret_cast<const v4i*>(wl + 1024);
+    if constexpr (ACT) {
+      read_b(bq, cur);
+      alo[0] = *reinterpret_cast<const v4i*>(wl);
+      ahi[0] = *reinterpret_cast<const v4i*>(wl + 1024);
+    }
     static_for<RPW>([&](auto t_const) {
       constexpr int t = decltype(t_const)::value;
       constexpr int q = t & 1;
-      if constexpr (t + 1 < RPW) {
+      if constexpr (ACT && t + 1 < RPW) {
         alo[1 - q] = *reinterpret_cast<const v4i*>(wl + (t + 1) * 2048);
         ahi[1 - q] = *reinterpret_cast<const v4i*>(wl + (t + 1) * 2048 + 1024);
       }
@@ -1555,34 +1578,43 @@ __global__ __launch_bounds__(512) void spense_gemm_big2_kernel(GemmArgs a) {
         de_load(std::integral_constant<int, 2 * t + 2>(), s + 1, nxt);
         de_load(std::integral_constant<int, 2 * t + 3>(), s + 1, nxt);
       }
+      if constexpr (ACT) {
 #pragma unroll
-      for (int c = 0; c < TC; ++c)
-        acc[t][c] = mma_dense(cat8(alo[q], ahi[q]), bq[c], acc[t][c], std::integral_constant<int, kFP8>());
+        for (int c = 0; c < TC; ++c)
+          acc[t][c] = mma_dense(cat8(alo[q], ahi[q]), bq[c], acc[t][c], std::integral_constant<int, kFP8>());
+      }
       __builtin_amdgcn_sched_barrier(0);
     });
   };
 
-  int s = 0;
-  if (n_sp > 0) {
-    static_for<XI + TU + 1>([&](auto j) { sp_load(j, 0, big_lds); });
-    static_for<XI + TU + 1>([&](auto j) { sp_load(j, 1, big_lds + kB2SStage); });
-    int k = 0;  // stage of step s
-    for (; s < n_sp; ++s) {
-      const int k2 = k == 0 ? 2 : k - 1;  // stage of step s + 2
-      sp_step(s, big_lds + k * kB2SStage, big_lds + k2 * kB2SStage);
-      k = k == 2 ? 0 : k + 1;
+  auto run = [&](auto act_const) __attribute__((always_inline)) {
+    int s = 0;
+    if (n_sp > 0) {
+      static_for<XI + TU + 1>([&](auto j) { sp_load(j, 0, big_lds); });
+      static_for<XI + TU + 1>([&](auto j) { sp_load(j, 1, big_lds + kB2SStage); });
+      int k = 0;  // stage of step s
+      for (; s < n_sp; ++s) {
+        const int k2 = k == 0 ? 2 : k - 1;  // stage of step s + 2
+        sp_step(act_const, s, big_lds + k * kB2SStage, big_lds + k2 * kB2SStage);
+        k = k == 2 ? 0 : k + 1;
+      }
+      xdl_fence();
     }
-    xdl_fence();
-  }
-  if (n_de > 0) {
-    if (n_sp > 0) barrier_vm_lgkm0<0>();  // every wave is done with the 2:4 stages
-    static_for<RPW>([&](auto j) { de_load(j, s, big_lds); });
-    for (; s < nst; ++s) {
-      const int k = (s - n_sp) & 1;
-      de_step(s, big_lds + k * kB2DStage, big_lds + (1 - k) * kB2DStage);
+    if (n_de > 0) {
+      if (n_sp > 0) barrier_vm_lgkm0<0>();  // every wave is done with the 2:4 stages
+      static_for<RPW>([&](auto j) { de_load(j, s, big_lds); });
+      for (; s < nst; ++s) {
+        const int k = (s - n_sp) & 1;
+        de_step(act_const, s, big_lds + k * kB2DStage, big_lds + (1 - k) * kB2DStage);
+      }
+      xdl_fence();
     }
-    xdl_fence();
+  };
+  if (half && wc >= 2) {
+    run(std::false_type());
+    return;
   }
+  run(std::true_type());
 #pragma unroll
   for (int t = 0; t < RPW; ++t)
 #pragma unroll

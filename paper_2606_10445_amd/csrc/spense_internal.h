@@ -74,7 +74,11 @@ struct GemmArgs {
   int32_t tiled;  // weight buffers in the tiled execution layout (fp8, row-split kernel)
   float* part;    // fp32 partial sums of K-sliced regions: part[(slice * M + m) * N + n]
   int32_t tblocks;  // large-M kernel: 256-token blocks (workgroups of a row block are adjacent)
+  // 256 x 256 kernel: workgroups from hg0 on (the last ones) compute 256 x 128 tiles of
+  // the last region's row blocks hrb0 .., hper of them per row block (hg0 = groups: none)
+  int32_t hg0, hrb0, hper;
   int32_t xgt, xrc;  // large-M kernel, XCD-aware order (0 = off): token blocks per XCD, row classes
+  int32_t xg1;       // the XCD-aware order covers workgroups [0, xg1); the rest keep their place
   int32_t nmat;
   // row-split kernel, several token blocks: 0 = grid (row groups, token blocks); 1 = one
   // dimension, the token blocks of a row group adjacent; 2 = one dimension, the token

@@ -41,7 +41,7 @@ def test_library_exports_every_declared_symbol(S):
     for n in _declared():
         assert hasattr(lib, n), f"{n} declared in include/ but not exported"
     assert set(_declared()) == set(S.EXPORTS)
-    assert S.spense_abi_version() == 10
+    assert S.spense_abi_version() == 11
 
 
 @pytest.mark.parametrize("N,K,split,db", [(256, 512, 0, 192), (256, 512, 1, 384), (25600, 5120, 0, 19200),
@@ -258,19 +258,26 @@ def test_obs_calls_validate_arguments_on_the_host(S):
 
 
 def test_large_m_xcd_order_is_a_permutation_of_the_grid():
-    """The large-M kernel's XCD-aware workgroup order (the same formula as the kernel and
-    the planner's precondition) visits every (row block, token block) pair exactly once."""
+    """The large-M kernels' XCD-aware workgroup order (the same formulas as the kernels and
+    the planner: GT the divisor of T nearest 4 whose token groups divide the 8 XCDs, the
+    order over the whole sets of RC row classes, the remaining row blocks in place after
+    them) visits every (row block, token block) pair exactly once."""
     for T in range(1, 33):
-        GT = 4 if T % 4 == 0 else (2 if T % 2 == 0 else 1)
+        cands = [d for d in range(1, T + 1) if T % d == 0 and 8 % (T // d) == 0]
+        if not cands:
+            continue  # the planner keeps the plain order
+        GT = min(cands, key=lambda d: (abs(d - 4), d))
         TGc = T // GT
-        for rbtot in (1, 2, 8, 40, 64, 150, 200, 216):
-            if 8 % TGc or rbtot % (8 // TGc):
-                continue  # the planner keeps the plain order
-            RC, G = 8 // TGc, rbtot * T
+        RC = 8 // TGc
+        for rbtot in (1, 2, 3, 8, 13, 40, 64, 100, 150, 200, 216):
+            rbx = rbtot // RC * RC
+            G, xg1 = rbtot * T, rbx * T
             seen = set()
             for g in range(G):
-                x, l = g & 7, g >> 3
-                seen.add(((l // GT) * RC + x // TGc) * T + (x % TGc) * GT + l % GT)
+                if g < xg1:
+                    x, l = g & 7, g >> 3
+                    g = ((l // GT) * RC + x // TGc) * T + (x % TGc) * GT + l % GT
+                seen.add(g)
             assert seen == set(range(G)), (T, rbtot)
 
 
@@ -399,7 +406,7 @@ def test_plan_override_is_checked_on_the_host(S):
            (rm, po(kernel=3, waves=16)),
            (rm, po(waves=8)),                       # a shape needs the kernel it is for
            (rm, po(kernel=5)), (rm, po(ksplit=9)), (rm, po(act_tiles=3)), (rm, po(waves_used=9)),
-           (rm, po(block_order=3)), (rm, po(xcd_order=2)), (rm, po(u8=2))]
+           (rm, po(block_order=3)), (rm, po(xcd_order=2)), (rm, po(u8=2)), (rm, po(half_row_blocks=-2))]
     for desc, p in bad:
         assert S.spense_gemm_planned_workspace_size(64, desc, p) == 0
         rc = S.spense_gemm_planned(1 << 28, 64, 25600, desc, None, None, 1 << 30, 5120, 0, 1 << 31, 1 << 26, p, None)

@@ -413,6 +413,31 @@ def test_large_m_kernel_exact_both_layouts(S, axis, M, N, K, db, kernel, waves):
         assert np.array_equal(run_gemm(S, w, X, sw, sx, False, big).view(np.uint16), ref["y_bf16"])
 
 
+# 256 x 256 kernel with its last row blocks as 256 x 128 tiles at the end of the grid:
+# (axis, M, N, K, db, half row blocks); ragged M (a half tile past M, a partial one),
+# ragged rows in both regions, the XCD-aware order on the full tiles with leftover row
+# blocks in place, and every row block split.
+BIG2_HALF_CASES = [(0, 700, 784, 640, 528, 1), (0, 700, 784, 640, 528, 3), (1, 300, 600, 1152, 896, 1),
+                   (0, 1024, 2048, 384, 1536, 2), (1, 2048, 1024, 256, 128, 3), (1, 2048, 1024, 256, 128, 4),
+                   (0, 520, 2304, 512, 1792, 5)]
+
+
+@pytest.mark.parametrize("axis,M,N,K,db,rh", BIG2_HALF_CASES)
+def test_large_m_half_tiles_exact(S, axis, M, N, K, db, rh):
+    """256 x 128 tail tiles (the waves of the missing token quarters only copy): bit-exact
+    against the oracle on exact-integer data, and equal to the plan without them."""
+    W, mask, X, sw, sx = gen.make_exact_int(17, M + N + rh, M, N, K, gaxis(axis), db, gen.FP8)
+    pw, (v, m, d) = compress_both(S, W, mask, FP8, axis, db)
+    ref = oracle.spense_gemm(X, v, m, d, N, K, FP8, axis, db, sw, sx)
+    pwt = S.tile(pw)
+    half = S.plan_override(kernel=BIG2, waves=8, half_row_blocks=rh)
+    whole = S.plan_override(kernel=BIG2, waves=8, half_row_blocks=0)
+    y32 = run_gemm(S, pwt, X, sw, sx, True, half)
+    assert np.array_equal(y32, ref["y_f32"])
+    assert np.array_equal(run_gemm(S, pwt, X, sw, sx, False, half).view(np.uint16), ref["y_bf16"])
+    assert np.array_equal(run_gemm(S, pwt, X, sw, sx, True, whole), y32)
+
+
 @pytest.mark.parametrize("kernel,waves", LARGE_M_KERNELS)
 @pytest.mark.parametrize("axis,db", [(0, 744), (1, 1536)])
 def test_large_m_kernel_random_within_bound(S, axis, db, kernel, waves):
