@@ -80,7 +80,7 @@ class spense_plan_override_t(ctypes.Structure):
                 ("act_tiles", ctypes.c_int32), ("ksplit", ctypes.c_int32), ("waves_used", ctypes.c_int32),
                 ("waves_used_dense", ctypes.c_int32), ("waves_used_24", ctypes.c_int32),
                 ("block_order", ctypes.c_int32), ("xcd_order", ctypes.c_int32), ("u8", ctypes.c_int32),
-                ("half_row_blocks", ctypes.c_int32)]
+                ("half_row_blocks", ctypes.c_int32), ("resident_x", ctypes.c_int32)]
 
 
 KERNEL_KSPLIT, KERNEL_ROWS, KERNEL_LARGE_M = 1, 2, 3

@@ -174,11 +174,11 @@ struct Plan {
 // choice to the planner.
 struct Override {
   int kernel = 0, rt = 0, waves = 0, ct = 0, ksplit = 0, wused = 0, wused_d = 0, wused_s = 0, order = -1, xcd = -1,
-      u8 = 0, halfrb = -1;
+      u8 = 0, halfrb = -1, xres = 0;
   bool operator==(const Override& o) const {
     return kernel == o.kernel && rt == o.rt && waves == o.waves && ct == o.ct && ksplit == o.ksplit &&
            wused == o.wused && wused_d == o.wused_d && wused_s == o.wused_s && order == o.order && xcd == o.xcd &&
-           u8 == o.u8 && halfrb == o.halfrb;
+           u8 == o.u8 && halfrb == o.halfrb && xres == o.xres;
   }
 };
 
@@ -206,6 +206,7 @@ int read_override(const spense_plan_override_t* ov, int32_t dtype, bool tiled, O
   o->xcd = ov->xcd_order;
   o->u8 = ov->u8;
   o->halfrb = ov->half_row_blocks;
+  o->xres = ov->resident_x;
   if (o->kernel < 0 || o->kernel > 4) return fail(SPENSE_ERR_ARG, "plan: unknown kernel %d", o->kernel);
   if (o->kernel == 1 && tiled) return fail(SPENSE_ERR_ARG, "plan: the K-split kernel reads the row-major layout only");
   if (o->kernel >= 3 && dtype != SPENSE_FP8_E4M3FN) return fail(SPENSE_ERR_ARG, "plan: the large-M kernels are fp8 only");
@@ -217,6 +218,7 @@ int read_override(const spense_plan_override_t* ov, int32_t dtype, bool tiled, O
   if (o->xcd < -1 || o->xcd > 1) return fail(SPENSE_ERR_ARG, "plan: xcd_order %d", o->xcd);
   if (o->u8 < 0 || o->u8 > 1) return fail(SPENSE_ERR_ARG, "plan: u8 %d", o->u8);
   if (o->halfrb < -1) return fail(SPENSE_ERR_ARG, "plan: half_row_blocks %d", o->halfrb);
+  if (o->xres < 0 || o->xres > 2) return fail(SPENSE_ERR_ARG, "plan: resident_x %d", o->xres);
   if (o->rt || o->waves) {
     bool okshape = false;
     if (o->kernel == 1) {
@@ -535,6 +537,20 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
     ksplit = chunks > 0 ? choose_ksplit(regs, nreg, pl->ls.ct, pl->ls.mblocks, chunks, M, ov) : 1;
     for (int i = 0; i < nreg; ++i) slice_cuts(regs[i], ksplit, kc, es, sparse_cost);
     choose_rows_per_group(regs, nreg, rt, waves, pl->ls.ct, pl->ls.mblocks, K, es, sparse_cost, ksplit, ov);
+    // One token tile, tiled fp8, 8 waves, no K slices: the activations of the whole K
+    // range stay in LDS (at most 160 KB: 20 chunks) and each wave streams its weights
+    // with no barrier after the first.  Measured on MI355X (graph replay, us, staged ->
+    // resident): gate / up at M = 1 / 8 / 16 17.9 / 17.6 / 17.9 -> 16.9 / 17.0 / 17.3; k
+    // at M = 1 5.8 -> 5.5 (but K-sliced), q and o at M = 16 8.7 / 9.8 -> 8.4 / 9.6.  Where
+    // a workgroup has few active waves the first barrier is not repaid (q and o at M = 1
+    // 8.0 / 9.2 -> 8.2 / 9.5), nor on down's K slices (M = 1 / 16: 19.4 / 20.4 -> 19.9 /
+    // 20.8), so it is used where every region gives a workgroup at least 4 waves.
+    if (ct == 1 && rt == 1 && waves == 8 && tiled && dtype == SPENSE_FP8_E4M3FN && ksplit == 1 && ov.xres != 1 &&
+        chunks * 8192 <= 160 * 1024) {
+      bool wide = true;
+      for (int i = 0; i < nreg; ++i) wide = wide && regs[i].wused >= 4;
+      if (wide || ov.xres == 2) pl->ls.xres = (int)chunks;
+    }
   }
   // 256 x 256 kernel: the last row blocks of the last region may run as 256 x 128 tiles
   // after every 256 x 256 tile, to fill the grid's last round

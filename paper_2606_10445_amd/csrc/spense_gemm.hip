@@ -695,13 +695,18 @@ __device__ __forceinline__ void barrier_vm_lgkm0() {
 // and slot c % NS), then a barrier that waits for the activations of chunk c+1 (issued
 // in step c+1-D, before that step's weights), so D chunks of weights stay in flight
 // across it.  The buffer being filled held chunk c-1, which every wave has finished.
-template <int DT, int CT, int RT, int WR, bool WM, int NS, int P, bool TL, int GM>
+//
+// XR (one token tile): the activations of every chunk of the workgroup's K range are
+// copied into dynamic LDS once, behind one barrier, and each wave then streams its
+// weights with no further barrier, as far ahead as its register slots allow.
+template <int DT, int CT, int RT, int WR, bool WM, int NS, int P, bool TL, int GM, bool XR = false>
 __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
   constexpr bool GR = GM == 1;   // grouped launch
   constexpr bool GLU = GM == 2;  // gate and up paired, the GLU step in the epilogue
   static_assert(!GLU || (RT == 1 && WR == 8), "paired gate / up: four waves per weight");
   static_assert(NS == 3 || NS == 4, "three or four pipeline slots");
   static_assert(!TL || (DT == kFP8 && WM), "the tiled layout is fp8 with whole-chunk metadata loads");
+  static_assert(!XR || (CT == 1 && GM == 0), "resident activations: one token tile, plain launch");
   constexpr int D = NS - 1;
   typedef XTile<DT, CT> XT;
   constexpr int KC = XT::CHUNK_K;
@@ -743,6 +748,7 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
   const bool active = wsel < R.wused && nbase < rowend;
 
   __shared__ __attribute__((aligned(1024))) uint8_t xbuf[NS][XT::BYTES];
+  extern __shared__ __attribute__((aligned(1024))) uint8_t xres[];  // XR: chunk c at (c - c_lo) * XT::BYTES
   constexpr bool FROM_MAT = GR || GLU;
   const __amdgpu_buffer_rsrc_t rx = rsrc(a.X, a.x_bytes),
                                rv = FROM_MAT ? rsrc(MD.values, MD.v_bytes) : rsrc(a.values, a.v_bytes),
@@ -798,6 +804,12 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
   auto xload = [&](int buf, int c) {
     x_to_lds<DT, CT, XI>(xbuf[buf], a, rx, m0, chunk_k(c), c < c_hi ? chunk_end(c) : -1, wave, lane);
   };
+  auto xtile = [&](int s, int c) -> const uint8_t* {
+    if constexpr (XR)
+      return xres + (c - c_lo) * XT::BYTES;
+    else
+      return xbuf[s];
+  };
 
   // A wave that owns rows loads weights and runs the MMAs; the others only stage
   // activations and take part in the barriers.  The two loops are separate so that no
@@ -808,24 +820,39 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
     // step's weights, then D-1 further steps of activations and weights
     constexpr int AFTER = ACT ? RT * NL + (D - 1) * (XI + RT * NL) : (D - 1) * XI;
     WChunk slot[NS][RT];
+    if constexpr (XR) {
+      // every chunk's activations, then the first D chunks of weights; the barrier waits
+      // for the activations only (loads complete in issue order)
+      for (int c = c_lo; c < c_hi; ++c)
+        x_to_lds<DT, CT, XI>(xres + (c - c_lo) * XT::BYTES, a, rx, m0, chunk_k(c), chunk_end(c), wave, lane);
+      if constexpr (ACT) {
 #pragma unroll
-    for (int d = 0; d < D; ++d) {
-      xload(d, c_lo + d);
-      if constexpr (ACT) load(slot[d], c_lo + d);
+        for (int d = 0; d < D; ++d) load(slot[d], c_lo + d);
+      }
+      barrier_vm<ACT ? D * RT * NL : 0>();
+      if constexpr (!ACT) return;
+    } else {
+#pragma unroll
+      for (int d = 0; d < D; ++d) {
+        xload(d, c_lo + d);
+        if constexpr (ACT) load(slot[d], c_lo + d);
+      }
+      barrier_vm<0>();
     }
-    barrier_vm<0>();
     auto step = [&](auto s_const, int c) {
       constexpr int S = decltype(s_const)::value;
       constexpr int SD = (S + D) % NS;
-      xload(SD, c + D);
-      __builtin_amdgcn_sched_barrier(0);
+      if constexpr (!XR) {
+        xload(SD, c + D);
+        __builtin_amdgcn_sched_barrier(0);
+      }
       if constexpr (ACT) {
         load(slot[SD], c + D);
         __builtin_amdgcn_sched_barrier(0);
-        mma_chunk<DT, CT, RT, WM, P>(acc, slot[S], c < n_sp, xbuf[S], li, lq);
+        mma_chunk<DT, CT, RT, WM, P>(acc, slot[S], c < n_sp, xtile(S, c), li, lq);
         __builtin_amdgcn_sched_barrier(0);
       }
-      barrier_vm<AFTER>();
+      if constexpr (!XR) barrier_vm<AFTER>();
     };
     int c = c_lo;
     for (; c + NS <= c_hi; c += NS) {
@@ -968,11 +995,36 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a) {
 // slots and two-step groups for four; fp8 without wide metadata loads (metadata rows not
 // 16-byte aligned, four separately masked loads per chunk) one step lighter, and even so
 // its four-tile, eight-wave instance spills a few registers.
+// The resident-activation instance's dynamic LDS above the default limit: a per-device
+// function attribute, set once per device under std::call_once.
+constexpr int kXresMaxBytes = 160 * 1024;
+std::once_flag g_xres_once[64];
+hipError_t g_xres_rc[64];
+
 template <int DT, int CT, int RT, int WR, bool WM, bool TL, int GM = 0>
-hipError_t launch_rows_wm(const dim3& grid, const dim3& block, const GemmArgs& a, hipStream_t s) {
+hipError_t launch_rows_wm(const dim3& grid, const dim3& block, const GemmArgs& a, hipStream_t s, int xres = 0) {
   constexpr bool light = DT == kFP8 && !WM;
   constexpr int NS = CT <= 2 && RT == 1 && !light ? 4 : 3;
   constexpr int P = CT == 1 && RT == 1 ? 4 : 1;
+  if constexpr (DT == kFP8 && CT == 1 && RT == 1 && WR == 8 && TL && GM == 0) {
+    if (xres > 0) {
+      const int lds = xres * XTile<DT, CT>::BYTES;
+      if (lds > kXresMaxBytes) return hipErrorInvalidValue;
+      auto k = spense_gemm_rows_kernel<DT, CT, RT, WR, WM, NS, P, TL, GM, true>;
+      int dev = 0;
+      hipError_t e = hipGetDevice(&dev);
+      if (e != hipSuccess) return e;
+      if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+      std::call_once(g_xres_once[dev], [&] {
+        g_xres_rc[dev] = hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                             kXresMaxBytes);
+      });
+      if (g_xres_rc[dev] != hipSuccess) return g_xres_rc[dev];
+      hipLaunchKernelGGL(k, grid, block, lds, s, a);
+      return hipGetLastError();
+    }
+  }
+  if (xres > 0) return hipErrorInvalidValue;
   hipLaunchKernelGGL((spense_gemm_rows_kernel<DT, CT, RT, WR, WM, NS, P, TL, GM>), grid, block, 0, s, a);
   return hipGetLastError();
 }
@@ -988,10 +1040,11 @@ hipError_t launch_rows(const LaunchShape& ls, const GemmArgs& a, hipStream_t s) 
       }
       return hipErrorInvalidValue;
     }
-    if (a.tiled) return launch_rows_wm<DT, CT, RT, WR, true, true>(grid, block, a, s);
+    if (a.tiled) return launch_rows_wm<DT, CT, RT, WR, true, true>(grid, block, a, s, ls.xres);
+    if (ls.xres) return hipErrorInvalidValue;
     if (a.m_ld_b % 16 == 0) return launch_rows_wm<DT, CT, RT, WR, true, false>(grid, block, a, s);
   }
-  if (a.tiled) return hipErrorInvalidValue;
+  if (a.tiled || ls.xres) return hipErrorInvalidValue;
   return launch_rows_wm<DT, CT, RT, WR, false, false>(grid, block, a, s);
 }
 

@@ -105,6 +105,7 @@ struct LaunchShape {
   int rows;     // row-split workgroups with activations staged in LDS
   int big;      // large-M kernels (fp8): 1 = 128-row x 256-token workgroup tiles, 2 = 256 x 256
   int glu;      // row-split kernel, gate and up paired: waves 0-3 gate tiles, 4-7 the same up tiles
+  int xres;     // row-split kernel, one token tile: >0 = the activations of all xres chunks stay in LDS
 };
 
 hipError_t launch_gemm(int dtype, const LaunchShape& ls, const GemmArgs& a, hipStream_t s);

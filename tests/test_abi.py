@@ -41,7 +41,7 @@ def test_library_exports_every_declared_symbol(S):
     for n in _declared():
         assert hasattr(lib, n), f"{n} declared in include/ but not exported"
     assert set(_declared()) == set(S.EXPORTS)
-    assert S.spense_abi_version() == 11
+    assert S.spense_abi_version() == 12
 
 
 @pytest.mark.parametrize("N,K,split,db", [(256, 512, 0, 192), (256, 512, 1, 384), (25600, 5120, 0, 19200),
@@ -406,7 +406,7 @@ def test_plan_override_is_checked_on_the_host(S):
            (rm, po(kernel=3, waves=16)),
            (rm, po(waves=8)),                       # a shape needs the kernel it is for
            (rm, po(kernel=5)), (rm, po(ksplit=9)), (rm, po(act_tiles=3)), (rm, po(waves_used=9)),
-           (rm, po(block_order=3)), (rm, po(xcd_order=2)), (rm, po(u8=2)), (rm, po(half_row_blocks=-2))]
+           (rm, po(block_order=3)), (rm, po(xcd_order=2)), (rm, po(u8=2)), (rm, po(half_row_blocks=-2)), (rm, po(resident_x=3))]
     for desc, p in bad:
         assert S.spense_gemm_planned_workspace_size(64, desc, p) == 0
         rc = S.spense_gemm_planned(1 << 28, 64, 25600, desc, None, None, 1 << 30, 5120, 0, 1 << 31, 1 << 26, p, None)

@@ -438,6 +438,29 @@ def test_large_m_half_tiles_exact(S, axis, M, N, K, db, rh):
     assert np.array_equal(run_gemm(S, pwt, X, sw, sx, True, whole), y32)
 
 
+# One token tile with the whole K range of activations resident in LDS: (axis, M, N, K,
+# db); ragged M, N and K, both regions, 1 to 20 chunks of 512 columns (the LDS limit).
+XRES_CASES = [(0, 1, 300, 640, 208), (0, 16, 1040, 5120, 784), (1, 7, 520, 2080, 1536), (1, 13, 264, 10240, 7680),
+              (0, 5, 2064, 10240, 1040), (1, 16, 48, 512, 256)]
+
+
+@pytest.mark.parametrize("axis,M,N,K,db", XRES_CASES)
+def test_resident_activations_exact(S, axis, M, N, K, db):
+    """The row-split kernel with every chunk's activations kept in LDS (forced on, also
+    where the planner would not choose it): bit-exact against the oracle on exact-integer
+    data and equal to the chunk-by-chunk staging."""
+    W, mask, X, sw, sx = gen.make_exact_int(19, M + N + K, M, N, K, gaxis(axis), db, gen.FP8)
+    pw, (v, m, d) = compress_both(S, W, mask, FP8, axis, db)
+    ref = oracle.spense_gemm(X, v, m, d, N, K, FP8, axis, db, sw, sx)
+    pwt = S.tile(pw)
+    on = S.plan_override(kernel=ROWS, row_tiles=1, waves=8, ksplit=1, resident_x=2)
+    off = S.plan_override(kernel=ROWS, row_tiles=1, waves=8, ksplit=1, resident_x=1)
+    y32 = run_gemm(S, pwt, X, sw, sx, True, on)
+    assert np.array_equal(y32, ref["y_f32"])
+    assert np.array_equal(run_gemm(S, pwt, X, sw, sx, False, on).view(np.uint16), ref["y_bf16"])
+    assert np.array_equal(run_gemm(S, pwt, X, sw, sx, True, off), y32)
+
+
 @pytest.mark.parametrize("kernel,waves", LARGE_M_KERNELS)
 @pytest.mark.parametrize("axis,db", [(0, 744), (1, 1536)])
 def test_large_m_kernel_random_within_bound(S, axis, db, kernel, waves):
