@@ -71,11 +71,17 @@ def kernel_source_sha():
 EAGER = False
 
 
+WARM_MS = 30.0  # untimed graph replays before the timed one, at least this long in total
+
+
 def time_launches(fn, steps, warmup, torch):
     """Run `warmup` eager steps, capture exactly `steps` launches in one HIP graph, and
     time one replay with HIP events on the stream the kernels run on (the current
     stream); returns ms per step.  The graph removes host launch overhead between the
-    kernels, as in a graph-captured decode loop."""
+    kernels, as in a graph-captured decode loop.  Before the timed replay, untimed
+    replays run for at least WARM_MS (at most 16 of them): the first replay uploads the
+    graph, and a GPU coming from lighter work needs some tens of milliseconds of load to
+    reach its steady clock (the first 2048-token GEMMs of a process measured ~8% slower)."""
     for i in range(warmup):
         fn(i)
     torch.cuda.synchronize()
@@ -92,11 +98,18 @@ def time_launches(fn, steps, warmup, torch):
     with torch.cuda.graph(g):
         for i in range(steps):
             fn(i)
-    g.replay()  # untimed: first replay uploads the graph
-    torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
+    warm = 0.0
+    for _ in range(16):  # untimed
+        t0.record(stream)
+        g.replay()
+        t1.record(stream)
+        torch.cuda.synchronize()
+        warm += t0.elapsed_time(t1)
+        if warm >= WARM_MS:
+            break
     t0.record(stream)
     g.replay()
     t1.record(stream)
