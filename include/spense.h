@@ -281,10 +281,11 @@ typedef struct spense_plan_override_t {
   int32_t half_row_blocks;  /* 256 x 256 kernel: -1 planner, else this many 256-row blocks
                                at the end of the last region run as 256 x 128 tiles, after
                                all 256 x 256 tiles (capped at the region's row blocks) */
-  int32_t resident_x;       /* row-split kernel with one token tile, tiled fp8, 8 waves, no
-                               K slices: 0 planner, 1 activations staged chunk by chunk,
-                               2 the whole K range of activations kept in LDS (where it
-                               fits: at most 20 chunks of 512 columns) */
+  int32_t resident_x;       /* row-split kernel with one or two token tiles, tiled fp8, 8
+                               waves, no K slices: 0 planner, 1 activations staged chunk by
+                               chunk, 2 the whole K range of activations kept in LDS (where
+                               it fits: 160 KB, i.e. 20 chunks of 512 columns with one token
+                               tile, 10 with two) */
 } spense_plan_override_t;
 
 /*

@@ -537,16 +537,18 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
     ksplit = chunks > 0 ? choose_ksplit(regs, nreg, pl->ls.ct, pl->ls.mblocks, chunks, M, ov) : 1;
     for (int i = 0; i < nreg; ++i) slice_cuts(regs[i], ksplit, kc, es, sparse_cost);
     choose_rows_per_group(regs, nreg, rt, waves, pl->ls.ct, pl->ls.mblocks, K, es, sparse_cost, ksplit, ov);
-    // One token tile, tiled fp8, 8 waves, no K slices: the activations of the whole K
-    // range stay in LDS (at most 160 KB: 20 chunks) and each wave streams its weights
-    // with no barrier after the first.  Measured on MI355X (graph replay, us, staged ->
-    // resident): gate / up at M = 1 / 8 / 16 17.9 / 17.6 / 17.9 -> 16.9 / 17.0 / 17.3; k
+    // One or two token tiles, tiled fp8, 8 waves, no K slices: the activations of the
+    // whole K range stay in LDS (at most 160 KB: 20 chunks with one token tile, 10 with
+    // two) and each wave streams its weights with no barrier after the first.  Measured
+    // on MI355X (graph replay, us, staged -> resident): gate / up at M = 1 / 8 / 16 17.9 /
+    // 17.6 / 17.9 -> 16.9 / 17.0 / 17.3, at M = 17 / 24 / 32 19.1 / 19.4 / 20.0 -> 18.6 /
+    // 18.7 / 19.3; k
     // at M = 1 5.8 -> 5.5 (but K-sliced), q and o at M = 16 8.7 / 9.8 -> 8.4 / 9.6.  Where
     // a workgroup has few active waves the first barrier is not repaid (q and o at M = 1
     // 8.0 / 9.2 -> 8.2 / 9.5), nor on down's K slices (M = 1 / 16: 19.4 / 20.4 -> 19.9 /
     // 20.8), so it is used where every region gives a workgroup at least 4 waves.
-    if (ct == 1 && rt == 1 && waves == 8 && tiled && dtype == SPENSE_FP8_E4M3FN && ksplit == 1 && ov.xres != 1 &&
-        chunks * 8192 <= 160 * 1024) {
+    if (ct <= 2 && rt == 1 && waves == 8 && tiled && dtype == SPENSE_FP8_E4M3FN && ksplit == 1 && ov.xres != 1 &&
+        chunks * 8192 * ct <= 160 * 1024) {
       bool wide = true;
       for (int i = 0; i < nreg; ++i) wide = wide && regs[i].wused >= 4;
       if (wide || ov.xres == 2) pl->ls.xres = (int)chunks;

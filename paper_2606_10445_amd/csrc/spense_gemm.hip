@@ -696,8 +696,8 @@ __device__ __forceinline__ void barrier_vm_lgkm0() {
 // in step c+1-D, before that step's weights), so D chunks of weights stay in flight
 // across it.  The buffer being filled held chunk c-1, which every wave has finished.
 //
-// XR (one token tile): the activations of every chunk of the workgroup's K range are
-// copied into dynamic LDS once, behind one barrier, and each wave then streams its
+// XR (one or two token tiles): the activations of every chunk of the workgroup's K range
+// are copied into dynamic LDS once, behind one barrier, and each wave then streams its
 // weights with no further barrier, as far ahead as its register slots allow.
 template <int DT, int CT, int RT, int WR, bool WM, int NS, int P, bool TL, int GM, bool XR = false>
 __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
@@ -706,7 +706,7 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
   static_assert(!GLU || (RT == 1 && WR == 8), "paired gate / up: four waves per weight");
   static_assert(NS == 3 || NS == 4, "three or four pipeline slots");
   static_assert(!TL || (DT == kFP8 && WM), "the tiled layout is fp8 with whole-chunk metadata loads");
-  static_assert(!XR || (CT == 1 && GM == 0), "resident activations: one token tile, plain launch");
+  static_assert(!XR || (CT <= 2 && GM == 0), "resident activations: one or two token tiles, plain launch");
   constexpr int D = NS - 1;
   typedef XTile<DT, CT> XT;
   constexpr int KC = XT::CHUNK_K;
@@ -995,18 +995,16 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a) {
 // slots and two-step groups for four; fp8 without wide metadata loads (metadata rows not
 // 16-byte aligned, four separately masked loads per chunk) one step lighter, and even so
 // its four-tile, eight-wave instance spills a few registers.
-// The resident-activation instance's dynamic LDS above the default limit: a per-device
-// function attribute, set once per device under std::call_once.
+// The resident-activation instances' dynamic LDS above the default limit: a per-device
+// function attribute, set once per (device, instance) under std::call_once.
 constexpr int kXresMaxBytes = 160 * 1024;
-std::once_flag g_xres_once[64];
-hipError_t g_xres_rc[64];
 
 template <int DT, int CT, int RT, int WR, bool WM, bool TL, int GM = 0>
 hipError_t launch_rows_wm(const dim3& grid, const dim3& block, const GemmArgs& a, hipStream_t s, int xres = 0) {
   constexpr bool light = DT == kFP8 && !WM;
   constexpr int NS = CT <= 2 && RT == 1 && !light ? 4 : 3;
   constexpr int P = CT == 1 && RT == 1 ? 4 : 1;
-  if constexpr (DT == kFP8 && CT == 1 && RT == 1 && WR == 8 && TL && GM == 0) {
+  if constexpr (DT == kFP8 && CT <= 2 && RT == 1 && WR == 8 && TL && GM == 0) {
     if (xres > 0) {
       const int lds = xres * XTile<DT, CT>::BYTES;
       if (lds > kXresMaxBytes) return hipErrorInvalidValue;
@@ -1015,11 +1013,13 @@ hipError_t launch_rows_wm(const dim3& grid, const dim3& block, const GemmArgs& a
       hipError_t e = hipGetDevice(&dev);
       if (e != hipSuccess) return e;
       if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
-      std::call_once(g_xres_once[dev], [&] {
-        g_xres_rc[dev] = hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize,
-                                             kXresMaxBytes);
+      static std::once_flag once[64];  // one set per instance of this function
+      static hipError_t rc[64];
+      std::call_once(once[dev], [&] {
+        rc[dev] = hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                      kXresMaxBytes);
       });
-      if (g_xres_rc[dev] != hipSuccess) return g_xres_rc[dev];
+      if (rc[dev] != hipSuccess) return rc[dev];
       hipLaunchKernelGGL(k, grid, block, lds, s, a);
       return hipGetLastError();
     }

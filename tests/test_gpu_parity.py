@@ -438,10 +438,12 @@ def test_large_m_half_tiles_exact(S, axis, M, N, K, db, rh):
     assert np.array_equal(run_gemm(S, pwt, X, sw, sx, True, whole), y32)
 
 
-# One token tile with the whole K range of activations resident in LDS: (axis, M, N, K,
-# db); ragged M, N and K, both regions, 1 to 20 chunks of 512 columns (the LDS limit).
+# One or two token tiles with the whole K range of activations resident in LDS: (axis, M,
+# N, K, db); ragged M, N and K, both regions, up to 20 chunks of 512 columns with one
+# token tile and 10 with two (the LDS limit).
 XRES_CASES = [(0, 1, 300, 640, 208), (0, 16, 1040, 5120, 784), (1, 7, 520, 2080, 1536), (1, 13, 264, 10240, 7680),
-              (0, 5, 2064, 10240, 1040), (1, 16, 48, 512, 256)]
+              (0, 5, 2064, 10240, 1040), (1, 16, 48, 512, 256), (0, 17, 1040, 5120, 784), (1, 32, 520, 4608, 3584),
+              (0, 29, 300, 640, 208)]
 
 
 @pytest.mark.parametrize("axis,M,N,K,db", XRES_CASES)
