@@ -1246,6 +1246,13 @@ int spense_gemm_grouped(const void* X, int64_t M, int64_t ldx, int32_t count, co
     groups += regs[i].nrb;
     a.reg[i] = regs[i];
   }
+  // activations resident in LDS wherever they fit (one or two token tiles, K <= 5120 with
+  // two): measured on MI355X (graph replay, us, staged -> resident): q / k / v grouped at
+  // M = 1 / 16 / 32 9.6 / 9.7 / 13.0 -> 8.8 / 9.1 / 11.3 (Seed-OSS shapes 10.8 / 11.3 /
+  // 13.6 -> 10.6 / 10.8 / 12.4), gate / up grouped 34.5 / 35.8 / 42.8 -> 34.0 / 35.0 /
+  // 41.4; unlike one weight alone, also with few waves per workgroup
+  const int64_t nch = ceil_div(K, kc);
+  if (ls.ct <= 2 && nch * 8192 * ls.ct <= 160 * 1024) ls.xres = (int)nch;
   a.nreg = nreg;
   a.groups = groups;
   a.tiled = 1;

@@ -706,7 +706,7 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
   static_assert(!GLU || (RT == 1 && WR == 8), "paired gate / up: four waves per weight");
   static_assert(NS == 3 || NS == 4, "three or four pipeline slots");
   static_assert(!TL || (DT == kFP8 && WM), "the tiled layout is fp8 with whole-chunk metadata loads");
-  static_assert(!XR || (CT <= 2 && GM == 0), "resident activations: one or two token tiles, plain launch");
+  static_assert(!XR || (CT <= 2 && GM <= 1), "resident activations: one or two token tiles, plain or grouped launch");
   constexpr int D = NS - 1;
   typedef XTile<DT, CT> XT;
   constexpr int KC = XT::CHUNK_K;
@@ -1004,7 +1004,7 @@ hipError_t launch_rows_wm(const dim3& grid, const dim3& block, const GemmArgs& a
   constexpr bool light = DT == kFP8 && !WM;
   constexpr int NS = CT <= 2 && RT == 1 && !light ? 4 : 3;
   constexpr int P = CT == 1 && RT == 1 ? 4 : 1;
-  if constexpr (DT == kFP8 && CT <= 2 && RT == 1 && WR == 8 && TL && GM == 0) {
+  if constexpr (DT == kFP8 && CT <= 2 && RT == 1 && WR == 8 && TL && GM <= 1) {
     if (xres > 0) {
       const int lds = xres * XTile<DT, CT>::BYTES;
       if (lds > kXresMaxBytes) return hipErrorInvalidValue;
@@ -1036,7 +1036,7 @@ hipError_t launch_rows(const LaunchShape& ls, const GemmArgs& a, hipStream_t s) 
     if (a.tiled && (a.nmat > 1 || ls.glu)) {  // grouped or paired launch: tiled fp8, 8 waves
       if constexpr (RT == 1 && WR == 8) {
         if (ls.glu) return launch_rows_wm<DT, CT, RT, WR, true, true, 2>(grid, block, a, s);
-        return launch_rows_wm<DT, CT, RT, WR, true, true, 1>(grid, block, a, s);
+        return launch_rows_wm<DT, CT, RT, WR, true, true, 1>(grid, block, a, s, ls.xres);
       }
       return hipErrorInvalidValue;
     }

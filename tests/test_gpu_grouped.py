@@ -66,6 +66,8 @@ GROUP_CASES = [  # M, K, [(N, dense fraction)]
     (64, 1024, [(320, 0.25), (64, 0.25), (64, 0.25)]),
     (100, 640, [(256, 0.0), (96, 1.0), (144, 0.25), (16, 0.25)]),
     (33, 384, [(512, 0.25)]),
+    (32, 5120, [(128, 0.25), (48, 0.25)]),   # two token tiles, activations resident: 160 KB
+    (9, 10240, [(96, 0.25), (32, 0.5)]),     # one token tile, 20 chunks resident
 ]
 
 
