@@ -442,8 +442,8 @@ def measure_down_sweep(torch, gen, S):
 def measure_seed_layer(torch, gen, S):
     """The Seed-OSS-36B-like layer linears (q 10240 x 5120, k / v 1024 x 5120, o 5120 x
     10240 input-split, gate / up 27648 x 5120, down 5120 x 27648 input-split; 25% dense)
-    per layer at M = 1 / 4 / 16 / 64 / 256 / 2048: seven launches, and at M <= 64 also
-    four (q, k, v and gate, up grouped); two copies of the set rotated."""
+    per layer at M = 1 / 4 / 16 / 64 / 256 / 2048: seven launches, and also four (q, k, v
+    and gate, up grouped); two copies of the set rotated."""
     shapes = gen.SEED_OSS_36B_LAYER
     mats = []
     for i, (name, n_, k_, ax) in enumerate(shapes):
@@ -474,8 +474,7 @@ def measure_seed_layer(torch, gen, S):
 
         steps = 20 if M >= 256 else 100
         rec = {"us_per_layer": round(time_launches(layer, steps, 3, torch) * 1e3, 1)}
-        if M <= 64:
-            rec["grouped_us_per_layer"] = round(time_launches(layer_grouped, steps, 3, torch) * 1e3, 1)
+        rec["grouped_us_per_layer"] = round(time_launches(layer_grouped, steps, 3, torch) * 1e3, 1)
         out[f"m{M}"] = rec
         del io
     return out

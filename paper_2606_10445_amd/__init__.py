@@ -638,16 +638,16 @@ def mlp(X: torch.Tensor, x_scale: torch.Tensor, gate: PackedWeight, up: PackedWe
     the quantisation from the epilogue's row maxima; otherwise G and U in fp32 and the GLU
     fused with the quantisation), Y = down(Hq) (input-split, bf16 out).  X: fp8 codes
     with x_scale."""
-    # the paired and grouped launches run the row-split kernel, which pays for one block
-    # of up to 64 tokens; above that two plans of their own (the large-M kernel on large
-    # weights) are faster
-    one_block = X.shape[0] <= 64
-    paired = (gate.kind == up.kind == SPENSE_LAYOUT_TILED and gate.dtype == up.dtype == SPENSE_FP8_E4M3FN
-              and gate.split == up.split == SPENSE_SPLIT_OUTPUT and one_block)
+    # the paired launch runs the row-split kernel, which pays for one block of up to 64
+    # tokens; above that the grouped call (one 256 x 256 tile grid over both weights where
+    # it fills the GPU, else a plan per weight) gives G and U
+    groupable = (gate.kind == up.kind == SPENSE_LAYOUT_TILED and gate.dtype == up.dtype == SPENSE_FP8_E4M3FN
+                 and gate.split == up.split == SPENSE_SPLIT_OUTPUT)
+    paired = groupable and X.shape[0] <= 64
     if paired and gate.N == up.N and gate.K == up.K and gate.dense_begin == up.dense_begin:
         Hq, sh = gemm_glu_fp8(X, gate, up, gate_scale, up_scale, x_scale, workspace=workspace)
     else:
-        if paired and gate.K == up.K:
+        if groupable and gate.K == up.K:
             scales = None if gate_scale is None and up_scale is None else [gate_scale, up_scale]
             G, U = gemm_grouped(X, [gate, up], scales, x_scale, out_f32=True)
         else:

@@ -1225,6 +1225,57 @@ int spense_gemm_grouped(const void* X, int64_t M, int64_t ldx, int32_t count, co
       slice_cuts(r, 1, kc, 1, sparse_cost);
       regs[nreg++] = r;
     }
+  // Many tokens: the 256 x 256 large-M kernel over every weight's regions in one grid, on
+  // the single-weight rule (at least 160 tiles; with two or three token blocks the last
+  // one full), with its tail tiles and XCD-aware order; small weights such as k and v then
+  // ride in q's grid instead of leaving most CUs idle (alone at M = 2048 they run 37 us on
+  // the row-split kernel).
+  const int64_t T256 = ceil_div(M, 256);
+  int64_t rb256 = 0;
+  for (int i = 0; i < nreg; ++i) rb256 += ceil_div(regs[i].rows, 256);
+  const bool big2 = M >= kBigMinM && rb256 * T256 >= 160 && (T256 >= 4 || M % 256 == 0);
+  if (M >= kBigMinM && !big2) {
+    // Between one token block and the 256 x 256 grid each weight's own plan (the 128 x
+    // 256 large-M kernel on large weights) beats one row-split grid over all of them
+    // (Seed-OSS q / k / v at M = 512: 75 against 95 us): one launch per weight.  Plans
+    // above 64 tokens use no K slices, so they need no workspace.
+    for (int i = 0; i < count; ++i) {
+      const int r = spense_gemm(X, M, ldx, packed[i], w_scales ? w_scales[i] : nullptr, x_scale, Y[i], ldy[i], out_flags,
+                                nullptr, 0, stream);
+      if (r) return r;
+    }
+    return ok();
+  }
+  if (big2) {
+    ls.rows = 0;
+    ls.big = 2;
+    ls.ct = 4;
+    ls.mblocks = 1;
+    const int64_t GT = xcd_token_group(T256);
+    const int64_t rc = GT > 0 ? 8 / (T256 / GT) : 1;
+    const int64_t rbl = ceil_div(regs[nreg - 1].rows, 256);
+    const int64_t half_rb = choose_half_rows(regs, nreg, T256, M, rc);
+    int32_t groups = 0;
+    for (int i = 0; i < nreg; ++i) {
+      regs[i].nrb = (int32_t)((ceil_div(regs[i].rows, 256) - (i == nreg - 1 ? half_rb : 0)) * T256);
+      regs[i].wg0 = groups;
+      groups += regs[i].nrb;
+      a.reg[i] = regs[i];
+    }
+    a.tblocks = (int32_t)T256;
+    a.hg0 = groups;
+    a.hrb0 = (int32_t)(rbl - half_rb);
+    a.hper = (int32_t)ceil_div(M, 128);
+    a.groups = (int32_t)(groups + half_rb * a.hper);
+    if (GT > 0) {
+      const int64_t rbx = (rb256 - half_rb) / rc * rc;
+      if (rbx > 0) {
+        a.xgt = (int32_t)GT;
+        a.xrc = (int32_t)rc;
+        a.xg1 = (int32_t)(rbx * T256);
+      }
+    }
+  } else {
   // rows per workgroup: w0 waves for dense regions, w1 for 2:4 regions (cost model of
   // pick_waves)
   const double tile_d = 16.0 * K, tile_s = 16.0 * sparse_cost * K, x_cost = 0.25 * 16.0 * ls.ct * K;
@@ -1253,8 +1304,9 @@ int spense_gemm_grouped(const void* X, int64_t M, int64_t ldx, int32_t count, co
   // 41.4; unlike one weight alone, also with few waves per workgroup
   const int64_t nch = ceil_div(K, kc);
   if (ls.ct <= 2 && nch * 8192 * ls.ct <= 160 * 1024) ls.xres = (int)nch;
-  a.nreg = nreg;
   a.groups = groups;
+  }
+  a.nreg = nreg;
   a.tiled = 1;
   a.X = static_cast<const uint8_t*>(X);
   a.ldx_b = ldx;
@@ -1288,7 +1340,7 @@ int spense_gemm_grouped(const void* X, int64_t M, int64_t ldx, int32_t count, co
   a.sw = m0.sw;
   a.vec_store = m0.vec_store;
   a.N = (int32_t)packed[0]->N;
-  if (groups == 0) return ok();
+  if (a.groups == 0) return ok();
   int rc = check_device();
   if (rc) return rc;
   hipError_t e = spense::launch_gemm(SPENSE_FP8_E4M3FN, ls, a, stream);

@@ -1437,6 +1437,9 @@ __device__ __forceinline__ void lds_load16(__amdgpu_buffer_rsrc_t r, uint8_t* ds
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)dst, 16, voff, soff, 0, AUX);
 }
 
+// GR: a grouped launch (several weights sharing X and K): up to kMaxRegions regions, each
+// reading its weight's buffers, output and scales from a.mat[R.mat].
+template <bool GR>
 __global__ __launch_bounds__(512) void spense_gemm_big2_kernel(GemmArgs a) {
   constexpr int WV = 8, NT = kB2RowTiles, RPW = 8, TC = 4;
   constexpr int TU = NT / WV;                // row tiles whose weights a wave copies
@@ -1459,7 +1462,13 @@ __global__ __launch_bounds__(512) void spense_gemm_big2_kernel(GemmArgs a) {
       const int x = g & 7, l = g >> 3, tg = x % TGc, rc = x / TGc;
       g = ((l / GT) * RC + rc) * T + tg * GT + l % GT;
     }
-    ri = (a.nreg > 1 && g >= a.reg[1].wg0) ? 1 : 0;
+    ri = 0;
+    if constexpr (GR) {
+      for (int i = 1; i < a.nreg; ++i)
+        if (g >= a.reg[i].wg0) ri = i;
+    } else {
+      ri = (a.nreg > 1 && g >= a.reg[1].wg0) ? 1 : 0;
+    }
     rb = (g - a.reg[ri].wg0) / a.tblocks;
     m0 = (g - a.reg[ri].wg0) % a.tblocks * kB2Tokens;
   } else {
@@ -1476,8 +1485,11 @@ __global__ __launch_bounds__(512) void spense_gemm_big2_kernel(GemmArgs a) {
   const int K = R.kend, kbound = R.kbound;
 
   extern __shared__ __attribute__((aligned(1024))) uint8_t big_lds[];
-  const __amdgpu_buffer_rsrc_t rx = rsrc(a.X, a.x_bytes), rv = rsrc(a.values, a.v_bytes),
-                               rm = rsrc(a.meta, a.m_bytes), rd = rsrc(a.dense, a.d_bytes);
+  const MatDesc& MD = a.mat[GR ? R.mat : 0];
+  const __amdgpu_buffer_rsrc_t rx = rsrc(a.X, a.x_bytes),
+                               rv = GR ? rsrc(MD.values, MD.v_bytes) : rsrc(a.values, a.v_bytes),
+                               rm = GR ? rsrc(MD.meta, MD.m_bytes) : rsrc(a.meta, a.m_bytes),
+                               rd = GR ? rsrc(MD.dense, MD.d_bytes) : rsrc(a.dense, a.d_bytes);
   v4f acc[RPW][TC];
 #pragma unroll
   for (int t = 0; t < RPW; ++t)
@@ -1674,7 +1686,12 @@ __global__ __launch_bounds__(512) void spense_gemm_big2_kernel(GemmArgs a) {
     for (int c = 0; c < TC; ++c) {
       const int m = m0 + 16 * (TC * wc + c) + li;
       const int n0 = rblk + 16 * (RPW * wr + t) + 4 * lq;
-      if (m < a.M && n0 < rowend) store4(a, acc[t][c], m, n0, rowend);
+      if (m < a.M && n0 < rowend) {
+        if constexpr (GR)
+          store4(MD.Y, MD.ldy, MD.sw, MD.vec_store, a, acc[t][c], m, n0, rowend);
+        else
+          store4(a, acc[t][c], m, n0, rowend);
+      }
     }
 }
 
@@ -1682,8 +1699,8 @@ __global__ __launch_bounds__(512) void spense_gemm_big2_kernel(GemmArgs a) {
 // attribute: set once per (device, kernel instance), under std::call_once, so that host
 // threads making their first large-M call together do not race.
 constexpr int kMaxDevices = 64;
-std::once_flag g_big_lds_once[kMaxDevices][2][3];  // [device][tiled][kernel instance]
-hipError_t g_big_lds_rc[kMaxDevices][2][3];
+std::once_flag g_big_lds_once[kMaxDevices][2][4];  // [device][tiled][kernel instance]
+hipError_t g_big_lds_rc[kMaxDevices][2][4];
 
 template <typename KernelT>
 hipError_t set_big_lds(KernelT k, int tiled, int which, int lds) {
@@ -1701,9 +1718,11 @@ hipError_t set_big_lds(KernelT k, int tiled, int which, int lds) {
 hipError_t launch_big2(const GemmArgs& a, hipStream_t s) {
   static_assert(kB2Lds <= 160 * 1024, "LDS of a CU");
   if (!a.tiled) return hipErrorInvalidValue;  // the planner sends row-major weights to the 128 x 256 kernel
-  hipError_t e = set_big_lds(spense_gemm_big2_kernel, 1, 2, kB2Lds);
+  const bool gr = a.nmat > 1;
+  auto k = gr ? spense_gemm_big2_kernel<true> : spense_gemm_big2_kernel<false>;
+  hipError_t e = set_big_lds(k, 1, gr ? 3 : 2, kB2Lds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(spense_gemm_big2_kernel, dim3(a.groups), dim3(512), kB2Lds, s, a);
+  hipLaunchKernelGGL(k, dim3(a.groups), dim3(512), kB2Lds, s, a);
   return hipGetLastError();
 }
 

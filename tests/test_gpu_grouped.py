@@ -87,6 +87,31 @@ def test_grouped_exact(S, M, K, shapes):
             assert np.array_equal(got, ref["y_f32" if out_f32 else "y_bf16"])
 
 
+# Many tokens: the grouped 256 x 256 large-M launch (at least 160 tiles), its tail tiles and
+# XCD-aware order over every weight's regions; between 64 tokens and that grid, one launch
+# per weight; (M, K, [(N, dense fraction)]).
+GROUP_LARGE_M_CASES = [
+    (4096, 256, [(1280, 0.25), (640, 0.25), (640, 0.5)]),   # 11 row blocks x 16 token blocks
+    (3400, 384, [(1536, 0.25), (768, 0.25), (768, 0.25)]),  # 12 x 14, ragged M
+    (520, 256, [(640, 0.25), (256, 0.25), (200, 0.5)]),     # 5 x 3: per-weight launches
+    (65, 512, [(512, 0.25), (128, 0.25)]),                  # just above the row-split range
+]
+
+
+@pytest.mark.parametrize("M,K,shapes", GROUP_LARGE_M_CASES)
+def test_grouped_large_m_exact(S, M, K, shapes):
+    say(f"[grouped large-M exact] M={M} K={K} {shapes}")
+    ws, X, sx = weights(11 + M % 7, shapes, M, K)
+    pws = [packed(S, W, mask, db) for (W, mask, sw, db) in ws]
+    sws = [tdev(sw) for (_, _, sw, _) in ws]
+    ys = S.gemm_grouped(tdev(X), pws, sws, tdev(sx), out_f32=True)
+    torch.cuda.synchronize()
+    for (W, mask, sw, db), y in zip(ws, ys):
+        v, m, d, bad = oracle.compress(W, mask, FP8, 0, db)
+        ref = oracle.spense_gemm(X, v, m, d, W.shape[0], K, FP8, 0, db, sw, sx)
+        assert np.array_equal(y.cpu().numpy(), ref["y_f32"])
+
+
 def test_grouped_random_within_bound(S):
     M, K = 48, 1536
     shapes = [(640, 0.25), (128, 0.25), (128, 0.25)]

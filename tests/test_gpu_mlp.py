@@ -159,7 +159,8 @@ def _packed(S, seed, name, N, K, axis, frac):
 
 @pytest.mark.timeout(300)
 @pytest.mark.parametrize("D,I,Ms,frac", [(256, 512, [1, 5, 33, 64, 65, 300], 0.25), (512, 768, [7], 0.5),
-                                         (5120, 25600, [64], 0.25)])
+                                         (5120, 25600, [64], 0.25),
+                                         (384, 4096, [2048], 0.25)])  # gate + up: one 256 x 256 grid
 def test_mlp_block_matches_oracle(S, D, I, Ms, frac):
     """gate / up (I x D, output-split) -> GLU + quantise -> down (D x I, input-split), in
     both storage layouts of the weights."""
