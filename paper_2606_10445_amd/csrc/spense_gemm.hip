@@ -301,17 +301,9 @@ __device__ __forceinline__ uint32_t bf16_bits(float v) {
 
 // Epilogue of 4 consecutive output rows n0.. of token m: (acc * w_scale[n]) * x_scale[m],
 // bf16 (round to nearest even) or fp32, one vector store where allowed.
-__device__ __forceinline__ void store4(void* Y, int64_t ldy, const float* sw, int vec_store, const GemmArgs& a,
-                                       v4f acc, int m, int n0, int rowend) {
-  const float xs = a.sx ? a.sx[m] : 1.0f;
-  float v[4];
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int n = n0 + r < rowend ? n0 + r : rowend - 1;
-    float y = acc[r];
-    if (sw) y = y * sw[n];
-    v[r] = y * xs;
-  }
+// Y[m, n0 + r] = v[r] for r < 4 (rows before rowend), bf16 RNE or fp32 per a.out_f32.
+__device__ __forceinline__ void put4(void* Y, int64_t ldy, int vec_store, const GemmArgs& a, const float (&v)[4], int m,
+                                     int n0, int rowend) {
   if (a.out_f32) {
     float* yp = reinterpret_cast<float*>(Y) + (int64_t)m * ldy + n0;
     if (vec_store && n0 + 3 < rowend) {
@@ -334,6 +326,58 @@ __device__ __forceinline__ void store4(void* Y, int64_t ldy, const float* sw, in
         if (n0 + r < rowend) yp[r] = (uint16_t)bb[r];
     }
   }
+}
+
+// The epilogue of one output quad: Y[m, n0 + r] = (acc[r] * w_scale[n]) * x_scale[m]
+// (each factor only where given), fp32, then put4.
+__device__ __forceinline__ void store4(void* Y, int64_t ldy, const float* sw, int vec_store, const GemmArgs& a,
+                                       v4f acc, int m, int n0, int rowend) {
+  const float xs = a.sx ? a.sx[m] : 1.0f;
+  float v[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int n = n0 + r < rowend ? n0 + r : rowend - 1;
+    float y = acc[r];
+    if (sw) y = y * sw[n];
+    v[r] = y * xs;
+  }
+  put4(Y, ldy, vec_store, a, v, m, n0, rowend);
+}
+
+// The scales of one wave's RT x CT output quads (rows n0 + 16 t + [0, 4), token m0 +
+// 16 c), loaded together before any output store: read next to each store, a scale load
+// would follow stores that may alias it and wait for their acknowledgement, one memory
+// round trip per quad.  Rows past the region and tokens past M read the last valid one
+// (their stores are skipped); a missing scale reads as 1.
+template <int RT, int CT>
+struct EpiScales {
+  float w[RT][4];
+  float x[CT];
+};
+
+template <int RT, int CT>
+__device__ __forceinline__ void epi_scales(EpiScales<RT, CT>& e, const float* sw, const float* sx, int M, int n0, int m0,
+                                           int rowend) {
+#pragma unroll
+  for (int t = 0; t < RT; ++t)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) e.w[t][r] = sw ? sw[min(n0 + 16 * t + r, rowend - 1)] : 1.0f;
+#pragma unroll
+  for (int c = 0; c < CT; ++c) e.x[c] = sx ? sx[min(m0 + 16 * c, M - 1)] : 1.0f;
+}
+
+// store4 of quad (t, c) with its scales from epi_scales: the same arithmetic, bit for bit.
+template <int RT, int CT>
+__device__ __forceinline__ void store4e(void* Y, int64_t ldy, bool wscaled, int vec_store, const GemmArgs& a,
+                                        const EpiScales<RT, CT>& e, int t, int c, v4f acc, int m, int n0, int rowend) {
+  float v[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    float y = acc[r];
+    if (wscaled) y = y * e.w[t][r];
+    v[r] = y * e.x[c];
+  }
+  put4(Y, ldy, vec_store, a, v, m, n0, rowend);
 }
 
 __device__ __forceinline__ void store4(const GemmArgs& a, v4f acc, int m, int n0, int rowend) {
@@ -866,6 +910,17 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
     if constexpr (NS == 4)
       if (c + 2 < c_hi) step(std::integral_constant<int, 2>(), c + 2);
   };
+  // the epilogue's scales, requested before any weight or activation so that they have
+  // long arrived when the stores begin (K slices write unscaled partials and need none)
+  EpiScales<RT, CT> es, eu;  // GLU: gate scales and token scales in es, up scales in eu
+  if constexpr (GLU) {
+    if (wave >= 4 && active) {
+      epi_scales(es, a.mat[0].sw, a.sx, a.M, nbase + 4 * lq, m0 + li, rowend);
+      epi_scales(eu, a.mat[1].sw, nullptr, a.M, nbase + 4 * lq, m0 + li, rowend);
+    }
+  } else {
+    if (active && R.ksplit == 1) epi_scales(es, MD.sw, a.sx, a.M, nbase + 4 * lq, m0 + li, rowend);
+  }
   if (active)
     run(std::true_type());
   else
@@ -896,14 +951,13 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
         const int n0 = nbase + 4 * lq;
         if (m >= a.M || n0 >= rowend) continue;
         const v4f gv = *reinterpret_cast<const v4f*>(ex + ((wsel * CT + cc) * 64 + lane) * 4);
-        const float xs = a.sx ? a.sx[m] : 1.0f;
+        const float xs = es.x[cc];
         float h[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int n = n0 + r < rowend ? n0 + r : rowend - 1;
           float gg = gv[r], uu = acc[0][cc][r];
-          if (G.sw) gg = gg * G.sw[n];
-          if (Up.sw) uu = uu * Up.sw[n];
+          if (G.sw) gg = gg * es.w[0][r];
+          if (Up.sw) uu = uu * eu.w[0][r];
           h[r] = glu_silu(gg * xs, uu * xs);
           if (n0 + r < rowend) tmax[cc] = fmaxf(tmax[cc], fabsf(h[r]));
         }
@@ -948,10 +1002,7 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
       const int n0 = nbase + 16 * t + 4 * lq;
       if (m >= a.M || n0 >= rowend) continue;
       if (R.ksplit == 1) {
-        if constexpr (GR)
-          store4(MD.Y, MD.ldy, MD.sw, MD.vec_store, a, acc[t][cc], m, n0, rowend);
-        else
-          store4(a, acc[t][cc], m, n0, rowend);
+        store4e(MD.Y, MD.ldy, MD.sw != nullptr, MD.vec_store, a, es, t, cc, acc[t][cc], m, n0, rowend);
       } else {  // unscaled fp32 partial of this K slice
         float* pp = a.part + ((int64_t)slice * a.M + m) * a.N + n0;
 #pragma unroll
@@ -1391,13 +1442,15 @@ __global__ __launch_bounds__(64 * WV) void spense_gemm_big_kernel(GemmArgs a) {
   if (n_de > 0) part(DE, NO, nst);
 
   xdl_fence();
+  EpiScales<RPW, TC> es;
+  epi_scales(es, a.sw, a.sx, a.M, rblk + 16 * RPW * wr + 4 * lq, m0 + 16 * TC * wc + li, rowend);
 #pragma unroll
   for (int t = 0; t < RPW; ++t)
 #pragma unroll
     for (int c = 0; c < TC; ++c) {
       const int m = m0 + 16 * (TC * wc + c) + li;
       const int n0 = rblk + 16 * (RPW * wr + t) + 4 * lq;
-      if (m < a.M && n0 < rowend) store4(a, acc[t][c], m, n0, rowend);
+      if (m < a.M && n0 < rowend) store4e(a.Y, a.ldy, a.sw != nullptr, a.vec_store, a, es, t, c, acc[t][c], m, n0, rowend);
     }
 }
 
@@ -1680,18 +1733,15 @@ __global__ __launch_bounds__(512) void spense_gemm_big2_kernel(GemmArgs a) {
     return;
   }
   run(std::true_type());
+  EpiScales<RPW, TC> es;
+  epi_scales(es, MD.sw, a.sx, a.M, rblk + 16 * RPW * wr + 4 * lq, m0 + 16 * TC * wc + li, rowend);
 #pragma unroll
   for (int t = 0; t < RPW; ++t)
 #pragma unroll
     for (int c = 0; c < TC; ++c) {
       const int m = m0 + 16 * (TC * wc + c) + li;
       const int n0 = rblk + 16 * (RPW * wr + t) + 4 * lq;
-      if (m < a.M && n0 < rowend) {
-        if constexpr (GR)
-          store4(MD.Y, MD.ldy, MD.sw, MD.vec_store, a, acc[t][c], m, n0, rowend);
-        else
-          store4(a, acc[t][c], m, n0, rowend);
-      }
+      if (m < a.M && n0 < rowend) store4e(MD.Y, MD.ldy, MD.sw != nullptr, MD.vec_store, a, es, t, c, acc[t][c], m, n0, rowend);
     }
 }
 
