@@ -881,7 +881,9 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
         xload(d, c_lo + d);
         if constexpr (ACT) load(slot[d], c_lo + d);
       }
-      barrier_vm<0>();
+      // the first chunk's activations only: the loads issued after them (D chunks of
+      // weights, D - 1 of activations) stay in flight while the next ones are requested
+      barrier_vm<AFTER>();
     }
     auto step = [&](auto s_const, int c) {
       constexpr int S = decltype(s_const)::value;
