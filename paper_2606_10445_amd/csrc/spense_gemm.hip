@@ -871,7 +871,10 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
         x_to_lds<DT, CT, XI>(xres + (c - c_lo) * XT::BYTES, a, rx, m0, chunk_k(c), chunk_end(c), wave, lane);
       if constexpr (ACT) {
 #pragma unroll
-        for (int d = 0; d < D; ++d) load(slot[d], c_lo + d);
+        for (int d = 0; d < D; ++d) {
+          __builtin_amdgcn_sched_barrier(0);  // each chunk's weights before the next chunk's
+          load(slot[d], c_lo + d);
+        }
       }
       barrier_vm<ACT ? D * RT * NL : 0>();
       if constexpr (!ACT) return;
@@ -879,10 +882,14 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
 #pragma unroll
       for (int d = 0; d < D; ++d) {
         xload(d, c_lo + d);
+        __builtin_amdgcn_sched_barrier(0);
         if constexpr (ACT) load(slot[d], c_lo + d);
+        __builtin_amdgcn_sched_barrier(0);
       }
       // the first chunk's activations only: the loads issued after them (D chunks of
-      // weights, D - 1 of activations) stay in flight while the next ones are requested
+      // weights, D - 1 of activations, in this order: the scheduling barriers keep a
+      // chunk's weight loads from sinking below the next chunk's) stay in flight while the
+      // next ones are requested
       barrier_vm<AFTER>();
     }
     auto step = [&](auto s_const, int c) {
