@@ -384,6 +384,54 @@ __device__ __forceinline__ void store4(const GemmArgs& a, v4f acc, int m, int n0
   store4(a.Y, a.ldy, a.sw, a.vec_store, a, acc, m, n0, rowend);
 }
 
+// A large-M workgroup's bf16 output tile through LDS, so that it leaves as whole token
+// rows: stored straight from the accumulators, each instruction would write 16 token rows
+// 32 bytes apiece, four times the write requests of whole rows (measured on the 256 x 256
+// kernel: about 9 us of store issue per tile against 2).  Token row r of the tile (NB
+// 16-byte blocks of eight outputs) sits at byte r * 16 NB, its block b stored at block
+// b ^ (r % NB), so that neither the quad writes nor the row reads meet in a bank.
+// out_tile_write: a wave's RT x CT quads (rows 16 (RT wr + t) + 4 lq + [0, 4) of the tile,
+// token 16 (CT wc + c) + li), scaled and rounded as store4e does.
+template <int RT, int CT, int NB>
+__device__ __forceinline__ void out_tile_write(uint8_t* ot, const v4f (&acc)[RT][CT], const EpiScales<RT, CT>& es,
+                                               bool wscaled, int wr, int wc, int li, int lq) {
+  typedef uint32_t u2 __attribute__((ext_vector_type(2)));
+#pragma unroll
+  for (int t = 0; t < RT; ++t)
+#pragma unroll
+    for (int c = 0; c < CT; ++c) {
+      float v[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float y = acc[t][c][r];
+        if (wscaled) y = y * es.w[t][r];
+        v[r] = y * es.x[c];
+      }
+      const int r = 16 * (CT * wc + c) + li, n = 16 * (RT * wr + t) + 4 * lq;
+      *reinterpret_cast<u2*>(ot + r * (16 * NB) + (((n >> 3) ^ (r % NB)) << 4) + (n & 7) * 2) =
+          (u2){bf16_bits(v[0]) | (bf16_bits(v[1]) << 16), bf16_bits(v[2]) | (bf16_bits(v[3]) << 16)};
+    }
+}
+
+// out_tile_store: the tile's first ntok token rows to Y (tile row 0 = output row rblk,
+// token 0 = m0), 16 bytes per thread; Y 16-byte aligned, ldy and rblk multiples of 8.
+template <int NB, int NTHR>
+__device__ __forceinline__ void out_tile_store(const uint8_t* ot, int ntok, int m0, int M, int rblk, int rowend, void* Y,
+                                               int64_t ldy) {
+  for (int q = threadIdx.x; q < ntok * NB; q += NTHR) {
+    const int r = q / NB, b = q % NB;
+    const int m = m0 + r, n = rblk + 8 * b;
+    if (m >= M || n >= rowend) continue;
+    const v4i d = *reinterpret_cast<const v4i*>(ot + r * (16 * NB) + ((b ^ (r % NB)) << 4));
+    uint16_t* yp = reinterpret_cast<uint16_t*>(Y) + (int64_t)m * ldy + n;
+    if (n + 8 <= rowend) {
+      *reinterpret_cast<v4i*>(yp) = d;
+    } else {
+      for (int e = 0; e < rowend - n; ++e) yp[e] = (uint16_t)((uint32_t)d[e >> 1] >> (16 * (e & 1)));
+    }
+  }
+}
+
 // ---------------------------------------------------------------- kernel
 template <int DT, int CT, int RT, int W, int U, bool WM>
 __global__ __launch_bounds__(64 * W) void spense_gemm_kernel(GemmArgs a) {
@@ -1453,6 +1501,15 @@ __global__ __launch_bounds__(64 * WV) void spense_gemm_big_kernel(GemmArgs a) {
   xdl_fence();
   EpiScales<RPW, TC> es;
   epi_scales(es, a.sw, a.sx, a.M, rblk + 16 * RPW * wr + 4 * lq, m0 + 16 * TC * wc + li, rowend);
+  if (!a.out_f32 && ((uintptr_t)a.Y % 16 == 0) && (a.ldy % 8 == 0) && (rblk % 8 == 0)) {
+    // whole token rows through LDS (out_tile_write)
+    static_assert(16 * NT * 2 * kBigTokens <= 3 * St::BYTES, "the output tile fits the stages");
+    barrier_vm_lgkm0<0>();  // every wave's last operand reads and copies are done
+    out_tile_write<RPW, TC, 2 * NT>(big_lds, acc, es, a.sw != nullptr, wr, wc, li, lq);
+    barrier_vm_lgkm0<0>();
+    out_tile_store<2 * NT, 64 * WV>(big_lds, kBigTokens, m0, a.M, rblk, rowend, a.Y, a.ldy);
+    return;
+  }
 #pragma unroll
   for (int t = 0; t < RPW; ++t)
 #pragma unroll
@@ -1737,21 +1794,34 @@ __global__ __launch_bounds__(512) void spense_gemm_big2_kernel(GemmArgs a) {
       xdl_fence();
     }
   };
-  if (half && wc >= 2) {
+  // bf16 output with 16-byte aligned rows leaves through LDS as whole token rows
+  // (out_tile_write); the waves of token quarters 2 and 3 of a 256 x 128 tile then only
+  // help with the stores
+  const bool idle = half && wc >= 2;
+  const bool via_lds = !a.out_f32 && ((uintptr_t)MD.Y % 16 == 0) && (MD.ldy % 8 == 0) && (rblk % 8 == 0);
+  if (idle) {
     run(std::false_type());
+    if (!via_lds) return;
+  } else {
+    run(std::true_type());
+  }
+  EpiScales<RPW, TC> es;
+  if (!idle) epi_scales(es, MD.sw, a.sx, a.M, rblk + 16 * RPW * wr + 4 * lq, m0 + 16 * TC * wc + li, rowend);
+  if (!via_lds) {
+#pragma unroll
+    for (int t = 0; t < RPW; ++t)
+#pragma unroll
+      for (int c = 0; c < TC; ++c) {
+        const int m = m0 + 16 * (TC * wc + c) + li;
+        const int n0 = rblk + 16 * (RPW * wr + t) + 4 * lq;
+        if (m < a.M && n0 < rowend) store4e(MD.Y, MD.ldy, MD.sw != nullptr, MD.vec_store, a, es, t, c, acc[t][c], m, n0, rowend);
+      }
     return;
   }
-  run(std::true_type());
-  EpiScales<RPW, TC> es;
-  epi_scales(es, MD.sw, a.sx, a.M, rblk + 16 * RPW * wr + 4 * lq, m0 + 16 * TC * wc + li, rowend);
-#pragma unroll
-  for (int t = 0; t < RPW; ++t)
-#pragma unroll
-    for (int c = 0; c < TC; ++c) {
-      const int m = m0 + 16 * (TC * wc + c) + li;
-      const int n0 = rblk + 16 * (RPW * wr + t) + 4 * lq;
-      if (m < a.M && n0 < rowend) store4e(MD.Y, MD.ldy, MD.sw != nullptr, MD.vec_store, a, es, t, c, acc[t][c], m, n0, rowend);
-    }
+  barrier_vm_lgkm0<0>();  // every wave's last operand reads and copies are done
+  if (!idle) out_tile_write<RPW, TC, kB2Rows / 8>(big_lds, acc, es, MD.sw != nullptr, wr, wc, li, lq);
+  barrier_vm_lgkm0<0>();
+  out_tile_store<kB2Rows / 8, 512>(big_lds, ntok, m0, a.M, rblk, rowend, MD.Y, MD.ldy);
 }
 
 // The large-M kernels' dynamic LDS above the default limit is a per-device function

@@ -413,6 +413,32 @@ def test_large_m_kernel_exact_both_layouts(S, axis, M, N, K, db, kernel, waves):
         assert np.array_equal(run_gemm(S, w, X, sw, sx, False, big).view(np.uint16), ref["y_bf16"])
 
 
+# bf16 output of the large-M kernels: through LDS as whole token rows where Y is 16-byte
+# aligned with ldy and the tile's first row multiples of 8, else quad by quad; (axis, M,
+# N, K, db) with N and the 2:4 / dense boundary off multiples of 8 (a partial last block,
+# a region starting mid-block) and ragged M.
+OUT_CASES = [(0, 300, 203, 384, 100), (1, 520, 203, 512, 256), (0, 700, 600, 256, 300)]
+
+
+@pytest.mark.parametrize("kernel,waves", LARGE_M_KERNELS)
+@pytest.mark.parametrize("axis,M,N,K,db", OUT_CASES)
+def test_large_m_output_paths_exact(S, axis, M, N, K, db, kernel, waves):
+    """Bit-exact bf16 output against the oracle with a contiguous Y and with leading
+    dimensions N + 8 (rows through LDS) and N + 3 (quad stores); the padding is untouched."""
+    W, mask, X, sw, sx = gen.make_exact_int(23, M + N, M, N, K, gaxis(axis), db, gen.FP8)
+    pw, (v, m, d) = compress_both(S, W, mask, FP8, axis, db)
+    ref = oracle.spense_gemm(X, v, m, d, N, K, FP8, axis, db, sw, sx)
+    big = S.plan_override(kernel=kernel, waves=waves)
+    pwt = S.tile(pw)
+    assert np.array_equal(run_gemm(S, pwt, X, sw, sx, False, big).view(np.uint16), ref["y_bf16"])
+    for pad in (8, 3):
+        Ybig = torch.full((M, N + pad), 7.0, dtype=torch.bfloat16, device="cuda")
+        S.gemm(tdev(X), pwt, tdev(sw), tdev(sx), out=Ybig[:, :N], plan=big)
+        torch.cuda.synchronize()
+        assert np.array_equal(tnp(Ybig[:, :N]).view(np.uint16), ref["y_bf16"])
+        assert torch.all(Ybig[:, N:] == 7.0)
+
+
 # 256 x 256 kernel with its last row blocks as 256 x 128 tiles at the end of the grid:
 # (axis, M, N, K, db, half row blocks); ragged M (a half tile past M, a partial one),
 # ragged rows in both regions, the XCD-aware order on the full tiles with leftover row
