@@ -1060,11 +1060,15 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
       if (m >= a.M || n0 >= rowend) continue;
       if (R.ksplit == 1) {
         store4e(MD.Y, MD.ldy, MD.sw != nullptr, MD.vec_store, a, es, t, cc, acc[t][cc], m, n0, rowend);
-      } else {  // unscaled fp32 partial of this K slice
+      } else {  // unscaled fp32 partial of this K slice, one 16-byte store where it can
         float* pp = a.part + ((int64_t)slice * a.M + m) * a.N + n0;
+        if (n0 + 3 < rowend && a.N % 4 == 0 && (uintptr_t)a.part % 16 == 0) {
+          *reinterpret_cast<v4f*>(pp) = acc[t][cc];
+        } else {
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          if (n0 + r < rowend) pp[r] = acc[t][cc][r];
+          for (int r = 0; r < 4; ++r)
+            if (n0 + r < rowend) pp[r] = acc[t][cc][r];
+        }
       }
     }
 }
