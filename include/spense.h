@@ -40,7 +40,7 @@
 extern "C" {
 #endif
 
-#define SPENSE_ABI_VERSION 12
+#define SPENSE_ABI_VERSION 13
 
 typedef enum spense_status {
   SPENSE_OK = 0,
@@ -505,6 +505,17 @@ const char* spense_last_error(void);
 
 /* SPENSE_ABI_VERSION of the built library. */
 int spense_abi_version(void);
+
+/*
+ * Dispatch log (no paper passage: an aid for reading what the planner chose).  With level
+ * >= 1 every call that makes a new plan for a single weight (the planner's choice for one
+ * dtype, M and weight geometry; later calls with the same key reuse it) writes one line to
+ * stderr naming the kernel and its shape; with level >= 2 every grouped and paired call
+ * does too.  The level starts at the value of the environment variable SPENSE_LOG when
+ * the library is loaded (0 when unset or not a number); it is read there only.  The log
+ * never changes a plan or a result.  Returns the previous level; thread-safe.
+ */
+int spense_set_log(int32_t level);
 
 #ifdef __cplusplus
 }

@@ -39,7 +39,7 @@ SPENSE_LAYOUT_ROWMAJOR = 0
 SPENSE_LAYOUT_TILED = 1
 SPENSE_NOALLOC_SCRATCH_BYTES = 16 << 20
 
-EXPORTS = ["spense_abi_version", "spense_last_error", "spense_layout", "spense_tiled_layout",
+EXPORTS = ["spense_abi_version", "spense_set_log", "spense_last_error", "spense_layout", "spense_tiled_layout",
            "spense_compress_workspace_size", "spense_compress", "spense_decompress", "spense_tile",
            "spense_gemm_workspace_size", "spense_gemm", "spense_dense_gemm_workspace_size", "spense_dense_gemm",
            "spense_quantize_fp8", "spense_glu_quantize_fp8", "spense_index_scores", "spense_dense_permutation",
@@ -105,6 +105,7 @@ def _load():
     P = ctypes.POINTER
     sig = {
         "spense_abi_version": (ctypes.c_int, []),
+        "spense_set_log": (ctypes.c_int, [i32]),
         "spense_last_error": (ctypes.c_char_p, []),
         "spense_layout": (ctypes.c_int, [i64, i64, i32, i32, i64, P(spense_layout_t)]),
         "spense_tiled_layout": (ctypes.c_int, [i64, i64, i32, i32, i64, P(spense_tiled_layout_t)]),
@@ -148,6 +149,10 @@ _lib = _load()
 # ------------------------------------------------------------------ raw C calls
 def spense_abi_version() -> int:
     return _lib.spense_abi_version()
+
+
+def spense_set_log(level: int) -> int:
+    return _lib.spense_set_log(level)
 
 
 def spense_last_error() -> str:

@@ -636,6 +636,32 @@ struct PlanCache {
 };
 thread_local PlanCache g_plans;
 
+// Dispatch log level (spense_set_log); the environment is read once, at load.
+std::atomic<int> g_log{0};
+__attribute__((constructor)) void read_log_env() {
+  const char* e = getenv("SPENSE_LOG");
+  if (e) g_log.store(atoi(e));
+}
+
+const char* kernel_name(const spense::LaunchShape& ls) {
+  if (ls.big == 2) return "large-M 256x256";
+  if (ls.big == 1) return "large-M 128x256";
+  if (ls.glu) return "row-split, gate/up paired";
+  return ls.rows ? "row-split" : "K-split";
+}
+
+void log_plan(const char* what, int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, int64_t dense_begin,
+              bool tiled, const spense::LaunchShape& ls, const spense::GemmArgs& a, size_t ws_bytes) {
+  fprintf(stderr,
+          "spense: %s dtype=%s M=%lld N=%lld K=%lld split=%s dense_begin=%lld layout=%s -> %s act_tiles=%d "
+          "row_tiles=%d waves=%d token_blocks=%d workgroups=%d regions=%d k_slices=%d resident_x=%d "
+          "half_tile_groups=%d workspace=%zu\n",
+          what, dtype == SPENSE_FP8_E4M3FN ? "fp8" : "bf16", (long long)M, (long long)N, (long long)K,
+          split == SPENSE_SPLIT_OUTPUT ? "output" : "input", (long long)dense_begin, tiled ? "tiled" : "row-major",
+          kernel_name(ls), ls.ct, ls.rt, ls.waves, ls.big ? a.tblocks : ls.mblocks, a.groups, a.nreg, a.nreg > 0 ? a.reg[0].ksplit : 1,
+          ls.xres, ls.big == 2 ? a.groups - a.hg0 : 0, ws_bytes);
+}
+
 const Plan& cached_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, int64_t dense_begin, bool tiled,
                         const Override& ov) {
   PlanCache& c = g_plans;
@@ -647,6 +673,9 @@ const Plan& cached_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int6
   if (c.used < kPlanCache) ++c.used;
   c.key[slot] = k;
   make_plan(dtype, M, N, split, K, dense_begin, tiled, ov, &c.plan[slot]);
+  if (g_log.load(std::memory_order_relaxed) >= 1)
+    log_plan("plan", dtype, M, N, split, K, dense_begin, tiled, c.plan[slot].ls, c.plan[slot].args,
+             c.plan[slot].ws_bytes);
   return c.plan[slot];
 }
 
@@ -843,6 +872,8 @@ int launch_glu_pair(const void* X, int64_t M, int64_t ldx, const spense_packed_t
   if (hmax && groups > ceil_div(N, 16) + 1) return fail(SPENSE_ERR_HIP, "internal: %d workgroups along N", groups);
   a.hmax = hmax;
   *groups_out = groups;
+  if (g_log.load(std::memory_order_relaxed) >= 2)
+    log_plan("paired gate/up", SPENSE_FP8_E4M3FN, M, N, SPENSE_SPLIT_OUTPUT, K, db, true, ls, a, 0);
   hipError_t e = spense::launch_gemm(SPENSE_FP8_E4M3FN, ls, a, stream);
   if (e != hipSuccess) return fail(SPENSE_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return SPENSE_OK;
@@ -869,6 +900,8 @@ int api_fail(int code, const char* fmt, ...) {
 extern "C" {
 
 int spense_abi_version(void) { return SPENSE_ABI_VERSION; }
+
+int spense_set_log(int32_t level) { return g_log.exchange(level); }
 
 const char* spense_last_error(void) { return g_err; }
 
@@ -1343,6 +1376,11 @@ int spense_gemm_grouped(const void* X, int64_t M, int64_t ldx, int32_t count, co
   if (a.groups == 0) return ok();
   int rc = check_device();
   if (rc) return rc;
+  if (g_log.load(std::memory_order_relaxed) >= 2) {
+    int64_t nsum = 0;
+    for (int i = 0; i < count; ++i) nsum += packed[i]->N;
+    log_plan("grouped", SPENSE_FP8_E4M3FN, M, nsum, SPENSE_SPLIT_OUTPUT, K, -1, true, ls, a, 0);
+  }
   hipError_t e = spense::launch_gemm(SPENSE_FP8_E4M3FN, ls, a, stream);
   if (e != hipSuccess) return fail(SPENSE_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();

@@ -41,7 +41,7 @@ def test_library_exports_every_declared_symbol(S):
     for n in _declared():
         assert hasattr(lib, n), f"{n} declared in include/ but not exported"
     assert set(_declared()) == set(S.EXPORTS)
-    assert S.spense_abi_version() == 12
+    assert S.spense_abi_version() == 13
 
 
 @pytest.mark.parametrize("N,K,split,db", [(256, 512, 0, 192), (256, 512, 1, 384), (25600, 5120, 0, 19200),
@@ -452,3 +452,28 @@ def test_binding_checks_tensors_before_the_library(S):
         S.dense_gemm(X, torch.zeros((N, K), dtype=torch.uint8), out=torch.empty((8, N - 1), dtype=torch.bfloat16))
     with pytest.raises(ValueError):
         S.dense_gemm(X.to(torch.bfloat16), torch.zeros((N, K), dtype=torch.uint8))
+
+
+def test_dispatch_log_names_the_plan_and_changes_nothing(S, capfd):
+    """spense_set_log(1): a new single-weight plan writes one stderr line naming its kernel
+    and shape; a reused plan writes none; the plan (here its workspace) is the same with the
+    log on and off."""
+    L = S.spense_layout(5120, 25600, 1, 1, 19200)
+    pk = S.spense_packed_t(1, 1, 5120, 25600, 19200, 4096, L.values_ld, 8192, L.meta_ld, 16384, L.dense_ld)
+    M = 61  # a geometry no other test of this process plans
+    prev = S.spense_set_log(0)
+    try:
+        capfd.readouterr()
+        quiet = S.spense_gemm_workspace_size(M, pk)
+        assert capfd.readouterr().err == ""
+        assert S.spense_set_log(1) == 0
+        Lg = S.spense_layout(9024, 5120, 1, 0, 7040)
+        pg = S.spense_packed_t(1, 0, 9024, 5120, 7040, 4096, Lg.values_ld, 8192, Lg.meta_ld, 16384, Lg.dense_ld)
+        S.spense_gemm_workspace_size(M, pg)  # new key: one line
+        S.spense_gemm_workspace_size(M, pg)  # cached: none
+        err = capfd.readouterr().err.strip().splitlines()
+        assert len(err) == 1 and err[0].startswith("spense: plan dtype=fp8 M=61 N=9024 K=5120 split=output"), err
+        assert "-> row-split" in err[0] and "k_slices=" in err[0]
+        assert S.spense_gemm_workspace_size(M, pk) == quiet  # the log does not change the plan
+    finally:
+        S.spense_set_log(prev)
