@@ -20,11 +20,13 @@
  *     call says otherwise.  spense_last_error() returns a thread-local message.
  *   - Matrices are row-major with an explicit leading dimension in elements.
  *   - Device pointers are plain HIP device addresses; the caller allocates and frees
- *     every buffer.  The library allocates no device or host memory of its own.  The
- *     only state it keeps is set once per device and never changes afterwards (the
- *     gfx950 check, the large-M kernel's LDS attribute, both under std::call_once or
- *     atomics) and a per-thread cache of recent execution plans; none of it changes a
- *     result, and no environment variable is read.
+ *     every buffer.  The library allocates no device or host memory of its own (the
+ *     one exception, spense_gemm_noalloc's file-scope scratch array, is described
+ *     there).  The only other state it keeps is set once per device and never changes
+ *     afterwards (the gfx950 check, the large-M kernels' LDS attributes, both under
+ *     std::call_once or atomics), a per-thread cache of recent execution plans and the
+ *     dispatch-log level (spense_set_log, an atomic); none of it changes a result.  The
+ *     only environment variable read is SPENSE_LOG, once, when the library loads.
  *   - Calls take a hipStream_t (0 = the null stream) and are asynchronous on it unless
  *     stated otherwise.
  */
