@@ -105,11 +105,13 @@ def test_grouped_large_m_exact(S, M, K, shapes):
     pws = [packed(S, W, mask, db) for (W, mask, sw, db) in ws]
     sws = [tdev(sw) for (_, _, sw, _) in ws]
     ys = S.gemm_grouped(tdev(X), pws, sws, tdev(sx), out_f32=True)
+    ys16 = S.gemm_grouped(tdev(X), pws, sws, tdev(sx))  # bf16: the output tile through LDS
     torch.cuda.synchronize()
-    for (W, mask, sw, db), y in zip(ws, ys):
+    for (W, mask, sw, db), y, y16 in zip(ws, ys, ys16):
         v, m, d, bad = oracle.compress(W, mask, FP8, 0, db)
         ref = oracle.spense_gemm(X, v, m, d, W.shape[0], K, FP8, 0, db, sw, sx)
         assert np.array_equal(y.cpu().numpy(), ref["y_f32"])
+        assert np.array_equal(y16.view(torch.int16).cpu().numpy().view(np.uint16), ref["y_bf16"])
 
 
 def test_grouped_random_within_bound(S):
