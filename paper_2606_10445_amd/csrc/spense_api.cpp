@@ -365,6 +365,7 @@ int choose_ksplit(const spense::Region* regs, int nreg, int ct, int mblocks, int
     has_24 = has_24 || (regs[i].kbound > 0 && regs[i].rows > 0);
   }
   int S = 1;
+  const int64_t by_tiles = ceil_div(1024, std::max<int64_t>(tiles, 1));
   // Weights of 128 tiles or more with one activation tile (M <= 16): only if every slice
   // keeps at least 12 chunks; a weight with a 2:4 part takes up to 4 slices (its chunks
   // carry fewer bytes, so the waves of one tile keep too few in flight), an all-dense one
@@ -373,7 +374,6 @@ int choose_ksplit(const spense::Region* regs, int nreg, int ct, int mblocks, int
   // 25.1 / 25.5 / 26.3, M = 4: 23.9 / 24.6 / 26.3, M = 16: 27.7 / 25.6 / 27.3.  More
   // activation tiles: slices of at least 5 chunks, below 512 tiles.
   if (mblocks == 1 && tiles < 1024) {
-    const int64_t by_tiles = ceil_div(1024, std::max<int64_t>(tiles, 1));
     if (tiles < 128) {
       // few rows (k / v): slices of two or more chunks pay at every M
       S = (int)std::max<int64_t>(1, std::min<int64_t>({4, by_tiles, chunks / 2}));
@@ -383,6 +383,18 @@ int choose_ksplit(const spense::Region* regs, int nreg, int ct, int mblocks, int
     } else if (tiles < 512) {
       S = (int)std::max<int64_t>(1, std::min<int64_t>({4, by_tiles, chunks / 5}));
     }
+  } else if (mblocks == 2 && tiles < 512) {
+    // Two token blocks (65-128 tokens), tiled layout, measured (us, slices 1 / 2 / 3 / 4):
+    // down (320 tiles, 50 chunks) M = 80: 48.3 / 38.5 / 37.0 / 43.8, M = 128: 50.6 /
+    // 40.6 / 38.9 / 45.9; k (64 tiles, 10 chunks) M = 80: 10.8 / 9.7 / 9.4 / 8.8, M = 128:
+    // 10.9 / 9.9 / 9.8 / 8.9; o (320 tiles, 16 chunks) M = 128: 19.0 / 19.8 / 21.4 / 25.1.
+    // Few rows: slices of two or more chunks; otherwise slices of at least 16 chunks.
+    S = (int)std::max<int64_t>(1, tiles < 128 ? std::min<int64_t>({4, by_tiles, chunks / 2})
+                                              : std::min<int64_t>({3, by_tiles, chunks / 16}));
+  } else if (mblocks == 3 && tiles < 512 && chunks >= 32) {
+    // 129-192 tokens: two slices of a long K only (down M = 192: 53.3 / 50.2 / 70.9; o,
+    // 16 chunks, M = 192: 20.4 / 23.6; four token blocks lose with any slices)
+    S = 2;
   }
   if (ov.ksplit >= 1) S = (int)std::max<int64_t>(1, std::min<int64_t>(ov.ksplit, chunks));
   return S;
@@ -1270,11 +1282,16 @@ int spense_gemm_grouped(const void* X, int64_t M, int64_t ldx, int32_t count, co
   if (M >= kBigMinM && !big2) {
     // Between one token block and the 256 x 256 grid each weight's own plan (the 128 x
     // 256 large-M kernel on large weights) beats one row-split grid over all of them
-    // (Seed-OSS q / k / v at M = 512: 75 against 95 us): one launch per weight.  Plans
-    // above 64 tokens use no K slices, so they need no workspace.
+    // (Seed-OSS q / k / v at M = 512: 75 against 95 us): one launch per weight, its plan
+    // held to one K slice so that it needs no workspace.
+    spense_plan_override_t one{};
+    one.ksplit = 1;
+    one.block_order = -1;
+    one.xcd_order = -1;
+    one.half_row_blocks = -1;
     for (int i = 0; i < count; ++i) {
-      const int r = spense_gemm(X, M, ldx, packed[i], w_scales ? w_scales[i] : nullptr, x_scale, Y[i], ldy[i], out_flags,
-                                nullptr, 0, stream);
+      const int r = spense_gemm_planned(X, M, ldx, packed[i], w_scales ? w_scales[i] : nullptr, x_scale, Y[i], ldy[i],
+                                        out_flags, nullptr, 0, &one, stream);
       if (r) return r;
     }
     return ok();

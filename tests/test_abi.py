@@ -363,9 +363,9 @@ def test_gemm_glu_fp8_validates_arguments_on_the_host(S):
 
 def test_k_slice_rule_on_the_layer_shapes(S):
     """Which Qwen3-like layer weights (tiled layout) the planner slices along K (a
-    workspace is needed exactly then): k / v (64 tiles) at every M up to 64, o (320 tiles, 16 chunks) from 17
-    tokens, down (50 chunks, with a 2:4 part) from one token, q (512 tiles) and gate
-    (1600 tiles) never; none beyond one block of 64 tokens."""
+    workspace is needed exactly then): k / v (64 tiles) at every M up to 128, o (320 tiles,
+    16 chunks) from 17 to 64 tokens, down (50 chunks, with a 2:4 part) from one token to
+    192, q (512 tiles) and gate (1600 tiles) never; none from four token blocks on."""
     def ws(N, K, split, M):
         db = N * 3 // 4 if split == 0 else K * 3 // 4
         L = S.spense_layout(N, K, 1, split, db)
@@ -379,7 +379,11 @@ def test_k_slice_rule_on_the_layer_shapes(S):
         assert ws(25600, 5120, 0, M) == 0  # gate / up
     assert ws(5120, 8192, 1, 1) == 0 and ws(5120, 8192, 1, 16) == 0  # o: one token block of 1-16
     assert ws(5120, 8192, 1, 17) > 0 and ws(5120, 8192, 1, 64) > 0  # o from 17 tokens
-    assert ws(1024, 5120, 0, 65) == 0 and ws(5120, 25600, 1, 200) == 0  # several token blocks
+    for M in (65, 100, 128):  # two token blocks: k / v and down sliced, o, q and gate not
+        assert ws(1024, 5120, 0, M) > 0 and ws(5120, 25600, 1, M) > 0
+        assert ws(5120, 8192, 1, M) == 0 and ws(8192, 5120, 0, M) == 0 and ws(25600, 5120, 0, M) == 0
+    assert ws(5120, 25600, 1, 192) > 0 and ws(1024, 5120, 0, 192) == 0  # three: only the long K
+    assert ws(1024, 5120, 0, 200) == 0 and ws(5120, 25600, 1, 200) == 0  # four or more token blocks
 
 
 def _down_desc(S, layout=0, dtype=1):

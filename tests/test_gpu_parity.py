@@ -413,6 +413,28 @@ def test_large_m_kernel_exact_both_layouts(S, axis, M, N, K, db, kernel, waves):
         assert np.array_equal(run_gemm(S, w, X, sw, sx, False, big).view(np.uint16), ref["y_bf16"])
 
 
+# K slices with two or three token blocks (65-192 tokens): few-row weights with a long K
+# take them from the planner; (axis, M, N, K, db) with the slice count the planner picks.
+KSLICE_BLOCK_CASES = [(1, 80, 2048, 24576, 18432, 3), (0, 100, 1024, 5120, 768, 4), (1, 150, 2048, 16384, 12288, 2),
+                      (0, 128, 1040, 6144, 784, 4)]
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("axis,M,N,K,db,slices", KSLICE_BLOCK_CASES)
+def test_k_slices_with_several_token_blocks_exact(S, axis, M, N, K, db, slices):
+    """The planner's K slices above 64 tokens (workspace = slices x M x N floats), and
+    forced 2 and 3 slices: bit-exact against the oracle on exact-integer data."""
+    say(f"[kslices blocks] axis={axis} M={M} N={N} K={K} db={db}")
+    W, mask, X, sw, sx = gen.make_exact_int(29, M + N, M, N, K, gaxis(axis), db, gen.FP8)
+    pw, (v, m, d) = compress_both(S, W, mask, FP8, axis, db)
+    ref = oracle.spense_gemm(X, v, m, d, N, K, FP8, axis, db, sw, sx)
+    pwt = S.tile(pw)
+    assert S.spense_gemm_workspace_size(M, pwt.desc) == slices * M * N * 4
+    for plan in (None, S.plan_override(kernel=ROWS, ksplit=2), S.plan_override(kernel=ROWS, ksplit=3)):
+        assert np.array_equal(run_gemm(S, pwt, X, sw, sx, True, plan), ref["y_f32"])
+        assert np.array_equal(run_gemm(S, pwt, X, sw, sx, False, plan).view(np.uint16), ref["y_bf16"])
+
+
 # bf16 output of the large-M kernels: through LDS as whole token rows where Y is 16-byte
 # aligned with ldy and the tile's first row multiples of 8, else quad by quad; (axis, M,
 # N, K, db) with N and the 2:4 / dense boundary off multiples of 8 (a partial last block,
