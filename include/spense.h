@@ -311,10 +311,10 @@ int spense_gemm_planned(const void* X, int64_t M, int64_t ldx, const spense_pack
  * 2:4 and dense regions and its own output; together they fill the GPU where one small
  * weight alone would need K slices and a second pass.  Up to 64 tokens it runs the
  * row-split kernel over all weights; where the weights' 256-row blocks times the 256-token
- * blocks of M fill the GPU (at least 160 tiles, and 4 token blocks or M a multiple of 256)
- * one 256 x 256 tile grid covers all weights; in between it issues one launch per weight
- * with that weight's own plan held to one K slice (several launches).  Weights: fp8 e4m3fn, output-split,
- * tiled layout (spense_tile), equal K; count in [1, 4].  w_scales (array of count
+ * blocks of M fill the GPU (at least 160 tiles) one 256 x 256 tile grid covers all
+ * weights; in between it issues one launch per weight with that weight's own plan held
+ * to one K slice (several launches).  Weights: fp8 e4m3fn, output-split, tiled layout
+ * (spense_tile), equal K; count in [1, 4].  w_scales (array of count
  * pointers, or NULL for none) and x_scale as in spense_gemm; Y[i] (bf16 or fp32 per
  * out_flags) with leading dimension ldy[i] >= N_i.  Results equal spense_gemm's up to the
  * order of the fp32 sum (no K slices here).  Allocates nothing; asynchronous.

@@ -278,7 +278,7 @@ int64_t choose_half_rows(const spense::Region* regs, int nreg, int64_t T, int64_
 }
 
 constexpr int64_t kBigMinM = 65;       // tokens from which the large-M kernel is used (fp8)
-constexpr int64_t kBigMinTiles = 128;  // and workgroup tiles (128 rows x 256 tokens) it needs
+constexpr int64_t kBigMinTiles = 120;  // and workgroup tiles (128 rows x 256 tokens) it needs
 
 // Waves (16-row tiles) per workgroup for each kind of region, w[kind] in [1, wmax]:
 // region i (rows[i] rows, kind[i] in {0, 1}, tile[i] the weight bytes one wave streams)
@@ -478,24 +478,29 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
   // o / gate / down shapes, M = 65 .. 2048, XCD-aware order): it wins above one row-split
   // token block (64 tokens) once there are at least 128 such tiles (gate / up at M = 96 /
   // 128 / 192: 42.5 / 43.2 / 46.0 vs 45.3 / 47.9 / 71.4 us; q at M = 512: 45 vs 54 us; o
-  // and down at M = 1024: 60 vs 97 and 156 vs 265 us); with fewer (q below 512 tokens, o
-  // and down below 1024), the row-split kernel's finer grid keeps more CUs busy.
+  // and down at M = 1024: 60 vs 97 and 156 vs 265 us); with fewer (q below 257 tokens, o
+  // and down below 513), the row-split kernel's finer grid keeps more CUs busy.  Since the
+  // output tile goes through LDS, 120 tiles suffice (o, down and Seed-OSS o at M = 513 /
+  // 576 / 700, 120 tiles: 50.7 / 50.6 / 51.5, 140.9 / 140.3 / 143.8 and 62.8 / 61.3 /
+  // 63.2 us against 58.6 / 57.4 / 62.7, 154.0 / 154.3 / 171.9 and 70.7 / 70.1 / 77.4 on
+  // row-split; at 80 tiles, M = 257-512, row-split stays ahead: o 33 against 50).
   int big = (dtype == SPENSE_FP8_E4M3FN && M >= kBigMinM && ceil_div(N, 128) * ceil_div(M, 256) >= kBigMinTiles) ? 1 : 0;
   // 256-row x 256-token tiles (tiled weights) once that grid has at least 160 workgroups:
   // measured on MI355X (us, 128 x 256 tiles -> 256 x 256): gate / up at M = 1024 / 2048
   // 177 / 312 -> 159 / 291, Seed-OSS gate 178 / 316 -> 168 / 290, down and o at M = 2048
   // (160 workgroups) 313 -> 267 and 120 -> 100, q at M = 2048 95 -> 91; with fewer
   // workgroups it loses (q at M = 1024, 128 workgroups: 49 -> 84; down at M = 1024, 80: 159
-  // -> 279).  With two or three token blocks the last one must be full: gate / up at M =
-  // 257 / 384 / 448 / 512 85 / 85 / 87 / 93 against 91 / 88 / 88 / 90, at M = 513 / 640 /
-  // 768 134 / 141 / 151 against 144 / 146 / 152 (Seed-OSS gate alike); from four blocks on
-  // (q at M = 1025-1792: 97-106 -> 88-96) a ragged last block is fine.
+  // -> 279).  A ragged last token block used to favour the 128 x 256 kernel at two or
+  // three blocks; since both kernels write their output tile through LDS and the 256 x
+  // 256 grid ends in 256 x 128 tiles, the 256 x 256 kernel wins there too (gate / up at
+  // M = 257 / 300 / 513 / 576 / 700: 65.8 / 66.7 / 82.9 / 84.4 / 87.0 against 68.2 / 67.9
+  // / 100.3 / 102.8 / 108.8 us; Seed-OSS gate alike).
   if (big && tiled) {
     const int64_t rb256 = split == SPENSE_SPLIT_OUTPUT
                               ? ceil_div(dense_begin, 256) + ceil_div(N - dense_begin, 256)
                               : ceil_div(N, 256);
     const int64_t tb256 = ceil_div(M, 256);
-    if (rb256 * tb256 >= 160 && (tb256 >= 4 || M % 256 == 0)) big = 2;
+    if (rb256 * tb256 >= 160) big = 2;
   }
   if (ov.kernel == 1 || ov.kernel == 2) big = 0;
   if (ov.kernel == 3) big = 1;  // fp8 (checked by read_override)
@@ -1278,7 +1283,7 @@ int spense_gemm_grouped(const void* X, int64_t M, int64_t ldx, int32_t count, co
   const int64_t T256 = ceil_div(M, 256);
   int64_t rb256 = 0;
   for (int i = 0; i < nreg; ++i) rb256 += ceil_div(regs[i].rows, 256);
-  const bool big2 = M >= kBigMinM && rb256 * T256 >= 160 && (T256 >= 4 || M % 256 == 0);
+  const bool big2 = M >= kBigMinM && rb256 * T256 >= 160;
   if (M >= kBigMinM && !big2) {
     // Between one token block and the 256 x 256 grid each weight's own plan (the 128 x
     // 256 large-M kernel on large weights) beats one row-split grid over all of them

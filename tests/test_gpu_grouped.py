@@ -94,6 +94,7 @@ GROUP_LARGE_M_CASES = [
     (4096, 256, [(1280, 0.25), (640, 0.25), (640, 0.5)]),   # 11 row blocks x 16 token blocks
     (3400, 384, [(1536, 0.25), (768, 0.25), (768, 0.25)]),  # 12 x 14, ragged M
     (520, 256, [(640, 0.25), (256, 0.25), (200, 0.5)]),     # 5 x 3: per-weight launches
+    (520, 256, [(10240, 0.25), (2048, 0.25), (2048, 0.5)]),  # 56 x 3 on the grid, a ragged third block
     (65, 512, [(512, 0.25), (128, 0.25)]),                  # just above the row-split range
 ]
 
