@@ -484,7 +484,14 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
   // 576 / 700, 120 tiles: 50.7 / 50.6 / 51.5, 140.9 / 140.3 / 143.8 and 62.8 / 61.3 /
   // 63.2 us against 58.6 / 57.4 / 62.7, 154.0 / 154.3 / 171.9 and 70.7 / 70.1 / 77.4 on
   // row-split; at 80 tiles, M = 257-512, row-split stays ahead: o 33 against 50).
-  int big = (dtype == SPENSE_FP8_E4M3FN && M >= kBigMinM && ceil_div(N, 128) * ceil_div(M, 256) >= kBigMinTiles) ? 1 : 0;
+  // Up to five 64-token blocks the row-split kernel also beats a grid of fewer than 160
+  // such tiles (q, 128 tiles, at M = 257 / 320: 31.7 / 31.9 against 35.7 / 35.1 us; at
+  // 384, six blocks, 45.1 against 35.6).
+  const int64_t tiles128 = ceil_div(N, 128) * ceil_div(M, 256);
+  int big = (dtype == SPENSE_FP8_E4M3FN && M >= kBigMinM && tiles128 >= kBigMinTiles &&
+             !(tiles128 < 160 && ceil_div(M, 64) <= 5))
+                ? 1
+                : 0;
   // 256-row x 256-token tiles (tiled weights) once that grid has at least 160 workgroups:
   // measured on MI355X (us, 128 x 256 tiles -> 256 x 256): gate / up at M = 1024 / 2048
   // 177 / 312 -> 159 / 291, Seed-OSS gate 178 / 316 -> 168 / 290, down and o at M = 2048
