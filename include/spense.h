@@ -261,7 +261,9 @@ typedef struct spense_plan_override_t {
                                layout only); 2 rows split, activations staged in LDS;
                                3 large-M tiles of 128 rows x 256 tokens; 4 large-M tiles
                                of 256 x 256 (tiled layout; a row-major weight runs 3)
-                               (3 and 4 fp8 only) */
+                               (3 and 4 fp8 only); 5 rows split with two 64-token halves
+                               per workgroup, 128 tokens a block (tiled fp8; no shape
+                               fields, no K slices) */
   int32_t row_tiles;        /* K-split kernel: 16-row tiles per workgroup (1, 2, 4); with
                                kernel 2: 1 or 2 (with 4 waves) */
   int32_t waves;            /* K-split kernel: 4, 8 or 16 waves per workgroup (row_tiles

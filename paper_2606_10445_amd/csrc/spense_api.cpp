@@ -207,7 +207,11 @@ int read_override(const spense_plan_override_t* ov, int32_t dtype, bool tiled, O
   o->u8 = ov->u8;
   o->halfrb = ov->half_row_blocks;
   o->xres = ov->resident_x;
-  if (o->kernel < 0 || o->kernel > 4) return fail(SPENSE_ERR_ARG, "plan: unknown kernel %d", o->kernel);
+  if (o->kernel < 0 || o->kernel > 5) return fail(SPENSE_ERR_ARG, "plan: unknown kernel %d", o->kernel);
+  if (o->kernel == 5 && (!tiled || dtype != SPENSE_FP8_E4M3FN))
+    return fail(SPENSE_ERR_ARG, "plan: the two-half row-split kernel reads tiled fp8 weights only");
+  if (o->kernel == 5 && (o->rt || o->waves || o->ct || o->ksplit > 1 || o->xres == 2))
+    return fail(SPENSE_ERR_ARG, "plan: the two-half row-split kernel has one shape (1 row tile, 8 waves, no K slices)");
   if (o->kernel == 1 && tiled) return fail(SPENSE_ERR_ARG, "plan: the K-split kernel reads the row-major layout only");
   if (o->kernel >= 3 && dtype != SPENSE_FP8_E4M3FN) return fail(SPENSE_ERR_ARG, "plan: the large-M kernels are fp8 only");
   if (o->ct < 0 || o->ct > 2) return fail(SPENSE_ERR_ARG, "plan: act_tiles %d (0, 1 or 2)", o->ct);
@@ -461,7 +465,7 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
     waves = 8;
   }
   if (ov.kernel == 1) rows_mode = 0;  // forced (checked against the layout by read_override)
-  if (ov.kernel == 2) rows_mode = 1;
+  if (ov.kernel == 2 || ov.kernel == 5) rows_mode = 1;
   if (rows_mode) {
     rt = 1;
     waves = 8;
@@ -509,10 +513,38 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
     const int64_t tb256 = ceil_div(M, 256);
     if (rb256 * tb256 >= 160) big = 2;
   }
-  if (ov.kernel == 1 || ov.kernel == 2) big = 0;
+  // Two 64-token halves per row-split workgroup (spense_gemm_rows2_kernel: 128 tokens a
+  // block, four token tiles, one row tile, eight waves, no K slices).  Each weight chunk
+  // feeds twice the tokens of the row-split kernel's, but the 128 KB of staged
+  // activations leave one workgroup per CU, so it needs several rounds of workgroups.
+  // Measured on MI355X (graph replay, us, planner's choice -> two halves): with one
+  // 128-token block (M = 65 / 100 / 128) it wins from 768 row tiles of 16 (gate / up
+  // 25600 x 5120 37.1 / 37.0 / 37.3 -> 29.1 / 29.5 / 31.2; 16384 x 5120 29.7 / 29.8 /
+  // 30.1 -> 23.7 / 24.1 / 25.8; 12288 x 5120 22.0 / 21.6 / 22.1 -> 21.3 / 20.5 / 20.8;
+  // 20480 x 4096 and the input-split 25600 x 5120 alike) and loses below (q, 512 tiles:
+  // 15.9 / 16.4 / 16.2 -> 18.2 / 19.0 / 19.2; 10240 x 5120 by 2-3 us).  With two blocks
+  // (M = 129 .. 256) the weight is read twice, so it only replaces row-split grids of
+  // three or four token blocks (q at M = 224 / 256 29.7 / 29.6 -> 24.0 / 24.0, at 160 /
+  // 192 21.9 / 22.2 -> 23.6 / 23.8; 10240 x 5120 at 160 / 192 / 224 25.1 / 26.5 / 31.0
+  // -> 25.1 / 25.1 / 25.2; 12288 x 5120 at 160 / 224 30.9 / 43.5 -> 28.4 / 29.7; the
+  // input-split 16384 x 8192 at 160 / 256 55.5 / 54.1 -> 40.8 / 45.2), not the large-M
+  // kernels (gate / up at M = 160 / 256: 37.7 / 43.5 against 56.3 / 59.6).
+  bool rows2 = ov.kernel == 5;
+  if (ov.kernel == 0 && !ov.rt && !ov.waves && !ov.ct && ov.ksplit <= 1 && !ov.wused && !ov.wused_d &&
+      !ov.wused_s && !ov.u8 && !ov.xres && tiled && dtype == SPENSE_FP8_E4M3FN && M > 64 && M <= 256) {
+    const int64_t rtiles = ceil_div(N, 16);
+    rows2 = M <= 128 ? rtiles >= 768 : (!big && rtiles >= (M <= 192 ? 640 : 512));
+  }
+  if (ov.kernel == 1 || ov.kernel == 2 || rows2) big = 0;
   if (ov.kernel == 3) big = 1;  // fp8 (checked by read_override)
   if (ov.kernel == 4) big = tiled ? 2 : 1;  // the 256 x 256 kernel reads the tiled layout
   pl->ls.big = big;
+  if (rows2) {
+    pl->ls.ct = 4;
+    pl->ls.mblocks = (int)ceil_div(M, 128);
+    pl->ls.rt = 1;
+    pl->ls.waves = 8;
+  }
   const int big_rows = big == 2 ? 256 : 128;  // rows of a large-M workgroup tile
   if (big) pl->ls.waves = (big == 1 && ov.waves == 4) ? 4 : 8;
   const int64_t tblocks = ceil_div(M, 256);
@@ -558,7 +590,7 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
     const int64_t kc = dtype == SPENSE_FP8_E4M3FN ? 512 : 256;
     int64_t chunks = 0;
     for (int i = 0; i < nreg; ++i) chunks = std::max(chunks, ceil_div(regs[i].kbound, kc) + ceil_div(K - regs[i].kbound, kc));
-    ksplit = chunks > 0 ? choose_ksplit(regs, nreg, pl->ls.ct, pl->ls.mblocks, chunks, M, ov) : 1;
+    ksplit = chunks > 0 && !rows2 ? choose_ksplit(regs, nreg, pl->ls.ct, pl->ls.mblocks, chunks, M, ov) : 1;
     for (int i = 0; i < nreg; ++i) slice_cuts(regs[i], ksplit, kc, es, sparse_cost);
     choose_rows_per_group(regs, nreg, rt, waves, pl->ls.ct, pl->ls.mblocks, K, es, sparse_cost, ksplit, ov);
     // One or two token tiles, tiled fp8, 8 waves, no K slices: the activations of the
@@ -571,7 +603,7 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
     // a workgroup has few active waves the first barrier is not repaid (q and o at M = 1
     // 8.0 / 9.2 -> 8.2 / 9.5), nor on down's K slices (M = 1 / 16: 19.4 / 20.4 -> 19.9 /
     // 20.8), so it is used where every region gives a workgroup at least 4 waves.
-    if (ct <= 2 && rt == 1 && waves == 8 && tiled && dtype == SPENSE_FP8_E4M3FN && ksplit == 1 && ov.xres != 1 &&
+    if (!rows2 && ct <= 2 && rt == 1 && waves == 8 && tiled && dtype == SPENSE_FP8_E4M3FN && ksplit == 1 && ov.xres != 1 &&
         chunks * 8192 * ct <= 160 * 1024) {
       bool wide = true;
       for (int i = 0; i < nreg; ++i) wide = wide && regs[i].wused >= 4;
@@ -634,8 +666,9 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
   // 19.3 / 38.0 / 47.6 -> 19.2 / 35.5 / 47.0; o and k within 1%.  Needs the row groups
   // to split evenly over the XCDs.
   a.mblk = pl->ls.mblocks;
-  a.rorder = pl->ls.rows && !big && pl->ls.mblocks > 1 ? (ov.order >= 0 ? ov.order : 2) : 0;
+  a.rorder = pl->ls.rows && !big && !rows2 && pl->ls.mblocks > 1 ? (ov.order >= 0 ? ov.order : 2) : 0;
   if (a.rorder == 2 && a.groups % 8) a.rorder = 0;
+  if (rows2) pl->ls.rows = 2;
   // K-sliced regions keep fp32 partial sums: slices x M x N floats
   pl->ws_bytes = ksplit > 1 ? (size_t)ksplit * (size_t)M * (size_t)N * sizeof(float) : 0;
 }
@@ -671,6 +704,7 @@ const char* kernel_name(const spense::LaunchShape& ls) {
   if (ls.big == 2) return "large-M 256x256";
   if (ls.big == 1) return "large-M 128x256";
   if (ls.glu) return "row-split, gate/up paired";
+  if (ls.rows == 2) return "row-split, two 64-token halves";
   return ls.rows ? "row-split" : "K-split";
 }
 

@@ -1076,6 +1076,121 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
     }
 }
 
+// Row-split kernel for two 64-token halves per workgroup (65-128 tokens per block): each
+// wave's weights of a chunk, in registers, feed the MMAs of both halves, so a weight row
+// is streamed once for up to 128 tokens instead of once per 64.  The activations of a
+// chunk (both halves, 64 KB) take two LDS buffers: chunk c + 1 is copied during step c
+// into the buffer chunk c - 1 left (every wave finished with it at the previous barrier),
+// and the barrier at the end of step c waits for it; the weights run NS - 1 chunks ahead
+// in NS register slots.  Plain launches of tiled fp8 weights, one row tile and eight
+// waves per workgroup, no K slices.
+template <int WR, int NS>
+__global__ __launch_bounds__(64 * WR) void spense_gemm_rows2_kernel(GemmArgs a) {
+  constexpr int DT = kFP8, CT = 4, RT = 1, D = NS - 1;
+  static_assert(NS == 2 || NS == 3, "two or three weight slots");
+  typedef XTile<DT, CT> XT;  // one 64-token half
+  constexpr int KC = XT::CHUNK_K;
+  constexpr int XI = XT::BYTES / 1024 / WR;  // 1 KB activation blocks per wave per half
+  static_assert(XI >= 1 && XI * 1024 * WR == XT::BYTES, "activation tile must split evenly");
+  constexpr int NL = ChunkLoads<true>::N;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int li = lane & 15, lq = lane >> 4;
+  const int g = blockIdx.x;
+  const int ri = (a.nreg > 1 && g >= a.reg[1].wg0) ? 1 : 0;
+  const Region& R = a.reg[ri];
+  const MatDesc& MD = a.mat[0];
+  const int rowend = R.row0 + R.rows;
+  const int nbase = R.row0 + ((g - R.wg0) * R.wused + wave) * 16;
+  const int m0 = blockIdx.y * 32 * CT;
+  const int K = R.kend, kbound = R.kbound;
+  const bool active = wave < R.wused && nbase < rowend;
+
+  __shared__ __attribute__((aligned(1024))) uint8_t xbuf[2][2 * XT::BYTES];
+  const __amdgpu_buffer_rsrc_t rx = rsrc(a.X, a.x_bytes), rv = rsrc(a.values, a.v_bytes),
+                               rm = rsrc(a.meta, a.m_bytes), rd = rsrc(a.dense, a.d_bytes);
+  v4f acc0[RT][CT], acc1[RT][CT];
+#pragma unroll
+  for (int c = 0; c < CT; ++c) acc0[0][c] = acc1[0][c] = (v4f){0.f, 0.f, 0.f, 0.f};
+
+  const int n_sp = (kbound + KC - 1) / KC, n_de = (K - kbound + KC - 1) / KC, nch = n_sp + n_de;
+  auto chunk_k = [&](int c) { return c < n_sp ? c * KC : kbound + (c - n_sp) * KC; };
+  auto chunk_end = [&](int c) { return c < n_sp ? kbound : K; };
+  const bool tok = nbase < rowend;
+  const uint32_t ts = (uint32_t)(nbase / 16), td = (uint32_t)((nbase - R.dense_row_off) / 16);
+  const uint32_t vt = ts * (uint32_t)n_sp * 4096u + 16u * lane, mt = ts * (uint32_t)n_sp * 1024u + 16u * lane,
+                 dt = td * (uint32_t)n_de * 8192u + 16u * lane;
+  auto load = [&](WChunk& W, int c) {
+    load_chunk_tiled(W, c < n_sp, tok && c < nch, c, max(c - n_sp, 0), vt, mt, dt, rv, rm, rd);
+  };
+  auto xload = [&](int c) {  // both halves of chunk c into buffer c % 2
+    uint8_t* b = xbuf[c & 1];
+    const int ke = c < nch ? chunk_end(c) : -1;
+    x_to_lds<DT, CT, XI>(b, a, rx, m0, chunk_k(c), ke, wave, lane);
+    x_to_lds<DT, CT, XI>(b + XT::BYTES, a, rx, m0 + 16 * CT, chunk_k(c), ke, wave, lane);
+  };
+
+  auto run = [&](auto act_const) {
+    constexpr bool ACT = decltype(act_const)::value;
+    WChunk slot[NS][RT];
+    // the first chunk's activations, then D chunks of weights; the barrier waits for the
+    // activations only (loads complete in issue order)
+    xload(0);
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (ACT) {
+#pragma unroll
+      for (int d = 0; d < D; ++d) {
+        load(slot[d][0], d);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    barrier_vm<ACT ? D * NL : 0>();
+    // step c: activations of chunk c + 1, weights of chunk c + 2, the MMAs of chunk c for
+    // both halves, then a barrier that waits for chunk c + 1's activations (issued before
+    // this step's weights, the only loads younger than them)
+    auto step = [&](auto s_const, int c) {
+      constexpr int S = decltype(s_const)::value;
+      xload(c + 1);
+      __builtin_amdgcn_sched_barrier(0);
+      if constexpr (ACT) {
+        load(slot[(S + D) % NS][0], c + D);
+        __builtin_amdgcn_sched_barrier(0);
+        const uint8_t* xb = xbuf[c & 1];
+        mma_chunk<DT, CT, RT, true, 1>(acc0, slot[S], c < n_sp, xb, li, lq);
+        mma_chunk<DT, CT, RT, true, 1>(acc1, slot[S], c < n_sp, xb + XT::BYTES, li, lq);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      barrier_vm<ACT ? NL : 0>();
+    };
+    int c = 0;
+    for (; c + NS <= nch; c += NS) {
+      step(std::integral_constant<int, 0>(), c);
+      step(std::integral_constant<int, 1>(), c + 1);
+      if constexpr (NS == 3) step(std::integral_constant<int, 2 % NS>(), c + 2);
+    }
+    if (c < nch) step(std::integral_constant<int, 0>(), c);
+    if constexpr (NS == 3)
+      if (c + 1 < nch) step(std::integral_constant<int, 1>(), c + 1);
+  };
+  if (active)
+    run(std::true_type());
+  else
+    run(std::false_type());
+  if (!active) return;
+  // the epilogue's scales only now: held through the loop they would push the kernel
+  // past the register file
+  EpiScales<RT, 2 * CT> es;
+  epi_scales(es, MD.sw, a.sx, a.M, nbase + 4 * lq, m0 + li, rowend);
+  xdl_fence();
+#pragma unroll
+  for (int c = 0; c < 2 * CT; ++c) {
+    const int m = m0 + 16 * c + li;
+    const int n0 = nbase + 4 * lq;
+    if (m >= a.M || n0 >= rowend) continue;
+    store4e(MD.Y, MD.ldy, MD.sw != nullptr, MD.vec_store, a, es, 0, c, c < CT ? acc0[0][c] : acc1[0][c - CT], m, n0,
+            rowend);
+  }
+}
+
 // Y of a K-sliced GEMM (the planner slices every region of a weight alike, KS slices):
 // the sum of the slices' fp32 partials in slice order, then the epilogue of store4
 // ((sum * w_scale[n]) * x_scale[m], bf16 or fp32).  One thread per output element; its
@@ -1882,6 +1997,15 @@ template <int DT>
 hipError_t launch_dt(const LaunchShape& ls, const GemmArgs& a, hipStream_t s) {
   if (ls.big) return DT == kFP8 ? launch_big(ls, a, s) : hipErrorInvalidValue;
   if (a.tiled && !ls.rows) return hipErrorInvalidValue;  // the K-split kernel reads the row-major layout only
+  if (ls.rows == 2) {  // two 64-token halves per workgroup: tiled fp8, 8 waves, one row tile
+    if constexpr (DT == kFP8) {
+      if (!a.tiled || ls.rt != 1 || ls.waves != 8 || a.nmat != 1 || a.reg[0].ksplit != 1) return hipErrorInvalidValue;
+      // two weight slots: with three the kernel spills past the register file
+      hipLaunchKernelGGL((spense_gemm_rows2_kernel<8, 2>), dim3(a.groups, ls.mblocks), dim3(512), 0, s, a);
+      return hipGetLastError();
+    }
+    return hipErrorInvalidValue;
+  }
   if (ls.rows) {
     if (ls.ct == 1) return launch_rows_ct<DT, 1>(ls, a, s);
     if (ls.ct == 2) return launch_rows_ct<DT, 2>(ls, a, s);

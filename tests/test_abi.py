@@ -386,6 +386,39 @@ def test_k_slice_rule_on_the_layer_shapes(S):
     assert ws(1024, 5120, 0, 200) == 0 and ws(5120, 25600, 1, 200) == 0  # four or more token blocks
 
 
+def test_two_half_rule_on_the_layer_shapes(S, capfd):
+    """Where the planner runs two 64-token halves per row-split workgroup (tiled fp8, seen
+    through the dispatch log): one 128-token block on weights of at least 768 row tiles
+    (gate / up, 1600; 12288 rows), not on q (512) or at 64 tokens; two blocks where the
+    row-split kernel would take three or four (q from 193 tokens, 640 tiles from 129), not
+    where the large-M kernel runs (gate / up) or above 256 tokens; the row-major layout
+    never."""
+    def kernel(N, K, split, M, layout=S.SPENSE_LAYOUT_TILED):
+        db = N * 3 // 4 if split == 0 else K * 3 // 4
+        L = S.spense_layout(N, K, 1, split, db)
+        p = S.spense_packed_t(1, split, N, K, db, 4096, L.values_ld, 8192, L.meta_ld, 16384, L.dense_ld, layout)
+        S.spense_gemm_workspace_size(M, p)
+        err = capfd.readouterr().err.strip().splitlines()
+        assert err, (N, K, split, M)  # planned once in this test; a cached plan would log nothing
+        return err[-1].split(" -> ")[1].split(" act_tiles")[0]
+    two = "row-split, two 64-token halves"
+    prev = S.spense_set_log(1)
+    try:
+        # token counts other tests do not plan on these geometries (plans are cached per thread)
+        capfd.readouterr()
+        for M in (66, 127):
+            assert kernel(25600, 5120, 0, M) == two and kernel(25600, 5120, 1, M) == two
+            assert kernel(12288, 5120, 0, M) == two
+            assert kernel(8192, 5120, 0, M) == "row-split" and kernel(10240, 5120, 0, M) == "row-split"
+        assert kernel(25600, 5120, 0, 63) == "row-split"
+        assert kernel(8192, 5120, 0, 191) == "row-split" and kernel(8192, 5120, 0, 193) == two
+        assert kernel(10240, 5120, 0, 131) == two and kernel(16384, 8192, 1, 131) == two
+        assert kernel(25600, 5120, 0, 131).startswith("large-M") and kernel(8192, 5120, 0, 257) != two
+        assert kernel(25600, 5120, 0, 99, layout=0) != two
+    finally:
+        S.spense_set_log(prev)
+
+
 def _down_desc(S, layout=0, dtype=1):
     L = S.spense_layout(5120, 25600, dtype, 1, 19200)
     return S.spense_packed_t(dtype, 1, 5120, 25600, 19200, 4096, L.values_ld, 8192, L.meta_ld, 16384, L.dense_ld,
@@ -403,13 +436,16 @@ def test_plan_override_is_checked_on_the_host(S):
     assert S.spense_gemm_planned_workspace_size(64, tl, po(kernel=2, ksplit=1)) == 0
     assert S.spense_gemm_planned_workspace_size(64, rm, po(kernel=1)) == 0  # no K slices in the K-split kernel
     assert S.spense_gemm_planned_workspace_size(64, rm, po(kernel=3)) == 0
+    assert S.spense_gemm_planned_workspace_size(100, tl, po(kernel=5)) == 0  # 128 tokens a block, no slices
     bad = [(tl, po(kernel=1)),                      # the K-split kernel reads the row-major layout only
            (bf, po(kernel=3)),                      # large-M is fp8 only
            (rm, po(kernel=2, row_tiles=4, waves=4)),  # no such row-split shape
            (rm, po(kernel=1, row_tiles=4, waves=8)),  # no such K-split shape
            (rm, po(kernel=3, waves=16)),
            (rm, po(waves=8)),                       # a shape needs the kernel it is for
-           (rm, po(kernel=5)), (rm, po(ksplit=9)), (rm, po(act_tiles=3)), (rm, po(waves_used=9)),
+           (rm, po(kernel=5)),                      # the two-half row-split kernel: tiled fp8 only,
+           (tl, po(kernel=5, ksplit=2)), (tl, po(kernel=5, waves=8)),  # one shape, no K slices
+           (rm, po(kernel=6)), (rm, po(ksplit=9)), (rm, po(act_tiles=3)), (rm, po(waves_used=9)),
            (rm, po(block_order=3)), (rm, po(xcd_order=2)), (rm, po(u8=2)), (rm, po(half_row_blocks=-2)), (rm, po(resident_x=3))]
     for desc, p in bad:
         assert S.spense_gemm_planned_workspace_size(64, desc, p) == 0

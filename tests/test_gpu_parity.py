@@ -435,6 +435,53 @@ def test_k_slices_with_several_token_blocks_exact(S, axis, M, N, K, db, slices):
         assert np.array_equal(run_gemm(S, pwt, X, sw, sx, False, plan).view(np.uint16), ref["y_bf16"])
 
 
+# The row-split kernel with two 64-token halves per workgroup (128 tokens a block; forced
+# through the plan override, kernel 5): (axis, N, K, db) over both regions, ragged rows and
+# columns, at token counts from one to several 128-token blocks.
+ROWS2_CASES = [(0, 784, 1536, 528), (1, 600, 2560, 1792), (0, 300, 512, 208), (1, 136, 1024, 1024)]
+
+
+@pytest.mark.parametrize("axis,N,K,db", ROWS2_CASES)
+def test_two_half_row_split_exact(S, axis, N, K, db):
+    """Bit-exact against the oracle on exact-integer data (fp32 and bf16 outputs)."""
+    ROWS2 = 5
+    for M in (1, 37, 64, 65, 100, 128, 129, 300):
+        say(f"[rows2] axis={axis} N={N} K={K} db={db} M={M}")
+        W, mask, X, sw, sx = gen.make_exact_int(31, M + N, M, N, K, gaxis(axis), db, gen.FP8)
+        pw, (v, m, d) = compress_both(S, W, mask, FP8, axis, db)
+        ref = oracle.spense_gemm(X, v, m, d, N, K, FP8, axis, db, sw, sx)
+        pwt = S.tile(pw)
+        plan = S.plan_override(kernel=ROWS2)
+        assert np.array_equal(run_gemm(S, pwt, X, sw, sx, True, plan), ref["y_f32"])
+        assert np.array_equal(run_gemm(S, pwt, X, sw, sx, False, plan).view(np.uint16), ref["y_bf16"])
+
+
+# The same kernel as the planner's own choice (tall weights at one 128-token block; two
+# blocks where the row-split kernel would take three or four): (axis, N, K, db, M).
+ROWS2_AUTO_CASES = [(0, 12288, 512, 9216, 100), (1, 12288, 384, 256, 127), (0, 8192, 512, 6144, 250),
+                    (0, 10240, 256, 7680, 131)]
+
+
+@pytest.mark.parametrize("axis,N,K,db,M", ROWS2_AUTO_CASES)
+def test_two_half_row_split_planned_exact(S, capfd, axis, N, K, db, M):
+    """Bit-exact against the oracle with no override, the dispatch log naming the kernel."""
+    say(f"[rows2 auto] axis={axis} N={N} K={K} db={db} M={M}")
+    W, mask, X, sw, sx = gen.make_exact_int(37, M + N, M, N, K, gaxis(axis), db, gen.FP8)
+    pw, (v, m, d) = compress_both(S, W, mask, FP8, axis, db)
+    ref = oracle.spense_gemm(X, v, m, d, N, K, FP8, axis, db, sw, sx)
+    pwt = S.tile(pw)
+    prev = S.spense_set_log(1)
+    try:
+        capfd.readouterr()
+        y32 = run_gemm(S, pwt, X, sw, sx, True)
+        log = capfd.readouterr().err
+    finally:
+        S.spense_set_log(prev)
+    assert "row-split, two 64-token halves" in log, log
+    assert np.array_equal(y32, ref["y_f32"])
+    assert np.array_equal(run_gemm(S, pwt, X, sw, sx, False).view(np.uint16), ref["y_bf16"])
+
+
 # bf16 output of the large-M kernels: through LDS as whole token rows where Y is 16-byte
 # aligned with ldy and the tile's first row multiples of 8, else quad by quad; (axis, M,
 # N, K, db) with N and the 2:4 / dense boundary off multiples of 8 (a partial last block,
