@@ -85,13 +85,24 @@ def time_launches(fn, steps, warmup, torch):
     for i in range(warmup):
         fn(i)
     torch.cuda.synchronize()
-    if EAGER:  # for profilers that follow individual dispatches
+    if EAGER:  # launch by launch (for profilers that follow individual dispatches)
+        stream = torch.cuda.current_stream()
         t0 = torch.cuda.Event(enable_timing=True)
         t1 = torch.cuda.Event(enable_timing=True)
-        t0.record()
+        warm = 0.0
+        for _ in range(16):  # untimed rounds, as for the graph below
+            t0.record(stream)
+            for i in range(steps):
+                fn(i)
+            t1.record(stream)
+            torch.cuda.synchronize()
+            warm += t0.elapsed_time(t1)
+            if warm >= WARM_MS:
+                break
+        t0.record(stream)
         for i in range(steps):
             fn(i)
-        t1.record()
+        t1.record(stream)
         torch.cuda.synchronize()
         return t0.elapsed_time(t1) / steps
     g = torch.cuda.CUDAGraph()
@@ -204,8 +215,12 @@ def measure_extras(args, torch, gen, S, ws, pws, copies, swd, mx, dws, dense_cop
     # distribution over 200 eager launches, each between two HIP events on the stream
     evs = [torch.cuda.Event(enable_timing=True) for _ in range(201)]
     stream = torch.cuda.current_stream()
-    for i in range(20):
+    t_end = time.perf_counter() + WARM_MS * 1e-3  # untimed launches to the steady clock
+    i = 0
+    while i < 20 or time.perf_counter() < t_end:
         S.gemm(Xd, pws[i % copies], swd, sxd, out=Y, workspace=ws)
+        i += 1
+    torch.cuda.synchronize()
     evs[0].record(stream)
     for i in range(200):
         S.gemm(Xd, pws[i % copies], swd, sxd, out=Y, workspace=ws)
