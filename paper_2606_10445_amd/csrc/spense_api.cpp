@@ -1437,13 +1437,13 @@ int spense_gemm_grouped(const void* X, int64_t M, int64_t ldx, int32_t count, co
   a.vec_store = m0.vec_store;
   a.N = (int32_t)packed[0]->N;
   if (a.groups == 0) return ok();
-  int rc = check_device();
-  if (rc) return rc;
   if (g_log.load(std::memory_order_relaxed) >= 2) {
     int64_t nsum = 0;
     for (int i = 0; i < count; ++i) nsum += packed[i]->N;
     log_plan("grouped", SPENSE_FP8_E4M3FN, M, nsum, SPENSE_SPLIT_OUTPUT, K, -1, true, ls, a, 0);
   }
+  int rc = check_device();
+  if (rc) return rc;
   hipError_t e = spense::launch_gemm(SPENSE_FP8_E4M3FN, ls, a, stream);
   if (e != hipSuccess) return fail(SPENSE_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();

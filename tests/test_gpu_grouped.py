@@ -68,6 +68,11 @@ GROUP_CASES = [  # M, K, [(N, dense fraction)]
     (33, 384, [(512, 0.25)]),
     (32, 5120, [(128, 0.25), (48, 0.25)]),   # two token tiles, activations resident: 160 KB
     (9, 10240, [(96, 0.25), (32, 0.5)]),     # one token tile, 20 chunks resident
+    # more row groups than CUs at 33-64 tokens (two rounds of workgroups)
+    (64, 1024, [(20480, 0.25), (20480, 0.25)]),
+    (64, 256, [(20480, 0.25), (20480, 0.25)]),   # one chunk
+    (40, 640, [(24576, 0.25), (8192, 0.5), (4096, 0.0), (1000, 1.0)]),  # four weights, all-2:4 and all-dense ones, ragged chunk
+    (33, 1536, [(32768, 0.25), (4104, 0.25)]),  # ragged last row group
 ]
 
 
