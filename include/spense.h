@@ -239,8 +239,8 @@ int spense_gemm(const void* X, int64_t M, int64_t ldx, const spense_packed_t* pa
  * without the workspace, the same plan and kernels, results bit for bit equal to
  * spense_gemm's.  The fp32 partial sums of K-sliced plans go to a scratch array of
  * SPENSE_NOALLOC_SCRATCH_BYTES that the library keeps on each device it runs on until the
- * process ends (the current plans need at most 4 slices x 64 tokens x fewer than 8192 rows x 4
- * bytes, under 8.4 MB).  Every call on a device shares that array, which keeps the last call's
+ * process ends (a K-sliced plan needs slices x M x N x 4 bytes: 15.7 MB for a 5120-row
+ * down projection at 65-128 tokens, 6 slices, or at 193-256, 3).  Every call on a device shares that array, which keeps the last call's
  * partial sums (each call writes every partial it reads): calls that overlap on one
  * device, from any stream or thread, race and must be serialised by the caller.
  * SPENSE_ERR_WS if the plan would need more scratch than the array holds.  No hipMalloc,
@@ -263,7 +263,7 @@ typedef struct spense_plan_override_t {
                                of 256 x 256 (tiled layout; a row-major weight runs 3)
                                (3 and 4 fp8 only); 5 rows split with two 64-token halves
                                per workgroup, 128 tokens a block (tiled fp8; no shape
-                               fields, no K slices) */
+                               fields; ksplit allowed) */
   int32_t row_tiles;        /* K-split kernel: 16-row tiles per workgroup (1, 2, 4); with
                                kernel 2: 1 or 2 (with 4 waves) */
   int32_t waves;            /* K-split kernel: 4, 8 or 16 waves per workgroup (row_tiles

@@ -210,8 +210,8 @@ int read_override(const spense_plan_override_t* ov, int32_t dtype, bool tiled, O
   if (o->kernel < 0 || o->kernel > 5) return fail(SPENSE_ERR_ARG, "plan: unknown kernel %d", o->kernel);
   if (o->kernel == 5 && (!tiled || dtype != SPENSE_FP8_E4M3FN))
     return fail(SPENSE_ERR_ARG, "plan: the two-half row-split kernel reads tiled fp8 weights only");
-  if (o->kernel == 5 && (o->rt || o->waves || o->ct || o->ksplit > 1 || o->xres == 2))
-    return fail(SPENSE_ERR_ARG, "plan: the two-half row-split kernel has one shape (1 row tile, 8 waves, no K slices)");
+  if (o->kernel == 5 && (o->rt || o->waves || o->ct || o->xres == 2))
+    return fail(SPENSE_ERR_ARG, "plan: the two-half row-split kernel has one shape (1 row tile, 8 waves)");
   if (o->kernel == 1 && tiled) return fail(SPENSE_ERR_ARG, "plan: the K-split kernel reads the row-major layout only");
   if (o->kernel >= 3 && dtype != SPENSE_FP8_E4M3FN) return fail(SPENSE_ERR_ARG, "plan: the large-M kernels are fp8 only");
   if (o->ct < 0 || o->ct > 2) return fail(SPENSE_ERR_ARG, "plan: act_tiles %d (0, 1 or 2)", o->ct);
@@ -529,11 +529,31 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
   // -> 25.1 / 25.1 / 25.2; 12288 x 5120 at 160 / 224 30.9 / 43.5 -> 28.4 / 29.7; the
   // input-split 16384 x 8192 at 160 / 256 55.5 / 54.1 -> 40.8 / 45.2), not the large-M
   // kernels (gate / up at M = 160 / 256: 37.7 / 43.5 against 56.3 / 59.6).
+  // On weights with fewer row tiles but a long K it runs with K slices instead (partials
+  // reduced as for the row-split kernel): down 5120 x 25600 (50 chunks) at M = 65 / 100 /
+  // 128 39.4 / 37.7 / 39.0 -> 33.3 / 36.2 / 37.4 with 6 slices (4: 35.9 / 37.6 / 38.9),
+  // at M = 256 61.2 -> 57.4 with 3; Seed-OSS down 5120 x 27648 41.1 / 39.6 / 41.1 -> 33.8
+  // / 36.3 / 38.1 and 64.9 -> 59.5; Seed-OSS o 5120 x 10240 (20 chunks) at M = 65 / 100
+  // 24.4 / 22.1 -> 20.1 / 21.8 with 4 (M = 128: 22.8 against 23.0).  At 129-192 tokens the
+  // row-split kernel's three blocks stay ahead (down at M = 160 / 192 49.0 / 50.3 against
+  // 55.6 / 55.6), as they do on o (16 chunks), q and k at every M here.
   bool rows2 = ov.kernel == 5;
+  int rows2_ks = 1;
   if (ov.kernel == 0 && !ov.rt && !ov.waves && !ov.ct && ov.ksplit <= 1 && !ov.wused && !ov.wused_d &&
       !ov.wused_s && !ov.u8 && !ov.xres && tiled && dtype == SPENSE_FP8_E4M3FN && M > 64 && M <= 256) {
     const int64_t rtiles = ceil_div(N, 16);
     rows2 = M <= 128 ? rtiles >= 768 : (!big && rtiles >= (M <= 192 ? 640 : 512));
+    const int64_t kch = split == SPENSE_SPLIT_INPUT ? ceil_div(dense_begin, 512) + ceil_div(K - dense_begin, 512)
+                                                    : ceil_div(K, 512);
+    if (!rows2 && ov.ksplit < 1 && rtiles < 768) {
+      if (kch >= 40 && (M <= 128 || (M > 192 && !big))) {
+        rows2 = true;
+        rows2_ks = M <= 128 ? 6 : 3;
+      } else if (kch >= 20 && M <= 96) {
+        rows2 = true;
+        rows2_ks = 4;
+      }
+    }
   }
   if (ov.kernel == 1 || ov.kernel == 2 || rows2) big = 0;
   if (ov.kernel == 3) big = 1;  // fp8 (checked by read_override)
@@ -590,7 +610,10 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
     const int64_t kc = dtype == SPENSE_FP8_E4M3FN ? 512 : 256;
     int64_t chunks = 0;
     for (int i = 0; i < nreg; ++i) chunks = std::max(chunks, ceil_div(regs[i].kbound, kc) + ceil_div(K - regs[i].kbound, kc));
-    ksplit = chunks > 0 && !rows2 ? choose_ksplit(regs, nreg, pl->ls.ct, pl->ls.mblocks, chunks, M, ov) : 1;
+    if (rows2)
+      ksplit = (int)std::max<int64_t>(1, std::min<int64_t>(ov.ksplit >= 1 ? ov.ksplit : rows2_ks, chunks));
+    else
+      ksplit = chunks > 0 ? choose_ksplit(regs, nreg, pl->ls.ct, pl->ls.mblocks, chunks, M, ov) : 1;
     for (int i = 0; i < nreg; ++i) slice_cuts(regs[i], ksplit, kc, es, sparse_cost);
     choose_rows_per_group(regs, nreg, rt, waves, pl->ls.ct, pl->ls.mblocks, K, es, sparse_cost, ksplit, ov);
     // One or two token tiles, tiled fp8, 8 waves, no K slices: the activations of the

@@ -1083,7 +1083,8 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows_kernel(GemmArgs a) {
 // into the buffer chunk c - 1 left (every wave finished with it at the previous barrier),
 // and the barrier at the end of step c waits for it; the weights run NS - 1 chunks ahead
 // in NS register slots.  Plain launches of tiled fp8 weights, one row tile and eight
-// waves per workgroup, no K slices.
+// waves per workgroup; with K slices (workgroups (row group, slice), slices of a row
+// group adjacent) each writes its unscaled fp32 partial sums for the reduction launch.
 template <int WR, int NS>
 __global__ __launch_bounds__(64 * WR) void spense_gemm_rows2_kernel(GemmArgs a) {
   constexpr int DT = kFP8, CT = 4, RT = 1, D = NS - 1;
@@ -1100,7 +1101,8 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows2_kernel(GemmArgs a) 
   const Region& R = a.reg[ri];
   const MatDesc& MD = a.mat[0];
   const int rowend = R.row0 + R.rows;
-  const int nbase = R.row0 + ((g - R.wg0) * R.wused + wave) * 16;
+  const int slice = (g - R.wg0) % R.ksplit, rgroup = (g - R.wg0) / R.ksplit;
+  const int nbase = R.row0 + (rgroup * R.wused + wave) * 16;
   const int m0 = blockIdx.y * 32 * CT;
   const int K = R.kend, kbound = R.kbound;
   const bool active = wave < R.wused && nbase < rowend;
@@ -1112,7 +1114,8 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows2_kernel(GemmArgs a) 
 #pragma unroll
   for (int c = 0; c < CT; ++c) acc0[0][c] = acc1[0][c] = (v4f){0.f, 0.f, 0.f, 0.f};
 
-  const int n_sp = (kbound + KC - 1) / KC, n_de = (K - kbound + KC - 1) / KC, nch = n_sp + n_de;
+  const int n_sp = (kbound + KC - 1) / KC, n_de = (K - kbound + KC - 1) / KC;
+  const int c_lo = R.cut[slice], c_hi = R.cut[slice + 1];  // this workgroup's chunks
   auto chunk_k = [&](int c) { return c < n_sp ? c * KC : kbound + (c - n_sp) * KC; };
   auto chunk_end = [&](int c) { return c < n_sp ? kbound : K; };
   const bool tok = nbase < rowend;
@@ -1120,11 +1123,11 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows2_kernel(GemmArgs a) 
   const uint32_t vt = ts * (uint32_t)n_sp * 4096u + 16u * lane, mt = ts * (uint32_t)n_sp * 1024u + 16u * lane,
                  dt = td * (uint32_t)n_de * 8192u + 16u * lane;
   auto load = [&](WChunk& W, int c) {
-    load_chunk_tiled(W, c < n_sp, tok && c < nch, c, max(c - n_sp, 0), vt, mt, dt, rv, rm, rd);
+    load_chunk_tiled(W, c < n_sp, tok && c < c_hi, c, max(c - n_sp, 0), vt, mt, dt, rv, rm, rd);
   };
   auto xload = [&](int c) {  // both halves of chunk c into buffer c % 2
     uint8_t* b = xbuf[c & 1];
-    const int ke = c < nch ? chunk_end(c) : -1;
+    const int ke = c < c_hi ? chunk_end(c) : -1;
     x_to_lds<DT, CT, XI>(b, a, rx, m0, chunk_k(c), ke, wave, lane);
     x_to_lds<DT, CT, XI>(b + XT::BYTES, a, rx, m0 + 16 * CT, chunk_k(c), ke, wave, lane);
   };
@@ -1134,12 +1137,12 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows2_kernel(GemmArgs a) 
     WChunk slot[NS][RT];
     // the first chunk's activations, then D chunks of weights; the barrier waits for the
     // activations only (loads complete in issue order)
-    xload(0);
+    xload(c_lo);
     __builtin_amdgcn_sched_barrier(0);
     if constexpr (ACT) {
 #pragma unroll
       for (int d = 0; d < D; ++d) {
-        load(slot[d][0], d);
+        load(slot[d][0], c_lo + d);
         __builtin_amdgcn_sched_barrier(0);
       }
     }
@@ -1161,21 +1164,40 @@ __global__ __launch_bounds__(64 * WR) void spense_gemm_rows2_kernel(GemmArgs a) 
       }
       barrier_vm<ACT ? NL : 0>();
     };
-    int c = 0;
-    for (; c + NS <= nch; c += NS) {
+    int c = c_lo;
+    for (; c + NS <= c_hi; c += NS) {
       step(std::integral_constant<int, 0>(), c);
       step(std::integral_constant<int, 1>(), c + 1);
       if constexpr (NS == 3) step(std::integral_constant<int, 2 % NS>(), c + 2);
     }
-    if (c < nch) step(std::integral_constant<int, 0>(), c);
+    if (c < c_hi) step(std::integral_constant<int, 0>(), c);
     if constexpr (NS == 3)
-      if (c + 1 < nch) step(std::integral_constant<int, 1>(), c + 1);
+      if (c + 1 < c_hi) step(std::integral_constant<int, 1>(), c + 1);
   };
   if (active)
     run(std::true_type());
   else
     run(std::false_type());
   if (!active) return;
+  if (R.ksplit > 1) {  // unscaled fp32 partials of this K slice, one 16-byte store where it can
+    xdl_fence();
+#pragma unroll
+    for (int c = 0; c < 2 * CT; ++c) {
+      const int m = m0 + 16 * c + li;
+      const int n0 = nbase + 4 * lq;
+      if (m >= a.M || n0 >= rowend) continue;
+      const v4f v = c < CT ? acc0[0][c] : acc1[0][c - CT];
+      float* pp = a.part + ((int64_t)slice * a.M + m) * a.N + n0;
+      if (n0 + 3 < rowend && a.N % 4 == 0 && (uintptr_t)a.part % 16 == 0) {
+        *reinterpret_cast<v4f*>(pp) = v;
+      } else {
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (n0 + r < rowend) pp[r] = v[r];
+      }
+    }
+    return;
+  }
   // the epilogue's scales only now: held through the loop they would push the kernel
   // past the register file
   EpiScales<RT, 2 * CT> es;
@@ -1999,7 +2021,9 @@ hipError_t launch_dt(const LaunchShape& ls, const GemmArgs& a, hipStream_t s) {
   if (a.tiled && !ls.rows) return hipErrorInvalidValue;  // the K-split kernel reads the row-major layout only
   if (ls.rows == 2) {  // two 64-token halves per workgroup: tiled fp8, 8 waves, one row tile
     if constexpr (DT == kFP8) {
-      if (!a.tiled || ls.rt != 1 || ls.waves != 8 || a.nmat != 1 || a.reg[0].ksplit != 1) return hipErrorInvalidValue;
+      if (!a.tiled || ls.rt != 1 || ls.waves != 8 || a.nmat != 1) return hipErrorInvalidValue;
+      for (int i = 0; i < a.nreg; ++i)
+        if (a.reg[i].ksplit > 1 && !a.part) return hipErrorInvalidValue;
       // two weight slots: with three the kernel spills past the register file
       hipLaunchKernelGGL((spense_gemm_rows2_kernel<8, 2>), dim3(a.groups, ls.mblocks), dim3(512), 0, s, a);
       return hipGetLastError();

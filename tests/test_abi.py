@@ -379,11 +379,13 @@ def test_k_slice_rule_on_the_layer_shapes(S):
         assert ws(25600, 5120, 0, M) == 0  # gate / up
     assert ws(5120, 8192, 1, 1) == 0 and ws(5120, 8192, 1, 16) == 0  # o: one token block of 1-16
     assert ws(5120, 8192, 1, 17) > 0 and ws(5120, 8192, 1, 64) > 0  # o from 17 tokens
-    for M in (65, 100, 128):  # two token blocks: k / v and down sliced, o, q and gate not
-        assert ws(1024, 5120, 0, M) > 0 and ws(5120, 25600, 1, M) > 0
+    for M in (65, 100, 128):  # two token blocks: k / v sliced, down as 6 slices of 128 tokens, o, q and gate not
+        assert ws(1024, 5120, 0, M) > 0 and ws(5120, 25600, 1, M) == 6 * M * 5120 * 4
         assert ws(5120, 8192, 1, M) == 0 and ws(8192, 5120, 0, M) == 0 and ws(25600, 5120, 0, M) == 0
     assert ws(5120, 25600, 1, 192) > 0 and ws(1024, 5120, 0, 192) == 0  # three: only the long K
-    assert ws(1024, 5120, 0, 200) == 0 and ws(5120, 25600, 1, 200) == 0  # four or more token blocks
+    assert ws(1024, 5120, 0, 200) == 0  # four or more token blocks
+    assert ws(5120, 25600, 1, 200) == 3 * 200 * 5120 * 4  # down from 193 tokens: 3 slices of 128 tokens
+    assert ws(5120, 25600, 1, 300) == 0
 
 
 def test_two_half_rule_on_the_layer_shapes(S, capfd):
@@ -415,6 +417,11 @@ def test_two_half_rule_on_the_layer_shapes(S, capfd):
         assert kernel(10240, 5120, 0, 131) == two and kernel(16384, 8192, 1, 131) == two
         assert kernel(25600, 5120, 0, 131).startswith("large-M") and kernel(8192, 5120, 0, 257) != two
         assert kernel(25600, 5120, 0, 99, layout=0) != two
+        # short weights with a long K: with K slices (down 50 chunks, Seed-OSS o 20)
+        assert kernel(5120, 25600, 1, 67) == two and kernel(5120, 25600, 1, 250) == two
+        assert kernel(5120, 25600, 1, 170) == "row-split"
+        assert kernel(5120, 10240, 1, 67) == two and kernel(5120, 10240, 1, 120) == "row-split"
+        assert kernel(5120, 8192, 1, 67) == "row-split"  # o, 16 chunks
     finally:
         S.spense_set_log(prev)
 
@@ -437,6 +444,7 @@ def test_plan_override_is_checked_on_the_host(S):
     assert S.spense_gemm_planned_workspace_size(64, rm, po(kernel=1)) == 0  # no K slices in the K-split kernel
     assert S.spense_gemm_planned_workspace_size(64, rm, po(kernel=3)) == 0
     assert S.spense_gemm_planned_workspace_size(100, tl, po(kernel=5)) == 0  # 128 tokens a block, no slices
+    assert S.spense_gemm_planned_workspace_size(100, tl, po(kernel=5, ksplit=3)) == 3 * 100 * 5120 * 4
     bad = [(tl, po(kernel=1)),                      # the K-split kernel reads the row-major layout only
            (bf, po(kernel=3)),                      # large-M is fp8 only
            (rm, po(kernel=2, row_tiles=4, waves=4)),  # no such row-split shape
@@ -444,7 +452,7 @@ def test_plan_override_is_checked_on_the_host(S):
            (rm, po(kernel=3, waves=16)),
            (rm, po(waves=8)),                       # a shape needs the kernel it is for
            (rm, po(kernel=5)),                      # the two-half row-split kernel: tiled fp8 only,
-           (tl, po(kernel=5, ksplit=2)), (tl, po(kernel=5, waves=8)),  # one shape, no K slices
+           (tl, po(kernel=5, waves=8)), (tl, po(kernel=5, act_tiles=2)),  # one shape
            (rm, po(kernel=6)), (rm, po(ksplit=9)), (rm, po(act_tiles=3)), (rm, po(waves_used=9)),
            (rm, po(block_order=3)), (rm, po(xcd_order=2)), (rm, po(u8=2)), (rm, po(half_row_blocks=-2)), (rm, po(resident_x=3))]
     for desc, p in bad:

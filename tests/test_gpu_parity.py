@@ -415,8 +415,8 @@ def test_large_m_kernel_exact_both_layouts(S, axis, M, N, K, db, kernel, waves):
 
 # K slices with two or three token blocks (65-192 tokens): few-row weights with a long K
 # take them from the planner; (axis, M, N, K, db) with the slice count the planner picks.
-KSLICE_BLOCK_CASES = [(1, 80, 2048, 24576, 18432, 3), (0, 100, 1024, 5120, 768, 4), (1, 150, 2048, 16384, 12288, 2),
-                      (0, 128, 1040, 6144, 784, 4)]
+KSLICE_BLOCK_CASES = [(1, 80, 2048, 24576, 18432, 6),  # 48 chunks: the planner takes two 64-token halves, 6 slices
+                      (0, 100, 1024, 5120, 768, 4), (1, 150, 2048, 16384, 12288, 2), (0, 128, 1040, 6144, 784, 4)]
 
 
 @pytest.mark.timeout(300)
@@ -451,15 +451,18 @@ def test_two_half_row_split_exact(S, axis, N, K, db):
         pw, (v, m, d) = compress_both(S, W, mask, FP8, axis, db)
         ref = oracle.spense_gemm(X, v, m, d, N, K, FP8, axis, db, sw, sx)
         pwt = S.tile(pw)
-        plan = S.plan_override(kernel=ROWS2)
-        assert np.array_equal(run_gemm(S, pwt, X, sw, sx, True, plan), ref["y_f32"])
-        assert np.array_equal(run_gemm(S, pwt, X, sw, sx, False, plan).view(np.uint16), ref["y_bf16"])
+        for ks in (1, 2, 3) if M in (37, 100, 300) else (1,):  # K slices: fp32 partials, then the reduction
+            plan = S.plan_override(kernel=ROWS2, ksplit=ks)
+            assert np.array_equal(run_gemm(S, pwt, X, sw, sx, True, plan), ref["y_f32"]), ks
+            assert np.array_equal(run_gemm(S, pwt, X, sw, sx, False, plan).view(np.uint16), ref["y_bf16"]), ks
 
 
 # The same kernel as the planner's own choice (tall weights at one 128-token block; two
 # blocks where the row-split kernel would take three or four): (axis, N, K, db, M).
 ROWS2_AUTO_CASES = [(0, 12288, 512, 9216, 100), (1, 12288, 384, 256, 127), (0, 8192, 512, 6144, 250),
-                    (0, 10240, 256, 7680, 131)]
+                    (0, 10240, 256, 7680, 131),
+                    # short weights with a long K: with K slices (6, 3 and 4)
+                    (1, 320, 20992, 15744, 100), (1, 200, 20480, 15360, 250), (1, 300, 10240, 7680, 90)]
 
 
 @pytest.mark.parametrize("axis,N,K,db,M", ROWS2_AUTO_CASES)

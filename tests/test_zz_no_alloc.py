@@ -40,8 +40,9 @@ def bits(t):
 
 
 # (name, N, K, split, first M, second M): down and o slice K into 4 at these token counts,
-# k (64 tiles) at every M
-CASES = [("down", 5120, 25600, 1, 64, 16), ("k", 1024, 5120, 0, 64, 1), ("seed_o", 5120, 10240, 1, 48, 20)]
+# k (64 tiles) at every M; down at 66-128 tokens runs as two 64-token halves in 6 slices
+CASES = [("down", 5120, 25600, 1, 64, 16), ("k", 1024, 5120, 0, 64, 1), ("seed_o", 5120, 10240, 1, 48, 20),
+         ("down_128", 5120, 25600, 1, 128, 66)]  # two 64-token halves, 6 K slices: 15.7 MB of scratch
 
 
 @pytest.mark.timeout(300)
