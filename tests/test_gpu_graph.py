@@ -2,8 +2,10 @@
 and replayed several times, with eager work and synchronisations between the replays,
 give the eager results bit for bit.  Covers a K-sliced GEMM (partials in the workspace,
 then the reduction launch), the grouped launch, the paired gate / up launch with the
-row-maxima quantisation, and the whole MLP block, on the Qwen3-like shapes at M = 16
-and M = 64 (random data; the comparison is against the same calls run eagerly)."""
+row-maxima quantisation, and the whole MLP block, on the Qwen3-like shapes at M = 16,
+64 and 100 (at 100 down runs as two 64-token halves in K slices and the grouped gate /
+up as one two-half launch per weight; random data; the comparison is against the same
+calls run eagerly)."""
 import sys
 
 import numpy as np
@@ -33,7 +35,7 @@ def packed(S, name, i, N, K, axis):
     return pw, torch.from_numpy(m.sw).cuda()
 
 
-@pytest.mark.parametrize("M", [16, 64])
+@pytest.mark.parametrize("M", [16, 64, 100])
 def test_graph_replays_match_eager(S, M):
     say(f"[graph] M={M}")
     D, I = 5120, 25600
