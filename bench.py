@@ -212,8 +212,10 @@ def measure_extras(args, torch, gen, S, ws, pws, copies, swd, mx, dws, dense_cop
     ex["us_per_gemm_eager"] = round(time_launches(lambda i: S.gemm(Xd, pws[i % copies], swd, sxd, out=Y, workspace=ws),
                                                   200, 20, torch) * 1e3, 3)
     EAGER = prev
-    # distribution over 200 eager launches, each between two HIP events on the stream
-    evs = [torch.cuda.Event(enable_timing=True) for _ in range(201)]
+    # distribution over 40 groups of 10 eager launches, each group between two HIP events on
+    # the stream (an event after every launch would add its own cost to each)
+    G, NG = 10, 40
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(NG + 1)]
     stream = torch.cuda.current_stream()
     t_end = time.perf_counter() + WARM_MS * 1e-3  # untimed launches to the steady clock
     i = 0
@@ -222,12 +224,14 @@ def measure_extras(args, torch, gen, S, ws, pws, copies, swd, mx, dws, dense_cop
         i += 1
     torch.cuda.synchronize()
     evs[0].record(stream)
-    for i in range(200):
-        S.gemm(Xd, pws[i % copies], swd, sxd, out=Y, workspace=ws)
-        evs[i + 1].record(stream)
+    for g in range(NG):
+        for i in range(G):
+            S.gemm(Xd, pws[(g * G + i) % copies], swd, sxd, out=Y, workspace=ws)
+        evs[g + 1].record(stream)
     torch.cuda.synchronize()
-    per = sorted(evs[i].elapsed_time(evs[i + 1]) * 1e3 for i in range(200))
-    ex["per_launch_us"] = {"p10": round(per[20], 2), "median": round(per[100], 2), "p90": round(per[180], 2)}
+    per = sorted(evs[g].elapsed_time(evs[g + 1]) * 1e3 / G for g in range(NG))
+    ex["per_launch_us"] = {"groups_of": G, "p10": round(per[NG // 10], 2), "median": round(per[NG // 2], 2),
+                           "p90": round(per[NG * 9 // 10], 2)}
     # compute-bound point: M = 2048 on the same weight
     Mb = 2048
     Xb, sxb = gen.make_x(2, 0, Mb, K, gen.FP8, "normal")
