@@ -457,6 +457,33 @@ def test_two_half_row_split_exact(S, axis, N, K, db):
             assert np.array_equal(run_gemm(S, pwt, X, sw, sx, False, plan).view(np.uint16), ref["y_bf16"]), ks
 
 
+# Its epilogue with N off multiples of 4 and a padded Y (leading dimension N + 8: 16-byte
+# stores where a quad fits; N + 3: scalar stores), with and without K slices (the
+# partials' scalar path): (axis, M, N, K, db).
+ROWS2_OUT_CASES = [(0, 100, 203, 384, 100), (1, 130, 203, 1536, 256)]
+
+
+@pytest.mark.parametrize("axis,M,N,K,db", ROWS2_OUT_CASES)
+def test_two_half_output_paths_exact(S, axis, M, N, K, db):
+    """Bit-exact bf16 and fp32 against the oracle into padded outputs; the padding is untouched."""
+    W, mask, X, sw, sx = gen.make_exact_int(27, M + N, M, N, K, gaxis(axis), db, gen.FP8)
+    pw, (v, m, d) = compress_both(S, W, mask, FP8, axis, db)
+    ref = oracle.spense_gemm(X, v, m, d, N, K, FP8, axis, db, sw, sx)
+    pwt = S.tile(pw)
+    for ks in (1, 3):
+        plan = S.plan_override(kernel=5, ksplit=ks)
+        for pad in (8, 3):
+            for out_f32 in (False, True):
+                dt = torch.float32 if out_f32 else torch.bfloat16
+                Ybig = torch.full((M, N + pad), 7.0, dtype=dt, device="cuda")
+                S.gemm(tdev(X), pwt, tdev(sw), tdev(sx), out=Ybig[:, :N], out_f32=out_f32, plan=plan)
+                torch.cuda.synchronize()
+                got = tnp(Ybig[:, :N])
+                want = ref["y_f32"] if out_f32 else ref["y_bf16"]
+                assert np.array_equal(got if out_f32 else got.view(np.uint16), want), (ks, pad, out_f32)
+                assert torch.all(Ybig[:, N:] == 7.0)
+
+
 # The same kernel as the planner's own choice (tall weights at one 128-token block; two
 # blocks where the row-split kernel would take three or four): (axis, N, K, db, M).
 ROWS2_AUTO_CASES = [(0, 12288, 512, 9216, 100), (1, 12288, 384, 256, 127), (0, 8192, 512, 6144, 250),
