@@ -203,14 +203,17 @@ int spense_tile(const spense_packed_t* src, const spense_packed_t* dst, hipStrea
  * Device workspace (bytes) that spense_gemm needs for this M and weight; 0 means none.
  * It is non-zero when the plan cuts K into slices run by separate workgroups (weights
  * with fewer than 1024 16-row tiles at up to 64 tokens, when every slice keeps enough of
- * K: e.g. k / v and down from one token on, o from 17 tokens): S x M x N fp32 partial sums,
+ * K: e.g. k / v and down from one token on, o from 17 tokens; few-row or long-K weights
+ * at two or three 64-token blocks; long-K weights of fewer than 768 tiles at 65-128 and
+ * 193-256 tokens, as 128-token blocks in 3 to 6 slices): S x M x N fp32 partial sums,
  * added in slice order by a second kernel of the same call.  The workspace is only
  * scratch between the two kernels of one call; calls that overlap on one workspace race.
  */
 size_t spense_gemm_workspace_size(int64_t M, const spense_packed_t* packed);
 
 /*
- * Y = X W^T for a packed Spense weight (either layout), in one kernel launch:
+ * Y = X W^T for a packed Spense weight (either layout), in one kernel launch (two when
+ * the plan slices K, see spense_gemm_workspace_size):
  *   Y[m, n] = round((sum_k x[m, k] * w[n, k]) * w_scale[n] * x_scale[m])
  * X: M x K device matrix of the weight's dtype, leading dimension ldx (elements).
  * w_scale: N fp32 per-output-channel scales; x_scale: M fp32 per-token scales; either
