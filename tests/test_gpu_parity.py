@@ -457,6 +457,33 @@ def test_two_half_row_split_exact(S, axis, N, K, db):
             assert np.array_equal(run_gemm(S, pwt, X, sw, sx, False, plan).view(np.uint16), ref["y_bf16"]), ks
 
 
+# Seeded random shapes for the same kernel: either split, any 2:4 / dense boundary (input
+# split: multiples of 32), ragged N and K, 65-300 tokens, 1-4 K slices.
+def _rows2_random_cases(n=10, seed=2411):
+    r = np.random.default_rng(seed)
+    out = []
+    for i in range(n):
+        axis = int(r.integers(0, 2))
+        N = int(r.integers(16, 1200))
+        K = 32 * int(r.integers(8, 100))
+        db = int(r.integers(0, N + 1)) if axis == 0 else 32 * int(r.integers(0, K // 32 + 1))
+        out.append((i, axis, N, K, db, int(r.integers(65, 301)), int(r.integers(1, 5))))
+    return out
+
+
+@pytest.mark.parametrize("i,axis,N,K,db,M,ks", _rows2_random_cases())
+def test_two_half_random_shapes_exact(S, i, axis, N, K, db, M, ks):
+    """Bit-exact against the oracle on exact-integer data, fp32 and bf16 outputs."""
+    say(f"[rows2 random] axis={axis} N={N} K={K} db={db} M={M} ks={ks}")
+    W, mask, X, sw, sx = gen.make_exact_int(33, i, M, N, K, gaxis(axis), db, gen.FP8)
+    pw, (v, m, d) = compress_both(S, W, mask, FP8, axis, db)
+    ref = oracle.spense_gemm(X, v, m, d, N, K, FP8, axis, db, sw, sx)
+    plan = S.plan_override(kernel=5, ksplit=ks)
+    pwt = S.tile(pw)
+    assert np.array_equal(run_gemm(S, pwt, X, sw, sx, True, plan), ref["y_f32"])
+    assert np.array_equal(run_gemm(S, pwt, X, sw, sx, False, plan).view(np.uint16), ref["y_bf16"])
+
+
 # Its epilogue with N off multiples of 4 and a padded Y (leading dimension N + 8: 16-byte
 # stores where a quad fits; N + 3: scalar stores), with and without K slices (the
 # partials' scalar path): (axis, M, N, K, db).
