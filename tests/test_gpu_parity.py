@@ -539,6 +539,34 @@ def test_two_half_row_split_planned_exact(S, capfd, axis, N, K, db, M):
     assert np.array_equal(run_gemm(S, pwt, X, sw, sx, False).view(np.uint16), ref["y_bf16"])
 
 
+# Seeded random shapes for the large-M kernels (forced): either split, any boundary, ragged
+# N and K, 200-1100 tokens (partial last token blocks of both tile heights).
+def _large_m_random_cases(n=6, seed=2412):
+    r = np.random.default_rng(seed)
+    out = []
+    for i in range(n):
+        axis = int(r.integers(0, 2))
+        N = int(r.integers(100, 1400))
+        K = 32 * int(r.integers(8, 60))
+        db = int(r.integers(0, N + 1)) if axis == 0 else 32 * int(r.integers(0, K // 32 + 1))
+        out.append((i, axis, N, K, db, int(r.integers(200, 1101))))
+    return out
+
+
+@pytest.mark.parametrize("kernel,waves", LARGE_M_KERNELS)
+@pytest.mark.parametrize("i,axis,N,K,db,M", _large_m_random_cases())
+def test_large_m_random_shapes_exact(S, i, axis, N, K, db, M, kernel, waves):
+    """Bit-exact fp32 and bf16 against the oracle on exact-integer data."""
+    say(f"[large-M random] kernel={kernel} waves={waves} axis={axis} N={N} K={K} db={db} M={M}")
+    W, mask, X, sw, sx = gen.make_exact_int(35, i, M, N, K, gaxis(axis), db, gen.FP8)
+    pw, (v, m, d) = compress_both(S, W, mask, FP8, axis, db)
+    ref = oracle.spense_gemm(X, v, m, d, N, K, FP8, axis, db, sw, sx)
+    plan = S.plan_override(kernel=kernel, waves=waves)
+    pwt = S.tile(pw)
+    assert np.array_equal(run_gemm(S, pwt, X, sw, sx, True, plan), ref["y_f32"])
+    assert np.array_equal(run_gemm(S, pwt, X, sw, sx, False, plan).view(np.uint16), ref["y_bf16"])
+
+
 # bf16 output of the large-M kernels: through LDS as whole token rows where Y is 16-byte
 # aligned with ldy and the tile's first row multiples of 8, else quad by quad; (axis, M,
 # N, K, db) with N and the 2:4 / dense boundary off multiples of 8 (a partial last block,
