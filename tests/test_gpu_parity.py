@@ -539,6 +539,35 @@ def test_two_half_row_split_planned_exact(S, capfd, axis, N, K, db, M):
     assert np.array_equal(run_gemm(S, pwt, X, sw, sx, False).view(np.uint16), ref["y_bf16"])
 
 
+# Seeded random shapes for the 64-token kernels (forced): the row-split kernel on either
+# layout with 1-4 K slices, the K-split kernel on the row-major layout; 1-64 tokens.
+def _rows_random_cases(n=10, seed=2413):
+    r = np.random.default_rng(seed)
+    out = []
+    for i in range(n):
+        axis = int(r.integers(0, 2))
+        N = int(r.integers(16, 1500))
+        K = 32 * int(r.integers(4, 120))
+        db = int(r.integers(0, N + 1)) if axis == 0 else 32 * int(r.integers(0, K // 32 + 1))
+        out.append((i, axis, N, K, db, int(r.integers(1, 65)), int(r.integers(1, 5))))
+    return out
+
+
+@pytest.mark.parametrize("i,axis,N,K,db,M,ks", _rows_random_cases())
+def test_rows_random_shapes_exact(S, i, axis, N, K, db, M, ks):
+    """Bit-exact fp32 and bf16 against the oracle on exact-integer data: row-split (tiled
+    and row-major, ks K slices) and K-split (row-major)."""
+    say(f"[rows random] axis={axis} N={N} K={K} db={db} M={M} ks={ks}")
+    W, mask, X, sw, sx = gen.make_exact_int(37, i, M, N, K, gaxis(axis), db, gen.FP8)
+    pw, (v, m, d) = compress_both(S, W, mask, FP8, axis, db)
+    ref = oracle.spense_gemm(X, v, m, d, N, K, FP8, axis, db, sw, sx)
+    pwt = S.tile(pw)
+    for w, plan in ((pwt, S.plan_override(kernel=ROWS, ksplit=ks)), (pw, S.plan_override(kernel=ROWS, ksplit=ks)),
+                    (pw, S.plan_override(kernel=1))):
+        assert np.array_equal(run_gemm(S, w, X, sw, sx, True, plan), ref["y_f32"]), plan.kernel
+        assert np.array_equal(run_gemm(S, w, X, sw, sx, False, plan).view(np.uint16), ref["y_bf16"]), plan.kernel
+
+
 # Seeded random shapes for the large-M kernels (forced): either split, any boundary, ragged
 # N and K, 200-1100 tokens (partial last token blocks of both tile heights).
 def _large_m_random_cases(n=6, seed=2412):
