@@ -120,6 +120,36 @@ def test_grouped_large_m_exact(S, M, K, shapes):
         assert np.array_equal(y16.view(torch.int16).cpu().numpy().view(np.uint16), ref["y_bf16"])
 
 
+# Seeded random groups: 1-4 output-split weights of ragged N sharing a ragged K, any
+# boundary, at token counts on each of the three paths (row-split grid up to 64, one
+# launch per weight, the 256 x 256 grid).
+def _grouped_random_cases(n=8, seed=2414):
+    r = np.random.default_rng(seed)
+    out = []
+    for i in range(n):
+        K = 32 * int(r.integers(4, 80))
+        shapes = [(int(r.integers(16, 2000)), float(r.choice([0.0, 0.25, 0.5, 1.0]))) for _ in range(int(r.integers(1, 5)))]
+        M = int(r.choice([int(r.integers(1, 65)), int(r.integers(65, 300)), int(r.integers(300, 1100))]))
+        out.append((i, M, K, shapes))
+    return out
+
+
+@pytest.mark.parametrize("i,M,K,shapes", _grouped_random_cases())
+def test_grouped_random_shapes_exact(S, i, M, K, shapes):
+    say(f"[grouped random] M={M} K={K} {shapes}")
+    ws, X, sx = weights(60 + i, shapes, M, K)
+    pws = [packed(S, W, mask, db) for (W, mask, sw, db) in ws]
+    sws = [tdev(sw) for (_, _, sw, _) in ws]
+    for out_f32 in (True, False):
+        ys = S.gemm_grouped(tdev(X), pws, sws, tdev(sx), out_f32=out_f32)
+        torch.cuda.synchronize()
+        for (W, mask, sw, db), y in zip(ws, ys):
+            v, m, d, bad = oracle.compress(W, mask, FP8, 0, db)
+            ref = oracle.spense_gemm(X, v, m, d, W.shape[0], K, FP8, 0, db, sw, sx)
+            got = y.cpu().numpy() if out_f32 else y.view(torch.int16).cpu().numpy().view(np.uint16)
+            assert np.array_equal(got, ref["y_f32" if out_f32 else "y_bf16"])
+
+
 def test_grouped_random_within_bound(S):
     M, K = 48, 1536
     shapes = [(640, 0.25), (128, 0.25), (128, 0.25)]
