@@ -190,8 +190,9 @@ def cpu_baseline(mx, Wcodes_dense, X, sx, M):
 
 def measure_extras(args, torch, gen, S, ws, pws, copies, swd, mx, dws, dense_copies, results):
     """Extra fields: %peak against a measured copy bandwidth, per-launch (eager) timing of
-    the main GEMM, MFMA utilisation at M = 2048 and the Qwen3-32B-like decoder-layer set
-    (q, k, v, o, gate, up, down at M = 64, seven GEMMs back to back, x64 layers)."""
+    the main GEMM, gate / up across 96-1024 tokens, MFMA utilisation at M = 2048 and the
+    Qwen3-32B-like decoder-layer set (q, k, v, o, gate, up, down at M = 64, seven GEMMs
+    back to back, x64 layers)."""
     ex = {}
     # device copy bandwidth (read + write) of 256 MiB, as a measured ceiling
     n = 256 << 20
@@ -232,6 +233,18 @@ def measure_extras(args, torch, gen, S, ws, pws, copies, swd, mx, dws, dense_cop
     per = sorted(evs[g].elapsed_time(evs[g + 1]) * 1e3 / G for g in range(NG))
     ex["per_launch_us"] = {"groups_of": G, "p10": round(per[NG // 10], 2), "median": round(per[NG // 2], 2),
                            "p90": round(per[NG * 9 // 10], 2)}
+    # gate / up between one token block and the compute-bound point (graph replay, the
+    # planner's kernel at each M: row-split, two 64-token halves, large-M tiles)
+    across = {}
+    for Ma in (96, 128, 192, 256, 384, 512, 1024):
+        Xa, sxa = gen.make_x(2, 0, Ma, K, gen.FP8, "normal")
+        Xad, sxad = torch.from_numpy(Xa).cuda(), torch.from_numpy(sxa).cuda()
+        Ya = torch.empty((Ma, N), dtype=torch.bfloat16, device="cuda")
+        ams = time_launches(lambda i: S.gemm(Xad, pws[i % copies], swd, sxad, out=Ya, workspace=ws), 20, 3, torch)
+        across[f"m{Ma}"] = {"us_per_gemm": round(ams * 1e3, 1),
+                            "tflops": round(alg_flops_spense(Ma, mx.dense_begin * K, (N - mx.dense_begin) * K)
+                                            / (ams * 1e-3) / 1e12, 1)}
+    ex["across_m"] = across
     # compute-bound point: M = 2048 on the same weight
     Mb = 2048
     Xb, sxb = gen.make_x(2, 0, Mb, K, gen.FP8, "normal")
