@@ -654,6 +654,13 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
   a.groups = groups;
   a.tiled = tiled ? 1 : 0;
   a.tblocks = (int32_t)tblocks;
+  // 256 x 256 kernel: blocks of 192 tokens where they need no more blocks than 256-token
+  // ones (257-384, 513-576, ... tokens): the same grid, a quarter of each tile's MMAs and
+  // activation copies fewer.  Measured on MI355X (graph replay, us, one box, 256 -> 192):
+  // gate / up at M = 257 / 300 / 384 / 540 / 576 65.8 / 65.7 / 66.4 / 86.1 / 87.0 -> 62.8 /
+  // 63.3 / 65.1 / 81.9 / 82.8; Seed-OSS gate 66.8 / 66.8 / 67.4 / 95.5 / 96.0 -> 63.3 /
+  // 63.6 / 65.9 / 88.0 / 89.3.
+  a.btok = big == 2 && M > 256 && ceil_div(M, 192) == tblocks ? 192 : 0;
   a.hg0 = groups;
   a.hrb0 = (int32_t)(rbl - half_rb);
   a.hper = (int32_t)ceil_div(M, 128);
@@ -1382,6 +1389,7 @@ int spense_gemm_grouped(const void* X, int64_t M, int64_t ldx, int32_t count, co
       a.reg[i] = regs[i];
     }
     a.tblocks = (int32_t)T256;
+    a.btok = M > 256 && ceil_div(M, 192) == T256 ? 192 : 0;  // as for one weight
     a.hg0 = groups;
     a.hrb0 = (int32_t)(rbl - half_rb);
     a.hper = (int32_t)ceil_div(M, 128);

@@ -1733,7 +1733,7 @@ __global__ __launch_bounds__(512) void spense_gemm_big2_kernel(GemmArgs a) {
       ri = (a.nreg > 1 && g >= a.reg[1].wg0) ? 1 : 0;
     }
     rb = (g - a.reg[ri].wg0) / a.tblocks;
-    m0 = (g - a.reg[ri].wg0) % a.tblocks * kB2Tokens;
+    m0 = (g - a.reg[ri].wg0) % a.tblocks * (a.btok > 0 ? a.btok : kB2Tokens);
   } else {
     const int h = g - a.hg0;
     ri = a.nreg - 1;
@@ -1744,7 +1744,8 @@ __global__ __launch_bounds__(512) void spense_gemm_big2_kernel(GemmArgs a) {
   const Region& R = a.reg[ri];
   const int rowend = R.row0 + R.rows;
   const int rblk = R.row0 + rb * kB2Rows;
-  const int ntok = half ? kB2Tokens / 2 : kB2Tokens;
+  // tokens of this tile: 256, or 192 (full tiles of a 192-token block), or 128 (half tiles)
+  const int ntok = half ? kB2Tokens / 2 : (a.btok > 0 ? a.btok : kB2Tokens);
   const int K = R.kend, kbound = R.kbound;
 
   extern __shared__ __attribute__((aligned(1024))) uint8_t big_lds[];
@@ -1837,7 +1838,7 @@ __global__ __launch_bounds__(512) void spense_gemm_big2_kernel(GemmArgs a) {
 
   // 2:4 step s from stage cur; the loads of step s + 2 go to stage nxt.  Per row tile t the
   // A fragment of tile t + 1 is read (other register set) before the 4 MMAs of tile t.
-  // ACT = false: a wave without tokens (the second half of a 256 x 128 tile) only copies.
+  // ACT = false: a wave without tokens (token quarters past a 128- or 192-token tile) only copies.
   auto sp_step = [&](auto act_const, int s, const uint8_t* cur, uint8_t* nxt) __attribute__((always_inline)) {
     constexpr bool ACT = decltype(act_const)::value;
     // this wave's loads of step s have landed once at most those of step s + 1 are pending
@@ -1939,9 +1940,9 @@ __global__ __launch_bounds__(512) void spense_gemm_big2_kernel(GemmArgs a) {
     }
   };
   // bf16 output with 16-byte aligned rows leaves through LDS as whole token rows
-  // (out_tile_write); the waves of token quarters 2 and 3 of a 256 x 128 tile then only
-  // help with the stores
-  const bool idle = half && wc >= 2;
+  // (out_tile_write); the waves of token quarters past the tile's tokens (2 and 3 of a 256
+  // x 128 tile, 3 of a 256 x 192 one) then only help with the stores
+  const bool idle = wc * (kB2Tokens / 4) >= ntok;
   const bool via_lds = !a.out_f32 && ((uintptr_t)MD.Y % 16 == 0) && (MD.ldy % 8 == 0) && (rblk % 8 == 0);
   if (idle) {
     run(std::false_type());

@@ -74,6 +74,7 @@ struct GemmArgs {
   int32_t tiled;  // weight buffers in the tiled execution layout (fp8, row-split kernel)
   float* part;    // fp32 partial sums of K-sliced regions: part[(slice * M + m) * N + n]
   int32_t tblocks;  // large-M kernel: 256-token blocks (workgroups of a row block are adjacent)
+  int32_t btok;     // 256 x 256 kernel: tokens of a full tile's block, 192 or 256 (0 = 256)
   // 256 x 256 kernel: workgroups from hg0 on (the last ones) compute 256 x 128 tiles of
   // the last region's row blocks hrb0 .., hper of them per row block (hg0 = groups: none)
   int32_t hg0, hrb0, hper;

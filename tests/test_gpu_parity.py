@@ -568,6 +568,30 @@ def test_rows_random_shapes_exact(S, i, axis, N, K, db, M, ks):
         assert np.array_equal(run_gemm(S, w, X, sw, sx, False, plan).view(np.uint16), ref["y_bf16"]), plan.kernel
 
 
+# The 256 x 256 kernel with 192-token blocks (257-384 and 513-576 tokens): (axis, M, N, K,
+# db), ragged N, the last block partly filled; bf16 through LDS (leading dimension N + 8)
+# and quad by quad (N + 3), and fp32.
+TILE192_CASES = [(0, 257, 700, 512, 300), (1, 300, 520, 768, 256), (0, 384, 1100, 384, 1000), (1, 560, 640, 640, 320)]
+
+
+@pytest.mark.parametrize("axis,M,N,K,db", TILE192_CASES)
+def test_256_row_tiles_of_192_tokens_exact(S, axis, M, N, K, db):
+    """Bit-exact against the oracle; the padding of Y is untouched."""
+    say(f"[tiles 192] axis={axis} M={M} N={N} K={K} db={db}")
+    W, mask, X, sw, sx = gen.make_exact_int(39, M + N, M, N, K, gaxis(axis), db, gen.FP8)
+    pw, (v, m, d) = compress_both(S, W, mask, FP8, axis, db)
+    ref = oracle.spense_gemm(X, v, m, d, N, K, FP8, axis, db, sw, sx)
+    big2 = S.plan_override(kernel=BIG2, waves=8)
+    pwt = S.tile(pw)
+    assert np.array_equal(run_gemm(S, pwt, X, sw, sx, True, big2), ref["y_f32"])
+    for pad in (0, 8, 3):
+        Ybig = torch.full((M, N + pad), 7.0, dtype=torch.bfloat16, device="cuda")
+        S.gemm(tdev(X), pwt, tdev(sw), tdev(sx), out=Ybig[:, :N], plan=big2)
+        torch.cuda.synchronize()
+        assert np.array_equal(tnp(Ybig[:, :N]), ref["y_bf16"]), pad
+        assert torch.all(Ybig[:, N:] == 7.0)
+
+
 # Seeded random shapes for the large-M kernels (forced): either split, any boundary, ragged
 # N and K, 200-1100 tokens (partial last token blocks of both tile heights).
 def _large_m_random_cases(n=6, seed=2412):
