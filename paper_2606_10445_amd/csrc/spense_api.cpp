@@ -514,7 +514,7 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
     if (rb256 * tb256 >= 160) big = 2;
   }
   // Two 64-token halves per row-split workgroup (spense_gemm_rows2_kernel: 128 tokens a
-  // block, four token tiles, one row tile, eight waves, no K slices).  Each weight chunk
+  // block, four token tiles, one row tile, eight waves).  Each weight chunk
   // feeds twice the tokens of the row-split kernel's, but the 128 KB of staged
   // activations leave one workgroup per CU, so it needs several rounds of workgroups.
   // Measured on MI355X (graph replay, us, planner's choice -> two halves): with one

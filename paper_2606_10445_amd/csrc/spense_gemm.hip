@@ -23,17 +23,19 @@
 //   holds logical K [16q, 16q+16) (half a metadata word, chosen by shifting); B holds K
 //   [8q, 8q+8) and [32+8q, 32+8q+8).
 //
-// Four GEMM kernels; the host planner picks one per call from M and the weight geometry:
+// Five GEMM kernels; the host planner picks one per call from M and the weight geometry:
 //   - spense_gemm_rows_kernel (decode, HBM-bound): each wave owns 16 weight rows over all
 //     of K; the waves of a workgroup share every chunk of activations through LDS (or
 //     keep all of them resident) and keep two chunks of weights in flight; K slices, where
 //     the weight has few rows, go through splitk_reduce_kernel;
+//   - spense_gemm_rows2_kernel (65-256 tokens): the same with two 64-token halves per
+//     workgroup, each weight chunk feeding both;
 //   - spense_gemm_kernel: a workgroup owns 16*RT weight rows and its W waves split the K
 //     range (cost-balanced on the host), U instruction steps per batch of loads; at the
 //     end the waves add their accumulators in LDS in wave order (deterministic);
 //   - spense_gemm_big_kernel / spense_gemm_big2_kernel (many tokens): 128 x 256 and
-//     256 x 256 workgroup tiles with both operands copied into LDS a few steps ahead; their
-//     bf16 output tile leaves through LDS as whole token rows.
+//     256 x 256 (or 256 x 192) workgroup tiles with both operands copied into LDS a few
+//     steps ahead; their bf16 output tile leaves through LDS as whole token rows.
 // All loads are range-checked buffer loads: a lane whose chunk lies past the end of its
 // range gets an out-of-range offset and reads zeros, so the loops have no divergent
 // branches.
