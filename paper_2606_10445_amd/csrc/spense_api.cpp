@@ -742,11 +742,13 @@ void log_plan(const char* what, int32_t dtype, int64_t M, int64_t N, int32_t spl
               bool tiled, const spense::LaunchShape& ls, const spense::GemmArgs& a, size_t ws_bytes) {
   fprintf(stderr,
           "spense: %s dtype=%s M=%lld N=%lld K=%lld split=%s dense_begin=%lld layout=%s -> %s act_tiles=%d "
-          "row_tiles=%d waves=%d token_blocks=%d workgroups=%d regions=%d k_slices=%d resident_x=%d "
-          "half_tile_groups=%d workspace=%zu\n",
+          "row_tiles=%d waves=%d token_blocks=%d block_tokens=%d workgroups=%d regions=%d k_slices=%d "
+          "resident_x=%d half_tile_groups=%d workspace=%zu\n",
           what, dtype == SPENSE_FP8_E4M3FN ? "fp8" : "bf16", (long long)M, (long long)N, (long long)K,
           split == SPENSE_SPLIT_OUTPUT ? "output" : "input", (long long)dense_begin, tiled ? "tiled" : "row-major",
-          kernel_name(ls), ls.ct, ls.rt, ls.waves, ls.big ? a.tblocks : ls.mblocks, a.groups, a.nreg, a.nreg > 0 ? a.reg[0].ksplit : 1,
+          kernel_name(ls), ls.ct, ls.rt, ls.waves, ls.big ? a.tblocks : ls.mblocks,
+          ls.big == 2 ? (a.btok > 0 ? a.btok : 256) : (ls.big ? 256 : (ls.rows == 2 ? 128 : 16 * ls.ct)), a.groups,
+          a.nreg, a.nreg > 0 ? a.reg[0].ksplit : 1,
           ls.xres, ls.big == 2 ? a.groups - a.hg0 : 0, ws_bytes);
 }
 

@@ -426,6 +426,26 @@ def test_two_half_rule_on_the_layer_shapes(S, capfd):
         S.spense_set_log(prev)
 
 
+def test_192_token_blocks_rule(S, capfd):
+    """The 256 x 256 kernel takes 192-token blocks where they need no more blocks than
+    256-token ones (257-384, 513-576 tokens), else 256, seen through the dispatch log."""
+    L = S.spense_layout(25600, 5120, 1, 0, 19200)
+    p = S.spense_packed_t(1, 0, 25600, 5120, 19200, 4096, L.values_ld, 8192, L.meta_ld, 16384, L.dense_ld,
+                          S.SPENSE_LAYOUT_TILED)
+    prev = S.spense_set_log(1)
+    try:
+        got = {}
+        for M in (259, 383, 389, 515, 575, 577, 2047):  # token counts no other test plans on this weight
+            capfd.readouterr()
+            S.spense_gemm_workspace_size(M, p)
+            line = capfd.readouterr().err.strip().splitlines()[-1]
+            assert "large-M 256x256" in line, line
+            got[M] = int(line.split("block_tokens=")[1].split()[0])
+        assert got == {259: 192, 383: 192, 389: 256, 515: 192, 575: 192, 577: 256, 2047: 256}, got
+    finally:
+        S.spense_set_log(prev)
+
+
 def _down_desc(S, layout=0, dtype=1):
     L = S.spense_layout(5120, 25600, dtype, 1, 19200)
     return S.spense_packed_t(dtype, 1, 5120, 25600, 19200, 4096, L.values_ld, 8192, L.meta_ld, 16384, L.dense_ld,
