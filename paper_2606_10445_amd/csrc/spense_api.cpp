@@ -537,21 +537,40 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
   // 24.4 / 22.1 -> 20.1 / 21.8 with 4 (M = 128: 22.8 against 23.0).  At 129-192 tokens the
   // row-split kernel's three blocks stay ahead (down at M = 160 / 192 49.0 / 50.3 against
   // 55.6 / 55.6), as they do on o (16 chunks), q and k at every M here.
+  // Past 256 tokens, on weights of 256 to 767 row tiles (the large-M grids have too few
+  // tiles there), it halves the row-split kernel's token blocks (us, planner's choice ->
+  // two halves): down 5120 x 25600 at M = 448 / 512 / 640 118.6 / 119.1 / 143.4 -> 100.8
+  // / 102.9 / 124.2, at M = 300 with 2 slices 91.5 -> 74.8; Seed-OSS down alike; o 5120 x
+  // 8192 at M = 448 / 512 / 640 43.7 / 44.5 / 50.7 -> 37.5 / 38.7 / 44.5; q (512 tiles)
+  // at M = 300 / 384 33.0 / 35.6 -> 30.7 / 31.5, also against the 128 x 256 kernel.  Not
+  // o and down at 321-384 tokens (six 64-token blocks: down 76.4 against 78.0), nor q
+  // from 385 on (the 128 x 256 kernel, 36.6 / 39.4 at 448 / 512 against 47.7 / 48.6).
   bool rows2 = ov.kernel == 5;
   int rows2_ks = 1;
   if (ov.kernel == 0 && !ov.rt && !ov.waves && !ov.ct && ov.ksplit <= 1 && !ov.wused && !ov.wused_d &&
-      !ov.wused_s && !ov.u8 && !ov.xres && tiled && dtype == SPENSE_FP8_E4M3FN && M > 64 && M <= 256) {
+      !ov.wused_s && !ov.u8 && !ov.xres && tiled && dtype == SPENSE_FP8_E4M3FN && M > 64 && M <= 640) {
     const int64_t rtiles = ceil_div(N, 16);
-    rows2 = M <= 128 ? rtiles >= 768 : (!big && rtiles >= (M <= 192 ? 640 : 512));
     const int64_t kch = split == SPENSE_SPLIT_INPUT ? ceil_div(dense_begin, 512) + ceil_div(K - dense_begin, 512)
                                                     : ceil_div(K, 512);
-    if (!rows2 && ov.ksplit < 1 && rtiles < 768) {
-      if (kch >= 40 && (M <= 128 || (M > 192 && !big))) {
+    if (M <= 256) {
+      rows2 = M <= 128 ? rtiles >= 768 : (!big && rtiles >= (M <= 192 ? 640 : 512));
+      if (!rows2 && ov.ksplit < 1 && rtiles < 768) {
+        if (kch >= 40 && (M <= 128 || (M > 192 && !big))) {
+          rows2 = true;
+          rows2_ks = M <= 128 ? 6 : 3;
+        } else if (kch >= 20 && M <= 96) {
+          rows2 = true;
+          rows2_ks = 4;
+        }
+      }
+    } else if (rtiles >= 256 && rtiles < 768) {
+      if (M > 384) {
+        rows2 = !big || rtiles < 512;  // down at 640 (128 x 256, 120 tiles) 143.9 against 124.2
+      } else if (rtiles >= 512) {
         rows2 = true;
-        rows2_ks = M <= 128 ? 6 : 3;
-      } else if (kch >= 20 && M <= 96) {
+      } else if (M <= 320 && kch >= 40 && ov.ksplit < 1) {
         rows2 = true;
-        rows2_ks = 4;
+        rows2_ks = 2;
       }
     }
   }

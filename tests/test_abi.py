@@ -385,7 +385,8 @@ def test_k_slice_rule_on_the_layer_shapes(S):
     assert ws(5120, 25600, 1, 192) > 0 and ws(1024, 5120, 0, 192) == 0  # three: only the long K
     assert ws(1024, 5120, 0, 200) == 0  # four or more token blocks
     assert ws(5120, 25600, 1, 200) == 3 * 200 * 5120 * 4  # down from 193 tokens: 3 slices of 128 tokens
-    assert ws(5120, 25600, 1, 300) == 0
+    assert ws(5120, 25600, 1, 300) == 2 * 300 * 5120 * 4  # 257-320: two halves in 2 slices
+    assert ws(5120, 25600, 1, 350) == 0 and ws(5120, 25600, 1, 500) == 0
 
 
 def test_two_half_rule_on_the_layer_shapes(S, capfd):
@@ -415,7 +416,15 @@ def test_two_half_rule_on_the_layer_shapes(S, capfd):
         assert kernel(25600, 5120, 0, 63) == "row-split"
         assert kernel(8192, 5120, 0, 191) == "row-split" and kernel(8192, 5120, 0, 193) == two
         assert kernel(10240, 5120, 0, 131) == two and kernel(16384, 8192, 1, 131) == two
-        assert kernel(25600, 5120, 0, 131).startswith("large-M") and kernel(8192, 5120, 0, 257) != two
+        assert kernel(25600, 5120, 0, 131).startswith("large-M") and kernel(25600, 5120, 0, 300).startswith("large-M")
+        # 257-640 tokens on 256-767 row tiles: q up to 384, o and down from 385 (and down
+        # at 257-320, in 2 slices), not the 128 x 256 kernel's q above 384
+        assert kernel(8192, 5120, 0, 257) == two and kernel(8192, 5120, 0, 383) == two
+        assert kernel(8192, 5120, 0, 449).startswith("large-M")
+        assert kernel(5120, 8192, 1, 450) == two and kernel(5120, 25600, 1, 639) == two
+        assert kernel(5120, 25600, 1, 301) == two and kernel(5120, 25600, 1, 350) == "row-split"
+        assert kernel(5120, 8192, 1, 301) == "row-split" and kernel(5120, 25600, 1, 700) != two
+        assert kernel(1024, 5120, 0, 450) != two  # k / v: 64 row tiles
         assert kernel(25600, 5120, 0, 99, layout=0) != two
         # short weights with a long K: with K slices (down 50 chunks, Seed-OSS o 20)
         assert kernel(5120, 25600, 1, 67) == two and kernel(5120, 25600, 1, 250) == two
