@@ -205,7 +205,7 @@ int spense_tile(const spense_packed_t* src, const spense_packed_t* dst, hipStrea
  * with fewer than 1024 16-row tiles at up to 64 tokens, when every slice keeps enough of
  * K: e.g. k / v and down from one token on, o from 17 tokens; few-row or long-K weights
  * at two or three 64-token blocks; long-K weights of fewer than 768 tiles at 65-128 and
- * 193-256 tokens, as 128-token blocks in 3 to 6 slices): S x M x N fp32 partial sums,
+ * 193-320 tokens, as 128-token blocks in 2 to 6 slices): S x M x N fp32 partial sums,
  * added in slice order by a second kernel of the same call.  The workspace is only
  * scratch between the two kernels of one call; calls that overlap on one workspace race.
  */
