@@ -537,18 +537,20 @@ void make_plan(int32_t dtype, int64_t M, int64_t N, int32_t split, int64_t K, in
   // 24.4 / 22.1 -> 20.1 / 21.8 with 4 (M = 128: 22.8 against 23.0).  At 129-192 tokens the
   // row-split kernel's three blocks stay ahead (down at M = 160 / 192 49.0 / 50.3 against
   // 55.6 / 55.6), as they do on o (16 chunks), q and k at every M here.
-  // Past 256 tokens, on weights of 256 to 767 row tiles (the large-M grids have too few
-  // tiles there), it halves the row-split kernel's token blocks (us, planner's choice ->
-  // two halves): down 5120 x 25600 at M = 448 / 512 / 640 118.6 / 119.1 / 143.4 -> 100.8
-  // / 102.9 / 124.2, at M = 300 with 2 slices 91.5 -> 74.8; Seed-OSS down alike; o 5120 x
-  // 8192 at M = 448 / 512 / 640 43.7 / 44.5 / 50.7 -> 37.5 / 38.7 / 44.5; q (512 tiles)
-  // at M = 300 / 384 33.0 / 35.6 -> 30.7 / 31.5, also against the 128 x 256 kernel.  Not
-  // o and down at 321-384 tokens (six 64-token blocks: down 76.4 against 78.0), nor q
-  // from 385 on (the 128 x 256 kernel, 36.6 / 39.4 at 448 / 512 against 47.7 / 48.6).
+  // Past 256 tokens (to 768), on weights of 256 to 767 row tiles (the large-M grids have
+  // too few tiles there), it halves the row-split kernel's token blocks (us, planner's
+  // choice -> two halves): down 5120 x 25600 at M = 448 / 512 / 640 / 768 118.6 / 119.1 /
+  // 143.4 / 150.7 -> 100.8 / 102.9 / 124.2 / 120.8, at M = 300 with 2 slices 91.5 ->
+  // 74.8; Seed-OSS down alike; o 5120 x 8192 at M = 448 / 512 / 640 / 768 43.7 / 44.5 /
+  // 50.7 / 53.1 -> 37.5 / 38.7 / 44.5 / 43.9; q (512 tiles) at M = 300 / 384 33.0 / 35.6
+  // -> 30.7 / 31.5, also against the 128 x 256 kernel.  Not o and down at 321-384 tokens
+  // (six 64-token blocks: down 76.4 against 78.0) nor from 769 (seven 128-token blocks:
+  // down at 896 149.6 against 201.2), nor q from 385 on (the 128 x 256 kernel, 36.6 /
+  // 39.4 at 448 / 512 against 47.7 / 48.6).
   bool rows2 = ov.kernel == 5;
   int rows2_ks = 1;
   if (ov.kernel == 0 && !ov.rt && !ov.waves && !ov.ct && ov.ksplit <= 1 && !ov.wused && !ov.wused_d &&
-      !ov.wused_s && !ov.u8 && !ov.xres && tiled && dtype == SPENSE_FP8_E4M3FN && M > 64 && M <= 640) {
+      !ov.wused_s && !ov.u8 && !ov.xres && tiled && dtype == SPENSE_FP8_E4M3FN && M > 64 && M <= 768) {
     const int64_t rtiles = ceil_div(N, 16);
     const int64_t kch = split == SPENSE_SPLIT_INPUT ? ceil_div(dense_begin, 512) + ceil_div(K - dense_begin, 512)
                                                     : ceil_div(K, 512);

@@ -417,13 +417,14 @@ def test_two_half_rule_on_the_layer_shapes(S, capfd):
         assert kernel(8192, 5120, 0, 191) == "row-split" and kernel(8192, 5120, 0, 193) == two
         assert kernel(10240, 5120, 0, 131) == two and kernel(16384, 8192, 1, 131) == two
         assert kernel(25600, 5120, 0, 131).startswith("large-M") and kernel(25600, 5120, 0, 300).startswith("large-M")
-        # 257-640 tokens on 256-767 row tiles: q up to 384, o and down from 385 (and down
+        # 257-768 tokens on 256-767 row tiles: q up to 384, o and down from 385 (and down
         # at 257-320, in 2 slices), not the 128 x 256 kernel's q above 384
         assert kernel(8192, 5120, 0, 257) == two and kernel(8192, 5120, 0, 383) == two
         assert kernel(8192, 5120, 0, 449).startswith("large-M")
         assert kernel(5120, 8192, 1, 450) == two and kernel(5120, 25600, 1, 639) == two
         assert kernel(5120, 25600, 1, 301) == two and kernel(5120, 25600, 1, 350) == "row-split"
-        assert kernel(5120, 8192, 1, 301) == "row-split" and kernel(5120, 25600, 1, 700) != two
+        assert kernel(5120, 8192, 1, 301) == "row-split" and kernel(5120, 25600, 1, 700) == two
+        assert kernel(5120, 25600, 1, 769) != two and kernel(5120, 8192, 1, 900) != two
         assert kernel(1024, 5120, 0, 450) != two  # k / v: 64 row tiles
         assert kernel(25600, 5120, 0, 99, layout=0) != two
         # short weights with a long K: with K slices (down 50 chunks, Seed-OSS o 20)

@@ -517,9 +517,9 @@ ROWS2_AUTO_CASES = [(0, 12288, 512, 9216, 100), (1, 12288, 384, 256, 127), (0, 8
                     (0, 10240, 256, 7680, 131),
                     # short weights with a long K: with K slices (6, 3 and 4)
                     (1, 320, 20992, 15744, 100), (1, 200, 20480, 15360, 250), (1, 300, 10240, 7680, 90),
-                    # 257-640 tokens on 256-767 row tiles (a long K at 300: 2 slices)
+                    # 257-768 tokens on 256-767 row tiles (a long K at 300: 2 slices)
                     (1, 4096, 20480, 15360, 300), (1, 4096, 1024, 768, 450), (0, 8192, 512, 6144, 300),
-                    (1, 4100, 2048, 1536, 600)]
+                    (1, 4100, 2048, 1536, 600), (0, 5000, 768, 3750, 700)]
 
 
 @pytest.mark.parametrize("axis,N,K,db,M", ROWS2_AUTO_CASES)
